@@ -1,0 +1,159 @@
+"""Plain fp64 CPU oracle for the ConvFirst residual block.
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the CPU-baseline leg
+of the benchmark may import this package; the product library never does.
+It shares no code with the GPU library.  Arrays in, arrays out, all float64
+numpy; callers widen their fp16/bf16 tensors exactly before calling.
+
+Each function below states the passage of Lavin, "On the Efficiency of
+Convolutional Neural Networks" (arXiv:2404.03617) that it implements; the
+arithmetic itself lives in ``cfref.c`` next to this file.
+
+Activation names: "gelu" (exact erf form), "relu", "none" (identity).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "cfref.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+ACTS = {"gelu": 0, "relu": 1, "none": 2}
+
+_dp = ctypes.POINTER(ctypes.c_double)
+
+
+def build(force: bool = True) -> str:
+    """Compile cfref.c with gcc -O2 (no fast-math) into liboracle.so."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-std=c99", "-D_POSIX_C_SOURCE=200809L", "-fPIC",
+                               "-shared", "-pthread", _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build()
+        L = ctypes.CDLL(_LIB)
+        i64 = ctypes.c_int64
+        ci = ctypes.c_int
+        L.cfref_act.restype = ctypes.c_double
+        L.cfref_act.argtypes = [ctypes.c_double, ci]
+        L.cfref_depthwise.argtypes = [_dp, _dp, _dp, _dp, ci, ci, ci, ci, ci, _dp, ci]
+        L.cfref_pointwise.argtypes = [_dp, _dp, _dp, _dp, i64, ci, ci, _dp, ci]
+        blk = [_dp] * 10 + [ci] * 7 + [_dp, ci]
+        L.cfref_block_forward.argtypes = blk
+        L.cfref_block_forward_loopfused.argtypes = blk
+        L.cfref_downsample.argtypes = [_dp, _dp, _dp, _dp, ci, ci, ci, ci, ci, _dp, ci]
+        L.cfref_default_threads.restype = ci
+        _lib = L
+    return _lib
+
+
+def _p(a):
+    """Pointer to a C-contiguous float64 array, or NULL for None."""
+    if a is None:
+        return None
+    assert a.dtype == np.float64 and a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(_dp)
+
+
+def _f64(a):
+    return None if a is None else np.ascontiguousarray(np.asarray(a, dtype=np.float64))
+
+
+def default_threads() -> int:
+    return lib().cfref_default_threads()
+
+
+def act(u: float, name: str = "gelu") -> float:
+    """phi of eq. e:ffn (Sec. 5.2), one scalar."""
+    return lib().cfref_act(float(u), ACTS[name])
+
+
+def depthwise(x, dw_w, s0=None, b0=None, nthreads: int = 0):
+    """Depth-wise k x k conv with floor(k/2) zero padding (Sec. 4.1.1,
+    eq. f:depth-wise-conv2d, K = C).  x [N,H,W,C], dw_w [k,k,C]."""
+    x, dw_w, s0, b0 = _f64(x), _f64(dw_w), _f64(s0), _f64(b0)
+    N, H, W, C = x.shape
+    k = dw_w.shape[0]
+    assert dw_w.shape == (k, k, C) and k % 2 == 1
+    d = np.empty_like(x)
+    lib().cfref_depthwise(_p(x), _p(dw_w), _p(s0), _p(b0), N, H, W, C, k, _p(d), nthreads)
+    return d
+
+
+def pointwise(x, a, s=None, b=None, nthreads: int = 0):
+    """Point-wise conv as the matrix product of eq. f:pointwise-matrix-conv2d.
+    x [..., Cin], a [Cout, Cin] -> [..., Cout]."""
+    x, a, s, b = _f64(x), _f64(a), _f64(s), _f64(b)
+    Cin = x.shape[-1]
+    Cout = a.shape[0]
+    assert a.shape == (Cout, Cin)
+    P = int(np.prod(x.shape[:-1]))
+    y = np.empty(x.shape[:-1] + (Cout,), dtype=np.float64)
+    lib().cfref_pointwise(_p(x), _p(a), _p(s), _p(b), P, Cin, Cout, _p(y), nthreads)
+    return y
+
+
+def block_forward(x, p: dict, act: str = "gelu", loopfused: bool = False, nthreads: int = 0,
+                  return_threads: bool = False):
+    """The ConvFirst block (Sec. 5.3 / 5.3.1) with depth-wise conv, folded norms
+    and the residual shortcut.  ``loopfused`` selects the eq. e:ffn-eff
+    evaluation order instead of the layer-by-layer one (eq. e:ffn).
+
+    p holds dw_w [k,k,C], w1 [E*C,C], w2 [C,E*C] and optional s0,b0 [C],
+    s1,b1 [E*C], s2,b2 [C]."""
+    x = _f64(x)
+    N, H, W, C = x.shape
+    dw_w, w1, w2 = _f64(p["dw_w"]), _f64(p["w1"]), _f64(p["w2"])
+    k = dw_w.shape[0]
+    EC = w1.shape[0]
+    assert dw_w.shape == (k, k, C) and w1.shape == (EC, C) and w2.shape == (C, EC)
+    assert EC % C == 0
+    E = EC // C
+    vec = [_f64(p.get(n)) for n in ("s0", "b0", "s1", "b1", "s2", "b2")]
+    y = np.empty_like(x)
+    fn = lib().cfref_block_forward_loopfused if loopfused else lib().cfref_block_forward
+    used = fn(_p(x), _p(dw_w), _p(vec[0]), _p(vec[1]), _p(w1), _p(vec[2]), _p(vec[3]),
+              _p(w2), _p(vec[4]), _p(vec[5]), N, H, W, C, E, k, ACTS[act], _p(y), nthreads)
+    return (y, used) if return_threads else y
+
+
+def downsample(x, wd, sd=None, bd=None, nthreads: int = 0):
+    """2x2 stride-2 conv (eq. f:conv2d with R = S = 2, stride 2, no padding).
+    x [N,H,W,Cin], wd [Cout,2,2,Cin] -> [N,H/2,W/2,Cout]."""
+    x, wd, sd, bd = _f64(x), _f64(wd), _f64(sd), _f64(bd)
+    N, H, W, Cin = x.shape
+    Cout = wd.shape[0]
+    assert wd.shape == (Cout, 2, 2, Cin) and H % 2 == 0 and W % 2 == 0
+    y = np.empty((N, H // 2, W // 2, Cout), dtype=np.float64)
+    rc = lib().cfref_downsample(_p(x), _p(wd), _p(sd), _p(bd), N, H, W, Cin, Cout, _p(y), nthreads)
+    assert rc >= 0
+    return y
+
+
+def stack_forward(x, layers: list, act: str = "gelu", nthreads: int = 0):
+    """A sequence of blocks and down-sampling layers applied in order.
+    layers: list of ("block", params) or ("down", params with wd, sd, bd)."""
+    y = _f64(x)
+    for kind, p in layers:
+        if kind == "block":
+            y = block_forward(y, p, act=act, nthreads=nthreads)
+        elif kind == "down":
+            y = downsample(y, p["wd"], p.get("sd"), p.get("bd"), nthreads=nthreads)
+        else:
+            raise ValueError(kind)
+    return y

@@ -1,0 +1,329 @@
+/*
+ * cfref.c -- plain fp64 CPU oracle for the ConvFirst residual block.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may call, link or
+ * load this file or the library built from it; only the tests, the smoke
+ * check and the CPU-baseline leg of the benchmark do.  It shares no code,
+ * header, constant or helper with the GPU library.
+ *
+ * Every quantity is a double.  Callers pass the exact (widened) values of the
+ * fp16/bf16 tensors the GPU consumes.  No blocking, no fusion, no reordering:
+ * each function is the definition it cites, written as loops.
+ *
+ * Paper: A. Lavin, "On the Efficiency of Convolutional Neural Networks",
+ * arXiv:2404.03617.
+ *
+ * Layouts (all row-major, channels fastest):
+ *   x, y, d     [N][H][W][C]           activations (NHWC), Sec. 4.1.1
+ *   dw_w        [k][k][C]              depth-wise taps, one k x k filter per channel
+ *   w1          [E*C][C]               expand weights, row r = hidden channel r
+ *   w2          [C][E*C]               project weights, row c = output channel c
+ *   wd          [Cout][2][2][Cin]      2x2 stride-2 down-sampling conv
+ *   scale/bias  per output channel; a NULL scale means 1, a NULL bias means 0
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <unistd.h>
+
+#define CFREF_ACT_GELU_ERF 0
+#define CFREF_ACT_RELU 1
+#define CFREF_ACT_IDENTITY 2
+
+int cfref_version(void) { return 1; }
+
+/* ------------------------------------------------------------------------ */
+/* Element-wise activation phi of the FFN (Sec. 5.2, eq. e:ffn).
+ * GELU uses the exact Gaussian-CDF form u * Phi(u), Phi(u) = (1 + erf(u/sqrt2))/2,
+ * with the C library's double-precision erf. */
+double cfref_act(double u, int act)
+{
+    if (act == CFREF_ACT_GELU_ERF)
+        return 0.5 * u * (1.0 + erf(u / sqrt(2.0)));
+    if (act == CFREF_ACT_RELU)
+        return u > 0.0 ? u : 0.0;
+    return u;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Depth-wise convolution, K = C (Sec. 4.1.1, eq. f:depth-wise-conv2d), with the
+ * implicit zero padding of floor(k/2) on every border (Sec. 4.1.1, text after
+ * eq. f:conv2d), taps centred on the output pixel, cross-correlation (no flip):
+ *   D[n,h,w,c] = s0[c] * sum_{i<k} sum_{j<k} A[i][j][c] * X[n, h+i-k/2, w+j-k/2, c] + b0[c]
+ * One output pixel. */
+static void dw_pixel(const double *x, const double *dw_w, const double *s0, const double *b0,
+                     int H, int W, int C, int k, int n, int h, int w, double *out /*[C]*/)
+{
+    int pad = k / 2;
+    for (int c = 0; c < C; c++) {
+        double acc = 0.0;
+        for (int i = 0; i < k; i++) {
+            int hh = h + i - pad;
+            if (hh < 0 || hh >= H)
+                continue; /* zero padding */
+            for (int j = 0; j < k; j++) {
+                int ww = w + j - pad;
+                if (ww < 0 || ww >= W)
+                    continue; /* zero padding */
+                double xv = x[(((int64_t)n * H + hh) * W + ww) * C + c];
+                double av = dw_w[((int64_t)i * k + j) * C + c];
+                acc += av * xv;
+            }
+        }
+        out[c] = (s0 ? s0[c] : 1.0) * acc + (b0 ? b0[c] : 0.0);
+    }
+}
+
+/* Point-wise convolution as a matrix product over the unfolded pixel index
+ * (Sec. 4.1.1, eq. f:pointwise-matrix-conv2d):
+ *   Y[p,o] = s[o] * sum_i A[o][i] * X[p,i] + b[o]         for one pixel p. */
+static void pw_pixel(const double *xin /*[Cin]*/, const double *a /*[Cout][Cin]*/,
+                     const double *s, const double *b, int Cin, int Cout, double *out /*[Cout]*/)
+{
+    for (int o = 0; o < Cout; o++) {
+        double acc = 0.0;
+        for (int i = 0; i < Cin; i++)
+            acc += a[(int64_t)o * Cin + i] * xin[i];
+        out[o] = (s ? s[o] : 1.0) * acc + (b ? b[o] : 0.0);
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Row-parallel driver: the work items are the N*H output rows (n, h). */
+typedef struct job job;
+typedef void (*row_fn)(const job *J, int n, int h, double *scratch);
+struct job {
+    row_fn fn;
+    int N, H, W, C, E, k, act, Cout;
+    const double *x, *dw_w, *s0, *b0, *w1, *s1, *b1, *w2, *s2, *b2;
+    double *y;
+    size_t scratch_doubles;
+    int64_t next_row; /* shared counter, taken under the lock */
+    pthread_mutex_t lock;
+};
+
+static void *worker(void *arg)
+{
+    job *J = (job *)arg;
+    double *scratch = (double *)malloc(J->scratch_doubles * sizeof(double) + 16);
+    int64_t rows = (int64_t)J->N * J->H;
+    for (;;) {
+        pthread_mutex_lock(&J->lock);
+        int64_t r = J->next_row++;
+        pthread_mutex_unlock(&J->lock);
+        if (r >= rows)
+            break;
+        J->fn(J, (int)(r / J->H), (int)(r % J->H), scratch);
+    }
+    free(scratch);
+    return NULL;
+}
+
+int cfref_default_threads(void)
+{
+    long n = sysconf(_SC_NPROCESSORS_ONLN);
+    return n > 0 ? (int)n : 1;
+}
+
+/* Runs J->fn over all rows on `nthreads` threads (<= 0: one per online CPU).
+ * Returns the number of threads actually used. */
+static int run_rows(job *J, int nthreads)
+{
+    if (nthreads <= 0)
+        nthreads = cfref_default_threads();
+    int64_t rows = (int64_t)J->N * J->H;
+    if (nthreads > rows)
+        nthreads = rows > 0 ? (int)rows : 1;
+    J->next_row = 0;
+    pthread_mutex_init(&J->lock, NULL);
+    pthread_t *t = (pthread_t *)malloc(sizeof(pthread_t) * nthreads);
+    for (int i = 0; i < nthreads; i++)
+        pthread_create(&t[i], NULL, worker, J);
+    for (int i = 0; i < nthreads; i++)
+        pthread_join(t[i], NULL);
+    free(t);
+    pthread_mutex_destroy(&J->lock);
+    return nthreads;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Depth-wise layer alone. */
+static void dw_row(const job *J, int n, int h, double *scratch)
+{
+    (void)scratch;
+    for (int w = 0; w < J->W; w++)
+        dw_pixel(J->x, J->dw_w, J->s0, J->b0, J->H, J->W, J->C, J->k, n, h, w,
+                 J->y + (((int64_t)n * J->H + h) * J->W + w) * J->C);
+}
+
+int cfref_depthwise(const double *x, const double *dw_w, const double *s0, const double *b0,
+                    int N, int H, int W, int C, int k, double *d, int nthreads)
+{
+    job J;
+    memset(&J, 0, sizeof J);
+    J.fn = dw_row;
+    J.N = N; J.H = H; J.W = W; J.C = C; J.k = k;
+    J.x = x; J.dw_w = dw_w; J.s0 = s0; J.b0 = b0; J.y = d;
+    J.scratch_doubles = 1;
+    return run_rows(&J, nthreads);
+}
+
+/* Point-wise layer alone over P = N*H*W pixels (rows are taken as 1 x P). */
+static void pw_row(const job *J, int n, int h, double *scratch)
+{
+    (void)scratch;
+    int64_t p = (int64_t)n * J->H + h; /* here H is the pixel count, N == 1 */
+    pw_pixel(J->x + p * J->C, J->w1, J->s1, J->b1, J->C, J->Cout, J->y + p * J->Cout);
+}
+
+int cfref_pointwise(const double *x, const double *a, const double *s, const double *b,
+                    int64_t P, int Cin, int Cout, double *y, int nthreads)
+{
+    job J;
+    memset(&J, 0, sizeof J);
+    J.fn = pw_row;
+    J.N = 1; J.H = (int)P; J.W = 1; J.C = Cin; J.Cout = Cout;
+    J.x = x; J.w1 = a; J.s1 = s; J.b1 = b; J.y = y;
+    J.scratch_doubles = 1;
+    return run_rows(&J, nthreads);
+}
+
+/* ------------------------------------------------------------------------ */
+/* The ConvFirst block, layer by layer (Sec. 5.3 and Sec. 5.3.1: grouped conv
+ * first -- here its depth-wise case -- then the FFN of eq. e:ffn, then the
+ * residual shortcut; every batch norm folded into a per-channel scale and
+ * bias after its linear layer):
+ *   D = s0 * dwconv(X) + b0
+ *   U = s1 * (D W1^T) + b1          hidden layer, E*C channels
+ *   G = phi(U)
+ *   Z = s2 * (G W2^T) + b2
+ *   Y = X + Z
+ * The hidden layer of a whole row of pixels is materialised here on purpose:
+ * this is the direct layer-by-layer algorithm. */
+static void block_row(const job *J, int n, int h, double *scratch)
+{
+    int W = J->W, C = J->C, EC = J->E * J->C;
+    double *D = scratch;              /* [W][C]  */
+    double *U = D + (size_t)W * C;    /* [W][EC] */
+    double *G = U + (size_t)W * EC;   /* [W][EC] */
+    double *Z = G + (size_t)W * EC;   /* [W][C]  */
+    for (int w = 0; w < W; w++)
+        dw_pixel(J->x, J->dw_w, J->s0, J->b0, J->H, W, C, J->k, n, h, w, D + (size_t)w * C);
+    for (int w = 0; w < W; w++)
+        pw_pixel(D + (size_t)w * C, J->w1, J->s1, J->b1, C, EC, U + (size_t)w * EC);
+    for (size_t e = 0; e < (size_t)W * EC; e++)
+        G[e] = cfref_act(U[e], J->act);
+    for (int w = 0; w < W; w++)
+        pw_pixel(G + (size_t)w * EC, J->w2, J->s2, J->b2, EC, C, Z + (size_t)w * C);
+    for (int w = 0; w < W; w++) {
+        int64_t base = (((int64_t)n * J->H + h) * W + w) * C;
+        for (int c = 0; c < C; c++)
+            J->y[base + c] = J->x[base + c] + Z[(size_t)w * C + c];
+    }
+}
+
+/* The same block with the FFN evaluated in the loop-fused order of
+ * eq. e:ffn-eff: one hidden channel r at a time, produced by column r of the
+ * expand and immediately consumed by row r of the project,
+ *   Z = sum_r phi(D U^r + a_r) V_r + b,
+ * with the output accumulator initialised from the block input (the residual
+ * shortcut, Sec. 5.3.1).  It must equal block_row up to rounding order; the
+ * tests use the pair to check eq. e:ffn-eff against eq. e:ffn. */
+static void block_row_loopfused(const job *J, int n, int h, double *scratch)
+{
+    int W = J->W, C = J->C, EC = J->E * J->C;
+    double *D = scratch;            /* [C] one pixel of the conv output */
+    double *Z = D + C;              /* [C] projected sum for that pixel */
+    for (int w = 0; w < W; w++) {
+        int64_t base = (((int64_t)n * J->H + h) * W + w) * C;
+        dw_pixel(J->x, J->dw_w, J->s0, J->b0, J->H, W, C, J->k, n, h, w, D);
+        for (int c = 0; c < C; c++)
+            Z[c] = 0.0;
+        for (int r = 0; r < EC; r++) {
+            double u = 0.0;
+            for (int c = 0; c < C; c++)
+                u += J->w1[(int64_t)r * C + c] * D[c];
+            u = (J->s1 ? J->s1[r] : 1.0) * u + (J->b1 ? J->b1[r] : 0.0);
+            double g = cfref_act(u, J->act);
+            for (int c = 0; c < C; c++)
+                Z[c] += J->w2[(int64_t)c * EC + r] * g;
+        }
+        for (int c = 0; c < C; c++)
+            J->y[base + c] = J->x[base + c] + (J->s2 ? J->s2[c] : 1.0) * Z[c] + (J->b2 ? J->b2[c] : 0.0);
+    }
+}
+
+static int block_common(row_fn fn, size_t scratch, const double *x, const double *dw_w,
+                        const double *s0, const double *b0, const double *w1, const double *s1,
+                        const double *b1, const double *w2, const double *s2, const double *b2,
+                        int N, int H, int W, int C, int E, int k, int act, double *y, int nthreads)
+{
+    job J;
+    memset(&J, 0, sizeof J);
+    J.fn = fn;
+    J.N = N; J.H = H; J.W = W; J.C = C; J.E = E; J.k = k; J.act = act;
+    J.x = x; J.dw_w = dw_w; J.s0 = s0; J.b0 = b0;
+    J.w1 = w1; J.s1 = s1; J.b1 = b1; J.w2 = w2; J.s2 = s2; J.b2 = b2;
+    J.y = y;
+    J.scratch_doubles = scratch;
+    return run_rows(&J, nthreads);
+}
+
+int cfref_block_forward(const double *x, const double *dw_w, const double *s0, const double *b0,
+                        const double *w1, const double *s1, const double *b1,
+                        const double *w2, const double *s2, const double *b2,
+                        int N, int H, int W, int C, int E, int k, int act, double *y, int nthreads)
+{
+    size_t scratch = (size_t)W * C * 2 + (size_t)W * E * C * 2;
+    return block_common(block_row, scratch, x, dw_w, s0, b0, w1, s1, b1, w2, s2, b2,
+                        N, H, W, C, E, k, act, y, nthreads);
+}
+
+int cfref_block_forward_loopfused(const double *x, const double *dw_w, const double *s0,
+                                  const double *b0, const double *w1, const double *s1,
+                                  const double *b1, const double *w2, const double *s2,
+                                  const double *b2, int N, int H, int W, int C, int E, int k,
+                                  int act, double *y, int nthreads)
+{
+    return block_common(block_row_loopfused, (size_t)C * 2, x, dw_w, s0, b0, w1, s1, b1, w2,
+                        s2, b2, N, H, W, C, E, k, act, y, nthreads);
+}
+
+/* ------------------------------------------------------------------------ */
+/* 2x2 stride-2 down-sampling convolution (the conv2d of eq. f:conv2d with
+ * R = S = 2, stride 2, no padding):
+ *   Yd[n,i,j,o] = sd[o] * sum_{a<2} sum_{b<2} sum_c Wd[o][a][b][c] * X[n, 2i+a, 2j+b, c] + bd[o]
+ * H and W must be even; the output is H/2 x W/2 x Cout. */
+static void down_row(const job *J, int n, int i, double *scratch)
+{
+    (void)scratch;
+    int H = J->H * 2, W = J->W * 2, Cin = J->C, Cout = J->Cout;
+    for (int j = 0; j < J->W; j++) {
+        double *out = J->y + (((int64_t)n * J->H + i) * J->W + j) * Cout;
+        for (int o = 0; o < Cout; o++) {
+            double acc = 0.0;
+            for (int a = 0; a < 2; a++)
+                for (int b = 0; b < 2; b++)
+                    for (int c = 0; c < Cin; c++)
+                        acc += J->w1[(((int64_t)o * 2 + a) * 2 + b) * Cin + c] *
+                               J->x[(((int64_t)n * H + 2 * i + a) * W + 2 * j + b) * Cin + c];
+            out[o] = (J->s1 ? J->s1[o] : 1.0) * acc + (J->b1 ? J->b1[o] : 0.0);
+        }
+    }
+}
+
+int cfref_downsample(const double *x, const double *wd, const double *sd, const double *bd,
+                     int N, int H, int W, int Cin, int Cout, double *y, int nthreads)
+{
+    if ((H % 2) || (W % 2))
+        return -1;
+    job J;
+    memset(&J, 0, sizeof J);
+    J.fn = down_row;
+    J.N = N; J.H = H / 2; J.W = W / 2; J.C = Cin; J.Cout = Cout;
+    J.x = x; J.w1 = wd; J.s1 = sd; J.b1 = bd; J.y = y;
+    J.scratch_doubles = 1;
+    return run_rows(&J, nthreads);
+}

@@ -1,0 +1,27 @@
+"""The five workloads the library is measured and checked on.
+
+Shapes follow the benchmark definitions: fp16/bf16 NHWC activations, E = 4,
+depth-wise k x k, GELU(erf), weights ~ N(0, 1/fan_in), biases ~ N(0, 0.01),
+scales 1, all seeded (``seed`` below feeds ``synth``).
+"""
+from __future__ import annotations
+
+WORKLOADS = {
+    # small latency case, oracle-sized
+    "block_n1_14x14_c64_e4_k3_f16": dict(kind="block", N=1, H=14, W=14, C=64, E=4, k=3,
+                                         dtype="f16", seed=1),
+    # the batch-128 single-block case the throughput metric is quoted on
+    "block_n128_56x56_c64_e4_k3_f16": dict(kind="block", N=128, H=56, W=56, C=64, E=4, k=3,
+                                           dtype="f16", seed=2),
+    "block_n128_14x14_c256_e4_k7_f16": dict(kind="block", N=128, H=14, W=14, C=256, E=4, k=7,
+                                            dtype="f16", seed=3),
+    # four stages, depths 2/2/6/2, widths 64/128/256/512 at 56/28/14/7, 2x2/s2 down-sampling
+    "stack_n128_56x56_d2262_c64to512_e4_k3_f16": dict(kind="stack", N=128, H=56, W=56,
+                                                      depths=(2, 2, 6, 2),
+                                                      widths=(64, 128, 256, 512), E=4, k=3,
+                                                      dtype="f16", seed=4),
+    "block_n1_7x7_c512_e4_k3_bf16": dict(kind="block", N=1, H=7, W=7, C=512, E=4, k=3,
+                                         dtype="bf16", seed=5),
+}
+
+BENCH_WORKLOAD = "block_n128_56x56_c64_e4_k3_f16"
