@@ -1,0 +1,216 @@
+"""Benchmark of the fused ConvFirst block on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu] [--no-extra]
+
+A step is one fused-block forward over one batch (N = 128, 56 x 56, C = 64,
+E = 4, depth-wise 3 x 3, GELU(erf), fp16 NHWC) with inputs resident in HBM.
+Steps rotate over several x/y buffer sets whose total exceeds the 256 MB
+Infinity Cache, so a step never reads what the previous one wrote.  HIP
+events on the launch stream bracket exactly K steps after W warm-up steps.
+
+Prints ONE JSON line: images/s (value), ms per step, computational efficiency
+(FLOPs of the block at the dense fp16 MFMA peak divided by the measured
+latency), the roofline of the kernel, the fp64 CPU oracle timed on a bounded
+sample on the host cores, and the other workloads (block C = 256 k = 7, the
+four-stage stack, the layer-by-layer baseline, the N = 1 latency cases).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+import paper_2404_03617_amd as cf
+from paper_2404_03617_amd import roofline as rl
+from paper_2404_03617_amd import synth
+from paper_2404_03617_amd.workloads import BENCH_WORKLOAD, WORKLOADS
+
+MALL_BYTES = 256 << 20
+
+
+def _sets_needed(bytes_per_set: int) -> int:
+    return max(2, min(16, -(-2 * MALL_BYTES // max(bytes_per_set, 1))))
+
+
+def _time(fn, steps: int, warmup: int, stream) -> float:
+    """Seconds per step from HIP events on `stream`."""
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for i in range(steps):
+        fn(warmup + i)
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / 1e3 / steps
+
+
+def block_case(name: str, steps: int, warmup: int, act: str = "gelu", unfused: bool = False):
+    w = WORKLOADS[name]
+    N, H, W, C, E, k = w["N"], w["H"], w["W"], w["C"], w["E"], w["k"]
+    eb = 2
+    nsets = _sets_needed(2 * N * H * W * C * eb)
+    xs = [synth.activations(w["seed"] + 100 * i, N, H, W, C, w["dtype"]).cuda() for i in range(nsets)]
+    ys = [torch.empty_like(xs[0]) for _ in range(nsets)]
+    p = {kk: (None if v is None else v.cuda()) for kk, v in
+         synth.block_params(w["seed"], 0, C, E, k, w["dtype"]).items()}
+    stream = torch.cuda.current_stream()
+    if unfused:
+        ws = torch.empty(cf.lib().cf_unfused_workspace_bytes(N, H, W, C, E, 0), dtype=torch.uint8,
+                         device="cuda")
+        fn = lambda i: cf.block_forward_unfused(xs[i % nsets], p, act=act, out=ys[i % nsets], ws=ws)
+    else:
+        fn = lambda i: cf.block_forward(xs[i % nsets], p, act=act, out=ys[i % nsets])
+    t = _time(fn, steps, warmup, stream)
+    flops = rl.block_flops(N, H, W, C, E, k)
+    return dict(N=N, seconds=t, flops=flops, bytes=rl.block_bytes_fused(N, H, W, C, E, k, eb))
+
+
+def split_case(name: str, steps: int, warmup: int):
+    w = WORKLOADS[name]
+    N, H, W, C, E, k = w["N"], w["H"], w["W"], w["C"], w["E"], w["k"]
+    x = synth.activations(w["seed"], N, H, W, C, w["dtype"]).cuda()
+    y = torch.empty_like(x)
+    p = {kk: (None if v is None else v.cuda()) for kk, v in
+         synth.block_params(w["seed"], 0, C, E, k, w["dtype"]).items()}
+    ws = torch.empty(cf.lib().cf_split_workspace_bytes(N, H, W, C, E, 0), dtype=torch.uint8, device="cuda")
+    t = _time(lambda i: cf.block_forward_split(x, p, out=y, ws=ws), steps, warmup, torch.cuda.current_stream())
+    return dict(N=N, seconds=t, flops=rl.block_flops(N, H, W, C, E, k))
+
+
+def stack_case(name: str, steps: int, warmup: int):
+    w = WORKLOADS[name]
+    N, H, W = w["N"], w["H"], w["W"]
+    depths, widths, E, k = w["depths"], w["widths"], w["E"], w["k"]
+    layers = [(kd, {kk: (None if v is None else v.cuda()) for kk, v in p.items()})
+              for kd, p in synth.stack_layers(w["seed"], depths, widths, E, k, w["dtype"])]
+    nsets = 2
+    xs = [synth.activations(w["seed"] + 100 * i, N, H, W, widths[0], w["dtype"]).cuda() for i in range(nsets)]
+    # one output buffer per stage / down-sampling step
+    bufs = []
+    h, ww = H, W
+    for s, c in enumerate(widths):
+        if s > 0:
+            h, ww = h // 2, ww // 2
+            bufs.append(torch.empty((N, h, ww, c), dtype=xs[0].dtype, device="cuda"))
+        bufs.append(torch.empty((N, h, ww, c), dtype=xs[0].dtype, device="cuda"))
+    t = _time(lambda i: cf.stack_forward(xs[i % nsets], layers, bufs=bufs), steps, warmup,
+              torch.cuda.current_stream())
+    kern = rl.stack_kernels(N, H, W, depths, widths, E, k)
+    flops = sum(n for _, n, _ in kern)
+    T, cmax = rl.waterline([(n, b) for _, n, b in kern])
+    return dict(N=N, seconds=t, flops=flops, waterline_T_min_s=T, waterline_C_max=cmax)
+
+
+def cpu_baseline(name: str, images: int = 4):
+    """The fp64 oracle on `images` images of the workload, all host cores."""
+    import oracle
+    w = WORKLOADS[name]
+    x = synth.activations(w["seed"], images, w["H"], w["W"], w["C"], w["dtype"])
+    p = synth.params_f64(synth.block_params(w["seed"], 0, w["C"], w["E"], w["k"], w["dtype"]))
+    xd = synth.to_f64(x)
+    t0 = time.perf_counter()
+    _, used = oracle.block_forward(xd, p, act="gelu", return_threads=True)
+    dt = time.perf_counter() - t0
+    return {"value": images / dt, "unit": "images/s", "cores": int(used), "kind": "oracle",
+            "sample": "%d of %d images of %s, fp64 C loops, %.1f s" % (images, w["N"], name, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=BENCH_WORKLOAD)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-extra", action="store_true")
+    ap.add_argument("--cpu-images", type=int, default=8)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this library has no multi-GPU path; run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    cf.lib()
+    name = args.workload
+    w = WORKLOADS[name]
+    res = block_case(name, args.steps, args.warmup)
+    t = res["seconds"]
+    N = res["N"]
+    ips = N / t
+    eff = rl.comp_eff(res["flops"], t)
+    gbps = res["bytes"] / t / 1e9
+    t_hbm = res["bytes"] / rl.PEAK_HBM_BPS
+    t_mfma = res["flops"] / rl.PEAK_FP16_FLOPS
+    bound = "hbm" if t_hbm >= t_mfma else "mfma"
+    if bound == "hbm":
+        roof = {"bound": "hbm", "achieved": round(gbps, 1), "peak": rl.PEAK_HBM_BPS / 1e9, "unit": "GB/s",
+                "frac": round(gbps * 1e9 / rl.PEAK_HBM_BPS, 4), "traffic": None}
+    else:
+        tf = res["flops"] / t / 1e12
+        roof = {"bound": "mfma", "achieved": round(tf, 1), "peak": rl.PEAK_FP16_FLOPS / 1e12,
+                "unit": "TFLOP/s", "frac": round(tf * 1e12 / rl.PEAK_FP16_FLOPS, 4), "traffic": None}
+    out = {
+        "metric": "images/sec and % of fp16 MFMA peak (computational efficiency), batch 128",
+        "value": round(ips, 1),
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(t * 1e3, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic (seeded N(0,1) activations, N(0,1/fan_in) weights)",
+        "config": {"workload": name, "N": w["N"], "H": w["H"], "W": w["W"], "C": w["C"], "E": w["E"],
+                   "k": w["k"], "act": "gelu_erf", "kernel": "fused block (1 launch)"},
+        "comp_eff": round(eff, 4),
+        "tflops": round(res["flops"] / t / 1e12, 1),
+        "hbm_gbps_algorithmic": round(gbps, 1),
+        "roofline": roof,
+    }
+    if not args.no_extra:
+        extra = {}
+        u = block_case(name, max(5, args.steps // 5), 2, unfused=True)
+        extra["unfused_same_workload"] = {"ms": round(u["seconds"] * 1e3, 4),
+                                          "images_per_s": round(u["N"] / u["seconds"], 1),
+                                          "comp_eff": round(rl.comp_eff(u["flops"], u["seconds"]), 4),
+                                          "fused_speedup": round(u["seconds"] / t, 2)}
+        r = block_case(name, max(5, args.steps // 5), 2, act="relu")
+        extra["relu_same_workload"] = {"ms": round(r["seconds"] * 1e3, 4),
+                                       "comp_eff": round(rl.comp_eff(r["flops"], r["seconds"]), 4)}
+        for nm in WORKLOADS:
+            wk = WORKLOADS[nm]
+            if nm == name:
+                continue
+            if wk["kind"] == "block":
+                b = block_case(nm, max(5, args.steps // 2), 3)
+                e = {"ms": round(b["seconds"] * 1e3, 4), "images_per_s": round(b["N"] / b["seconds"], 1),
+                     "comp_eff": round(rl.comp_eff(b["flops"], b["seconds"]), 4)}
+                if wk["N"] * wk["H"] * wk["W"] <= 256:
+                    s = split_case(nm, max(5, args.steps // 2), 3)
+                    e["split_ms"] = round(s["seconds"] * 1e3, 4)
+                extra[nm] = e
+            else:
+                s = stack_case(nm, max(3, args.steps // 5), 2)
+                extra[nm] = {"ms": round(s["seconds"] * 1e3, 4), "images_per_s": round(s["N"] / s["seconds"], 1),
+                             "comp_eff": round(rl.comp_eff(s["flops"], s["seconds"]), 4),
+                             "waterline_C_max": round(s["waterline_C_max"], 4)}
+        out["other_workloads"] = extra
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(name, args.cpu_images)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,145 @@
+/*
+ * convfirst.h -- C ABI of the MI355X (gfx950) ConvFirst block-fusion library.
+ *
+ * The library evaluates the ConvFirst residual block of A. Lavin, "On the
+ * Efficiency of Convolutional Neural Networks" (arXiv:2404.03617), Sec. 5.3,
+ * with the block-fusion schedule of Sec. 5.3.1: one kernel loads an input
+ * tile, runs the k x k depth-wise convolution, initialises the output
+ * accumulators with the input tile (residual shortcut), then loops over
+ * chunks of hidden channels -- expand, activation, project -- in the
+ * loop-fused order of eq. e:ffn-eff, and stores the output tile once.  The
+ * hidden layer (E*C channels per pixel) never reaches device memory.
+ *
+ * Block definition (every batch norm folded into a per-channel scale and bias
+ * after its linear layer, Sec. 5.3.1 last paragraph):
+ *   D = s0 * dwconv_k(X) + b0                 depth-wise, zero padding k/2, Sec. 4.1.1
+ *   U = s1 * (D W1^T) + b1                    expand to E*C channels, eq. e:ffn
+ *   Z = s2 * (phi(U) W2^T) + b2               project back to C
+ *   Y = X + Z                                 residual shortcut
+ *
+ * Conventions shared by every entry point
+ *   - Pointers named x, y, w*, s*, b*, ws are DEVICE pointers; the
+ *     cf_*_params structs themselves live in host memory and are read during
+ *     the call only.
+ *   - Activations are NHWC, channels fastest: x[N][H][W][C].  All tensors of a
+ *     call share one I/O dtype (cf_dtype); scales and biases are fp32.
+ *   - A NULL scale means all ones; a NULL bias means all zeros.
+ *   - The caller owns every buffer.  The library allocates no device memory;
+ *     buffers must stay valid until the work queued on `stream` completes.
+ *   - Every *_forward call is asynchronous on `stream` (a hipStream_t passed
+ *     as void*; NULL is the null stream).  Nothing is synchronised.
+ *   - Arguments are validated on the host before anything is queued; on any
+ *     non-CF_OK status nothing was launched and outputs are untouched, except
+ *     CF_ERR_HIP, which reports a launch failure after validation passed.
+ *     cf_last_error() returns a thread-local message for the last failure.
+ *   - x, y and ws must not overlap each other (fused halos make in-place
+ *     evaluation unsafe) and must be 16-byte aligned.
+ *   - Results are deterministic: the same inputs give bit-identical outputs.
+ */
+#ifndef CONVFIRST_H
+#define CONVFIRST_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CF_ABI_VERSION 1
+
+typedef enum {
+    CF_OK = 0,
+    CF_ERR_INVALID = 1,     /* null pointer, bad size, overlap, misalignment, bad enum */
+    CF_ERR_UNSUPPORTED = 2, /* valid request this build has no kernel for (e.g. C % 32 != 0) */
+    CF_ERR_WORKSPACE = 3,   /* workspace smaller than the matching *_workspace_bytes() */
+    CF_ERR_HIP = 4          /* the HIP runtime reported an error at launch */
+} cf_status;
+
+typedef enum { CF_F16 = 0, CF_BF16 = 1 } cf_dtype;
+
+/* Activation phi after the expand layer (eq. e:ffn).  GELU is the exact
+ * Gaussian-CDF form u * Phi(u); the fp16 kernels evaluate it with a
+ * polynomial approximation whose absolute error is below 3.5e-3 for |u| < 10
+ * and below 1.3e-3 * |u| everywhere; bf16 kernels use fp32 erf.
+ * CF_ACT_NONE makes the block affine (used by tests). */
+typedef enum { CF_ACT_GELU_ERF = 0, CF_ACT_RELU = 1, CF_ACT_NONE = 2 } cf_act;
+
+/* Weights of one block (all device pointers).
+ *   dw_w  [k][k][C]     depth-wise taps (tap-major, channels fastest)
+ *   w1    [E*C][C]      expand, row r = hidden channel r (torch Linear layout)
+ *   w2    [C][E*C]      project, row c = output channel c
+ *   dw_scale/dw_bias [C], s1/b1 [E*C], s2/b2 [C]  fp32, each may be NULL */
+typedef struct {
+    const void *dw_w;
+    const float *dw_scale, *dw_bias;
+    const void *w1;
+    const float *s1, *b1;
+    const void *w2;
+    const float *s2, *b2;
+} cf_block_params;
+
+/* 2x2 stride-2 down-sampling conv: w [Cout][2][2][Cin]; scale/bias [Cout] fp32. */
+typedef struct {
+    const void *w;
+    const float *scale, *bias;
+} cf_down_params;
+
+/* One ConvFirst block, fused (Sec. 5.3.1, eq. e:ffn-eff): y = block(x).
+ * x, y: [N][H][W][C].  Supported: C in {64, 128, 256, 512}, E >= 1,
+ * k in {1, 3, 5, 7}; any N, H, W >= 1.  Other C return CF_ERR_UNSUPPORTED. */
+cf_status cf_block_forward(const void *x, void *y, const cf_block_params *p,
+                           int N, int H, int W, int C, int E, int k,
+                           cf_dtype dt, cf_act act, void *stream);
+
+/* `depth` consecutive blocks of the same shape (a network stage, the unit the
+ * paper benchmarks, Sec. 5.5.3).  Intermediate activations ping-pong between
+ * y and ws; blocks[depth] are host-side structs of device pointers.
+ * ws needs cf_stage_workspace_bytes() bytes (0 for depth == 1). */
+cf_status cf_stage_forward(const void *x, void *y, void *ws, size_t ws_bytes,
+                           const cf_block_params *blocks, int depth,
+                           int N, int H, int W, int C, int E, int k,
+                           cf_dtype dt, cf_act act, void *stream);
+size_t cf_stage_workspace_bytes(int depth, int N, int H, int W, int C, cf_dtype dt);
+
+/* 2x2 stride-2 conv between stages: y[n][i][j][o] = scale[o] * sum_{a,b,c}
+ * w[o][a][b][c] * x[n][2i+a][2j+b][c] + bias[o]  (eq. f:conv2d with R = S = 2,
+ * stride 2, no padding; no activation, no residual).  H and W must be even;
+ * y is [N][H/2][W/2][Cout].  Cin and Cout must be multiples of 32. */
+cf_status cf_downsample_forward(const void *x, void *y, const cf_down_params *p,
+                                int N, int H, int W, int Cin, int Cout,
+                                cf_dtype dt, void *stream);
+
+/* The same block executed layer by layer (Fig. f:convfirst-tensor-machine (a)):
+ * three kernels -- depth-wise, expand GEMM + activation, project GEMM +
+ * residual -- with the depth-wise output (P*C) and the hidden layer (P*E*C)
+ * round-tripping through ws.  The comparison path for the fused kernel. */
+cf_status cf_block_forward_unfused(const void *x, void *y, void *ws, size_t ws_bytes,
+                                   const cf_block_params *p,
+                                   int N, int H, int W, int C, int E, int k,
+                                   cf_dtype dt, cf_act act, void *stream);
+size_t cf_unfused_workspace_bytes(int N, int H, int W, int C, int E, cf_dtype dt);
+
+/* The fused block with its hidden channels split over `groups` workgroups per
+ * pixel tile, for small N*H*W where one tile per CU would idle the chip
+ * (the channel partition with partial sums of Sec. 5.3.1, Fig.
+ * f:convfirst-tensor-machine (c), applied to the hidden dimension).  Each
+ * group writes an fp32 partial of the projected output to ws; a second kernel
+ * adds the groups in a fixed order, plus b2 and the residual, so the result is
+ * deterministic.  groups must divide E*C/32; groups <= 0 picks a default.
+ * ws needs cf_split_workspace_bytes() bytes. */
+cf_status cf_block_forward_split(const void *x, void *y, void *ws, size_t ws_bytes,
+                                 const cf_block_params *p,
+                                 int N, int H, int W, int C, int E, int k, int groups,
+                                 cf_dtype dt, cf_act act, void *stream);
+size_t cf_split_workspace_bytes(int N, int H, int W, int C, int E, int groups);
+
+/* Thread-local message describing the most recent non-CF_OK status. */
+const char *cf_last_error(void);
+const char *cf_status_string(cf_status s);
+int cf_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CONVFIRST_H */

@@ -1,0 +1,311 @@
+// cf_api.hip -- the C ABI of include/convfirst.h: argument validation on the
+// host (no HIP call before every check has passed), dispatch to the launchers
+// of cf_fused.hip / cf_unfused.hip, and error reporting.
+#include "convfirst.h"
+#include "cf_kernels.h"
+
+#include <hip/hip_runtime.h>
+
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <string.h>
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+cf_status fail(cf_status s, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+cf_status hip_fail(hipError_t e, const char *what) {
+    return fail(CF_ERR_HIP, "%s: HIP error %d (%s)", what, (int)e, hipGetErrorString(e));
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+bool overlap(const void *a, size_t na, const void *b, size_t nb) {
+    const uintptr_t x0 = (uintptr_t)a, x1 = x0 + na, y0 = (uintptr_t)b, y1 = y0 + nb;
+    return x0 < y1 && y0 < x1;
+}
+
+size_t elem_bytes(cf_dtype dt) { return 2; }
+
+// Checks shared by every block entry point.  `what` names the entry point.
+cf_status check_block(const char *what, const void *x, const void *y, const cf_block_params *p, int N, int H, int W,
+                      int C, int E, int k, cf_dtype dt, cf_act act) {
+    if (!x || !y)
+        return fail(CF_ERR_INVALID, "%s: x and y must be non-NULL", what);
+    if (!p)
+        return fail(CF_ERR_INVALID, "%s: params must be non-NULL", what);
+    if (!p->dw_w || !p->w1 || !p->w2)
+        return fail(CF_ERR_INVALID, "%s: dw_w, w1 and w2 must be non-NULL", what);
+    if (N <= 0 || H <= 0 || W <= 0 || C <= 0 || E <= 0 || k <= 0)
+        return fail(CF_ERR_INVALID, "%s: sizes must be positive (N=%d H=%d W=%d C=%d E=%d k=%d)", what, N, H, W, C,
+                    E, k);
+    if (k % 2 == 0 || k > 7)
+        return fail(CF_ERR_INVALID, "%s: k must be 1, 3, 5 or 7 (got %d)", what, k);
+    if ((int)dt != CF_F16 && (int)dt != CF_BF16)
+        return fail(CF_ERR_INVALID, "%s: unknown dtype %d", what, (int)dt);
+    if ((int)act != CF_ACT_GELU_ERF && (int)act != CF_ACT_RELU && (int)act != CF_ACT_NONE)
+        return fail(CF_ERR_INVALID, "%s: unknown activation %d", what, (int)act);
+    const double elems = (double)N * H * W * C;
+    const double hidden = (double)E * C;
+    if (elems > 4.0e12 || hidden > 65536.0 || (double)H * W > 2.0e9)
+        return fail(CF_ERR_INVALID, "%s: tensor too large", what);
+    const void *ptrs[] = {x, y, p->dw_w, p->w1, p->w2, p->dw_scale, p->dw_bias, p->s1, p->b1, p->s2, p->b2};
+    for (const void *q : ptrs)
+        if (q && !aligned16(q))
+            return fail(CF_ERR_INVALID, "%s: every tensor pointer must be 16-byte aligned", what);
+    const size_t bytes = (size_t)N * H * W * C * elem_bytes(dt);
+    if (overlap(x, bytes, y, bytes))
+        return fail(CF_ERR_INVALID, "%s: x and y overlap (in-place evaluation is not supported)", what);
+    if (C != 64 && C != 128 && C != 256 && C != 512)
+        return fail(CF_ERR_UNSUPPORTED, "%s: C=%d has no kernel (supported: 64, 128, 256, 512)", what, C);
+    if ((double)N * H * W > 2147483647.0 - 4096.0)
+        return fail(CF_ERR_UNSUPPORTED, "%s: N*H*W must stay below 2^31 pixels", what);
+    return CF_OK;
+}
+
+cf::BlockW to_w(const cf_block_params *p) {
+    cf::BlockW w;
+    w.dw_w = p->dw_w;
+    w.s0 = p->dw_scale;
+    w.b0 = p->dw_bias;
+    w.w1 = p->w1;
+    w.s1 = p->s1;
+    w.b1 = p->b1;
+    w.w2 = p->w2;
+    w.s2 = p->s2;
+    w.b2 = p->b2;
+    return w;
+}
+
+cf::Shape to_shape(int N, int H, int W, int C, int E, int k, cf_dtype dt, cf_act act) {
+    cf::Shape s;
+    s.N = N;
+    s.H = H;
+    s.W = W;
+    s.C = C;
+    s.E = E;
+    s.k = k;
+    s.bf16 = dt == CF_BF16;
+    s.act = (int)act;
+    return s;
+}
+
+cf_status check_fit(const char *what, const cf::Shape &s) {
+    const size_t lds = cf::fused_lds_bytes(s);
+    if (lds == 0 || lds > 160 * 1024)
+        return fail(CF_ERR_UNSUPPORTED, "%s: tile for W=%d C=%d k=%d needs %zu bytes of LDS (limit 163840)", what, s.W,
+                    s.C, s.k, lds);
+    return CF_OK;
+}
+
+size_t round256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+int default_groups(int N, int H, int W, int C, int E) {
+    // enough (tile, group) pairs to give every CU one, with groups | E*C/32
+    const int chunks = E * C / 32;
+    const int64_t P = (int64_t)N * H * W;
+    const int M = C == 64 ? 256 : C == 512 ? 64 : 128;
+    const int64_t tiles = (P + M - 1) / M;
+    int best = 1;
+    for (int g = 1; g <= chunks; g++) {
+        if (chunks % g)
+            continue;
+        if (tiles * g <= 256)
+            best = g;
+    }
+    return best;
+}
+
+}  // namespace
+
+extern "C" {
+
+int cf_abi_version(void) { return CF_ABI_VERSION; }
+
+const char *cf_last_error(void) { return g_err; }
+
+const char *cf_status_string(cf_status s) {
+    switch (s) {
+    case CF_OK: return "CF_OK";
+    case CF_ERR_INVALID: return "CF_ERR_INVALID";
+    case CF_ERR_UNSUPPORTED: return "CF_ERR_UNSUPPORTED";
+    case CF_ERR_WORKSPACE: return "CF_ERR_WORKSPACE";
+    case CF_ERR_HIP: return "CF_ERR_HIP";
+    }
+    return "unknown cf_status";
+}
+
+cf_status cf_block_forward(const void *x, void *y, const cf_block_params *p, int N, int H, int W, int C, int E, int k,
+                           cf_dtype dt, cf_act act, void *stream) {
+    cf_status st = check_block("cf_block_forward", x, y, p, N, H, W, C, E, k, dt, act);
+    if (st != CF_OK)
+        return st;
+    const cf::Shape s = to_shape(N, H, W, C, E, k, dt, act);
+    if ((st = check_fit("cf_block_forward", s)) != CF_OK)
+        return st;
+    hipError_t e = cf::launch_fused_block(x, y, to_w(p), s, 1, nullptr, (hipStream_t)stream);
+    if (e != hipSuccess)
+        return hip_fail(e, "cf_block_forward");
+    g_err[0] = 0;
+    return CF_OK;
+}
+
+size_t cf_stage_workspace_bytes(int depth, int N, int H, int W, int C, cf_dtype dt) {
+    if (depth <= 1 || N <= 0 || H <= 0 || W <= 0 || C <= 0)
+        return 0;
+    return (size_t)N * H * W * C * elem_bytes(dt);
+}
+
+cf_status cf_stage_forward(const void *x, void *y, void *ws, size_t ws_bytes, const cf_block_params *blocks,
+                           int depth, int N, int H, int W, int C, int E, int k, cf_dtype dt, cf_act act,
+                           void *stream) {
+    if (depth <= 0 || !blocks)
+        return fail(CF_ERR_INVALID, "cf_stage_forward: depth must be positive and blocks non-NULL");
+    for (int i = 0; i < depth; i++) {
+        cf_status st = check_block("cf_stage_forward", x, y, &blocks[i], N, H, W, C, E, k, dt, act);
+        if (st != CF_OK)
+            return st;
+    }
+    const size_t need = cf_stage_workspace_bytes(depth, N, H, W, C, dt);
+    const size_t bytes = (size_t)N * H * W * C * elem_bytes(dt);
+    if (need) {
+        if (!ws)
+            return fail(CF_ERR_INVALID, "cf_stage_forward: ws must be non-NULL for depth > 1");
+        if (!aligned16(ws))
+            return fail(CF_ERR_INVALID, "cf_stage_forward: ws must be 16-byte aligned");
+        if (ws_bytes < need)
+            return fail(CF_ERR_WORKSPACE, "cf_stage_forward: ws has %zu bytes, needs %zu", ws_bytes, need);
+        if (overlap(ws, need, x, bytes) || overlap(ws, need, y, bytes))
+            return fail(CF_ERR_INVALID, "cf_stage_forward: ws overlaps x or y");
+    }
+    const cf::Shape s = to_shape(N, H, W, C, E, k, dt, act);
+    cf_status st = check_fit("cf_stage_forward", s);
+    if (st != CF_OK)
+        return st;
+    // block i writes y when (depth-1-i) is even, else ws, so the last one lands in y
+    const void *in = x;
+    for (int i = 0; i < depth; i++) {
+        void *out = ((depth - 1 - i) % 2 == 0) ? y : ws;
+        hipError_t e = cf::launch_fused_block(in, out, to_w(&blocks[i]), s, 1, nullptr, (hipStream_t)stream);
+        if (e != hipSuccess)
+            return hip_fail(e, "cf_stage_forward");
+        in = out;
+    }
+    g_err[0] = 0;
+    return CF_OK;
+}
+
+cf_status cf_downsample_forward(const void *x, void *y, const cf_down_params *p, int N, int H, int W, int Cin,
+                                int Cout, cf_dtype dt, void *stream) {
+    const char *what = "cf_downsample_forward";
+    if (!x || !y || !p || !p->w)
+        return fail(CF_ERR_INVALID, "%s: x, y, params and w must be non-NULL", what);
+    if (N <= 0 || H <= 0 || W <= 0 || Cin <= 0 || Cout <= 0)
+        return fail(CF_ERR_INVALID, "%s: sizes must be positive", what);
+    if ((int)dt != CF_F16 && (int)dt != CF_BF16)
+        return fail(CF_ERR_INVALID, "%s: unknown dtype %d", what, (int)dt);
+    if ((double)N * H * W * (Cin > Cout ? Cin : Cout) > 4.0e12)
+        return fail(CF_ERR_INVALID, "%s: tensor too large", what);
+    const void *ptrs[] = {x, y, p->w, p->scale, p->bias};
+    for (const void *q : ptrs)
+        if (q && !aligned16(q))
+            return fail(CF_ERR_INVALID, "%s: every tensor pointer must be 16-byte aligned", what);
+    const size_t xb = (size_t)N * H * W * Cin * 2, yb = (size_t)N * (H / 2) * (W / 2) * Cout * 2;
+    if (overlap(x, xb, y, yb))
+        return fail(CF_ERR_INVALID, "%s: x and y overlap", what);
+    if (H % 2 || W % 2)
+        return fail(CF_ERR_UNSUPPORTED, "%s: H and W must be even (got %d x %d)", what, H, W);
+    if (Cin % 32 || Cout % 64)
+        return fail(CF_ERR_UNSUPPORTED, "%s: needs Cin %% 32 == 0 and Cout %% 64 == 0 (got %d, %d)", what, Cin,
+                    Cout);
+    hipError_t e = cf::launch_downsample(x, y, p->w, p->scale, p->bias, N, H, W, Cin, Cout, dt == CF_BF16,
+                                         (hipStream_t)stream);
+    if (e != hipSuccess)
+        return hip_fail(e, what);
+    g_err[0] = 0;
+    return CF_OK;
+}
+
+size_t cf_unfused_workspace_bytes(int N, int H, int W, int C, int E, cf_dtype dt) {
+    if (N <= 0 || H <= 0 || W <= 0 || C <= 0 || E <= 0)
+        return 0;
+    const size_t P = (size_t)N * H * W;
+    return round256(P * C * elem_bytes(dt)) + P * (size_t)E * C * elem_bytes(dt);
+}
+
+cf_status cf_block_forward_unfused(const void *x, void *y, void *ws, size_t ws_bytes, const cf_block_params *p, int N,
+                                   int H, int W, int C, int E, int k, cf_dtype dt, cf_act act, void *stream) {
+    const char *what = "cf_block_forward_unfused";
+    cf_status st = check_block(what, x, y, p, N, H, W, C, E, k, dt, act);
+    if (st != CF_OK)
+        return st;
+    const size_t need = cf_unfused_workspace_bytes(N, H, W, C, E, dt);
+    const size_t bytes = (size_t)N * H * W * C * elem_bytes(dt);
+    if (!ws)
+        return fail(CF_ERR_INVALID, "%s: ws must be non-NULL", what);
+    if (!aligned16(ws))
+        return fail(CF_ERR_INVALID, "%s: ws must be 16-byte aligned", what);
+    if (ws_bytes < need)
+        return fail(CF_ERR_WORKSPACE, "%s: ws has %zu bytes, needs %zu", what, ws_bytes, need);
+    if (overlap(ws, need, x, bytes) || overlap(ws, need, y, bytes))
+        return fail(CF_ERR_INVALID, "%s: ws overlaps x or y", what);
+    void *d = ws;
+    void *h = (char *)ws + round256((size_t)N * H * W * C * elem_bytes(dt));
+    hipError_t e = cf::launch_unfused_block(x, y, d, h, to_w(p), to_shape(N, H, W, C, E, k, dt, act),
+                                            (hipStream_t)stream);
+    if (e != hipSuccess)
+        return hip_fail(e, what);
+    g_err[0] = 0;
+    return CF_OK;
+}
+
+size_t cf_split_workspace_bytes(int N, int H, int W, int C, int E, int groups) {
+    if (N <= 0 || H <= 0 || W <= 0 || C <= 0 || E <= 0)
+        return 0;
+    if (groups <= 0)
+        groups = default_groups(N, H, W, C, E);
+    return (size_t)groups * N * H * W * C * sizeof(float);
+}
+
+cf_status cf_block_forward_split(const void *x, void *y, void *ws, size_t ws_bytes, const cf_block_params *p, int N,
+                                 int H, int W, int C, int E, int k, int groups, cf_dtype dt, cf_act act,
+                                 void *stream) {
+    const char *what = "cf_block_forward_split";
+    cf_status st = check_block(what, x, y, p, N, H, W, C, E, k, dt, act);
+    if (st != CF_OK)
+        return st;
+    if (groups <= 0)
+        groups = default_groups(N, H, W, C, E);
+    const int chunks = E * C / 32;
+    if (groups > chunks || chunks % groups)
+        return fail(CF_ERR_INVALID, "%s: groups=%d must divide E*C/32=%d", what, groups, chunks);
+    const size_t need = cf_split_workspace_bytes(N, H, W, C, E, groups);
+    const size_t bytes = (size_t)N * H * W * C * elem_bytes(dt);
+    if (!ws)
+        return fail(CF_ERR_INVALID, "%s: ws must be non-NULL", what);
+    if (!aligned16(ws))
+        return fail(CF_ERR_INVALID, "%s: ws must be 16-byte aligned", what);
+    if (ws_bytes < need)
+        return fail(CF_ERR_WORKSPACE, "%s: ws has %zu bytes, needs %zu", what, ws_bytes, need);
+    if (overlap(ws, need, x, bytes) || overlap(ws, need, y, bytes))
+        return fail(CF_ERR_INVALID, "%s: ws overlaps x or y", what);
+    const cf::Shape s = to_shape(N, H, W, C, E, k, dt, act);
+    if ((st = check_fit(what, s)) != CF_OK)
+        return st;
+    hipError_t e = cf::launch_fused_block(x, y, to_w(p), s, groups, (float *)ws, (hipStream_t)stream);
+    if (e != hipSuccess)
+        return hip_fail(e, what);
+    g_err[0] = 0;
+    return CF_OK;
+}
+
+}  // extern "C"

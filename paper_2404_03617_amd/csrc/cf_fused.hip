@@ -1,0 +1,136 @@
+// cf_fused.hip -- the ConvFirst block-fusion kernel for gfx950 (MI355X).
+//
+// One workgroup (4 waves) owns a tile of M consecutive pixels of the
+// flattened N*H*W index and evaluates the whole residual block for it
+// (Sec. 5.3.1 of Lavin, arXiv:2404.03617):
+//   1. the input rows the tile touches, plus k/2 halo rows, are copied into
+//      LDS with 16-byte loads, in channel slabs of at most 64 channels;
+//   2. each lane runs the k x k depth-wise conv for 16-pixel blocks on the
+//      VALU and keeps the result as MFMA B-operand fragments in registers;
+//   3. the output accumulators (fp32, in registers) start from the input
+//      tile centre plus b2: the residual shortcut costs no extra HBM read;
+//   4. a loop over chunks of 32 hidden channels (eq. e:ffn-eff) computes
+//      H^T = W1_chunk * D^T on MFMA 16x16x32 with b1 in the C operand, applies
+//      phi, and feeds the result straight from the accumulator registers into
+//      the project MFMA  Out^T += W2_chunk * H^T  -- the hidden tile never
+//      touches LDS or HBM;
+//   5. the output tile is converted (round to nearest even) and stored once.
+//
+// Transposed ("swap-AB") products make the MFMA output layout (4 consecutive
+// rows per lane) line up with the operand layout of the next MFMA.  Within a
+// chunk of 32 hidden channels the expand rows are gathered in the order
+// sigma(rb, m) = 8*(m/4) + 4*rb + m%4 so that lane group g ends up holding
+// hidden channels 8g..8g+7: then both weight fragments are single contiguous
+// 16-byte loads and the project K index is the hidden index.
+//
+// Weights are staged per chunk into LDS in fragment order (lane-contiguous,
+// conflict-free ds_read_b128), with s1/s2 folded in while staging.  When all
+// E*C/32 chunks fit in LDS (C = 64) they are staged once per persistent
+// workgroup; otherwise they stream through a double buffer per tile.
+//
+// Hidden-split mode (grid.y > 1): workgroup (tile, g) runs only its range of
+// chunks and writes an fp32 partial of the projected output; a second kernel
+// adds the partials in group order plus b2 and the residual.
+#include "cf_fused_impl.h"
+
+#include <mutex>
+
+namespace cf {
+
+namespace fused {
+namespace {
+
+// y = x + b2 + sum_g partial[g]  (groups added in increasing order)
+template <typename T>
+__global__ __launch_bounds__(256) void split_reduce_kernel(const uint16_t *x, uint16_t *y, const float *partial,
+                                                           const float *b2, int64_t P, int C, int groups) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // one thread per 4 channels
+    const int64_t n4 = P * C / 4;
+    if (i >= n4)
+        return;
+    const int64_t e = i * 4;
+    const int c = (int)(e % C);
+    float4v s = b2 ? *reinterpret_cast<const float4v *>(b2 + c) : float4v{0.f, 0.f, 0.f, 0.f};
+    for (int gi = 0; gi < groups; gi++)
+        s += *reinterpret_cast<const float4v *>(partial + (size_t)gi * P * C + e);
+    const u32x2 xv = *reinterpret_cast<const u32x2 *>(x + e);
+    u32x2 o;
+    o[0] = T::pack2(T::lo(xv[0]) + s[0], T::hi(xv[0]) + s[1]);
+    o[1] = T::pack2(T::lo(xv[1]) + s[2], T::hi(xv[1]) + s[3]);
+    *reinterpret_cast<u32x2 *>(y + e) = o;
+}
+
+}  // namespace
+}  // namespace fused
+
+using namespace fused;
+
+int device_cu_count() {
+    static std::mutex mu;
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return 256;
+    std::lock_guard<std::mutex> lk(mu);
+    if (!cached[dev]) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            n = 256;
+        cached[dev] = n;
+    }
+    return cached[dev];
+}
+
+size_t fused_lds_bytes(const Shape &s) {
+    if (s.C != 64 && s.C != 128 && s.C != 256 && s.C != 512)
+        return 0;
+    const int64_t P = (int64_t)s.N * s.H * s.W;
+    return lds_bytes_for(s.C, s.k, s.W, s.E, P, 1, false, 1);
+}
+
+hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Shape &s, int groups,
+                              float *partial, hipStream_t st) {
+    FusedArgs a{};
+    a.x = (const uint16_t *)x;
+    a.y = (uint16_t *)y;
+    a.dw_w = (const uint16_t *)w.dw_w;
+    a.s0 = w.s0;
+    a.b0 = w.b0;
+    a.w1 = (const uint16_t *)w.w1;
+    a.s1 = w.s1;
+    a.b1 = w.b1;
+    a.w2 = (const uint16_t *)w.w2;
+    a.s2 = w.s2;
+    a.b2 = w.b2;
+    a.partial = partial;
+    a.N = s.N;
+    a.H = s.H;
+    a.W = s.W;
+    a.E = s.E;
+    a.P = (uint32_t)((int64_t)s.N * s.H * s.W);
+    hipError_t e;
+    switch (s.C * 2 + s.bf16) {
+    case 128: e = launch_c64_F16(a, s.k, s.act, groups, st); break;
+    case 129: e = launch_c64_BF16(a, s.k, s.act, groups, st); break;
+    case 256: e = launch_c128_F16(a, s.k, s.act, groups, st); break;
+    case 257: e = launch_c128_BF16(a, s.k, s.act, groups, st); break;
+    case 512: e = launch_c256_F16(a, s.k, s.act, groups, st); break;
+    case 513: e = launch_c256_BF16(a, s.k, s.act, groups, st); break;
+    case 1024: e = launch_c512_F16(a, s.k, s.act, groups, st); break;
+    case 1025: e = launch_c512_BF16(a, s.k, s.act, groups, st); break;
+    default: return hipErrorInvalidValue;
+    }
+    if (e != hipSuccess || groups <= 1)
+        return e;
+    const int64_t n4 = (int64_t)a.P * s.C / 4;
+    const int nb = (int)((n4 + 255) / 256);
+    if (s.bf16)
+        hipLaunchKernelGGL(split_reduce_kernel<BF16>, dim3(nb), dim3(256), 0, st, a.x, a.y, partial, w.b2, a.P, s.C,
+                           groups);
+    else
+        hipLaunchKernelGGL(split_reduce_kernel<F16>, dim3(nb), dim3(256), 0, st, a.x, a.y, partial, w.b2, a.P, s.C,
+                           groups);
+    return hipGetLastError();
+}
+
+}  // namespace cf

@@ -1,0 +1,10 @@
+// Fused-block kernel instantiations for C = 128, BF16 I/O.
+#include "cf_fused_impl.h"
+
+namespace cf {
+namespace fused {
+hipError_t launch_c128_BF16(const FusedArgs &a, int k, int act, int groups, hipStream_t st) {
+    return launch_ct<128, BF16>(a, k, act, groups, st);
+}
+}  // namespace fused
+}  // namespace cf

@@ -1,0 +1,49 @@
+// cf_kernels.h -- host-side launcher interface between the C ABI layer
+// (cf_api.cpp) and the HIP kernels.  Internal; argument checking has already
+// happened when these are called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace cf {
+
+struct BlockW {
+    const void *dw_w;
+    const float *s0, *b0;
+    const void *w1;
+    const float *s1, *b1;
+    const void *w2;
+    const float *s2, *b2;
+};
+
+struct Shape {
+    int N, H, W, C, E, k;
+    int bf16;  // 0: fp16, 1: bf16
+    int act;   // 0 GELU(erf), 1 ReLU, 2 identity
+};
+
+// Fused block.  groups > 1 selects the hidden-split variant: partial (fp32,
+// [groups][N*H*W][C]) receives each group's projection and a reduction kernel
+// writes y.  Returns hipSuccess or the launch error.
+hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Shape &s,
+                              int groups, float *partial, hipStream_t st);
+
+// Layer-by-layer path: depth-wise -> d, expand + act -> h, project + residual -> y.
+hipError_t launch_unfused_block(const void *x, void *y, void *d, void *h, const BlockW &w,
+                                const Shape &s, hipStream_t st);
+
+// 2x2 stride-2 conv as a GEMM over the space-to-depth view of x.
+hipError_t launch_downsample(const void *x, void *y, const void *wd, const float *sd,
+                             const float *bd, int N, int H, int W, int Cin, int Cout, int bf16,
+                             hipStream_t st);
+
+// Upper bound of dynamic LDS the fused kernel needs for this shape (bytes);
+// 0 when no kernel configuration fits.
+size_t fused_lds_bytes(const Shape &s);
+
+// Number of compute units of the current device (cached per device).
+int device_cu_count();
+
+}  // namespace cf

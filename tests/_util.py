@@ -1,0 +1,36 @@
+"""Shared helpers for the tests: seeded inputs, oracle calls, error metrics."""
+import numpy as np
+import torch
+
+import oracle
+from paper_2404_03617_amd import synth
+
+# max |gpu - ref| <= TOL * max |ref|, for fp16 and bf16 I/O alike
+TOL = 2e-2
+
+
+def make_block(seed, N, H, W, C, E, k, dtype="f16", scales="uniform", bias_std=1.0, layer=0):
+    x = synth.activations(seed, N, H, W, C, dtype)
+    p = synth.block_params(seed, layer, C, E, k, dtype, scales=scales, bias_std=bias_std)
+    return x, p
+
+
+def to_dev(p, dev="cuda"):
+    return {k: (None if v is None else v.to(dev)) for k, v in p.items()}
+
+
+def oracle_block(x, p, act="gelu", images=None):
+    xs = x if images is None else x[list(images)]
+    return oracle.block_forward(synth.to_f64(xs), synth.params_f64(p), act=act)
+
+
+def rel_err(gpu, ref):
+    g = gpu.detach().to("cpu").to(torch.float64).numpy() if isinstance(gpu, torch.Tensor) else gpu
+    err = np.abs(g - ref)
+    return float(err.max() / max(np.abs(ref).max(), 1e-30)), float(err.max()), float(np.abs(ref).max())
+
+
+def assert_close(gpu, ref, tol=TOL, what=""):
+    r, e, m = rel_err(gpu, ref)
+    assert r <= tol, "%s: max|err|=%.3e max|ref|=%.3e ratio=%.3e > %.1e" % (what, e, m, r, tol)
+    return r

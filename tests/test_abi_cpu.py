@@ -1,0 +1,123 @@
+"""The C ABI library on a host without a GPU: it loads, exports every entry
+point that include/convfirst.h declares, and rejects bad arguments before any
+HIP call.  No compute call is made here."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2404_03617_amd as cf
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "convfirst.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(cf.library_path()),
+                                reason="libconvfirst.so not built")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(cf_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_binding_symbols():
+    assert set(declared_functions()) == set(cf.EXPORTED_SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = ctypes.CDLL(cf.library_path())
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_abi_version_and_status_strings():
+    L = cf.lib()
+    assert L.cf_abi_version() == 1
+    for s, name in enumerate(["CF_OK", "CF_ERR_INVALID", "CF_ERR_UNSUPPORTED", "CF_ERR_WORKSPACE",
+                              "CF_ERR_HIP"]):
+        assert L.cf_status_string(s).decode() == name
+
+
+# Fake, aligned, non-overlapping "device" addresses: validation never touches them.
+X, Y, WS = 0x10000000, 0x20000000, 0x30000000
+DW, W1, W2 = 0x40000000, 0x41000000, 0x42000000
+
+
+def params(**kw):
+    base = dict(dw_w=DW, dw_scale=None, dw_bias=None, w1=W1, s1=None, b1=None, w2=W2, s2=None,
+                b2=None)
+    base.update(kw)
+    return cf._BlockParams(**base)
+
+
+def block(x=X, y=Y, p=None, N=1, H=8, W=8, C=64, E=4, k=3, dt=0, act=0):
+    p = params() if p is None else p
+    return cf.lib().cf_block_forward(x, y, ctypes.byref(p), N, H, W, C, E, k, dt, act, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=None), cf.CF_ERR_INVALID),
+    (dict(y=None), cf.CF_ERR_INVALID),
+    (dict(p=params(dw_w=None)), cf.CF_ERR_INVALID),
+    (dict(p=params(w1=None)), cf.CF_ERR_INVALID),
+    (dict(p=params(w2=None)), cf.CF_ERR_INVALID),
+    (dict(N=0), cf.CF_ERR_INVALID),
+    (dict(H=-1), cf.CF_ERR_INVALID),
+    (dict(E=0), cf.CF_ERR_INVALID),
+    (dict(k=2), cf.CF_ERR_INVALID),
+    (dict(k=9), cf.CF_ERR_INVALID),
+    (dict(dt=7), cf.CF_ERR_INVALID),
+    (dict(act=5), cf.CF_ERR_INVALID),
+    (dict(x=X + 8), cf.CF_ERR_INVALID),                      # misaligned
+    (dict(p=params(b1=W1 + 4)), cf.CF_ERR_INVALID),          # misaligned bias
+    (dict(y=X + 64), cf.CF_ERR_INVALID),                     # overlaps x
+    (dict(C=48), cf.CF_ERR_UNSUPPORTED),
+    (dict(C=96), cf.CF_ERR_UNSUPPORTED),
+    (dict(W=4096), cf.CF_ERR_UNSUPPORTED),                   # halo does not fit LDS
+])
+def test_block_forward_rejects(kw, status):
+    assert block(**kw) == status
+    assert cf.lib().cf_last_error().decode().startswith("cf_block_forward")
+
+
+def test_workspace_queries():
+    L = cf.lib()
+    P = 2 * 5 * 7
+    assert L.cf_stage_workspace_bytes(1, 2, 5, 7, 64, 0) == 0
+    assert L.cf_stage_workspace_bytes(3, 2, 5, 7, 64, 0) == P * 64 * 2
+    need = L.cf_unfused_workspace_bytes(2, 5, 7, 64, 4, 0)
+    assert need >= P * 64 * 2 + P * 256 * 2
+    assert L.cf_split_workspace_bytes(1, 7, 7, 512, 4, 8) == 8 * 49 * 512 * 4
+
+
+def test_stage_and_unfused_and_split_reject_short_workspace():
+    L = cf.lib()
+    p = params()
+    arr = (cf._BlockParams * 2)(p, p)
+    assert L.cf_stage_forward(X, Y, WS, 16, arr, 2, 1, 8, 8, 64, 4, 3, 0, 0, None) == cf.CF_ERR_WORKSPACE
+    assert L.cf_stage_forward(X, Y, None, 0, arr, 2, 1, 8, 8, 64, 4, 3, 0, 0, None) == cf.CF_ERR_INVALID
+    assert L.cf_stage_forward(X, Y, X, 1 << 20, arr, 2, 1, 8, 8, 64, 4, 3, 0, 0, None) == cf.CF_ERR_INVALID
+    assert L.cf_block_forward_unfused(X, Y, WS, 16, ctypes.byref(p), 1, 8, 8, 64, 4, 3, 0, 0,
+                                      None) == cf.CF_ERR_WORKSPACE
+    assert L.cf_block_forward_split(X, Y, WS, 16, ctypes.byref(p), 1, 8, 8, 64, 4, 3, 2, 0, 0,
+                                    None) == cf.CF_ERR_WORKSPACE
+    # groups must divide E*C/32 = 8
+    assert L.cf_block_forward_split(X, Y, WS, 1 << 30, ctypes.byref(p), 1, 8, 8, 64, 4, 3, 3, 0, 0,
+                                    None) == cf.CF_ERR_INVALID
+
+
+def test_downsample_rejects():
+    L = cf.lib()
+    dp = cf._DownParams(w=W1, scale=None, bias=None)
+    ok = dict(N=1, H=8, W=8, Cin=64, Cout=128)
+    def call(x=X, y=Y, p=dp, N=1, H=8, W=8, Cin=64, Cout=128, dt=0):
+        return L.cf_downsample_forward(x, y, ctypes.byref(p) if p is not None else None, N, H, W,
+                                       Cin, Cout, dt, None)
+    assert call(H=7) == cf.CF_ERR_UNSUPPORTED
+    assert call(Cout=96) == cf.CF_ERR_UNSUPPORTED
+    assert call(x=None) == cf.CF_ERR_INVALID
+    assert call(p=cf._DownParams(w=None)) == cf.CF_ERR_INVALID
+    assert call(y=X + 16) == cf.CF_ERR_INVALID
+    assert call(dt=3) == cf.CF_ERR_INVALID

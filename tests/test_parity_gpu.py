@@ -1,0 +1,157 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle.
+
+Gate: max |gpu - oracle| <= 2e-2 * max |oracle| (fp16 and bf16 I/O).
+Small shapes are compared element by element over the whole output; the
+batch-128 workloads are run at full size and compared on a subset of images
+(images are independent: see the oracle's batch-independence pin)."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2404_03617_amd as cf
+from paper_2404_03617_amd import synth
+from paper_2404_03617_amd.workloads import WORKLOADS
+
+from _util import TOL, assert_close, make_block, oracle_block, rel_err, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+SWEEP = [
+    # C, E, k, N, H, W
+    (64, 4, 3, 2, 9, 13),
+    (64, 4, 3, 1, 14, 14),
+    (64, 2, 1, 3, 5, 7),
+    (64, 1, 5, 1, 6, 17),
+    (64, 4, 7, 2, 3, 4),     # H, W < k: every tap row/column crosses the border
+    (64, 6, 3, 1, 1, 1),     # a single pixel
+    (64, 3, 3, 1, 1, 37),    # one row
+    (64, 4, 3, 1, 40, 1),    # one column
+    (128, 4, 3, 2, 11, 10),
+    (128, 2, 5, 1, 7, 9),
+    (256, 4, 7, 2, 14, 14),
+    (256, 1, 3, 1, 5, 6),
+    (512, 4, 3, 1, 7, 7),
+    (512, 2, 1, 2, 3, 5),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("case", SWEEP, ids=lambda c: "C%d_E%d_k%d_N%d_%dx%d" % c)
+def test_fused_block_matches_oracle(case, dtype):
+    C, E, k, N, H, W = case
+    say("fused", case, dtype)
+    x, p = make_block(11, N, H, W, C, E, k, dtype)
+    for act in ("gelu", "relu", "none"):
+        y = cf.block_forward(x.cuda(), to_dev(p), act=act)
+        torch.cuda.synchronize()
+        assert_close(y, oracle_block(x, p, act), what="%s %s %s" % (case, dtype, act))
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("case", [(64, 4, 3, 2, 9, 13), (128, 2, 5, 1, 7, 9), (256, 4, 7, 1, 14, 14),
+                                  (512, 4, 3, 1, 7, 7)], ids=lambda c: "C%d_E%d_k%d_N%d_%dx%d" % c)
+def test_unfused_and_split_match_oracle(case, dtype):
+    C, E, k, N, H, W = case
+    say("unfused/split", case, dtype)
+    x, p = make_block(12, N, H, W, C, E, k, dtype)
+    ref = oracle_block(x, p, "gelu")
+    xd, pd = x.cuda(), to_dev(p)
+    assert_close(cf.block_forward_unfused(xd, pd), ref, what="unfused")
+    chunks = E * C // 32
+    for groups in sorted({1, 2, chunks}):
+        assert_close(cf.block_forward_split(xd, pd, groups=groups), ref, what="split g=%d" % groups)
+
+
+def test_default_scales_and_no_biases():
+    """NULL scales (ones) and NULL biases (zeros) take the same path as explicit ones."""
+    say("null scales")
+    x, p = make_block(13, 2, 8, 9, 64, 4, 3, "f16", scales="none", bias_std=None)
+    y = cf.block_forward(x.cuda(), to_dev(p))
+    assert_close(y, oracle_block(x, p), what="null scale/bias")
+
+
+def test_zero_project_weights_pass_the_residual_exactly():
+    say("zero w2")
+    x, p = make_block(14, 2, 7, 9, 128, 4, 3, "f16", scales="uniform", bias_std=1.0)
+    p["w2"] = torch.zeros_like(p["w2"])
+    p["b2"] = None
+    y = cf.block_forward(x.cuda(), to_dev(p))
+    assert torch.equal(y.cpu(), x)
+
+
+def test_deterministic_and_batch_independent():
+    say("determinism")
+    x, p = make_block(15, 3, 12, 12, 64, 4, 3, "f16")
+    xd, pd = x.cuda(), to_dev(p)
+    a = cf.block_forward(xd, pd)
+    b = cf.block_forward(xd, pd)
+    assert torch.equal(a, b)
+    one = cf.block_forward(xd[1:2].contiguous(), pd)
+    assert torch.equal(a[1:2], one)
+
+
+def test_stage_and_downsample_match_oracle():
+    say("stage+down")
+    layers = synth.stack_layers(16, depths=(2, 1), widths=(64, 128), E=4, k=3, dtype="f16",
+                                scales="uniform", bias_std=0.5)
+    x = synth.activations(16, 2, 12, 10, 64, "f16")
+    y = cf.stack_forward(x.cuda(), [(kd, to_dev(p)) for kd, p in layers])
+    ref = oracle.stack_forward(synth.to_f64(x), [(kd, synth.params_f64(p)) for kd, p in layers])
+    assert y.shape == (2, 6, 5, 128)
+    assert_close(y, ref, what="stage+down")
+    # the down-sampling layer alone
+    pdn = layers[2][1]
+    z = cf.downsample_forward(x.cuda(), to_dev(pdn))
+    refz = oracle.downsample(synth.to_f64(x), *[synth.to_f64(pdn[n]) for n in ("wd", "sd", "bd")])
+    assert_close(z, refz, tol=1e-2, what="downsample")
+
+
+# ---------------------------------------------------------------- the five workloads
+def _workload_inputs(name):
+    w = WORKLOADS[name]
+    x = synth.activations(w["seed"], w["N"], w["H"], w["W"], w.get("C", (w.get("widths") or [0])[0]),
+                          w["dtype"])
+    return w, x
+
+
+@pytest.mark.parametrize("name", [n for n, w in WORKLOADS.items() if w["kind"] == "block"])
+def test_workload_block(name):
+    w, x = _workload_inputs(name)
+    say("workload", name)
+    p = synth.block_params(w["seed"], 0, w["C"], w["E"], w["k"], w["dtype"])
+    xd, pd = x.cuda(), to_dev(p)
+    y = cf.block_forward(xd, pd)
+    torch.cuda.synchronize()
+    imgs = list(range(w["N"])) if w["N"] <= 4 else [0, 1, w["N"] // 2 - 1, w["N"] - 1]
+    ref = oracle_block(x, p, images=imgs)
+    r = assert_close(y.cpu()[imgs], ref, what=name)
+    say("  fused rel err %.2e" % r)
+    yu = cf.block_forward_unfused(xd, pd)
+    assert_close(yu.cpu()[imgs], ref, what=name + " unfused")
+    if w["N"] * w["H"] * w["W"] <= 64 * 4:
+        ys = cf.block_forward_split(xd, pd)
+        assert_close(ys.cpu()[imgs], ref, what=name + " split")
+
+
+def test_workload_stack():
+    name = "stack_n128_56x56_d2262_c64to512_e4_k3_f16"
+    w = WORKLOADS[name]
+    say("workload", name)
+    x = synth.activations(w["seed"], w["N"], w["H"], w["W"], w["widths"][0], w["dtype"])
+    layers = synth.stack_layers(w["seed"], w["depths"], w["widths"], w["E"], w["k"], w["dtype"])
+    y = cf.stack_forward(x.cuda(), [(kd, to_dev(p)) for kd, p in layers])
+    torch.cuda.synchronize()
+    assert y.shape == (w["N"], 7, 7, 512)
+    imgs = [0, w["N"] - 1]
+    ref = oracle.stack_forward(synth.to_f64(x[imgs]), [(kd, synth.params_f64(p)) for kd, p in layers])
+    r = assert_close(y.cpu()[imgs], ref, what=name)
+    say("  stack rel err %.2e" % r)
