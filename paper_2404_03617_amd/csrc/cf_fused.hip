@@ -85,7 +85,7 @@ size_t fused_lds_bytes(const Shape &s) {
     if (s.C != 64 && s.C != 128 && s.C != 256 && s.C != 512)
         return 0;
     const int64_t P = (int64_t)s.N * s.H * s.W;
-    return lds_bytes_for(s.C, s.k, s.W, s.E, P, 1, false, 1);
+    return lds_bytes_for(s.C, s.k, s.W, s.E, P, 1, false, 1, s.bf16 != 0);
 }
 
 hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Shape &s, int groups,

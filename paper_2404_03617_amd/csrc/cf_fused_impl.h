@@ -92,6 +92,37 @@ __device__ __forceinline__ u32x4 lds_ld16(const uint8_t *base, uint32_t off) {
     return *reinterpret_cast<const u32x4 *>(base + off);
 }
 
+// s_waitcnt vmcnt(n) leaving LDS/export counters alone (gfx9 encoding:
+// vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+// Wait until at most n vector-memory operations of this wave are
+// outstanding (n is clamped to 16; a smaller bound only waits longer).
+__device__ __forceinline__ void wait_vmcnt_le(int n) {
+    switch (n < 0 ? 0 : n > 16 ? 16 : n) {
+    case 0: wait_vmcnt<0>(); break;
+    case 1: wait_vmcnt<1>(); break;
+    case 2: wait_vmcnt<2>(); break;
+    case 3: wait_vmcnt<3>(); break;
+    case 4: wait_vmcnt<4>(); break;
+    case 5: wait_vmcnt<5>(); break;
+    case 6: wait_vmcnt<6>(); break;
+    case 7: wait_vmcnt<7>(); break;
+    case 8: wait_vmcnt<8>(); break;
+    case 9: wait_vmcnt<9>(); break;
+    case 10: wait_vmcnt<10>(); break;
+    case 11: wait_vmcnt<11>(); break;
+    case 12: wait_vmcnt<12>(); break;
+    case 13: wait_vmcnt<13>(); break;
+    case 14: wait_vmcnt<14>(); break;
+    case 15: wait_vmcnt<15>(); break;
+    default: wait_vmcnt<16>(); break;
+    }
+}
+
 // One wave-wide 16-byte global->LDS copy: lane l's 16 bytes land at
 // lds_wave_base + 16 * l.
 __device__ __forceinline__ void dma16(const void *src, uint8_t *lds_wave_base) {
@@ -155,6 +186,53 @@ __device__ __forceinline__ uint32_t act_q(float a, float b) {
     }
 }
 
+// Activation of NP packed pairs at once, written stage by stage across the
+// pairs so the NP independent dependency chains interleave in the VALU.
+template <typename T, int ACT, int NP>
+__device__ __forceinline__ void act_pairs(const float (&a)[2 * NP], uint32_t (&out)[NP]) {
+    if constexpr (ACT == ACT_GELU && !T::is_bf16) {
+        const half2v c0 = {(_Float16)1.54974312f, (_Float16)1.54974312f};
+        const half2v c1 = {(_Float16)-3.45119285f, (_Float16)-3.45119285f};
+        const half2v c2 = {(_Float16)5.28594729f, (_Float16)5.28594729f};
+        const half2v c3 = {(_Float16)-4.21833024f, (_Float16)-4.21833024f};
+        const half2v c4 = {(_Float16)1.36138518f, (_Float16)1.36138518f};
+        const half2v half_ = {(_Float16)0.5f, (_Float16)0.5f};
+        const half2v zero = {(_Float16)0.0f, (_Float16)0.0f};
+        const half2v one = {(_Float16)1.0f, (_Float16)1.0f};
+        half2v w[NP], sq[NP], q[NP];
+#pragma unroll
+        for (int p = 0; p < NP; p++) {
+            w[p].x = (_Float16)a[2 * p];
+            w[p].y = (_Float16)a[2 * p + 1];
+        }
+#pragma unroll
+        for (int p = 0; p < NP; p++)
+            sq[p] = w[p] * w[p];
+#pragma unroll
+        for (int p = 0; p < NP; p++)
+            q[p] = __builtin_elementwise_fma(sq[p], c4, c3);
+#pragma unroll
+        for (int p = 0; p < NP; p++)
+            q[p] = __builtin_elementwise_fma(sq[p], q[p], c2);
+#pragma unroll
+        for (int p = 0; p < NP; p++)
+            q[p] = __builtin_elementwise_fma(sq[p], q[p], c1);
+#pragma unroll
+        for (int p = 0; p < NP; p++)
+            q[p] = __builtin_elementwise_fma(sq[p], q[p], c0);
+#pragma unroll
+        for (int p = 0; p < NP; p++)
+            q[p] = __builtin_elementwise_min(__builtin_elementwise_max(__builtin_elementwise_fma(w[p], q[p], half_), zero), one);
+#pragma unroll
+        for (int p = 0; p < NP; p++)
+            out[p] = __builtin_bit_cast(uint32_t, w[p] * q[p]);
+    } else {
+#pragma unroll
+        for (int p = 0; p < NP; p++)
+            out[p] = act_q<T, ACT>(a[2 * p], a[2 * p + 1]);
+    }
+}
+
 template <int C, int KS, int NWAVE, int NB, typename T, int ACT, bool RESIDENT>
 struct Fused {
     static constexpr int NT = NWAVE * 64;
@@ -170,6 +248,10 @@ struct Fused {
     static constexpr int PIECES = (8 * C + NT - 1) / NT;  // 16-byte weight pieces per thread per chunk
     static constexpr int PSTRIDE = CS * 2;      // bytes per pixel in a halo slab
     static constexpr float QS = 0.25f;          // activation-variable scale
+    // staged per-channel constants: s0/4, b0/4 (fp16 or fp32), b2/4 (fp32)
+    static constexpr int CST_B0 = T::is_bf16 ? 4 * C : 2 * C;
+    static constexpr int CST_B2 = 2 * CST_B0;
+    static constexpr int CST_BYTES = CST_B2 + 4 * C;
 
     // ------------------------------------------------------------------ weights
     // Chunk layout in LDS: [KST][64 lanes][16 B] W1 fragments, then
@@ -244,23 +326,12 @@ struct Fused {
         }
     }
 
-    // One chunk of 32 hidden channels for this wave's NB pixel blocks.
-    static __device__ __forceinline__ void chunk_compute(const uint8_t *buf, int lane, const u32x4 (&dfr)[KST][NB],
-                                                         float16v (&acc)[CB][NB]) {
+    // Expand of one chunk of 32 hidden channels for this wave's NB pixel
+    // blocks: hacc = W1_chunk D^T + b1 (b1 enters through the C operand).
+    static __device__ __forceinline__ void expand(const uint8_t *buf, int lane, const u32x4 (&dfr)[KST][NB],
+                                                  float16v (&hacc)[NB]) {
         const int h = lane >> 5;
-        float16v bias;
-        {
-            const float4v *bp = reinterpret_cast<const float4v *>(buf + 128 * C + h * 64);
-#pragma unroll
-            for (int q = 0; q < 4; q++) {
-                const float4v v = bp[q];
-                bias[4 * q + 0] = v[0];
-                bias[4 * q + 1] = v[1];
-                bias[4 * q + 2] = v[2];
-                bias[4 * q + 3] = v[3];
-            }
-        }
-        float16v hacc[NB];
+        const float16v bias = *reinterpret_cast<const float16v *>(buf + 128 * C + h * 64);
 #pragma unroll
         for (int ks = 0; ks < KST; ks++) {
             const u32x4 af = lds_ld16(buf, (uint32_t)((ks * 64 + lane) * 16));
@@ -268,6 +339,12 @@ struct Fused {
             for (int b = 0; b < NB; b++)
                 hacc[b] = mfma32(af, dfr[ks][b], ks == 0 ? bias : hacc[b], T{});
         }
+    }
+
+    // Activation of an expanded chunk and its projection onto the output
+    // accumulators: acc += W2_chunk phi(hacc).
+    static __device__ __forceinline__ void project(const uint8_t *buf, int lane, const float16v (&hacc)[NB],
+                                                   float16v (&acc)[CB][NB]) {
         u32x4 hid[NB][2];
 #pragma unroll
         for (int b = 0; b < NB; b++)
@@ -285,6 +362,100 @@ struct Fused {
                 for (int b = 0; b < NB; b++)
                     acc[cb][b] = mfma32(wf, hid[b][kk], acc[cb][b], T{});
             }
+    }
+
+    // ---- software-pipelined FFN over NCH resident chunks.
+    // Iteration c: activation of chunk c (VALU), expand of chunk c+1 and
+    // project of chunk c-1 (MFMA) -- mutually independent, so the scheduler
+    // interleaves one MFMA with a run of VALU instructions -- while the LDS
+    // fragments of the next iteration are fetched.
+    static __device__ __forceinline__ void load_w1(const uint8_t *buf, int lane, u32x4 (&w1)[KST], float16v &bias) {
+        bias = *reinterpret_cast<const float16v *>(buf + 128 * C + (lane >> 5) * 64);
+#pragma unroll
+        for (int ks = 0; ks < KST; ks++)
+            w1[ks] = lds_ld16(buf, (uint32_t)((ks * 64 + lane) * 16));
+    }
+    static __device__ __forceinline__ void load_w2(const uint8_t *buf, int lane, u32x4 (&w2)[CB][2]) {
+#pragma unroll
+        for (int cb = 0; cb < CB; cb++)
+#pragma unroll
+            for (int kk = 0; kk < 2; kk++)
+                w2[cb][kk] = lds_ld16(buf, (uint32_t)(W1_BYTES + ((cb * 2 + kk) * 64 + lane) * 16));
+    }
+    static __device__ __forceinline__ void mma_expand(const u32x4 (&w1)[KST], const float16v &bias,
+                                                      const u32x4 (&dfr)[KST][NB], float16v (&hh)[NB]) {
+#pragma unroll
+        for (int ks = 0; ks < KST; ks++)
+#pragma unroll
+            for (int b = 0; b < NB; b++)
+                hh[b] = mfma32(w1[ks], dfr[ks][b], ks == 0 ? bias : hh[b], T{});
+    }
+    static __device__ __forceinline__ void mma_project(const u32x4 (&w2)[CB][2], const u32x4 (&hid)[NB][2],
+                                                       float16v (&acc)[CB][NB]) {
+#pragma unroll
+        for (int kk = 0; kk < 2; kk++)
+#pragma unroll
+            for (int cb = 0; cb < CB; cb++)
+#pragma unroll
+                for (int b = 0; b < NB; b++)
+                    acc[cb][b] = mfma32(w2[cb][kk], hid[b][kk], acc[cb][b], T{});
+    }
+    static __device__ __forceinline__ void activate(const float16v (&hh)[NB], u32x4 (&hid)[NB][2]) {
+        float v[NB * 16];
+#pragma unroll
+        for (int b = 0; b < NB; b++)
+#pragma unroll
+            for (int e = 0; e < 16; e++)
+                v[b * 16 + e] = hh[b][e];
+        uint32_t o[NB * 8];
+        act_pairs<T, ACT, NB * 8>(v, o);
+#pragma unroll
+        for (int b = 0; b < NB; b++)
+#pragma unroll
+            for (int kk = 0; kk < 2; kk++)
+#pragma unroll
+                for (int p = 0; p < 4; p++)
+                    hid[b][kk][p] = o[b * 8 + kk * 4 + p];
+    }
+
+    template <int NCH>
+    static __device__ __forceinline__ void ffn_pipelined(const uint8_t *wbuf, int lane, const u32x4 (&dfr)[KST][NB],
+                                                         float16v (&acc)[CB][NB]) {
+        float16v hh[2][NB];
+        u32x4 hid[2][NB][2];
+        u32x4 w1[2][KST];
+        float16v bias[2];
+        u32x4 w2[2][CB][2];
+        load_w1(wbuf, lane, w1[0], bias[0]);
+        mma_expand(w1[0], bias[0], dfr, hh[0]);
+        if constexpr (NCH > 1)
+            load_w1(wbuf + CHUNK_BYTES, lane, w1[1], bias[1]);
+#pragma unroll
+        for (int c = 0; c < NCH; c++) {
+            const int cur = c & 1, nxt = cur ^ 1;
+            if (c + 2 < NCH)
+                load_w1(wbuf + (size_t)(c + 2) * CHUNK_BYTES, lane, w1[cur], bias[cur]);
+            load_w2(wbuf + (size_t)c * CHUNK_BYTES, lane, w2[cur]);
+            activate(hh[cur], hid[cur]);
+            if (c + 1 < NCH)
+                mma_expand(w1[nxt], bias[nxt], dfr, hh[nxt]);
+            if (c >= 1)
+                mma_project(w2[nxt], hid[nxt], acc);
+            // interleave: one MFMA, then a run of VALU instructions
+#pragma unroll
+            for (int g = 0; g < KST * NB + 2 * CB * NB; g++) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
+            }
+        }
+        mma_project(w2[(NCH - 1) & 1], hid[(NCH - 1) & 1], acc);
+    }
+
+    static __device__ __forceinline__ void chunk_compute(const uint8_t *buf, int lane, const u32x4 (&dfr)[KST][NB],
+                                                         float16v (&acc)[CB][NB]) {
+        float16v hacc[NB];
+        expand(buf, lane, dfr, hacc);
+        project(buf, lane, hacc, acc);
     }
 
     // ------------------------------------------------------------------ halo
@@ -360,12 +531,26 @@ struct Fused {
         const uint32_t dw_bytes = ((uint32_t)KS * KS * PSTRIDE + 255u) & ~255u;
         const uint32_t hbuf_bytes = ((halo_bytes + 255u) & ~255u) + dw_bytes;
         uint8_t *wbuf = smem + NHBUF * hbuf_bytes;
+        // per-channel constants staged once: s0/4 and b0/4 (packed fp16 for
+        // fp16 I/O, fp32 for bf16), then (b2/4) in fp32
+        uint8_t *cst = wbuf + (size_t)(RESIDENT ? a.chunks_per_group : 2) * CHUNK_BYTES;
         const uint32_t zrow = (uint32_t)a.halo_rows * WP * PSTRIDE;  // byte offset of the zero row
 
         // Halo buffers start at zero: pad columns and the zero row are never
         // written again.
         for (uint32_t i = tid; i < NHBUF * hbuf_bytes / 16; i += NT)
             reinterpret_cast<u32x4 *>(smem)[i] = u32x4{0u, 0u, 0u, 0u};
+        for (int c = tid; c < C; c += NT) {
+            const float sq = (a.s0 ? a.s0[c] : 1.0f) * QS, bq = (a.b0 ? a.b0[c] : 0.0f) * QS;
+            if constexpr (!T::is_bf16) {
+                reinterpret_cast<_Float16 *>(cst)[c] = (_Float16)sq;
+                reinterpret_cast<_Float16 *>(cst + CST_B0)[c] = (_Float16)bq;
+            } else {
+                reinterpret_cast<float *>(cst)[c] = sq;
+                reinterpret_cast<float *>(cst + CST_B0)[c] = bq;
+            }
+            reinterpret_cast<float *>(cst + CST_B2)[c] = (split || !a.b2) ? 0.0f : a.b2[c] * QS;
+        }
         __syncthreads();
 
         if constexpr (RESIDENT) {
@@ -390,6 +575,11 @@ struct Fused {
             issue_slab(a, smem, smem + hbuf_bytes - dw_bytes, g_lo, rows, 0, wv, lane);
         }
         int item = 0;
+        // vector-memory operations this wave issued after the copy of the
+        // next halo item (the previous tile's output stores): memory
+        // operations retire in order, so waiting for "at most this many
+        // outstanding" waits for the copy but not for the stores
+        int stores_after_copy = 0;
         for (; tile < a.ntiles; tile += gridDim.x) {
             uint32_t p0, pend, g_lo;
             int rows;
@@ -421,6 +611,19 @@ struct Fused {
                 }
                 rmask[b] = msk;
             }
+            // byte offset of tap column j, K step ksl, within a halo row:
+            // column * 128 + ((2*ksl + h) ^ (column & 7)) * 16
+            uint32_t colx[NB][KSL][KS];
+#pragma unroll
+            for (int b = 0; b < NB; b++)
+#pragma unroll
+                for (int j = 0; j < KS; j++) {
+                    const uint32_t col = (uint32_t)(lcol[b] - PAD + j);
+                    const uint32_t base = (col << 7) | (((uint32_t)h ^ (col & 7u)) << 4);
+#pragma unroll
+                    for (int ksl = 0; ksl < KSL; ksl++)
+                        colx[b][ksl][j] = base ^ ((uint32_t)ksl << 5);
+                }
 
             u32x4 dfr[KST][NB];
             float16v acc[CB][NB];
@@ -431,8 +634,12 @@ struct Fused {
                 // in the LDS address space (ds_read, not flat loads)
                 uint8_t *halo = smem + ((NHBUF == 2 && (item & 1)) ? hbuf_bytes : 0u);
                 const uint8_t *dww = halo + hbuf_bytes - dw_bytes;
-                __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of the item have landed
-                __syncthreads();                 // ... and every other wave's
+                // this wave's copies of the item have landed ...
+                if constexpr (RESIDENT && NSLAB == 1)
+                    wait_vmcnt_le(stores_after_copy);
+                else
+                    __builtin_amdgcn_s_waitcnt(0);
+                __syncthreads();  // ... and every other wave's
                 if (NHBUF == 2) {
                     uint8_t *nb = smem + (((item + 1) & 1) ? hbuf_bytes : 0u);
                     if (slab + 1 < NSLAB)
@@ -446,62 +653,60 @@ struct Fused {
                 }
 
                 // ---- depth-wise conv on the VALU for the K steps of this slab
+                if constexpr (!T::is_bf16) {
+                    half2v accd[KSL][NB][4];
 #pragma unroll
-                for (int ksl = 0; ksl < KSL; ksl++) {
-                    const int ks = slab * KSL + ksl;
-                    const int c0 = ks * 16 + 8 * h;               // global channel of this lane's 8
-                    const uint32_t qc = (uint32_t)(2 * ksl + h);  // logical 16-byte chunk in the slab
-                    float sv[8], bv[8];
-#pragma unroll
-                    for (int e = 0; e < 8; e++) {
-                        sv[e] = (a.s0 ? a.s0[c0 + e] : 1.0f) * QS;
-                        bv[e] = (a.b0 ? a.b0[c0 + e] : 0.0f) * QS;
-                    }
-                    if constexpr (!T::is_bf16) {
-                        half2v accd[NB][4];
+                    for (int ksl = 0; ksl < KSL; ksl++)
 #pragma unroll
                         for (int b = 0; b < NB; b++)
 #pragma unroll
                             for (int q = 0; q < 4; q++)
-                                accd[b][q] = half2v{(_Float16)0.0f, (_Float16)0.0f};
+                                accd[ksl][b][q] = half2v{(_Float16)0.0f, (_Float16)0.0f};
 #pragma unroll 1
-                        for (int i = 0; i < KS; i++) {
+                    for (int i = 0; i < KS; i++) {
+                        uint32_t rowoff[NB];
+#pragma unroll
+                        for (int b = 0; b < NB; b++)
+                            rowoff[b] = ((rmask[b] >> i) & 1u) ? ctr[b] + (uint32_t)((i - PAD) * WP * PSTRIDE) : zrow;
+#pragma unroll
+                        for (int ksl = 0; ksl < KSL; ksl++) {
                             Pack8 wr[KS];
 #pragma unroll
                             for (int j = 0; j < KS; j++)
-                                wr[j].u = lds_ld16(dww, (uint32_t)((i * KS + j) * PSTRIDE) + qc * 16);
+                                wr[j].u = lds_ld16(dww, (uint32_t)((i * KS + j) * PSTRIDE + ((2 * ksl + h) << 4)));
 #pragma unroll
-                            for (int b = 0; b < NB; b++) {
-                                const bool ok = (rmask[b] >> i) & 1u;
-                                const uint32_t rowbase = ok ? ctr[b] + (uint32_t)((i - PAD) * WP * PSTRIDE) : zrow;
+                            for (int b = 0; b < NB; b++)
 #pragma unroll
                                 for (int j = 0; j < KS; j++) {
-                                    const uint32_t col = (uint32_t)(lcol[b] - PAD + j);
                                     Pack8 v;
-                                    v.u = lds_ld16(halo, rowbase + col * PSTRIDE + swz(col, qc) * 16);
+                                    v.u = lds_ld16(halo, rowoff[b] + colx[b][ksl][j]);
 #pragma unroll
-                                    for (int q = 0; q < 4; q++) {
-                                        const half2v xv = __builtin_bit_cast(half2v, v.w[q]);
-                                        const half2v wv2 = __builtin_bit_cast(half2v, wr[j].w[q]);
-                                        accd[b][q] = __builtin_elementwise_fma(xv, wv2, accd[b][q]);
-                                    }
+                                    for (int q = 0; q < 4; q++)
+                                        accd[ksl][b][q] = __builtin_elementwise_fma(
+                                            __builtin_bit_cast(half2v, v.w[q]), __builtin_bit_cast(half2v, wr[j].w[q]),
+                                            accd[ksl][b][q]);
                                 }
-                            }
-                            __builtin_amdgcn_sched_barrier(0);
                         }
-                        half2v sh[4], bh[4];
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
 #pragma unroll
-                        for (int q = 0; q < 4; q++) {
-                            sh[q] = half2v{(_Float16)sv[2 * q], (_Float16)sv[2 * q + 1]};
-                            bh[q] = half2v{(_Float16)bv[2 * q], (_Float16)bv[2 * q + 1]};
-                        }
+                    for (int ksl = 0; ksl < KSL; ksl++) {
+                        const int c0 = (slab * KSL + ksl) * 16 + 8 * h;
+                        Pack8 sp, bp;
+                        sp.u = *reinterpret_cast<const u32x4 *>(cst + 2 * c0);
+                        bp.u = *reinterpret_cast<const u32x4 *>(cst + CST_B0 + 2 * c0);
 #pragma unroll
                         for (int b = 0; b < NB; b++)
 #pragma unroll
                             for (int q = 0; q < 4; q++)
-                                dfr[ks][b][q] = __builtin_bit_cast(
-                                    uint32_t, __builtin_elementwise_fma(accd[b][q], sh[q], bh[q]));
-                    } else {
+                                dfr[slab * KSL + ksl][b][q] = __builtin_bit_cast(
+                                    uint32_t, __builtin_elementwise_fma(accd[ksl][b][q], __builtin_bit_cast(half2v, sp.w[q]),
+                                                                        __builtin_bit_cast(half2v, bp.w[q])));
+                    }
+                } else {
+#pragma unroll
+                    for (int ksl = 0; ksl < KSL; ksl++) {
+                        const int c0 = (slab * KSL + ksl) * 16 + 8 * h;
                         float accd[NB][8];
 #pragma unroll
                         for (int b = 0; b < NB; b++)
@@ -510,17 +715,18 @@ struct Fused {
                                 accd[b][e] = 0.0f;
 #pragma unroll 1
                         for (int i = 0; i < KS; i++) {
+                            uint32_t rowoff[NB];
+#pragma unroll
+                            for (int b = 0; b < NB; b++)
+                                rowoff[b] = ((rmask[b] >> i) & 1u) ? ctr[b] + (uint32_t)((i - PAD) * WP * PSTRIDE) : zrow;
 #pragma unroll
                             for (int j = 0; j < KS; j++) {
                                 Pack8 wr;
-                                wr.u = lds_ld16(dww, (uint32_t)((i * KS + j) * PSTRIDE) + qc * 16);
+                                wr.u = lds_ld16(dww, (uint32_t)((i * KS + j) * PSTRIDE + ((2 * ksl + h) << 4)));
 #pragma unroll
                                 for (int b = 0; b < NB; b++) {
-                                    const bool ok = (rmask[b] >> i) & 1u;
-                                    const uint32_t rowbase = ok ? ctr[b] + (uint32_t)((i - PAD) * WP * PSTRIDE) : zrow;
-                                    const uint32_t col = (uint32_t)(lcol[b] - PAD + j);
                                     Pack8 v;
-                                    v.u = lds_ld16(halo, rowbase + col * PSTRIDE + swz(col, qc) * 16);
+                                    v.u = lds_ld16(halo, rowoff[b] + colx[b][ksl][j]);
 #pragma unroll
                                     for (int q = 0; q < 4; q++) {
                                         accd[b][2 * q] = fmaf(T::lo(v.w[q]), T::lo(wr.w[q]), accd[b][2 * q]);
@@ -529,42 +735,42 @@ struct Fused {
                                 }
                             }
                         }
+                        const float *sq = reinterpret_cast<const float *>(cst) + c0;
+                        const float *bq = reinterpret_cast<const float *>(cst + CST_B0) + c0;
 #pragma unroll
                         for (int b = 0; b < NB; b++)
 #pragma unroll
                             for (int q = 0; q < 4; q++)
-                                dfr[ks][b][q] = T::pack2(fmaf(accd[b][2 * q], sv[2 * q], bv[2 * q]),
-                                                         fmaf(accd[b][2 * q + 1], sv[2 * q + 1], bv[2 * q + 1]));
+                                dfr[slab * KSL + ksl][b][q] =
+                                    T::pack2(fmaf(accd[b][2 * q], sq[2 * q], bq[2 * q]),
+                                             fmaf(accd[b][2 * q + 1], sq[2 * q + 1], bq[2 * q + 1]));
                     }
                 }
 
-                // ---- residual shortcut from the halo centre: acc = (x + b2) / 4
+                // ---- residual shortcut from the halo centre: acc = x / 4 + b2 / 4
                 if constexpr (NSLAB == 1) {
 #pragma unroll
                     for (int cb = 0; cb < CB; cb++) {
                         const int cc = cb * 32 + 16 * h;
-                        float16v bias;
-#pragma unroll
-                        for (int e = 0; e < 16; e++)
-                            bias[e] = (split || !a.b2) ? 0.0f : a.b2[cc + e];
+                        const float16v bias = *reinterpret_cast<const float16v *>(cst + CST_B2 + 4 * cc);
 #pragma unroll
                         for (int b = 0; b < NB; b++) {
                             if (split) {
                                 acc[cb][b] = bias;
                                 continue;
                             }
-                            const uint32_t col = (uint32_t)lcol[b];
                             const uint32_t q0 = (uint32_t)(4 * cb + 2 * h);
+                            const uint32_t col = (uint32_t)lcol[b];
                             Pack8 v0, v1;
-                            v0.u = lds_ld16(halo, ctr[b] + col * PSTRIDE + swz(col, q0) * 16);
-                            v1.u = lds_ld16(halo, ctr[b] + col * PSTRIDE + swz(col, q0 + 1) * 16);
+                            v0.u = lds_ld16(halo, ctr[b] + (col << 7) + (swz(col, q0) << 4));
+                            v1.u = lds_ld16(halo, ctr[b] + (col << 7) + (swz(col, q0 + 1) << 4));
                             float16v t;
 #pragma unroll
                             for (int q = 0; q < 4; q++) {
-                                t[2 * q] = (T::lo(v0.w[q]) + bias[2 * q]) * QS;
-                                t[2 * q + 1] = (T::hi(v0.w[q]) + bias[2 * q + 1]) * QS;
-                                t[8 + 2 * q] = (T::lo(v1.w[q]) + bias[8 + 2 * q]) * QS;
-                                t[8 + 2 * q + 1] = (T::hi(v1.w[q]) + bias[8 + 2 * q + 1]) * QS;
+                                t[2 * q] = fmaf(T::lo(v0.w[q]), QS, bias[2 * q]);
+                                t[2 * q + 1] = fmaf(T::hi(v0.w[q]), QS, bias[2 * q + 1]);
+                                t[8 + 2 * q] = fmaf(T::lo(v1.w[q]), QS, bias[8 + 2 * q]);
+                                t[8 + 2 * q + 1] = fmaf(T::hi(v1.w[q]), QS, bias[8 + 2 * q + 1]);
                             }
                             acc[cb][b] = t;
                         }
@@ -608,14 +814,10 @@ struct Fused {
                                 t[8 + 2 * q] = T::lo(v1.w[q]);
                                 t[8 + 2 * q + 1] = T::hi(v1.w[q]);
                             }
-                            if (a.b2) {
-#pragma unroll
-                                for (int e = 0; e < 16; e++)
-                                    t[e] += a.b2[cc + e];
-                            }
+                            const float16v bias = *reinterpret_cast<const float16v *>(cst + CST_B2 + 4 * cc);
 #pragma unroll
                             for (int e = 0; e < 16; e++)
-                                t[e] *= QS;
+                                t[e] = fmaf(t[e], QS, bias[e]);
                         }
                         acc[cb][b] = t;
                     }
@@ -624,8 +826,26 @@ struct Fused {
 
             // ---- FFN: loop over hidden chunks (eq. e:ffn-eff)
             if constexpr (RESIDENT) {
-                for (int ch = ch_begin; ch < ch_end; ch++)
-                    chunk_compute(wbuf + (size_t)(ch - ch_begin) * CHUNK_BYTES, lane, dfr, acc);
+              if (ch_end - ch_begin == 8) {
+                ffn_pipelined<8>(wbuf, lane, dfr, acc);
+              } else {
+                // Software pipeline: the expand MFMAs of chunk c+1 are issued
+                // before the activation of chunk c, so the matrix cores work
+                // while the VALU evaluates phi.
+                float16v hA[NB], hB[NB];
+                int ch = ch_begin;
+                expand(wbuf, lane, dfr, hA);
+                for (; ch + 2 <= ch_end; ch += 2) {
+                    const uint8_t *b0p = wbuf + (size_t)(ch - ch_begin) * CHUNK_BYTES;
+                    expand(b0p + CHUNK_BYTES, lane, dfr, hB);
+                    project(b0p, lane, hA, acc);
+                    if (ch + 2 < ch_end)
+                        expand(b0p + 2 * CHUNK_BYTES, lane, dfr, hA);
+                    project(b0p + CHUNK_BYTES, lane, hB, acc);
+                }
+                if (ch < ch_end)
+                    project(wbuf + (size_t)(ch - ch_begin) * CHUNK_BYTES, lane, hA, acc);
+              }
             } else {
                 if (a.dma_weights) {
                     chunk_dma(a, ch_begin, wv, lane, wbuf);
@@ -666,8 +886,12 @@ struct Fused {
             }
 
             // ---- epilogue: y = 4 * acc, one store of the output tile
+            stores_after_copy = 0;
 #pragma unroll
             for (int b = 0; b < NB; b++) {
+                // wave-uniform count; an under-count only makes the wait stricter
+                if (__builtin_amdgcn_read_exec() && __ballot(valid[b]))
+                    stores_after_copy += CB * (split ? 4 : 2);
                 if (!valid[b])
                     continue;
 #pragma unroll
@@ -727,7 +951,8 @@ inline int halo_rows_for(int M, int k, int W, int64_t P) {
     return (int)span + 2 * (k / 2);
 }
 
-inline size_t lds_bytes_for(int C, int k, int W, int E, int64_t P, int groups, bool resident, int nhbuf) {
+inline size_t lds_bytes_for(int C, int k, int W, int E, int64_t P, int groups, bool resident, int nhbuf,
+                            bool bf16) {
     const int pad = k / 2;
     const int halo_rows = halo_rows_for(tile_pixels(C), k, W, P);
     const size_t halo = (size_t)(halo_rows + 1) * (W + 2 * pad) * 128;
@@ -735,7 +960,7 @@ inline size_t lds_bytes_for(int C, int k, int W, int E, int64_t P, int groups, b
     const size_t hbuf = ((halo + 255) & ~(size_t)255) + dw;
     const int chunks = E * C / 32 / groups;
     const size_t wb = (size_t)(resident ? chunks : 2) * (128 * C + 128);
-    return nhbuf * hbuf + wb;
+    return nhbuf * hbuf + wb + (bf16 ? 12 : 8) * (size_t)C;
 }
 
 template <int C, int KS, typename T, int ACT>
@@ -745,12 +970,12 @@ hipError_t launch_t(const FusedArgs &a0, int groups, hipStream_t st) {
     FusedArgs a = a0;
     const int M = NWAVE * NB * 32;
     const int chunks = a.E * C / 32;
-    const size_t lds_res = lds_bytes_for(C, KS, a.W, a.E, a.P, groups, true, 1);
+    const size_t lds_res = lds_bytes_for(C, KS, a.W, a.E, a.P, groups, true, 1, T::is_bf16);
     const bool resident = cfgc.resident && lds_res <= 160 * 1024;
-    size_t lds = resident ? lds_res : lds_bytes_for(C, KS, a.W, a.E, a.P, groups, false, 1);
+    size_t lds = resident ? lds_res : lds_bytes_for(C, KS, a.W, a.E, a.P, groups, false, 1, T::is_bf16);
     a.nhbuf = 1;
     if (C > 64) {
-        const size_t lds2 = lds_bytes_for(C, KS, a.W, a.E, a.P, groups, resident, 2);
+        const size_t lds2 = lds_bytes_for(C, KS, a.W, a.E, a.P, groups, resident, 2, T::is_bf16);
         if (lds2 <= 160 * 1024) {
             lds = lds2;
             a.nhbuf = 2;
