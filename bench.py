@@ -31,6 +31,52 @@ from paper_2404_03617_amd import synth
 from paper_2404_03617_amd.workloads import BENCH_WORKLOAD, WORKLOADS
 
 MALL_BYTES = 256 << 20
+HERE = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(HERE, "paper_2404_03617_amd", "csrc")
+PROFILES = os.path.join(HERE, "profiles")
+# sources of the C = 64 fp16 fused kernel; the counter-based traffic figure is
+# reported only while they hash to the value recorded with the counters
+FUSED_SOURCES = ("cf_fused_impl.h", "cf_device.h", "cf_fused_c64_f16.hip")
+
+
+def fused_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in FUSED_SOURCES:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(name: str):
+    """HBM bytes per launch of the fused kernel from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary, or None when it is absent or was taken
+    on different kernel sources."""
+    path = os.path.join(PROFILES, "fused_block_%s.md" % name)
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and line.startswith("- "):
+                k, v = line[2:].split(":", 1)
+                fields[k.strip()] = v.strip().strip("`")
+    if fields.get("kernel source hash") != fused_source_hash():
+        return None
+    try:
+        return int(fields["traffic bytes per launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def calib_copy():
+    """A plain elementwise kernel over a known size (256 MiB read, 256 MiB
+    written) whose FETCH_SIZE / WRITE_SIZE calibrate the counters."""
+    a = torch.ones(128 << 20, dtype=torch.float16, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        torch.neg(a, out=b)
+    torch.cuda.synchronize()
 
 
 def _sets_needed(bytes_per_set: int) -> int:
@@ -52,7 +98,22 @@ def _time(fn, steps: int, warmup: int, stream) -> float:
     return start.elapsed_time(end) / 1e3 / steps
 
 
-def block_case(name: str, steps: int, warmup: int, act: str = "gelu", unfused: bool = False):
+def _time_each(fn, steps: int, stream) -> float:
+    """Average seconds of one launch, each bracketed by its own HIP events on
+    `stream` (the per-kernel duration the roofline divides by)."""
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for i in range(steps):
+        starts[i].record(stream)
+        fn(i)
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    return sum(a.elapsed_time(b) for a, b in zip(starts, ends)) / 1e3 / steps
+
+
+def block_case(name: str, steps: int, warmup: int, act: str = "gelu", unfused: bool = False,
+               per_launch: bool = False):
     w = WORKLOADS[name]
     N, H, W, C, E, k = w["N"], w["H"], w["W"], w["C"], w["E"], w["k"]
     eb = 2
@@ -69,8 +130,10 @@ def block_case(name: str, steps: int, warmup: int, act: str = "gelu", unfused: b
     else:
         fn = lambda i: cf.block_forward(xs[i % nsets], p, act=act, out=ys[i % nsets])
     t = _time(fn, steps, warmup, stream)
+    t_kernel = _time_each(fn, steps, stream) if per_launch else t
     flops = rl.block_flops(N, H, W, C, E, k)
-    return dict(N=N, seconds=t, flops=flops, bytes=rl.block_bytes_fused(N, H, W, C, E, k, eb))
+    return dict(N=N, seconds=t, kernel_seconds=t_kernel, flops=flops,
+                bytes=rl.block_bytes_fused(N, H, W, C, E, k, eb))
 
 
 def split_case(name: str, steps: int, warmup: int):
@@ -109,18 +172,26 @@ def stack_case(name: str, steps: int, warmup: int):
     return dict(N=N, seconds=t, flops=flops, waterline_T_min_s=T, waterline_C_max=cmax)
 
 
-def cpu_baseline(name: str, images: int = 4):
-    """The fp64 oracle on `images` images of the workload, all host cores."""
+def cpu_baseline(name: str, min_seconds: float = 12.0):
+    """The fp64 oracle on the workload's full batch, all host cores, repeated
+    until at least `min_seconds` of CPU work have been timed."""
     import oracle
     w = WORKLOADS[name]
-    x = synth.activations(w["seed"], images, w["H"], w["W"], w["C"], w["dtype"])
+    x = synth.activations(w["seed"], w["N"], w["H"], w["W"], w["C"], w["dtype"])
     p = synth.params_f64(synth.block_params(w["seed"], 0, w["C"], w["E"], w["k"], w["dtype"]))
     xd = synth.to_f64(x)
+    passes, used = 0, 0
     t0 = time.perf_counter()
-    _, used = oracle.block_forward(xd, p, act="gelu", return_threads=True)
-    dt = time.perf_counter() - t0
-    return {"value": images / dt, "unit": "images/s", "cores": int(used), "kind": "oracle",
-            "sample": "%d of %d images of %s, fp64 C loops, %.1f s" % (images, w["N"], name, dt)}
+    while True:
+        _, used = oracle.block_forward(xd, p, act="gelu", return_threads=True)
+        passes += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    images = passes * w["N"]
+    return {"value": round(images / dt, 2), "unit": "images/s", "cores": int(used), "kind": "oracle",
+            "sample": "%d passes over the %d-image batch of %s (fp64 C loops), %.1f s"
+                      % (passes, w["N"], name, dt)}
 
 
 def main():
@@ -131,7 +202,9 @@ def main():
     ap.add_argument("--workload", default=BENCH_WORKLOAD)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
-    ap.add_argument("--cpu-images", type=int, default=8)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run a 256 MiB elementwise copy (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this library has no multi-GPU path; run with --gpus 1",
@@ -143,22 +216,24 @@ def main():
     cf.lib()
     name = args.workload
     w = WORKLOADS[name]
-    res = block_case(name, args.steps, args.warmup)
+    res = block_case(name, args.steps, args.warmup, per_launch=True)
     t = res["seconds"]
+    tk = res["kernel_seconds"]
     N = res["N"]
     ips = N / t
     eff = rl.comp_eff(res["flops"], t)
-    gbps = res["bytes"] / t / 1e9
+    gbps = res["bytes"] / tk / 1e9
     t_hbm = res["bytes"] / rl.PEAK_HBM_BPS
     t_mfma = res["flops"] / rl.PEAK_FP16_FLOPS
     bound = "hbm" if t_hbm >= t_mfma else "mfma"
     if bound == "hbm":
         roof = {"bound": "hbm", "achieved": round(gbps, 1), "peak": rl.PEAK_HBM_BPS / 1e9, "unit": "GB/s",
-                "frac": round(gbps * 1e9 / rl.PEAK_HBM_BPS, 4), "traffic": None}
+                "frac": round(gbps * 1e9 / rl.PEAK_HBM_BPS, 4), "traffic": measured_traffic(name)}
     else:
-        tf = res["flops"] / t / 1e12
+        tf = res["flops"] / tk / 1e12
         roof = {"bound": "mfma", "achieved": round(tf, 1), "peak": rl.PEAK_FP16_FLOPS / 1e12,
-                "unit": "TFLOP/s", "frac": round(tf * 1e12 / rl.PEAK_FP16_FLOPS, 4), "traffic": None}
+                "unit": "TFLOP/s", "frac": round(tf * 1e12 / rl.PEAK_FP16_FLOPS, 4),
+                "traffic": measured_traffic(name)}
     out = {
         "metric": "images/sec and % of fp16 MFMA peak (computational efficiency), batch 128",
         "value": round(ips, 1),
@@ -176,7 +251,7 @@ def main():
                    "k": w["k"], "act": "gelu_erf", "kernel": "fused block (1 launch)"},
         "comp_eff": round(eff, 4),
         "tflops": round(res["flops"] / t / 1e12, 1),
-        "hbm_gbps_algorithmic": round(gbps, 1),
+        "kernel_us": round(tk * 1e6, 2),
         "roofline": roof,
     }
     if not args.no_extra:
@@ -207,8 +282,10 @@ def main():
                              "comp_eff": round(rl.comp_eff(s["flops"], s["seconds"]), 4),
                              "waterline_C_max": round(s["waterline_C_max"], 4)}
         out["other_workloads"] = extra
+    if args.calib_copy:
+        calib_copy()
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(name, args.cpu_images)
+        out["cpu_baseline"] = cpu_baseline(name, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 

@@ -82,15 +82,15 @@ struct BF16 {
 // positive, so past the fitted range P grows monotonically and the [0, 1]
 // clamp (folded into v_pk_fma_f16) saturates it on the correct side; fp16
 // overflow of w*w gives +-inf, which clamps the same way.  Measured over all
-// finite fp16 inputs, in units of u: |error| < 4.3e-3 for |u| < 10 and
-// < 3.8e-3 * |u| beyond.
+// finite fp16 inputs, in units of u: |error| < 4.1e-3 for |u| < 10 and exact
+// (the clamp saturates) beyond.
 // Cost: 7 packed instructions per pair of hidden values.
 __device__ __forceinline__ half2v gelu_pk_f16_quarter(half2v w) {
-    const half2v c0 = {(_Float16)1.54974312f, (_Float16)1.54974312f};
-    const half2v c1 = {(_Float16)-3.45119285f, (_Float16)-3.45119285f};
-    const half2v c2 = {(_Float16)5.28594729f, (_Float16)5.28594729f};
-    const half2v c3 = {(_Float16)-4.21833024f, (_Float16)-4.21833024f};
-    const half2v c4 = {(_Float16)1.36138518f, (_Float16)1.36138518f};
+    const half2v c0 = {(_Float16)1.54939579f, (_Float16)1.54939579f};
+    const half2v c1 = {(_Float16)-3.45025448f, (_Float16)-3.45025448f};
+    const half2v c2 = {(_Float16)5.28372267f, (_Float16)5.28372267f};
+    const half2v c3 = {(_Float16)-4.21061152f, (_Float16)-4.21061152f};
+    const half2v c4 = {(_Float16)1.34444057f, (_Float16)1.34444057f};
     const half2v half_ = {(_Float16)0.5f, (_Float16)0.5f};
     const half2v zero = {(_Float16)0.0f, (_Float16)0.0f};
     const half2v one = {(_Float16)1.0f, (_Float16)1.0f};
