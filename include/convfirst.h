@@ -59,7 +59,7 @@ typedef enum { CF_F16 = 0, CF_BF16 = 1 } cf_dtype;
 
 /* Activation phi after the expand layer (eq. e:ffn).  GELU is the exact
  * Gaussian-CDF form u * Phi(u).  The fused fp16 kernels evaluate it with a
- * packed-fp16 polynomial whose absolute error is below 4.1e-3 for |u| < 10
+ * packed-fp16 polynomial whose absolute error is below 3.4e-3 for |u| < 10
  * and zero beyond (it saturates to 0 and u); the fused bf16 kernels and the
  * layer-by-layer kernels use fp32 erf.
  * CF_ACT_NONE makes the block affine (used by tests). */

@@ -191,14 +191,9 @@ __device__ __forceinline__ uint32_t act_q(float a, float b) {
 template <typename T, int ACT, int NP>
 __device__ __forceinline__ void act_pairs(const float (&a)[2 * NP], uint32_t (&out)[NP]) {
     if constexpr (ACT == ACT_GELU && !T::is_bf16) {
-        const half2v c0 = {(_Float16)1.54974312f, (_Float16)1.54974312f};
-        const half2v c1 = {(_Float16)-3.45119285f, (_Float16)-3.45119285f};
-        const half2v c2 = {(_Float16)5.28594729f, (_Float16)5.28594729f};
-        const half2v c3 = {(_Float16)-4.21833024f, (_Float16)-4.21833024f};
-        const half2v c4 = {(_Float16)1.36138518f, (_Float16)1.36138518f};
-        const half2v half_ = {(_Float16)0.5f, (_Float16)0.5f};
-        const half2v zero = {(_Float16)0.0f, (_Float16)0.0f};
-        const half2v one = {(_Float16)1.0f, (_Float16)1.0f};
+        const half2v c0 = splat2(GELU_Q0), c1 = splat2(GELU_Q1), c2 = splat2(GELU_Q2);
+        const half2v c3 = splat2(GELU_Q3), c4 = splat2(GELU_Q4);
+        const half2v half_ = splat2(0.5f), zero = splat2(0.0f), one = splat2(1.0f);
         half2v w[NP], sq[NP], q[NP];
 #pragma unroll
         for (int p = 0; p < NP; p++) {

@@ -20,7 +20,7 @@ import numpy as np
 from scipy.optimize import minimize
 from scipy.special import erf
 
-A = 4.0       # fit range in u
+A = 3.5       # fit range in u
 DEG = 4       # degree of Q in w*w
 
 
