@@ -1,0 +1,697 @@
+// cf_block64.h -- fused ConvFirst block for C = 64 channels, fp16 I/O, on
+// gfx950.  Instantiated per depth-wise size in cf_block64_k*.hip.
+//
+// The block (Sec. 5.3 of Lavin, arXiv:2404.03617, norms folded to scale and
+// bias) is evaluated by one persistent workgroup of 8 waves per CU with the
+// block-fusion schedule of Sec. 5.3.1 / 5.5.1.  Differences from the generic
+// kernel in cf_fused_impl.h, all aimed at the VALU and LDS budgets of the
+// C = 64 case:
+//
+//  * Work is dealt in blocks of 32 consecutive pixels (N*H*W flattened).  Each
+//    workgroup owns a contiguous range of blocks (ranges of neighbouring
+//    workgroups sit on the same XCD, so halo rows shared by two ranges hit the
+//    same L2) and walks it in tiles of up to 12 blocks.  In a 12-block tile
+//    waves 0-3 take two blocks (64 pixels) and waves 4-7 one block; waves w
+//    and w+4 share a SIMD, so every SIMD carries three blocks.
+//  * W1, W2 (with s1, s2 folded in) and b1 stay in LDS for the whole kernel.
+//  * The input tile plus halo is copied into LDS through registers (coalesced
+//    16-byte loads); the copy of the next tile is spread over the FFN chunk
+//    loop of the current one.  Pixels sit 144 bytes apart (128 data + 16 pad): eight
+//    lanes reading the same channel chunk of eight neighbouring pixels hit
+//    eight different bank groups, and every tap is the pixel's base address
+//    plus a compile-time offset (fixed row stride), so the depth-wise loop
+//    issues no address arithmetic.  Taps that fall outside the pixel's image
+//    are redirected, row by row, to a zero area.
+//  * Depth-wise conv on the VALU in packed fp16.  A two-block wave lets each
+//    lane compute one pixel for all 16 channels of a K step; the taps are then
+//    wave-uniform and come from scalar registers (s_load), and one
+//    v_permlane32_swap per register pair rearranges the result into the two
+//    MFMA B fragments.  A one-block wave uses the B-fragment lane layout
+//    directly with the taps from LDS.
+//  * FFN per 32-hidden chunk on v_mfma_f32_32x32x16_f16 with swapped operands
+//    (weights = A, pixels = B), the sigma/tau row orders of cf_fused_impl.h,
+//    b1 in the C operand, GELU evaluated on interleaved fp16 pairs.
+//  * Accumulators start at x/4 + b2/4 read from the LDS halo (residual), the
+//    activation variable is u/4 (exact power-of-two scaling), output 4*acc.
+#pragma once
+#include "cf_fused_impl.h"
+
+namespace cf {
+namespace b64 {
+
+using fused::FastDiv;
+using fused::fdiv;
+using fused::mfma32;
+using fused::float16v;
+using fused::sigma_row;
+using fused::tau_row;
+
+constexpr int C = 64;
+constexpr int NWAVE = 8;
+constexpr int NT = NWAVE * 64;
+constexpr int KST = C / 16;          // expand K steps
+constexpr int CB = C / 32;           // 32-channel output blocks
+constexpr int MAX_TB = 16;           // blocks per tile (two per wave at most)
+constexpr int PIX = 144;             // LDS bytes per halo pixel
+constexpr int CHUNK_W1 = KST * 1024; // W1 fragments of one 32-hidden chunk
+constexpr int CHUNK_W2 = 2 * CB * 1024;
+constexpr float QS = 0.25f;
+
+struct Args {
+    const uint16_t *x;
+    uint16_t *y;
+    const uint16_t *dw_w;
+    const float *s0, *b0;
+    const uint16_t *w1;
+    const float *s1, *b1;
+    const uint16_t *w2;
+    const float *s2, *b2;
+    int H, W, NH;        // NH = N*H (global image rows)
+    int nch;             // hidden chunks = E*C/32
+    uint32_t P;          // N*H*W < 2^31
+    FastDiv divW, divH;
+    int nblocks;         // ceil(P / 32)
+    int range_base, range_extra;  // blocks per workgroup: base (+1 for the first `extra`)
+    int tile_max;        // largest tile, <= MAX_TB blocks
+    uint32_t rs;         // LDS bytes per halo row: (W + 2*pad) * PIX
+    int halo_rows;       // data rows of the halo buffer
+    // LDS byte offsets
+    uint32_t off_w2, off_b1, off_cst, off_dwt, off_halo, off_zero;
+};
+
+// LDS map: [W1 nch*4 KB][W2 nch*4 KB][b1/4 nch*128 B][cst 512 B][taps k*k*128 B]
+//          [halo halo_rows * rs][zero area]
+struct Layout {
+    uint32_t w2, b1, cst, dwt, halo, zero, total;
+};
+
+inline Layout layout_for(int nch, int k, int halo_rows, uint32_t rs) {
+    Layout L;
+    L.w2 = (uint32_t)nch * CHUNK_W1;
+    L.b1 = L.w2 + (uint32_t)nch * CHUNK_W2;
+    L.cst = L.b1 + (uint32_t)nch * 128;
+    L.dwt = L.cst + 512;
+    L.halo = (L.dwt + (uint32_t)k * k * 128 + 255) & ~255u;
+    L.zero = L.halo + (uint32_t)halo_rows * rs;
+    L.total = L.zero + (uint32_t)k * PIX + 128;
+    return L;
+}
+
+// halo rows a tile of tb blocks can touch (data rows, without the zero area)
+inline int halo_rows_for(int tb, int k, int W, int64_t NH) {
+    int64_t span = (int64_t)(32 * tb - 1) / W + 2;
+    if (span > NH)
+        span = NH;
+    return (int)span + 2 * (k / 2);
+}
+
+__device__ __forceinline__ u32x4 ld16(const uint8_t *base, uint32_t off) {
+    return *reinterpret_cast<const u32x4 *>(base + off);
+}
+__device__ __forceinline__ half2v h2(uint32_t w) { return __builtin_bit_cast(half2v, w); }
+__device__ __forceinline__ uint32_t u32(half2v v) { return __builtin_bit_cast(uint32_t, v); }
+
+template <int KS, int ACT>
+struct K64 {
+    static constexpr int PAD = KS / 2;
+
+    // ---- activation of 2*NP fp32 values (scaled by 1/4) into NP packed pairs.
+    // Written stage by stage so the NP dependency chains interleave.
+    template <int NP>
+    static __device__ __forceinline__ void activate(const float *a, uint32_t *out) {
+        half2v w[NP];
+#pragma unroll
+        for (int p = 0; p < NP; p++) {
+            w[p].x = (_Float16)a[2 * p];
+            w[p].y = (_Float16)a[2 * p + 1];
+        }
+        if constexpr (ACT == ACT_GELU) {
+            half2v s[NP], q[NP];
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                s[p] = w[p] * w[p];
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                q[p] = __builtin_elementwise_fma(s[p], splat2(GELU_Q4), splat2(GELU_Q3));
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                q[p] = __builtin_elementwise_fma(s[p], q[p], splat2(GELU_Q2));
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                q[p] = __builtin_elementwise_fma(s[p], q[p], splat2(GELU_Q1));
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                q[p] = __builtin_elementwise_fma(s[p], q[p], splat2(GELU_Q0));
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                q[p] = __builtin_elementwise_min(
+                    __builtin_elementwise_max(__builtin_elementwise_fma(w[p], q[p], splat2(0.5f)), splat2(0.0f)),
+                    splat2(1.0f));
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                out[p] = u32(w[p] * q[p]);
+        } else if constexpr (ACT == ACT_RELU) {
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                out[p] = u32(__builtin_elementwise_max(w[p], splat2(0.0f)));
+        } else {
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                out[p] = u32(w[p]);
+        }
+    }
+
+    // ---- one-time staging: weights in MFMA fragment order with s1/s2 folded,
+    // b1/4 in expand register order, per-channel constants, depth-wise taps.
+    static __device__ void stage(const Args &a, uint8_t *smem, int tid) {
+        const int pieces = a.nch * 512;  // 16-byte pieces: 256 of W1 + 256 of W2 per chunk
+        for (int p = tid; p < pieces; p += NT) {
+            const int ch = p >> 9, r = p & 511;
+            const int lane = r & 63, f = r >> 6;  // f < 4: W1 K step; f >= 4: W2 (cb, kk)
+            const int hh = lane >> 5, mm = lane & 31;
+            const uint16_t *src;
+            float sc;
+            uint32_t dst;
+            if (f < KST) {
+                const int row = ch * 32 + sigma_row(mm);
+                src = a.w1 + (size_t)row * C + f * 16 + 8 * hh;
+                sc = a.s1 ? a.s1[row] : 1.0f;
+                dst = (uint32_t)ch * CHUNK_W1 + (uint32_t)(f * 64 + lane) * 16;
+            } else {
+                const int g = f - KST, cb = g >> 1, kk = g & 1;
+                const int row = cb * 32 + tau_row(mm);
+                src = a.w2 + (size_t)row * (a.nch * 32) + ch * 32 + 16 * kk + 8 * hh;
+                sc = a.s2 ? a.s2[row] : 1.0f;
+                dst = a.off_w2 + (uint32_t)ch * CHUNK_W2 + (uint32_t)(g * 64 + lane) * 16;
+            }
+            Pack8 v;
+            v.u = *reinterpret_cast<const u32x4 *>(src);
+            if (sc != 1.0f) {
+#pragma unroll
+                for (int q = 0; q < 4; q++)
+                    v.w[q] = F16::pack2(F16::lo(v.w[q]) * sc, F16::hi(v.w[q]) * sc);
+            }
+            *reinterpret_cast<u32x4 *>(smem + dst) = v.u;
+        }
+        // b1 / 4: chunk ch, half h, register e = 4t + i  <->  hidden 16(t>>1) + 8h + 4(t&1) + i
+        for (int p = tid; p < a.nch * 32; p += NT) {
+            const int ch = p >> 5, e = p & 31, hh = e >> 4, t = (e >> 2) & 3, i = e & 3;
+            const int r = ch * 32 + 16 * (t >> 1) + 8 * hh + 4 * (t & 1) + i;
+            reinterpret_cast<float *>(smem + a.off_b1)[p] = a.b1 ? a.b1[r] * QS : 0.0f;
+        }
+        for (int c = tid; c < C; c += NT) {
+            reinterpret_cast<_Float16 *>(smem + a.off_cst)[c] = (_Float16)((a.s0 ? a.s0[c] : 1.0f) * QS);
+            reinterpret_cast<_Float16 *>(smem + a.off_cst + 128)[c] = (_Float16)((a.b0 ? a.b0[c] : 0.0f) * QS);
+            reinterpret_cast<float *>(smem + a.off_cst + 256)[c] = a.b2 ? a.b2[c] * QS : 0.0f;
+        }
+        for (int p = tid; p < KS * KS * 8; p += NT)
+            reinterpret_cast<u32x4 *>(smem + a.off_dwt)[p] = reinterpret_cast<const u32x4 *>(a.dw_w)[p];
+    }
+
+    // ---- halo copy of the tile starting at block t0 with nblk blocks.
+    // Row r of the buffer holds global image row g_lo - PAD + r; pixel column c
+    // (c = image column + PAD) starts at r*rs + c*PIX; 16-byte slot s of a row
+    // interior belongs to pixel s / 9, chunk s % 9 (chunk 8 is padding and gets
+    // a copy of chunk 7).
+    static __device__ __forceinline__ void tile_rows(const Args &a, int t0, int nblk, uint32_t &g_lo, int &rows) {
+        const uint32_t p0 = (uint32_t)t0 * 32;
+        uint32_t pend = p0 + (uint32_t)nblk * 32;
+        if (pend > a.P)
+            pend = a.P;
+        g_lo = fdiv(p0, a.divW);
+        rows = (int)(fdiv(pend - 1, a.divW) - g_lo) + 1 + 2 * PAD;
+    }
+
+    // ---- halo copy.  Row r of the buffer holds global image row g_lo - PAD + r;
+    // pixel column c (= image column + PAD) starts at r*rs + c*PIX.  A row of
+    // the image is W*128 contiguous bytes; wave wv copies its 1 KB part wv
+    // (W + 2*PAD <= 64, so a row has at most 8 parts): lane l moves bytes
+    // 16l..16l+15 of the part, i.e. chunk l % 8 of pixel 8*wv + l / 8, with a
+    // plain coalesced 16-byte global load and a 16-byte LDS write.
+    struct RowCopy {
+        int goff;       // byte offset in the image row, -1 if this lane has no data
+        uint32_t loff;  // byte offset in the halo row
+    };
+    static __device__ __forceinline__ RowCopy row_copy(const Args &a, int wv, int lane) {
+        const int px = 8 * wv + (lane >> 3), c = lane & 7;
+        RowCopy rc;
+        rc.goff = px < a.W ? px * (C * 2) + c * 16 : -1;
+        rc.loff = (uint32_t)(PAD + px) * PIX + (uint32_t)c * 16;
+        return rc;
+    }
+    struct NextHalo {
+        uint32_t g_lo;
+        int rows;  // 0: nothing to copy
+    };
+    // rows r = ch, ch + nch, ... of the next tile pass through registers: loaded
+    // during chunk ch, written to LDS during chunk ch + 1
+    struct Staged {
+        u32x4 v[2];
+        int r[2];
+    };
+    static __device__ __forceinline__ void load_rows(const Args &a, const NextHalo &nh, const RowCopy &rc, int ch,
+                                                     Staged &st) {
+#pragma unroll
+        for (int q = 0; q < 2; q++) {
+            const int r = ch + q * a.nch;
+            const int grow = (int)nh.g_lo - PAD + r;
+            st.r[q] = -1;
+            if (r < nh.rows && grow >= 0 && grow < a.NH && rc.goff >= 0) {
+                st.v[q] = *reinterpret_cast<const u32x4 *>(reinterpret_cast<const uint8_t *>(a.x) +
+                                                           (size_t)grow * a.W * (C * 2) + rc.goff);
+                st.r[q] = r;
+            }
+        }
+    }
+    static __device__ __forceinline__ void write_rows(const Args &a, uint8_t *smem, const RowCopy &rc,
+                                                      const Staged &st) {
+#pragma unroll
+        for (int q = 0; q < 2; q++)
+            if (st.r[q] >= 0)
+                *reinterpret_cast<u32x4 *>(smem + a.off_halo + (uint32_t)st.r[q] * a.rs + rc.loff) = st.v[q];
+    }
+    // whole halo at once (first tile)
+    static __device__ __forceinline__ void copy_halo(const Args &a, uint8_t *smem, int t0, int nblk,
+                                                     const RowCopy &rc) {
+        NextHalo nh;
+        tile_rows(a, t0, nblk, nh.g_lo, nh.rows);
+        for (int r = 0; r < nh.rows; r++) {
+            const int grow = (int)nh.g_lo - PAD + r;
+            if (grow >= 0 && grow < a.NH && rc.goff >= 0)
+                *reinterpret_cast<u32x4 *>(smem + a.off_halo + (uint32_t)r * a.rs + rc.loff) =
+                    *reinterpret_cast<const u32x4 *>(reinterpret_cast<const uint8_t *>(a.x) +
+                                                     (size_t)grow * a.W * (C * 2) + rc.goff);
+        }
+    }
+
+    // Base addresses of the KS tap rows of a pixel: the top-left tap of the
+    // pixel's window plus i*rs for row i, or (for rows outside the pixel's
+    // image, and for invalid pixels) an address that lands every tap of that
+    // row in the zero area.
+    static __device__ __forceinline__ void tap_bases(const Args &a, uint32_t pix, bool valid, uint32_t g_lo,
+                                                     uint32_t extra, uint32_t (&base)[KS], uint32_t &centre) {
+        uint32_t topleft = 0, hh = 0;
+        if (valid) {
+            const uint32_t gg = fdiv(pix, a.divW);
+            const uint32_t wc = pix - gg * (uint32_t)a.W;
+            hh = gg - fdiv(gg, a.divH) * (uint32_t)a.H;
+            topleft = a.off_halo + (gg - g_lo) * a.rs + wc * PIX;
+        }
+        centre = topleft + PAD * a.rs + PAD * PIX + extra;
+#pragma unroll
+        for (int i = 0; i < KS; i++) {
+            const int hr = (int)hh + i - PAD;
+            const bool in = valid && hr >= 0 && hr < a.H;
+            base[i] = (in ? topleft + (uint32_t)i * a.rs : a.off_zero) + extra;
+        }
+    }
+
+    // ---- depth-wise conv, two-block wave: lane l computes pixel l of the
+    // wave's 64 (block j0 for l < 32, block j1 above) for all 16 channels of
+    // each K step with wave-uniform taps, then swaps halves into B fragments.
+    static __device__ __forceinline__ void dw_pair(const Args &a, const uint8_t *smem, const uint32_t (&base)[KS],
+                                                   u32x4 (&dfr)[KST][2]) {
+        typedef const __attribute__((address_space(4))) uint32_t *cptr;
+        const cptr wq = (cptr)a.dw_w;
+#pragma unroll
+        for (int ks = 0; ks < KST; ks++) {
+            uint32_t d[2][4];
+#pragma unroll
+            for (int c8 = 0; c8 < 2; c8++) {
+                const int q = 2 * ks + c8;  // 16-byte channel chunk
+                half2v acc[4] = {splat2(0.0f), splat2(0.0f), splat2(0.0f), splat2(0.0f)};
+#pragma unroll
+                for (int i = 0; i < KS; i++) {
+#pragma unroll
+                    for (int j = 0; j < KS; j++) {
+                        Pack8 v;
+                        v.u = ld16(smem, base[i] + (uint32_t)(j * PIX + q * 16));
+                        const int wo = ((i * KS + j) * C + q * 8) / 2;  // dword index of the taps
+                        const uint32_t w0 = wq[wo], w1 = wq[wo + 1], w2 = wq[wo + 2], w3 = wq[wo + 3];
+                        acc[0] = __builtin_elementwise_fma(h2(v.w[0]), h2(w0), acc[0]);
+                        acc[1] = __builtin_elementwise_fma(h2(v.w[1]), h2(w1), acc[1]);
+                        acc[2] = __builtin_elementwise_fma(h2(v.w[2]), h2(w2), acc[2]);
+                        acc[3] = __builtin_elementwise_fma(h2(v.w[3]), h2(w3), acc[3]);
+                    }
+                }
+                Pack8 sp, bp;
+                sp.u = ld16(smem, a.off_cst + q * 16);
+                bp.u = ld16(smem, a.off_cst + 128 + q * 16);
+#pragma unroll
+                for (int e = 0; e < 4; e++)
+                    d[c8][e] = u32(__builtin_elementwise_fma(acc[e], h2(sp.w[e]), h2(bp.w[e])));
+            }
+            // lanes 32-63 of d[0] <-> lanes 0-31 of d[1]
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                const auto r = __builtin_amdgcn_permlane32_swap(d[0][e], d[1][e], false, false);
+                dfr[ks][0][e] = r[0];
+                dfr[ks][1][e] = r[1];
+            }
+        }
+    }
+
+    // ---- depth-wise conv, one-block wave: lane (h, m) computes channels
+    // 16ks + 8h .. +7 of pixel m (the B-fragment layout); taps from LDS.
+    static __device__ __forceinline__ void dw_single(const Args &a, const uint8_t *smem, const uint32_t (&base)[KS],
+                                                     int h, u32x4 (&dfr)[KST][2]) {
+        const uint32_t wbase = a.off_dwt + (uint32_t)h * 16;
+#pragma unroll
+        for (int ks = 0; ks < KST; ks++) {
+            half2v acc[4] = {splat2(0.0f), splat2(0.0f), splat2(0.0f), splat2(0.0f)};
+#pragma unroll
+            for (int i = 0; i < KS; i++) {
+#pragma unroll
+                for (int j = 0; j < KS; j++) {
+                    Pack8 v, w;
+                    v.u = ld16(smem, base[i] + (uint32_t)(j * PIX + 2 * ks * 16));
+                    w.u = ld16(smem, wbase + (uint32_t)((i * KS + j) * 128 + 2 * ks * 16));
+#pragma unroll
+                    for (int e = 0; e < 4; e++)
+                        acc[e] = __builtin_elementwise_fma(h2(v.w[e]), h2(w.w[e]), acc[e]);
+                }
+            }
+            Pack8 sp, bp;
+            sp.u = ld16(smem, a.off_cst + (uint32_t)(2 * ks + h) * 16);
+            bp.u = ld16(smem, a.off_cst + 128 + (uint32_t)(2 * ks + h) * 16);
+#pragma unroll
+            for (int e = 0; e < 4; e++)
+                dfr[ks][0][e] = u32(__builtin_elementwise_fma(acc[e], h2(sp.w[e]), h2(bp.w[e])));
+        }
+    }
+
+    // ---- residual start: acc = x/4 + b2/4 from the halo centre, MFMA layout
+    // (lane (h, m): channels cb*32 + 16h .. +15 of pixel m of block b).
+    template <int NB>
+    static __device__ __forceinline__ void residual(const Args &a, const uint8_t *smem, const uint32_t (&centre)[2],
+                                                    int h, float16v (&acc)[CB][2]) {
+#pragma unroll
+        for (int cb = 0; cb < CB; cb++) {
+            const float16v bias = *reinterpret_cast<const float16v *>(smem + a.off_cst + 256 + (cb * 32 + 16 * h) * 4);
+#pragma unroll
+            for (int b = 0; b < NB; b++) {
+                Pack8 v0, v1;
+                v0.u = ld16(smem, centre[b] + (uint32_t)(cb * 64));
+                v1.u = ld16(smem, centre[b] + (uint32_t)(cb * 64 + 16));
+                float16v t;
+#pragma unroll
+                for (int q = 0; q < 4; q++) {
+                    t[2 * q] = fmaf(F16::lo(v0.w[q]), QS, bias[2 * q]);
+                    t[2 * q + 1] = fmaf(F16::hi(v0.w[q]), QS, bias[2 * q + 1]);
+                    t[8 + 2 * q] = fmaf(F16::lo(v1.w[q]), QS, bias[8 + 2 * q]);
+                    t[8 + 2 * q + 1] = fmaf(F16::hi(v1.w[q]), QS, bias[8 + 2 * q + 1]);
+                }
+                acc[cb][b] = t;
+            }
+        }
+    }
+
+    // ---- FFN over all hidden chunks (eq. e:ffn-eff): expand, phi, project.
+    // Software-pipelined by one chunk: while chunk c is activated and
+    // projected, the fragments of chunk c+1 are already loaded and its expand
+    // is issued between the activation and the projection of chunk c, so no
+    // instruction waits on an LDS read or on an MFMA result it just issued.
+    template <int NB>
+    static __device__ __forceinline__ void expand(const uint8_t *w1p, const uint8_t *b1p, int ch,
+                                                  const u32x4 (&dfr)[KST][2], float16v (&hh)[2]) {
+        u32x4 w1f[KST];
+#pragma unroll
+        for (int ks = 0; ks < KST; ks++)
+            w1f[ks] = *reinterpret_cast<const u32x4 *>(w1p + ch * CHUNK_W1 + ks * 1024);
+        const float16v bias = *reinterpret_cast<const float16v *>(b1p + ch * 128);
+#pragma unroll
+        for (int b = 0; b < NB; b++)
+            hh[b] = bias;
+#pragma unroll
+        for (int ks = 0; ks < KST; ks++)
+#pragma unroll
+            for (int b = 0; b < NB; b++)
+                hh[b] = mfma32(w1f[ks], dfr[ks][b], hh[b], F16{});
+    }
+
+    template <int NB, bool MORE>
+    static __device__ __forceinline__ void chunk_step(const Args &a, uint8_t *smem, const NextHalo &nh,
+                                                      const RowCopy &rc, Staged &stg, const uint8_t *w1p, const uint8_t *w2p,
+                                                      const uint8_t *b1p, int ch, const u32x4 (&dfr)[KST][2],
+                                                      float16v (&hc)[2], float16v (&acc)[CB][2]) {
+        u32x4 w2f[2 * CB];
+#pragma unroll
+        for (int g = 0; g < 2 * CB; g++)
+            w2f[g] = *reinterpret_cast<const u32x4 *>(w2p + ch * CHUNK_W2 + g * 1024);
+        float v[NB * 16];
+#pragma unroll
+        for (int b = 0; b < NB; b++)
+#pragma unroll
+            for (int e = 0; e < 16; e++)
+                v[b * 16 + e] = hc[b][e];
+        uint32_t o[NB * 8];
+        activate<NB * 8>(v, o);
+        if constexpr (MORE)
+            expand<NB>(w1p, b1p, ch + 1, dfr, hc);
+        write_rows(a, smem, rc, stg);
+        load_rows(a, nh, rc, ch, stg);
+#pragma unroll
+        for (int kk = 0; kk < 2; kk++)
+#pragma unroll
+            for (int cb = 0; cb < CB; cb++)
+#pragma unroll
+                for (int b = 0; b < NB; b++) {
+                    u32x4 hid;
+#pragma unroll
+                    for (int p = 0; p < 4; p++)
+                        hid[p] = o[b * 8 + kk * 4 + p];
+                    acc[cb][b] = mfma32(w2f[cb * 2 + kk], hid, acc[cb][b], F16{});
+                }
+    }
+
+    template <int NB>
+    static __device__ __forceinline__ void ffn(const Args &a, uint8_t *smem, int lane, const NextHalo &nh,
+                                               const RowCopy &rc, const u32x4 (&dfr)[KST][2],
+                                               float16v (&acc)[CB][2]) {
+        const int h = lane >> 5;
+        const uint8_t *w1p = smem + lane * 16;
+        const uint8_t *w2p = smem + a.off_w2 + lane * 16;
+        const uint8_t *b1p = smem + a.off_b1 + h * 64;
+        float16v hc[2];
+        Staged stg;
+        stg.r[0] = stg.r[1] = -1;
+        expand<NB>(w1p, b1p, 0, dfr, hc);
+#pragma unroll 1
+        for (int ch = 0; ch + 1 < a.nch; ch++)
+            chunk_step<NB, true>(a, smem, nh, rc, stg, w1p, w2p, b1p, ch, dfr, hc, acc);
+        chunk_step<NB, false>(a, smem, nh, rc, stg, w1p, w2p, b1p, a.nch - 1, dfr, hc, acc);
+        write_rows(a, smem, rc, stg);
+    }
+
+    template <int NB>
+    static __device__ __forceinline__ int store(const Args &a, const uint32_t (&pix)[2], const bool (&valid)[2],
+                                                int h, const float16v (&acc)[CB][2]) {
+        int n = 0;
+#pragma unroll
+        for (int b = 0; b < NB; b++) {
+            if (__builtin_amdgcn_read_exec() && __ballot(valid[b]))
+                n += 2 * CB;
+            if (!valid[b])
+                continue;
+#pragma unroll
+            for (int cb = 0; cb < CB; cb++) {
+                u32x4 o0, o1;
+#pragma unroll
+                for (int q = 0; q < 4; q++) {
+                    o0[q] = F16::pack2(4.0f * acc[cb][b][2 * q], 4.0f * acc[cb][b][2 * q + 1]);
+                    o1[q] = F16::pack2(4.0f * acc[cb][b][8 + 2 * q], 4.0f * acc[cb][b][8 + 2 * q + 1]);
+                }
+                u32x4 *dst = reinterpret_cast<u32x4 *>(a.y + (size_t)pix[b] * C + cb * 32 + 16 * h);
+                dst[0] = o0;
+                dst[1] = o1;
+            }
+        }
+        return n;
+    }
+
+    static __device__ void run(const Args &a, uint8_t *smem) {
+        const int tid = threadIdx.x;
+        const int lane = tid & 63, wv = tid >> 6;
+        const int h = lane >> 5, m = lane & 31;
+
+        // block range of this workgroup; consecutive ranges on one XCD
+        const int G = gridDim.x;
+        const int g = (G % 8 == 0) ? (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8 : blockIdx.x;
+        const int lo = g * a.range_base + (g < a.range_extra ? g : a.range_extra);
+        const int hi = lo + a.range_base + (g < a.range_extra ? 1 : 0);
+
+        // zero the halo region and the zero area once; stage weights
+        for (uint32_t i = a.off_halo / 16 + tid; i < (a.off_zero + KS * PIX + 128) / 16; i += NT)
+            reinterpret_cast<u32x4 *>(smem)[i] = u32x4{0u, 0u, 0u, 0u};
+        stage(a, smem, tid);
+        __syncthreads();
+
+        const RowCopy rc = row_copy(a, wv, lane);
+        // the range is cut into nt tiles of nearly equal size (<= tile_max)
+        const int range = hi - lo;
+        const int nt = (range + a.tile_max - 1) / a.tile_max;
+        const int tsz = nt ? range / nt : 0, tex = nt ? range % nt : 0;
+        if (nt > 0)
+            copy_halo(a, smem, lo, tsz + (tex > 0 ? 1 : 0), rc);
+
+        int t0 = lo;
+        for (int it = 0; it < nt; it++) {
+            const int nblk = tsz + (it < tex ? 1 : 0);
+            uint32_t g_lo;
+            int rows;
+            tile_rows(a, t0, nblk, g_lo, rows);
+            // this wave's blocks: w (if w < nblk) and 8 + w (if 8 + w < nblk)
+            const int nb = (wv < nblk ? 1 : 0) + (wv + 8 < nblk ? 1 : 0);
+            const int jb[2] = {wv, wv + 8};
+
+            // MFMA-layout pixels of lane (h, m) and their halo centres
+            uint32_t pix[2], centre[2];
+            bool valid[2];
+#pragma unroll
+            for (int b = 0; b < 2; b++) {
+                pix[b] = (uint32_t)(t0 + jb[b]) * 32 + m;
+                valid[b] = (b < nb) && pix[b] < a.P;
+                uint32_t bs[KS];
+                tap_bases(a, pix[b], valid[b], g_lo, (uint32_t)h * 32, bs, centre[b]);
+            }
+
+            __syncthreads();  // the tile's halo is in LDS
+
+            u32x4 dfr[KST][2];
+            float16v acc[CB][2];
+            if (nb == 2) {
+                // depth-wise layout: lane l -> pixel l & 31 of block jb[l >> 5]
+                const uint32_t pd = (uint32_t)(t0 + jb[h]) * 32 + m;
+                uint32_t bs[KS], cdummy;
+                tap_bases(a, pd, pd < a.P, g_lo, 0u, bs, cdummy);
+                dw_pair(a, smem, bs, dfr);
+                residual<2>(a, smem, centre, h, acc);
+            } else if (nb == 1) {
+                uint32_t bs[KS], cdummy;
+                tap_bases(a, pix[0], valid[0], g_lo, (uint32_t)h * 16, bs, cdummy);
+                dw_single(a, smem, bs, h, dfr);
+                residual<1>(a, smem, centre, h, acc);
+            }
+            __syncthreads();  // the halo buffer is free
+            NextHalo nh{0u, 0};
+            const int t1 = t0 + nblk;
+            const int nblk1 = tsz + (it + 1 < tex ? 1 : 0);
+            if (it + 1 < nt)
+                tile_rows(a, t1, nblk1, nh.g_lo, nh.rows);
+
+            if (nb == 2) {
+                ffn<2>(a, smem, lane, nh, rc, dfr, acc);
+                store<2>(a, pix, valid, h, acc);
+            } else if (nb == 1) {
+                ffn<1>(a, smem, lane, nh, rc, dfr, acc);
+                store<1>(a, pix, valid, h, acc);
+            } else if (nh.rows > 0) {
+                copy_halo(a, smem, t1, nblk1, rc);
+            }
+            t0 = t1;
+            (void)rows;
+        }
+        __builtin_amdgcn_s_waitcnt(0);
+    }
+};
+
+template <int KS, int ACT>
+__global__ __launch_bounds__(NT, 1) void block64_kernel(Args a) {
+    extern __shared__ __attribute__((aligned(256))) uint8_t smem[];
+    K64<KS, ACT>::run(a, smem);
+}
+
+// ---------------------------------------------------------------------------
+// Host side.  Returns hipErrorInvalidConfiguration when the shape needs the
+// generic kernel (W too wide for the fixed halo row, or LDS does not fit).
+inline bool plan(int N, int H, int W, int E, int k, int &tb, int &halo_rows, uint32_t &rs, Layout &L) {
+    const int pad = k / 2;
+    if (W + 2 * pad > 64 || E * C % 32 != 0 || E * C / 32 > 8)
+        return false;
+    rs = (uint32_t)(W + 2 * pad) * PIX;
+    const int64_t NH = (int64_t)N * H;
+    for (tb = MAX_TB; tb >= 1; tb--) {
+        halo_rows = halo_rows_for(tb, k, W, NH);
+        L = layout_for(E * C / 32, k, halo_rows, rs);
+        if (L.total <= 160 * 1024)
+            return true;
+    }
+    return false;
+}
+
+template <int KS>
+hipError_t launch_k(const void *x, void *y, const BlockW &w, const Shape &s, hipStream_t st) {
+    int tb, halo_rows;
+    uint32_t rs;
+    Layout L;
+    if (!plan(s.N, s.H, s.W, s.E, KS, tb, halo_rows, rs, L))
+        return hipErrorInvalidConfiguration;
+    Args a{};
+    a.x = (const uint16_t *)x;
+    a.y = (uint16_t *)y;
+    a.dw_w = (const uint16_t *)w.dw_w;
+    a.s0 = w.s0;
+    a.b0 = w.b0;
+    a.w1 = (const uint16_t *)w.w1;
+    a.s1 = w.s1;
+    a.b1 = w.b1;
+    a.w2 = (const uint16_t *)w.w2;
+    a.s2 = w.s2;
+    a.b2 = w.b2;
+    a.H = s.H;
+    a.W = s.W;
+    a.NH = s.N * s.H;
+    a.nch = s.E * C / 32;
+    const int64_t P = (int64_t)s.N * s.H * s.W;
+    a.P = (uint32_t)P;
+    a.divW = fused::make_fastdiv((uint32_t)s.W);
+    a.divH = fused::make_fastdiv((uint32_t)s.H);
+    a.nblocks = (int)((P + 31) / 32);
+    int G = device_cu_count();
+    if (G > a.nblocks)
+        G = a.nblocks;
+    a.range_base = a.nblocks / G;
+    a.range_extra = a.nblocks % G;
+    a.tile_max = tb;
+    a.rs = rs;
+    a.halo_rows = halo_rows;
+    a.off_w2 = L.w2;
+    a.off_b1 = L.b1;
+    a.off_cst = L.cst;
+    a.off_dwt = L.dwt;
+    a.off_halo = L.halo;
+    a.off_zero = L.zero;
+    hipError_t e;
+    switch (s.act) {
+    case ACT_GELU: {
+        auto kf = block64_kernel<KS, ACT_GELU>;
+        if ((e = hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L.total)))
+            return e;
+        hipLaunchKernelGGL(kf, dim3(G), dim3(NT), L.total, st, a);
+        break;
+    }
+    case ACT_RELU: {
+        auto kf = block64_kernel<KS, ACT_RELU>;
+        if ((e = hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L.total)))
+            return e;
+        hipLaunchKernelGGL(kf, dim3(G), dim3(NT), L.total, st, a);
+        break;
+    }
+    default: {
+        auto kf = block64_kernel<KS, ACT_NONE>;
+        if ((e = hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L.total)))
+            return e;
+        hipLaunchKernelGGL(kf, dim3(G), dim3(NT), L.total, st, a);
+        break;
+    }
+    }
+    return hipGetLastError();
+}
+
+}  // namespace b64
+
+#define CF_B64_UNITS(X) X(1) X(3) X(5) X(7)
+#define CF_DECL_B64(K) hipError_t launch_block64_k##K(const void *x, void *y, const BlockW &w, const Shape &s, hipStream_t st);
+CF_B64_UNITS(CF_DECL_B64)
+
+}  // namespace cf

@@ -1,0 +1,8 @@
+// cf_block64_k7.hip -- C = 64 fused block kernel, 7x7 depth-wise (see cf_block64.h).
+#include "cf_block64.h"
+
+namespace cf {
+hipError_t launch_block64_k7(const void *x, void *y, const BlockW &w, const Shape &s, hipStream_t st) {
+    return b64::launch_k<7>(x, y, w, s, st);
+}
+}  // namespace cf

@@ -31,6 +31,7 @@
 // Hidden-split mode (grid.y > 1): workgroup (tile, g) runs only its range of
 // chunks and writes an fp32 partial of the projected output; a second kernel
 // adds the partials in group order plus b2 and the residual.
+#include "cf_block64.h"
 #include "cf_fused_impl.h"
 
 #include <mutex>
@@ -109,6 +110,16 @@ hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Sha
     a.E = s.E;
     a.P = (uint32_t)((int64_t)s.N * s.H * s.W);
     hipError_t e;
+    if (s.C == 64 && !s.bf16 && groups <= 1) {
+        switch (s.k) {
+        case 1: e = launch_block64_k1(x, y, w, s, st); break;
+        case 3: e = launch_block64_k3(x, y, w, s, st); break;
+        case 5: e = launch_block64_k5(x, y, w, s, st); break;
+        default: e = launch_block64_k7(x, y, w, s, st); break;
+        }
+        if (e != hipErrorInvalidConfiguration)
+            return e;
+    }
     switch (s.C * 2 + s.bf16) {
     case 128: e = launch_c64_F16(a, s.k, s.act, groups, st); break;
     case 129: e = launch_c64_BF16(a, s.k, s.act, groups, st); break;
