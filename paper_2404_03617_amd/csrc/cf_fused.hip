@@ -32,6 +32,7 @@
 // chunks and writes an fp32 partial of the projected output; a second kernel
 // adds the partials in group order plus b2 and the residual.
 #include "cf_block64.h"
+#include "cf_wide.h"
 #include "cf_fused_impl.h"
 
 #include <mutex>
@@ -117,6 +118,11 @@ hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Sha
         case 5: e = launch_block64_k5(x, y, w, s, st); break;
         default: e = launch_block64_k7(x, y, w, s, st); break;
         }
+        if (e != hipErrorInvalidConfiguration)
+            return e;
+    }
+    if ((s.C == 128 || s.C == 256) && !s.bf16 && groups <= 1) {
+        e = s.C == 128 ? launch_wide_c128(x, y, w, s, st) : launch_wide_c256(x, y, w, s, st);
         if (e != hipErrorInvalidConfiguration)
             return e;
     }

@@ -1,0 +1,611 @@
+// cf_wide.h -- fused ConvFirst block for C = 128 and C = 256 channels, fp16
+// I/O, on gfx950.  Instantiated per channel count in cf_wide_c*.hip.
+//
+// Block fusion (Sec. 5.3.1 / 5.5.1 of Lavin, arXiv:2404.03617) with one
+// persistent workgroup of 8 waves per CU.  A tile is 4 blocks of 32
+// consecutive pixels (N*H*W flattened); block b belongs to the wave pair
+// (b, b + 4), which shares a SIMD.  Each workgroup owns a contiguous range of
+// blocks.
+//
+//  * Depth-wise conv in slabs of 128 channels, channel-major: lane l handles
+//    channels 4*(l % 32) .. +3 of the slab with its taps held in registers;
+//    each half-wave walks 8 pixels.  A tap is one 8-byte LDS read of the halo
+//    (contiguous across the lanes) and two packed fp16 FMAs.  The result goes
+//    through a small LDS buffer and is read back as MFMA B fragments, so no
+//    weight is re-read per pixel.
+//  * FFN (eq. e:ffn-eff) in steps of two 32-hidden chunks on
+//    v_mfma_f32_32x32x16_f16 with swapped operands and the sigma/tau row
+//    orders of cf_fused_impl.h.  In step s wave r of a pair expands chunk
+//    2s + r (b1 through the C operand), applies phi on fp16 pairs and puts the
+//    result in LDS; after a barrier each wave projects its half of the output
+//    channels over both chunks.  The W1 fragments of a step and its W2
+//    fragments live in two LDS buffers, each refilled by asynchronous
+//    global->LDS copies while the other one is in use.  s1 scales the expand
+//    accumulators, s2 the output.
+//  * The halo region is reused for the weight buffers once the depth-wise conv
+//    of a tile is done.
+//  * Epilogue y = x + s2 Z + b2 with x read back from global memory (it was just
+//    read for the halo) -- the residual costs no extra HBM traffic.
+// The activation variable is scaled by 1/4 as in the other kernels.
+#pragma once
+#include "cf_fused_impl.h"
+
+namespace cf {
+namespace wide {
+
+using fused::FastDiv;
+using fused::fdiv;
+using fused::float16v;
+using fused::mfma32;
+using fused::sigma_row;
+using fused::tau_row;
+
+constexpr int NW = 8;               // waves; two per 32-pixel block
+constexpr int NBLK = 4;             // blocks per tile
+constexpr int NT = NW * 64;
+constexpr int CS = 128;              // channels per depth-wise slab
+constexpr int HPX = CS * 2;          // halo bytes per pixel (one slab)
+constexpr int DPX = CS * 2 + 16;     // D-buffer bytes per pixel (padded against bank conflicts)
+constexpr float QS = 0.25f;
+
+struct Args {
+    const uint16_t *x;
+    uint16_t *y;
+    const uint16_t *dw_w;
+    const float *s0, *b0;
+    const uint16_t *w1;
+    const float *s1, *b1;
+    const uint16_t *w2;
+    const float *s2, *b2;
+    int H, W, NH;
+    int nch;              // hidden chunks = E*C/32
+    uint32_t P;
+    FastDiv divW, divH;
+    int range_base, range_extra;
+    uint32_t rsl;         // halo row bytes: (W + 2*pad) * HPX
+    uint32_t off_b1, off_s2b2, off_s1, off_g, off_d, off_big, off_zero;
+};
+
+template <int C>
+struct Geo {
+    static constexpr int KST = C / 16;
+    static constexpr int CB = C / 32;
+    static constexpr int NSLAB = C / CS;
+    static constexpr int BUF_A = 2 * KST * 1024;   // W1 fragments of the two chunks of a step
+    static constexpr int BUF_B = 2 * 2 * CB * 1024; // W2 fragments of the two chunks of a step
+    static constexpr int PA = BUF_A / 16 / NT;      // 16-byte pieces per thread
+    static constexpr int PB = BUF_B / 16 / NT;
+};
+
+struct Layout {
+    uint32_t b1, s2b2, s1, g, d, big, zero, total;
+};
+
+// [b1/4 regs nch*128][4*s2 | b2  C*8][s1 regs nch*128][G 4 blocks x 2 chunks x 2 KB]
+// [overlay: halo + D buffer  |  W1 buffers A0 A1 + W2 buffers B0 B1][zero]
+template <int C>
+inline Layout layout_for(int nch, int k, int halo_rows, uint32_t rsl) {
+    Layout L;
+    L.b1 = 0;
+    L.s2b2 = L.b1 + (uint32_t)nch * 128;
+    L.s1 = L.s2b2 + (uint32_t)C * 8;
+    L.g = (L.s1 + (uint32_t)nch * 128 + 255) & ~255u;
+    L.big = L.g + NBLK * 2 * 2048;
+    const uint32_t halo = (uint32_t)halo_rows * rsl;
+    L.d = L.big + ((halo + 255) & ~255u);
+    const uint32_t hd = (L.d - L.big) + NBLK * 32 * DPX;
+    const uint32_t bufs = 2 * (Geo<C>::BUF_A + Geo<C>::BUF_B);
+    L.zero = L.big + (hd > bufs ? hd : bufs);
+    L.total = L.zero + (uint32_t)k * HPX + 64;
+    return L;
+}
+
+inline int halo_rows_for(int k, int W, int64_t NH) {
+    int64_t span = (int64_t)(32 * NBLK - 1) / W + 2;
+    if (span > NH)
+        span = NH;
+    return (int)span + 2 * (k / 2);
+}
+
+// Workgroup barrier that waits only for this wave's LDS traffic (lgkmcnt),
+// not for its outstanding global->LDS copies: those are waited for
+// explicitly, per buffer, with partial vmcnt waits.  The empty asm statements
+// keep the compiler from moving memory accesses across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // vmcnt 63, expcnt 7, lgkmcnt 0
+    __asm__ volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    __asm__ volatile("" ::: "memory");
+}
+
+__device__ __forceinline__ u32x4 ld16(const uint8_t *base, uint32_t off) {
+    return *reinterpret_cast<const u32x4 *>(base + off);
+}
+__device__ __forceinline__ half2v h2(uint32_t w) { return __builtin_bit_cast(half2v, w); }
+__device__ __forceinline__ uint32_t u32(half2v v) { return __builtin_bit_cast(uint32_t, v); }
+
+template <int C, int KS, int ACT>
+struct Kw {
+    typedef Geo<C> G;
+    static constexpr int KST = G::KST, CB = G::CB, NSLAB = G::NSLAB, PA = G::PA, PB = G::PB;
+    static constexpr int CBH = CB / 2;  // output blocks per wave of a pair
+    static constexpr int PAD = KS / 2;
+
+    template <int NP>
+    static __device__ __forceinline__ void activate(const float *a, uint32_t *out) {
+        half2v w[NP];
+#pragma unroll
+        for (int p = 0; p < NP; p++) {
+            w[p].x = (_Float16)a[2 * p];
+            w[p].y = (_Float16)a[2 * p + 1];
+        }
+        if constexpr (ACT == ACT_GELU) {
+            half2v s[NP], q[NP];
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                s[p] = w[p] * w[p];
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                q[p] = __builtin_elementwise_fma(s[p], splat2(GELU_Q4), splat2(GELU_Q3));
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                q[p] = __builtin_elementwise_fma(s[p], q[p], splat2(GELU_Q2));
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                q[p] = __builtin_elementwise_fma(s[p], q[p], splat2(GELU_Q1));
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                q[p] = __builtin_elementwise_fma(s[p], q[p], splat2(GELU_Q0));
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                q[p] = __builtin_elementwise_min(
+                    __builtin_elementwise_max(__builtin_elementwise_fma(w[p], q[p], splat2(0.5f)), splat2(0.0f)),
+                    splat2(1.0f));
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                out[p] = u32(w[p] * q[p]);
+        } else if constexpr (ACT == ACT_RELU) {
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                out[p] = u32(__builtin_elementwise_max(w[p], splat2(0.0f)));
+        } else {
+#pragma unroll
+            for (int p = 0; p < NP; p++)
+                out[p] = u32(w[p]);
+        }
+    }
+
+    // ---- per-kernel staging of the small vectors (register order).
+    // Expand register e = 4t + i of lane half h <-> hidden 16(t>>1) + 8h + 4(t&1) + i.
+    static __device__ void stage_vectors(const Args &a, uint8_t *smem, int tid) {
+        for (int p = tid; p < a.nch * 32; p += NT) {
+            const int ch = p >> 5, e = p & 31, hh = e >> 4, t = (e >> 2) & 3, i = e & 3;
+            const int r = ch * 32 + 16 * (t >> 1) + 8 * hh + 4 * (t & 1) + i;
+            reinterpret_cast<float *>(smem + a.off_b1)[p] = a.b1 ? a.b1[r] * QS : 0.0f;
+            reinterpret_cast<float *>(smem + a.off_s1)[p] = a.s1 ? a.s1[r] : 1.0f;
+        }
+        for (int c = tid; c < C; c += NT) {
+            reinterpret_cast<float *>(smem + a.off_s2b2)[c] = 4.0f * (a.s2 ? a.s2[c] : 1.0f);
+            reinterpret_cast<float *>(smem + a.off_s2b2 + 4 * C)[c] = a.b2 ? a.b2[c] : 0.0f;
+        }
+
+    }
+
+    // ---- weight buffers.  Buffer A of step s holds the W1 fragments (rows in
+    // sigma order) of chunks 2s and 2s + 1: fragment j*KST + ks; buffer B the
+    // W2 fragments (rows in tau order): fragment j*2*CB + 2*cb + kk.
+    // Asynchronous global->LDS copies of a step's weight fragments: one
+    // 16-byte-per-lane DMA instruction per 1 KB fragment; wave wv copies
+    // fragments wv, wv + NW, ...
+    // buffers: A0 A1 B0 B1; step s uses A_(s&1) and B_(s&1)
+    static constexpr int FA = (2 * KST + NW - 1) / NW;    // DMA instructions per wave for an A buffer
+    static constexpr int FB = (4 * CB + NW - 1) / NW;     // ... for a B buffer
+    static_assert(2 * KST % NW == 0 && 4 * CB % NW == 0, "uniform DMA count per wave");
+    static __device__ __forceinline__ uint8_t *buf_a(const Args &a, uint8_t *smem, int slot) {
+        return smem + a.off_big + slot * G::BUF_A;
+    }
+    static __device__ __forceinline__ uint8_t *buf_b(const Args &a, uint8_t *smem, int slot) {
+        return smem + a.off_big + 2 * G::BUF_A + slot * G::BUF_B;
+    }
+    static __device__ __forceinline__ void dma_a(const Args &a, uint8_t *smem, int step, int wv, int lane) {
+        uint8_t *buf = buf_a(a, smem, step & 1);
+        const uint16_t *w1 = a.w1 + (size_t)step * 64 * C;  // wave-uniform
+        const uint32_t lo = (uint32_t)(sigma_row(lane & 31) * C + 8 * (lane >> 5));
+#pragma unroll
+        for (int f = wv; f < 2 * KST; f += NW) {
+            const int j = f / KST, ks = f % KST;
+            fused::dma16(w1 + (lo + (uint32_t)(j * 32 * C + ks * 16)), buf + f * 1024);
+        }
+    }
+    static __device__ __forceinline__ void dma_b(const Args &a, uint8_t *smem, int step, int wv, int lane) {
+        uint8_t *buf = buf_b(a, smem, step & 1);
+        const uint16_t *w2 = a.w2 + (size_t)step * 64;  // wave-uniform
+        const uint32_t ec = (uint32_t)a.nch * 32;
+        const uint32_t lo = (uint32_t)tau_row(lane & 31) * ec + 8 * (lane >> 5);
+#pragma unroll
+        for (int f = wv; f < 4 * CB; f += NW) {
+            const int j = f / (2 * CB), g = f % (2 * CB), cb = g >> 1, kk = g & 1;
+            fused::dma16(w2 + (lo + (uint32_t)(cb * 32) * ec + (uint32_t)(j * 32 + 16 * kk)), buf + f * 1024);
+        }
+    }
+
+    // ---- halo slab copy (synchronous, through registers): rows of the tile's
+    // image rows g_lo - PAD .., channels slab*128 .. +127, pad columns zeroed.
+    static __device__ void copy_slab(const Args &a, uint8_t *smem, uint32_t g_lo, int rows, int slab, int tid) {
+        const int WP = a.W + 2 * PAD;
+        const int per_row = WP * 16;  // 16-byte chunks per halo row
+        const int total = rows * per_row;
+        const uint8_t *xb = reinterpret_cast<const uint8_t *>(a.x);
+        // batches of 8 chunks per thread: all loads of a batch are in flight
+        // before the first LDS write
+        for (int c0 = 0; c0 < total; c0 += 8 * NT) {
+            u32x4 v[8];
+            uint32_t dst[8];
+#pragma unroll
+            for (int u = 0; u < 8; u++) {
+                const int ci = c0 + u * NT + tid;
+                const int r = ci / per_row, rem = ci - r * per_row;
+                const int col = rem >> 4, q = rem & 15;
+                const int px = col - PAD;
+                const int grow = (int)g_lo - PAD + r;
+                dst[u] = ci < total ? a.off_big + (uint32_t)r * a.rsl + (uint32_t)col * HPX + q * 16 : 0xffffffffu;
+                v[u] = u32x4{0u, 0u, 0u, 0u};
+                if (ci < total && px >= 0 && px < a.W && grow >= 0 && grow < a.NH)
+                    v[u] = *reinterpret_cast<const u32x4 *>(xb + ((size_t)grow * a.W + px) * (C * 2) + slab * HPX +
+                                                            q * 16);
+            }
+#pragma unroll
+            for (int u = 0; u < 8; u++)
+                if (dst[u] != 0xffffffffu)
+                    *reinterpret_cast<u32x4 *>(smem + dst[u]) = v[u];
+        }
+    }
+
+    // ---- depth-wise conv of one slab, channel-major.  Wave r of block b's pair
+    // takes pixels 16r .. 16r + 15 of the block, half-wave hw 8 of them; lane
+    // channel group cq (4 channels).  Tap rows are the outer loop so only one
+    // row of taps is held in registers at a time.
+    static __device__ void dw_slab(const Args &a, uint8_t *smem, uint32_t g_lo, uint32_t pblk, int b, int r,
+                                   int slab, int lane) {
+        const int hw = lane >> 5, cq = lane & 31;
+        const int c0 = slab * CS + 4 * cq;
+        const int q0 = 16 * r + 8 * hw;  // first pixel of this half-wave within the block
+        uint32_t topleft[8];
+        int hh[8];
+        {
+            uint32_t p = pblk + q0;
+            uint32_t gg = fdiv(p < a.P ? p : 0u, a.divW);
+            int wc = (int)(p - gg * (uint32_t)a.W);
+            int hr = (int)(gg - fdiv(gg, a.divH) * (uint32_t)a.H);
+#pragma unroll
+            for (int i = 0; i < 8; i++, p++) {
+                topleft[i] = a.off_big + (gg - g_lo) * a.rsl + (uint32_t)wc * HPX + (uint32_t)cq * 8;
+                hh[i] = p < a.P ? hr : -KS - 1;  // invalid pixels read zeros only
+                if (++wc == a.W) {
+                    wc = 0;
+                    gg++;
+                    if (++hr == a.H)
+                        hr = 0;
+                }
+            }
+        }
+        half2v acc[8][2];
+#pragma unroll
+        for (int i = 0; i < 8; i++)
+            acc[i][0] = acc[i][1] = splat2(0.0f);
+        // one tap row per iteration
+        // (bounds the loads the scheduler can hoist)
+#pragma unroll 1
+        for (int ti = 0; ti < KS; ti++) {
+            u32x2 wt[KS];
+#pragma unroll
+            for (int tj = 0; tj < KS; tj++)
+                wt[tj] = *reinterpret_cast<const u32x2 *>(a.dw_w + (size_t)(ti * KS + tj) * C + c0);
+#pragma unroll
+            for (int i = 0; i < 8; i++) {
+                const int hr = hh[i] + ti - PAD;
+                const uint32_t rb = (hr >= 0 && hr < a.H) ? topleft[i] + (uint32_t)ti * a.rsl : a.off_zero;
+#pragma unroll
+                for (int tj = 0; tj < KS; tj++) {
+                    const u32x2 v = *reinterpret_cast<const u32x2 *>(smem + rb + (uint32_t)tj * HPX);
+                    acc[i][0] = __builtin_elementwise_fma(h2(v[0]), h2(wt[tj][0]), acc[i][0]);
+                    acc[i][1] = __builtin_elementwise_fma(h2(v[1]), h2(wt[tj][1]), acc[i][1]);
+                }
+            }
+        }
+        half2v s0q[2], b0q[2];
+#pragma unroll
+        for (int e = 0; e < 2; e++) {
+            const int c = c0 + 2 * e;
+            s0q[e] = half2v{(_Float16)((a.s0 ? a.s0[c] : 1.0f) * QS), (_Float16)((a.s0 ? a.s0[c + 1] : 1.0f) * QS)};
+            b0q[e] = half2v{(_Float16)((a.b0 ? a.b0[c] : 0.0f) * QS), (_Float16)((a.b0 ? a.b0[c + 1] : 0.0f) * QS)};
+        }
+        const uint32_t dbase = a.off_d + (uint32_t)(32 * b + q0) * DPX + (uint32_t)(4 * cq) * 2;
+#pragma unroll
+        for (int i = 0; i < 8; i++) {
+            u32x2 d;
+            d[0] = u32(__builtin_elementwise_fma(acc[i][0], s0q[0], b0q[0]));
+            d[1] = u32(__builtin_elementwise_fma(acc[i][1], s0q[1], b0q[1]));
+            *reinterpret_cast<u32x2 *>(smem + dbase + (uint32_t)i * DPX) = d;
+        }
+    }
+
+    // ---- FFN for block b of the tile by wave r of its pair; dfr = D as B
+    // fragments, acc = this wave's half of the output channels.
+    static __device__ void ffn(const Args &a, uint8_t *smem, int tid, int lane, int b, int r,
+                               const u32x4 (&dfr)[KST], float16v (&acc)[CBH]) {
+        const int h = lane >> 5;
+        const int nsteps = a.nch / 2;
+        const int wv = tid >> 6;
+        uint8_t *gmine = smem + a.off_g + (uint32_t)(b * 2 + r) * 2048;
+        // prologue: A0 B0 A1 B1 in flight; A0 and B0 must land
+        dma_a(a, smem, 0, wv, lane);
+        dma_b(a, smem, 0, wv, lane);
+        if (nsteps > 1) {
+            dma_a(a, smem, 1, wv, lane);
+            dma_b(a, smem, 1, wv, lane);
+            fused::wait_vmcnt<FA + FB>();
+        } else {
+            fused::wait_vmcnt<0>();
+        }
+        lds_barrier();
+#pragma unroll 1
+        for (int s = 0; s < nsteps; s++) {
+            uint8_t *bufa = buf_a(a, smem, s & 1);
+            uint8_t *bufb = buf_b(a, smem, s & 1);
+            // ---- expand chunk 2s + r: U/4 = s1 * (W1 D/4) + b1/4, phi, hidden tile to LDS
+            const int ch = 2 * s + r;
+            const uint8_t *wa = bufa + (uint32_t)(r * KST * 1024 + lane * 16);
+            // fragments stream through a 4-deep register window; the
+            // scheduling groups keep 4 LDS reads in flight ahead of the MFMAs
+            float16v hh;
+#pragma unroll
+            for (int e = 0; e < 16; e++)
+                hh[e] = 0.0f;
+            u32x4 wf[4];
+#pragma unroll
+            for (int i = 0; i < 4; i++)
+                wf[i] = ld16(wa, i * 1024);
+#pragma unroll
+            for (int ks = 0; ks < KST; ks++) {
+                hh = mfma32(wf[ks & 3], dfr[ks], hh, F16{});
+                if (ks + 4 < KST)
+                    wf[ks & 3] = ld16(wa, (ks + 4) * 1024);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);
+#pragma unroll
+            for (int ks = 0; ks + 4 < KST; ks++) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);
+            const float16v s1v = *reinterpret_cast<const float16v *>(smem + a.off_s1 + ch * 128 + h * 64);
+            const float16v b1v = *reinterpret_cast<const float16v *>(smem + a.off_b1 + ch * 128 + h * 64);
+            float v[16];
+#pragma unroll
+            for (int e = 0; e < 16; e++)
+                v[e] = fmaf(hh[e], s1v[e], b1v[e]);
+            uint32_t o[8];
+            activate<8>(v, o);
+            *reinterpret_cast<u32x4 *>(gmine + lane * 32) = u32x4{o[0], o[1], o[2], o[3]};
+            *reinterpret_cast<u32x4 *>(gmine + lane * 32 + 16) = u32x4{o[4], o[5], o[6], o[7]};
+            // B_(s+1) goes into the slot B_(s-1) used (free since the last barrier)
+            if (s >= 1 && s + 1 < nsteps)
+                dma_b(a, smem, s + 1, wv, lane);
+            // B_s landed (issued after it: A_(s+1), B_(s+1) when they exist)
+            if (s + 1 < nsteps)
+                fused::wait_vmcnt<FA + FB>();
+            else
+                fused::wait_vmcnt<0>();
+            lds_barrier();  // hidden tiles and B_s visible; A_s free
+            // ---- project both chunks onto this wave's output half
+            {
+                constexpr int NF = 4 * CBH;  // W2 fragments used by this wave per step
+                u32x4 hid[2][2];
+#pragma unroll
+                for (int j = 0; j < 2; j++) {
+                    const uint8_t *gp = smem + a.off_g + (uint32_t)(b * 2 + j) * 2048 + lane * 32;
+                    hid[j][0] = ld16(gp, 0);
+                    hid[j][1] = ld16(gp, 16);
+                }
+                // MFMA i: chunk j = i / (2*CBH), K step kk = (i / CBH) % 2, output block
+                // c = i % CBH -- consecutive MFMAs feed different accumulators
+                auto frag = [&](int i) {
+                    const int j = i / (2 * CBH), kk = (i / CBH) & 1, c = i % CBH;
+                    return ld16(bufb, (uint32_t)((j * 2 * CB + 2 * (CBH * r + c) + kk) * 1024 + lane * 16));
+                };
+                u32x4 wf[4];
+#pragma unroll
+                for (int i = 0; i < 4; i++)
+                    wf[i] = frag(i);
+#pragma unroll
+                for (int i = 0; i < NF; i++) {
+                    const int j = i / (2 * CBH), kk = (i / CBH) & 1, c = i % CBH;
+                    acc[c] = mfma32(wf[i & 3], hid[j][kk], acc[c], F16{});
+                    if (i + 4 < NF)
+                        wf[i & 3] = frag(i + 4);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x100, 8, 2);
+#pragma unroll
+                for (int i = 0; i + 4 < NF; i++) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 2);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x008, 4, 2);
+            }
+            // copies are issued after the MFMAs of a phase so that a full
+            // copy queue does not hold up the matrix instructions
+            if (s + 2 < nsteps)
+                dma_a(a, smem, s + 2, wv, lane);
+            // A_(s+1) landed (issued after it: B_(s+1), and A_(s+2) when it exists)
+            if (s + 2 < nsteps)
+                fused::wait_vmcnt<FB + FA>();
+            else if (s + 1 < nsteps)
+                fused::wait_vmcnt<FB>();
+            lds_barrier();  // B_s and the hidden tiles are free; A_(s+1) visible
+        }
+        __syncthreads();  // the weight buffers (halo region) are free for the next tile
+    }
+
+    static __device__ void run(const Args &a, uint8_t *smem) {
+        const int tid = threadIdx.x;
+        const int lane = tid & 63, wv = tid >> 6;
+        const int h = lane >> 5, m = lane & 31;
+
+        const int Gn = gridDim.x;
+        const int g = (Gn % 8 == 0) ? (blockIdx.x % 8) * (Gn / 8) + blockIdx.x / 8 : blockIdx.x;
+        const int lo = g * a.range_base + (g < a.range_extra ? g : a.range_extra);
+        const int hi = lo + a.range_base + (g < a.range_extra ? 1 : 0);
+
+        for (uint32_t i = a.off_zero / 16 + tid; i < (a.off_zero + KS * HPX + 64) / 16; i += NT)
+            reinterpret_cast<u32x4 *>(smem)[i] = u32x4{0u, 0u, 0u, 0u};
+        stage_vectors(a, smem, tid);
+
+        const int b = wv & (NBLK - 1), r = wv >> 2;  // block of the tile, role in its pair
+        for (int t0 = lo; t0 < hi; t0 += NBLK) {
+            const int nblk = hi - t0 < NBLK ? hi - t0 : NBLK;
+            const uint32_t p0 = (uint32_t)t0 * 32;
+            uint32_t pend = p0 + (uint32_t)nblk * 32;
+            if (pend > a.P)
+                pend = a.P;
+            const uint32_t g_lo = fdiv(p0, a.divW);
+            const int rows = (int)(fdiv(pend - 1, a.divW) - g_lo) + 1 + 2 * PAD;
+            const bool mine = b < nblk;
+            const uint32_t pblk = p0 + 32u * b;
+
+            u32x4 dfr[KST];
+#pragma unroll
+            for (int slab = 0; slab < NSLAB; slab++) {
+                __syncthreads();  // halo / D buffers free
+                copy_slab(a, smem, g_lo, rows, slab, tid);
+                __syncthreads();
+                if (mine)
+                    dw_slab(a, smem, g_lo, pblk, b, r, slab, lane);
+                __syncthreads();
+#pragma unroll
+                for (int k8 = 0; k8 < CS / 16; k8++)
+                    dfr[slab * (CS / 16) + k8] =
+                        ld16(smem, a.off_d + (uint32_t)(32 * b + m) * DPX + (uint32_t)(k8 * 16 + 8 * h) * 2);
+            }
+            __syncthreads();  // D and halo reads done before the weight buffers overwrite them
+
+            float16v acc[CBH];
+#pragma unroll
+            for (int c = 0; c < CBH; c++)
+#pragma unroll
+                for (int e = 0; e < 16; e++)
+                    acc[c][e] = 0.0f;
+            ffn(a, smem, tid, lane, b, r, dfr, acc);
+
+            // epilogue: y = x + 4 * acc + b2 on this wave's output half
+            const uint32_t pix = pblk + m;
+            if (mine && pix < a.P) {
+#pragma unroll
+                for (int c = 0; c < CBH; c++) {
+                    const int cc = (r * CBH + c) * 32 + 16 * h;
+                    const float16v sv = *reinterpret_cast<const float16v *>(smem + a.off_s2b2 + cc * 4);
+                    const float16v bv = *reinterpret_cast<const float16v *>(smem + a.off_s2b2 + 4 * C + cc * 4);
+                    const u32x4 *xs = reinterpret_cast<const u32x4 *>(a.x + (size_t)pix * C + cc);
+                    Pack8 x0, x1;
+                    x0.u = xs[0];
+                    x1.u = xs[1];
+                    u32x4 o0, o1;
+#pragma unroll
+                    for (int q = 0; q < 4; q++) {
+                        o0[q] = F16::pack2(fmaf(acc[c][2 * q], sv[2 * q], F16::lo(x0.w[q]) + bv[2 * q]),
+                                           fmaf(acc[c][2 * q + 1], sv[2 * q + 1], F16::hi(x0.w[q]) + bv[2 * q + 1]));
+                        o1[q] = F16::pack2(fmaf(acc[c][8 + 2 * q], sv[8 + 2 * q], F16::lo(x1.w[q]) + bv[8 + 2 * q]),
+                                           fmaf(acc[c][8 + 2 * q + 1], sv[8 + 2 * q + 1], F16::hi(x1.w[q]) + bv[8 + 2 * q + 1]));
+                    }
+                    u32x4 *dst = reinterpret_cast<u32x4 *>(a.y + (size_t)pix * C + cc);
+                    dst[0] = o0;
+                    dst[1] = o1;
+                }
+            }
+        }
+    }
+};
+
+template <int C, int KS, int ACT>
+__global__ __launch_bounds__(NT, 1) void wide_kernel(Args a) {
+    extern __shared__ __attribute__((aligned(256))) uint8_t smem[];
+    Kw<C, KS, ACT>::run(a, smem);
+}
+
+template <int C, int KS>
+hipError_t launch_ck(const void *x, void *y, const BlockW &w, const Shape &s, hipStream_t st) {
+    const int pad = KS / 2;
+    const int64_t NH = (int64_t)s.N * s.H;
+    const int halo_rows = halo_rows_for(KS, s.W, NH);
+    const uint32_t rsl = (uint32_t)(s.W + 2 * pad) * HPX;
+    const int nch = s.E * C / 32;
+    const Layout L = layout_for<C>(nch, KS, halo_rows, rsl);
+    if (L.total > 160 * 1024)
+        return hipErrorInvalidConfiguration;
+    Args a{};
+    a.x = (const uint16_t *)x;
+    a.y = (uint16_t *)y;
+    a.dw_w = (const uint16_t *)w.dw_w;
+    a.s0 = w.s0;
+    a.b0 = w.b0;
+    a.w1 = (const uint16_t *)w.w1;
+    a.s1 = w.s1;
+    a.b1 = w.b1;
+    a.w2 = (const uint16_t *)w.w2;
+    a.s2 = w.s2;
+    a.b2 = w.b2;
+    a.H = s.H;
+    a.W = s.W;
+    a.NH = s.N * s.H;
+    a.nch = nch;
+    const int64_t P = (int64_t)s.N * s.H * s.W;
+    a.P = (uint32_t)P;
+    a.divW = fused::make_fastdiv((uint32_t)s.W);
+    a.divH = fused::make_fastdiv((uint32_t)s.H);
+    const int nblocks = (int)((P + 31) / 32);
+    int Gn = device_cu_count();
+    if (Gn > nblocks)
+        Gn = nblocks;
+    a.range_base = nblocks / Gn;
+    a.range_extra = nblocks % Gn;
+    a.rsl = rsl;
+    a.off_b1 = L.b1;
+    a.off_g = L.g;
+    a.off_s1 = L.s1;
+    a.off_s2b2 = L.s2b2;
+    a.off_d = L.d;
+    a.off_big = L.big;
+    a.off_zero = L.zero;
+    hipError_t e;
+#define CF_WIDE_LAUNCH(ACTV)                                                                                         \
+    {                                                                                                                 \
+        auto kf = wide_kernel<C, KS, ACTV>;                                                                          \
+        if ((e = hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L.total))) \
+            return e;                                                                                                 \
+        hipLaunchKernelGGL(kf, dim3(Gn), dim3(NT), L.total, st, a);                                                  \
+    }
+    switch (s.act) {
+    case ACT_GELU: CF_WIDE_LAUNCH(ACT_GELU) break;
+    case ACT_RELU: CF_WIDE_LAUNCH(ACT_RELU) break;
+    default: CF_WIDE_LAUNCH(ACT_NONE) break;
+    }
+#undef CF_WIDE_LAUNCH
+    return hipGetLastError();
+}
+
+template <int C>
+hipError_t launch_c(const void *x, void *y, const BlockW &w, const Shape &s, hipStream_t st) {
+    switch (s.k) {
+    case 1: return launch_ck<C, 1>(x, y, w, s, st);
+    case 3: return launch_ck<C, 3>(x, y, w, s, st);
+    case 5: return launch_ck<C, 5>(x, y, w, s, st);
+    default: return launch_ck<C, 7>(x, y, w, s, st);
+    }
+}
+
+}  // namespace wide
+
+hipError_t launch_wide_c128(const void *x, void *y, const BlockW &w, const Shape &s, hipStream_t st);
+hipError_t launch_wide_c256(const void *x, void *y, const BlockW &w, const Shape &s, hipStream_t st);
+
+}  // namespace cf
