@@ -95,7 +95,11 @@ cf_status cf_block_forward(const void *x, void *y, const cf_block_params *p,
 /* `depth` consecutive blocks of the same shape (a network stage, the unit the
  * paper benchmarks, Sec. 5.5.3).  Intermediate activations ping-pong between
  * y and ws; blocks[depth] are host-side structs of device pointers.
- * ws needs cf_stage_workspace_bytes() bytes (0 for depth == 1). */
+ * cf_stage_workspace_bytes() returns the recommended ws size.  The minimum is
+ * N*H*W*C*2 bytes (rounded up to 256) for depth > 1 and 0 for depth == 1;
+ * for C = 512 fp16 the recommended size adds room for fp32 partial outputs,
+ * and with it each block splits its hidden layer over several workgroups
+ * (results identical up to fp32 summation order, still deterministic). */
 cf_status cf_stage_forward(const void *x, void *y, void *ws, size_t ws_bytes,
                            const cf_block_params *blocks, int depth,
                            int N, int H, int W, int C, int E, int k,

@@ -159,10 +159,35 @@ cf_status cf_block_forward(const void *x, void *y, const cf_block_params *p, int
     return CF_OK;
 }
 
-size_t cf_stage_workspace_bytes(int depth, int N, int H, int W, int C, cf_dtype dt) {
+// Minimum stage workspace: the ping-pong buffer (depth > 1).
+size_t stage_ws_min(int depth, int N, int H, int W, int C, cf_dtype dt) {
     if (depth <= 1 || N <= 0 || H <= 0 || W <= 0 || C <= 0)
         return 0;
-    return (size_t)N * H * W * C * elem_bytes(dt);
+    return round256((size_t)N * H * W * C * elem_bytes(dt));
+}
+
+// Hidden-layer groups a C = 512 fp16 stage uses when the workspace allows it:
+// enough (tile, group) pairs to fill the chip, at most STAGE_GROUPS.
+constexpr int STAGE_GROUPS = 4;
+int stage_groups(int N, int H, int W, int C, int E, cf_dtype dt) {
+    if (C != 512 || dt != CF_F16)
+        return 1;
+    const int64_t tiles = ((int64_t)N * H * W + 127) / 128;
+    const int chunks = E * C / 32;
+    const int cus = cf::device_cu_count();
+    int g = 1;
+    while (g * 2 <= STAGE_GROUPS && chunks % (g * 2) == 0 && tiles * g * 2 <= cus + cus / 4)
+        g *= 2;
+    return g;
+}
+
+size_t cf_stage_workspace_bytes(int depth, int N, int H, int W, int C, cf_dtype dt) {
+    if (N <= 0 || H <= 0 || W <= 0 || C <= 0)
+        return 0;
+    size_t b = stage_ws_min(depth, N, H, W, C, dt);
+    if (C == 512 && dt == CF_F16)
+        b += (size_t)STAGE_GROUPS * N * H * W * C * sizeof(float);
+    return b;
 }
 
 cf_status cf_stage_forward(const void *x, void *y, void *ws, size_t ws_bytes, const cf_block_params *blocks,
@@ -175,7 +200,7 @@ cf_status cf_stage_forward(const void *x, void *y, void *ws, size_t ws_bytes, co
         if (st != CF_OK)
             return st;
     }
-    const size_t need = cf_stage_workspace_bytes(depth, N, H, W, C, dt);
+    const size_t need = stage_ws_min(depth, N, H, W, C, dt);
     const size_t bytes = (size_t)N * H * W * C * elem_bytes(dt);
     if (need) {
         if (!ws)
@@ -191,11 +216,22 @@ cf_status cf_stage_forward(const void *x, void *y, void *ws, size_t ws_bytes, co
     cf_status st = check_fit("cf_stage_forward", s);
     if (st != CF_OK)
         return st;
+    // hidden-layer split with fp32 partials after the ping-pong buffer, when
+    // the workspace holds them
+    int groups = 1;
+    float *partial = nullptr;
+    const int g = stage_groups(N, H, W, C, E, dt);
+    const size_t pbytes = (size_t)g * N * H * W * C * sizeof(float);
+    if (g > 1 && ws && aligned16(ws) && ws_bytes >= need + pbytes &&
+        !overlap((char *)ws + need, pbytes, x, bytes) && !overlap((char *)ws + need, pbytes, y, bytes)) {
+        groups = g;
+        partial = (float *)((char *)ws + need);
+    }
     // block i writes y when (depth-1-i) is even, else ws, so the last one lands in y
     const void *in = x;
     for (int i = 0; i < depth; i++) {
         void *out = ((depth - 1 - i) % 2 == 0) ? y : ws;
-        hipError_t e = cf::launch_fused_block(in, out, to_w(&blocks[i]), s, 1, nullptr, (hipStream_t)stream);
+        hipError_t e = cf::launch_fused_block(in, out, to_w(&blocks[i]), s, groups, partial, (hipStream_t)stream);
         if (e != hipSuccess)
             return hip_fail(e, "cf_stage_forward");
         in = out;

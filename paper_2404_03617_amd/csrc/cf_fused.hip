@@ -126,6 +126,16 @@ hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Sha
         if (e != hipErrorInvalidConfiguration)
             return e;
     }
+    bool done = false;
+    if (s.C == 512 && !s.bf16) {
+        e = launch_wide_c512(x, y, w, s, groups, partial, st);
+        if (e != hipErrorInvalidConfiguration) {
+            if (e != hipSuccess)
+                return e;
+            done = true;
+        }
+    }
+    if (!done) {
     switch (s.C * 2 + s.bf16) {
     case 128: e = launch_c64_F16(a, s.k, s.act, groups, st); break;
     case 129: e = launch_c64_BF16(a, s.k, s.act, groups, st); break;
@@ -136,6 +146,7 @@ hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Sha
     case 1024: e = launch_c512_F16(a, s.k, s.act, groups, st); break;
     case 1025: e = launch_c512_BF16(a, s.k, s.act, groups, st); break;
     default: return hipErrorInvalidValue;
+    }
     }
     if (e != hipSuccess || groups <= 1)
         return e;

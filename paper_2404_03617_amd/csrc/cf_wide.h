@@ -177,14 +177,17 @@ struct Kw {
 
     // ---- per-kernel staging of the small vectors (register order).
     // Expand register e = 4t + i of lane half h <-> hidden 16(t>>1) + 8h + 4(t&1) + i.
-    static __device__ void stage_vectors(const Args &a, uint8_t *smem, int tid) {
-        for (int p = tid; p < a.nch * 32; p += NT) {
-            const int ch = p >> 5, e = p & 31, hh = e >> 4, t = (e >> 2) & 3, i = e & 3;
+    template <int NTV = NT>
+    static __device__ void stage_vectors(const Args &a, uint8_t *smem, int tid, int ch0 = 0, int nchv = -1) {
+        if (nchv < 0)
+            nchv = a.nch;
+        for (int p = tid; p < nchv * 32; p += NTV) {
+            const int ch = ch0 + (p >> 5), e = p & 31, hh = e >> 4, t = (e >> 2) & 3, i = e & 3;
             const int r = ch * 32 + 16 * (t >> 1) + 8 * hh + 4 * (t & 1) + i;
             reinterpret_cast<float *>(smem + a.off_b1)[p] = a.b1 ? a.b1[r] * QS : 0.0f;
             reinterpret_cast<float *>(smem + a.off_s1)[p] = a.s1 ? a.s1[r] : 1.0f;
         }
-        for (int c = tid; c < C; c += NT) {
+        for (int c = tid; c < C; c += NTV) {
             reinterpret_cast<float *>(smem + a.off_s2b2)[c] = 4.0f * (a.s2 ? a.s2[c] : 1.0f);
             reinterpret_cast<float *>(smem + a.off_s2b2 + 4 * C)[c] = a.b2 ? a.b2[c] : 0.0f;
         }
@@ -231,6 +234,7 @@ struct Kw {
 
     // ---- halo slab copy (synchronous, through registers): rows of the tile's
     // image rows g_lo - PAD .., channels slab*128 .. +127, pad columns zeroed.
+    template <int NTV = NT>
     static __device__ void copy_slab(const Args &a, uint8_t *smem, uint32_t g_lo, int rows, int slab, int tid) {
         const int WP = a.W + 2 * PAD;
         const int per_row = WP * 16;  // 16-byte chunks per halo row
@@ -238,12 +242,12 @@ struct Kw {
         const uint8_t *xb = reinterpret_cast<const uint8_t *>(a.x);
         // batches of 8 chunks per thread: all loads of a batch are in flight
         // before the first LDS write
-        for (int c0 = 0; c0 < total; c0 += 8 * NT) {
+        for (int c0 = 0; c0 < total; c0 += 8 * NTV) {
             u32x4 v[8];
             uint32_t dst[8];
 #pragma unroll
             for (int u = 0; u < 8; u++) {
-                const int ci = c0 + u * NT + tid;
+                const int ci = c0 + u * NTV + tid;
                 const int r = ci / per_row, rem = ci - r * per_row;
                 const int col = rem >> 4, q = rem & 15;
                 const int px = col - PAD;
@@ -526,6 +530,198 @@ struct Kw {
     }
 };
 
+// ---------------------------------------------------------------------------
+// C = 512: one wave per 32-pixel block (4 waves, one per SIMD, 512 registers
+// each: the 512-channel accumulators of a block alone take 256).  The FFN
+// walks the hidden chunks of its group one at a time; W1 and W2 fragments of
+// a chunk (64 KB) stream through a two-slot LDS ring by asynchronous copies
+// issued one chunk ahead.  With grid.y > 1 the hidden chunks are split over
+// workgroups: each writes 4 s2 W2 phi(U) of its chunks as an fp32 partial and
+// a second kernel adds the partials in group order, b2 and x.
+struct SoloArgs {
+    Args a;
+    float *partial;  // [groups][P][C] fp32, or nullptr (one group: write y)
+    int chunks_per_group;
+    int ntiles;
+};
+
+template <int KS, int ACT>
+struct Ks {
+    static constexpr int C = 512;
+    static constexpr int NWS = 4, NTS = NWS * 64;
+    typedef Kw<C, KS, ACT> K;
+    static constexpr int KST = C / 16, CB = C / 32, NSLAB = C / CS;
+    static constexpr int SLOT = (KST + 2 * CB) * 1024;  // one chunk: W1 then W2 fragments
+    static constexpr int FPW = (KST + 2 * CB) / NWS;     // DMA instructions per wave per chunk
+
+    static __device__ __forceinline__ void dma_chunk(const Args &a, uint8_t *smem, int ch, int slot, int wv,
+                                                     int lane) {
+        uint8_t *buf = smem + a.off_big + slot * SLOT;
+        const uint16_t *w1 = a.w1 + (size_t)ch * 32 * C;
+        const uint16_t *w2 = a.w2 + (size_t)ch * 32;
+        const uint32_t ec = (uint32_t)a.nch * 32;
+        const uint32_t lo1 = (uint32_t)(sigma_row(lane & 31) * C + 8 * (lane >> 5));
+        const uint32_t lo2 = (uint32_t)tau_row(lane & 31) * ec + 8 * (lane >> 5);
+#pragma unroll
+        for (int f = wv; f < KST + 2 * CB; f += NWS) {
+            if (f < KST) {
+                fused::dma16(w1 + (lo1 + (uint32_t)(f * 16)), buf + f * 1024);
+            } else {
+                const int g = f - KST, cb = g >> 1, kk = g & 1;
+                fused::dma16(w2 + (lo2 + (uint32_t)(cb * 32) * ec + (uint32_t)(16 * kk)), buf + f * 1024);
+            }
+        }
+    }
+
+    static __device__ void run(const SoloArgs &sa, uint8_t *smem) {
+        const Args &a = sa.a;
+        const int tid = threadIdx.x;
+        const int lane = tid & 63, wv = tid >> 6;
+        const int h = lane >> 5, m = lane & 31;
+        const int grp = blockIdx.y;
+        const int ch0 = grp * sa.chunks_per_group, nchg = sa.chunks_per_group;
+
+        for (uint32_t i = a.off_zero / 16 + tid; i < (a.off_zero + KS * HPX + 64) / 16; i += NTS)
+            reinterpret_cast<u32x4 *>(smem)[i] = u32x4{0u, 0u, 0u, 0u};
+        K::template stage_vectors<NTS>(a, smem, tid, ch0, nchg);
+
+        for (int tile = blockIdx.x; tile < sa.ntiles; tile += gridDim.x) {
+            const uint32_t p0 = (uint32_t)tile * 128;
+            uint32_t pend = p0 + 128;
+            if (pend > a.P)
+                pend = a.P;
+            const uint32_t g_lo = fdiv(p0, a.divW);
+            const int rows = (int)(fdiv(pend - 1, a.divW) - g_lo) + 1 + 2 * K::PAD;
+            const uint32_t pblk = p0 + 32u * wv;
+            const bool mine = pblk < a.P;
+
+            u32x4 dfr[KST];
+#pragma unroll
+            for (int slab = 0; slab < NSLAB; slab++) {
+                __syncthreads();
+                K::template copy_slab<NTS>(a, smem, g_lo, rows, slab, tid);
+                __syncthreads();
+                if (mine) {
+                    K::dw_slab(a, smem, g_lo, pblk, wv, 0, slab, lane);
+                    K::dw_slab(a, smem, g_lo, pblk, wv, 1, slab, lane);
+                }
+                __syncthreads();
+#pragma unroll
+                for (int k8 = 0; k8 < CS / 16; k8++)
+                    dfr[slab * (CS / 16) + k8] =
+                        ld16(smem, a.off_d + (uint32_t)(32 * wv + m) * DPX + (uint32_t)(k8 * 16 + 8 * h) * 2);
+            }
+            __syncthreads();  // D and halo reads done before the ring overwrites them
+
+            float16v acc[CB];
+#pragma unroll
+            for (int c = 0; c < CB; c++)
+#pragma unroll
+                for (int e = 0; e < 16; e++)
+                    acc[c][e] = 0.0f;
+
+            dma_chunk(a, smem, ch0, 0, wv, lane);
+#pragma unroll 1
+            for (int c = 0; c < nchg; c++) {
+                fused::wait_vmcnt<0>();  // this wave's copies of chunk c have landed
+                lds_barrier();           // everyone's have; the other slot is free
+                if (c + 1 < nchg)
+                    dma_chunk(a, smem, ch0 + c + 1, (c + 1) & 1, wv, lane);
+                const uint8_t *slot = smem + a.off_big + (c & 1) * SLOT + lane * 16;
+                // expand (4-deep fragment window)
+                float16v hh;
+#pragma unroll
+                for (int e = 0; e < 16; e++)
+                    hh[e] = 0.0f;
+                u32x4 wf[4];
+#pragma unroll
+                for (int i = 0; i < 4; i++)
+                    wf[i] = ld16(slot, i * 1024);
+#pragma unroll
+                for (int ks = 0; ks < KST; ks++) {
+                    hh = mfma32(wf[ks & 3], dfr[ks], hh, F16{});
+                    if (ks + 4 < KST)
+                        wf[ks & 3] = ld16(slot, (ks + 4) * 1024);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);
+#pragma unroll
+                for (int ks = 0; ks + 4 < KST; ks++) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);
+                const float16v s1v = *reinterpret_cast<const float16v *>(smem + a.off_s1 + c * 128 + h * 64);
+                const float16v b1v = *reinterpret_cast<const float16v *>(smem + a.off_b1 + c * 128 + h * 64);
+                float v[16];
+#pragma unroll
+                for (int e = 0; e < 16; e++)
+                    v[e] = fmaf(hh[e], s1v[e], b1v[e]);
+                uint32_t o[8];
+                K::template activate<8>(v, o);
+                const u32x4 hid[2] = {u32x4{o[0], o[1], o[2], o[3]}, u32x4{o[4], o[5], o[6], o[7]}};
+                // project: MFMA i -> K step kk = i / CB, output block i % CB
+#pragma unroll
+                for (int i = 0; i < 4; i++)
+                    wf[i] = ld16(slot, (KST + 2 * (i % CB) + i / CB) * 1024);
+#pragma unroll
+                for (int i = 0; i < 2 * CB; i++) {
+                    acc[i % CB] = mfma32(wf[i & 3], hid[i / CB], acc[i % CB], F16{});
+                    if (i + 4 < 2 * CB)
+                        wf[i & 3] = ld16(slot, (KST + 2 * ((i + 4) % CB) + (i + 4) / CB) * 1024);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x100, 4, 2);
+#pragma unroll
+                for (int i = 0; i + 4 < 2 * CB; i++) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 2);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x008, 4, 2);
+            }
+            __syncthreads();  // the ring is free for the next tile
+
+            const uint32_t pix = pblk + m;
+            if (mine && pix < a.P) {
+#pragma unroll
+                for (int cb = 0; cb < CB; cb++) {
+                    const int cc = cb * 32 + 16 * h;
+                    const float16v sv = *reinterpret_cast<const float16v *>(smem + a.off_s2b2 + cc * 4);
+                    if (sa.partial) {
+                        float4v *dst = reinterpret_cast<float4v *>(sa.partial + ((size_t)grp * a.P + pix) * C + cc);
+#pragma unroll
+                        for (int q = 0; q < 4; q++)
+                            dst[q] = float4v{acc[cb][4 * q] * sv[4 * q], acc[cb][4 * q + 1] * sv[4 * q + 1],
+                                             acc[cb][4 * q + 2] * sv[4 * q + 2], acc[cb][4 * q + 3] * sv[4 * q + 3]};
+                    } else {
+                        const float16v bv = *reinterpret_cast<const float16v *>(smem + a.off_s2b2 + 4 * C + cc * 4);
+                        const u32x4 *xs = reinterpret_cast<const u32x4 *>(a.x + (size_t)pix * C + cc);
+                        Pack8 x0, x1;
+                        x0.u = xs[0];
+                        x1.u = xs[1];
+                        u32x4 o0, o1;
+#pragma unroll
+                        for (int q = 0; q < 4; q++) {
+                            o0[q] = F16::pack2(fmaf(acc[cb][2 * q], sv[2 * q], F16::lo(x0.w[q]) + bv[2 * q]),
+                                               fmaf(acc[cb][2 * q + 1], sv[2 * q + 1], F16::hi(x0.w[q]) + bv[2 * q + 1]));
+                            o1[q] = F16::pack2(
+                                fmaf(acc[cb][8 + 2 * q], sv[8 + 2 * q], F16::lo(x1.w[q]) + bv[8 + 2 * q]),
+                                fmaf(acc[cb][8 + 2 * q + 1], sv[8 + 2 * q + 1], F16::hi(x1.w[q]) + bv[8 + 2 * q + 1]));
+                        }
+                        u32x4 *dst = reinterpret_cast<u32x4 *>(a.y + (size_t)pix * C + cc);
+                        dst[0] = o0;
+                        dst[1] = o1;
+                    }
+                }
+            }
+        }
+    }
+};
+
+template <int KS, int ACT>
+__global__ __launch_bounds__(256, 1) void solo_kernel(SoloArgs sa) {
+    extern __shared__ __attribute__((aligned(256))) uint8_t smem[];
+    Ks<KS, ACT>::run(sa, smem);
+}
+
 template <int C, int KS, int ACT>
 __global__ __launch_bounds__(NT, 1) void wide_kernel(Args a) {
     extern __shared__ __attribute__((aligned(256))) uint8_t smem[];
@@ -603,9 +799,102 @@ hipError_t launch_c(const void *x, void *y, const BlockW &w, const Shape &s, hip
     }
 }
 
+// C = 512 launcher.  groups > 1 requires `partial` ([groups][P][C] fp32); the
+// caller then runs the ordered reduction.
+template <int KS>
+hipError_t launch_solo(const void *x, void *y, const BlockW &w, const Shape &s, int groups, float *partial,
+                       hipStream_t st) {
+    constexpr int C = 512;
+    const int pad = KS / 2;
+    const int nch = s.E * C / 32;
+    if (groups < 1 || nch % groups)
+        return hipErrorInvalidValue;
+    const int nchg = nch / groups;
+    const int64_t NH = (int64_t)s.N * s.H;
+    const int halo_rows = halo_rows_for(KS, s.W, NH);
+    const uint32_t rsl = (uint32_t)(s.W + 2 * pad) * HPX;
+    // [b1 regs][s1 regs][4 s2 | b2][overlay: halo + D | ring of two chunks][zero]
+    Layout L;
+    L.b1 = 0;
+    L.s1 = (uint32_t)nchg * 128;
+    L.s2b2 = L.s1 + (uint32_t)nchg * 128;
+    L.g = 0;
+    L.big = (L.s2b2 + C * 8 + 255) & ~255u;
+    L.d = L.big + (((uint32_t)halo_rows * rsl + 255) & ~255u);
+    const uint32_t hd = (L.d - L.big) + NBLK * 32 * DPX;
+    const uint32_t ring = 2u * Ks<KS, ACT_NONE>::SLOT;
+    L.zero = L.big + (hd > ring ? hd : ring);
+    L.total = L.zero + (uint32_t)KS * HPX + 64;
+    if (L.total > 160 * 1024)
+        return hipErrorInvalidConfiguration;
+    SoloArgs sa{};
+    Args &a = sa.a;
+    a.x = (const uint16_t *)x;
+    a.y = (uint16_t *)y;
+    a.dw_w = (const uint16_t *)w.dw_w;
+    a.s0 = w.s0;
+    a.b0 = w.b0;
+    a.w1 = (const uint16_t *)w.w1;
+    a.s1 = w.s1;
+    a.b1 = w.b1;
+    a.w2 = (const uint16_t *)w.w2;
+    a.s2 = w.s2;
+    a.b2 = w.b2;
+    a.H = s.H;
+    a.W = s.W;
+    a.NH = s.N * s.H;
+    a.nch = nch;
+    const int64_t P = (int64_t)s.N * s.H * s.W;
+    a.P = (uint32_t)P;
+    a.divW = fused::make_fastdiv((uint32_t)s.W);
+    a.divH = fused::make_fastdiv((uint32_t)s.H);
+    a.rsl = rsl;
+    a.off_b1 = L.b1;
+    a.off_s1 = L.s1;
+    a.off_s2b2 = L.s2b2;
+    a.off_g = L.g;
+    a.off_d = L.d;
+    a.off_big = L.big;
+    a.off_zero = L.zero;
+    sa.partial = groups > 1 ? partial : nullptr;
+    sa.chunks_per_group = nchg;
+    sa.ntiles = (int)((P + 127) / 128);
+    const int cus = device_cu_count();
+    int gx = (cus + groups - 1) / groups;
+    if (gx > sa.ntiles)
+        gx = sa.ntiles;
+    hipError_t e;
+#define CF_SOLO_LAUNCH(ACTV)                                                                                         \
+    {                                                                                                                 \
+        auto kf = solo_kernel<KS, ACTV>;                                                                             \
+        if ((e = hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L.total))) \
+            return e;                                                                                                 \
+        hipLaunchKernelGGL(kf, dim3(gx, groups), dim3(256), L.total, st, sa);                                       \
+    }
+    switch (s.act) {
+    case ACT_GELU: CF_SOLO_LAUNCH(ACT_GELU) break;
+    case ACT_RELU: CF_SOLO_LAUNCH(ACT_RELU) break;
+    default: CF_SOLO_LAUNCH(ACT_NONE) break;
+    }
+#undef CF_SOLO_LAUNCH
+    return hipGetLastError();
+}
+
+inline hipError_t launch_c512(const void *x, void *y, const BlockW &w, const Shape &s, int groups, float *partial,
+                              hipStream_t st) {
+    switch (s.k) {
+    case 1: return launch_solo<1>(x, y, w, s, groups, partial, st);
+    case 3: return launch_solo<3>(x, y, w, s, groups, partial, st);
+    case 5: return launch_solo<5>(x, y, w, s, groups, partial, st);
+    default: return launch_solo<7>(x, y, w, s, groups, partial, st);
+    }
+}
+
 }  // namespace wide
 
 hipError_t launch_wide_c128(const void *x, void *y, const BlockW &w, const Shape &s, hipStream_t st);
 hipError_t launch_wide_c256(const void *x, void *y, const BlockW &w, const Shape &s, hipStream_t st);
+hipError_t launch_wide_c512(const void *x, void *y, const BlockW &w, const Shape &s, int groups, float *partial,
+                            hipStream_t st);
 
 }  // namespace cf

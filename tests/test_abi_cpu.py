@@ -86,7 +86,11 @@ def test_workspace_queries():
     L = cf.lib()
     P = 2 * 5 * 7
     assert L.cf_stage_workspace_bytes(1, 2, 5, 7, 64, 0) == 0
-    assert L.cf_stage_workspace_bytes(3, 2, 5, 7, 64, 0) == P * 64 * 2
+    assert L.cf_stage_workspace_bytes(3, 2, 5, 7, 64, 0) == (P * 64 * 2 + 255) // 256 * 256
+    # C = 512 fp16: room for fp32 partials of up to 4 hidden groups (recommended size)
+    assert L.cf_stage_workspace_bytes(1, 2, 5, 7, 512, 0) == 4 * P * 512 * 4
+    assert L.cf_stage_workspace_bytes(2, 2, 5, 7, 512, 0) == P * 512 * 2 + 4 * P * 512 * 4
+    assert L.cf_stage_workspace_bytes(2, 2, 5, 7, 512, 1) == P * 512 * 2
     need = L.cf_unfused_workspace_bytes(2, 5, 7, 64, 4, 0)
     assert need >= P * 64 * 2 + P * 256 * 2
     assert L.cf_split_workspace_bytes(1, 7, 7, 512, 4, 8) == 8 * 49 * 512 * 4
