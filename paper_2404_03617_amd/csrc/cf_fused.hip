@@ -1,35 +1,21 @@
-// cf_fused.hip -- the ConvFirst block-fusion kernel for gfx950 (MI355X).
+// cf_fused.hip -- dispatch of the ConvFirst block-fusion kernels (Sec. 5.3.1,
+// Sec. 5.5.1 of Lavin, arXiv:2404.03617) and the hidden-split reduction.
 //
-// One workgroup (4 waves) owns a tile of M consecutive pixels of the
-// flattened N*H*W index and evaluates the whole residual block for it
-// (Sec. 5.3.1 of Lavin, arXiv:2404.03617):
-//   1. the input rows the tile touches, plus k/2 halo rows, are copied into
-//      LDS with 16-byte loads, in channel slabs of at most 64 channels;
-//   2. each lane runs the k x k depth-wise conv for 16-pixel blocks on the
-//      VALU and keeps the result as MFMA B-operand fragments in registers;
-//   3. the output accumulators (fp32, in registers) start from the input
-//      tile centre plus b2: the residual shortcut costs no extra HBM read;
-//   4. a loop over chunks of 32 hidden channels (eq. e:ffn-eff) computes
-//      H^T = W1_chunk * D^T on MFMA 16x16x32 with b1 in the C operand, applies
-//      phi, and feeds the result straight from the accumulator registers into
-//      the project MFMA  Out^T += W2_chunk * H^T  -- the hidden tile never
-//      touches LDS or HBM;
-//   5. the output tile is converted (round to nearest even) and stored once.
+// Every fused kernel evaluates the whole residual block for a range of
+// 32-pixel blocks of the flattened N*H*W index: halo rows into LDS, k x k
+// depth-wise conv on the VALU, then a loop over chunks of 32 hidden channels
+// (eq. e:ffn-eff) with expand and project on v_mfma_f32_32x32x16, phi in
+// between, and one store of the output tile.  The hidden values never reach
+// device memory.
 //
-// Transposed ("swap-AB") products make the MFMA output layout (4 consecutive
-// rows per lane) line up with the operand layout of the next MFMA.  Within a
-// chunk of 32 hidden channels the expand rows are gathered in the order
-// sigma(rb, m) = 8*(m/4) + 4*rb + m%4 so that lane group g ends up holding
-// hidden channels 8g..8g+7: then both weight fragments are single contiguous
-// 16-byte loads and the project K index is the hidden index.
-//
-// Weights are staged per chunk into LDS in fragment order (lane-contiguous,
-// conflict-free ds_read_b128), with s1/s2 folded in while staging.  When all
-// E*C/32 chunks fit in LDS (C = 64) they are staged once per persistent
-// workgroup; otherwise they stream through a double buffer per tile.
+//   C = 64, fp16        cf_block64.h  all weights resident in LDS, 64-pixel waves
+//   C = 128/256, fp16   cf_wide.h     wave pairs per block, DMA-fed weight buffers
+//   C = 512, fp16       cf_wide.h     one wave per block, chunk ring, optional
+//                                     hidden groups (fp32 partials + reduction)
+//   bf16, other shapes  cf_fused_impl.h
 //
 // Hidden-split mode (grid.y > 1): workgroup (tile, g) runs only its range of
-// chunks and writes an fp32 partial of the projected output; a second kernel
+// chunks and writes an fp32 partial of the projected output; split_reduce_kernel
 // adds the partials in group order plus b2 and the residual.
 #include "cf_block64.h"
 #include "cf_wide.h"
