@@ -53,7 +53,7 @@ constexpr int KST = C / 16;          // expand K steps
 constexpr int CB = C / 32;           // 32-channel output blocks
 constexpr int MAX_TB = 16;           // blocks per tile (two per wave at most)
 constexpr int PIX = 144;             // LDS bytes per halo pixel
-constexpr int CHUNK_W1 = KST * 1024; // W1 fragments of one 32-hidden chunk
+constexpr int CHUNK_W1 = (KST + 1) * 1024;  // W1 fragments of one 32-hidden chunk, then the b1 fragment
 constexpr int CHUNK_W2 = 2 * CB * 1024;
 constexpr float QS = 0.25f;
 
@@ -76,24 +76,25 @@ struct Args {
     uint32_t rs;         // LDS bytes per halo row: (W + 2*pad) * PIX
     int halo_rows;       // data rows of the halo buffer
     // LDS byte offsets
-    uint32_t off_w2, off_b1, off_cst, off_dwt, off_halo, off_zero;
+    uint32_t off_w2, off_b1, off_cst, off_dwt, off_halo, off_zero, off_trash;
 };
 
-// LDS map: [W1 nch*4 KB][W2 nch*4 KB][b1/4 nch*128 B][cst 512 B][taps k*k*128 B]
-//          [halo halo_rows * rs][zero area]
+// LDS map: [W1 + b1 nch*5 KB][W2 nch*4 KB][cst 512 B][taps k*k*128 B]
+//          [halo halo_rows * rs][zero area][trash 1 KB]
 struct Layout {
-    uint32_t w2, b1, cst, dwt, halo, zero, total;
+    uint32_t w2, b1, cst, dwt, halo, zero, trash, total;
 };
 
 inline Layout layout_for(int nch, int k, int halo_rows, uint32_t rs) {
     Layout L;
     L.w2 = (uint32_t)nch * CHUNK_W1;
-    L.b1 = L.w2 + (uint32_t)nch * CHUNK_W2;
-    L.cst = L.b1 + (uint32_t)nch * 128;
+    L.b1 = 0;  // the b1 fragments sit in the W1 chunks
+    L.cst = L.w2 + (uint32_t)nch * CHUNK_W2;
     L.dwt = L.cst + 512;
     L.halo = (L.dwt + (uint32_t)k * k * 128 + 255) & ~255u;
     L.zero = L.halo + (uint32_t)halo_rows * rs;
-    L.total = L.zero + (uint32_t)k * PIX + 128;
+    L.trash = (L.zero + (uint32_t)k * PIX + 128 + 15) & ~15u;
+    L.total = L.trash + 1024;
     return L;
 }
 
@@ -193,11 +194,17 @@ struct K64 {
             }
             *reinterpret_cast<u32x4 *>(smem + dst) = v.u;
         }
-        // b1 / 4: chunk ch, half h, register e = 4t + i  <->  hidden 16(t>>1) + 8h + 4(t&1) + i
-        for (int p = tid; p < a.nch * 32; p += NT) {
-            const int ch = p >> 5, e = p & 31, hh = e >> 4, t = (e >> 2) & 3, i = e & 3;
-            const int r = ch * 32 + 16 * (t >> 1) + 8 * hh + 4 * (t & 1) + i;
-            reinterpret_cast<float *>(smem + a.off_b1)[p] = a.b1 ? a.b1[r] * QS : 0.0f;
+        // b1 / 4 as the A fragment of a fifth expand K step: row m of chunk ch
+        // (hidden ch*32 + sigma(m)) holds b1/4 at k = 0 and zeros elsewhere; it
+        // meets a constant B fragment that is 1 at k = 0 for every pixel.
+        for (int p = tid; p < a.nch * 64; p += NT) {
+            const int ch = p >> 6, lane = p & 63;
+            u32x4 v = {0u, 0u, 0u, 0u};
+            if (lane < 32 && a.b1) {
+                const _Float16 bv = (_Float16)(a.b1[ch * 32 + sigma_row(lane)] * QS);
+                v[0] = (uint32_t)__builtin_bit_cast(uint16_t, bv);
+            }
+            *reinterpret_cast<u32x4 *>(smem + (uint32_t)ch * CHUNK_W1 + (uint32_t)(KST * 64 + lane) * 16) = v;
         }
         for (int c = tid; c < C; c += NT) {
             reinterpret_cast<_Float16 *>(smem + a.off_cst)[c] = (_Float16)((a.s0 ? a.s0[c] : 1.0f) * QS);
@@ -243,32 +250,29 @@ struct K64 {
         uint32_t g_lo;
         int rows;  // 0: nothing to copy
     };
-    // rows r = ch, ch + nch, ... of the next tile pass through registers: loaded
-    // during chunk ch, written to LDS during chunk ch + 1
+    // Row r of the next tile passes through registers: fetched in FFN step r
+    // into one of two buffers (by the parity of r) and written to LDS in step
+    // r + 2, so each load has two steps to land.  Branch-free, so that a step
+    // stays one basic block: lanes with nothing to copy read the first 16
+    // bytes of x and write them to a trash area.
     struct Staged {
-        u32x4 v[2];
-        int r[2];
+        u32x4 v;
+        uint32_t dst;  // LDS destination (the trash area for lanes with nothing to copy)
     };
-    static __device__ __forceinline__ void load_rows(const Args &a, const NextHalo &nh, const RowCopy &rc, int ch,
-                                                     Staged &st) {
-#pragma unroll
-        for (int q = 0; q < 2; q++) {
-            const int r = ch + q * a.nch;
-            const int grow = (int)nh.g_lo - PAD + r;
-            st.r[q] = -1;
-            if (r < nh.rows && grow >= 0 && grow < a.NH && rc.goff >= 0) {
-                st.v[q] = *reinterpret_cast<const u32x4 *>(reinterpret_cast<const uint8_t *>(a.x) +
-                                                           (size_t)grow * a.W * (C * 2) + rc.goff);
-                st.r[q] = r;
-            }
-        }
+    static __device__ __forceinline__ void load_row(const Args &a, const NextHalo &nh, const RowCopy &rc, int r,
+                                                    int lane, Staged &st) {
+        const uint8_t *xb = reinterpret_cast<const uint8_t *>(a.x);
+        const int grow = (int)nh.g_lo - PAD + r;
+        const bool okr = r < nh.rows && grow >= 0 && grow < a.NH;  // wave-uniform
+        const bool ok = okr && rc.goff >= 0;
+        const uint32_t gr = okr ? (uint32_t)grow : 0u;
+        const uint32_t go = ok ? (uint32_t)rc.goff : 0u;
+        const uint64_t src = (uint64_t)gr * (uint32_t)(a.W * C * 2) + go;
+        st.v = *reinterpret_cast<const u32x4 *>(xb + src);
+        st.dst = ok ? a.off_halo + (uint32_t)r * a.rs + rc.loff : a.off_trash + (uint32_t)lane * 16;
     }
-    static __device__ __forceinline__ void write_rows(const Args &a, uint8_t *smem, const RowCopy &rc,
-                                                      const Staged &st) {
-#pragma unroll
-        for (int q = 0; q < 2; q++)
-            if (st.r[q] >= 0)
-                *reinterpret_cast<u32x4 *>(smem + a.off_halo + (uint32_t)st.r[q] * a.rs + rc.loff) = st.v[q];
+    static __device__ __forceinline__ void write_row(uint8_t *smem, const Staged &st) {
+        *reinterpret_cast<u32x4 *>(smem + st.dst) = st.v;
     }
     // whole halo at once (first tile)
     static __device__ __forceinline__ void copy_halo(const Args &a, uint8_t *smem, int t0, int nblk,
@@ -306,78 +310,102 @@ struct K64 {
         }
     }
 
-    // ---- depth-wise conv, two-block wave: lane l computes pixel l of the
-    // wave's 64 (block j0 for l < 32, block j1 above) for all 16 channels of
-    // each K step with wave-uniform taps, then swaps halves into B fragments.
-    static __device__ __forceinline__ void dw_pair(const Args &a, const uint8_t *smem, const uint32_t (&base)[KS],
-                                                   u32x4 (&dfr)[KST][2]) {
-        typedef const __attribute__((address_space(4))) uint32_t *cptr;
-        const cptr wq = (cptr)a.dw_w;
+    // ---- depth-wise conv (Sec. 4.1.1, degenerate group width 1) of NQ 16-byte
+    // channel chunks.  Chunk qi of a lane reads pixel data at
+    // base[i] + j*PIX + qi*vstep and taps at wbase + (i*KS + j)*128 + qi*wstep
+    // (taps are read from LDS: a scalar load would share the lgkm counter with
+    // the LDS reads and force a full drain before every use).  The work is cut
+    // into units of one tap row of one chunk; the reads of unit u + DIST are
+    // issued before unit u is computed, through a register ring.
+    static constexpr int DIST = KS <= 1 ? 6 : KS <= 3 ? 3 : 1;
+    template <int NQ>
+    static __device__ __forceinline__ void dw_conv(const uint8_t *smem, const uint32_t (&base)[KS], uint32_t wbase,
+                                                   uint32_t vstep, uint32_t wstep, uint32_t cst, uint32_t cstep,
+                                                   uint32_t (&d)[NQ][4]) {
+        constexpr int NU = NQ * KS, R = DIST + 1;
+        u32x4 vb[R][KS], wb[R][KS];
 #pragma unroll
-        for (int ks = 0; ks < KST; ks++) {
-            uint32_t d[2][4];
+        for (int u = 0; u < DIST && u < NU; u++) {
+            const int qi = u / KS, i = u % KS;
 #pragma unroll
-            for (int c8 = 0; c8 < 2; c8++) {
-                const int q = 2 * ks + c8;  // 16-byte channel chunk
-                half2v acc[4] = {splat2(0.0f), splat2(0.0f), splat2(0.0f), splat2(0.0f)};
+            for (int j = 0; j < KS; j++) {
+                vb[u % R][j] = ld16(smem, base[i] + (uint32_t)(j * PIX + qi * vstep));
+                wb[u % R][j] = ld16(smem, wbase + (uint32_t)((i * KS + j) * 128 + qi * wstep));
+            }
+        }
+        half2v acc[4];
 #pragma unroll
-                for (int i = 0; i < KS; i++) {
+        for (int u = 0; u < NU; u++) {
+            const int qi = u / KS, i = u % KS;
+            if (u + DIST < NU) {
+                const int un = u + DIST, qn = un / KS, in = un % KS;
 #pragma unroll
-                    for (int j = 0; j < KS; j++) {
-                        Pack8 v;
-                        v.u = ld16(smem, base[i] + (uint32_t)(j * PIX + q * 16));
-                        const int wo = ((i * KS + j) * C + q * 8) / 2;  // dword index of the taps
-                        const uint32_t w0 = wq[wo], w1 = wq[wo + 1], w2 = wq[wo + 2], w3 = wq[wo + 3];
-                        acc[0] = __builtin_elementwise_fma(h2(v.w[0]), h2(w0), acc[0]);
-                        acc[1] = __builtin_elementwise_fma(h2(v.w[1]), h2(w1), acc[1]);
-                        acc[2] = __builtin_elementwise_fma(h2(v.w[2]), h2(w2), acc[2]);
-                        acc[3] = __builtin_elementwise_fma(h2(v.w[3]), h2(w3), acc[3]);
-                    }
+                for (int j = 0; j < KS; j++) {
+                    vb[un % R][j] = ld16(smem, base[in] + (uint32_t)(j * PIX + qn * vstep));
+                    wb[un % R][j] = ld16(smem, wbase + (uint32_t)((in * KS + j) * 128 + qn * wstep));
                 }
-                Pack8 sp, bp;
-                sp.u = ld16(smem, a.off_cst + q * 16);
-                bp.u = ld16(smem, a.off_cst + 128 + q * 16);
+            }
+            if (i == 0) {
 #pragma unroll
                 for (int e = 0; e < 4; e++)
-                    d[c8][e] = u32(__builtin_elementwise_fma(acc[e], h2(sp.w[e]), h2(bp.w[e])));
+                    acc[e] = splat2(0.0f);
             }
-            // lanes 32-63 of d[0] <-> lanes 0-31 of d[1]
 #pragma unroll
-            for (int e = 0; e < 4; e++) {
-                const auto r = __builtin_amdgcn_permlane32_swap(d[0][e], d[1][e], false, false);
-                dfr[ks][0][e] = r[0];
-                dfr[ks][1][e] = r[1];
+            for (int j = 0; j < KS; j++) {
+                Pack8 v, w;
+                v.u = vb[u % R][j];
+                w.u = wb[u % R][j];
+#pragma unroll
+                for (int e = 0; e < 4; e++)
+                    acc[e] = __builtin_elementwise_fma(h2(v.w[e]), h2(w.w[e]), acc[e]);
+            }
+            if (i == KS - 1) {
+                Pack8 sp, bp;
+                sp.u = ld16(smem, cst + (uint32_t)(qi * cstep));
+                bp.u = ld16(smem, cst + 128 + (uint32_t)(qi * cstep));
+#pragma unroll
+                for (int e = 0; e < 4; e++)
+                    d[qi][e] = u32(__builtin_elementwise_fma(acc[e], h2(sp.w[e]), h2(bp.w[e])));
+            }
+            // this unit: the reads of unit u + DIST, then its FMAs (pinned for
+            // small kernels; for k >= 5 the order is left to the compiler,
+            // whose group solver does not finish on that many units)
+            if constexpr (KS <= 3) {
+                __builtin_amdgcn_sched_group_barrier(0x100, 2 * KS, 0);
+                __builtin_amdgcn_sched_group_barrier(0x002, 4 * KS, 0);
             }
         }
     }
 
-    // ---- depth-wise conv, one-block wave: lane (h, m) computes channels
-    // 16ks + 8h .. +7 of pixel m (the B-fragment layout); taps from LDS.
+    // two-block wave: lane l computes pixel l of the wave's 64 (block j0 for
+    // l < 32, block j1 above) for all 16 channels of each K step (taps are the
+    // same for every lane), then swaps halves into the two B fragments.
+    static __device__ __forceinline__ void dw_pair(const Args &a, const uint8_t *smem, const uint32_t (&base)[KS],
+                                                   u32x4 (&dfr)[KST][2]) {
+        uint32_t d[2 * KST][4];
+        dw_conv<2 * KST>(smem, base, a.off_dwt, 16u, 16u, a.off_cst, 16u, d);
+        // lanes 32-63 of chunk 2ks <-> lanes 0-31 of chunk 2ks+1
+#pragma unroll
+        for (int ks = 0; ks < KST; ks++)
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                const auto r = __builtin_amdgcn_permlane32_swap(d[2 * ks][e], d[2 * ks + 1][e], false, false);
+                dfr[ks][0][e] = r[0];
+                dfr[ks][1][e] = r[1];
+            }
+    }
+
+    // one-block wave: lane (h, m) computes channels 16ks + 8h .. +7 of pixel m
+    // (the B-fragment layout; base already includes the 16h byte offset).
     static __device__ __forceinline__ void dw_single(const Args &a, const uint8_t *smem, const uint32_t (&base)[KS],
                                                      int h, u32x4 (&dfr)[KST][2]) {
-        const uint32_t wbase = a.off_dwt + (uint32_t)h * 16;
+        uint32_t d[KST][4];
+        dw_conv<KST>(smem, base, a.off_dwt + (uint32_t)h * 16, 32u, 32u, a.off_cst + (uint32_t)h * 16, 32u, d);
 #pragma unroll
-        for (int ks = 0; ks < KST; ks++) {
-            half2v acc[4] = {splat2(0.0f), splat2(0.0f), splat2(0.0f), splat2(0.0f)};
-#pragma unroll
-            for (int i = 0; i < KS; i++) {
-#pragma unroll
-                for (int j = 0; j < KS; j++) {
-                    Pack8 v, w;
-                    v.u = ld16(smem, base[i] + (uint32_t)(j * PIX + 2 * ks * 16));
-                    w.u = ld16(smem, wbase + (uint32_t)((i * KS + j) * 128 + 2 * ks * 16));
-#pragma unroll
-                    for (int e = 0; e < 4; e++)
-                        acc[e] = __builtin_elementwise_fma(h2(v.w[e]), h2(w.w[e]), acc[e]);
-                }
-            }
-            Pack8 sp, bp;
-            sp.u = ld16(smem, a.off_cst + (uint32_t)(2 * ks + h) * 16);
-            bp.u = ld16(smem, a.off_cst + 128 + (uint32_t)(2 * ks + h) * 16);
+        for (int ks = 0; ks < KST; ks++)
 #pragma unroll
             for (int e = 0; e < 4; e++)
-                dfr[ks][0][e] = u32(__builtin_elementwise_fma(acc[e], h2(sp.w[e]), h2(bp.w[e])));
-        }
+                dfr[ks][0][e] = d[ks][e];
     }
 
     // ---- residual start: acc = x/4 + b2/4 from the halo centre, MFMA layout
@@ -407,80 +435,120 @@ struct K64 {
     }
 
     // ---- FFN over all hidden chunks (eq. e:ffn-eff): expand, phi, project.
-    // Software-pipelined by one chunk: while chunk c is activated and
-    // projected, the fragments of chunk c+1 are already loaded and its expand
-    // is issued between the activation and the projection of chunk c, so no
-    // instruction waits on an LDS read or on an MFMA result it just issued.
+    // Three-stage software pipeline over the chunks: step s issues the expand
+    // MFMAs of chunk s, activates chunk s-1 (VALU) and issues the project
+    // MFMAs of chunk s-2.  The three are independent, so the matrix and vector
+    // instructions of a step are interleaved (one MFMA, then a run of VALU
+    // instructions that execute while it runs) and no instruction waits on an
+    // MFMA result issued in the same step.  Two expand accumulator sets (u0,
+    // u1) and two activated sets (g0, g1) alternate between even and odd steps.
     template <int NB>
-    static __device__ __forceinline__ void expand(const uint8_t *w1p, const uint8_t *b1p, int ch,
-                                                  const u32x4 (&dfr)[KST][2], float16v (&hh)[2]) {
-        u32x4 w1f[KST];
-#pragma unroll
-        for (int ks = 0; ks < KST; ks++)
-            w1f[ks] = *reinterpret_cast<const u32x4 *>(w1p + ch * CHUNK_W1 + ks * 1024);
-        const float16v bias = *reinterpret_cast<const float16v *>(b1p + ch * 128);
+    static __device__ __forceinline__ void act_blocks(const float16v (&u)[2], uint32_t (&g)[16]) {
 #pragma unroll
         for (int b = 0; b < NB; b++)
-            hh[b] = bias;
 #pragma unroll
-        for (int ks = 0; ks < KST; ks++)
+            for (int p0 = 0; p0 < 8; p0 += 4) {
+                float v[8];
 #pragma unroll
-            for (int b = 0; b < NB; b++)
-                hh[b] = mfma32(w1f[ks], dfr[ks][b], hh[b], F16{});
+                for (int i = 0; i < 8; i++)
+                    v[i] = u[b][2 * p0 + i];
+                activate<4>(v, &g[b * 8 + p0]);
+            }
     }
 
-    template <int NB, bool MORE>
-    static __device__ __forceinline__ void chunk_step(const Args &a, uint8_t *smem, const NextHalo &nh,
-                                                      const RowCopy &rc, Staged &stg, const uint8_t *w1p, const uint8_t *w2p,
-                                                      const uint8_t *b1p, int ch, const u32x4 (&dfr)[KST][2],
-                                                      float16v (&hc)[2], float16v (&acc)[CB][2]) {
-        u32x4 w2f[2 * CB];
+    struct Ffn {
+        const uint8_t *w1p, *w2p;
+        u32x4 ones;  // B fragment: 1 at k = 0 for every pixel (bias K step)
+        NextHalo nh;
+        RowCopy rc;
+        int lane;
+    };
+
+    template <int NB, bool EXP, bool ACTV, bool PROJ>
+    static __device__ __forceinline__ void step(const Args &a, uint8_t *smem, const Ffn &f, Staged &stg, int s,
+                                                const u32x4 (&dfr)[KST][2], float16v (&ue)[2],
+                                                const float16v (&ua)[2], uint32_t (&ga)[16],
+                                                const uint32_t (&gp)[16], float16v (&acc)[CB][2]) {
+        // halo row s - 2 of the next tile goes to LDS, row s is fetched
+        if constexpr (PROJ)
+            write_row(smem, stg);
+        load_row(a, f.nh, f.rc, s, f.lane, stg);
+        if constexpr (ACTV)
+            act_blocks<NB>(ua, ga);
+        if constexpr (EXP) {
+            const uint8_t *wp = f.w1p + s * CHUNK_W1;
+            const u32x4 bfr = *reinterpret_cast<const u32x4 *>(wp + KST * 1024);
 #pragma unroll
-        for (int g = 0; g < 2 * CB; g++)
-            w2f[g] = *reinterpret_cast<const u32x4 *>(w2p + ch * CHUNK_W2 + g * 1024);
-        float v[NB * 16];
+            for (int b = 0; b < NB; b++)
+                ue[b] = mfma32(bfr, f.ones, float16v{}, F16{});
 #pragma unroll
-        for (int b = 0; b < NB; b++)
+            for (int ks = 0; ks < KST; ks++) {
+                const u32x4 w1f = *reinterpret_cast<const u32x4 *>(wp + ks * 1024);
 #pragma unroll
-            for (int e = 0; e < 16; e++)
-                v[b * 16 + e] = hc[b][e];
-        uint32_t o[NB * 8];
-        activate<NB * 8>(v, o);
-        if constexpr (MORE)
-            expand<NB>(w1p, b1p, ch + 1, dfr, hc);
-        write_rows(a, smem, rc, stg);
-        load_rows(a, nh, rc, ch, stg);
+                for (int b = 0; b < NB; b++)
+                    ue[b] = mfma32(w1f, dfr[ks][b], ue[b], F16{});
+            }
+        }
+        if constexpr (PROJ) {
 #pragma unroll
-        for (int kk = 0; kk < 2; kk++)
+            for (int kk = 0; kk < 2; kk++)
 #pragma unroll
-            for (int cb = 0; cb < CB; cb++)
+                for (int cb = 0; cb < CB; cb++) {
+                    const u32x4 w2f = *reinterpret_cast<const u32x4 *>(f.w2p + (s - 2) * CHUNK_W2 +
+                                                                      (cb * 2 + kk) * 1024);
 #pragma unroll
-                for (int b = 0; b < NB; b++) {
-                    u32x4 hid;
+                    for (int b = 0; b < NB; b++) {
+                        u32x4 hid;
 #pragma unroll
-                    for (int p = 0; p < 4; p++)
-                        hid[p] = o[b * 8 + kk * 4 + p];
-                    acc[cb][b] = mfma32(w2f[cb * 2 + kk], hid, acc[cb][b], F16{});
+                        for (int p = 0; p < 4; p++)
+                            hid[p] = gp[b * 8 + kk * 4 + p];
+                        acc[cb][b] = mfma32(w2f, hid, acc[cb][b], F16{});
+                    }
                 }
+        }
+        // Interleave: fragment reads ahead of their use, one MFMA, then the
+        // VALU instructions that execute in its shadow.
+        constexpr int NM = (EXP ? NB * (KST + 1) : 0) + (PROJ ? NB * 2 * CB : 0);
+        constexpr int NV = ACTV ? NB * 64 : 0;
+        if constexpr (NM > 0 && NV > 0) {
+            constexpr int VPER = (NV - 8 + NM - 1) / NM;
+            __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
+#pragma unroll
+            for (int i = 0; i < NM; i++) {
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x002, VPER, 0);
+            }
+        }
     }
 
     template <int NB>
     static __device__ __forceinline__ void ffn(const Args &a, uint8_t *smem, int lane, const NextHalo &nh,
                                                const RowCopy &rc, const u32x4 (&dfr)[KST][2],
                                                float16v (&acc)[CB][2]) {
-        const int h = lane >> 5;
-        const uint8_t *w1p = smem + lane * 16;
-        const uint8_t *w2p = smem + a.off_w2 + lane * 16;
-        const uint8_t *b1p = smem + a.off_b1 + h * 64;
-        float16v hc[2];
-        Staged stg;
-        stg.r[0] = stg.r[1] = -1;
-        expand<NB>(w1p, b1p, 0, dfr, hc);
+        Ffn f;
+        f.w1p = smem + lane * 16;
+        f.w2p = smem + a.off_w2 + lane * 16;
+        f.ones = u32x4{lane < 32 ? 0x3c00u : 0u, 0u, 0u, 0u};
+        f.nh = nh;
+        f.rc = rc;
+        f.lane = lane;
+        float16v u0[2], u1[2];
+        uint32_t g0[16], g1[16];
+        Staged st0, st1;  // halo rows of even / odd steps
+        const int n = a.nch;  // even, >= 2
+        step<NB, true, false, false>(a, smem, f, st0, 0, dfr, u0, u1, g1, g0, acc);
+        step<NB, true, true, false>(a, smem, f, st1, 1, dfr, u1, u0, g0, g1, acc);
 #pragma unroll 1
-        for (int ch = 0; ch + 1 < a.nch; ch++)
-            chunk_step<NB, true>(a, smem, nh, rc, stg, w1p, w2p, b1p, ch, dfr, hc, acc);
-        chunk_step<NB, false>(a, smem, nh, rc, stg, w1p, w2p, b1p, a.nch - 1, dfr, hc, acc);
-        write_rows(a, smem, rc, stg);
+        for (int s = 2; s < n; s += 2) {
+            step<NB, true, true, true>(a, smem, f, st0, s, dfr, u0, u1, g1, g0, acc);
+            step<NB, true, true, true>(a, smem, f, st1, s + 1, dfr, u1, u0, g0, g1, acc);
+        }
+        step<NB, false, true, true>(a, smem, f, st0, n, dfr, u0, u1, g1, g0, acc);
+        step<NB, false, false, true>(a, smem, f, st1, n + 1, dfr, u1, u0, g0, g1, acc);
+        write_row(smem, st0);
+        write_row(smem, st1);
     }
 
     template <int NB>
@@ -527,16 +595,16 @@ struct K64 {
         __syncthreads();
 
         const RowCopy rc = row_copy(a, wv, lane);
-        // the range is cut into nt tiles of nearly equal size (<= tile_max)
+        // the range is cut into tiles of tile_max blocks and a last, smaller
+        // one: a full tile gives every SIMD the same number of blocks
         const int range = hi - lo;
         const int nt = (range + a.tile_max - 1) / a.tile_max;
-        const int tsz = nt ? range / nt : 0, tex = nt ? range % nt : 0;
         if (nt > 0)
-            copy_halo(a, smem, lo, tsz + (tex > 0 ? 1 : 0), rc);
+            copy_halo(a, smem, lo, range < a.tile_max ? range : a.tile_max, rc);
 
         int t0 = lo;
         for (int it = 0; it < nt; it++) {
-            const int nblk = tsz + (it < tex ? 1 : 0);
+            const int nblk = (hi - t0) < a.tile_max ? (hi - t0) : a.tile_max;
             uint32_t g_lo;
             int rows;
             tile_rows(a, t0, nblk, g_lo, rows);
@@ -575,7 +643,7 @@ struct K64 {
             __syncthreads();  // the halo buffer is free
             NextHalo nh{0u, 0};
             const int t1 = t0 + nblk;
-            const int nblk1 = tsz + (it + 1 < tex ? 1 : 0);
+            const int nblk1 = (hi - t1) < a.tile_max ? (hi - t1) : a.tile_max;
             if (it + 1 < nt)
                 tile_rows(a, t1, nblk1, nh.g_lo, nh.rows);
 
@@ -604,16 +672,21 @@ __global__ __launch_bounds__(NT, 1) void block64_kernel(Args a) {
 // ---------------------------------------------------------------------------
 // Host side.  Returns hipErrorInvalidConfiguration when the shape needs the
 // generic kernel (W too wide for the fixed halo row, or LDS does not fit).
-inline bool plan(int N, int H, int W, int E, int k, int &tb, int &halo_rows, uint32_t &rs, Layout &L) {
+inline bool plan(int N, int H, int W, int E, int k, int max_range, int &tb, int &halo_rows, uint32_t &rs,
+                 Layout &L) {
     const int pad = k / 2;
     if (W + 2 * pad > 64 || E * C % 32 != 0 || E * C / 32 > 8)
         return false;
     rs = (uint32_t)(W + 2 * pad) * PIX;
     const int64_t NH = (int64_t)N * H;
+    const int nch = E * C / 32;
+    // the next tile's halo rows are copied one per FFN step (nch + 2 steps),
+    // so a tile may touch at most nch + 2 rows, unless every workgroup has a
+    // single tile (the first tile is copied whole)
     for (tb = MAX_TB; tb >= 1; tb--) {
         halo_rows = halo_rows_for(tb, k, W, NH);
-        L = layout_for(E * C / 32, k, halo_rows, rs);
-        if (L.total <= 160 * 1024)
+        L = layout_for(nch, k, halo_rows, rs);
+        if (L.total <= 160 * 1024 && (halo_rows <= nch + 2 || max_range <= tb))
             return true;
     }
     return false;
@@ -621,10 +694,15 @@ inline bool plan(int N, int H, int W, int E, int k, int &tb, int &halo_rows, uin
 
 template <int KS>
 hipError_t launch_k(const void *x, void *y, const BlockW &w, const Shape &s, hipStream_t st) {
+    const int64_t P = (int64_t)s.N * s.H * s.W;
+    const int nblocks = (int)((P + 31) / 32);
+    int G = device_cu_count();
+    if (G > nblocks)
+        G = nblocks;
     int tb, halo_rows;
     uint32_t rs;
     Layout L;
-    if (!plan(s.N, s.H, s.W, s.E, KS, tb, halo_rows, rs, L))
+    if (!plan(s.N, s.H, s.W, s.E, KS, (nblocks + G - 1) / G, tb, halo_rows, rs, L))
         return hipErrorInvalidConfiguration;
     Args a{};
     a.x = (const uint16_t *)x;
@@ -642,14 +720,10 @@ hipError_t launch_k(const void *x, void *y, const BlockW &w, const Shape &s, hip
     a.W = s.W;
     a.NH = s.N * s.H;
     a.nch = s.E * C / 32;
-    const int64_t P = (int64_t)s.N * s.H * s.W;
     a.P = (uint32_t)P;
     a.divW = fused::make_fastdiv((uint32_t)s.W);
     a.divH = fused::make_fastdiv((uint32_t)s.H);
-    a.nblocks = (int)((P + 31) / 32);
-    int G = device_cu_count();
-    if (G > a.nblocks)
-        G = a.nblocks;
+    a.nblocks = nblocks;
     a.range_base = a.nblocks / G;
     a.range_extra = a.nblocks % G;
     a.tile_max = tb;
@@ -661,6 +735,7 @@ hipError_t launch_k(const void *x, void *y, const BlockW &w, const Shape &s, hip
     a.off_dwt = L.dwt;
     a.off_halo = L.halo;
     a.off_zero = L.zero;
+    a.off_trash = L.trash;
     hipError_t e;
     switch (s.act) {
     case ACT_GELU: {

@@ -56,6 +56,22 @@ def test_fused_block_matches_oracle(case, dtype):
         assert_close(y, oracle_block(x, p, act), what="%s %s %s" % (case, dtype, act))
 
 
+# Batches large enough that every workgroup walks several tiles, with halo
+# spans that exceed a short tile's row budget (the next tile's halo rows are
+# copied while the current tile's FFN runs).
+@pytest.mark.parametrize("case", [(28, 256, 3), (28, 200, 7), (14, 1024, 3), (7, 4096, 3)],
+                         ids=lambda c: "W%d_N%d_k%d" % c)
+def test_c64_many_tiles_per_workgroup(case):
+    W, N, k = case
+    say("c64 many tiles", case)
+    x, p = make_block(21, N, W, W, 64, 4, k, "f16")
+    y = cf.block_forward(x.cuda(), to_dev(p))
+    torch.cuda.synchronize()
+    imgs = [0, 1, N // 3, N // 2 - 1, N - 1]
+    ref = oracle_block(x, p, images=imgs)
+    assert_close(y.cpu()[imgs], ref, what="c64 W=%d N=%d k=%d" % (W, N, k))
+
+
 @pytest.mark.parametrize("dtype", ["f16", "bf16"])
 @pytest.mark.parametrize("case", [(64, 4, 3, 2, 9, 13), (128, 2, 5, 1, 7, 9), (256, 4, 7, 1, 14, 14),
                                   (512, 4, 3, 1, 7, 7)], ids=lambda c: "C%d_E%d_k%d_N%d_%dx%d" % c)
