@@ -265,24 +265,40 @@ struct Kw {
         }
     }
 
-    // ---- depth-wise conv of one slab, channel-major.  Wave r of block b's pair
-    // takes pixels 16r .. 16r + 15 of the block, half-wave hw 8 of them; lane
-    // channel group cq (4 channels).  Tap rows are the outer loop so only one
-    // row of taps is held in registers at a time.
-    static __device__ void dw_slab(const Args &a, uint8_t *smem, uint32_t g_lo, uint32_t pblk, int b, int r,
+    // ---- depth-wise conv of one slab, channel-major.  Lane channel group cq
+    // (4 channels) of half-wave hw computes NPX consecutive pixels starting at
+    // pixel q0 = q0base + NPX * hw of block b.  All taps of the lane's channels
+    // and its s0 / b0 are loaded once (a single round trip), then the tap rows
+    // are unrolled so that the LDS reads can run ahead of the FMAs.
+    template <int NPX>
+    static __device__ void dw_slab(const Args &a, uint8_t *smem, uint32_t g_lo, uint32_t pblk, int b, int q0base,
                                    int slab, int lane) {
         const int hw = lane >> 5, cq = lane & 31;
         const int c0 = slab * CS + 4 * cq;
-        const int q0 = 16 * r + 8 * hw;  // first pixel of this half-wave within the block
-        uint32_t topleft[8];
-        int hh[8];
+        const int q0 = q0base + NPX * hw;  // first pixel of this half-wave within the block
+        // taps: all at once for k <= 3; for larger k one row at a time, the
+        // next row's loads issued before the current row is computed
+        constexpr int TR = (KS <= 3 && C < 512) ? KS : 1;  // tap rows held per load batch
+        u32x2 wt[2][TR * KS];
+#pragma unroll
+        for (int t = 0; t < TR * KS; t++)
+            wt[0][t] = *reinterpret_cast<const u32x2 *>(a.dw_w + (size_t)t * C + c0);
+        half2v s0q[2], b0q[2];
+#pragma unroll
+        for (int e = 0; e < 2; e++) {
+            const int c = c0 + 2 * e;
+            s0q[e] = half2v{(_Float16)((a.s0 ? a.s0[c] : 1.0f) * QS), (_Float16)((a.s0 ? a.s0[c + 1] : 1.0f) * QS)};
+            b0q[e] = half2v{(_Float16)((a.b0 ? a.b0[c] : 0.0f) * QS), (_Float16)((a.b0 ? a.b0[c + 1] : 0.0f) * QS)};
+        }
+        uint32_t topleft[NPX];
+        int hh[NPX];
         {
             uint32_t p = pblk + q0;
             uint32_t gg = fdiv(p < a.P ? p : 0u, a.divW);
             int wc = (int)(p - gg * (uint32_t)a.W);
             int hr = (int)(gg - fdiv(gg, a.divH) * (uint32_t)a.H);
 #pragma unroll
-            for (int i = 0; i < 8; i++, p++) {
+            for (int i = 0; i < NPX; i++, p++) {
                 topleft[i] = a.off_big + (gg - g_lo) * a.rsl + (uint32_t)wc * HPX + (uint32_t)cq * 8;
                 hh[i] = p < a.P ? hr : -KS - 1;  // invalid pixels read zeros only
                 if (++wc == a.W) {
@@ -293,40 +309,49 @@ struct Kw {
                 }
             }
         }
-        half2v acc[8][2];
+        half2v acc[NPX][2];
 #pragma unroll
-        for (int i = 0; i < 8; i++)
+        for (int i = 0; i < NPX; i++)
             acc[i][0] = acc[i][1] = splat2(0.0f);
-        // one tap row per iteration
-        // (bounds the loads the scheduler can hoist)
-#pragma unroll 1
-        for (int ti = 0; ti < KS; ti++) {
-            u32x2 wt[KS];
+        auto row = [&](int ti, const u32x2 *w) {
 #pragma unroll
-            for (int tj = 0; tj < KS; tj++)
-                wt[tj] = *reinterpret_cast<const u32x2 *>(a.dw_w + (size_t)(ti * KS + tj) * C + c0);
-#pragma unroll
-            for (int i = 0; i < 8; i++) {
+            for (int i = 0; i < NPX; i++) {
                 const int hr = hh[i] + ti - PAD;
                 const uint32_t rb = (hr >= 0 && hr < a.H) ? topleft[i] + (uint32_t)ti * a.rsl : a.off_zero;
 #pragma unroll
                 for (int tj = 0; tj < KS; tj++) {
                     const u32x2 v = *reinterpret_cast<const u32x2 *>(smem + rb + (uint32_t)tj * HPX);
-                    acc[i][0] = __builtin_elementwise_fma(h2(v[0]), h2(wt[tj][0]), acc[i][0]);
-                    acc[i][1] = __builtin_elementwise_fma(h2(v[1]), h2(wt[tj][1]), acc[i][1]);
+                    acc[i][0] = __builtin_elementwise_fma(h2(v[0]), h2(w[tj][0]), acc[i][0]);
+                    acc[i][1] = __builtin_elementwise_fma(h2(v[1]), h2(w[tj][1]), acc[i][1]);
+                }
+            }
+        };
+        if constexpr (TR == KS) {
+#pragma unroll
+            for (int ti = 0; ti < KS; ti++)
+                row(ti, &wt[0][ti * KS]);
+        } else {
+#pragma unroll 1
+            for (int ti = 0; ti < KS; ti += 2) {
+                if (ti + 1 < KS) {
+#pragma unroll
+                    for (int tj = 0; tj < KS; tj++)
+                        wt[1][tj] = *reinterpret_cast<const u32x2 *>(a.dw_w + (size_t)((ti + 1) * KS + tj) * C + c0);
+                }
+                row(ti, wt[0]);
+                if (ti + 1 < KS) {
+                    if (ti + 2 < KS) {
+#pragma unroll
+                        for (int tj = 0; tj < KS; tj++)
+                            wt[0][tj] = *reinterpret_cast<const u32x2 *>(a.dw_w + (size_t)((ti + 2) * KS + tj) * C + c0);
+                    }
+                    row(ti + 1, wt[1]);
                 }
             }
         }
-        half2v s0q[2], b0q[2];
-#pragma unroll
-        for (int e = 0; e < 2; e++) {
-            const int c = c0 + 2 * e;
-            s0q[e] = half2v{(_Float16)((a.s0 ? a.s0[c] : 1.0f) * QS), (_Float16)((a.s0 ? a.s0[c + 1] : 1.0f) * QS)};
-            b0q[e] = half2v{(_Float16)((a.b0 ? a.b0[c] : 0.0f) * QS), (_Float16)((a.b0 ? a.b0[c + 1] : 0.0f) * QS)};
-        }
         const uint32_t dbase = a.off_d + (uint32_t)(32 * b + q0) * DPX + (uint32_t)(4 * cq) * 2;
 #pragma unroll
-        for (int i = 0; i < 8; i++) {
+        for (int i = 0; i < NPX; i++) {
             u32x2 d;
             d[0] = u32(__builtin_elementwise_fma(acc[i][0], s0q[0], b0q[0]));
             d[1] = u32(__builtin_elementwise_fma(acc[i][1], s0q[1], b0q[1]));
@@ -484,7 +509,7 @@ struct Kw {
                 copy_slab(a, smem, g_lo, rows, slab, tid);
                 __syncthreads();
                 if (mine)
-                    dw_slab(a, smem, g_lo, pblk, b, r, slab, lane);
+                    dw_slab<8>(a, smem, g_lo, pblk, b, 16 * r, slab, lane);
                 __syncthreads();
 #pragma unroll
                 for (int k8 = 0; k8 < CS / 16; k8++)
@@ -545,34 +570,70 @@ struct SoloArgs {
     int ntiles;
 };
 
-template <int KS, int ACT>
+template <int C, int KS, int ACT>
 struct Ks {
-    static constexpr int C = 512;
     static constexpr int NWS = 4, NTS = NWS * 64;
     typedef Kw<C, KS, ACT> K;
     static constexpr int KST = C / 16, CB = C / 32, NSLAB = C / CS;
-    static constexpr int SLOT = (KST + 2 * CB) * 1024;  // one chunk: W1 then W2 fragments
-    static constexpr int FPW = (KST + 2 * CB) / NWS;     // DMA instructions per wave per chunk
+    // One chunk of weights in LDS, filled by LDS-DMA instructions of 1 KB each
+    // that read contiguous memory; every instruction's KB sits at a pitch of
+    // PITCH bytes (16 bytes of padding), which makes the A-fragment reads
+    // below hit 16 different bank groups per 16 lanes:
+    //  * W1 (rows of C halves, contiguous in memory): C = 512: instruction j
+    //    copies row j; C = 256: instruction j copies rows j and j + 16 (the two
+    //    rows are read by different 16-lane groups).  The expand fragment of K
+    //    step ks, lane (h, m), is row sigma(m), bytes 32 ks + 16 h.
+    //  * W2: each of the C rows contributes 64 contiguous bytes (its 32 hidden
+    //    columns).  Output blocks are taken four at a time; within such a set,
+    //    instruction i (0..7) holds, for each of the four blocks, the rows
+    //    tau(m) with m = 4i .. 4i+3, at slot 4 * block + m % 4.  The project
+    //    fragment (cb, kk), lane (h, m), is then at
+    //    (cb/4)*8*PITCH + (m/4)*PITCH + (cb%4)*256 + (m%4)*64 + 32 kk + 16 h.
+    static constexpr int PITCH = 1040;
+    static constexpr int RPI = 1024 / (2 * C);           // W1 rows per instruction
+    static constexpr int NI1 = 32 / RPI, NI2 = 2 * CB;    // instructions per chunk
+    static constexpr int W2OFF = NI1 * PITCH;
+    static constexpr int SLOT = W2OFF + NI2 * PITCH;
+    static_assert((C == 512 || C == 256) && CB % 4 == 0, "solo kernel: C = 256 or 512");
+    static constexpr int WIN = C == 512 ? 4 : 8;  // fragment reads in flight (registers permitting)
 
+    // LDS offset of W1 row r inside a chunk slot
+    static __device__ __forceinline__ uint32_t w1_row(int r) {
+        return RPI == 1 ? (uint32_t)r * PITCH : (uint32_t)(r & 15) * PITCH + (uint32_t)(r >> 4) * (2 * C);
+    }
+
+    // This wave's 1 KB pieces of a chunk: NPW copies, piece q -> (global
+    // source of the lane's 16 bytes, byte offset of the piece in the slot).
+    static constexpr int NPW = (NI1 + NI2) / NWS;
+    static __device__ __forceinline__ void chunk_piece(const Args &a, int ch, int q, int wv, int lane,
+                                                       const uint16_t *&src, uint32_t &off) {
+        const uint32_t ec = (uint32_t)a.nch * 32;
+        if (q < NI1 / NWS) {
+            // W1: lane -> row (instruction j) + 16 * (lane / 32) for C = 256, piece lane % (64 / RPI)
+            const int j = wv + NWS * q;
+            const int lr = RPI == 1 ? 0 : 16 * (lane >> 5), lp = RPI == 1 ? lane : (lane & 31);
+            src = a.w1 + ((size_t)ch * 32 + lr + j) * C + 8 * lp;
+            off = (uint32_t)j * PITCH;
+        } else {
+            // W2: lane -> slot s = lane / 4 (block of the set s / 4, row m = 4 i + s % 4), piece lane % 4
+            const int j = wv + NWS * (q - NI1 / NWS), st = j >> 3, i = j & 7;
+            const int sl = lane >> 2, bq = sl >> 2, r4 = sl & 3, pc = lane & 3;
+            const uint32_t o = (uint32_t)(4 * st + bq) * 32 + (uint32_t)tau_row(4 * i + r4);
+            src = a.w2 + (size_t)o * ec + (size_t)ch * 32 + 8 * pc;
+            off = W2OFF + (uint32_t)j * PITCH;
+        }
+    }
     static __device__ __forceinline__ void dma_chunk(const Args &a, uint8_t *smem, int ch, int slot, int wv,
                                                      int lane) {
         uint8_t *buf = smem + a.off_big + slot * SLOT;
-        const uint16_t *w1 = a.w1 + (size_t)ch * 32 * C;
-        const uint16_t *w2 = a.w2 + (size_t)ch * 32;
-        const uint32_t ec = (uint32_t)a.nch * 32;
-        const uint32_t lo1 = (uint32_t)(sigma_row(lane & 31) * C + 8 * (lane >> 5));
-        const uint32_t lo2 = (uint32_t)tau_row(lane & 31) * ec + 8 * (lane >> 5);
 #pragma unroll
-        for (int f = wv; f < KST + 2 * CB; f += NWS) {
-            if (f < KST) {
-                fused::dma16(w1 + (lo1 + (uint32_t)(f * 16)), buf + f * 1024);
-            } else {
-                const int g = f - KST, cb = g >> 1, kk = g & 1;
-                fused::dma16(w2 + (lo2 + (uint32_t)(cb * 32) * ec + (uint32_t)(16 * kk)), buf + f * 1024);
-            }
+        for (int q = 0; q < NPW; q++) {
+            const uint16_t *src;
+            uint32_t off;
+            chunk_piece(a, ch, q, wv, lane, src, off);
+            fused::dma16(src, buf + off);
         }
     }
-
     static __device__ void run(const SoloArgs &sa, uint8_t *smem) {
         const Args &a = sa.a;
         const int tid = threadIdx.x;
@@ -602,8 +663,13 @@ struct Ks {
                 K::template copy_slab<NTS>(a, smem, g_lo, rows, slab, tid);
                 __syncthreads();
                 if (mine) {
-                    K::dw_slab(a, smem, g_lo, pblk, wv, 0, slab, lane);
-                    K::dw_slab(a, smem, g_lo, pblk, wv, 1, slab, lane);
+                    // 16 pixels per half-wave; 8 at a time where registers are short
+                    if constexpr (KS >= 7 || C == 512) {
+                        K::template dw_slab<8>(a, smem, g_lo, pblk, wv, 0, slab, lane);
+                        K::template dw_slab<8>(a, smem, g_lo, pblk, wv, 16, slab, lane);
+                    } else {
+                        K::template dw_slab<16>(a, smem, g_lo, pblk, wv, 0, slab, lane);
+                    }
                 }
                 __syncthreads();
 #pragma unroll
@@ -627,29 +693,31 @@ struct Ks {
                 lds_barrier();           // everyone's have; the other slot is free
                 if (c + 1 < nchg)
                     dma_chunk(a, smem, ch0 + c + 1, (c + 1) & 1, wv, lane);
-                const uint8_t *slot = smem + a.off_big + (c & 1) * SLOT + lane * 16;
+                const uint8_t *slot = smem + a.off_big + (c & 1) * SLOT;
+                const uint8_t *f1 = slot + w1_row(sigma_row(m)) + h * 16;
+                const uint8_t *f2 = slot + W2OFF + (m >> 2) * PITCH + (m & 3) * 64 + h * 16;
                 // expand (4-deep fragment window)
                 float16v hh;
 #pragma unroll
                 for (int e = 0; e < 16; e++)
                     hh[e] = 0.0f;
-                u32x4 wf[4];
+                u32x4 wf[WIN];
 #pragma unroll
-                for (int i = 0; i < 4; i++)
-                    wf[i] = ld16(slot, i * 1024);
+                for (int i = 0; i < WIN; i++)
+                    wf[i] = ld16(f1, i * 32);
 #pragma unroll
                 for (int ks = 0; ks < KST; ks++) {
-                    hh = mfma32(wf[ks & 3], dfr[ks], hh, F16{});
-                    if (ks + 4 < KST)
-                        wf[ks & 3] = ld16(slot, (ks + 4) * 1024);
+                    hh = mfma32(wf[ks % WIN], dfr[ks], hh, F16{});
+                    if (ks + WIN < KST)
+                        wf[ks % WIN] = ld16(f1, (ks + WIN) * 32);
                 }
-                __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);
+                __builtin_amdgcn_sched_group_barrier(0x100, WIN, 1);
 #pragma unroll
-                for (int ks = 0; ks + 4 < KST; ks++) {
+                for (int ks = 0; ks + WIN < KST; ks++) {
                     __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
                     __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
                 }
-                __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);
+                __builtin_amdgcn_sched_group_barrier(0x008, WIN, 1);
                 const float16v s1v = *reinterpret_cast<const float16v *>(smem + a.off_s1 + c * 128 + h * 64);
                 const float16v b1v = *reinterpret_cast<const float16v *>(smem + a.off_b1 + c * 128 + h * 64);
                 float v[16];
@@ -660,22 +728,27 @@ struct Ks {
                 K::template activate<8>(v, o);
                 const u32x4 hid[2] = {u32x4{o[0], o[1], o[2], o[3]}, u32x4{o[4], o[5], o[6], o[7]}};
                 // project: MFMA i -> K step kk = i / CB, output block i % CB
+                // W2 fragment (cb, kk) of MFMA i: cb = i % CB, kk = i / CB
+                auto w2off = [](int i) {
+                    const int cb = i % CB, kk = i / CB;
+                    return (uint32_t)((cb >> 2) * 8 * PITCH + (cb & 3) * 256 + kk * 32);
+                };
 #pragma unroll
-                for (int i = 0; i < 4; i++)
-                    wf[i] = ld16(slot, (KST + 2 * (i % CB) + i / CB) * 1024);
+                for (int i = 0; i < WIN; i++)
+                    wf[i] = ld16(f2, w2off(i));
 #pragma unroll
                 for (int i = 0; i < 2 * CB; i++) {
-                    acc[i % CB] = mfma32(wf[i & 3], hid[i / CB], acc[i % CB], F16{});
-                    if (i + 4 < 2 * CB)
-                        wf[i & 3] = ld16(slot, (KST + 2 * ((i + 4) % CB) + (i + 4) / CB) * 1024);
+                    acc[i % CB] = mfma32(wf[i % WIN], hid[i / CB], acc[i % CB], F16{});
+                    if (i + WIN < 2 * CB)
+                        wf[i % WIN] = ld16(f2, w2off(i + WIN));
                 }
-                __builtin_amdgcn_sched_group_barrier(0x100, 4, 2);
+                __builtin_amdgcn_sched_group_barrier(0x100, WIN, 2);
 #pragma unroll
-                for (int i = 0; i + 4 < 2 * CB; i++) {
+                for (int i = 0; i + WIN < 2 * CB; i++) {
                     __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
                     __builtin_amdgcn_sched_group_barrier(0x100, 1, 2);
                 }
-                __builtin_amdgcn_sched_group_barrier(0x008, 4, 2);
+                __builtin_amdgcn_sched_group_barrier(0x008, WIN, 2);
             }
             __syncthreads();  // the ring is free for the next tile
 
@@ -716,10 +789,10 @@ struct Ks {
     }
 };
 
-template <int KS, int ACT>
+template <int C, int KS, int ACT>
 __global__ __launch_bounds__(256, 1) void solo_kernel(SoloArgs sa) {
     extern __shared__ __attribute__((aligned(256))) uint8_t smem[];
-    Ks<KS, ACT>::run(sa, smem);
+    Ks<C, KS, ACT>::run(sa, smem);
 }
 
 template <int C, int KS, int ACT>
@@ -801,10 +874,9 @@ hipError_t launch_c(const void *x, void *y, const BlockW &w, const Shape &s, hip
 
 // C = 512 launcher.  groups > 1 requires `partial` ([groups][P][C] fp32); the
 // caller then runs the ordered reduction.
-template <int KS>
+template <int C, int KS>
 hipError_t launch_solo(const void *x, void *y, const BlockW &w, const Shape &s, int groups, float *partial,
                        hipStream_t st) {
-    constexpr int C = 512;
     const int pad = KS / 2;
     const int nch = s.E * C / 32;
     if (groups < 1 || nch % groups)
@@ -822,7 +894,7 @@ hipError_t launch_solo(const void *x, void *y, const BlockW &w, const Shape &s, 
     L.big = (L.s2b2 + C * 8 + 255) & ~255u;
     L.d = L.big + (((uint32_t)halo_rows * rsl + 255) & ~255u);
     const uint32_t hd = (L.d - L.big) + NBLK * 32 * DPX;
-    const uint32_t ring = 2u * Ks<KS, ACT_NONE>::SLOT;
+    const uint32_t ring = 2u * Ks<C, KS, ACT_NONE>::SLOT;
     L.zero = L.big + (hd > ring ? hd : ring);
     L.total = L.zero + (uint32_t)KS * HPX + 64;
     if (L.total > 160 * 1024)
@@ -866,7 +938,7 @@ hipError_t launch_solo(const void *x, void *y, const BlockW &w, const Shape &s, 
     hipError_t e;
 #define CF_SOLO_LAUNCH(ACTV)                                                                                         \
     {                                                                                                                 \
-        auto kf = solo_kernel<KS, ACTV>;                                                                             \
+        auto kf = solo_kernel<C, KS, ACTV>;                                                                             \
         if ((e = hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L.total))) \
             return e;                                                                                                 \
         hipLaunchKernelGGL(kf, dim3(gx, groups), dim3(256), L.total, st, sa);                                       \
@@ -883,10 +955,10 @@ hipError_t launch_solo(const void *x, void *y, const BlockW &w, const Shape &s, 
 inline hipError_t launch_c512(const void *x, void *y, const BlockW &w, const Shape &s, int groups, float *partial,
                               hipStream_t st) {
     switch (s.k) {
-    case 1: return launch_solo<1>(x, y, w, s, groups, partial, st);
-    case 3: return launch_solo<3>(x, y, w, s, groups, partial, st);
-    case 5: return launch_solo<5>(x, y, w, s, groups, partial, st);
-    default: return launch_solo<7>(x, y, w, s, groups, partial, st);
+    case 1: return launch_solo<512, 1>(x, y, w, s, groups, partial, st);
+    case 3: return launch_solo<512, 3>(x, y, w, s, groups, partial, st);
+    case 5: return launch_solo<512, 5>(x, y, w, s, groups, partial, st);
+    default: return launch_solo<512, 7>(x, y, w, s, groups, partial, st);
     }
 }
 
