@@ -93,20 +93,31 @@ struct GemmArgs {
 constexpr int GK = 32;
 constexpr int LDS_STRIDE = 40;  // halves per LDS row (32 + 8 pad)
 
+// Start of A row p (its K = 0 element): for the space-to-depth view,
+// k = (a*2 + b)*Cin + c reads x[n][2i+a][2j+b][c], and row p = (n, i, j)
+// starts at x[n][2i][2j][0]; a K step of 32 never crosses a (a, b) boundary
+// (Cin is a multiple of 32), so a load is row start + tap offset + c.
 template <int AMODE>
-__device__ __forceinline__ const uint16_t *a_row_ptr(const GemmArgs &g, int64_t p, int k) {
+__device__ __forceinline__ const uint16_t *a_row_start(const GemmArgs &g, int64_t p) {
     if constexpr (AMODE == A_PLAIN) {
-        return g.a + p * g.K + k;
+        return g.a + p * g.K;
     } else {
-        // k = (a*2 + b)*Cin + c  ->  x[n][2i+a][2j+b][c]
-        const int j = (int)(p % g.Wo);
         const int64_t ni = p / g.Wo;
-        const int i = (int)(ni % g.Ho);
+        const int j = (int)(p - ni * g.Wo);
         const int64_t n = ni / g.Ho;
-        const int ab = k / g.Cin, c = k - ab * g.Cin;
-        const int aa = ab >> 1, bb = ab & 1;
+        const int i = (int)(ni - n * g.Ho);
         const int64_t W = 2 * (int64_t)g.Wo;
-        return g.a + (((n * 2 * g.Ho + 2 * i + aa) * W + 2 * j + bb) * g.Cin + c);
+        return g.a + ((n * 2 * g.Ho + 2 * i) * W + 2 * j) * g.Cin;
+    }
+}
+// offset of element k from the row start
+template <int AMODE>
+__device__ __forceinline__ int64_t a_col_off(const GemmArgs &g, int k) {
+    if constexpr (AMODE == A_PLAIN) {
+        return k;
+    } else {
+        const int ab = k / g.Cin, c = k - ab * g.Cin;
+        return ((int64_t)(ab >> 1) * 2 * g.Wo + (ab & 1)) * g.Cin + c;
     }
 }
 
@@ -131,15 +142,22 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
         for (int j = 0; j < FM; j++)
             acc[i][j] = float4v{0.f, 0.f, 0.f, 0.f};
 
+    // this thread's A rows, decomposed once
+    const uint16_t *arow[A_PIECES];
+    bool aok[A_PIECES];
+#pragma unroll
+    for (int q = 0; q < A_PIECES; q++) {
+        const int64_t p = p0 + (q * 256 + tid) / (GK / 8);
+        aok[q] = p < g.P;
+        arow[q] = a_row_start<AMODE>(g, aok[q] ? p : 0);
+    }
     u32x4 ra[A_PIECES], rbv[B_PIECES];
     auto load = [&](int k0) {
+        const int64_t koff = a_col_off<AMODE>(g, k0);
 #pragma unroll
         for (int q = 0; q < A_PIECES; q++) {
-            const int pc = q * 256 + tid;
-            const int r = pc / (GK / 8), c8 = pc % (GK / 8);
-            const int64_t p = p0 + r;
-            ra[q] = p < g.P ? *reinterpret_cast<const u32x4 *>(a_row_ptr<AMODE>(g, p, k0 + c8 * 8))
-                            : u32x4{0u, 0u, 0u, 0u};
+            const int c8 = (q * 256 + tid) % (GK / 8);
+            ra[q] = aok[q] ? *reinterpret_cast<const u32x4 *>(arow[q] + koff + c8 * 8) : u32x4{0u, 0u, 0u, 0u};
         }
 #pragma unroll
         for (int q = 0; q < B_PIECES; q++) {
