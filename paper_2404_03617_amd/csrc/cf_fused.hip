@@ -39,7 +39,18 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const uint16_t *x, ui
     const int64_t e = i * 4;
     const int c = (int)(e % C);
     float4v s = b2 ? *reinterpret_cast<const float4v *>(b2 + c) : float4v{0.f, 0.f, 0.f, 0.f};
-    for (int gi = 0; gi < groups; gi++)
+    // groups are added in increasing order; eight loads are issued at a time
+    int gi = 0;
+    for (; gi + 8 <= groups; gi += 8) {
+        float4v v[8];
+#pragma unroll
+        for (int u = 0; u < 8; u++)
+            v[u] = *reinterpret_cast<const float4v *>(partial + (size_t)(gi + u) * P * C + e);
+#pragma unroll
+        for (int u = 0; u < 8; u++)
+            s += v[u];
+    }
+    for (; gi < groups; gi++)
         s += *reinterpret_cast<const float4v *>(partial + (size_t)gi * P * C + e);
     const u32x2 xv = *reinterpret_cast<const u32x2 *>(x + e);
     u32x2 o;
@@ -97,7 +108,16 @@ hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Sha
     a.E = s.E;
     a.P = (uint32_t)((int64_t)s.N * s.H * s.W);
     hipError_t e;
-    if (s.C == 64 && !s.bf16 && groups <= 1) {
+    bool done = false;
+    if (groups > 1) {
+        e = launch_small_split(x, w, s, groups, partial, st);
+        if (e != hipErrorInvalidConfiguration) {
+            if (e != hipSuccess)
+                return e;
+            done = true;
+        }
+    }
+    if (!done && s.C == 64 && !s.bf16 && groups <= 1) {
         switch (s.k) {
         case 1: e = launch_block64_k1(x, y, w, s, st); break;
         case 3: e = launch_block64_k3(x, y, w, s, st); break;
@@ -107,13 +127,12 @@ hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Sha
         if (e != hipErrorInvalidConfiguration)
             return e;
     }
-    if ((s.C == 128 || s.C == 256) && !s.bf16 && groups <= 1) {
+    if (!done && (s.C == 128 || s.C == 256) && !s.bf16 && groups <= 1) {
         e = s.C == 128 ? launch_wide_c128(x, y, w, s, st) : launch_wide_c256(x, y, w, s, st);
         if (e != hipErrorInvalidConfiguration)
             return e;
     }
-    bool done = false;
-    if (s.C == 512 && !s.bf16) {
+    if (!done && s.C == 512 && !s.bf16) {
         e = launch_wide_c512(x, y, w, s, groups, partial, st);
         if (e != hipErrorInvalidConfiguration) {
             if (e != hipSuccess)

@@ -30,6 +30,12 @@ struct Shape {
 hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Shape &s,
                               int groups, float *partial, hipStream_t st);
 
+// Small-batch hidden-split path (at most 8 tiles of 128 pixels): writes the
+// groups' partials only (the caller runs the reduction).  Returns
+// hipErrorInvalidConfiguration when the shape does not suit it.
+hipError_t launch_small_split(const void *x, const BlockW &w, const Shape &s, int groups, float *partial,
+                              hipStream_t st);
+
 // Layer-by-layer path: depth-wise -> d, expand + act -> h, project + residual -> y.
 hipError_t launch_unfused_block(const void *x, void *y, void *d, void *h, const BlockW &w,
                                 const Shape &s, hipStream_t st);
