@@ -125,3 +125,59 @@ def test_downsample_rejects():
     assert call(p=cf._DownParams(w=None)) == cf.CF_ERR_INVALID
     assert call(y=X + 16) == cf.CF_ERR_INVALID
     assert call(dt=3) == cf.CF_ERR_INVALID
+
+
+def _sigma(m):
+    return 16 * (m >> 4) + 8 * ((m >> 2) & 1) + 4 * ((m >> 3) & 1) + (m & 3)
+
+
+def _tau(m):
+    return 16 * ((m >> 2) & 1) + 4 * (m >> 3) + (m & 3)
+
+
+def test_c512_dma_layouts_are_conflict_free():
+    """The C = 512 kernel's LDS weight layouts (restated from its DMA and
+    fragment-read address formulas): every DMA instruction fills one
+    contiguous KB at a 1040-byte pitch, every byte of the chunk has exactly one
+    place, and each 16-lane group of an A-fragment read hits 16 distinct
+    16-byte bank groups."""
+    PITCH, C = 1040, 512
+    assert sorted(_sigma(m) for m in range(32)) == list(range(32))
+    assert sorted(_tau(m) for m in range(32)) == list(range(32))
+    # W1: row r of the chunk (1 KB) is instruction r; fragment (ks, lane h, m) = row sigma(m), bytes 32 ks + 16 h
+    seen = set()
+    for r in range(32):
+        for b in range(0, 2 * C, 16):
+            a = r * PITCH + b
+            assert a not in seen
+            seen.add(a)
+    for ks in range(C // 16):
+        for h in range(2):
+            for grp in (range(16), range(16, 32)):
+                banks = {((_sigma(m) * PITCH + 32 * ks + 16 * h) // 16) % 16 for m in grp}
+                assert len(banks) == 16
+    # W2: instruction j = 8 * set + i; lane l -> slot l // 4 (block of the set slot // 4, row m = 4 i + slot % 4),
+    # 16-byte piece l % 4 of the row's 64 bytes
+    W2OFF = 32 * PITCH
+    where = {}
+    for j in range(32):
+        st, i = j >> 3, j & 7
+        for lane in range(64):
+            sl, pc = lane >> 2, lane & 3
+            o = (4 * st + (sl >> 2)) * 32 + _tau(4 * i + (sl & 3))
+            key = (o, pc)
+            assert key not in where
+            where[key] = W2OFF + j * PITCH + 16 * lane
+    assert len(where) == C * 4
+    for cb in range(C // 32):
+        for kk in range(2):
+            for h in range(2):
+                for grp in (range(16), range(16, 32)):
+                    addrs = []
+                    for m in grp:
+                        # the kernel's read address: per-lane base + (cb, kk) offset
+                        a = W2OFF + (m >> 2) * PITCH + (m & 3) * 64 + 16 * h + (cb >> 2) * 8 * PITCH + (cb & 3) * 256 + 32 * kk
+                        # it must be where the DMA put row cb*32 + tau(m), piece 2 kk + h
+                        assert a == where[(cb * 32 + _tau(m), 2 * kk + h)]
+                        addrs.append(a)
+                    assert len({(a // 16) % 16 for a in addrs}) == 16
