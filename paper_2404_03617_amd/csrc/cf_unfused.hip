@@ -69,10 +69,11 @@ __global__ __launch_bounds__(256) void dw_kernel(const uint16_t *x, uint16_t *d,
 }
 
 // ---------------------------------------------------------------------------
-// Tiled MFMA GEMM.  Block tile BM pixels x BN outputs x 32 K, 4 waves as
+// Tiled MFMA GEMM.  Block tile BM pixels x BN outputs x GK of K, 4 waves as
 // 2 x 2, each wave (BM/2) x (BN/2).  Operand tiles go global -> registers ->
-// LDS with a padded row stride (80 bytes) against bank conflicts, double
-// buffered over K.
+// LDS with a padded row stride against bank conflicts; LDS is double
+// buffered and the register copies run two K steps ahead, so two global
+// round trips are in flight while a step computes.
 enum { EPI_EXPAND = 0, EPI_PROJECT = 1, EPI_AFFINE = 2 };
 enum { A_PLAIN = 0, A_SPACE_TO_DEPTH = 1 };
 
@@ -90,13 +91,11 @@ struct GemmArgs {
     int Ho, Wo, Cin;
 };
 
-constexpr int GK = 32;
-constexpr int LDS_STRIDE = 40;  // halves per LDS row (32 + 8 pad)
 
 // Start of A row p (its K = 0 element): for the space-to-depth view,
 // k = (a*2 + b)*Cin + c reads x[n][2i+a][2j+b][c], and row p = (n, i, j)
-// starts at x[n][2i][2j][0]; a K step of 32 never crosses a (a, b) boundary
-// (Cin is a multiple of 32), so a load is row start + tap offset + c.
+// starts at x[n][2i][2j][0]; a K step of GK never crosses a (a, b) boundary
+// (Cin is a multiple of GK), so a load is row start + tap offset + c.
 template <int AMODE>
 __device__ __forceinline__ const uint16_t *a_row_start(const GemmArgs &g, int64_t p) {
     if constexpr (AMODE == A_PLAIN) {
@@ -121,8 +120,9 @@ __device__ __forceinline__ int64_t a_col_off(const GemmArgs &g, int k) {
     }
 }
 
-template <typename T, int BM, int BN, int EPI, int AMODE>
+template <typename T, int BM, int BN, int GK, int EPI, int AMODE>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
+    constexpr int LDS_STRIDE = GK + 8;  // halves per LDS row (8 halves of padding)
     constexpr int WM = BM / 2, WN = BN / 2;  // per-wave tile (pixels x outputs)
     constexpr int FM = WM / 16, FN = WN / 16;
     constexpr int A_PIECES = BM * GK / 8 / 256;  // 16-byte pieces per thread
@@ -182,28 +182,66 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     };
 
     const int nk = g.K / GK;
+    auto compute = [&](int buf) {
+#pragma unroll
+        for (int ks = 0; ks < GK / 32; ks++) {
+            u32x4 fa[FN], fb[FM];
+#pragma unroll
+            for (int i = 0; i < FN; i++)
+                fa[i] = *reinterpret_cast<const u32x4 *>(
+                    &sb[buf][(wn * WN + i * 16 + (lane & 15)) * LDS_STRIDE + 32 * ks + 8 * (lane >> 4)]);
+#pragma unroll
+            for (int j = 0; j < FM; j++)
+                fb[j] = *reinterpret_cast<const u32x4 *>(
+                    &sa[buf][(wm * WM + j * 16 + (lane & 15)) * LDS_STRIDE + 32 * ks + 8 * (lane >> 4)]);
+#pragma unroll
+            for (int i = 0; i < FN; i++)
+#pragma unroll
+                for (int j = 0; j < FM; j++)
+                    acc[i][j] = T::mfma(fa[i], fb[j], acc[i][j]);
+        }
+    };
+    // two register sets: set (kt & 1) holds K step kt + 2 once its loads land
+    u32x4 ra2[A_PIECES], rb2[B_PIECES];
     load(0);
     store(0);
+    if (nk > 1)
+        load(GK);
+#pragma unroll
+    for (int q = 0; q < A_PIECES; q++)
+        ra2[q] = ra[q];
+#pragma unroll
+    for (int q = 0; q < B_PIECES; q++)
+        rb2[q] = rbv[q];
+    // ra2/rb2: step 1 (if any); ra/rbv: free
     for (int kt = 0; kt < nk; kt++) {
         __syncthreads();
         const int buf = kt & 1;
-        const bool more = kt + 1 < nk;
-        if (more)
-            load((kt + 1) * GK);
-        u32x4 fa[FN], fb[FM];
+        if (kt + 2 < nk)
+            load((kt + 2) * GK);  // into ra/rbv
+        compute(buf);
+        if (kt + 1 < nk) {
+            // step kt + 1 (in ra2/rb2) goes to the other LDS buffer
 #pragma unroll
-        for (int i = 0; i < FN; i++)
-            fa[i] = *reinterpret_cast<const u32x4 *>(&sb[buf][(wn * WN + i * 16 + (lane & 15)) * LDS_STRIDE + 8 * (lane >> 4)]);
+            for (int q = 0; q < A_PIECES; q++) {
+                const int pc = q * 256 + tid;
+                const int r = pc / (GK / 8), c8 = pc % (GK / 8);
+                *reinterpret_cast<u32x4 *>(&sa[buf ^ 1][r * LDS_STRIDE + c8 * 8]) = ra2[q];
+            }
 #pragma unroll
-        for (int j = 0; j < FM; j++)
-            fb[j] = *reinterpret_cast<const u32x4 *>(&sa[buf][(wm * WM + j * 16 + (lane & 15)) * LDS_STRIDE + 8 * (lane >> 4)]);
+            for (int q = 0; q < B_PIECES; q++) {
+                const int pc = q * 256 + tid;
+                const int r = pc / (GK / 8), c8 = pc % (GK / 8);
+                *reinterpret_cast<u32x4 *>(&sb[buf ^ 1][r * LDS_STRIDE + c8 * 8]) = rb2[q];
+            }
+        }
+        // the loads of step kt + 2 become the next step's pending set
 #pragma unroll
-        for (int i = 0; i < FN; i++)
+        for (int q = 0; q < A_PIECES; q++)
+            ra2[q] = ra[q];
 #pragma unroll
-            for (int j = 0; j < FM; j++)
-                acc[i][j] = T::mfma(fa[i], fb[j], acc[i][j]);
-        if (more)
-            store(buf ^ 1);
+        for (int q = 0; q < B_PIECES; q++)
+            rb2[q] = rbv[q];
     }
 
     // epilogue: lane holds outputs o0 + wn*WN + i*16 + 4*(lane>>4) + e, pixel p0 + wm*WM + j*16 + (lane&15)
@@ -245,17 +283,30 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     }
 }
 
-template <typename T, int EPI, int AMODE>
-hipError_t gemm(const GemmArgs &g, hipStream_t st) {
-    // BN must divide NO; all NO used here are multiples of 64.
-    if (g.NO % 128 == 0) {
+template <typename T, int GK, int EPI, int AMODE>
+hipError_t gemm_k(const GemmArgs &g, hipStream_t st) {
+    // BN must divide NO; all NO used here are multiples of 64.  Where 128 x 128
+    // tiles would leave compute units short of work, 64-pixel tiles (the
+    // small weight operand is re-read, not the activations).
+    const int64_t tiles128 = ((g.P + 127) / 128) * (g.NO / 128);
+    if (g.NO % 128 == 0 && tiles128 >= 2 * device_cu_count()) {
         dim3 grid((unsigned)((g.P + 127) / 128), g.NO / 128);
-        hipLaunchKernelGGL((gemm_kernel<T, 128, 128, EPI, AMODE>), grid, dim3(256), 0, st, g);
+        hipLaunchKernelGGL((gemm_kernel<T, 128, 128, GK, EPI, AMODE>), grid, dim3(256), 0, st, g);
+    } else if (g.NO % 128 == 0) {
+        dim3 grid((unsigned)((g.P + 63) / 64), g.NO / 128);
+        hipLaunchKernelGGL((gemm_kernel<T, 64, 128, GK, EPI, AMODE>), grid, dim3(256), 0, st, g);
     } else {
         dim3 grid((unsigned)((g.P + 127) / 128), g.NO / 64);
-        hipLaunchKernelGGL((gemm_kernel<T, 128, 64, EPI, AMODE>), grid, dim3(256), 0, st, g);
+        hipLaunchKernelGGL((gemm_kernel<T, 128, 64, GK, EPI, AMODE>), grid, dim3(256), 0, st, g);
     }
     return hipGetLastError();
+}
+
+template <typename T, int EPI, int AMODE>
+hipError_t gemm(const GemmArgs &g, hipStream_t st) {
+    // K steps of 64 where K (and, for the space-to-depth view, Cin) allow it
+    const bool k64 = g.K % 64 == 0 && (AMODE == A_PLAIN || g.Cin % 64 == 0);
+    return k64 ? gemm_k<T, 64, EPI, AMODE>(g, st) : gemm_k<T, 32, EPI, AMODE>(g, st);
 }
 
 template <typename T>
