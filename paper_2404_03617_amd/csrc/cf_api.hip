@@ -335,7 +335,8 @@ cf_status cf_block_forward_split(const void *x, void *y, void *ws, size_t ws_byt
     if (overlap(ws, need, x, bytes) || overlap(ws, need, y, bytes))
         return fail(CF_ERR_INVALID, "%s: ws overlaps x or y", what);
     const cf::Shape s = to_shape(N, H, W, C, E, k, dt, act);
-    if ((st = check_fit(what, s)) != CF_OK)
+    const size_t small_lds = cf::small_split_lds_bytes(s);
+    if (!(small_lds > 0 && small_lds <= 160 * 1024) && (st = check_fit(what, s)) != CF_OK)
         return st;
     hipError_t e = cf::launch_fused_block(x, y, to_w(p), s, groups, (float *)ws, (hipStream_t)stream);
     if (e != hipSuccess)

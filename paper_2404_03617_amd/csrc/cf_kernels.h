@@ -36,6 +36,8 @@ hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Sha
 hipError_t launch_small_split(const void *x, const BlockW &w, const Shape &s, int groups, float *partial,
                               hipStream_t st);
 
+size_t small_split_lds_bytes(const Shape &s);  // 0: the small-batch path does not apply
+
 // Layer-by-layer path: depth-wise -> d, expand + act -> h, project + residual -> y.
 hipError_t launch_unfused_block(const void *x, void *y, void *d, void *h, const BlockW &w,
                                 const Shape &s, hipStream_t st);

@@ -6,7 +6,8 @@
 // Grid: (tiles of at most TP pixels, hidden groups, output slices of 128).  One
 // workgroup of 4 waves:
 //  1. copies the input rows of its tile plus the k/2 halo rows into LDS
-//     (zero-filled padding, all loads in flight before the first LDS write),
+//     (in-image columns only; rows outside the batch are zero-filled; all
+//     loads in flight before the first LDS write),
 //  2. computes the depth-wise conv with one thread per (pixel, 8 channels)
 //     into an LDS D buffer, d = s0 * conv + b0,
 //  3. wave w takes pixels 32w .. 32w+31 of the tile: it reads its D columns
@@ -65,7 +66,7 @@ struct Kern {
         uint32_t pend = p0 + (uint32_t)a.tp;
         if (pend > a.P)
             pend = a.P;
-        const int WP = a.W + 2 * PAD;
+        const int WP = a.W;  // LDS columns: the image's own (taps outside it are skipped)
         const uint32_t g_lo = p0 / (uint32_t)a.W;  // first image row (over N*H) of the tile
         const int rows = a.halo_rows;
         const int ob = blockIdx.z;  // output half
@@ -110,7 +111,7 @@ struct Kern {
                     const int ci = c0 + u * NT + tid;
                     const int r = ci / (WP * C8), rem = ci - r * (WP * C8);
                     const int col = rem / C8, q = rem - col * C8;
-                    const int px = col - PAD, grow = (int)g_lo - PAD + r;
+                    const int px = col, grow = (int)g_lo - PAD + r;
                     dst[u] = ci < total ? (r * WP + col) * PIXB + q * 16 : -1;
                     v[u] = u32x4{0u, 0u, 0u, 0u};
                     if (ci < total && px >= 0 && px < a.W && grow >= 0 && grow < a.NH)
@@ -157,8 +158,11 @@ struct Kern {
                         const int r = (int)(gg - g_lo) + i;
 #pragma unroll
                         for (int j = 0; j < KS; j++) {
+                            const int wj = wc + j - PAD;
+                            if (wj < 0 || wj >= a.W)
+                                continue;  // zero padding
                             Pack8 xv;
-                            xv.u = *reinterpret_cast<const u32x4 *>(smem + (r * WP + wc + j) * PIXB + q * 16);
+                            xv.u = *reinterpret_cast<const u32x4 *>(smem + (r * WP + wj) * PIXB + q * 16);
 #pragma unroll
                             for (int e = 0; e < 4; e++) {
                                 acc[2 * e] = fmaf(T::lo(xv.w[e]), T::lo(wt[i * KS + j].w[e]), acc[2 * e]);
@@ -293,6 +297,21 @@ hipError_t launch_t(Args a, int k, int tiles, int groups, size_t lds, hipStream_
 
 }  // namespace small
 
+// LDS bytes the small-batch kernel needs for this shape, 0 if it does not apply.
+size_t small_split_lds_bytes(const Shape &s) {
+    const int64_t P = (int64_t)s.N * s.H * s.W;
+    const int tp = P < small::TPMAX ? (int)P : small::TPMAX;
+    const int64_t tiles = (P + tp - 1) / tp;
+    if (tiles > 8 || (s.C != 64 && s.C != 128 && s.C != 256 && s.C != 512))
+        return 0;
+    int64_t span = (int64_t)(tp - 1) / s.W + 2;
+    if (span > (int64_t)s.N * s.H)
+        span = (int64_t)s.N * s.H;
+    const size_t pixb = (size_t)s.C * 2 + 16;
+    const size_t off_d = (((size_t)(span + 2 * (s.k / 2)) * s.W * pixb) + 255) & ~(size_t)255;
+    return off_d + (size_t)tp * pixb;
+}
+
 // Small-batch hidden-split path: partial[g][P][C] = s2 * (W2 phi(s1 W1 D + b1))
 // restricted to the chunks of group g.  Returns hipErrorInvalidConfiguration
 // when the shape does not suit it (more than 8 tiles of 128 pixels, or a tile
@@ -311,7 +330,7 @@ hipError_t launch_small_split(const void *x, const BlockW &w, const Shape &s, in
         span = (int64_t)s.N * s.H;
     const int halo_rows = (int)span + 2 * pad;
     const size_t pixb = (size_t)s.C * 2 + 16;
-    const size_t off_d = (((size_t)halo_rows * (s.W + 2 * pad) * pixb) + 255) & ~(size_t)255;
+    const size_t off_d = (((size_t)halo_rows * s.W * pixb) + 255) & ~(size_t)255;
     const size_t lds = off_d + (size_t)tp * pixb;
     if (lds > 160 * 1024)
         return hipErrorInvalidConfiguration;

@@ -87,6 +87,28 @@ def test_unfused_and_split_match_oracle(case, dtype):
         assert_close(cf.block_forward_split(xd, pd, groups=groups), ref, what="split g=%d" % groups)
 
 
+# The small-batch split kernel: several tiles of 128 pixels (up to its limit
+# of 8), pixel counts that are not multiples of 32, odd widths, every k.
+@pytest.mark.parametrize("case", [
+    # C, E, k, N, H, W, groups, dtype
+    (64, 4, 3, 4, 16, 16, 4, "f16"),     # 1024 pixels: 8 tiles
+    (64, 2, 7, 3, 5, 11, 2, "bf16"),     # 165 pixels, k = 7 on a 5-row image
+    (128, 4, 5, 2, 9, 7, 8, "f16"),
+    (256, 1, 1, 1, 3, 13, 8, "bf16"),
+    (256, 4, 7, 2, 14, 14, 16, "f16"),
+    (512, 4, 7, 1, 7, 7, 32, "bf16"),
+    (512, 2, 5, 2, 6, 5, 4, "f16"),
+], ids=lambda c: "C%d_E%d_k%d_N%d_%dx%d_g%d_%s" % c)
+def test_small_batch_split_matches_oracle(case):
+    C, E, k, N, H, W, groups, dtype = case
+    say("small split", case)
+    x, p = make_block(31, N, H, W, C, E, k, dtype)
+    y = cf.block_forward_split(x.cuda(), to_dev(p), groups=groups)
+    torch.cuda.synchronize()
+    ref = oracle_block(x, p)
+    assert_close(y.cpu(), ref, what="split %s" % (case,))
+
+
 def test_default_scales_and_no_biases():
     """NULL scales (ones) and NULL biases (zeros) take the same path as explicit ones."""
     say("null scales")
