@@ -304,9 +304,20 @@ hipError_t gemm_k(const GemmArgs &g, hipStream_t st) {
 
 template <typename T, int EPI, int AMODE>
 hipError_t gemm(const GemmArgs &g, hipStream_t st) {
-    // K steps of 64 where K (and, for the space-to-depth view, Cin) allow it
-    const bool k64 = g.K % 64 == 0 && (AMODE == A_PLAIN || g.Cin % 64 == 0);
-    return k64 ? gemm_k<T, 64, EPI, AMODE>(g, st) : gemm_k<T, 32, EPI, AMODE>(g, st);
+    if constexpr (AMODE == A_PLAIN) {
+        // layer-by-layer GEMMs (large P): 128-pixel tiles, K steps of 32
+        if (g.NO % 128 == 0) {
+            dim3 grid((unsigned)((g.P + 127) / 128), g.NO / 128);
+            hipLaunchKernelGGL((gemm_kernel<T, 128, 128, 32, EPI, AMODE>), grid, dim3(256), 0, st, g);
+        } else {
+            dim3 grid((unsigned)((g.P + 127) / 128), g.NO / 64);
+            hipLaunchKernelGGL((gemm_kernel<T, 128, 64, 32, EPI, AMODE>), grid, dim3(256), 0, st, g);
+        }
+        return hipGetLastError();
+    } else {
+        // down-sampling: K steps of 64 where Cin allows it
+        return g.Cin % 64 == 0 ? gemm_k<T, 64, EPI, AMODE>(g, st) : gemm_k<T, 32, EPI, AMODE>(g, st);
+    }
 }
 
 template <typename T>
