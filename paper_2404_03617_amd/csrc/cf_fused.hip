@@ -14,9 +14,10 @@
 //                                     hidden groups (fp32 partials + reduction)
 //   bf16, other shapes  cf_fused_impl.h
 //
-// Hidden-split mode (grid.y > 1): workgroup (tile, g) runs only its range of
+// Hidden-split mode (groups > 1): workgroup (tile, g) runs only its range of
 // chunks and writes an fp32 partial of the projected output; split_reduce_kernel
-// adds the partials in group order plus b2 and the residual.
+// adds the partials in group order plus b2 and the residual.  Batches of at
+// most 8 tiles of 128 pixels use the small-batch kernel of cf_small.hip.
 #include "cf_block64.h"
 #include "cf_wide.h"
 #include "cf_fused_impl.h"
