@@ -139,6 +139,23 @@ cf_status cf_block_forward_split(const void *x, void *y, void *ws, size_t ws_byt
 size_t cf_split_workspace_bytes(int N, int H, int W, int C, int E, int groups);
 
 /* Thread-local message describing the most recent non-CF_OK status. */
+/* Autotune (Sec. 5.5: the kernel class enumerates the valid kernel
+ * configurations for the block's parameters, runs each, keeps the fastest).
+ * Same arguments and validation as cf_block_forward.  Synchronous: runs every
+ * configuration that applies to the shape on `stream` (a few launches each,
+ * timed with events), stores the fastest in a per-process cache keyed by
+ * (device, N, H, W, C, E, k, dtype, act), and leaves y holding the block's
+ * output computed with it.  Later cf_block_forward calls with that key use the
+ * cached configuration.  The cache is guarded by a mutex; results of every
+ * configuration agree within the parity tolerance (they differ only in tiling
+ * and in which kernel implements the block). */
+cf_status cf_block_autotune(const void *x, void *y, const cf_block_params *p,
+                            int N, int H, int W, int C, int E, int k,
+                            cf_dtype dt, cf_act act, void *stream);
+/* The cached configuration id for a key (0 = default kernel and tiling), or -1
+ * for invalid arguments. */
+int cf_block_tuned_config(int N, int H, int W, int C, int E, int k, cf_dtype dt, cf_act act);
+
 const char *cf_last_error(void);
 const char *cf_status_string(cf_status s);
 int cf_abi_version(void);

@@ -18,7 +18,8 @@ import os
 import torch
 
 __all__ = [
-    "lib", "library_path", "block_forward", "stage_forward", "downsample_forward",
+    "lib", "library_path", "block_forward", "block_autotune", "block_tuned_config", "stage_forward",
+    "downsample_forward",
     "block_forward_unfused", "block_forward_split", "stack_forward", "ConvFirstBlock",
     "CFError", "EXPORTED_SYMBOLS",
 ]
@@ -33,7 +34,8 @@ ACTS = {"gelu": 0, "relu": 1, "none": 2}
 EXPORTED_SYMBOLS = (
     "cf_block_forward", "cf_stage_forward", "cf_stage_workspace_bytes", "cf_downsample_forward",
     "cf_block_forward_unfused", "cf_unfused_workspace_bytes", "cf_block_forward_split",
-    "cf_split_workspace_bytes", "cf_last_error", "cf_status_string", "cf_abi_version",
+    "cf_split_workspace_bytes", "cf_block_autotune", "cf_block_tuned_config", "cf_last_error",
+    "cf_status_string", "cf_abi_version",
 )
 
 
@@ -78,6 +80,8 @@ def lib():
             "cf_unfused_workspace_bytes": (sz, [i, i, i, i, i, i]),
             "cf_block_forward_split": (i, [vp, vp, vp, sz, bp, i, i, i, i, i, i, i, i, i, vp]),
             "cf_split_workspace_bytes": (sz, [i, i, i, i, i, i]),
+            "cf_block_autotune": (i, [vp, vp, bp, i, i, i, i, i, i, i, i, vp]),
+            "cf_block_tuned_config": (i, [i, i, i, i, i, i, i, i]),
             "cf_last_error": (ctypes.c_char_p, []),
             "cf_status_string": (ctypes.c_char_p, [i]),
             "cf_abi_version": (i, []),
@@ -150,6 +154,25 @@ def block_forward(x: torch.Tensor, p: dict, act: str = "gelu", out: torch.Tensor
     _check(lib().cf_block_forward(_ptr(x), _ptr(y), ctypes.byref(bp), N, H, W, C, E, k,
                                   DTYPES[x.dtype], ACTS[act], _stream(stream)))
     return y
+
+
+def block_autotune(x: torch.Tensor, p: dict, act: str = "gelu", out: torch.Tensor | None = None,
+                   stream=None) -> torch.Tensor:
+    """Time every kernel configuration that applies to this block shape, cache
+    the fastest for later block_forward calls, return the block's output."""
+    N, H, W, C, E, k = _block_shape(x, p)
+    y = torch.empty_like(x) if out is None else out
+    keep = []
+    bp = _block_struct(p, keep)
+    _check(lib().cf_block_autotune(_ptr(x), _ptr(y), ctypes.byref(bp), N, H, W, C, E, k,
+                                   DTYPES[x.dtype], ACTS[act], _stream(stream)))
+    return y
+
+
+def block_tuned_config(x_shape, C: int, E: int, k: int, dtype=torch.float16, act: str = "gelu") -> int:
+    """Cached configuration id for a block shape (0: default kernel and tiling)."""
+    N, H, W = x_shape[0], x_shape[1], x_shape[2]
+    return lib().cf_block_tuned_config(N, H, W, C, E, k, DTYPES[dtype], ACTS[act])
 
 
 def stage_forward(x: torch.Tensor, blocks: list, act: str = "gelu", out=None, ws=None,

@@ -11,6 +11,9 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <map>
+#include <mutex>
+
 namespace {
 
 thread_local char g_err[512] = "";
@@ -109,6 +112,33 @@ cf_status check_fit(const char *what, const cf::Shape &s) {
 
 size_t round256(size_t v) { return (v + 255) & ~(size_t)255; }
 
+// ---- autotune cache: (device, shape, dtype, activation) -> kernel configuration
+struct TuneKey {
+    int dev, N, H, W, C, E, k, bf16, act;
+    bool operator<(const TuneKey &o) const {
+        const int a[9] = {dev, N, H, W, C, E, k, bf16, act};
+        const int b[9] = {o.dev, o.N, o.H, o.W, o.C, o.E, o.k, o.bf16, o.act};
+        for (int i = 0; i < 9; i++)
+            if (a[i] != b[i])
+                return a[i] < b[i];
+        return false;
+    }
+};
+std::mutex g_tune_mu;
+std::map<TuneKey, int> g_tune;
+
+TuneKey tune_key(const cf::Shape &s) {
+    int dev = 0;
+    (void)hipGetDevice(&dev);
+    return TuneKey{dev, s.N, s.H, s.W, s.C, s.E, s.k, s.bf16, s.act};
+}
+
+int tuned_config(const cf::Shape &s) {
+    std::lock_guard<std::mutex> lk(g_tune_mu);
+    const auto it = g_tune.find(tune_key(s));
+    return it == g_tune.end() ? cf::CFG_DEFAULT : it->second;
+}
+
 int default_groups(int N, int H, int W, int C, int E) {
     // enough (tile, group) pairs to give every CU one, with groups | E*C/32
     const int chunks = E * C / 32;
@@ -149,9 +179,10 @@ cf_status cf_block_forward(const void *x, void *y, const cf_block_params *p, int
     cf_status st = check_block("cf_block_forward", x, y, p, N, H, W, C, E, k, dt, act);
     if (st != CF_OK)
         return st;
-    const cf::Shape s = to_shape(N, H, W, C, E, k, dt, act);
+    cf::Shape s = to_shape(N, H, W, C, E, k, dt, act);
     if ((st = check_fit("cf_block_forward", s)) != CF_OK)
         return st;
+    s.cfg = tuned_config(s);
     hipError_t e = cf::launch_fused_block(x, y, to_w(p), s, 1, nullptr, (hipStream_t)stream);
     if (e != hipSuccess)
         return hip_fail(e, "cf_block_forward");
@@ -343,6 +374,70 @@ cf_status cf_block_forward_split(const void *x, void *y, void *ws, size_t ws_byt
         return hip_fail(e, what);
     g_err[0] = 0;
     return CF_OK;
+}
+
+cf_status cf_block_autotune(const void *x, void *y, const cf_block_params *p, int N, int H, int W, int C, int E,
+                            int k, cf_dtype dt, cf_act act, void *stream) {
+    const char *what = "cf_block_autotune";
+    cf_status st = check_block(what, x, y, p, N, H, W, C, E, k, dt, act);
+    if (st != CF_OK)
+        return st;
+    cf::Shape s = to_shape(N, H, W, C, E, k, dt, act);
+    if ((st = check_fit(what, s)) != CF_OK)
+        return st;
+    hipStream_t strm = (hipStream_t)stream;
+    hipEvent_t e0, e1;
+    hipError_t e;
+    if ((e = hipEventCreate(&e0)) != hipSuccess)
+        return hip_fail(e, what);
+    if ((e = hipEventCreate(&e1)) != hipSuccess) {
+        (void)hipEventDestroy(e0);
+        return hip_fail(e, what);
+    }
+    int best = cf::CFG_DEFAULT;
+    float best_ms = 0.0f;
+    for (int cfg = 0; cfg < cf::CFG_COUNT; cfg++) {
+        s.cfg = cfg;
+        if (!cf::cfg_applies(s, cfg))
+            continue;
+        // one untimed launch, then three timed ones
+        if ((e = cf::launch_fused_block(x, y, to_w(p), s, 1, nullptr, strm)) != hipSuccess)
+            break;
+        (void)hipEventRecord(e0, strm);
+        for (int r = 0; r < 3 && e == hipSuccess; r++)
+            e = cf::launch_fused_block(x, y, to_w(p), s, 1, nullptr, strm);
+        (void)hipEventRecord(e1, strm);
+        if (e != hipSuccess || (e = hipEventSynchronize(e1)) != hipSuccess)
+            break;
+        float ms = 0.0f;
+        (void)hipEventElapsedTime(&ms, e0, e1);
+        if (cfg == cf::CFG_DEFAULT || ms < best_ms) {
+            best = cfg;
+            best_ms = ms;
+        }
+    }
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    if (e != hipSuccess)
+        return hip_fail(e, what);
+    {
+        std::lock_guard<std::mutex> lk(g_tune_mu);
+        g_tune[tune_key(s)] = best;
+    }
+    // leave y holding the output of the chosen configuration
+    s.cfg = best;
+    if ((e = cf::launch_fused_block(x, y, to_w(p), s, 1, nullptr, strm)) != hipSuccess ||
+        (e = hipStreamSynchronize(strm)) != hipSuccess)
+        return hip_fail(e, what);
+    g_err[0] = 0;
+    return CF_OK;
+}
+
+int cf_block_tuned_config(int N, int H, int W, int C, int E, int k, cf_dtype dt, cf_act act) {
+    if (N <= 0 || H <= 0 || W <= 0 || C <= 0 || E <= 0 || k <= 0 || (dt != CF_F16 && dt != CF_BF16) ||
+        (act != CF_ACT_GELU_ERF && act != CF_ACT_RELU && act != CF_ACT_NONE))
+        return -1;
+    return tuned_config(to_shape(N, H, W, C, E, k, dt, act));
 }
 
 }  // extern "C"

@@ -672,8 +672,8 @@ __global__ __launch_bounds__(NT, 1) void block64_kernel(Args a) {
 // ---------------------------------------------------------------------------
 // Host side.  Returns hipErrorInvalidConfiguration when the shape needs the
 // generic kernel (W too wide for the fixed halo row, or LDS does not fit).
-inline bool plan(int N, int H, int W, int E, int k, int max_range, int &tb, int &halo_rows, uint32_t &rs,
-                 Layout &L) {
+inline bool plan(int N, int H, int W, int E, int k, int max_range, int tb_limit, int &tb, int &halo_rows,
+                 uint32_t &rs, Layout &L) {
     const int pad = k / 2;
     if (W + 2 * pad > 64 || E * C % 32 != 0 || E * C / 32 > 8)
         return false;
@@ -683,7 +683,7 @@ inline bool plan(int N, int H, int W, int E, int k, int max_range, int &tb, int 
     // the next tile's halo rows are copied one per FFN step (nch + 2 steps),
     // so a tile may touch at most nch + 2 rows, unless every workgroup has a
     // single tile (the first tile is copied whole)
-    for (tb = MAX_TB; tb >= 1; tb--) {
+    for (tb = tb_limit < MAX_TB ? tb_limit : MAX_TB; tb >= 1; tb--) {
         halo_rows = halo_rows_for(tb, k, W, NH);
         L = layout_for(nch, k, halo_rows, rs);
         if (L.total <= 160 * 1024 && (halo_rows <= nch + 2 || max_range <= tb))
@@ -702,7 +702,17 @@ hipError_t launch_k(const void *x, void *y, const BlockW &w, const Shape &s, hip
     int tb, halo_rows;
     uint32_t rs;
     Layout L;
-    if (!plan(s.N, s.H, s.W, s.E, KS, (nblocks + G - 1) / G, tb, halo_rows, rs, L))
+    int tb_limit = MAX_TB;
+    if (s.cfg == CFG_HALF_TILE) {
+        // half of the largest tile that fits
+        int tb0, hr0;
+        uint32_t rs0;
+        Layout L0;
+        if (!plan(s.N, s.H, s.W, s.E, KS, (nblocks + G - 1) / G, MAX_TB, tb0, hr0, rs0, L0))
+            return hipErrorInvalidConfiguration;
+        tb_limit = tb0 / 2 > 0 ? tb0 / 2 : 1;
+    }
+    if (!plan(s.N, s.H, s.W, s.E, KS, (nblocks + G - 1) / G, tb_limit, tb, halo_rows, rs, L))
         return hipErrorInvalidConfiguration;
     Args a{};
     a.x = (const uint16_t *)x;

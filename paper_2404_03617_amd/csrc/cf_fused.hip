@@ -118,7 +118,8 @@ hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Sha
             done = true;
         }
     }
-    if (!done && s.C == 64 && !s.bf16 && groups <= 1) {
+    const bool special = s.cfg != CFG_GENERIC;
+    if (!done && special && s.C == 64 && !s.bf16 && groups <= 1) {
         switch (s.k) {
         case 1: e = launch_block64_k1(x, y, w, s, st); break;
         case 3: e = launch_block64_k3(x, y, w, s, st); break;
@@ -128,12 +129,12 @@ hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Sha
         if (e != hipErrorInvalidConfiguration)
             return e;
     }
-    if (!done && (s.C == 128 || s.C == 256) && !s.bf16 && groups <= 1) {
+    if (!done && special && (s.C == 128 || s.C == 256) && !s.bf16 && groups <= 1) {
         e = s.C == 128 ? launch_wide_c128(x, y, w, s, st) : launch_wide_c256(x, y, w, s, st);
         if (e != hipErrorInvalidConfiguration)
             return e;
     }
-    if (!done && s.C == 512 && !s.bf16) {
+    if (!done && special && s.C == 512 && !s.bf16) {
         e = launch_wide_c512(x, y, w, s, groups, partial, st);
         if (e != hipErrorInvalidConfiguration) {
             if (e != hipSuccess)
@@ -165,6 +166,15 @@ hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Sha
         hipLaunchKernelGGL(split_reduce_kernel<F16>, dim3(nb), dim3(256), 0, st, a.x, a.y, partial, w.b2, a.P, s.C,
                            groups);
     return hipGetLastError();
+}
+
+bool cfg_applies(const Shape &s, int cfg) {
+    switch (cfg) {
+    case CFG_DEFAULT: return true;
+    case CFG_GENERIC: return fused_lds_bytes(s) > 0 && fused_lds_bytes(s) <= 160 * 1024;
+    case CFG_HALF_TILE: return s.C == 64 && !s.bf16;
+    default: return false;
+    }
 }
 
 }  // namespace cf

@@ -22,7 +22,18 @@ struct Shape {
     int N, H, W, C, E, k;
     int bf16;  // 0: fp16, 1: bf16
     int act;   // 0 GELU(erf), 1 ReLU, 2 identity
+    int cfg = 0;  // kernel configuration (CFG_*), chosen by the autotuner
 };
+
+// Kernel configurations of the fused block (the autotuner's candidates).
+enum {
+    CFG_DEFAULT = 0,     // the shape's specialised kernel, full-size tiles
+    CFG_GENERIC = 1,     // the generic fused kernel (cf_fused_impl.h)
+    CFG_HALF_TILE = 2,   // C = 64 fp16 kernel with tiles of at most half the blocks
+    CFG_COUNT = 3
+};
+// Whether configuration cfg applies to shape s.
+bool cfg_applies(const Shape &s, int cfg);
 
 // Fused block.  groups > 1 selects the hidden-split variant: partial (fp32,
 // [groups][N*H*W][C]) receives each group's projection and a reduction kernel

@@ -109,6 +109,24 @@ def test_small_batch_split_matches_oracle(case):
     assert_close(y.cpu(), ref, what="split %s" % (case,))
 
 
+@pytest.mark.parametrize("case", [(64, 4, 3, 4, 28, 28, "f16"), (128, 4, 3, 2, 14, 14, "f16"),
+                                  (256, 2, 5, 2, 7, 9, "bf16")], ids=lambda c: "C%d_E%d_k%d_N%d_%dx%d_%s" % c)
+def test_autotune_caches_a_configuration_that_matches_the_oracle(case):
+    C, E, k, N, H, W, dtype = case
+    say("autotune", case)
+    x, p = make_block(41, N, H, W, C, E, k, dtype)
+    xd, pd = x.cuda(), to_dev(p)
+    y = cf.block_autotune(xd, pd)
+    torch.cuda.synchronize()
+    ref = oracle_block(x, p)
+    assert_close(y.cpu(), ref, what="autotune %s" % (case,))
+    cfg = cf.block_tuned_config(x.shape, C, E, k, x.dtype)
+    assert cfg >= 0
+    y2 = cf.block_forward(xd, pd)  # uses the cached configuration
+    torch.cuda.synchronize()
+    assert_close(y2.cpu(), ref, what="tuned forward %s" % (case,))
+
+
 def test_default_scales_and_no_biases():
     """NULL scales (ones) and NULL biases (zeros) take the same path as explicit ones."""
     say("null scales")
