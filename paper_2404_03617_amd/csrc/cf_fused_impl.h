@@ -124,10 +124,52 @@ __device__ __forceinline__ void wait_vmcnt_le(int n) {
 }
 
 // One wave-wide 16-byte global->LDS copy: lane l's 16 bytes land at
-// lds_wave_base + 16 * l.
+// lds_wave_base + 16 * l (a wave-uniform LDS address).  Issued as inline
+// assembly: the compiler's wait-count pass cannot tell which LDS bytes a
+// pending copy writes, so for its own builtin it waits for every outstanding
+// copy (vmcnt 0) before each later LDS read, and a prefetch becomes a
+// synchronous copy.  The pass does not see these copies; every caller waits
+// for them itself (s_waitcnt vmcnt) before the destination is read or
+// published by a barrier.  Vector-memory operations of a wave complete in
+// issue order, so a wait the compiler places for one of its own loads stays
+// correct (it can only wait longer).  M0, which holds the LDS address of the
+// copy, is restored afterwards.
 __device__ __forceinline__ void dma16(const void *src, uint8_t *lds_wave_base) {
-    __builtin_amdgcn_global_load_lds((__attribute__((address_space(1))) void *)src,
-                                     (__attribute__((address_space(3))) void *)lds_wave_base, 16, 0, 0);
+    const uint32_t lds = (uint32_t)__builtin_amdgcn_readfirstlane(
+        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds_wave_base);
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, off\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(src), "s"(lds)
+        : "memory");
+}
+
+// The same copy from a wave-uniform base address (held in SGPRs) plus a
+// 32-bit per-lane byte offset, so that a wave keeps one VGPR per copy pattern
+// instead of a 64-bit address per copy.
+__device__ __forceinline__ void dma16s(const void *base, uint32_t voff, uint8_t *lds_wave_base) {
+    const uint32_t lds = (uint32_t)__builtin_amdgcn_readfirstlane(
+        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds_wave_base);
+    const uint64_t b = (uint64_t)(uintptr_t)base;
+    // (readfirstlane returns int: go through uint32_t so that neither half is sign-extended)
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+    const uint64_t bu = ((uint64_t)hi << 32) | (uint64_t)lo;
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %3\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, %2\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(voff), "s"(bu), "s"(lds)
+        : "memory");
 }
 
 __device__ __forceinline__ float16v mfma32(const u32x4 &a, const u32x4 &b, const float16v &c, F16) {

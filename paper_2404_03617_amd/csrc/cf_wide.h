@@ -210,25 +210,30 @@ struct Kw {
     static __device__ __forceinline__ uint8_t *buf_b(const Args &a, uint8_t *smem, int slot) {
         return smem + a.off_big + 2 * G::BUF_A + slot * G::BUF_B;
     }
+    // (the source of a copy is a wave-uniform base plus the lane's byte offset)
     static __device__ __forceinline__ void dma_a(const Args &a, uint8_t *smem, int step, int wv, int lane) {
         uint8_t *buf = buf_a(a, smem, step & 1);
-        const uint16_t *w1 = a.w1 + (size_t)step * 64 * C;  // wave-uniform
-        const uint32_t lo = (uint32_t)(sigma_row(lane & 31) * C + 8 * (lane >> 5));
+        const uint16_t *w1 = a.w1 + (size_t)step * 64 * C;
+        const uint32_t lo = (uint32_t)(sigma_row(lane & 31) * C + 8 * (lane >> 5)) * 2;
+        const int wu = __builtin_amdgcn_readfirstlane(wv);
 #pragma unroll
-        for (int f = wv; f < 2 * KST; f += NW) {
+        for (int i = 0; i < FA; i++) {
+            const int f = wu + NW * i;
             const int j = f / KST, ks = f % KST;
-            fused::dma16(w1 + (lo + (uint32_t)(j * 32 * C + ks * 16)), buf + f * 1024);
+            fused::dma16s(w1 + (j * 32 * C + ks * 16), lo, buf + f * 1024);
         }
     }
     static __device__ __forceinline__ void dma_b(const Args &a, uint8_t *smem, int step, int wv, int lane) {
         uint8_t *buf = buf_b(a, smem, step & 1);
-        const uint16_t *w2 = a.w2 + (size_t)step * 64;  // wave-uniform
+        const uint16_t *w2 = a.w2 + (size_t)step * 64;
         const uint32_t ec = (uint32_t)a.nch * 32;
-        const uint32_t lo = (uint32_t)tau_row(lane & 31) * ec + 8 * (lane >> 5);
+        const uint32_t lo = ((uint32_t)tau_row(lane & 31) * ec + 8 * (lane >> 5)) * 2;
+        const int wu = __builtin_amdgcn_readfirstlane(wv);
 #pragma unroll
-        for (int f = wv; f < 4 * CB; f += NW) {
+        for (int i = 0; i < FB; i++) {
+            const int f = wu + NW * i;
             const int j = f / (2 * CB), g = f % (2 * CB), cb = g >> 1, kk = g & 1;
-            fused::dma16(w2 + (lo + (uint32_t)(cb * 32) * ec + (uint32_t)(j * 32 + 16 * kk)), buf + f * 1024);
+            fused::dma16s(w2 + ((size_t)(cb * 32) * ec + (j * 32 + 16 * kk)), lo, buf + f * 1024);
         }
     }
 
@@ -602,36 +607,50 @@ struct Ks {
         return RPI == 1 ? (uint32_t)r * PITCH : (uint32_t)(r & 15) * PITCH + (uint32_t)(r >> 4) * (2 * C);
     }
 
-    // This wave's 1 KB pieces of a chunk: NPW copies, piece q -> (global
-    // source of the lane's 16 bytes, byte offset of the piece in the slot).
+    // This wave's 1 KB pieces of a chunk: NPW copies.  The source of a
+    // lane's 16 bytes in piece q is a wave-uniform base (piece_base) plus a
+    // per-lane byte offset that depends only on the kind of piece (lane_offs).
     static constexpr int NPW = (NI1 + NI2) / NWS;
-    static __device__ __forceinline__ void chunk_piece(const Args &a, int ch, int q, int wv, int lane,
-                                                       const uint16_t *&src, uint32_t &off) {
-        const uint32_t ec = (uint32_t)a.nch * 32;
+    struct LaneOffs {
+        uint32_t w1, w2;
+    };
+    static __device__ __forceinline__ LaneOffs lane_offs(const Args &a, int lane) {
+        LaneOffs o;
+        // W1: lane -> row 16 * (lane / 32) of the instruction's pair (C = 256), piece lane % (64 / RPI)
+        const int lr = RPI == 1 ? 0 : 16 * (lane >> 5), lp = RPI == 1 ? lane : (lane & 31);
+        o.w1 = (uint32_t)(lr * C + 8 * lp) * 2;
+        // W2: lane -> slot s = lane / 4 (block bq = s / 4 of the set, row m % 4 = s % 4), piece lane % 4;
+        // with m = 4 i + s % 4, tau(m) = 16 (i & 1) + 4 (i >> 1) + s % 4
+        const int sl = lane >> 2, bq = sl >> 2, r4 = sl & 3, pc = lane & 3;
+        o.w2 = ((uint32_t)(32 * bq + r4) * (uint32_t)(a.nch * 32) + 8 * pc) * 2;
+        return o;
+    }
+    static __device__ __forceinline__ void piece_base(const Args &a, int ch, int q, int wu, const uint16_t *&base,
+                                                      bool &w1, uint32_t &off) {
+        const size_t ec = (size_t)a.nch * 32;
         if (q < NI1 / NWS) {
-            // W1: lane -> row (instruction j) + 16 * (lane / 32) for C = 256, piece lane % (64 / RPI)
-            const int j = wv + NWS * q;
-            const int lr = RPI == 1 ? 0 : 16 * (lane >> 5), lp = RPI == 1 ? lane : (lane & 31);
-            src = a.w1 + ((size_t)ch * 32 + lr + j) * C + 8 * lp;
+            const int j = wu + NWS * q;  // instruction j: row j (and j + 16 for C = 256)
+            base = a.w1 + ((size_t)ch * 32 + j) * C;
+            w1 = true;
             off = (uint32_t)j * PITCH;
         } else {
-            // W2: lane -> slot s = lane / 4 (block of the set s / 4, row m = 4 i + s % 4), piece lane % 4
-            const int j = wv + NWS * (q - NI1 / NWS), st = j >> 3, i = j & 7;
-            const int sl = lane >> 2, bq = sl >> 2, r4 = sl & 3, pc = lane & 3;
-            const uint32_t o = (uint32_t)(4 * st + bq) * 32 + (uint32_t)tau_row(4 * i + r4);
-            src = a.w2 + (size_t)o * ec + (size_t)ch * 32 + 8 * pc;
+            const int j = wu + NWS * (q - NI1 / NWS), st = j >> 3, i = j & 7;
+            base = a.w2 + (size_t)(128 * st + 16 * (i & 1) + 4 * (i >> 1)) * ec + (size_t)ch * 32;
+            w1 = false;
             off = W2OFF + (uint32_t)j * PITCH;
         }
     }
     static __device__ __forceinline__ void dma_chunk(const Args &a, uint8_t *smem, int ch, int slot, int wv,
-                                                     int lane) {
+                                                     const LaneOffs &lo) {
         uint8_t *buf = smem + a.off_big + slot * SLOT;
+        const int wu = __builtin_amdgcn_readfirstlane(wv);
 #pragma unroll
         for (int q = 0; q < NPW; q++) {
-            const uint16_t *src;
+            const uint16_t *base;
+            bool w1;
             uint32_t off;
-            chunk_piece(a, ch, q, wv, lane, src, off);
-            fused::dma16(src, buf + off);
+            piece_base(a, ch, q, wu, base, w1, off);
+            fused::dma16s(base, w1 ? lo.w1 : lo.w2, buf + off);
         }
     }
     static __device__ void run(const SoloArgs &sa, uint8_t *smem) {
@@ -641,6 +660,7 @@ struct Ks {
         const int h = lane >> 5, m = lane & 31;
         const int grp = blockIdx.y;
         const int ch0 = grp * sa.chunks_per_group, nchg = sa.chunks_per_group;
+        const LaneOffs lofs = lane_offs(a, lane);
 
         for (uint32_t i = a.off_zero / 16 + tid; i < (a.off_zero + KS * HPX + 64) / 16; i += NTS)
             reinterpret_cast<u32x4 *>(smem)[i] = u32x4{0u, 0u, 0u, 0u};
@@ -686,13 +706,13 @@ struct Ks {
                 for (int e = 0; e < 16; e++)
                     acc[c][e] = 0.0f;
 
-            dma_chunk(a, smem, ch0, 0, wv, lane);
+            dma_chunk(a, smem, ch0, 0, wv, lofs);
 #pragma unroll 1
             for (int c = 0; c < nchg; c++) {
                 fused::wait_vmcnt<0>();  // this wave's copies of chunk c have landed
                 lds_barrier();           // everyone's have; the other slot is free
                 if (c + 1 < nchg)
-                    dma_chunk(a, smem, ch0 + c + 1, (c + 1) & 1, wv, lane);
+                    dma_chunk(a, smem, ch0 + c + 1, (c + 1) & 1, wv, lofs);
                 const uint8_t *slot = smem + a.off_big + (c & 1) * SLOT;
                 const uint8_t *f1 = slot + w1_row(sigma_row(m)) + h * 16;
                 const uint8_t *f2 = slot + W2OFF + (m >> 2) * PITCH + (m & 3) * 64 + h * 16;
