@@ -14,9 +14,10 @@
 //    waves 0-3 take two blocks (64 pixels) and waves 4-7 one block; waves w
 //    and w+4 share a SIMD, so every SIMD carries three blocks.
 //  * W1, W2 (with s1, s2 folded in) and b1 stay in LDS for the whole kernel.
-//  * The input tile plus halo is copied into LDS through registers (coalesced
-//    16-byte loads); the copy of the next tile is spread over the FFN chunk
-//    loop of the current one.  Pixels sit 144 bytes apart (128 data + 16 pad): eight
+//  * The input tile plus halo is copied into LDS by LDS-DMA (global_load_lds,
+//    1 KB per wave instruction, no registers); the copies of the next tile
+//    are issued when the FFN of the current one starts and land while it
+//    runs.  Pixels sit 144 bytes apart (128 data + 16 pad): eight
 //    lanes reading the same channel chunk of eight neighbouring pixels hit
 //    eight different bank groups, and every tap is the pixel's base address
 //    plus a compile-time offset (fixed row stride), so the depth-wise loop
@@ -24,13 +25,13 @@
 //    are redirected, row by row, to a zero area.
 //  * Depth-wise conv on the VALU in packed fp16.  A two-block wave lets each
 //    lane compute one pixel for all 16 channels of a K step; the taps are then
-//    wave-uniform and come from scalar registers (s_load), and one
-//    v_permlane32_swap per register pair rearranges the result into the two
-//    MFMA B fragments.  A one-block wave uses the B-fragment lane layout
-//    directly with the taps from LDS.
+//    wave-uniform (broadcast LDS reads), and one v_permlane32_swap per
+//    register pair rearranges the result into the two MFMA B fragments.  A
+//    one-block wave uses the B-fragment lane layout directly.
 //  * FFN per 32-hidden chunk on v_mfma_f32_32x32x16_f16 with swapped operands
 //    (weights = A, pixels = B), the sigma/tau row orders of cf_fused_impl.h,
-//    b1 in the C operand, GELU evaluated on interleaved fp16 pairs.
+//    b1 as a fifth expand K step (a b1/4 fragment against a constant-one B
+//    fragment), GELU evaluated on interleaved fp16 pairs.
 //  * Accumulators start at x/4 + b2/4 read from the LDS halo (residual), the
 //    activation variable is u/4 (exact power-of-two scaling), output 4*acc.
 #pragma once
@@ -229,64 +230,55 @@ struct K64 {
         rows = (int)(fdiv(pend - 1, a.divW) - g_lo) + 1 + 2 * PAD;
     }
 
-    // ---- halo copy.  Row r of the buffer holds global image row g_lo - PAD + r;
-    // pixel column c (= image column + PAD) starts at r*rs + c*PIX.  A row of
-    // the image is W*128 contiguous bytes; wave wv copies its 1 KB part wv
-    // (W + 2*PAD <= 64, so a row has at most 8 parts): lane l moves bytes
-    // 16l..16l+15 of the part, i.e. chunk l % 8 of pixel 8*wv + l / 8, with a
-    // plain coalesced 16-byte global load and a 16-byte LDS write.
-    struct RowCopy {
-        int goff;       // byte offset in the image row, -1 if this lane has no data
-        uint32_t loff;  // byte offset in the halo row
+    // ---- halo copy through LDS-DMA.  Row r of the buffer holds global image
+    // row g_lo - PAD + r; pixel column c (= image column + PAD) starts at
+    // r*rs + c*PIX.  The interior of a buffer row (W pixels from column PAD)
+    // is 9W consecutive 16-byte slots: slot s belongs to pixel s / 9, chunk
+    // s % 9, where chunk 8 is padding that receives a second copy of chunk 7
+    // and is never read.  One DMA instruction fills 64 consecutive slots
+    // (1 KB): wave wv fills slots 64 wv .. 64 wv + 63 of every row (9W <= 512),
+    // with the lanes past the last slot switched off so that the pad columns
+    // keep their zeros.  Rows outside the images are not copied (no tap reads
+    // them).  The lane mask goes into EXEC inside the copy's instruction
+    // group.
+    struct HaloLane {
+        uint32_t goff;  // byte offset in the image row of this lane's slot
+        uint32_t loff;  // LDS byte offset of this wave's part inside a buffer row
+        uint64_t mask;  // lanes whose slot lies inside the row
     };
-    static __device__ __forceinline__ RowCopy row_copy(const Args &a, int wv, int lane) {
-        const int px = 8 * wv + (lane >> 3), c = lane & 7;
-        RowCopy rc;
-        rc.goff = px < a.W ? px * (C * 2) + c * 16 : -1;
-        rc.loff = (uint32_t)(PAD + px) * PIX + (uint32_t)c * 16;
-        return rc;
+    static __device__ __forceinline__ HaloLane halo_lane(const Args &a, int wv, int lane) {
+        HaloLane hl;
+        const int s0 = 64 * __builtin_amdgcn_readfirstlane(wv), sl = s0 + lane, px = sl / 9, q = sl % 9;
+        hl.goff = (uint32_t)px * (C * 2) + (uint32_t)(q < 8 ? q : 7) * 16;
+        hl.loff = (uint32_t)PAD * PIX + (uint32_t)s0 * 16;
+        hl.mask = __ballot(sl < 9 * a.W);
+        return hl;
+    }
+    // Copy buffer row r of the tile whose first image row is g_lo (rows
+    // rows).  Branch-free, so that an FFN step stays one basic block: when the
+    // wave has nothing to copy, every lane moves the first 16 bytes of x into
+    // a trash area instead (the mask never goes empty).
+    static __device__ __forceinline__ void issue_row(const Args &a, uint8_t *smem, const HaloLane &hl, uint32_t g_lo,
+                                                     int rows, int r) {
+        const int grow = (int)g_lo - PAD + r;
+        const bool ok = r < rows && grow >= 0 && grow < a.NH && hl.mask != 0;  // wave-uniform
+        // masks rather than selects around the address arithmetic (a select
+        // of a 64-bit product becomes a branch)
+        const uint32_t okm = ok ? ~0u : 0u;
+        const size_t rb = (size_t)((uint32_t)grow & okm) * (size_t)((uint32_t)a.W * (C * 2));
+        const uint32_t lds = ok ? a.off_halo + (uint32_t)r * a.rs + hl.loff : a.off_trash;
+        fused::dma16m(reinterpret_cast<const uint8_t *>(a.x) + rb, hl.goff & okm, smem + lds,
+                      ok ? hl.mask : ~0ull);
+    }
+    static __device__ __forceinline__ void issue_halo(const Args &a, uint8_t *smem, const HaloLane &hl, uint32_t g_lo,
+                                                      int rows) {
+        for (int r = 0; r < rows; r++)
+            issue_row(a, smem, hl, g_lo, rows, r);
     }
     struct NextHalo {
         uint32_t g_lo;
         int rows;  // 0: nothing to copy
     };
-    // Row r of the next tile passes through registers: fetched in FFN step r
-    // into one of two buffers (by the parity of r) and written to LDS in step
-    // r + 2, so each load has two steps to land.  Branch-free, so that a step
-    // stays one basic block: lanes with nothing to copy read the first 16
-    // bytes of x and write them to a trash area.
-    struct Staged {
-        u32x4 v;
-        uint32_t dst;  // LDS destination (the trash area for lanes with nothing to copy)
-    };
-    static __device__ __forceinline__ void load_row(const Args &a, const NextHalo &nh, const RowCopy &rc, int r,
-                                                    int lane, Staged &st) {
-        const uint8_t *xb = reinterpret_cast<const uint8_t *>(a.x);
-        const int grow = (int)nh.g_lo - PAD + r;
-        const bool okr = r < nh.rows && grow >= 0 && grow < a.NH;  // wave-uniform
-        const bool ok = okr && rc.goff >= 0;
-        const uint32_t gr = okr ? (uint32_t)grow : 0u;
-        const uint32_t go = ok ? (uint32_t)rc.goff : 0u;
-        const uint64_t src = (uint64_t)gr * (uint32_t)(a.W * C * 2) + go;
-        st.v = *reinterpret_cast<const u32x4 *>(xb + src);
-        st.dst = ok ? a.off_halo + (uint32_t)r * a.rs + rc.loff : a.off_trash + (uint32_t)lane * 16;
-    }
-    static __device__ __forceinline__ void write_row(uint8_t *smem, const Staged &st) {
-        *reinterpret_cast<u32x4 *>(smem + st.dst) = st.v;
-    }
-    // whole halo at once (first tile)
-    static __device__ __forceinline__ void copy_halo(const Args &a, uint8_t *smem, int t0, int nblk,
-                                                     const RowCopy &rc) {
-        NextHalo nh;
-        tile_rows(a, t0, nblk, nh.g_lo, nh.rows);
-        for (int r = 0; r < nh.rows; r++) {
-            const int grow = (int)nh.g_lo - PAD + r;
-            if (grow >= 0 && grow < a.NH && rc.goff >= 0)
-                *reinterpret_cast<u32x4 *>(smem + a.off_halo + (uint32_t)r * a.rs + rc.loff) =
-                    *reinterpret_cast<const u32x4 *>(reinterpret_cast<const uint8_t *>(a.x) +
-                                                     (size_t)grow * a.W * (C * 2) + rc.goff);
-        }
-    }
 
     // Base addresses of the KS tap rows of a pixel: the top-left tap of the
     // pixel's window plus i*rs for row i, or (for rows outside the pixel's
@@ -459,20 +451,17 @@ struct K64 {
     struct Ffn {
         const uint8_t *w1p, *w2p;
         u32x4 ones;  // B fragment: 1 at k = 0 for every pixel (bias K step)
+        uint8_t *smem;
+        HaloLane hl;
         NextHalo nh;
-        RowCopy rc;
-        int lane;
     };
 
     template <int NB, bool EXP, bool ACTV, bool PROJ>
-    static __device__ __forceinline__ void step(const Args &a, uint8_t *smem, const Ffn &f, Staged &stg, int s,
-                                                const u32x4 (&dfr)[KST][2], float16v (&ue)[2],
-                                                const float16v (&ua)[2], uint32_t (&ga)[16],
+    static __device__ __forceinline__ void step(const Args &a, const Ffn &f, int s, const u32x4 (&dfr)[KST][2],
+                                                float16v (&ue)[2], const float16v (&ua)[2], uint32_t (&ga)[16],
                                                 const uint32_t (&gp)[16], float16v (&acc)[CB][2]) {
-        // halo row s - 2 of the next tile goes to LDS, row s is fetched
-        if constexpr (PROJ)
-            write_row(smem, stg);
-        load_row(a, f.nh, f.rc, s, f.lane, stg);
+        // halo row s of the next tile (the tile touches at most nch + 2 rows)
+        issue_row(a, f.smem, f.hl, f.nh.g_lo, f.nh.rows, s);
         if constexpr (ACTV)
             act_blocks<NB>(ua, ga);
         if constexpr (EXP) {
@@ -524,31 +513,28 @@ struct K64 {
     }
 
     template <int NB>
-    static __device__ __forceinline__ void ffn(const Args &a, uint8_t *smem, int lane, const NextHalo &nh,
-                                               const RowCopy &rc, const u32x4 (&dfr)[KST][2],
+    static __device__ __forceinline__ void ffn(const Args &a, uint8_t *smem, int lane, const HaloLane &hl,
+                                               const NextHalo &nh, const u32x4 (&dfr)[KST][2],
                                                float16v (&acc)[CB][2]) {
         Ffn f;
         f.w1p = smem + lane * 16;
         f.w2p = smem + a.off_w2 + lane * 16;
         f.ones = u32x4{lane < 32 ? 0x3c00u : 0u, 0u, 0u, 0u};
+        f.smem = smem;
+        f.hl = hl;
         f.nh = nh;
-        f.rc = rc;
-        f.lane = lane;
         float16v u0[2], u1[2];
         uint32_t g0[16], g1[16];
-        Staged st0, st1;  // halo rows of even / odd steps
         const int n = a.nch;  // even, >= 2
-        step<NB, true, false, false>(a, smem, f, st0, 0, dfr, u0, u1, g1, g0, acc);
-        step<NB, true, true, false>(a, smem, f, st1, 1, dfr, u1, u0, g0, g1, acc);
+        step<NB, true, false, false>(a, f, 0, dfr, u0, u1, g1, g0, acc);
+        step<NB, true, true, false>(a, f, 1, dfr, u1, u0, g0, g1, acc);
 #pragma unroll 1
         for (int s = 2; s < n; s += 2) {
-            step<NB, true, true, true>(a, smem, f, st0, s, dfr, u0, u1, g1, g0, acc);
-            step<NB, true, true, true>(a, smem, f, st1, s + 1, dfr, u1, u0, g0, g1, acc);
+            step<NB, true, true, true>(a, f, s, dfr, u0, u1, g1, g0, acc);
+            step<NB, true, true, true>(a, f, s + 1, dfr, u1, u0, g0, g1, acc);
         }
-        step<NB, false, true, true>(a, smem, f, st0, n, dfr, u0, u1, g1, g0, acc);
-        step<NB, false, false, true>(a, smem, f, st1, n + 1, dfr, u1, u0, g0, g1, acc);
-        write_row(smem, st0);
-        write_row(smem, st1);
+        step<NB, false, true, true>(a, f, n, dfr, u0, u1, g1, g0, acc);
+        step<NB, false, false, true>(a, f, n + 1, dfr, u1, u0, g0, g1, acc);
     }
 
     template <int NB>
@@ -594,13 +580,18 @@ struct K64 {
         stage(a, smem, tid);
         __syncthreads();
 
-        const RowCopy rc = row_copy(a, wv, lane);
+        const HaloLane hl = halo_lane(a, wv, lane);
         // the range is cut into tiles of tile_max blocks and a last, smaller
         // one: a full tile gives every SIMD the same number of blocks
         const int range = hi - lo;
         const int nt = (range + a.tile_max - 1) / a.tile_max;
-        if (nt > 0)
-            copy_halo(a, smem, lo, range < a.tile_max ? range : a.tile_max, rc);
+        if (nt > 0) {
+            uint32_t g0;
+            int r0;
+            tile_rows(a, lo, range < a.tile_max ? range : a.tile_max, g0, r0);
+            issue_halo(a, smem, hl, g0, r0);
+        }
+        int pending = 0;  // output stores this wave issued after its last halo copies
 
         int t0 = lo;
         for (int it = 0; it < nt; it++) {
@@ -608,6 +599,7 @@ struct K64 {
             uint32_t g_lo;
             int rows;
             tile_rows(a, t0, nblk, g_lo, rows);
+            (void)rows;
             // this wave's blocks: w (if w < nblk) and 8 + w (if 8 + w < nblk)
             const int nb = (wv < nblk ? 1 : 0) + (wv + 8 < nblk ? 1 : 0);
             const int jb[2] = {wv, wv + 8};
@@ -623,7 +615,11 @@ struct K64 {
                 tap_bases(a, pix[b], valid[b], g_lo, (uint32_t)h * 32, bs, centre[b]);
             }
 
-            __syncthreads();  // the tile's halo is in LDS
+            // this wave's halo copies have landed (vector-memory operations
+            // complete in order; the stores issued after them may still be
+            // in flight) ...
+            fused::wait_vmcnt_le(pending);
+            __syncthreads();  // ... and every other wave's: the tile's halo is in LDS
 
             u32x4 dfr[KST][2];
             float16v acc[CB][2];
@@ -641,23 +637,24 @@ struct K64 {
                 residual<1>(a, smem, centre, h, acc);
             }
             __syncthreads();  // the halo buffer is free
-            NextHalo nh{0u, 0};
+            // the next tile's halo streams into LDS, a row per FFN step
             const int t1 = t0 + nblk;
-            const int nblk1 = (hi - t1) < a.tile_max ? (hi - t1) : a.tile_max;
-            if (it + 1 < nt)
+            NextHalo nh{0u, 0};
+            if (it + 1 < nt) {
+                const int nblk1 = (hi - t1) < a.tile_max ? (hi - t1) : a.tile_max;
                 tile_rows(a, t1, nblk1, nh.g_lo, nh.rows);
-
+            }
+            pending = 0;
             if (nb == 2) {
-                ffn<2>(a, smem, lane, nh, rc, dfr, acc);
-                store<2>(a, pix, valid, h, acc);
+                ffn<2>(a, smem, lane, hl, nh, dfr, acc);
+                pending = store<2>(a, pix, valid, h, acc);
             } else if (nb == 1) {
-                ffn<1>(a, smem, lane, nh, rc, dfr, acc);
-                store<1>(a, pix, valid, h, acc);
-            } else if (nh.rows > 0) {
-                copy_halo(a, smem, t1, nblk1, rc);
+                ffn<1>(a, smem, lane, hl, nh, dfr, acc);
+                pending = store<1>(a, pix, valid, h, acc);
+            } else {
+                issue_halo(a, smem, hl, nh.g_lo, nh.rows);
             }
             t0 = t1;
-            (void)rows;
         }
         __builtin_amdgcn_s_waitcnt(0);
     }
@@ -675,7 +672,8 @@ __global__ __launch_bounds__(NT, 1) void block64_kernel(Args a) {
 inline bool plan(int N, int H, int W, int E, int k, int max_range, int tb_limit, int &tb, int &halo_rows,
                  uint32_t &rs, Layout &L) {
     const int pad = k / 2;
-    if (W + 2 * pad > 64 || E * C % 32 != 0 || E * C / 32 > 8)
+    // a row of the halo is one DMA instruction per wave: 9W slots <= 8 * 64
+    if (W > 56 || E * C % 32 != 0 || E * C / 32 > 8)
         return false;
     rs = (uint32_t)(W + 2 * pad) * PIX;
     const int64_t NH = (int64_t)N * H;

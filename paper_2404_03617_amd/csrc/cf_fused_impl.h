@@ -172,6 +172,35 @@ __device__ __forceinline__ void dma16s(const void *base, uint32_t voff, uint8_t 
         : "memory");
 }
 
+// dma16s for the lanes set in a wave-uniform, nonzero mask (EXEC is set
+// and restored inside the instruction group, so the copy needs no
+// divergent branch).
+__device__ __forceinline__ void dma16m(const void *base, uint32_t voff, uint8_t *lds_wave_base, uint64_t mask) {
+    const uint32_t lds = (uint32_t)__builtin_amdgcn_readfirstlane(
+        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds_wave_base);
+    const uint64_t b = (uint64_t)(uintptr_t)base;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+    const uint64_t bu = ((uint64_t)hi << 32) | (uint64_t)lo;
+    const uint32_t mlo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)mask);
+    const uint32_t mhi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(mask >> 32));
+    const uint64_t mu = ((uint64_t)mhi << 32) | (uint64_t)mlo;
+    uint64_t saved_exec;
+    uint32_t saved_m0;
+    asm volatile(
+        "s_mov_b64 %0, exec\n\t"
+        "s_mov_b64 exec, %5\n\t"
+        "s_mov_b32 %1, m0\n\t"
+        "s_mov_b32 m0, %4\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %2, %3\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "s_mov_b64 exec, %0"
+        : "=&s"(saved_exec), "=&s"(saved_m0)
+        : "v"(voff), "s"(bu), "s"(lds), "s"(mu)
+        : "memory");
+}
+
 __device__ __forceinline__ float16v mfma32(const u32x4 &a, const u32x4 &b, const float16v &c, F16) {
     Pack8 pa, pb;
     pa.u = a;
