@@ -201,6 +201,7 @@ struct Kw {
     // 16-byte-per-lane DMA instruction per 1 KB fragment; wave wv copies
     // fragments wv, wv + NW, ...
     // buffers: A0 A1 B0 B1; step s uses A_(s&1) and B_(s&1)
+    static constexpr int PW = C == 256 ? 8 : 4;            // weight fragments in flight per wave (measured)
     static constexpr int FA = (2 * KST + NW - 1) / NW;    // DMA instructions per wave for an A buffer
     static constexpr int FB = (4 * CB + NW - 1) / NW;     // ... for a B buffer
     static_assert(2 * KST % NW == 0 && 4 * CB % NW == 0, "uniform DMA count per wave");
@@ -390,29 +391,30 @@ struct Kw {
             // ---- expand chunk 2s + r: U/4 = s1 * (W1 D/4) + b1/4, phi, hidden tile to LDS
             const int ch = 2 * s + r;
             const uint8_t *wa = bufa + (uint32_t)(r * KST * 1024 + lane * 16);
-            // fragments stream through a 4-deep register window; the
-            // scheduling groups keep 4 LDS reads in flight ahead of the MFMAs
+            // fragments stream through a PW-deep register window; the
+            // scheduling groups keep PW LDS reads in flight ahead of the MFMAs
+            // (LDS latency with eight waves reading far exceeds one MFMA)
             float16v hh;
 #pragma unroll
             for (int e = 0; e < 16; e++)
                 hh[e] = 0.0f;
-            u32x4 wf[4];
+            u32x4 wf[PW];
 #pragma unroll
-            for (int i = 0; i < 4; i++)
+            for (int i = 0; i < PW; i++)
                 wf[i] = ld16(wa, i * 1024);
 #pragma unroll
             for (int ks = 0; ks < KST; ks++) {
-                hh = mfma32(wf[ks & 3], dfr[ks], hh, F16{});
-                if (ks + 4 < KST)
-                    wf[ks & 3] = ld16(wa, (ks + 4) * 1024);
+                hh = mfma32(wf[ks % PW], dfr[ks], hh, F16{});
+                if (ks + PW < KST)
+                    wf[ks % PW] = ld16(wa, (ks + PW) * 1024);
             }
-            __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);
+            __builtin_amdgcn_sched_group_barrier(0x100, PW, 1);
 #pragma unroll
-            for (int ks = 0; ks + 4 < KST; ks++) {
+            for (int ks = 0; ks + PW < KST; ks++) {
                 __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
                 __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
             }
-            __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);
+            __builtin_amdgcn_sched_group_barrier(0x008, PW, 1);
             const float16v s1v = *reinterpret_cast<const float16v *>(smem + a.off_s1 + ch * 128 + h * 64);
             const float16v b1v = *reinterpret_cast<const float16v *>(smem + a.off_b1 + ch * 128 + h * 64);
             float v[16];
@@ -448,24 +450,24 @@ struct Kw {
                     const int j = i / (2 * CBH), kk = (i / CBH) & 1, c = i % CBH;
                     return ld16(bufb, (uint32_t)((j * 2 * CB + 2 * (CBH * r + c) + kk) * 1024 + lane * 16));
                 };
-                u32x4 wf[4];
+                u32x4 wf[PW];
 #pragma unroll
-                for (int i = 0; i < 4; i++)
+                for (int i = 0; i < PW; i++)
                     wf[i] = frag(i);
 #pragma unroll
                 for (int i = 0; i < NF; i++) {
                     const int j = i / (2 * CBH), kk = (i / CBH) & 1, c = i % CBH;
-                    acc[c] = mfma32(wf[i & 3], hid[j][kk], acc[c], F16{});
-                    if (i + 4 < NF)
-                        wf[i & 3] = frag(i + 4);
+                    acc[c] = mfma32(wf[i % PW], hid[j][kk], acc[c], F16{});
+                    if (i + PW < NF)
+                        wf[i % PW] = frag(i + PW);
                 }
-                __builtin_amdgcn_sched_group_barrier(0x100, 8, 2);
+                __builtin_amdgcn_sched_group_barrier(0x100, PW + 4, 2);
 #pragma unroll
-                for (int i = 0; i + 4 < NF; i++) {
+                for (int i = 0; i + PW < NF; i++) {
                     __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
                     __builtin_amdgcn_sched_group_barrier(0x100, 1, 2);
                 }
-                __builtin_amdgcn_sched_group_barrier(0x008, 4, 2);
+                __builtin_amdgcn_sched_group_barrier(0x008, PW, 2);
             }
             // copies are issued after the MFMAs of a phase so that a full
             // copy queue does not hold up the matrix instructions
