@@ -71,10 +71,14 @@ struct Geo {
     static constexpr int KST = C / 16;
     static constexpr int CB = C / 32;
     static constexpr int NSLAB = C / CS;
-    static constexpr int BUF_A = 2 * KST * 1024;   // W1 fragments of the two chunks of a step
-    static constexpr int BUF_B = 2 * 2 * CB * 1024; // W2 fragments of the two chunks of a step
-    static constexpr int PA = BUF_A / 16 / NT;      // 16-byte pieces per thread
-    static constexpr int PB = BUF_B / 16 / NT;
+    // weight buffers of a step (two chunks): LDS-DMA instructions of 1 KB at
+    // a pitch of PITCH bytes
+    static constexpr int PITCH = 1040;
+    static constexpr int RPI = 1024 / (2 * C);      // W1 rows per instruction
+    static constexpr int NIA = 64 / RPI;            // instructions of an A buffer (64 W1 rows)
+    static constexpr int NIB = C / 8;               // instructions of a B buffer (C segments of 128 bytes)
+    static constexpr int BUF_A = NIA * PITCH;
+    static constexpr int BUF_B = NIB * PITCH;
 };
 
 struct Layout {
@@ -127,7 +131,7 @@ __device__ __forceinline__ uint32_t u32(half2v v) { return __builtin_bit_cast(ui
 template <int C, int KS, int ACT>
 struct Kw {
     typedef Geo<C> G;
-    static constexpr int KST = G::KST, CB = G::CB, NSLAB = G::NSLAB, PA = G::PA, PB = G::PB;
+    static constexpr int KST = G::KST, CB = G::CB, NSLAB = G::NSLAB, PITCH = G::PITCH, RPI = G::RPI;
     static constexpr int CBH = CB / 2;  // output blocks per wave of a pair
     static constexpr int PAD = KS / 2;
 
@@ -197,45 +201,80 @@ struct Kw {
     // ---- weight buffers.  Buffer A of step s holds the W1 fragments (rows in
     // sigma order) of chunks 2s and 2s + 1: fragment j*KST + ks; buffer B the
     // W2 fragments (rows in tau order): fragment j*2*CB + 2*cb + kk.
-    // Asynchronous global->LDS copies of a step's weight fragments: one
-    // 16-byte-per-lane DMA instruction per 1 KB fragment; wave wv copies
-    // fragments wv, wv + NW, ...
-    // buffers: A0 A1 B0 B1; step s uses A_(s&1) and B_(s&1)
+    // ---- weight buffers A0 A1 B0 B1 (step s uses A_(s&1) and B_(s&1)),
+    // filled by LDS-DMA, wave wv issuing instructions wv, wv + NW, ...  Every LDS-DMA instruction reads contiguous runs of
+    // memory (8 cache lines per KB, against 32 when a KB is gathered in
+    // fragment order, which the vector memory unit serves about five times
+    // slower), and the instructions sit PITCH bytes apart (16 of padding), so
+    // that the fragment reads below hit 16 different bank groups per 16 lanes.
+    //  * A (W1, 64 rows of C halves per step): row r of chunk j is numbered
+    //    (q, u) with q = 2j + r / 16, u = r % 16, and sits in instruction
+    //    u + 16 (q / RPI) at byte (q % RPI) * 2C.  The rows sigma(m) read by one
+    //    16-lane group have 16 different u, hence 16 different instructions.
+    //  * B (W2: each of the C output rows contributes its 64 hidden columns of
+    //    the step, 128 contiguous bytes): instruction 8 set + i holds, for the
+    //    two output blocks 2 set + bb, the rows tau(m) with
+    //    m = 16 mhi + 2 i + mlo at slot 4 bb + 2 mhi + mlo.  One 16-lane group
+    //    reads 8 instructions x 2 slot parities.  With that numbering
+    //    tau(m) = T(i) + 8 mhi + mlo, T(i) = 16 ((i >> 1) & 1) + 4 (i >> 2) + 2 (i & 1),
+    //    so the source of a lane is a wave-uniform base plus a lane offset.
     static constexpr int PW = C == 256 ? 8 : 4;            // weight fragments in flight per wave (measured)
-    static constexpr int FA = (2 * KST + NW - 1) / NW;    // DMA instructions per wave for an A buffer
-    static constexpr int FB = (4 * CB + NW - 1) / NW;     // ... for a B buffer
-    static_assert(2 * KST % NW == 0 && 4 * CB % NW == 0, "uniform DMA count per wave");
+    static constexpr int FA = G::NIA / NW;                 // DMA instructions per wave for an A buffer
+    static constexpr int FB = G::NIB / NW;                 // ... for a B buffer
+    static_assert(G::NIA % NW == 0 && G::NIB % NW == 0, "uniform DMA count per wave");
     static __device__ __forceinline__ uint8_t *buf_a(const Args &a, uint8_t *smem, int slot) {
         return smem + a.off_big + slot * G::BUF_A;
     }
     static __device__ __forceinline__ uint8_t *buf_b(const Args &a, uint8_t *smem, int slot) {
         return smem + a.off_big + 2 * G::BUF_A + slot * G::BUF_B;
     }
-    // (the source of a copy is a wave-uniform base plus the lane's byte offset)
-    static __device__ __forceinline__ void dma_a(const Args &a, uint8_t *smem, int step, int wv, int lane) {
+    static __device__ __forceinline__ uint32_t t_of(int i) {
+        return (uint32_t)(16 * ((i >> 1) & 1) + 4 * (i >> 2) + 2 * (i & 1));
+    }
+    // lane byte offsets of the sources (A: 16-row group g, piece p; B: slot, piece)
+    static __device__ __forceinline__ uint32_t lane_a(int lane) {
+        const int per = 64 / RPI, g = lane / per, p = lane % per;
+        return (uint32_t)(16 * g * C + 8 * p) * 2;
+    }
+    static __device__ __forceinline__ uint32_t lane_b(const Args &a, int lane) {
+        const int slot = lane >> 3, piece = lane & 7;
+        const int bb = slot >> 2, mhi = (slot >> 1) & 1, mlo = slot & 1;
+        return ((uint32_t)(32 * bb + 8 * mhi + mlo) * (uint32_t)(a.nch * 32) + 8 * piece) * 2;
+    }
+    static __device__ __forceinline__ void dma_a(const Args &a, uint8_t *smem, int step, int wv, uint32_t la) {
         uint8_t *buf = buf_a(a, smem, step & 1);
-        const uint16_t *w1 = a.w1 + (size_t)step * 64 * C;
-        const uint32_t lo = (uint32_t)(sigma_row(lane & 31) * C + 8 * (lane >> 5)) * 2;
         const int wu = __builtin_amdgcn_readfirstlane(wv);
 #pragma unroll
         for (int i = 0; i < FA; i++) {
-            const int f = wu + NW * i;
-            const int j = f / KST, ks = f % KST;
-            fused::dma16s(w1 + (j * 32 * C + ks * 16), lo, buf + f * 1024);
+            const int I = wu + NW * i;
+            const int row = 64 * step + 32 * (I >> 4) + (I & 15);
+            fused::dma16s(a.w1 + (size_t)row * C, la, buf + I * PITCH);
         }
     }
-    static __device__ __forceinline__ void dma_b(const Args &a, uint8_t *smem, int step, int wv, int lane) {
+    static __device__ __forceinline__ void dma_b(const Args &a, uint8_t *smem, int step, int wv, uint32_t lb) {
         uint8_t *buf = buf_b(a, smem, step & 1);
-        const uint16_t *w2 = a.w2 + (size_t)step * 64;
-        const uint32_t ec = (uint32_t)a.nch * 32;
-        const uint32_t lo = ((uint32_t)tau_row(lane & 31) * ec + 8 * (lane >> 5)) * 2;
+        const size_t ec = (size_t)a.nch * 32;
         const int wu = __builtin_amdgcn_readfirstlane(wv);
 #pragma unroll
         for (int i = 0; i < FB; i++) {
-            const int f = wu + NW * i;
-            const int j = f / (2 * CB), g = f % (2 * CB), cb = g >> 1, kk = g & 1;
-            fused::dma16s(w2 + ((size_t)(cb * 32) * ec + (j * 32 + 16 * kk)), lo, buf + f * 1024);
+            const int I = wu + NW * i;
+            fused::dma16s(a.w2 + ((size_t)(64 * (I >> 3)) + t_of(I & 7)) * ec + 64 * step, lb, buf + I * PITCH);
         }
+    }
+    // fragment bases of lane (h, m): expand reads W1 row sigma(m) of chunk r
+    // (K step ks at +32 ks); project reads output row tau(m) of block cb,
+    // hidden columns of chunk j (at a compile-time offset per fragment)
+    static __device__ __forceinline__ uint32_t frag_a(int r, int lane) {
+        const int h = lane >> 5, rho = sigma_row(lane & 31);
+        const int q = 2 * r + (rho >> 4), u = rho & 15;
+        return (uint32_t)((u + 16 * (q / RPI)) * PITCH + (q % RPI) * 2 * C + 16 * h);
+    }
+    static __device__ __forceinline__ uint32_t frag_b(int lane) {
+        const int h = lane >> 5, m = lane & 31;
+        return (uint32_t)(((m >> 1) & 7) * PITCH + (2 * (m >> 4) + (m & 1)) * 128 + 16 * h);
+    }
+    static constexpr uint32_t frag_b_off(int cb, int j, int kk) {
+        return (uint32_t)((8 * (cb >> 1)) * PITCH + 4 * (cb & 1) * 128 + 64 * j + 32 * kk);
     }
 
     // ---- halo slab copy (synchronous, through registers): rows of the tile's
@@ -374,11 +413,12 @@ struct Kw {
         const int wv = tid >> 6;
         uint8_t *gmine = smem + a.off_g + (uint32_t)(b * 2 + r) * 2048;
         // prologue: A0 B0 A1 B1 in flight; A0 and B0 must land
-        dma_a(a, smem, 0, wv, lane);
-        dma_b(a, smem, 0, wv, lane);
+        const uint32_t la = lane_a(lane), lb = lane_b(a, lane);
+        dma_a(a, smem, 0, wv, la);
+        dma_b(a, smem, 0, wv, lb);
         if (nsteps > 1) {
-            dma_a(a, smem, 1, wv, lane);
-            dma_b(a, smem, 1, wv, lane);
+            dma_a(a, smem, 1, wv, la);
+            dma_b(a, smem, 1, wv, lb);
             fused::wait_vmcnt<FA + FB>();
         } else {
             fused::wait_vmcnt<0>();
@@ -388,9 +428,13 @@ struct Kw {
         for (int s = 0; s < nsteps; s++) {
             uint8_t *bufa = buf_a(a, smem, s & 1);
             uint8_t *bufb = buf_b(a, smem, s & 1);
+            // B_(s+1) goes into the slot B_(s-1) used, free since the last
+            // barrier; issued first, so that the copies run beside the MFMAs
+            if (s >= 1 && s + 1 < nsteps)
+                dma_b(a, smem, s + 1, wv, lb);
             // ---- expand chunk 2s + r: U/4 = s1 * (W1 D/4) + b1/4, phi, hidden tile to LDS
             const int ch = 2 * s + r;
-            const uint8_t *wa = bufa + (uint32_t)(r * KST * 1024 + lane * 16);
+            const uint8_t *wa = bufa + frag_a(r, lane);
             // fragments stream through a PW-deep register window; the
             // scheduling groups keep PW LDS reads in flight ahead of the MFMAs
             // (LDS latency with eight waves reading far exceeds one MFMA)
@@ -401,12 +445,12 @@ struct Kw {
             u32x4 wf[PW];
 #pragma unroll
             for (int i = 0; i < PW; i++)
-                wf[i] = ld16(wa, i * 1024);
+                wf[i] = ld16(wa, i * 32);
 #pragma unroll
             for (int ks = 0; ks < KST; ks++) {
                 hh = mfma32(wf[ks % PW], dfr[ks], hh, F16{});
                 if (ks + PW < KST)
-                    wf[ks % PW] = ld16(wa, (ks + PW) * 1024);
+                    wf[ks % PW] = ld16(wa, (ks + PW) * 32);
             }
             __builtin_amdgcn_sched_group_barrier(0x100, PW, 1);
 #pragma unroll
@@ -425,15 +469,15 @@ struct Kw {
             activate<8>(v, o);
             *reinterpret_cast<u32x4 *>(gmine + lane * 32) = u32x4{o[0], o[1], o[2], o[3]};
             *reinterpret_cast<u32x4 *>(gmine + lane * 32 + 16) = u32x4{o[4], o[5], o[6], o[7]};
-            // B_(s+1) goes into the slot B_(s-1) used (free since the last barrier)
-            if (s >= 1 && s + 1 < nsteps)
-                dma_b(a, smem, s + 1, wv, lane);
             // B_s landed (issued after it: A_(s+1), B_(s+1) when they exist)
             if (s + 1 < nsteps)
                 fused::wait_vmcnt<FA + FB>();
             else
                 fused::wait_vmcnt<0>();
             lds_barrier();  // hidden tiles and B_s visible; A_s free
+            // A_(s+2) goes into A_s's slot
+            if (s + 2 < nsteps)
+                dma_a(a, smem, s + 2, wv, la);
             // ---- project both chunks onto this wave's output half
             {
                 constexpr int NF = 4 * CBH;  // W2 fragments used by this wave per step
@@ -446,9 +490,12 @@ struct Kw {
                 }
                 // MFMA i: chunk j = i / (2*CBH), K step kk = (i / CBH) % 2, output block
                 // c = i % CBH -- consecutive MFMAs feed different accumulators
+                // block cb = CBH r + c (CBH even): set CBH r / 2 + c / 2, bb = c % 2
+                static_assert(CBH % 2 == 0, "output blocks in pairs");
+                const uint8_t *wb = bufb + frag_b(lane) + (uint32_t)(4 * CBH * r * PITCH);
                 auto frag = [&](int i) {
                     const int j = i / (2 * CBH), kk = (i / CBH) & 1, c = i % CBH;
-                    return ld16(bufb, (uint32_t)((j * 2 * CB + 2 * (CBH * r + c) + kk) * 1024 + lane * 16));
+                    return ld16(wb, frag_b_off(c, j, kk));
                 };
                 u32x4 wf[PW];
 #pragma unroll
@@ -469,10 +516,6 @@ struct Kw {
                 }
                 __builtin_amdgcn_sched_group_barrier(0x008, PW, 2);
             }
-            // copies are issued after the MFMAs of a phase so that a full
-            // copy queue does not hold up the matrix instructions
-            if (s + 2 < nsteps)
-                dma_a(a, smem, s + 2, wv, lane);
             // A_(s+1) landed (issued after it: B_(s+1), and A_(s+2) when it exists)
             if (s + 2 < nsteps)
                 fused::wait_vmcnt<FB + FA>();

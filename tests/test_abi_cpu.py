@@ -181,3 +181,67 @@ def test_c512_dma_layouts_are_conflict_free():
                         assert a == where[(cb * 32 + _tau(m), 2 * kk + h)]
                         addrs.append(a)
                     assert len({(a // 16) % 16 for a in addrs}) == 16
+
+
+@pytest.mark.parametrize("C", [128, 256])
+def test_pair_kernel_dma_layouts_map_fragments_without_conflicts(C):
+    """The C = 128 / 256 pair kernel's weight buffers (restated from its DMA
+    and fragment-read address formulas): every 16-byte piece of a step's 64 W1
+    rows and C W2 row segments is copied to exactly one place, every fragment
+    read finds there the W1 / W2 elements its MFMA needs, and each 16-lane
+    group of a read hits 16 distinct 16-byte bank groups."""
+    PITCH, RPI = 1040, 1024 // (2 * C)
+    NIA, NIB = 64 // RPI, C // 8
+    CBH, KST = C // 64, C // 16
+    # A: instruction I, lane l -> 16-row group g, piece p of W1 row 32 (I >> 4) + (I & 15) + 16 g of the step
+    per = 64 // RPI
+    where_a = {}
+    for I in range(NIA):
+        for lane in range(64):
+            g, p = lane // per, lane % per
+            key = (32 * (I >> 4) + (I & 15) + 16 * g, p)
+            assert key not in where_a
+            where_a[key] = I * PITCH + 16 * lane
+    assert len(where_a) == 64 * (C // 8)
+    for r in range(2):  # the chunk a wave expands
+        for ks in range(KST):
+            for h in range(2):
+                for grp in (range(16), range(16, 32)):
+                    addrs = []
+                    for m in grp:
+                        rho = _sigma(m)
+                        q, u = 2 * r + (rho >> 4), rho & 15
+                        a = (u + 16 * (q // RPI)) * PITCH + (q % RPI) * 2 * C + 16 * h + 32 * ks
+                        assert a == where_a[(32 * r + rho, 2 * ks + h)]
+                        addrs.append(a)
+                    assert len({(a // 16) % 16 for a in addrs}) == 16
+    # B: instruction I = 8 set + i, lane l -> slot l >> 3, piece l & 7 of the step's 64 columns of W2 row
+    # (2 set + bb) * 32 + tau(16 mhi + 2 i + mlo); the kernel forms that row as a wave-uniform
+    # 64 set + T(i) plus the lane's 32 bb + 8 mhi + mlo
+    def T(i):
+        return 16 * ((i >> 1) & 1) + 4 * (i >> 2) + 2 * (i & 1)
+    where_b = {}
+    for I in range(NIB):
+        st, i = I >> 3, I & 7
+        for lane in range(64):
+            slot, piece = lane >> 3, lane & 7
+            bb, mhi, mlo = slot >> 2, (slot >> 1) & 1, slot & 1
+            o = (2 * st + bb) * 32 + _tau(16 * mhi + 2 * i + mlo)
+            assert o == 64 * st + T(i) + 32 * bb + 8 * mhi + mlo
+            assert (o, piece) not in where_b
+            where_b[(o, piece)] = I * PITCH + 16 * lane
+    assert len(where_b) == C * 8
+    for r in range(2):  # the output half a wave projects
+        for c in range(CBH):
+            for j in range(2):
+                for kk in range(2):
+                    for h in range(2):
+                        for grp in (range(16), range(16, 32)):
+                            addrs = []
+                            for m in grp:
+                                base = ((m >> 1) & 7) * PITCH + (2 * (m >> 4) + (m & 1)) * 128 + 16 * h \
+                                    + 4 * CBH * r * PITCH
+                                a = base + 8 * (c >> 1) * PITCH + 4 * (c & 1) * 128 + 64 * j + 32 * kk
+                                assert a == where_b[((CBH * r + c) * 32 + _tau(m), 4 * j + 2 * kk + h)]
+                                addrs.append(a)
+                            assert len({(a // 16) % 16 for a in addrs}) == 16
