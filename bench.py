@@ -170,12 +170,20 @@ def stack_case(name: str, steps: int, warmup: int):
             h, ww = h // 2, ww // 2
             bufs.append(torch.empty((N, h, ww, c), dtype=xs[0].dtype, device="cuda"))
         bufs.append(torch.empty((N, h, ww, c), dtype=xs[0].dtype, device="cuda"))
-    t = _time(lambda i: cf.stack_forward(xs[i % nsets], layers, bufs=bufs), steps, warmup,
-              torch.cuda.current_stream())
+    eager = lambda i: cf.stack_forward(xs[i % nsets], layers, bufs=bufs)
+    t_eager = _time(eager, steps, warmup, torch.cuda.current_stream())
+    # the launch sequence replayed as one HIP graph per input set
+    try:
+        graphs = [cf.capture_stack(xs[i], layers, bufs) for i in range(nsets)]
+        t = _time(lambda i: graphs[i % nsets].replay(), steps, warmup, torch.cuda.current_stream())
+        mode = "hipGraph replay"
+    except Exception as e:  # capture unavailable: the eager launches are the figure
+        t, mode = t_eager, "eager launches (graph capture failed: %s)" % (str(e).splitlines() or ["?"])[0]
     kern = rl.stack_kernels(N, H, W, depths, widths, E, k)
     flops = sum(n for _, n, _ in kern)
     T, cmax = rl.waterline([(n, b) for _, n, b in kern])
-    return dict(N=N, seconds=t, flops=flops, waterline_T_min_s=T, waterline_C_max=cmax)
+    return dict(N=N, seconds=t, eager_seconds=t_eager, mode=mode, flops=flops, waterline_T_min_s=T,
+                waterline_C_max=cmax)
 
 
 def cpu_baseline(name: str, min_seconds: float = 12.0):
@@ -287,6 +295,7 @@ def main():
                 s = stack_case(nm, max(3, args.steps // 5), 2)
                 extra[nm] = {"ms": round(s["seconds"] * 1e3, 4), "images_per_s": round(s["N"] / s["seconds"], 1),
                              "comp_eff": round(rl.comp_eff(s["flops"], s["seconds"]), 4),
+                             "mode": s["mode"], "eager_ms": round(s["eager_seconds"] * 1e3, 4),
                              "waterline_C_max": round(s["waterline_C_max"], 4)}
         out["other_workloads"] = extra
     if args.calib_copy:

@@ -20,7 +20,7 @@ import torch
 __all__ = [
     "lib", "library_path", "block_forward", "block_autotune", "block_tuned_config", "stage_forward",
     "downsample_forward",
-    "block_forward_unfused", "block_forward_split", "stack_forward", "ConvFirstBlock",
+    "block_forward_unfused", "block_forward_split", "stack_forward", "capture_stack", "ConvFirstBlock",
     "CFError", "EXPORTED_SYMBOLS",
 ]
 
@@ -266,6 +266,21 @@ def stack_forward(x: torch.Tensor, layers: list, act: str = "gelu", stream=None,
             i = j
         step += 1
     return y
+
+
+def capture_stack(x: torch.Tensor, layers: list, bufs: list, act: str = "gelu") -> "torch.cuda.CUDAGraph":
+    """Record the launches of stack_forward(x, layers, bufs=bufs) -- one per
+    fused stage and per down-sampling step -- into one HIP graph.  A replay
+    reruns them on the contents x and bufs have at that time (write the next
+    input into x in place); the result is bufs[-1].  The stage workspaces come
+    from the graph's private memory pool during capture, so a replay allocates
+    nothing.  x, bufs and the layer weights must outlive the graph."""
+    stack_forward(x, layers, act=act, bufs=bufs)  # library loaded, device attributes cached
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        stack_forward(x, layers, act=act, bufs=bufs)
+    return g
 
 
 class ConvFirstBlock(torch.nn.Module):
