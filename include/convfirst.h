@@ -50,7 +50,7 @@ extern "C" {
 typedef enum {
     CF_OK = 0,
     CF_ERR_INVALID = 1,     /* null pointer, bad size, overlap, misalignment, bad enum */
-    CF_ERR_UNSUPPORTED = 2, /* valid request this build has no kernel for (e.g. C % 32 != 0) */
+    CF_ERR_UNSUPPORTED = 2, /* valid request the library has no kernel for (e.g. C % 32 != 0) */
     CF_ERR_WORKSPACE = 3,   /* workspace smaller than the matching *_workspace_bytes() */
     CF_ERR_HIP = 4          /* the HIP runtime reported an error at launch */
 } cf_status;
