@@ -35,6 +35,8 @@ SWEEP = [
     (64, 6, 3, 1, 1, 1),     # a single pixel
     (64, 3, 3, 1, 1, 37),    # one row
     (64, 4, 3, 1, 40, 1),    # one column
+    (64, 4, 3, 1, 3, 56),    # widest row of the 64-channel kernel's halo copy (9 W = 504 slots)
+    (64, 4, 3, 1, 3, 61),    # wider rows: the generic kernel takes the shape
     (128, 4, 3, 2, 11, 10),
     (128, 2, 5, 1, 7, 9),
     (256, 4, 7, 2, 14, 14),
