@@ -174,7 +174,8 @@ __device__ __forceinline__ void dma16s(const void *base, uint32_t voff, uint8_t 
 
 // dma16s for the lanes set in a wave-uniform, nonzero mask (EXEC is set
 // and restored inside the instruction group, so the copy needs no
-// divergent branch).
+// divergent branch).  The mask replaces EXEC rather than narrowing it: call
+// it from wave-uniform control flow, with every lane active.
 __device__ __forceinline__ void dma16m(const void *base, uint32_t voff, uint8_t *lds_wave_base, uint64_t mask) {
     const uint32_t lds = (uint32_t)__builtin_amdgcn_readfirstlane(
         (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds_wave_base);
