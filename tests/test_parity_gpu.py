@@ -193,6 +193,14 @@ def test_workload_block(name):
     ref = oracle_block(x, p, images=imgs)
     r = assert_close(y.cpu()[imgs], ref, what=name)
     say("  fused rel err %.2e" % r)
+    # the benchmark tunes the shape before timing it: check the configuration
+    # the tuner picks here, at full size, and the launches that use it
+    yt = cf.block_autotune(xd, pd)
+    yt2 = cf.block_forward(xd, pd)
+    torch.cuda.synchronize()
+    say("  tuned configuration %d" % cf.block_tuned_config(x.shape, w["C"], w["E"], w["k"], x.dtype))
+    assert_close(yt.cpu()[imgs], ref, what=name + " tuned")
+    assert torch.equal(yt, yt2)
     yu = cf.block_forward_unfused(xd, pd)
     assert_close(yu.cpu()[imgs], ref, what=name + " unfused")
     if w["N"] * w["H"] * w["W"] <= 64 * 4:
