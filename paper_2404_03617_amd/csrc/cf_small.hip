@@ -47,7 +47,10 @@ struct Args {
     int tp;           // pixels per tile
     int halo_rows;    // LDS halo rows per tile
     int chunks_per_group;
-    uint32_t off_d;   // LDS byte offset of the D buffer
+    uint32_t off_d;     // LDS byte offset of the D buffer
+    uint32_t off_zero;  // LDS byte offset of one zero pixel (taps outside the image read it)
+    uint32_t off_s2;    // LDS byte offset of this output slice's s2 (fp32)
+    fused::FastDiv divW, divH;
 };
 
 template <typename T, int C, int KS>
@@ -100,6 +103,12 @@ struct Kern {
         if constexpr (PRELOAD)
             load_chunk(ch0);
 
+        // the zero pixel, and s2 of this output slice
+        for (int i = tid; i < PIXB / 16; i += NT)
+            *reinterpret_cast<u32x4 *>(smem + a.off_zero + i * 16) = u32x4{0u, 0u, 0u, 0u};
+        for (int i = tid; i < CO; i += NT)
+            reinterpret_cast<float *>(smem + a.off_s2)[i] = a.s2 ? a.s2[ob * CO + i] : 1.0f;
+
         // 1. halo rows g_lo - PAD .. into LDS, padded pixels zero
         {
             const int total = rows * WP * C8;
@@ -127,57 +136,119 @@ struct Kern {
 
         // 2. depth-wise conv: item = (pixel of the tile, 8 channels); NT is a
         // multiple of C/8, so a thread always works on the same channel chunk
-        // q and holds its taps, s0 and b0 in registers
+        // q and holds its taps, s0 and b0 in registers.  A tap outside the
+        // pixel's image reads the zero pixel, so the reads of a kernel row
+        // carry no branch and are issued ahead of its FMAs (one wave per
+        // SIMD: nothing else hides their latency).
         {
             const int q = tid % C8;
+            constexpr bool TF = KS <= 3;  // taps as fp32 and branch-free reads (registers permitting)
             Pack8 wt[KS * KS];
 #pragma unroll
             for (int t = 0; t < KS * KS; t++)
                 wt[t].u = *reinterpret_cast<const u32x4 *>(a.dw_w + (size_t)t * C + q * 8);
+            float wtf[TF ? KS * KS : 1][8];
+            if constexpr (TF) {
+#pragma unroll
+                for (int t = 0; t < KS * KS; t++)
+#pragma unroll
+                    for (int e = 0; e < 4; e++) {
+                        wtf[t][2 * e] = T::lo(wt[t].w[e]);
+                        wtf[t][2 * e + 1] = T::hi(wt[t].w[e]);
+                    }
+            }
             float sc[8], bi[8];
 #pragma unroll
             for (int e = 0; e < 8; e++) {
                 sc[e] = a.s0 ? a.s0[q * 8 + e] : 1.0f;
                 bi[e] = a.b0 ? a.b0[q * 8 + e] : 0.0f;
             }
-            for (int pl = tid / C8; pl < a.tp; pl += NT / C8) {
-                const uint32_t p = p0 + pl;
-                float acc[8];
-#pragma unroll
-                for (int e = 0; e < 8; e++)
-                    acc[e] = 0.0f;
-                if (p < a.P) {
-                    const uint32_t gg = p / (uint32_t)a.W;
-                    const int wc = (int)(p - gg * (uint32_t)a.W);
-                    const int hr = (int)(gg % (uint32_t)a.H);
-#pragma unroll
+            if constexpr (TF) {
+                const uint32_t zaddr = a.off_zero + (uint32_t)q * 16;
+                for (int pl = tid / C8; pl < a.tp; pl += NT / C8) {
+                    const uint32_t p = p0 + pl;
+                    const bool pv = p < a.P;
+                    const uint32_t pc = pv ? p : p0;
+                    const uint32_t gg = fused::fdiv(pc, a.divW);
+                    const int wc = (int)(pc - gg * (uint32_t)a.W);
+                    const int hr = (int)(gg - fused::fdiv(gg, a.divH) * (uint32_t)a.H);
+                    float acc[8];
+    #pragma unroll
+                    for (int e = 0; e < 8; e++)
+                        acc[e] = 0.0f;
+    #pragma unroll
                     for (int i = 0; i < KS; i++) {
-                        const int hi = hr + i - PAD;
-                        if (hi < 0 || hi >= a.H)
-                            continue;  // rows of another image: zero padding
+                        const int hi = hr + i - PAD;  // rows of another image or outside the batch: zero padding
+                        const bool rok = pv && hi >= 0 && hi < a.H;
                         const int r = (int)(gg - g_lo) + i;
-#pragma unroll
+                        Pack8 xv[KS];
+    #pragma unroll
                         for (int j = 0; j < KS; j++) {
                             const int wj = wc + j - PAD;
-                            if (wj < 0 || wj >= a.W)
-                                continue;  // zero padding
-                            Pack8 xv;
-                            xv.u = *reinterpret_cast<const u32x4 *>(smem + (r * WP + wj) * PIXB + q * 16);
-#pragma unroll
+                            const bool ok = rok && wj >= 0 && wj < a.W;
+                            const uint32_t ad = ok ? (uint32_t)((r * WP + wj) * PIXB + q * 16) : zaddr;
+                            xv[j].u = *reinterpret_cast<const u32x4 *>(smem + ad);
+                        }
+    #pragma unroll
+                        for (int j = 0; j < KS; j++)
+    #pragma unroll
                             for (int e = 0; e < 4; e++) {
-                                acc[2 * e] = fmaf(T::lo(xv.w[e]), T::lo(wt[i * KS + j].w[e]), acc[2 * e]);
-                                acc[2 * e + 1] = fmaf(T::hi(xv.w[e]), T::hi(wt[i * KS + j].w[e]), acc[2 * e + 1]);
+                                const float w0 = TF ? wtf[TF ? i * KS + j : 0][2 * e] : T::lo(wt[i * KS + j].w[e]);
+                                const float w1 = TF ? wtf[TF ? i * KS + j : 0][2 * e + 1] : T::hi(wt[i * KS + j].w[e]);
+                                acc[2 * e] = fmaf(T::lo(xv[j].w[e]), w0, acc[2 * e]);
+                                acc[2 * e + 1] = fmaf(T::hi(xv[j].w[e]), w1, acc[2 * e + 1]);
+                            }
+                    }
+                    u32x4 d;
+    #pragma unroll
+                    for (int e = 0; e < 4; e++)
+                        d[e] = pv ? T::pack2(fmaf(acc[2 * e], sc[2 * e], bi[2 * e]),
+                                             fmaf(acc[2 * e + 1], sc[2 * e + 1], bi[2 * e + 1]))
+                                  : 0u;
+                    *reinterpret_cast<u32x4 *>(smem + a.off_d + pl * PIXB + q * 16) = d;
+                }
+            } else {
+                // k >= 5: the taps stay packed and rows outside the image are
+                // skipped (registers do not allow every read of a pixel ahead)
+                for (int pl = tid / C8; pl < a.tp; pl += NT / C8) {
+                    const uint32_t p = p0 + pl;
+                    float acc[8];
+    #pragma unroll
+                    for (int e = 0; e < 8; e++)
+                        acc[e] = 0.0f;
+                    if (p < a.P) {
+                        const uint32_t gg = p / (uint32_t)a.W;
+                        const int wc = (int)(p - gg * (uint32_t)a.W);
+                        const int hr = (int)(gg % (uint32_t)a.H);
+    #pragma unroll
+                        for (int i = 0; i < KS; i++) {
+                            const int hi = hr + i - PAD;
+                            if (hi < 0 || hi >= a.H)
+                                continue;  // rows of another image: zero padding
+                            const int r = (int)(gg - g_lo) + i;
+    #pragma unroll
+                            for (int j = 0; j < KS; j++) {
+                                const int wj = wc + j - PAD;
+                                if (wj < 0 || wj >= a.W)
+                                    continue;  // zero padding
+                                Pack8 xv;
+                                xv.u = *reinterpret_cast<const u32x4 *>(smem + (r * WP + wj) * PIXB + q * 16);
+    #pragma unroll
+                                for (int e = 0; e < 4; e++) {
+                                    acc[2 * e] = fmaf(T::lo(xv.w[e]), T::lo(wt[i * KS + j].w[e]), acc[2 * e]);
+                                    acc[2 * e + 1] = fmaf(T::hi(xv.w[e]), T::hi(wt[i * KS + j].w[e]), acc[2 * e + 1]);
+                                }
                             }
                         }
                     }
+                    u32x4 d;
+    #pragma unroll
+                    for (int e = 0; e < 4; e++)
+                        d[e] = p < a.P ? T::pack2(fmaf(acc[2 * e], sc[2 * e], bi[2 * e]),
+                                                  fmaf(acc[2 * e + 1], sc[2 * e + 1], bi[2 * e + 1]))
+                                       : 0u;
+                    *reinterpret_cast<u32x4 *>(smem + a.off_d + pl * PIXB + q * 16) = d;
                 }
-                u32x4 d;
-#pragma unroll
-                for (int e = 0; e < 4; e++)
-                    d[e] = p < a.P ? T::pack2(fmaf(acc[2 * e], sc[2 * e], bi[2 * e]),
-                                              fmaf(acc[2 * e + 1], sc[2 * e + 1], bi[2 * e + 1]))
-                                   : 0u;
-                *reinterpret_cast<u32x4 *>(smem + a.off_d + pl * PIXB + q * 16) = d;
             }
         }
         __syncthreads();
@@ -246,10 +317,11 @@ struct Kern {
 #pragma unroll
                 for (int q = 0; q < 4; q++) {
                     const int c = cb * 32 + 16 * h + 4 * q;
+                    const float4v s2v = *reinterpret_cast<const float4v *>(smem + a.off_s2 + c * 4);
                     float4v v;
 #pragma unroll
                     for (int e = 0; e < 4; e++)
-                        v[e] = acc[cb][4 * q + e] * (a.s2 ? a.s2[ob * CO + c + e] : 1.0f);
+                        v[e] = acc[cb][4 * q + e] * s2v[e];
                     *reinterpret_cast<float4v *>(dst + c) = v;
                 }
             }
@@ -309,7 +381,9 @@ size_t small_split_lds_bytes(const Shape &s) {
         span = (int64_t)s.N * s.H;
     const size_t pixb = (size_t)s.C * 2 + 16;
     const size_t off_d = (((size_t)(span + 2 * (s.k / 2)) * s.W * pixb) + 255) & ~(size_t)255;
-    return off_d + (size_t)tp * pixb;
+    const size_t co = s.C < 128 ? (size_t)s.C : 128;
+    // [halo][D buffer][zero pixel][s2 of the output slice]
+    return off_d + (size_t)(tp + 1) * pixb + co * 4;
 }
 
 // Small-batch hidden-split path: partial[g][P][C] = s2 * (W2 phi(s1 W1 D + b1))
@@ -331,7 +405,10 @@ hipError_t launch_small_split(const void *x, const BlockW &w, const Shape &s, in
     const int halo_rows = (int)span + 2 * pad;
     const size_t pixb = (size_t)s.C * 2 + 16;
     const size_t off_d = (((size_t)halo_rows * s.W * pixb) + 255) & ~(size_t)255;
-    const size_t lds = off_d + (size_t)tp * pixb;
+    const size_t off_zero = off_d + (size_t)tp * pixb;
+    const size_t off_s2 = off_zero + pixb;
+    const size_t co = s.C < 128 ? (size_t)s.C : 128;
+    const size_t lds = off_s2 + co * 4;
     if (lds > 160 * 1024)
         return hipErrorInvalidConfiguration;
     small::Args a{};
@@ -356,6 +433,10 @@ hipError_t launch_small_split(const void *x, const BlockW &w, const Shape &s, in
     a.halo_rows = halo_rows;
     a.chunks_per_group = s.E * s.C / 32 / groups;
     a.off_d = (uint32_t)off_d;
+    a.off_zero = (uint32_t)off_zero;
+    a.off_s2 = (uint32_t)off_s2;
+    a.divW = fused::make_fastdiv((uint32_t)s.W);
+    a.divH = fused::make_fastdiv((uint32_t)s.H);
     return s.bf16 ? small::launch_t<BF16>(a, s.k, tiles, groups, lds, st)
                   : small::launch_t<F16>(a, s.k, tiles, groups, lds, st);
 }
