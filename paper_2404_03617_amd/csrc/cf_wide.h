@@ -685,12 +685,14 @@ struct Ks {
             off = W2OFF + (uint32_t)j * PITCH;
         }
     }
+    // pieces Q0 .. Q1-1 of this wave's copies of chunk ch (W1 pieces first)
+    template <int Q0 = 0, int Q1 = NPW>
     static __device__ __forceinline__ void dma_chunk(const Args &a, uint8_t *smem, int ch, int slot, int wv,
                                                      const LaneOffs &lo) {
         uint8_t *buf = smem + a.off_big + slot * SLOT;
         const int wu = __builtin_amdgcn_readfirstlane(wv);
 #pragma unroll
-        for (int q = 0; q < NPW; q++) {
+        for (int q = Q0; q < Q1; q++) {
             const uint16_t *base;
             bool w1;
             uint32_t off;
@@ -756,8 +758,11 @@ struct Ks {
             for (int c = 0; c < nchg; c++) {
                 fused::wait_vmcnt<0>();  // this wave's copies of chunk c have landed
                 lds_barrier();           // everyone's have; the other slot is free
+                // the next chunk's copies in two halves (W1 now, W2 before the
+                // project), so that each burst fits the copy queue and drains
+                // beside the MFMAs instead of holding the wave at issue
                 if (c + 1 < nchg)
-                    dma_chunk(a, smem, ch0 + c + 1, (c + 1) & 1, wv, lofs);
+                    dma_chunk<0, NPW / 2>(a, smem, ch0 + c + 1, (c + 1) & 1, wv, lofs);
                 const uint8_t *slot = smem + a.off_big + (c & 1) * SLOT;
                 const uint8_t *f1 = slot + w1_row(sigma_row(m)) + h * 16;
                 const uint8_t *f2 = slot + W2OFF + (m >> 2) * PITCH + (m & 3) * 64 + h * 16;
@@ -798,6 +803,8 @@ struct Ks {
                     const int cb = i % CB, kk = i / CB;
                     return (uint32_t)((cb >> 2) * 8 * PITCH + (cb & 3) * 256 + kk * 32);
                 };
+                if (c + 1 < nchg)
+                    dma_chunk<NPW / 2, NPW>(a, smem, ch0 + c + 1, (c + 1) & 1, wv, lofs);
 #pragma unroll
                 for (int i = 0; i < WIN; i++)
                     wf[i] = ld16(f2, w2off(i));
