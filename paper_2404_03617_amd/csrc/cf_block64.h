@@ -107,6 +107,9 @@ inline int halo_rows_for(int tb, int k, int W, int64_t NH) {
     return (int)span + 2 * (k / 2);
 }
 
+__device__ __forceinline__ uint32_t lds_addr(const uint8_t *p) {
+    return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const uint8_t *)p;
+}
 __device__ __forceinline__ u32x4 ld16(const uint8_t *base, uint32_t off) {
     return *reinterpret_cast<const u32x4 *>(base + off);
 }
@@ -254,31 +257,53 @@ struct K64 {
         hl.mask = __ballot(sl < 9 * a.W);
         return hl;
     }
-    // Copy buffer row r of the tile whose first image row is g_lo (rows
-    // rows).  Branch-free, so that an FFN step stays one basic block: when the
-    // wave has nothing to copy, every lane moves the first 16 bytes of x into
-    // a trash area instead (the mask never goes empty).
-    static __device__ __forceinline__ void issue_row(const Args &a, uint8_t *smem, const HaloLane &hl, uint32_t g_lo,
-                                                     int rows, int r) {
-        const int grow = (int)g_lo - PAD + r;
-        const bool ok = r < rows && grow >= 0 && grow < a.NH && hl.mask != 0;  // wave-uniform
-        // masks rather than selects around the address arithmetic (a select
-        // of a 64-bit product becomes a branch)
-        const uint32_t okm = ok ? ~0u : 0u;
-        const size_t rb = (size_t)((uint32_t)grow & okm) * (size_t)((uint32_t)a.W * (C * 2));
-        const uint32_t lds = ok ? a.off_halo + (uint32_t)r * a.rs + hl.loff : a.off_trash;
-        fused::dma16m(reinterpret_cast<const uint8_t *>(a.x) + rb, hl.goff & okm, smem + lds,
-                      ok ? hl.mask : ~0ull);
-    }
-    static __device__ __forceinline__ void issue_halo(const Args &a, uint8_t *smem, const HaloLane &hl, uint32_t g_lo,
-                                                      int rows) {
-        for (int r = 0; r < rows; r++)
-            issue_row(a, smem, hl, g_lo, rows, r);
-    }
+    // The next tile's copy, set up once per tile: buffer row r holds image row
+    // (over N*H) g_lo - PAD + r, and rows rlo .. rlo + span - 1 are the ones
+    // inside the images (span = 0 for a wave whose lanes all lie past the
+    // row's end, or when there is no next tile).  gbase is the global address
+    // of row rlo -- always a valid image row, so a copy that is not needed can
+    // read it harmlessly.
     struct NextHalo {
-        uint32_t g_lo;
-        int rows;  // 0: nothing to copy
+        const uint8_t *gbase;
+        uint32_t rlo, span;
     };
+    static __device__ __forceinline__ NextHalo next_halo(const Args &a, const HaloLane &hl, uint32_t g_lo,
+                                                         int rows) {
+        int rlo = PAD - (int)g_lo;
+        if (rlo < 0)
+            rlo = 0;
+        int rhi = a.NH - (int)g_lo + PAD;
+        if (rhi > rows)
+            rhi = rows;
+        if (hl.mask == 0 || rhi < rlo)
+            rhi = rlo;
+        NextHalo nh;
+        nh.rlo = (uint32_t)rlo;
+        nh.span = (uint32_t)(rhi - rlo);
+        nh.gbase = reinterpret_cast<const uint8_t *>(a.x) +
+                   (size_t)((int)g_lo - PAD + rlo) * (size_t)((uint32_t)a.W * (C * 2));
+        return nh;
+    }
+    // Copy buffer row r.  Branch-free, so that an FFN step stays one basic
+    // block: for a row that is not needed every lane reads the first 16 bytes
+    // of row rlo into a trash area instead (the mask never goes empty).
+    static __device__ __forceinline__ void issue_row(const Args &a, uint32_t lds_base, const HaloLane &hl,
+                                                     const NextHalo &nh, int r) {
+        // okm = all ones when rlo <= r < rlo + span; masks rather than
+        // selects, which the compiler would turn back into a branch
+        const int d = r - (int)nh.rlo;
+        const uint32_t okm = (uint32_t)(~(d >> 31) & ((d - (int)nh.span) >> 31));
+        const uint64_t okm64 = (uint64_t)(int64_t)(int32_t)okm;
+        const uint32_t row_off = ((uint32_t)d & okm) * ((uint32_t)a.W * (C * 2));  // < 2^32: a few image rows
+        const uint32_t dst = a.off_halo + (uint32_t)r * a.rs + hl.loff;
+        const uint32_t lds = lds_base + a.off_trash + ((dst - a.off_trash) & okm);
+        fused::dma16m_at(nh.gbase + row_off, hl.goff & okm, lds, hl.mask | ~okm64);
+    }
+    static __device__ __forceinline__ void issue_halo(const Args &a, uint32_t lds_base, const HaloLane &hl,
+                                                      const NextHalo &nh, int rows) {
+        for (int r = 0; r < rows; r++)
+            issue_row(a, lds_base, hl, nh, r);
+    }
 
     // Base addresses of the KS tap rows of a pixel: the top-left tap of the
     // pixel's window plus i*rs for row i, or (for rows outside the pixel's
@@ -451,7 +476,7 @@ struct K64 {
     struct Ffn {
         const uint8_t *w1p, *w2p;
         u32x4 ones;  // B fragment: 1 at k = 0 for every pixel (bias K step)
-        uint8_t *smem;
+        uint32_t lds_base;  // LDS byte address of the dynamic area
         HaloLane hl;
         NextHalo nh;
     };
@@ -461,7 +486,7 @@ struct K64 {
                                                 float16v (&ue)[2], const float16v (&ua)[2], uint32_t (&ga)[16],
                                                 const uint32_t (&gp)[16], float16v (&acc)[CB][2]) {
         // halo row s of the next tile (the tile touches at most nch + 2 rows)
-        issue_row(a, f.smem, f.hl, f.nh.g_lo, f.nh.rows, s);
+        issue_row(a, f.lds_base, f.hl, f.nh, s);
         if constexpr (ACTV)
             act_blocks<NB>(ua, ga);
         if constexpr (EXP) {
@@ -520,7 +545,7 @@ struct K64 {
         f.w1p = smem + lane * 16;
         f.w2p = smem + a.off_w2 + lane * 16;
         f.ones = u32x4{lane < 32 ? 0x3c00u : 0u, 0u, 0u, 0u};
-        f.smem = smem;
+        f.lds_base = lds_addr(smem);
         f.hl = hl;
         f.nh = nh;
         float16v u0[2], u1[2];
@@ -589,7 +614,7 @@ struct K64 {
             uint32_t g0;
             int r0;
             tile_rows(a, lo, range < a.tile_max ? range : a.tile_max, g0, r0);
-            issue_halo(a, smem, hl, g0, r0);
+            issue_halo(a, lds_addr(smem), hl, next_halo(a, hl, g0, r0), r0);
         }
         int pending = 0;  // output stores this wave issued after its last halo copies
 
@@ -639,11 +664,13 @@ struct K64 {
             __syncthreads();  // the halo buffer is free
             // the next tile's halo streams into LDS, a row per FFN step
             const int t1 = t0 + nblk;
-            NextHalo nh{0u, 0};
+            uint32_t g1 = 0;
+            int rows1 = 0;
             if (it + 1 < nt) {
                 const int nblk1 = (hi - t1) < a.tile_max ? (hi - t1) : a.tile_max;
-                tile_rows(a, t1, nblk1, nh.g_lo, nh.rows);
+                tile_rows(a, t1, nblk1, g1, rows1);
             }
+            const NextHalo nh = next_halo(a, hl, g1, rows1);
             pending = 0;
             if (nb == 2) {
                 ffn<2>(a, smem, lane, hl, nh, dfr, acc);
@@ -652,7 +679,7 @@ struct K64 {
                 ffn<1>(a, smem, lane, hl, nh, dfr, acc);
                 pending = store<1>(a, pix, valid, h, acc);
             } else {
-                issue_halo(a, smem, hl, nh.g_lo, nh.rows);
+                issue_halo(a, lds_addr(smem), hl, nh, rows1);
             }
             t0 = t1;
         }

@@ -202,6 +202,33 @@ __device__ __forceinline__ void dma16m(const void *base, uint32_t voff, uint8_t 
         : "memory");
 }
 
+// As dma16m, with the destination given as an LDS byte address rather than a
+// generic pointer (no address-space conversion in the caller's loop).
+__device__ __forceinline__ void dma16m_at(const void *base, uint32_t voff, uint32_t lds_addr, uint64_t mask) {
+    const uint32_t lds = (uint32_t)__builtin_amdgcn_readfirstlane(lds_addr);
+    const uint64_t b = (uint64_t)(uintptr_t)base;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+    const uint64_t bu = ((uint64_t)hi << 32) | (uint64_t)lo;
+    const uint32_t mlo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)mask);
+    const uint32_t mhi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(mask >> 32));
+    const uint64_t mu = ((uint64_t)mhi << 32) | (uint64_t)mlo;
+    uint64_t saved_exec;
+    uint32_t saved_m0;
+    asm volatile(
+        "s_mov_b64 %0, exec\n\t"
+        "s_mov_b64 exec, %5\n\t"
+        "s_mov_b32 %1, m0\n\t"
+        "s_mov_b32 m0, %4\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %2, %3\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "s_mov_b64 exec, %0"
+        : "=&s"(saved_exec), "=&s"(saved_m0)
+        : "v"(voff), "s"(bu), "s"(lds), "s"(mu)
+        : "memory");
+}
+
 __device__ __forceinline__ float16v mfma32(const u32x4 &a, const u32x4 &b, const float16v &c, F16) {
     Pack8 pa, pb;
     pa.u = a;
