@@ -40,6 +40,31 @@ using fused::mfma32;
 using fused::sigma_row;
 using fused::tau_row;
 
+// LDS byte address of a pointer into the dynamic LDS area
+__device__ __forceinline__ uint32_t lds_addr(const uint8_t *p) {
+    return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const uint8_t *)p;
+}
+// One LDS-DMA instruction (64 lanes x 16 bytes from base + voff to LDS
+// address lds_addr .. + 1 KB), as fused::dma16s, with the destination given as
+// an LDS address (no generic-pointer conversion in the callers' loops).
+__device__ __forceinline__ void dma16s_at(const void *base, uint32_t voff, uint32_t lds_addr_) {
+    const uint32_t lds = (uint32_t)__builtin_amdgcn_readfirstlane(lds_addr_);
+    const uint64_t b = (uint64_t)(uintptr_t)base;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+    const uint64_t bu = ((uint64_t)hi << 32) | (uint64_t)lo;
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %3\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, %2\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(voff), "s"(bu), "s"(lds)
+        : "memory");
+}
+
 constexpr int NW = 8;               // waves; two per 32-pixel block
 constexpr int NBLK = 4;             // blocks per tile
 constexpr int NT = NW * 64;
@@ -241,25 +266,42 @@ struct Kw {
         const int bb = slot >> 2, mhi = (slot >> 1) & 1, mlo = slot & 1;
         return ((uint32_t)(32 * bb + 8 * mhi + mlo) * (uint32_t)(a.nch * 32) + 8 * piece) * 2;
     }
-    static __device__ __forceinline__ void dma_a(const Args &a, uint8_t *smem, int step, int wv, uint32_t la) {
-        uint8_t *buf = buf_a(a, smem, step & 1);
+    // Wave wv issues instructions I = wv + NW i of every buffer.  With NW = 8
+    // and wv < 8, A's instruction I holds W1 row 32 (i >> 1) + 8 (i & 1) + wv
+    // of the step and B's holds output rows 64 i + T(wv): the sources are a
+    // per-wave base plus compile-time (A) or per-launch (B) offsets, set up
+    // once so that a copy costs a few scalar instructions.
+    static_assert(NW == 8, "DMA instruction numbering assumes eight waves");
+    struct DmaBase {
+        const uint8_t *a0;    // W1 row wv (step 0)
+        const uint8_t *b0;    // W2 row T(wv), hidden column 0
+        uint32_t bstride;     // bytes from W2 row r to row r + 64
+        uint32_t lds_a, lds_b;  // LDS address of instruction wv in buffers A0 / B0
+    };
+    static __device__ __forceinline__ DmaBase dma_base(const Args &a, uint8_t *smem, int wv) {
         const int wu = __builtin_amdgcn_readfirstlane(wv);
-#pragma unroll
-        for (int i = 0; i < FA; i++) {
-            const int I = wu + NW * i;
-            const int row = 64 * step + 32 * (I >> 4) + (I & 15);
-            fused::dma16s(a.w1 + (size_t)row * C, la, buf + I * PITCH);
-        }
+        const uint32_t ec = (uint32_t)a.nch * 32;
+        DmaBase d;
+        d.a0 = reinterpret_cast<const uint8_t *>(a.w1) + (size_t)wu * (C * 2);
+        d.b0 = reinterpret_cast<const uint8_t *>(a.w2) + (size_t)t_of(wu) * ec * 2;
+        d.bstride = 64u * ec * 2u;
+        d.lds_a = lds_addr(buf_a(a, smem, 0)) + (uint32_t)wu * PITCH;
+        d.lds_b = lds_addr(buf_b(a, smem, 0)) + (uint32_t)wu * PITCH;
+        return d;
     }
-    static __device__ __forceinline__ void dma_b(const Args &a, uint8_t *smem, int step, int wv, uint32_t lb) {
-        uint8_t *buf = buf_b(a, smem, step & 1);
-        const size_t ec = (size_t)a.nch * 32;
-        const int wu = __builtin_amdgcn_readfirstlane(wv);
+    static __device__ __forceinline__ void dma_a(const DmaBase &d, int step, uint32_t la) {
+        const uint8_t *src = d.a0 + (size_t)step * (64 * C * 2);
+        const uint32_t lds = d.lds_a + (uint32_t)(step & 1) * G::BUF_A;
 #pragma unroll
-        for (int i = 0; i < FB; i++) {
-            const int I = wu + NW * i;
-            fused::dma16s(a.w2 + ((size_t)(64 * (I >> 3)) + t_of(I & 7)) * ec + 64 * step, lb, buf + I * PITCH);
-        }
+        for (int i = 0; i < FA; i++)
+            dma16s_at(src + (32 * (i >> 1) + 8 * (i & 1)) * (C * 2), la, lds + (uint32_t)(i * NW * PITCH));
+    }
+    static __device__ __forceinline__ void dma_b(const DmaBase &d, int step, uint32_t lb) {
+        const uint8_t *src = d.b0 + (size_t)step * 128;
+        const uint32_t lds = d.lds_b + (uint32_t)(step & 1) * G::BUF_B;
+#pragma unroll
+        for (int i = 0; i < FB; i++)
+            dma16s_at(src + (size_t)(i * d.bstride), lb, lds + (uint32_t)(i * NW * PITCH));
     }
     // fragment bases of lane (h, m): expand reads W1 row sigma(m) of chunk r
     // (K step ks at +32 ks); project reads output row tau(m) of block cb,
@@ -414,11 +456,12 @@ struct Kw {
         uint8_t *gmine = smem + a.off_g + (uint32_t)(b * 2 + r) * 2048;
         // prologue: A0 B0 A1 B1 in flight; A0 and B0 must land
         const uint32_t la = lane_a(lane), lb = lane_b(a, lane);
-        dma_a(a, smem, 0, wv, la);
-        dma_b(a, smem, 0, wv, lb);
+        const DmaBase db = dma_base(a, smem, wv);
+        dma_a(db, 0, la);
+        dma_b(db, 0, lb);
         if (nsteps > 1) {
-            dma_a(a, smem, 1, wv, la);
-            dma_b(a, smem, 1, wv, lb);
+            dma_a(db, 1, la);
+            dma_b(db, 1, lb);
             fused::wait_vmcnt<FA + FB>();
         } else {
             fused::wait_vmcnt<0>();
@@ -431,7 +474,7 @@ struct Kw {
             // B_(s+1) goes into the slot B_(s-1) used, free since the last
             // barrier; issued first, so that the copies run beside the MFMAs
             if (s >= 1 && s + 1 < nsteps)
-                dma_b(a, smem, s + 1, wv, lb);
+                dma_b(db, s + 1, lb);
             // ---- expand chunk 2s + r: U/4 = s1 * (W1 D/4) + b1/4, phi, hidden tile to LDS
             const int ch = 2 * s + r;
             const uint8_t *wa = bufa + frag_a(r, lane);
@@ -477,7 +520,7 @@ struct Kw {
             lds_barrier();  // hidden tiles and B_s visible; A_s free
             // A_(s+2) goes into A_s's slot
             if (s + 2 < nsteps)
-                dma_a(a, smem, s + 2, wv, la);
+                dma_a(db, s + 2, la);
             // ---- project both chunks onto this wave's output half
             {
                 constexpr int NF = 4 * CBH;  // W2 fragments used by this wave per step
