@@ -713,34 +713,42 @@ struct Ks {
         o.w2 = ((uint32_t)(32 * bq + r4) * (uint32_t)(a.nch * 32) + 8 * pc) * 2;
         return o;
     }
-    static __device__ __forceinline__ void piece_base(const Args &a, int ch, int q, int wu, const uint16_t *&base,
-                                                      bool &w1, uint32_t &off) {
-        const size_t ec = (size_t)a.nch * 32;
-        if (q < NI1 / NWS) {
-            const int j = wu + NWS * q;  // instruction j: row j (and j + 16 for C = 256)
-            base = a.w1 + ((size_t)ch * 32 + j) * C;
-            w1 = true;
-            off = (uint32_t)j * PITCH;
-        } else {
-            const int j = wu + NWS * (q - NI1 / NWS), st = j >> 3, i = j & 7;
-            base = a.w2 + (size_t)(128 * st + 16 * (i & 1) + 4 * (i >> 1)) * ec + (size_t)ch * 32;
-            w1 = false;
-            off = W2OFF + (uint32_t)j * PITCH;
-        }
+    // Wave wv copies pieces q = 0 .. NPW - 1: W1 instruction j = wv + NWS q
+    // (rows ch*32 + j), then W2 instruction j = wv + NWS q' (q' = q - NI1/NWS)
+    // with set st = j >> 3 and index i = j & 7, that is output rows
+    // 128 st + 16 (i & 1) + 4 (i >> 1) = R(wv) + 128 (q' >> 1) + 8 (q' & 1),
+    // R(wv) = 16 (wv & 1) + 4 (wv >> 1) (NWS = 4, wv < 4).  The per-wave
+    // bases are set up once; a piece adds a compile-time or per-launch offset.
+    static_assert(NWS == 4, "piece numbering assumes four waves");
+    struct CopyBase {
+        const uint8_t *w1, *w2;  // W1 row wv, W2 row R(wv) (chunk 0)
+        uint32_t e2;             // bytes per W2 row
+        uint32_t lds;            // LDS address of instruction wv in slot 0
+    };
+    static __device__ __forceinline__ CopyBase copy_base(const Args &a, uint8_t *smem, int wv) {
+        const int wu = __builtin_amdgcn_readfirstlane(wv);
+        CopyBase cb;
+        cb.e2 = (uint32_t)a.nch * 64;
+        cb.w1 = reinterpret_cast<const uint8_t *>(a.w1) + (size_t)wu * (C * 2);
+        cb.w2 = reinterpret_cast<const uint8_t *>(a.w2) + (size_t)(16 * (wu & 1) + 4 * (wu >> 1)) * cb.e2;
+        cb.lds = lds_addr(smem + a.off_big) + (uint32_t)wu * PITCH;
+        return cb;
     }
     // pieces Q0 .. Q1-1 of this wave's copies of chunk ch (W1 pieces first)
     template <int Q0 = 0, int Q1 = NPW>
-    static __device__ __forceinline__ void dma_chunk(const Args &a, uint8_t *smem, int ch, int slot, int wv,
-                                                     const LaneOffs &lo) {
-        uint8_t *buf = smem + a.off_big + slot * SLOT;
-        const int wu = __builtin_amdgcn_readfirstlane(wv);
+    static __device__ __forceinline__ void dma_chunk(const CopyBase &cb, int ch, int slot, const LaneOffs &lo) {
+        const uint8_t *s1 = cb.w1 + (size_t)ch * (32 * C * 2);
+        const uint8_t *s2 = cb.w2 + (size_t)ch * 64;
+        const uint32_t lds = cb.lds + (uint32_t)slot * SLOT;
 #pragma unroll
         for (int q = Q0; q < Q1; q++) {
-            const uint16_t *base;
-            bool w1;
-            uint32_t off;
-            piece_base(a, ch, q, wu, base, w1, off);
-            fused::dma16s(base, w1 ? lo.w1 : lo.w2, buf + off);
+            if (q < NI1 / NWS) {
+                dma16s_at(s1 + q * NWS * (C * 2), lo.w1, lds + (uint32_t)(q * NWS * PITCH));
+            } else {
+                const int qq = q - NI1 / NWS;
+                dma16s_at(s2 + (size_t)((uint32_t)(128 * (qq >> 1) + 8 * (qq & 1)) * cb.e2), lo.w2,
+                          lds + (uint32_t)(W2OFF + qq * NWS * PITCH));
+            }
         }
     }
     static __device__ void run(const SoloArgs &sa, uint8_t *smem) {
@@ -751,6 +759,7 @@ struct Ks {
         const int grp = blockIdx.y;
         const int ch0 = grp * sa.chunks_per_group, nchg = sa.chunks_per_group;
         const LaneOffs lofs = lane_offs(a, lane);
+        const CopyBase cpb = copy_base(a, smem, wv);
 
         for (uint32_t i = a.off_zero / 16 + tid; i < (a.off_zero + KS * HPX + 64) / 16; i += NTS)
             reinterpret_cast<u32x4 *>(smem)[i] = u32x4{0u, 0u, 0u, 0u};
@@ -796,7 +805,7 @@ struct Ks {
                 for (int e = 0; e < 16; e++)
                     acc[c][e] = 0.0f;
 
-            dma_chunk(a, smem, ch0, 0, wv, lofs);
+            dma_chunk(cpb, ch0, 0, lofs);
 #pragma unroll 1
             for (int c = 0; c < nchg; c++) {
                 fused::wait_vmcnt<0>();  // this wave's copies of chunk c have landed
@@ -805,7 +814,7 @@ struct Ks {
                 // project), so that each burst fits the copy queue and drains
                 // beside the MFMAs instead of holding the wave at issue
                 if (c + 1 < nchg)
-                    dma_chunk<0, NPW / 2>(a, smem, ch0 + c + 1, (c + 1) & 1, wv, lofs);
+                    dma_chunk<0, NPW / 2>(cpb, ch0 + c + 1, (c + 1) & 1, lofs);
                 const uint8_t *slot = smem + a.off_big + (c & 1) * SLOT;
                 const uint8_t *f1 = slot + w1_row(sigma_row(m)) + h * 16;
                 const uint8_t *f2 = slot + W2OFF + (m >> 2) * PITCH + (m & 3) * 64 + h * 16;
@@ -847,7 +856,7 @@ struct Ks {
                     return (uint32_t)((cb >> 2) * 8 * PITCH + (cb & 3) * 256 + kk * 32);
                 };
                 if (c + 1 < nchg)
-                    dma_chunk<NPW / 2, NPW>(a, smem, ch0 + c + 1, (c + 1) & 1, wv, lofs);
+                    dma_chunk<NPW / 2, NPW>(cpb, ch0 + c + 1, (c + 1) & 1, lofs);
 #pragma unroll
                 for (int i = 0; i < WIN; i++)
                     wf[i] = ld16(f2, w2off(i));
