@@ -245,3 +245,72 @@ def test_pair_kernel_dma_layouts_map_fragments_without_conflicts(C):
                                 assert a == where_b[((CBH * r + c) * 32 + _tau(m), 4 * j + 2 * kk + h)]
                                 addrs.append(a)
                             assert len({(a // 16) % 16 for a in addrs}) == 16
+
+
+@pytest.mark.parametrize("C", [128, 256, 512])
+def test_per_wave_copy_bases_match_the_layout_numbering(C):
+    """The kernels issue a wave's copies from a per-wave base plus fixed
+    offsets (restated here from their address formulas); wave wv's i-th copy
+    must be exactly layout instruction I = wv + NW i, whose source row the
+    layout tests above check.  Pair kernel (C = 128 / 256, NW = 8): A copy i
+    reads W1 row wv + 32 (i >> 1) + 8 (i & 1) of the step, B copy i output
+    row T(wv) + 64 i.  C = 512 ring (NW = 4): W1 copy q reads chunk row
+    wv + 4 q, W2 copy q output row R(wv) + 128 (q >> 1) + 8 (q & 1)."""
+    def T(i):
+        return 16 * ((i >> 1) & 1) + 4 * (i >> 2) + 2 * (i & 1)
+    PITCH = 1040
+    if C < 512:
+        NW, RPI = 8, 1024 // (2 * C)
+        NIA, NIB = 64 // RPI, C // 8
+        covered_a, covered_b = set(), set()
+        for wv in range(NW):
+            for i in range(NIA // NW):
+                I = wv + NW * i
+                assert wv + 32 * (i >> 1) + 8 * (i & 1) == 32 * (I >> 4) + (I & 15)
+                assert wv * PITCH + i * NW * PITCH == I * PITCH  # LDS destination
+                covered_a.add(I)
+            for i in range(NIB // NW):
+                I = wv + NW * i
+                assert T(wv) + 64 * i == 64 * (I >> 3) + T(I & 7)
+                covered_b.add(I)
+        assert covered_a == set(range(NIA)) and covered_b == set(range(NIB))
+    else:
+        NWS, NI1, NI2 = 4, 32, 2 * (C // 32)
+        covered1, covered2 = set(), set()
+        for wv in range(NWS):
+            R = 16 * (wv & 1) + 4 * (wv >> 1)
+            for q in range(NI1 // NWS):
+                covered1.add(wv + NWS * q)
+            for q in range(NI2 // NWS):
+                j = wv + NWS * q
+                st, i = j >> 3, j & 7
+                assert R + 128 * (q >> 1) + 8 * (q & 1) == 128 * st + 16 * (i & 1) + 4 * (i >> 1)
+                covered2.add(j)
+        assert covered1 == set(range(NI1)) and covered2 == set(range(NI2))
+
+
+def test_c64_next_halo_rows_and_masks():
+    """The C = 64 kernel's per-tile halo set-up (restated from next_halo and
+    issue_row): buffer row r holds image row g_lo - PAD + r; rows rlo ..
+    rlo + span - 1 are exactly the ones inside the images and the tile; the
+    base row rlo is always a real image row (a skipped copy reads it); and the
+    branch-free mask ~(d >> 31) & ((d - span) >> 31) (32-bit arithmetic
+    shifts) selects exactly 0 <= d < span."""
+    def asr(v):  # 32-bit arithmetic shift right by 31
+        v &= 0xFFFFFFFF
+        return 0xFFFFFFFF if v & 0x80000000 else 0
+    for PAD in (0, 1, 2, 3):
+        for NH in (1, 2, 5, 56, 7168):
+            for g_lo in sorted({0, 1, 2, NH // 2, NH - 2, NH - 1} & set(range(NH))):
+                for rows in (0, 1, 4, 10, 14):
+                    rlo = max(PAD - g_lo, 0)
+                    rhi = min(NH - g_lo + PAD, rows)
+                    if rhi < rlo:
+                        rhi = rlo
+                    span = rhi - rlo
+                    assert 0 <= g_lo - PAD + rlo < NH
+                    for r in range(rows + 3):
+                        want = r < rows and 0 <= g_lo - PAD + r < NH
+                        d = r - rlo
+                        okm = (~asr(d) & 0xFFFFFFFF) & asr(d - span)
+                        assert (okm == 0xFFFFFFFF) == want and okm in (0, 0xFFFFFFFF)
