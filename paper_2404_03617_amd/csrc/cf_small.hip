@@ -50,6 +50,7 @@ struct Args {
     uint32_t off_d;     // LDS byte offset of the D buffer
     uint32_t off_zero;  // LDS byte offset of one zero pixel (taps outside the image read it)
     uint32_t off_s2;    // LDS byte offset of this output slice's s2 (fp32)
+    uint32_t off_w1;    // C = 512: LDS byte offset of the first chunk's W1 rows (0: W1 from global memory)
     fused::FastDiv divW, divH;
 };
 
@@ -61,6 +62,11 @@ struct Kern {
     static constexpr int HB = C == 512 ? 8 : 16;  // halo loads in flight per thread
     // request the first chunk's weights at kernel start (registers permitting)
     static constexpr bool PRELOAD = KS <= 3;
+    // C = 512: a W1 row is 1 KB, one LDS-DMA instruction; rows sit W1P bytes
+    // apart so that the 16 rows sigma(m) of a 16-lane fragment read fall in
+    // 16 different bank groups
+    static constexpr bool LW1 = C == 512;
+    static constexpr uint32_t W1P = 1040;
 
     static __device__ void run(const Args &a, uint8_t *smem) {
         const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -80,11 +86,13 @@ struct Kern {
         // depth-wise conv (one wave per SIMD: the registers are there).
         u32x4 w1r[KST], w2r[2 * CBO];
         float s1r[16], b1r[16];
-        auto load_chunk = [&](int ch) {
+        auto load_chunk = [&](int ch, bool with_w1) {
             const uint16_t *w1p = a.w1 + (size_t)(ch * 32 + sigma_row(m)) * C + 8 * h;
+            if (with_w1) {
 #pragma unroll
-            for (int ks = 0; ks < KST; ks++)
-                w1r[ks] = *reinterpret_cast<const u32x4 *>(w1p + 16 * ks);
+                for (int ks = 0; ks < KST; ks++)
+                    w1r[ks] = *reinterpret_cast<const u32x4 *>(w1p + 16 * ks);
+            }
 #pragma unroll
             for (int i = 0; i < 2 * CBO; i++) {
                 const int cb = i >> 1, kk = i & 1;
@@ -100,8 +108,21 @@ struct Kern {
                 b1r[e] = a.b1 ? a.b1[r] : 0.0f;
             }
         };
+        // C = 512 with room in LDS: the first chunk's W1 (32 KB, the same for
+        // every wave) is copied once per workgroup, 1 KB per contiguous
+        // LDS-DMA instruction, instead of being gathered four times into
+        // registers; wave wv copies rows wv, wv + 4, ...
+        const bool lw1 = LW1 && a.off_w1 != 0;
+        if (lw1) {
+            const uint16_t *src = a.w1 + (size_t)ch0 * 32 * C;
+#pragma unroll
+            for (int i = 0; i < 8; i++) {
+                const int r = wv + 4 * i;
+                fused::dma16s(src + (size_t)r * C, (uint32_t)lane * 16, smem + a.off_w1 + (uint32_t)r * W1P);
+            }
+        }
         if constexpr (PRELOAD)
-            load_chunk(ch0);
+            load_chunk(ch0, !lw1);
 
         // the zero pixel, and s2 of this output slice
         for (int i = tid; i < PIXB / 16; i += NT)
@@ -251,6 +272,8 @@ struct Kern {
                 }
             }
         }
+        if (lw1)
+            fused::wait_vmcnt<0>();  // this wave's W1 copies have landed (published by the barrier)
         __syncthreads();
 
         // 3. this wave's pixels as B fragments: lane (h, m) = channels 16 ks + 8 h .. of pixel 32 wv + m
@@ -258,7 +281,14 @@ struct Kern {
         if (32 * wv >= a.tp)
             return;  // no pixels for this wave (no barrier follows)
         if constexpr (!PRELOAD)
-            load_chunk(ch0);
+            load_chunk(ch0, !lw1);
+        if (lw1) {
+            // fragment (ks, lane h, m) = W1 row sigma(m), halves 16 ks + 8 h ..
+            const uint8_t *w1l = smem + a.off_w1 + (uint32_t)sigma_row(m) * W1P + 16 * h;
+#pragma unroll
+            for (int ks = 0; ks < KST; ks++)
+                w1r[ks] = *reinterpret_cast<const u32x4 *>(w1l + 32 * ks);
+        }
         u32x4 dfr[KST];
 #pragma unroll
         for (int ks = 0; ks < KST; ks++)
@@ -305,7 +335,7 @@ struct Kern {
                 acc[cb] = mfma32(w2r[i], hid, acc[cb], T{});
             }
             if (ch + 1 < ch0 + a.chunks_per_group)
-                load_chunk(ch + 1);
+                load_chunk(ch + 1, true);
         }
 
         // 4. partial = s2 * projection: register e of acc[cb] <-> channel ob*CO + cb*32 + 16h + e
@@ -369,7 +399,8 @@ hipError_t launch_t(Args a, int k, int tiles, int groups, size_t lds, hipStream_
 
 }  // namespace small
 
-// LDS bytes the small-batch kernel needs for this shape, 0 if it does not apply.
+// LDS bytes the small-batch kernel needs for this shape, 0 if it does not apply
+// (the C = 512 launch adds the first chunk's W1 rows when they still fit).
 size_t small_split_lds_bytes(const Shape &s) {
     const int64_t P = (int64_t)s.N * s.H * s.W;
     const int tp = P < small::TPMAX ? (int)P : small::TPMAX;
@@ -408,9 +439,18 @@ hipError_t launch_small_split(const void *x, const BlockW &w, const Shape &s, in
     const size_t off_zero = off_d + (size_t)tp * pixb;
     const size_t off_s2 = off_zero + pixb;
     const size_t co = s.C < 128 ? (size_t)s.C : 128;
-    const size_t lds = off_s2 + co * 4;
+    size_t lds = off_s2 + co * 4;
     if (lds > 160 * 1024)
         return hipErrorInvalidConfiguration;
+    // C = 512: the first chunk's W1 rows through LDS when they fit beside the rest
+    size_t off_w1 = 0;
+    if (s.C == 512) {
+        const size_t o = (lds + 15) & ~(size_t)15;
+        if (o + 32 * (size_t)1040 <= 160 * 1024) {
+            off_w1 = o;
+            lds = o + 32 * (size_t)1040;
+        }
+    }
     small::Args a{};
     a.x = (const uint16_t *)x;
     a.dw_w = (const uint16_t *)w.dw_w;
@@ -435,6 +475,7 @@ hipError_t launch_small_split(const void *x, const BlockW &w, const Shape &s, in
     a.off_d = (uint32_t)off_d;
     a.off_zero = (uint32_t)off_zero;
     a.off_s2 = (uint32_t)off_s2;
+    a.off_w1 = (uint32_t)off_w1;
     a.divW = fused::make_fastdiv((uint32_t)s.W);
     a.divH = fused::make_fastdiv((uint32_t)s.H);
     return s.bf16 ? small::launch_t<BF16>(a, s.k, tiles, groups, lds, st)
