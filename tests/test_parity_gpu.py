@@ -98,8 +98,10 @@ def test_unfused_and_split_match_oracle(case, dtype):
     (128, 4, 5, 2, 9, 7, 8, "f16"),
     (256, 1, 1, 1, 3, 13, 8, "bf16"),
     (256, 4, 7, 2, 14, 14, 16, "f16"),
-    (512, 4, 7, 1, 7, 7, 32, "bf16"),
-    (512, 2, 5, 2, 6, 5, 4, "f16"),
+    (512, 4, 7, 1, 7, 7, 32, "bf16"),    # C = 512, halo + D leave no room: W1 into registers
+    (512, 2, 5, 2, 6, 5, 4, "f16"),      # (same)
+    (512, 4, 3, 1, 7, 7, 64, "f16"),     # C = 512, first chunk's W1 through LDS (one chunk per group)
+    (512, 2, 1, 1, 5, 6, 8, "bf16"),     # W1 of the first chunk through LDS, later chunks into registers
 ], ids=lambda c: "C%d_E%d_k%d_N%d_%dx%d_g%d_%s" % c)
 def test_small_batch_split_matches_oracle(case):
     C, E, k, N, H, W, groups, dtype = case
