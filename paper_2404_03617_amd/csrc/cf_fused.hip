@@ -119,6 +119,15 @@ hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Sha
         }
     }
     const bool special = s.cfg != CFG_GENERIC;
+    // C = 512 in bf16 has no streaming kernel of its own: for a small batch the
+    // single-group small kernel (four workgroups, one per 128 output channels,
+    // each walking all hidden chunks) replaces the generic kernel's single
+    // workgroup.
+    if (!done && special && s.C == 512 && s.bf16 && groups <= 1) {
+        e = launch_small_split(x, w, s, 1, nullptr, st, y);
+        if (e != hipErrorInvalidConfiguration)
+            return e;
+    }
     if (!done && special && s.C == 64 && !s.bf16 && groups <= 1) {
         switch (s.k) {
         case 1: e = launch_block64_k1(x, y, w, s, st); break;

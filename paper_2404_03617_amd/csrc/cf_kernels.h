@@ -42,10 +42,11 @@ hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Sha
                               int groups, float *partial, hipStream_t st);
 
 // Small-batch hidden-split path (at most 8 tiles of 128 pixels): writes the
-// groups' partials only (the caller runs the reduction).  Returns
+// groups' partials only (the caller runs the reduction), or, with one group
+// and y non-null, the block output y itself.  Returns
 // hipErrorInvalidConfiguration when the shape does not suit it.
 hipError_t launch_small_split(const void *x, const BlockW &w, const Shape &s, int groups, float *partial,
-                              hipStream_t st);
+                              hipStream_t st, void *y = nullptr);
 
 size_t small_split_lds_bytes(const Shape &s);  // 0: the small-batch path does not apply
 

@@ -42,6 +42,8 @@ struct Args {
     const uint16_t *w2;
     const float *s2;
     float *partial;  // [groups][P][C]
+    uint16_t *y;     // one hidden group: the block output itself (no partials)
+    const float *b2;
     int H, W, NH, C, EC, act;
     uint32_t P;
     int tp;           // pixels per tile
@@ -338,9 +340,34 @@ struct Kern {
                 load_chunk(ch + 1, true);
         }
 
-        // 4. partial = s2 * projection: register e of acc[cb] <-> channel ob*CO + cb*32 + 16h + e
+        // 4. partial = s2 * projection: register e of acc[cb] <-> channel ob*CO + cb*32 + 16h + e.
+        // With one hidden group and an output pointer the projection is the
+        // whole sum: y = x + s2 * projection + b2, rounded, is stored instead.
         const uint32_t p = p0 + pl;
-        if (pl < a.tp && p < a.P) {
+        if (a.y && pl < a.tp && p < a.P) {
+#pragma unroll
+            for (int cb = 0; cb < CBO; cb++) {
+                const int cl = cb * 32 + 16 * h, c = ob * CO + cl;  // 16 channels c .. c + 15
+                const uint16_t *xp = a.x + (size_t)p * C + c;
+                Pack8 xv[2];
+                xv[0].u = *reinterpret_cast<const u32x4 *>(xp);
+                xv[1].u = *reinterpret_cast<const u32x4 *>(xp + 8);
+                u32x4 o[2];
+#pragma unroll
+                for (int hv = 0; hv < 2; hv++)
+#pragma unroll
+                    for (int q = 0; q < 4; q++) {
+                        const int e0 = 8 * hv + 2 * q;
+                        const float *s2l = reinterpret_cast<const float *>(smem + a.off_s2) + cl + e0;
+                        const float bb0 = a.b2 ? a.b2[c + e0] : 0.0f, bb1 = a.b2 ? a.b2[c + e0 + 1] : 0.0f;
+                        o[hv][q] = T::pack2(T::lo(xv[hv].w[q]) + fmaf(acc[cb][e0], s2l[0], bb0),
+                                            T::hi(xv[hv].w[q]) + fmaf(acc[cb][e0 + 1], s2l[1], bb1));
+                    }
+                uint16_t *yp = a.y + (size_t)p * C + c;
+                *reinterpret_cast<u32x4 *>(yp) = o[0];
+                *reinterpret_cast<u32x4 *>(yp + 8) = o[1];
+            }
+        } else if (pl < a.tp && p < a.P) {
             float *dst = a.partial + ((size_t)blockIdx.y * a.P + p) * C + ob * CO;
 #pragma unroll
             for (int cb = 0; cb < CBO; cb++) {
@@ -418,11 +445,14 @@ size_t small_split_lds_bytes(const Shape &s) {
 }
 
 // Small-batch hidden-split path: partial[g][P][C] = s2 * (W2 phi(s1 W1 D + b1))
-// restricted to the chunks of group g.  Returns hipErrorInvalidConfiguration
+// restricted to the chunks of group g, or with groups = 1 and y non-null
+// y = x + s2 * (W2 phi(s1 W1 D + b1)) + b2.  Returns hipErrorInvalidConfiguration
 // when the shape does not suit it (more than 8 tiles of 128 pixels, or a tile
 // whose halo and D buffer exceed the LDS).
 hipError_t launch_small_split(const void *x, const BlockW &w, const Shape &s, int groups, float *partial,
-                              hipStream_t st) {
+                              hipStream_t st, void *y) {
+    if (y && groups != 1)
+        return hipErrorInvalidValue;
     const int64_t P = (int64_t)s.N * s.H * s.W;
     const int tp = P < small::TPMAX ? (int)P : small::TPMAX;
     const int tiles = (int)((P + tp - 1) / tp);
@@ -462,6 +492,8 @@ hipError_t launch_small_split(const void *x, const BlockW &w, const Shape &s, in
     a.w2 = (const uint16_t *)w.w2;
     a.s2 = w.s2;
     a.partial = partial;
+    a.y = (uint16_t *)y;
+    a.b2 = w.b2;
     a.H = s.H;
     a.W = s.W;
     a.NH = s.N * s.H;
