@@ -53,6 +53,7 @@ struct Args {
     uint32_t off_zero;  // LDS byte offset of one zero pixel (taps outside the image read it)
     uint32_t off_s2;    // LDS byte offset of this output slice's s2 (fp32)
     uint32_t off_w1;    // C = 512: LDS byte offset of the first chunk's W1 rows (0: W1 from global memory)
+    int ring;           // C = 512: later chunks' W1 through a two-slot LDS ring at offset 0 (0: registers)
     fused::FastDiv divW, divH;
 };
 
@@ -69,6 +70,7 @@ struct Kern {
     // 16 different bank groups
     static constexpr bool LW1 = C == 512;
     static constexpr uint32_t W1P = 1040;
+    static constexpr uint32_t RSLOT = 32 * W1P;  // one chunk's W1 rows in the ring
 
     static __device__ void run(const Args &a, uint8_t *smem) {
         const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -280,7 +282,22 @@ struct Kern {
 
         // 3. this wave's pixels as B fragments: lane (h, m) = channels 16 ks + 8 h .. of pixel 32 wv + m
         const int pl = 32 * wv + m;
-        if (32 * wv >= a.tp)
+        // C = 512 with several chunks per group: once every wave holds its D
+        // fragments the halo and D areas are no longer read, and they hold a
+        // two-slot ring of W1 chunks copied by contiguous LDS-DMA (32 KB per
+        // chunk once per workgroup, instead of gathered by each wave).  Every
+        // wave then takes part in the copies and barriers, pixels or not.
+        const bool ring = LW1 && a.ring != 0;
+        const int nchg = a.chunks_per_group;
+        auto issue_ring = [&](int ch, int slot) {
+            const uint16_t *src = a.w1 + (size_t)ch * 32 * C;
+#pragma unroll
+            for (int i = 0; i < 8; i++) {
+                const int r = wv + 4 * i;
+                fused::dma16s(src + (size_t)r * C, (uint32_t)lane * 16, smem + (uint32_t)slot * RSLOT + (uint32_t)r * W1P);
+            }
+        };
+        if (!ring && 32 * wv >= a.tp)
             return;  // no pixels for this wave (no barrier follows)
         if constexpr (!PRELOAD)
             load_chunk(ch0, !lw1);
@@ -297,6 +314,12 @@ struct Kern {
             dfr[ks] = pl < a.tp ? *reinterpret_cast<const u32x4 *>(smem + a.off_d + pl * PIXB + (16 * ks + 8 * h) * 2)
                                 : u32x4{0u, 0u, 0u, 0u};
 
+        if (ring) {
+            __syncthreads();  // every wave holds its D fragments: halo and D areas free
+            if (nchg > 1)
+                issue_ring(ch0 + 1, 0);  // chunk j >= 1 goes to slot (j - 1) & 1
+        }
+
         float16v acc[CBO];
 #pragma unroll
         for (int c = 0; c < CBO; c++)
@@ -304,7 +327,18 @@ struct Kern {
             for (int e = 0; e < 16; e++)
                 acc[c][e] = 0.0f;
 
-        for (int ch = ch0; ch < ch0 + a.chunks_per_group; ch++) {
+        for (int ch = ch0; ch < ch0 + nchg; ch++) {
+            const int j = ch - ch0;
+            if (ring && j >= 1) {
+                fused::wait_vmcnt<0>();  // this wave's copies of chunk j (and its W2, s1, b1) landed
+                __syncthreads();         // chunk j visible; chunk j - 1's slot free
+                if (j + 1 < nchg)
+                    issue_ring(ch + 1, j & 1);
+                const uint8_t *w1l = smem + (uint32_t)((j - 1) & 1) * RSLOT + (uint32_t)sigma_row(m) * W1P + 16 * h;
+#pragma unroll
+                for (int ks = 0; ks < KST; ks++)
+                    w1r[ks] = *reinterpret_cast<const u32x4 *>(w1l + 32 * ks);
+            }
             float16v hh;
 #pragma unroll
             for (int e = 0; e < 16; e++)
@@ -336,8 +370,8 @@ struct Kern {
                 const u32x4 hid = {g[4 * kk], g[4 * kk + 1], g[4 * kk + 2], g[4 * kk + 3]};
                 acc[cb] = mfma32(w2r[i], hid, acc[cb], T{});
             }
-            if (ch + 1 < ch0 + a.chunks_per_group)
-                load_chunk(ch + 1, true);
+            if (ch + 1 < ch0 + nchg)
+                load_chunk(ch + 1, !ring);
         }
 
         // 4. partial = s2 * projection: register e of acc[cb] <-> channel ob*CO + cb*32 + 16h + e.
@@ -508,6 +542,7 @@ hipError_t launch_small_split(const void *x, const BlockW &w, const Shape &s, in
     a.off_zero = (uint32_t)off_zero;
     a.off_s2 = (uint32_t)off_s2;
     a.off_w1 = (uint32_t)off_w1;
+    a.ring = (s.C == 512 && a.chunks_per_group > 1 && off_zero >= 2 * (size_t)32 * 1040) ? 1 : 0;
     a.divW = fused::make_fastdiv((uint32_t)s.W);
     a.divH = fused::make_fastdiv((uint32_t)s.H);
     return s.bf16 ? small::launch_t<BF16>(a, s.k, tiles, groups, lds, st)
