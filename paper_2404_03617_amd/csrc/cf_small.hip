@@ -12,10 +12,14 @@
 //     into an LDS D buffer, d = s0 * conv + b0,
 //  3. wave w takes pixels 32w .. 32w+31 of the tile: it reads its D columns
 //     as MFMA B fragments, then for each hidden chunk of its group runs the
-//     expand (W1 fragments straight from global memory into registers),
-//     phi(s1 * u + b1) in fp32, and the project onto its output channels,
+//     expand (W1 fragments from global memory into registers; for C = 512,
+//     where a W1 row is one 1 KB copy, through LDS by LDS-DMA instead: the
+//     first chunk beside the halo, later chunks through a two-slot ring in
+//     the halo and D areas), phi(s1 * u + b1) in fp32, and the project onto
+//     its output channels,
 //  4. writes s2 * (its projection) as an fp32 partial; a second kernel adds
-//     the groups' partials in order, b2 and x.
+//     the groups' partials in order, b2 and x.  With a single group the
+//     workgroup stores y = x + s2 * projection + b2 itself.
 // The products use v_mfma_f32_32x32x16 with weights as the A operand (rows in
 // the sigma / tau orders of cf_fused_impl.h) and pixels as the B operand.
 #include "cf_device.h"
