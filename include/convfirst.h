@@ -138,7 +138,6 @@ cf_status cf_block_forward_split(const void *x, void *y, void *ws, size_t ws_byt
                                  cf_dtype dt, cf_act act, void *stream);
 size_t cf_split_workspace_bytes(int N, int H, int W, int C, int E, int groups);
 
-/* Thread-local message describing the most recent non-CF_OK status. */
 /* Autotune (Sec. 5.5: the kernel class enumerates the valid kernel
  * configurations for the block's parameters, runs each, keeps the fastest).
  * Same arguments and validation as cf_block_forward.  Synchronous: runs every
@@ -156,6 +155,7 @@ cf_status cf_block_autotune(const void *x, void *y, const cf_block_params *p,
  * for invalid arguments. */
 int cf_block_tuned_config(int N, int H, int W, int C, int E, int k, cf_dtype dt, cf_act act);
 
+/* Thread-local message describing the most recent non-CF_OK status. */
 const char *cf_last_error(void);
 const char *cf_status_string(cf_status s);
 int cf_abi_version(void);

@@ -57,6 +57,9 @@ def lib():
         L.cfref_block_forward.argtypes = blk
         L.cfref_block_forward_loopfused.argtypes = blk
         L.cfref_downsample.argtypes = [_dp, _dp, _dp, _dp, ci, ci, ci, ci, ci, _dp, ci]
+        L.cfref_grouped_conv.argtypes = [_dp, _dp] + [ci] * 9 + [_dp]
+        L.cfref_gconv.argtypes = [_dp, _dp, _dp, _dp, ci, ci, ci, ci, ci, ci, _dp, ci]
+        L.cfref_gblock_forward.argtypes = [_dp] * 10 + [ci] * 8 + [_dp, ci]
         L.cfref_default_threads.restype = ci
         _lib = L
     return _lib
@@ -142,6 +145,57 @@ def downsample(x, wd, sd=None, bd=None, nthreads: int = 0):
     y = np.empty((N, H // 2, W // 2, Cout), dtype=np.float64)
     rc = lib().cfref_downsample(_p(x), _p(wd), _p(sd), _p(bd), N, H, W, Cin, Cout, _p(y), nthreads)
     assert rc >= 0
+    return y
+
+
+def grouped_conv(x, a, groups: int, stride: int = 1, pad: int = 0):
+    """Grouped convolution exactly as eq. f:grouped-conv2d (Sec. 4.1.1) writes
+    it: weights a [K, R, S, T] in the paper's index order, T = C / groups,
+    group of output channel k = floor(k C / (K T)).  x [N,H,W,C] -> [N,Ho,Wo,K].
+    Serial, for small cross-checks."""
+    x, a = _f64(x), _f64(a)
+    N, H, W, C = x.shape
+    K, R, S, T = a.shape
+    assert R == S and C % groups == 0 and T == C // groups
+    Ho = (H + 2 * pad - R) // stride + 1
+    Wo = (W + 2 * pad - R) // stride + 1
+    y = np.empty((N, Ho, Wo, K), dtype=np.float64)
+    rc = lib().cfref_grouped_conv(_p(x), _p(a), N, H, W, C, K, R, T, stride, pad, _p(y))
+    assert rc == 0
+    return y
+
+
+def gconv(x, a, s0=None, b0=None, nthreads: int = 0):
+    """The block's grouped layer: k x k, C -> C channels, group width gw,
+    floor(k/2) zero padding (Sec. 5.3 with eq. f:grouped-conv2d).
+    x [N,H,W,C], a [k,k,C,gw] (the library's tap layout)."""
+    x, a, s0, b0 = _f64(x), _f64(a), _f64(s0), _f64(b0)
+    N, H, W, C = x.shape
+    k, _, C2, gw = a.shape
+    assert a.shape == (k, k, C, gw) and C2 == C and C % gw == 0 and k % 2 == 1
+    d = np.empty_like(x)
+    rc = lib().cfref_gconv(_p(x), _p(a), _p(s0), _p(b0), N, H, W, C, k, gw, _p(d), nthreads)
+    assert rc > 0
+    return d
+
+
+def gblock_forward(x, p: dict, act: str = "relu", nthreads: int = 0):
+    """The ConvFirst block as the paper defines it (Sec. 5.3): grouped k x k
+    conv (group width gw), FFN, residual; norms folded to scale and bias.
+    p holds gw_w [k,k,C,gw], w1 [E*C,C], w2 [C,E*C] and optional s0,b0 [C],
+    s1,b1 [E*C], s2,b2 [C].  The paper's block uses ReLU (Sec. 5.3)."""
+    x = _f64(x)
+    N, H, W, C = x.shape
+    a, w1, w2 = _f64(p["gw_w"]), _f64(p["w1"]), _f64(p["w2"])
+    k, _, _, gw = a.shape
+    EC = w1.shape[0]
+    assert a.shape == (k, k, C, gw) and w1.shape == (EC, C) and w2.shape == (C, EC) and EC % C == 0
+    vec = [_f64(p.get(n)) for n in ("s0", "b0", "s1", "b1", "s2", "b2")]
+    y = np.empty_like(x)
+    rc = lib().cfref_gblock_forward(_p(x), _p(a), _p(vec[0]), _p(vec[1]), _p(w1), _p(vec[2]),
+                                    _p(vec[3]), _p(w2), _p(vec[4]), _p(vec[5]), N, H, W, C, EC // C,
+                                    k, gw, ACTS[act], _p(y), nthreads)
+    assert rc > 0
     return y
 
 

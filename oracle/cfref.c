@@ -96,7 +96,7 @@ typedef struct job job;
 typedef void (*row_fn)(const job *J, int n, int h, double *scratch);
 struct job {
     row_fn fn;
-    int N, H, W, C, E, k, act, Cout;
+    int N, H, W, C, E, k, act, Cout, gw;
     const double *x, *dw_w, *s0, *b0, *w1, *s1, *b1, *w2, *s2, *b2;
     double *y;
     size_t scratch_doubles;
@@ -325,5 +325,149 @@ int cfref_downsample(const double *x, const double *wd, const double *sd, const 
     J.N = N; J.H = H / 2; J.W = W / 2; J.C = Cin; J.Cout = Cout;
     J.x = x; J.w1 = wd; J.s1 = sd; J.b1 = bd; J.y = y;
     J.scratch_doubles = 1;
+    return run_rows(&J, nthreads);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Grouped convolution, eq. f:grouped-conv2d (Sec. 4.1.1), in the paper's own
+ * index order: weights A[K][R][S][T], T = C / G input channels per group,
+ * group index g(k) = floor(k * C / (K * T)).  Zero padding `pad` on every
+ * border and a stride, taps not flipped:
+ *   Y[n,ho,wo,k] = sum_{r<R} sum_{s<S} sum_{t<T} A[k][r][s][t] *
+ *                  X[n, ho*stride + r - pad, wo*stride + s - pad, g(k)*T + t]
+ * Output size Ho = (H + 2 pad - R) / stride + 1, Wo likewise (R = S).
+ * Serial; used on small inputs to cross-check the block's grouped layer
+ * against the paper's definition.  Returns -1 on inconsistent sizes. */
+int cfref_grouped_conv(const double *x, const double *a, int N, int H, int W, int C, int K, int R,
+                       int T, int stride, int pad, double *y)
+{
+    if (T <= 0 || C % T || R <= 0 || stride <= 0 || pad < 0)
+        return -1;
+    int Ho = (H + 2 * pad - R) / stride + 1;
+    int Wo = (W + 2 * pad - R) / stride + 1;
+    if (Ho <= 0 || Wo <= 0)
+        return -1;
+    for (int n = 0; n < N; n++)
+        for (int ho = 0; ho < Ho; ho++)
+            for (int wo = 0; wo < Wo; wo++)
+                for (int k = 0; k < K; k++) {
+                    int g = (int)(((int64_t)k * C) / ((int64_t)K * T));
+                    double acc = 0.0;
+                    for (int r = 0; r < R; r++) {
+                        int hh = ho * stride + r - pad;
+                        if (hh < 0 || hh >= H)
+                            continue;
+                        for (int q = 0; q < R; q++) {
+                            int ww = wo * stride + q - pad;
+                            if (ww < 0 || ww >= W)
+                                continue;
+                            for (int t = 0; t < T; t++)
+                                acc += a[(((int64_t)k * R + r) * R + q) * T + t] *
+                                       x[(((int64_t)n * H + hh) * W + ww) * C + (int64_t)g * T + t];
+                        }
+                    }
+                    y[(((int64_t)n * Ho + ho) * Wo + wo) * K + k] = acc;
+                }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* The ConvFirst block as the paper defines it (Sec. 5.3): a k x k grouped
+ * convolution of group width gw with C input and C output channels, then the
+ * FFN, then the residual shortcut, each batch norm folded into a per-channel
+ * scale and bias.  Grouped taps in the library's layout A[i][j][c][t]
+ * (tap-major, then output channel, then the input channel within the output
+ * channel's group); output channel c reads input channels
+ * floor(c / gw) * gw + t (eq. f:grouped-conv2d with K = C, T = gw):
+ *   D[n,h,w,c] = s0[c] * sum_{i<k} sum_{j<k} sum_{t<gw} A[i][j][c][t] *
+ *                X[n, h+i-k/2, w+j-k/2, floor(c/gw)*gw + t] + b0[c]
+ * One output pixel. */
+static void gconv_pixel(const double *x, const double *a, const double *s0, const double *b0,
+                        int H, int W, int C, int k, int gw, int n, int h, int w, double *out /*[C]*/)
+{
+    int pad = k / 2;
+    for (int c = 0; c < C; c++) {
+        int first = (c / gw) * gw;
+        double acc = 0.0;
+        for (int i = 0; i < k; i++) {
+            int hh = h + i - pad;
+            if (hh < 0 || hh >= H)
+                continue; /* zero padding */
+            for (int j = 0; j < k; j++) {
+                int ww = w + j - pad;
+                if (ww < 0 || ww >= W)
+                    continue; /* zero padding */
+                for (int t = 0; t < gw; t++)
+                    acc += a[(((int64_t)i * k + j) * C + c) * gw + t] *
+                           x[(((int64_t)n * H + hh) * W + ww) * C + first + t];
+            }
+        }
+        out[c] = (s0 ? s0[c] : 1.0) * acc + (b0 ? b0[c] : 0.0);
+    }
+}
+
+/* Grouped layer alone. */
+static void gconv_row(const job *J, int n, int h, double *scratch)
+{
+    (void)scratch;
+    for (int w = 0; w < J->W; w++)
+        gconv_pixel(J->x, J->dw_w, J->s0, J->b0, J->H, J->W, J->C, J->k, J->gw, n, h, w,
+                    J->y + (((int64_t)n * J->H + h) * J->W + w) * J->C);
+}
+
+int cfref_gconv(const double *x, const double *a, const double *s0, const double *b0,
+                int N, int H, int W, int C, int k, int gw, double *d, int nthreads)
+{
+    if (gw <= 0 || C % gw)
+        return -1;
+    job J;
+    memset(&J, 0, sizeof J);
+    J.fn = gconv_row;
+    J.N = N; J.H = H; J.W = W; J.C = C; J.k = k; J.gw = gw;
+    J.x = x; J.dw_w = a; J.s0 = s0; J.b0 = b0; J.y = d;
+    J.scratch_doubles = 1;
+    return run_rows(&J, nthreads);
+}
+
+/* The grouped block layer by layer: D (grouped conv), U = s1 (D W1^T) + b1,
+ * G = phi(U), Z = s2 (G W2^T) + b2, Y = X + Z (eq. e:ffn, Sec. 5.3). */
+static void gblock_row(const job *J, int n, int h, double *scratch)
+{
+    int W = J->W, C = J->C, EC = J->E * J->C;
+    double *D = scratch;              /* [W][C]  */
+    double *U = D + (size_t)W * C;    /* [W][EC] */
+    double *G = U + (size_t)W * EC;   /* [W][EC] */
+    double *Z = G + (size_t)W * EC;   /* [W][C]  */
+    for (int w = 0; w < W; w++)
+        gconv_pixel(J->x, J->dw_w, J->s0, J->b0, J->H, W, C, J->k, J->gw, n, h, w, D + (size_t)w * C);
+    for (int w = 0; w < W; w++)
+        pw_pixel(D + (size_t)w * C, J->w1, J->s1, J->b1, C, EC, U + (size_t)w * EC);
+    for (size_t e = 0; e < (size_t)W * EC; e++)
+        G[e] = cfref_act(U[e], J->act);
+    for (int w = 0; w < W; w++)
+        pw_pixel(G + (size_t)w * EC, J->w2, J->s2, J->b2, EC, C, Z + (size_t)w * C);
+    for (int w = 0; w < W; w++) {
+        int64_t base = (((int64_t)n * J->H + h) * W + w) * C;
+        for (int c = 0; c < C; c++)
+            J->y[base + c] = J->x[base + c] + Z[(size_t)w * C + c];
+    }
+}
+
+int cfref_gblock_forward(const double *x, const double *a, const double *s0, const double *b0,
+                         const double *w1, const double *s1, const double *b1,
+                         const double *w2, const double *s2, const double *b2,
+                         int N, int H, int W, int C, int E, int k, int gw, int act, double *y,
+                         int nthreads)
+{
+    if (gw <= 0 || C % gw)
+        return -1;
+    job J;
+    memset(&J, 0, sizeof J);
+    J.fn = gblock_row;
+    J.N = N; J.H = H; J.W = W; J.C = C; J.E = E; J.k = k; J.gw = gw; J.act = act;
+    J.x = x; J.dw_w = a; J.s0 = s0; J.b0 = b0;
+    J.w1 = w1; J.s1 = s1; J.b1 = b1; J.w2 = w2; J.s2 = s2; J.b2 = b2;
+    J.y = y;
+    J.scratch_doubles = (size_t)W * C * 2 + (size_t)W * E * C * 2;
     return run_rows(&J, nthreads);
 }

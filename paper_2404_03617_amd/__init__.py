@@ -17,11 +17,17 @@ import os
 
 import torch
 
+from .convert import (block_params_from_modules, down_params_from_modules, down_weight_from_conv2d,
+                      dw_weight_from_conv2d, fold_batchnorm, grouped_block_params_from_modules,
+                      grouped_weight_from_conv2d, pw_weight_from_conv2d)
+
 __all__ = [
     "lib", "library_path", "block_forward", "block_autotune", "block_tuned_config", "stage_forward",
     "downsample_forward",
     "block_forward_unfused", "block_forward_split", "stack_forward", "capture_stack", "ConvFirstBlock",
-    "CFError", "EXPORTED_SYMBOLS",
+    "CFError", "EXPORTED_SYMBOLS", "dw_weight_from_conv2d", "grouped_weight_from_conv2d",
+    "pw_weight_from_conv2d", "down_weight_from_conv2d", "fold_batchnorm", "block_params_from_modules",
+    "grouped_block_params_from_modules", "down_params_from_modules",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -34,8 +40,8 @@ ACTS = {"gelu": 0, "relu": 1, "none": 2}
 EXPORTED_SYMBOLS = (
     "cf_block_forward", "cf_stage_forward", "cf_stage_workspace_bytes", "cf_downsample_forward",
     "cf_block_forward_unfused", "cf_unfused_workspace_bytes", "cf_block_forward_split",
-    "cf_split_workspace_bytes", "cf_block_autotune", "cf_block_tuned_config", "cf_last_error",
-    "cf_status_string", "cf_abi_version",
+    "cf_split_workspace_bytes", "cf_block_autotune",
+    "cf_block_tuned_config", "cf_last_error", "cf_status_string", "cf_abi_version",
 )
 
 
@@ -112,6 +118,8 @@ def _stream(stream):
 
 
 def _dims(x: torch.Tensor):
+    if not isinstance(x, torch.Tensor):
+        raise TypeError("x must be a torch.Tensor")
     if x.dim() != 4:
         raise ValueError("x must be [N, H, W, C]")
     if not x.is_contiguous():
@@ -121,36 +129,110 @@ def _dims(x: torch.Tensor):
     return tuple(int(v) for v in x.shape)
 
 
-def _block_struct(p: dict, keep: list) -> _BlockParams:
-    names = {"dw_w": "dw_w", "dw_scale": "s0", "dw_bias": "b0", "w1": "w1", "s1": "s1",
-             "b1": "b1", "w2": "w2", "s2": "s2", "b2": "b2"}
-    vals = {}
-    for field, key in names.items():
-        t = p.get(key)
-        if t is not None:
-            if not t.is_contiguous():
-                raise ValueError("parameter %s must be contiguous" % key)
-            keep.append(t)
-        vals[field] = None if t is None else t.data_ptr()
-    return _BlockParams(**vals)
+def _check_tensor(name: str, t, shape, dtype, device: torch.device):
+    """Shape, dtype, layout and device of one argument, checked before any
+    pointer reaches the library (the C ABI cannot check sizes or address
+    spaces)."""
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError("%s must have shape %s, got %s" % (name, tuple(shape), tuple(t.shape)))
+    if t.dtype != dtype:
+        raise ValueError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if t.device != device:
+        raise ValueError("%s is on %s but x is on %s" % (name, t.device, device))
+
+
+def _check_device(x: torch.Tensor):
+    if x.device.type != "cuda":
+        raise ValueError("x must be a GPU tensor (got device %s)" % x.device)
+
+
+# parameter key -> (shape as a function of C, E*C, k; kind): kind "w" is in
+# x's dtype, "v" is fp32
+_BLOCK_SHAPES = {
+    "dw_w": (lambda C, EC, k: (k, k, C), "w"),
+    "s0": (lambda C, EC, k: (C,), "v"), "b0": (lambda C, EC, k: (C,), "v"),
+    "w1": (lambda C, EC, k: (EC, C), "w"),
+    "s1": (lambda C, EC, k: (EC,), "v"), "b1": (lambda C, EC, k: (EC,), "v"),
+    "w2": (lambda C, EC, k: (C, EC), "w"),
+    "s2": (lambda C, EC, k: (C,), "v"), "b2": (lambda C, EC, k: (C,), "v"),
+}
+_FIELDS = {"dw_w": "dw_w", "s0": "dw_scale", "b0": "dw_bias", "w1": "w1", "s1": "s1",
+           "b1": "b1", "w2": "w2", "s2": "s2", "b2": "b2"}
 
 
 def _block_shape(x, p):
     N, H, W, C = _dims(x)
+    for key in ("dw_w", "w1", "w2"):
+        if not isinstance(p.get(key), torch.Tensor):
+            raise ValueError("block parameter %s is required" % key)
+    if p["dw_w"].dim() != 3 or p["w1"].dim() != 2:
+        raise ValueError("dw_w must be [k, k, C] and w1 [E*C, C]")
     k = int(p["dw_w"].shape[0])
     EC = int(p["w1"].shape[0])
-    if EC % C:
-        raise ValueError("w1 rows must be a multiple of C")
+    if EC % C or EC == 0:
+        raise ValueError("w1 rows must be a positive multiple of C")
     return N, H, W, C, EC // C, k
+
+
+def _block_struct(x: torch.Tensor, p: dict, keep: list) -> _BlockParams:
+    """Validate every block parameter against x, then build the ABI struct."""
+    N, H, W, C, E, k = _block_shape(x, p)
+    unknown = set(p) - set(_BLOCK_SHAPES)
+    if unknown:
+        raise ValueError("unknown block parameters: %s" % sorted(unknown))
+    vals = {}
+    for key, (shape_of, kind) in _BLOCK_SHAPES.items():
+        t = p.get(key)
+        if t is not None:
+            _check_tensor(key, t, shape_of(C, E * C, k), x.dtype if kind == "w" else torch.float32,
+                          x.device)
+            keep.append(t)
+        vals[_FIELDS[key]] = None if t is None else t.data_ptr()
+    return _BlockParams(**vals)
+
+
+def _out(x: torch.Tensor, out, shape=None):
+    shape = tuple(x.shape) if shape is None else tuple(shape)
+    if out is None:
+        return torch.empty(shape, dtype=x.dtype, device=x.device)
+    _check_tensor("out", out, shape, x.dtype, x.device)
+    return out
+
+
+def _workspace(x: torch.Tensor, ws, need: int):
+    """The caller's workspace (uint8, on x's device, at least `need` bytes) or a
+    fresh one."""
+    if ws is None:
+        return torch.empty(need, dtype=torch.uint8, device=x.device) if need else None
+    if not isinstance(ws, torch.Tensor) or ws.dtype != torch.uint8 or not ws.is_contiguous():
+        raise ValueError("ws must be a contiguous uint8 tensor")
+    if ws.device != x.device:
+        raise ValueError("ws is on %s but x is on %s" % (ws.device, x.device))
+    if ws.numel() < need:
+        raise ValueError("ws has %d bytes, needs %d" % (ws.numel(), need))
+    return ws
+
+
+def _prepare_block(x: torch.Tensor, p: dict, act: str, out):
+    """Every check of a block call, in an order that needs no GPU: shapes and
+    dtypes first, then devices.  Returns (y, struct, keep, dims)."""
+    if act not in ACTS:
+        raise ValueError("act must be one of %s" % sorted(ACTS))
+    keep = []
+    bp = _block_struct(x, p, keep)
+    _check_device(x)
+    y = _out(x, out)
+    return y, bp, keep, _block_shape(x, p)
 
 
 def block_forward(x: torch.Tensor, p: dict, act: str = "gelu", out: torch.Tensor | None = None,
                   stream=None) -> torch.Tensor:
     """Fused ConvFirst block (one kernel launch): y = x + FFN(dwconv(x))."""
-    N, H, W, C, E, k = _block_shape(x, p)
-    y = torch.empty_like(x) if out is None else out
-    keep = []
-    bp = _block_struct(p, keep)
+    y, bp, keep, (N, H, W, C, E, k) = _prepare_block(x, p, act, out)
     _check(lib().cf_block_forward(_ptr(x), _ptr(y), ctypes.byref(bp), N, H, W, C, E, k,
                                   DTYPES[x.dtype], ACTS[act], _stream(stream)))
     return y
@@ -160,10 +242,7 @@ def block_autotune(x: torch.Tensor, p: dict, act: str = "gelu", out: torch.Tenso
                    stream=None) -> torch.Tensor:
     """Time every kernel configuration that applies to this block shape, cache
     the fastest for later block_forward calls, return the block's output."""
-    N, H, W, C, E, k = _block_shape(x, p)
-    y = torch.empty_like(x) if out is None else out
-    keep = []
-    bp = _block_struct(p, keep)
+    y, bp, keep, (N, H, W, C, E, k) = _prepare_block(x, p, act, out)
     _check(lib().cf_block_autotune(_ptr(x), _ptr(y), ctypes.byref(bp), N, H, W, C, E, k,
                                    DTYPES[x.dtype], ACTS[act], _stream(stream)))
     return y
@@ -178,14 +257,22 @@ def block_tuned_config(x_shape, C: int, E: int, k: int, dtype=torch.float16, act
 def stage_forward(x: torch.Tensor, blocks: list, act: str = "gelu", out=None, ws=None,
                   stream=None) -> torch.Tensor:
     """`len(blocks)` fused blocks of one shape, ping-ponging through ws."""
-    N, H, W, C, E, k = _block_shape(x, blocks[0])
-    y = torch.empty_like(x) if out is None else out
+    if not blocks:
+        raise ValueError("a stage needs at least one block")
+    if act not in ACTS:
+        raise ValueError("act must be one of %s" % sorted(ACTS))
+    keep = []
+    structs = [_block_struct(x, b, keep) for b in blocks]
+    dims = {_block_shape(x, b) for b in blocks}
+    if len(dims) != 1:
+        raise ValueError("every block of a stage must have the same shape")
+    N, H, W, C, E, k = dims.pop()
+    _check_device(x)
+    y = _out(x, out)
     L = lib()
     need = L.cf_stage_workspace_bytes(len(blocks), N, H, W, C, DTYPES[x.dtype])
-    if ws is None and need:
-        ws = torch.empty(need, dtype=torch.uint8, device=x.device)
-    keep = []
-    arr = (_BlockParams * len(blocks))(*[_block_struct(b, keep) for b in blocks])
+    ws = _workspace(x, ws, need)
+    arr = (_BlockParams * len(blocks))(*structs)
     _check(L.cf_stage_forward(_ptr(x), _ptr(y), _ptr(ws), 0 if ws is None else ws.numel(),
                               arr, len(blocks), N, H, W, C, E, k, DTYPES[x.dtype], ACTS[act],
                               _stream(stream)))
@@ -195,10 +282,17 @@ def stage_forward(x: torch.Tensor, blocks: list, act: str = "gelu", out=None, ws
 def downsample_forward(x: torch.Tensor, p: dict, out=None, stream=None) -> torch.Tensor:
     """2x2 stride-2 conv: p has wd [Cout,2,2,Cin] and optional fp32 sd, bd [Cout]."""
     N, H, W, Cin = _dims(x)
-    Cout = int(p["wd"].shape[0])
-    y = out if out is not None else torch.empty((N, H // 2, W // 2, Cout), dtype=x.dtype,
-                                                device=x.device)
-    dp = _DownParams(w=p["wd"].data_ptr(),
+    wd = p.get("wd")
+    if not isinstance(wd, torch.Tensor) or wd.dim() != 4:
+        raise ValueError("downsample parameter wd [Cout, 2, 2, Cin] is required")
+    Cout = int(wd.shape[0])
+    _check_tensor("wd", wd, (Cout, 2, 2, Cin), x.dtype, x.device)
+    for key in ("sd", "bd"):
+        if p.get(key) is not None:
+            _check_tensor(key, p[key], (Cout,), torch.float32, x.device)
+    _check_device(x)
+    y = _out(x, out, (N, H // 2, W // 2, Cout))
+    dp = _DownParams(w=wd.data_ptr(),
                      scale=None if p.get("sd") is None else p["sd"].data_ptr(),
                      bias=None if p.get("bd") is None else p["bd"].data_ptr())
     _check(lib().cf_downsample_forward(_ptr(x), _ptr(y), ctypes.byref(dp), N, H, W, Cin, Cout,
@@ -209,14 +303,9 @@ def downsample_forward(x: torch.Tensor, p: dict, out=None, stream=None) -> torch
 def block_forward_unfused(x: torch.Tensor, p: dict, act: str = "gelu", out=None, ws=None,
                           stream=None) -> torch.Tensor:
     """Layer-by-layer block: depth-wise, expand GEMM, project GEMM (3 launches)."""
-    N, H, W, C, E, k = _block_shape(x, p)
-    y = torch.empty_like(x) if out is None else out
+    y, bp, keep, (N, H, W, C, E, k) = _prepare_block(x, p, act, out)
     L = lib()
-    need = L.cf_unfused_workspace_bytes(N, H, W, C, E, DTYPES[x.dtype])
-    if ws is None:
-        ws = torch.empty(need, dtype=torch.uint8, device=x.device)
-    keep = []
-    bp = _block_struct(p, keep)
+    ws = _workspace(x, ws, L.cf_unfused_workspace_bytes(N, H, W, C, E, DTYPES[x.dtype]))
     _check(L.cf_block_forward_unfused(_ptr(x), _ptr(y), _ptr(ws), ws.numel(), ctypes.byref(bp),
                                       N, H, W, C, E, k, DTYPES[x.dtype], ACTS[act], _stream(stream)))
     return y
@@ -230,14 +319,9 @@ def split_workspace_bytes(x_shape, C: int, E: int, groups: int = 0) -> int:
 def block_forward_split(x: torch.Tensor, p: dict, act: str = "gelu", groups: int = 0, out=None,
                         ws=None, stream=None) -> torch.Tensor:
     """Fused block with hidden channels split over `groups` workgroups per tile."""
-    N, H, W, C, E, k = _block_shape(x, p)
-    y = torch.empty_like(x) if out is None else out
+    y, bp, keep, (N, H, W, C, E, k) = _prepare_block(x, p, act, out)
     L = lib()
-    need = L.cf_split_workspace_bytes(N, H, W, C, E, groups)
-    if ws is None:
-        ws = torch.empty(need, dtype=torch.uint8, device=x.device)
-    keep = []
-    bp = _block_struct(p, keep)
+    ws = _workspace(x, ws, L.cf_split_workspace_bytes(N, H, W, C, E, groups))
     _check(L.cf_block_forward_split(_ptr(x), _ptr(y), _ptr(ws), ws.numel(), ctypes.byref(bp),
                                     N, H, W, C, E, k, groups, DTYPES[x.dtype], ACTS[act],
                                     _stream(stream)))
@@ -258,12 +342,14 @@ def stack_forward(x: torch.Tensor, layers: list, act: str = "gelu", stream=None,
         if kind == "down":
             y = downsample_forward(y, p, out=out, stream=stream)
             i += 1
-        else:
+        elif kind == "block":
             j = i
             while j < len(layers) and layers[j][0] == "block":
                 j += 1
             y = stage_forward(y, [q for _, q in layers[i:j]], act=act, out=out, stream=stream)
             i = j
+        else:
+            raise ValueError("unknown layer kind %r" % (kind,))
         step += 1
     return y
 
@@ -295,6 +381,12 @@ class ConvFirstBlock(torch.nn.Module):
         self._keys = [k for k, v in params.items() if v is not None]
         for k in self._keys:
             self.register_buffer(k, params[k])
+
+    @classmethod
+    def from_modules(cls, dw, bn0, pw1, bn1, pw2, bn2, act: str = "gelu", dtype=torch.float16):
+        """Build from torch layers (depth-wise nn.Conv2d, 1x1 convs or Linears,
+        inference-mode BatchNorm2d or None), folding each batch norm."""
+        return cls(block_params_from_modules(dw, bn0, pw1, bn1, pw2, bn2, dtype), act=act)
 
     def params(self) -> dict:
         return {k: getattr(self, k) for k in self._keys}

@@ -104,10 +104,17 @@ cf::Shape to_shape(int N, int H, int W, int C, int E, int k, cf_dtype dt, cf_act
 
 cf_status check_fit(const char *what, const cf::Shape &s) {
     const size_t lds = cf::fused_lds_bytes(s);
-    if (lds == 0 || lds > 160 * 1024)
-        return fail(CF_ERR_UNSUPPORTED, "%s: tile for W=%d C=%d k=%d needs %zu bytes of LDS (limit 163840)", what, s.W,
-                    s.C, s.k, lds);
-    return CF_OK;
+    if (lds > 0 && lds <= 160 * 1024)
+        return CF_OK;
+    // C = 512 in bf16 runs the single-group small kernel (one 128-pixel tile per
+    // workgroup) whenever its halo and D buffer fit
+    if (s.C == 512 && s.bf16) {
+        const size_t sl = cf::small_split_lds_bytes(s, true);
+        if (sl > 0 && sl <= 160 * 1024)
+            return CF_OK;
+    }
+    return fail(CF_ERR_UNSUPPORTED, "%s: tile for W=%d C=%d k=%d needs %zu bytes of LDS (limit 163840)", what, s.W,
+                s.C, s.k, lds);
 }
 
 size_t round256(size_t v) { return (v + 255) & ~(size_t)255; }
@@ -153,6 +160,26 @@ int default_groups(int N, int H, int W, int C, int E) {
             best = g;
     }
     return best;
+}
+
+// Checks of the split entry point; on success *need holds the
+// bytes of fp32 partials the call writes (groups * N*H*W * C * 4).
+cf_status check_split(const char *what, const void *x, const void *y, const cf_block_params *p, int N, int H, int W,
+                      int C, int E, int k, int &groups, cf_dtype dt, cf_act act, size_t *need) {
+    cf_status st = check_block(what, x, y, p, N, H, W, C, E, k, dt, act);
+    if (st != CF_OK)
+        return st;
+    if (groups <= 0)
+        groups = default_groups(N, H, W, C, E);
+    const int chunks = E * C / 32;
+    if (groups > chunks || chunks % groups)
+        return fail(CF_ERR_INVALID, "%s: groups=%d must divide E*C/32=%d", what, groups, chunks);
+    *need = (size_t)groups * N * H * W * C * sizeof(float);
+    const cf::Shape s = to_shape(N, H, W, C, E, k, dt, act);
+    const size_t small_lds = cf::small_split_lds_bytes(s);
+    if (!(small_lds > 0 && small_lds <= 160 * 1024) && (st = check_fit(what, s)) != CF_OK)
+        return st;
+    return CF_OK;
 }
 
 }  // namespace
@@ -347,15 +374,10 @@ cf_status cf_block_forward_split(const void *x, void *y, void *ws, size_t ws_byt
                                  int H, int W, int C, int E, int k, int groups, cf_dtype dt, cf_act act,
                                  void *stream) {
     const char *what = "cf_block_forward_split";
-    cf_status st = check_block(what, x, y, p, N, H, W, C, E, k, dt, act);
+    size_t need = 0;
+    cf_status st = check_split(what, x, y, p, N, H, W, C, E, k, groups, dt, act, &need);
     if (st != CF_OK)
         return st;
-    if (groups <= 0)
-        groups = default_groups(N, H, W, C, E);
-    const int chunks = E * C / 32;
-    if (groups > chunks || chunks % groups)
-        return fail(CF_ERR_INVALID, "%s: groups=%d must divide E*C/32=%d", what, groups, chunks);
-    const size_t need = cf_split_workspace_bytes(N, H, W, C, E, groups);
     const size_t bytes = (size_t)N * H * W * C * elem_bytes(dt);
     if (!ws)
         return fail(CF_ERR_INVALID, "%s: ws must be non-NULL", what);
@@ -365,11 +387,8 @@ cf_status cf_block_forward_split(const void *x, void *y, void *ws, size_t ws_byt
         return fail(CF_ERR_WORKSPACE, "%s: ws has %zu bytes, needs %zu", what, ws_bytes, need);
     if (overlap(ws, need, x, bytes) || overlap(ws, need, y, bytes))
         return fail(CF_ERR_INVALID, "%s: ws overlaps x or y", what);
-    const cf::Shape s = to_shape(N, H, W, C, E, k, dt, act);
-    const size_t small_lds = cf::small_split_lds_bytes(s);
-    if (!(small_lds > 0 && small_lds <= 160 * 1024) && (st = check_fit(what, s)) != CF_OK)
-        return st;
-    hipError_t e = cf::launch_fused_block(x, y, to_w(p), s, groups, (float *)ws, (hipStream_t)stream);
+    hipError_t e = cf::launch_fused_block(x, y, to_w(p), to_shape(N, H, W, C, E, k, dt, act), groups, (float *)ws,
+                                          (hipStream_t)stream);
     if (e != hipSuccess)
         return hip_fail(e, what);
     g_err[0] = 0;

@@ -775,21 +775,21 @@ hipError_t launch_k(const void *x, void *y, const BlockW &w, const Shape &s, hip
     switch (s.act) {
     case ACT_GELU: {
         auto kf = block64_kernel<KS, ACT_GELU>;
-        if ((e = hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L.total)))
+        if ((e = allow_full_lds((const void *)kf)))
             return e;
         hipLaunchKernelGGL(kf, dim3(G), dim3(NT), L.total, st, a);
         break;
     }
     case ACT_RELU: {
         auto kf = block64_kernel<KS, ACT_RELU>;
-        if ((e = hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L.total)))
+        if ((e = allow_full_lds((const void *)kf)))
             return e;
         hipLaunchKernelGGL(kf, dim3(G), dim3(NT), L.total, st, a);
         break;
     }
     default: {
         auto kf = block64_kernel<KS, ACT_NONE>;
-        if ((e = hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L.total)))
+        if ((e = allow_full_lds((const void *)kf)))
             return e;
         hipLaunchKernelGGL(kf, dim3(G), dim3(NT), L.total, st, a);
         break;

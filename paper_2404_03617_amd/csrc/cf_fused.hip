@@ -119,10 +119,10 @@ hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Sha
         }
     }
     const bool special = s.cfg != CFG_GENERIC;
-    // C = 512 in bf16 has no streaming kernel of its own: for a small batch the
-    // single-group small kernel (four workgroups, one per 128 output channels,
-    // each walking all hidden chunks) replaces the generic kernel's single
-    // workgroup.
+    // C = 512 in bf16 has no streaming kernel of its own: the single-group
+    // small kernel (one workgroup per 128-pixel tile and 128 output channels,
+    // each walking all hidden chunks) replaces the generic kernel, whose tile
+    // does not fit the LDS beyond a few image rows.
     if (!done && special && s.C == 512 && s.bf16 && groups <= 1) {
         e = launch_small_split(x, w, s, 1, nullptr, st, y);
         if (e != hipErrorInvalidConfiguration)

@@ -1092,7 +1092,7 @@ hipError_t launch_t(const FusedArgs &a0, int groups, hipStream_t st) {
     if constexpr (cfgc.resident) {
         if (resident) {
             auto kfn = fused_block_kernel<C, KS, NWAVE, NB, T, ACT, true>;
-            e = hipFuncSetAttribute((const void *)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            e = allow_full_lds((const void *)kfn);
             if (e != hipSuccess)
                 return e;
             hipLaunchKernelGGL(kfn, grid, dim3(NWAVE * 64), lds, st, a);
@@ -1100,7 +1100,7 @@ hipError_t launch_t(const FusedArgs &a0, int groups, hipStream_t st) {
         }
     }
     auto kfn = fused_block_kernel<C, KS, NWAVE, NB, T, ACT, false>;
-    e = hipFuncSetAttribute((const void *)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    e = allow_full_lds((const void *)kfn);
     if (e != hipSuccess)
         return e;
     hipLaunchKernelGGL(kfn, grid, dim3(NWAVE * 64), lds, st, a);

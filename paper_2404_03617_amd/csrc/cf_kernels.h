@@ -1,5 +1,5 @@
 // cf_kernels.h -- host-side launcher interface between the C ABI layer
-// (cf_api.cpp) and the HIP kernels.  Internal; argument checking has already
+// (cf_api.hip) and the HIP kernels.  Internal; argument checking has already
 // happened when these are called.
 #pragma once
 
@@ -7,7 +7,30 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <mutex>
+#include <set>
+#include <utility>
+
 namespace cf {
+
+// Raise a kernel's dynamic-LDS limit to the 160 KB of a CU, once per (device,
+// kernel) in the process; later launches of that kernel make no runtime call
+// for it (the attribute is a limit, the launch still passes its own size).
+inline hipError_t allow_full_lds(const void *kernel) {
+    static std::mutex mu;
+    static std::set<std::pair<int, const void *>> done;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return e;
+    std::lock_guard<std::mutex> lk(mu);
+    if (done.count({dev, kernel}))
+        return hipSuccess;
+    e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e == hipSuccess)
+        done.insert({dev, kernel});
+    return e;
+}
 
 struct BlockW {
     const void *dw_w;
@@ -48,7 +71,10 @@ hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Sha
 hipError_t launch_small_split(const void *x, const BlockW &w, const Shape &s, int groups, float *partial,
                               hipStream_t st, void *y = nullptr);
 
-size_t small_split_lds_bytes(const Shape &s);  // 0: the small-batch path does not apply
+// LDS bytes of the small-batch kernel for this shape; 0 when it does not apply.
+// direct: one hidden group writing y (no tile-count limit); otherwise the
+// partials of the split variant (at most 8 tiles).
+size_t small_split_lds_bytes(const Shape &s, bool direct = false);
 
 // Layer-by-layer path: depth-wise -> d, expand + act -> h, project + residual -> y.
 hipError_t launch_unfused_block(const void *x, void *y, void *d, void *h, const BlockW &w,

@@ -433,7 +433,7 @@ __global__ __launch_bounds__(NT, 1) void small_kernel(Args a) {
 template <typename T, int C, int KS>
 hipError_t launch_tk(Args a, int tiles, int groups, size_t lds, hipStream_t st) {
     auto kf = small_kernel<T, C, KS>;
-    hipError_t e = hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipError_t e = allow_full_lds((const void *)kf);
     if (e != hipSuccess)
         return e;
     hipLaunchKernelGGL(kf, dim3(tiles, groups, Kern<T, C, KS>::OSPLIT), dim3(NT), lds, st, a);
@@ -464,61 +464,81 @@ hipError_t launch_t(Args a, int k, int tiles, int groups, size_t lds, hipStream_
 
 }  // namespace small
 
+// Tile plan of the small-batch kernel: pixels per tile, halo rows, LDS offsets.
+struct SmallPlan {
+    int tp, tiles, halo_rows;
+    size_t off_d, off_zero, off_s2, off_w1, lds;
+};
+
+// false when the kernel does not apply (partials for more than 8 tiles, or no
+// tile fits the LDS).  Writing y directly (one group, no partials), a tile may
+// shrink below 128 pixels in steps of 32 until its halo and D buffer fit; the
+// waves left without pixels idle.
+static bool small_plan(const Shape &s, bool direct, SmallPlan &pl) {
+    if (s.C != 64 && s.C != 128 && s.C != 256 && s.C != 512)
+        return false;
+    const int64_t P = (int64_t)s.N * s.H * s.W;
+    int tp = P < small::TPMAX ? (int)P : small::TPMAX;
+    for (;;) {
+        const int64_t tiles = (P + tp - 1) / tp;
+        if ((!direct && tiles > 8) || tiles > ((int64_t)1 << 30))
+            return false;
+        // image rows a tile of tp consecutive pixels touches, plus the halo
+        int64_t span = (int64_t)(tp - 1) / s.W + 2;
+        if (span > (int64_t)s.N * s.H)
+            span = (int64_t)s.N * s.H;
+        const int halo_rows = (int)span + 2 * (s.k / 2);
+        const size_t pixb = (size_t)s.C * 2 + 16;
+        pl.off_d = (((size_t)halo_rows * s.W * pixb) + 255) & ~(size_t)255;
+        pl.off_zero = pl.off_d + (size_t)tp * pixb;
+        pl.off_s2 = pl.off_zero + pixb;
+        const size_t co = s.C < 128 ? (size_t)s.C : 128;
+        pl.lds = pl.off_s2 + co * 4;
+        if (pl.lds <= 160 * 1024) {
+            pl.tp = tp;
+            pl.tiles = (int)tiles;
+            pl.halo_rows = halo_rows;
+            break;
+        }
+        if (!direct || tp <= 32)
+            return false;
+        tp = ((tp - 1) / 32) * 32;  // next smaller multiple of 32
+    }
+    // C = 512: the first chunk's W1 rows through LDS when they fit beside the rest
+    pl.off_w1 = 0;
+    if (s.C == 512) {
+        const size_t o = (pl.lds + 15) & ~(size_t)15;
+        if (o + 32 * (size_t)1040 <= 160 * 1024) {
+            pl.off_w1 = o;
+            pl.lds = o + 32 * (size_t)1040;
+        }
+    }
+    return true;
+}
+
 // LDS bytes the small-batch kernel needs for this shape, 0 if it does not apply
 // (the C = 512 launch adds the first chunk's W1 rows when they still fit).
-size_t small_split_lds_bytes(const Shape &s) {
-    const int64_t P = (int64_t)s.N * s.H * s.W;
-    const int tp = P < small::TPMAX ? (int)P : small::TPMAX;
-    const int64_t tiles = (P + tp - 1) / tp;
-    if (tiles > 8 || (s.C != 64 && s.C != 128 && s.C != 256 && s.C != 512))
-        return 0;
-    int64_t span = (int64_t)(tp - 1) / s.W + 2;
-    if (span > (int64_t)s.N * s.H)
-        span = (int64_t)s.N * s.H;
-    const size_t pixb = (size_t)s.C * 2 + 16;
-    const size_t off_d = (((size_t)(span + 2 * (s.k / 2)) * s.W * pixb) + 255) & ~(size_t)255;
-    const size_t co = s.C < 128 ? (size_t)s.C : 128;
-    // [halo][D buffer][zero pixel][s2 of the output slice]
-    return off_d + (size_t)(tp + 1) * pixb + co * 4;
+size_t small_split_lds_bytes(const Shape &s, bool direct) {
+    SmallPlan pl;
+    return small_plan(s, direct, pl) ? pl.lds : 0;
 }
 
 // Small-batch hidden-split path: partial[g][P][C] = s2 * (W2 phi(s1 W1 D + b1))
 // restricted to the chunks of group g, or with groups = 1 and y non-null
 // y = x + s2 * (W2 phi(s1 W1 D + b1)) + b2.  Returns hipErrorInvalidConfiguration
-// when the shape does not suit it (more than 8 tiles of 128 pixels, or a tile
-// whose halo and D buffer exceed the LDS).
+// when the shape does not suit it (partials for more than 8 tiles of 128
+// pixels, or no tile whose halo and D buffer fit the LDS).  Writing y
+// directly, every workgroup owns one tile, so any number of tiles works.
 hipError_t launch_small_split(const void *x, const BlockW &w, const Shape &s, int groups, float *partial,
                               hipStream_t st, void *y) {
     if (y && groups != 1)
         return hipErrorInvalidValue;
+    SmallPlan pl;
+    if (!small_plan(s, y != nullptr, pl))
+        return hipErrorInvalidConfiguration;
     const int64_t P = (int64_t)s.N * s.H * s.W;
-    const int tp = P < small::TPMAX ? (int)P : small::TPMAX;
-    const int tiles = (int)((P + tp - 1) / tp);
-    if (tiles > 8 || (s.C != 64 && s.C != 128 && s.C != 256 && s.C != 512))
-        return hipErrorInvalidConfiguration;
-    const int pad = s.k / 2;
-    // image rows a tile of tp consecutive pixels touches, plus the halo
-    int64_t span = (int64_t)(tp - 1) / s.W + 2;
-    if (span > (int64_t)s.N * s.H)
-        span = (int64_t)s.N * s.H;
-    const int halo_rows = (int)span + 2 * pad;
-    const size_t pixb = (size_t)s.C * 2 + 16;
-    const size_t off_d = (((size_t)halo_rows * s.W * pixb) + 255) & ~(size_t)255;
-    const size_t off_zero = off_d + (size_t)tp * pixb;
-    const size_t off_s2 = off_zero + pixb;
-    const size_t co = s.C < 128 ? (size_t)s.C : 128;
-    size_t lds = off_s2 + co * 4;
-    if (lds > 160 * 1024)
-        return hipErrorInvalidConfiguration;
-    // C = 512: the first chunk's W1 rows through LDS when they fit beside the rest
-    size_t off_w1 = 0;
-    if (s.C == 512) {
-        const size_t o = (lds + 15) & ~(size_t)15;
-        if (o + 32 * (size_t)1040 <= 160 * 1024) {
-            off_w1 = o;
-            lds = o + 32 * (size_t)1040;
-        }
-    }
+    const int tp = pl.tp, tiles = pl.tiles, halo_rows = pl.halo_rows;
+    const size_t off_d = pl.off_d, off_zero = pl.off_zero, off_s2 = pl.off_s2, off_w1 = pl.off_w1, lds = pl.lds;
     small::Args a{};
     a.x = (const uint16_t *)x;
     a.dw_w = (const uint16_t *)w.dw_w;

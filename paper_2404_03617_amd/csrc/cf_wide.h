@@ -973,7 +973,7 @@ hipError_t launch_ck(const void *x, void *y, const BlockW &w, const Shape &s, hi
 #define CF_WIDE_LAUNCH(ACTV)                                                                                         \
     {                                                                                                                 \
         auto kf = wide_kernel<C, KS, ACTV>;                                                                          \
-        if ((e = hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L.total))) \
+        if ((e = allow_full_lds((const void *)kf))) \
             return e;                                                                                                 \
         hipLaunchKernelGGL(kf, dim3(Gn), dim3(NT), L.total, st, a);                                                  \
     }
@@ -1063,7 +1063,7 @@ hipError_t launch_solo(const void *x, void *y, const BlockW &w, const Shape &s, 
 #define CF_SOLO_LAUNCH(ACTV)                                                                                         \
     {                                                                                                                 \
         auto kf = solo_kernel<C, KS, ACTV>;                                                                             \
-        if ((e = hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L.total))) \
+        if ((e = allow_full_lds((const void *)kf))) \
             return e;                                                                                                 \
         hipLaunchKernelGGL(kf, dim3(gx, groups), dim3(256), L.total, st, sa);                                       \
     }

@@ -7,6 +7,11 @@ from paper_2404_03617_amd import synth
 
 # max |gpu - ref| <= TOL * max |ref|, for fp16 and bf16 I/O alike
 TOL = 2e-2
+# Diagnostic bound for fp16 I/O, not the gate: the kernels keep the depth-wise
+# output and the hidden values in fp16 and accumulate in fp32, which puts
+# max|err| / max|ref| near 1e-3; a dropped bias, a wrong scale or a misplaced
+# fragment that the loose gate could absorb shows up well above this.
+DIAG_F16 = 5e-3
 
 
 def make_block(seed, N, H, W, C, E, k, dtype="f16", scales="uniform", bias_std=1.0, layer=0):
@@ -30,7 +35,17 @@ def rel_err(gpu, ref):
     return float(err.max() / max(np.abs(ref).max(), 1e-30)), float(err.max()), float(np.abs(ref).max())
 
 
-def assert_close(gpu, ref, tol=TOL, what=""):
+def assert_close(gpu, ref, tol=TOL, what="", diag=None):
+    """The parity gate (and, when `diag` is given, the tighter diagnostic
+    bound).  Prints the measured ratio so every run records it."""
     r, e, m = rel_err(gpu, ref)
+    print("  %s: max|err|/max|ref| = %.2e (max|ref| %.3g)" % (what, r, m), flush=True)
     assert r <= tol, "%s: max|err|=%.3e max|ref|=%.3e ratio=%.3e > %.1e" % (what, e, m, r, tol)
+    if diag is not None:
+        assert r <= diag, "%s: diagnostic bound: ratio %.3e > %.1e" % (what, r, diag)
     return r
+
+
+def log_uniform(seed, tid, n, lo, hi):
+    """Per-channel scales spread over several decades (folded batch norms)."""
+    return synth.to_f32(np.exp(synth.draw_uniform(seed, tid, (n,), np.log(lo), np.log(hi))))

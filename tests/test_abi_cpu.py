@@ -314,3 +314,4 @@ def test_c64_next_halo_rows_and_masks():
                         d = r - rlo
                         okm = (~asr(d) & 0xFFFFFFFF) & asr(d - span)
                         assert (okm == 0xFFFFFFFF) == want and okm in (0, 0xFFFFFFFF)
+

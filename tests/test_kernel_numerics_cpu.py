@@ -1,0 +1,103 @@
+"""Host-side checks of the kernels' own arithmetic choices (CPU only).
+
+The fp16 fused kernels evaluate GELU with a packed-fp16 polynomial in the
+scaled variable w = u / 4 (cf_device.h).  The header promises
+|GELU_device(u) - u * Phi(u)| < 3.4e-3 for |u| < 10 and exact saturation
+beyond.  This test replays the device sequence -- every fp16 rounding of
+s = w*w, four Horner fmas, p = fma(w, q, 0.5), clamp to [0, 1], w * p --
+over every finite fp16 w, with the coefficients parsed from the kernel
+header (so it checks what the kernels compile), against Phi computed with
+math.erf in double precision.
+"""
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+DEVICE_H = os.path.join(ROOT, "paper_2404_03617_amd", "csrc", "cf_device.h")
+HEADER = os.path.join(ROOT, "include", "convfirst.h")
+
+BOUND = 3.4e-3  # the figure quoted by include/convfirst.h and cf_device.h
+
+
+def kernel_coefficients():
+    src = open(DEVICE_H).read()
+    c = [float(re.search(r"GELU_Q%d\s*=\s*([-+0-9.eE]+)f" % i, src).group(1)) for i in range(5)]
+    return c
+
+
+def f16(v):
+    return np.asarray(v, dtype=np.float64).astype(np.float16).astype(np.float64)
+
+
+def device_gelu_quarter(w, c):
+    """GELU(4 w) / 4 as the kernels evaluate it: each packed fp16 operation
+    rounds once to fp16 (fp16 x fp16 products are exact in fp64, so rounding
+    the fp64 fma result once reproduces the hardware fma)."""
+    c = [float(f16(v)) for v in c]
+    s = f16(w * w)
+    q = f16(s * c[4] + c[3])
+    q = f16(s * q + c[2])
+    q = f16(s * q + c[1])
+    q = f16(s * q + c[0])
+    p = np.minimum(np.maximum(f16(w * q + 0.5), 0.0), 1.0)
+    return f16(w * p)
+
+
+def all_finite_f16():
+    h = np.arange(65536, dtype=np.uint16).view(np.float16)
+    return h[np.isfinite(h)].astype(np.float64)
+
+
+def exact_gelu(u):
+    phi = np.frompyfunc(lambda v: 0.5 * (1.0 + math.erf(v / math.sqrt(2.0))), 1, 1)
+    return u * phi(u).astype(np.float64)
+
+
+def gelu_errors(c):
+    w = all_finite_f16()
+    u = 4.0 * w
+    with np.errstate(over="ignore", invalid="ignore"):
+        got = 4.0 * device_gelu_quarter(w, c)
+    err = np.abs(got - exact_gelu(u))
+    inner = np.abs(u) < 10.0
+    return got, err, inner, u
+
+
+def test_header_quotes_the_bound_this_test_checks():
+    assert "3.4e-3" in open(HEADER).read()
+    assert "3.4e-3" in open(DEVICE_H).read()
+
+
+def test_fp16_gelu_error_bound_over_every_finite_input():
+    got, err, inner, u = gelu_errors(kernel_coefficients())
+    assert np.isfinite(got).all(), "the device sequence produced inf or NaN"
+    assert err[inner].max() < BOUND, "max |error| for |u| < 10 is %.3e" % err[inner].max()
+    # beyond |u| = 10 the clamp saturates: GELU(u) = u above, 0 below, to
+    # within the fp16 rounding of u itself (u is exact: w is fp16)
+    assert (err[~inner] / np.abs(u[~inner])).max() < 1e-15
+
+
+def test_fp16_gelu_is_monotone_where_the_exact_function_is():
+    """GELU is increasing for u > -0.75; the device curve must not dip by more
+    than the error bound there (a wrong-signed coefficient would)."""
+    w = np.sort(all_finite_f16())
+    u = 4.0 * w
+    keep = (u > -0.5) & (u < 10.0)
+    with np.errstate(over="ignore", invalid="ignore"):
+        g = 4.0 * device_gelu_quarter(w[keep], kernel_coefficients())
+    drops = np.maximum.accumulate(g) - g
+    assert drops.max() < 2 * BOUND
+
+
+@pytest.mark.parametrize("i,delta", [(0, 0.01), (2, -0.05), (4, 0.02)])
+def test_the_bound_detects_a_perturbed_coefficient(i, delta):
+    """A small change to any one coefficient breaks the bound: the test is
+    tight enough to notice a mistyped constant."""
+    c = kernel_coefficients()
+    c[i] += delta
+    _, err, inner, _ = gelu_errors(c)
+    assert err[inner].max() > BOUND

@@ -1,9 +1,9 @@
 """Parity of the HIP path (through the C ABI) with the fp64 oracle.
 
-Gate: max |gpu - oracle| <= 2e-2 * max |oracle| (fp16 and bf16 I/O).
-Small shapes are compared element by element over the whole output; the
-batch-128 workloads are run at full size and compared on a subset of images
-(images are independent: see the oracle's batch-independence pin)."""
+Gate: max |gpu - oracle| <= 2e-2 * max |oracle| (fp16 and bf16 I/O); the fp16
+sweep also meets a tighter diagnostic bound (DIAG_F16).  Every output is
+compared element by element over the whole tensor, the batch-128 workloads and
+the four-stage stack included."""
 import sys
 
 import numpy as np
@@ -15,7 +15,7 @@ import paper_2404_03617_amd as cf
 from paper_2404_03617_amd import synth
 from paper_2404_03617_amd.workloads import WORKLOADS
 
-from _util import TOL, assert_close, make_block, oracle_block, rel_err, to_dev
+from _util import DIAG_F16, TOL, assert_close, log_uniform, make_block, oracle_block, rel_err, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -55,7 +55,8 @@ def test_fused_block_matches_oracle(case, dtype):
     for act in ("gelu", "relu", "none"):
         y = cf.block_forward(x.cuda(), to_dev(p), act=act)
         torch.cuda.synchronize()
-        assert_close(y, oracle_block(x, p, act), what="%s %s %s" % (case, dtype, act))
+        assert_close(y, oracle_block(x, p, act), what="%s %s %s" % (case, dtype, act),
+                     diag=DIAG_F16 if dtype == "f16" else None)
 
 
 # Batches large enough that every workgroup walks several tiles, with halo
@@ -69,9 +70,7 @@ def test_c64_many_tiles_per_workgroup(case):
     x, p = make_block(21, N, W, W, 64, 4, k, "f16")
     y = cf.block_forward(x.cuda(), to_dev(p))
     torch.cuda.synchronize()
-    imgs = [0, 1, N // 3, N // 2 - 1, N - 1]
-    ref = oracle_block(x, p, images=imgs)
-    assert_close(y.cpu()[imgs], ref, what="c64 W=%d N=%d k=%d" % (W, N, k))
+    assert_close(y.cpu(), oracle_block(x, p), what="c64 W=%d N=%d k=%d" % (W, N, k), diag=DIAG_F16)
 
 
 @pytest.mark.parametrize("dtype", ["f16", "bf16"])
@@ -159,6 +158,46 @@ def test_deterministic_and_batch_independent():
     assert torch.equal(a[1:2], one)
 
 
+# Every kernel family: replacing image 0's input must leave every other image's
+# output bit for bit unchanged (no halo or tile reads across images), and must
+# change image 0's.
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("case", [(64, 4, 3, 5, 14, 14), (128, 4, 3, 5, 11, 13), (256, 4, 7, 5, 14, 14),
+                                  (512, 4, 3, 5, 7, 7), (256, 2, 5, 3, 9, 6)],
+                         ids=lambda c: "C%d_E%d_k%d_N%d_%dx%d" % c)
+def test_images_are_independent(case, dtype):
+    C, E, k, N, H, W = case
+    say("batch independence", case, dtype)
+    x, p = make_block(17, N, H, W, C, E, k, dtype)
+    xd, pd = x.cuda(), to_dev(p)
+    y = cf.block_forward(xd, pd)
+    x2 = xd.clone()
+    x2[0] = synth.activations(18, 1, H, W, C, dtype)[0].cuda()
+    y2 = cf.block_forward(x2, pd)
+    torch.cuda.synchronize()
+    assert torch.equal(y[1:], y2[1:]), "other images changed when image 0 did"
+    assert not torch.equal(y[0], y2[0])
+    assert_close(y2, oracle_block(x2.cpu(), p), what="perturbed batch %s %s" % (case, dtype))
+
+
+# Folded batch norms give per-channel scales over several decades; the fp16
+# C = 64 kernel folds s1 and s2 into fp16 weights, so check that path (and the
+# others) over scales from 1e-3 to 1e2.
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("C", [64, 128, 256, 512])
+def test_wide_range_scales(C, dtype):
+    E, k = 4, 3
+    say("wide scales", C, dtype)
+    x, p = make_block(51, 2, 7, 9, C, E, k, dtype, bias_std=0.5)
+    p["s0"] = log_uniform(51, 901, C, 1e-2, 1e1)
+    p["s1"] = log_uniform(51, 902, E * C, 1e-3, 1e2)
+    p["s2"] = log_uniform(51, 903, C, 1e-2, 1e1)
+    y = cf.block_forward(x.cuda(), to_dev(p))
+    torch.cuda.synchronize()
+    assert torch.isfinite(y).all()
+    assert_close(y, oracle_block(x, p), what="wide scales C=%d %s" % (C, dtype))
+
+
 def test_stage_and_downsample_match_oracle():
     say("stage+down")
     layers = synth.stack_layers(16, depths=(2, 1), widths=(64, 128), E=4, k=3, dtype="f16",
@@ -191,23 +230,26 @@ def test_workload_block(name):
     xd, pd = x.cuda(), to_dev(p)
     y = cf.block_forward(xd, pd)
     torch.cuda.synchronize()
-    imgs = list(range(w["N"])) if w["N"] <= 4 else [0, 1, w["N"] // 2 - 1, w["N"] - 1]
-    ref = oracle_block(x, p, images=imgs)
-    r = assert_close(y.cpu()[imgs], ref, what=name)
-    say("  fused rel err %.2e" % r)
+    ref = oracle_block(x, p)                       # the whole batch
+    assert_close(y.cpu(), ref, what=name)
     # the benchmark tunes the shape before timing it: check the configuration
     # the tuner picks here, at full size, and the launches that use it
     yt = cf.block_autotune(xd, pd)
     yt2 = cf.block_forward(xd, pd)
     torch.cuda.synchronize()
     say("  tuned configuration %d" % cf.block_tuned_config(x.shape, w["C"], w["E"], w["k"], x.dtype))
-    assert_close(yt.cpu()[imgs], ref, what=name + " tuned")
+    assert_close(yt.cpu(), ref, what=name + " tuned")
     assert torch.equal(yt, yt2)
     yu = cf.block_forward_unfused(xd, pd)
-    assert_close(yu.cpu()[imgs], ref, what=name + " unfused")
+    assert_close(yu.cpu(), ref, what=name + " unfused")
     if w["N"] * w["H"] * w["W"] <= 64 * 4:
         ys = cf.block_forward_split(xd, pd)
-        assert_close(ys.cpu()[imgs], ref, what=name + " split")
+        assert_close(ys.cpu(), ref, what=name + " split")
+    del ref
+    # ReLU at full size (the benchmark reports it beside GELU)
+    yr = cf.block_forward(xd, pd, act="relu")
+    torch.cuda.synchronize()
+    assert_close(yr.cpu(), oracle_block(x, p, "relu"), what=name + " relu")
 
 
 def test_stack_graph_replays_match_eager():
@@ -243,7 +285,7 @@ def test_workload_stack():
     y = cf.stack_forward(x.cuda(), [(kd, to_dev(p)) for kd, p in layers])
     torch.cuda.synchronize()
     assert y.shape == (w["N"], 7, 7, 512)
-    imgs = [0, w["N"] - 1]
-    ref = oracle.stack_forward(synth.to_f64(x[imgs]), [(kd, synth.params_f64(p)) for kd, p in layers])
-    r = assert_close(y.cpu()[imgs], ref, what=name)
+    # all 128 images through the fp64 oracle (a few seconds on the host cores)
+    ref = oracle.stack_forward(synth.to_f64(x), [(kd, synth.params_f64(p)) for kd, p in layers])
+    r = assert_close(y.cpu(), ref, what=name)
     say("  stack rel err %.2e" % r)
