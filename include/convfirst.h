@@ -138,6 +138,23 @@ cf_status cf_block_forward_split(const void *x, void *y, void *ws, size_t ws_byt
                                  cf_dtype dt, cf_act act, void *stream);
 size_t cf_split_workspace_bytes(int N, int H, int W, int C, int E, int groups);
 
+/* Allocation-free variant of cf_block_forward_split, for callers that cannot
+ * allocate device memory: code under stream capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same arguments and result as
+ * cf_block_forward_split with the same `groups` (bit for bit), minus the
+ * workspace: the fp32 partials go to a static device array of
+ * CF_SPLIT_SCRATCH_BYTES bytes that the library holds on every GPU it runs on
+ * until the process ends.  It calls no allocating routine.  A call whose
+ * partials (cf_split_workspace_bytes) exceed the array returns
+ * CF_ERR_WORKSPACE and launches nothing.  Every call on one GPU shares that
+ * GPU's array, so calls that overlap in time on one GPU (other streams, other
+ * threads) race and must be serialised by the caller; the array needs no
+ * clearing (each call overwrites the part it reads). */
+#define CF_SPLIT_SCRATCH_BYTES ((size_t)16 << 20)
+cf_status cf_block_forward_split_noalloc(const void *x, void *y, const cf_block_params *p,
+                                         int N, int H, int W, int C, int E, int k, int groups,
+                                         cf_dtype dt, cf_act act, void *stream);
+
 /* Autotune (Sec. 5.5: the kernel class enumerates the valid kernel
  * configurations for the block's parameters, runs each, keeps the fastest).
  * Same arguments and validation as cf_block_forward.  Synchronous: runs every

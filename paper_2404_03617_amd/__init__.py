@@ -24,7 +24,7 @@ from .convert import (block_params_from_modules, down_params_from_modules, down_
 __all__ = [
     "lib", "library_path", "block_forward", "block_autotune", "block_tuned_config", "stage_forward",
     "downsample_forward",
-    "block_forward_unfused", "block_forward_split", "stack_forward", "capture_stack", "ConvFirstBlock",
+    "block_forward_unfused", "block_forward_split", "block_forward_split_noalloc", "stack_forward", "capture_stack", "ConvFirstBlock",
     "CFError", "EXPORTED_SYMBOLS", "dw_weight_from_conv2d", "grouped_weight_from_conv2d",
     "pw_weight_from_conv2d", "down_weight_from_conv2d", "fold_batchnorm", "block_params_from_modules",
     "grouped_block_params_from_modules", "down_params_from_modules",
@@ -40,7 +40,7 @@ ACTS = {"gelu": 0, "relu": 1, "none": 2}
 EXPORTED_SYMBOLS = (
     "cf_block_forward", "cf_stage_forward", "cf_stage_workspace_bytes", "cf_downsample_forward",
     "cf_block_forward_unfused", "cf_unfused_workspace_bytes", "cf_block_forward_split",
-    "cf_split_workspace_bytes", "cf_block_autotune",
+    "cf_split_workspace_bytes", "cf_block_forward_split_noalloc", "cf_block_autotune",
     "cf_block_tuned_config", "cf_last_error", "cf_status_string", "cf_abi_version",
 )
 
@@ -86,6 +86,7 @@ def lib():
             "cf_unfused_workspace_bytes": (sz, [i, i, i, i, i, i]),
             "cf_block_forward_split": (i, [vp, vp, vp, sz, bp, i, i, i, i, i, i, i, i, i, vp]),
             "cf_split_workspace_bytes": (sz, [i, i, i, i, i, i]),
+            "cf_block_forward_split_noalloc": (i, [vp, vp, bp, i, i, i, i, i, i, i, i, i, vp]),
             "cf_block_autotune": (i, [vp, vp, bp, i, i, i, i, i, i, i, i, vp]),
             "cf_block_tuned_config": (i, [i, i, i, i, i, i, i, i]),
             "cf_last_error": (ctypes.c_char_p, []),
@@ -325,6 +326,18 @@ def block_forward_split(x: torch.Tensor, p: dict, act: str = "gelu", groups: int
     _check(L.cf_block_forward_split(_ptr(x), _ptr(y), _ptr(ws), ws.numel(), ctypes.byref(bp),
                                     N, H, W, C, E, k, groups, DTYPES[x.dtype], ACTS[act],
                                     _stream(stream)))
+    return y
+
+
+def block_forward_split_noalloc(x: torch.Tensor, p: dict, act: str = "gelu", groups: int = 0, out=None,
+                                stream=None) -> torch.Tensor:
+    """block_forward_split without a workspace: the library keeps the fp32
+    partials in a static device array (16 MiB per GPU), so with `out` given the
+    call allocates nothing.  Calls that overlap on one GPU race (see the C
+    header)."""
+    y, bp, keep, (N, H, W, C, E, k) = _prepare_block(x, p, act, out)
+    _check(lib().cf_block_forward_split_noalloc(_ptr(x), _ptr(y), ctypes.byref(bp), N, H, W, C, E, k, groups,
+                                                DTYPES[x.dtype], ACTS[act], _stream(stream)))
     return y
 
 

@@ -14,7 +14,15 @@
 #include <map>
 #include <mutex>
 
+// The fp32 partials of cf_block_forward_split_noalloc live in this static
+// device array; each GPU the library runs on holds its own copy until the
+// process ends.  In host code the name is not a device address: launches and
+// copies use the address hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) unsigned char scratch[CF_SPLIT_SCRATCH_BYTES];
+
 namespace {
+
+constexpr size_t SCRATCH_BYTES = CF_SPLIT_SCRATCH_BYTES;
 
 thread_local char g_err[512] = "";
 
@@ -162,7 +170,7 @@ int default_groups(int N, int H, int W, int C, int E) {
     return best;
 }
 
-// Checks of the split entry point; on success *need holds the
+// Checks shared by the two split entry points; on success *need holds the
 // bytes of fp32 partials the call writes (groups * N*H*W * C * 4).
 cf_status check_split(const char *what, const void *x, const void *y, const cf_block_params *p, int N, int H, int W,
                       int C, int E, int k, int &groups, cf_dtype dt, cf_act act, size_t *need) {
@@ -180,6 +188,34 @@ cf_status check_split(const char *what, const void *x, const void *y, const cf_b
     if (!(small_lds > 0 && small_lds <= 160 * 1024) && (st = check_fit(what, s)) != CF_OK)
         return st;
     return CF_OK;
+}
+
+// ---- the allocation-free split variant's scratch (the array is defined at
+// file scope above the namespace): its device address comes from
+// hipGetSymbolAddress, looked up once per device with that device current.
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[MAX_DEVICES] = {};
+
+hipError_t scratch_on_current_device(void **out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return e;
+    if (dev < 0 || dev >= MAX_DEVICES)
+        return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess)
+            return e;
+        if (!ptr || ((uintptr_t)ptr & 255u))
+            return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
 }
 
 }  // namespace
@@ -389,6 +425,30 @@ cf_status cf_block_forward_split(const void *x, void *y, void *ws, size_t ws_byt
         return fail(CF_ERR_INVALID, "%s: ws overlaps x or y", what);
     hipError_t e = cf::launch_fused_block(x, y, to_w(p), to_shape(N, H, W, C, E, k, dt, act), groups, (float *)ws,
                                           (hipStream_t)stream);
+    if (e != hipSuccess)
+        return hip_fail(e, what);
+    g_err[0] = 0;
+    return CF_OK;
+}
+
+cf_status cf_block_forward_split_noalloc(const void *x, void *y, const cf_block_params *p, int N, int H, int W, int C,
+                                         int E, int k, int groups, cf_dtype dt, cf_act act, void *stream) {
+    const char *what = "cf_block_forward_split_noalloc";
+    size_t need = 0;
+    cf_status st = check_split(what, x, y, p, N, H, W, C, E, k, groups, dt, act, &need);
+    if (st != CF_OK)
+        return st;
+    if (need > SCRATCH_BYTES)
+        return fail(CF_ERR_WORKSPACE,
+                    "%s: the fp32 partials of %d groups need %zu bytes; the static scratch holds %zu "
+                    "(use fewer groups or cf_block_forward_split with a workspace)",
+                    what, groups, need, SCRATCH_BYTES);
+    void *ws = nullptr;
+    hipError_t e = scratch_on_current_device(&ws);
+    if (e != hipSuccess)
+        return hip_fail(e, what);
+    e = cf::launch_fused_block(x, y, to_w(p), to_shape(N, H, W, C, E, k, dt, act), groups, (float *)ws,
+                               (hipStream_t)stream);
     if (e != hipSuccess)
         return hip_fail(e, what);
     g_err[0] = 0;

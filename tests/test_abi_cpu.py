@@ -315,3 +315,18 @@ def test_c64_next_halo_rows_and_masks():
                         okm = (~asr(d) & 0xFFFFFFFF) & asr(d - span)
                         assert (okm == 0xFFFFFFFF) == want and okm in (0, 0xFFFFFFFF)
 
+
+def test_split_noalloc_rejects_before_any_launch():
+    """The allocation-free split entry point: partials beyond its static
+    scratch return CF_ERR_WORKSPACE, bad groups CF_ERR_INVALID, both on the
+    host before any HIP call."""
+    L = cf.lib()
+    p = params()
+    # N = 3, 14x14, C = 256, E = 4, 32 groups: 3*196*256*4*32 bytes = 19.3 MB > 16 MiB
+    assert L.cf_block_forward_split_noalloc(X, Y, ctypes.byref(p), 3, 14, 14, 256, 4, 3, 32, 0, 0,
+                                            None) == cf.CF_ERR_WORKSPACE
+    assert "scratch" in L.cf_last_error().decode()
+    assert L.cf_block_forward_split_noalloc(X, Y, ctypes.byref(p), 1, 8, 8, 64, 4, 3, 3, 0, 0,
+                                            None) == cf.CF_ERR_INVALID
+    assert L.cf_block_forward_split_noalloc(None, Y, ctypes.byref(p), 1, 8, 8, 64, 4, 3, 2, 0, 0,
+                                            None) == cf.CF_ERR_INVALID
