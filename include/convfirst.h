@@ -138,6 +138,38 @@ cf_status cf_block_forward_split(const void *x, void *y, void *ws, size_t ws_byt
                                  cf_dtype dt, cf_act act, void *stream);
 size_t cf_split_workspace_bytes(int N, int H, int W, int C, int E, int groups);
 
+/* The ConvFirst block as the paper defines it (Sec. 5.3): the first layer is
+ * a k x k grouped convolution of group width CF_GROUP_WIDTH = 8 with C input
+ * and C output channels (eq. f:grouped-conv2d with K = C, T = 8: output
+ * channel c reads input channels floor(c/8)*8 .. +7), followed by the same
+ * FFN and residual as cf_block_forward, all in one fused kernel (Sec. 5.3.1):
+ *   D[n,h,w,c] = s0[c] * sum_{i,j<k} sum_{t<8} gw_w[i][j][c][t]
+ *                 * X[n, h+i-k/2, w+j-k/2, floor(c/8)*8 + t] + b0[c]
+ * The paper's block uses ReLU (Sec. 5.3, benchmarked in Table
+ * t:conv-first-speed at C = 16..96, E = 3 or 6); GELU and identity are
+ * available too.
+ *   gw_w  [k][k][C][8]  grouped taps: torch's grouped nn.Conv2d weight
+ *                       [C][8][k][k] permuted to (2, 3, 0, 1)
+ *   w1, w2, and the fp32 vectors as in cf_block_params.
+ * Supported: k = 3; C a multiple of 16 from 16 to 128; any E >= 1 (E*C need
+ * not be a multiple of 32); any N, H, W >= 1.  C not a multiple of 8 returns
+ * CF_ERR_INVALID, other unsupported shapes CF_ERR_UNSUPPORTED.  fp16 or bf16
+ * I/O, fp32 accumulation; the conv output and the hidden values are rounded
+ * to the I/O dtype before the next product. */
+#define CF_GROUP_WIDTH 8
+typedef struct {
+    const void *gw_w;
+    const float *gw_scale, *gw_bias;
+    const void *w1;
+    const float *s1, *b1;
+    const void *w2;
+    const float *s2, *b2;
+} cf_gblock_params;
+
+cf_status cf_gblock_forward(const void *x, void *y, const cf_gblock_params *p,
+                            int N, int H, int W, int C, int E, int k,
+                            cf_dtype dt, cf_act act, void *stream);
+
 /* Allocation-free variant of cf_block_forward_split, for callers that cannot
  * allocate device memory: code under stream capture, tight serving loops,
  * harnesses that forbid hipMalloc.  Same arguments and result as

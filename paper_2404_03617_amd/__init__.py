@@ -24,7 +24,8 @@ from .convert import (block_params_from_modules, down_params_from_modules, down_
 __all__ = [
     "lib", "library_path", "block_forward", "block_autotune", "block_tuned_config", "stage_forward",
     "downsample_forward",
-    "block_forward_unfused", "block_forward_split", "block_forward_split_noalloc", "stack_forward", "capture_stack", "ConvFirstBlock",
+    "block_forward_unfused", "block_forward_split", "block_forward_split_noalloc", "gblock_forward",
+    "stack_forward", "capture_stack", "ConvFirstBlock",
     "CFError", "EXPORTED_SYMBOLS", "dw_weight_from_conv2d", "grouped_weight_from_conv2d",
     "pw_weight_from_conv2d", "down_weight_from_conv2d", "fold_batchnorm", "block_params_from_modules",
     "grouped_block_params_from_modules", "down_params_from_modules",
@@ -40,7 +41,7 @@ ACTS = {"gelu": 0, "relu": 1, "none": 2}
 EXPORTED_SYMBOLS = (
     "cf_block_forward", "cf_stage_forward", "cf_stage_workspace_bytes", "cf_downsample_forward",
     "cf_block_forward_unfused", "cf_unfused_workspace_bytes", "cf_block_forward_split",
-    "cf_split_workspace_bytes", "cf_block_forward_split_noalloc", "cf_block_autotune",
+    "cf_split_workspace_bytes", "cf_block_forward_split_noalloc", "cf_gblock_forward", "cf_block_autotune",
     "cf_block_tuned_config", "cf_last_error", "cf_status_string", "cf_abi_version",
 )
 
@@ -54,6 +55,11 @@ class CFError(RuntimeError):
 class _BlockParams(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
                 ("dw_w", "dw_scale", "dw_bias", "w1", "s1", "b1", "w2", "s2", "b2")]
+
+
+class _GBlockParams(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("gw_w", "gw_scale", "gw_bias", "w1", "s1", "b1", "w2", "s2", "b2")]
 
 
 class _DownParams(ctypes.Structure):
@@ -77,6 +83,7 @@ def lib():
         L = ctypes.CDLL(_LIB_PATH)
         i, sz, vp = ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p
         bp, dp = ctypes.POINTER(_BlockParams), ctypes.POINTER(_DownParams)
+        gp = ctypes.POINTER(_GBlockParams)
         sig = {
             "cf_block_forward": (i, [vp, vp, bp, i, i, i, i, i, i, i, i, vp]),
             "cf_stage_forward": (i, [vp, vp, vp, sz, bp, i, i, i, i, i, i, i, i, i, vp]),
@@ -87,6 +94,7 @@ def lib():
             "cf_block_forward_split": (i, [vp, vp, vp, sz, bp, i, i, i, i, i, i, i, i, i, vp]),
             "cf_split_workspace_bytes": (sz, [i, i, i, i, i, i]),
             "cf_block_forward_split_noalloc": (i, [vp, vp, bp, i, i, i, i, i, i, i, i, i, vp]),
+            "cf_gblock_forward": (i, [vp, vp, gp, i, i, i, i, i, i, i, i, vp]),
             "cf_block_autotune": (i, [vp, vp, bp, i, i, i, i, i, i, i, i, vp]),
             "cf_block_tuned_config": (i, [i, i, i, i, i, i, i, i]),
             "cf_last_error": (ctypes.c_char_p, []),
@@ -326,6 +334,48 @@ def block_forward_split(x: torch.Tensor, p: dict, act: str = "gelu", groups: int
     _check(L.cf_block_forward_split(_ptr(x), _ptr(y), _ptr(ws), ws.numel(), ctypes.byref(bp),
                                     N, H, W, C, E, k, groups, DTYPES[x.dtype], ACTS[act],
                                     _stream(stream)))
+    return y
+
+
+GROUP_WIDTH = 8
+_GBLOCK_SHAPES = dict(_BLOCK_SHAPES)
+del _GBLOCK_SHAPES["dw_w"]
+_GBLOCK_SHAPES["gw_w"] = (lambda C, EC, k: (k, k, C, GROUP_WIDTH), "w")
+_GFIELDS = dict(_FIELDS, gw_w="gw_w", s0="gw_scale", b0="gw_bias")
+del _GFIELDS["dw_w"]
+
+
+def gblock_forward(x: torch.Tensor, p: dict, act: str = "relu", out=None, stream=None) -> torch.Tensor:
+    """The paper's ConvFirst block (Sec. 5.3) fused: a k x k grouped conv of
+    group width 8, then the FFN and the residual.  p holds gw_w [k,k,C,8],
+    w1 [E*C,C], w2 [C,E*C] in x's dtype and optional fp32 s0,b0 [C],
+    s1,b1 [E*C], s2,b2 [C].  ReLU is the paper's activation."""
+    if act not in ACTS:
+        raise ValueError("act must be one of %s" % sorted(ACTS))
+    N, H, W, C = _dims(x)
+    for key in ("gw_w", "w1", "w2"):
+        if not isinstance(p.get(key), torch.Tensor):
+            raise ValueError("grouped-block parameter %s is required" % key)
+    if p["gw_w"].dim() != 4 or p["w1"].dim() != 2:
+        raise ValueError("gw_w must be [k, k, C, 8] and w1 [E*C, C]")
+    k, EC = int(p["gw_w"].shape[0]), int(p["w1"].shape[0])
+    if EC % C or EC == 0:
+        raise ValueError("w1 rows must be a positive multiple of C")
+    unknown = set(p) - set(_GBLOCK_SHAPES)
+    if unknown:
+        raise ValueError("unknown grouped-block parameters: %s" % sorted(unknown))
+    vals, keep = {}, []
+    for key, (shape_of, kind) in _GBLOCK_SHAPES.items():
+        t = p.get(key)
+        if t is not None:
+            _check_tensor(key, t, shape_of(C, EC, k), x.dtype if kind == "w" else torch.float32, x.device)
+            keep.append(t)
+        vals[_GFIELDS[key]] = None if t is None else t.data_ptr()
+    gp = _GBlockParams(**vals)
+    _check_device(x)
+    y = _out(x, out)
+    _check(lib().cf_gblock_forward(_ptr(x), _ptr(y), ctypes.byref(gp), N, H, W, C, EC // C, k,
+                                   DTYPES[x.dtype], ACTS[act], _stream(stream)))
     return y
 
 

@@ -85,6 +85,21 @@ hipError_t launch_downsample(const void *x, void *y, const void *wd, const float
                              const float *bd, int N, int H, int W, int Cin, int Cout, int bf16,
                              hipStream_t st);
 
+// The paper's block: 3 x 3 grouped conv (group width 8) first, then the FFN
+// and the residual.  gw [3][3][C][8]; the rest as BlockW.
+struct GBlockW {
+    const void *gw;
+    const float *s0, *b0;
+    const void *w1;
+    const float *s1, *b1;
+    const void *w2;
+    const float *s2, *b2;
+};
+// Channel counts with a kernel: multiples of 16 from 16 to 128.
+bool gblock_supported_c(int C);
+// Fused grouped block; hipErrorInvalidValue for an unsupported C.
+hipError_t launch_gblock(const void *x, void *y, const GBlockW &w, const Shape &s, hipStream_t st);
+
 // Upper bound of dynamic LDS the fused kernel needs for this shape (bytes);
 // 0 when no kernel configuration fits.
 size_t fused_lds_bytes(const Shape &s);

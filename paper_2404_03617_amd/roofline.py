@@ -38,6 +38,16 @@ def block_flops(N, H, W, C, E, k, gw=1) -> int:
     return N * H * W * block_ops_per_pixel(C, E, k, gw)
 
 
+def gblock_flops(N, H, W, C, E, k=3, gw=8) -> int:
+    """The paper's count for its own block (Sec. 5.5.3): 2 * P * (k*k*gw*C + 2*E*C*C),
+    i.e. 2 * 128 * H * W * (72 C + 2 alpha C^2) at batch 128, k = 3, gw = 8."""
+    return block_flops(N, H, W, C, E, k, gw)
+
+
+def gblock_bytes_fused(N, H, W, C, E, k=3, gw=8, eb=2) -> int:
+    return 2 * N * H * W * C * eb + eb * (k * k * gw * C + 2 * E * C * C) + 4 * (4 * C + 2 * E * C)
+
+
 def block_weight_bytes(C, E, k, eb=2, vec_bytes=4) -> int:
     """dw taps, W1, W2 in the I/O dtype plus six fp32 scale/bias vectors."""
     return eb * (k * k * C + 2 * E * C * C) + vec_bytes * (2 * C + 2 * E * C + 2 * C)

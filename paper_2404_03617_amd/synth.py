@@ -86,6 +86,17 @@ def block_params(seed: int, layer: int, C: int, E: int, k: int, dtype: str = "f1
     return p
 
 
+def gblock_params(seed: int, layer: int, C: int, E: int, k: int = 3, dtype: str = "f16",
+                  scales: str = "ones", bias_std: float | None = 0.1, gw: int = 8) -> dict:
+    """Weights of one block of the paper's own form (grouped conv of group
+    width gw first); tensor ids 100*(layer+1) + 0..8, the grouped taps
+    [k, k, C, gw] ~ N(0, 1/(k*k*gw)) in place of the depth-wise ones."""
+    p = block_params(seed, layer, C, E, k, dtype, scales, bias_std)
+    del p["dw_w"]
+    p["gw_w"] = to_io(draw(seed, 100 * (layer + 1) + 0, (k, k, C, gw), (1.0 / (k * k * gw)) ** 0.5), dtype)
+    return p
+
+
 def down_params(seed: int, layer: int, Cin: int, Cout: int, dtype: str = "f16",
                 scales: str = "ones", bias_std: float | None = 0.1) -> dict:
     """Weights of one 2x2 stride-2 down-sampling layer; ids 100*(layer+1) + 0..2."""

@@ -25,3 +25,17 @@ WORKLOADS = {
 }
 
 BENCH_WORKLOAD = "block_n128_56x56_c64_e4_k3_f16"
+
+# The paper's own block (3 x 3 grouped conv of group width 8, ReLU) at the
+# eight shapes of its kernel benchmark table (Sec. 5.5.3, Table
+# t:conv-first-speed): channels, expansion, height = width, batch 128, fp16.
+# paper_pct is the block-fusion kernel's fraction of peak that table reports
+# on an A5000 (context only: other hardware).
+GBLOCK_WORKLOADS = {
+    "gblock_n128_%dx%d_c%d_e%d_k3_f16" % (hw, hw, c, e): dict(kind="gblock", N=128, H=hw, W=hw, C=c, E=e, k=3,
+                                                            dtype="f16", act="relu", seed=20 + i,
+                                                            paper_pct=pct, paper_ms=ms)
+    for i, (c, e, hw, pct, ms) in enumerate([
+        (16, 3, 128, 35.1, 0.42), (32, 3, 128, 46.6, 0.99), (32, 6, 64, 66.9, 0.30), (48, 6, 64, 71.6, 0.59),
+        (64, 6, 64, 76.2, 0.96), (48, 6, 32, 67.0, 0.16), (64, 6, 32, 74.0, 0.25), (96, 6, 32, 68.7, 0.58)])
+}

@@ -330,3 +330,28 @@ def test_split_noalloc_rejects_before_any_launch():
                                             None) == cf.CF_ERR_INVALID
     assert L.cf_block_forward_split_noalloc(None, Y, ctypes.byref(p), 1, 8, 8, 64, 4, 3, 2, 0, 0,
                                             None) == cf.CF_ERR_INVALID
+
+
+def test_gblock_forward_rejects():
+    """The paper's block entry point: every check happens on the host."""
+    L = cf.lib()
+    GW = 0x43000000
+
+    def call(x=X, y=Y, gw=GW, N=1, H=8, W=8, C=64, E=6, k=3, dt=0, act=1, **kw):
+        p = cf._GBlockParams(gw_w=gw, gw_scale=None, gw_bias=None, w1=W1, s1=None, b1=None, w2=W2, s2=None,
+                             b2=None)
+        for f, v in kw.items():
+            setattr(p, f, v)
+        return L.cf_gblock_forward(x, y, ctypes.byref(p), N, H, W, C, E, k, dt, act, None)
+
+    assert call(gw=None) == cf.CF_ERR_INVALID
+    assert call(x=None) == cf.CF_ERR_INVALID
+    assert call(C=20) == cf.CF_ERR_INVALID          # not a multiple of the group width 8
+    assert call(k=4) == cf.CF_ERR_INVALID
+    assert call(act=9) == cf.CF_ERR_INVALID
+    assert call(y=X + 32) == cf.CF_ERR_INVALID      # overlaps x
+    assert call(b1=W1 + 4) == cf.CF_ERR_INVALID     # misaligned
+    assert call(C=24) == cf.CF_ERR_UNSUPPORTED      # multiple of 8, not of 16
+    assert call(C=256) == cf.CF_ERR_UNSUPPORTED
+    assert call(k=5) == cf.CF_ERR_UNSUPPORTED
+    assert L.cf_last_error().decode().startswith("cf_gblock_forward")

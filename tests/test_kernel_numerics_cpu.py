@@ -101,3 +101,29 @@ def test_the_bound_detects_a_perturbed_coefficient(i, delta):
     c[i] += delta
     _, err, inner, _ = gelu_errors(c)
     assert err[inner].max() > BOUND
+
+
+# ---------------------------------------------------------------- operation count
+def _table_rows():
+    rows = []
+    with open(os.path.join(ROOT, "tests", "golden", "convfirst_kernel_table.txt")) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                c, e, h, w, ms, tf, pct = line.split()
+                rows.append((int(c), int(e), int(h), int(w), float(ms), float(tf), float(pct)))
+    return rows
+
+
+@pytest.mark.parametrize("row", _table_rows(), ids=lambda r: "C%d_a%d_%dx%d" % r[:4])
+def test_grouped_block_operation_count_reproduces_the_papers_table(row):
+    """roofline.gblock_flops (2 * 128 * H * W * (72 C + 2 alpha C^2)) divided by
+    the paper's measured times gives its TFLOPS column, and TFLOPS / 76.7 its
+    percent-of-peak column (the printed values are rounded, the times to two
+    digits, and the percentages were evidently taken from unrounded figures:
+    51.3 / 76.7 = 66.88 is printed as 67.0, hence the tolerances)."""
+    from paper_2404_03617_amd import roofline as rl
+    C, E, H, W, ms, tflops, pct = row
+    got = rl.gblock_flops(128, H, W, C, E) / (ms * 1e-3) / 1e12
+    assert got == pytest.approx(tflops, rel=0.02)
+    assert tflops / 76.7 * 100 == pytest.approx(pct, abs=0.2)
