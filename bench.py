@@ -10,9 +10,13 @@ events on the launch stream bracket exactly K steps after W warm-up steps.
 
 Prints ONE JSON line: images/s (value), ms per step, computational efficiency
 (FLOPs of the block at the dense fp16 MFMA peak divided by the measured
-latency), the roofline of the kernel, the fp64 CPU oracle timed on a bounded
-sample on the host cores, and the other workloads (block C = 256 k = 7, the
-four-stage stack, the layer-by-layer baseline, the N = 1 latency cases).
+latency), the roofline of the kernel (the timed region's average per launch),
+the GFX clock read under load, the fp64 CPU oracle timed on a bounded sample
+on the host cores, and the other workloads: the layer-by-layer baseline with
+its own waterline, ReLU, block C = 256 k = 7 with its roofline, the N = 1
+latency cases, the four-stage stack with a per-launch waterline report
+(fused against layer-by-layer), and the paper's own block (grouped conv of
+group width 8, ReLU) at the eight shapes of its kernel benchmark table.
 """
 from __future__ import annotations
 
@@ -28,7 +32,7 @@ import torch
 import paper_2404_03617_amd as cf
 from paper_2404_03617_amd import roofline as rl
 from paper_2404_03617_amd import synth
-from paper_2404_03617_amd.workloads import BENCH_WORKLOAD, WORKLOADS
+from paper_2404_03617_amd.workloads import BENCH_WORKLOAD, GBLOCK_WORKLOADS, WORKLOADS
 
 MALL_BYTES = 256 << 20
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -98,22 +102,7 @@ def _time(fn, steps: int, warmup: int, stream) -> float:
     return start.elapsed_time(end) / 1e3 / steps
 
 
-def _time_each(fn, steps: int, stream) -> float:
-    """Average seconds of one launch, each bracketed by its own HIP events on
-    `stream` (the per-kernel duration the roofline divides by)."""
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
-    torch.cuda.synchronize()
-    for i in range(steps):
-        starts[i].record(stream)
-        fn(i)
-        ends[i].record(stream)
-    torch.cuda.synchronize()
-    return sum(a.elapsed_time(b) for a, b in zip(starts, ends)) / 1e3 / steps
-
-
-def block_case(name: str, steps: int, warmup: int, act: str = "gelu", unfused: bool = False,
-               per_launch: bool = False):
+def block_case(name: str, steps: int, warmup: int, act: str = "gelu", unfused: bool = False):
     w = WORKLOADS[name]
     N, H, W, C, E, k = w["N"], w["H"], w["W"], w["C"], w["E"], w["k"]
     eb = 2
@@ -136,10 +125,9 @@ def block_case(name: str, steps: int, warmup: int, act: str = "gelu", unfused: b
         cfg = cf.block_tuned_config(xs[0].shape, C, E, k, xs[0].dtype, act)
         fn = lambda i: cf.block_forward(xs[i % nsets], p, act=act, out=ys[i % nsets])
     t = _time(fn, steps, warmup, stream)
-    t_kernel = _time_each(fn, steps, stream) if per_launch else t
     flops = rl.block_flops(N, H, W, C, E, k)
-    return dict(N=N, seconds=t, kernel_seconds=t_kernel, flops=flops, kernel_config=cfg,
-                bytes=rl.block_bytes_fused(N, H, W, C, E, k, eb))
+    return dict(N=N, seconds=t, flops=flops, kernel_config=cfg,
+                bytes=rl.block_bytes_fused(N, H, W, C, E, k, eb), launch=fn)
 
 
 def split_case(name: str, steps: int, warmup: int):
@@ -186,6 +174,123 @@ def stack_case(name: str, steps: int, warmup: int):
                 waterline_C_max=cmax)
 
 
+def roofline_entry(flops: float, nbytes: float, seconds: float) -> dict:
+    """Roofline of one kernel (or one launch sequence): the bound is the roof
+    its operational intensity meets first (HBM below the ridge, MFMA above)."""
+    t_hbm, t_mfma = nbytes / rl.PEAK_HBM_BPS, flops / rl.PEAK_FP16_FLOPS
+    if t_hbm >= t_mfma:
+        a = nbytes / seconds / 1e9
+        return {"bound": "hbm", "achieved": round(a, 1), "peak": rl.PEAK_HBM_BPS / 1e9, "unit": "GB/s",
+                "frac": round(a * 1e9 / rl.PEAK_HBM_BPS, 4)}
+    a = flops / seconds / 1e12
+    return {"bound": "mfma", "achieved": round(a, 1), "peak": rl.PEAK_FP16_FLOPS / 1e12, "unit": "TFLOP/s",
+            "frac": round(a * 1e12 / rl.PEAK_FP16_FLOPS, 4)}
+
+
+def gblock_case(name: str, steps: int, warmup: int):
+    """The paper's own block (grouped 3x3 conv, group width 8, ReLU) at one of
+    the shapes of its kernel benchmark table, batch 128."""
+    w = GBLOCK_WORKLOADS[name]
+    N, H, W, C, E, k = w["N"], w["H"], w["W"], w["C"], w["E"], w["k"]
+    nsets = _sets_needed(2 * N * H * W * C * 2)
+    xs = [synth.activations(w["seed"] + 100 * i, N, H, W, C, w["dtype"]).cuda() for i in range(nsets)]
+    ys = [torch.empty_like(xs[0]) for _ in range(nsets)]
+    p = {kk: (None if v is None else v.cuda()) for kk, v in
+         synth.gblock_params(w["seed"], 0, C, E, k, w["dtype"]).items()}
+    t = _time(lambda i: cf.gblock_forward(xs[i % nsets], p, act=w["act"], out=ys[i % nsets]), steps, warmup,
+              torch.cuda.current_stream())
+    flops = rl.gblock_flops(N, H, W, C, E, k)
+    nbytes = rl.gblock_bytes_fused(N, H, W, C, E, k)
+    return {"ms": round(t * 1e3, 4), "images_per_s": round(N / t, 1), "tflops": round(flops / t / 1e12, 1),
+            "comp_eff": round(rl.comp_eff(flops, t), 4), "roofline": roofline_entry(flops, nbytes, t),
+            "paper_A5000_comp_eff": round(w["paper_pct"] / 100, 3), "paper_A5000_ms": w["paper_ms"]}
+
+
+def stack_waterline(name: str, steps: int, warmup: int):
+    """Per-launch waterline of the four-stage stack (Sec. 4, eqs.
+    e:total-attainable-latency and e:max-comp-eff): for every launch its
+    operations n_i, algorithmic bytes b_i, operational intensity, roofline
+    minimum t_min,i and measured time; then T_min and C_max of the fused
+    schedule (one kernel per block) beside the layer-by-layer one (three per
+    block).  Each stage and down-sampling call is timed on its own (eager,
+    HIP events); a block's time is its stage's time over the depth."""
+    w = WORKLOADS[name]
+    N, H, W = w["N"], w["H"], w["W"]
+    depths, widths, E, k = w["depths"], w["widths"], w["E"], w["k"]
+    layers = [(kd, {kk: (None if v is None else v.cuda()) for kk, v in p.items()})
+              for kd, p in synth.stack_layers(w["seed"], depths, widths, E, k, w["dtype"])]
+    stream = torch.cuda.current_stream()
+    x = synth.activations(w["seed"], N, H, W, widths[0], w["dtype"]).cuda()
+    rows = []
+    h, ww, i = H, W, 0
+    for s_, (d, c) in enumerate(zip(depths, widths)):
+        if s_ > 0:
+            kind, p = layers[i]
+            cin = widths[s_ - 1]
+            xin = x
+            out = torch.empty((N, h // 2, ww // 2, c), dtype=x.dtype, device="cuda")
+            t = _time(lambda j: cf.downsample_forward(xin, p, out=out), steps, warmup, stream)
+            n_i, b_i = rl.down_flops(N, h, ww, cin, c), rl.down_bytes(N, h, ww, cin, c)
+            rows.append(("down%d %dx%d %d->%d" % (s_, h, ww, cin, c), 1, n_i, b_i, t))
+            x = out
+            h, ww = h // 2, ww // 2
+            i += 1
+        blocks = [p for _, p in layers[i:i + d]]
+        xin = x
+        out = torch.empty_like(x)
+        ws = torch.empty(cf.lib().cf_stage_workspace_bytes(d, N, h, ww, c, 0), dtype=torch.uint8, device="cuda")
+        t = _time(lambda j: cf.stage_forward(xin, blocks, out=out, ws=ws), steps, warmup, stream)
+        n_i, b_i = rl.block_flops(N, h, ww, c, E, k), rl.block_bytes_fused(N, h, ww, c, E, k)
+        rows.append(("stage%d block %dx%d C=%d" % (s_ + 1, h, ww, c), d, n_i, b_i, t / d))
+        x = out
+        i += d
+    table = []
+    for nm, reps, n_i, b_i, t in rows:
+        tmin = rl.t_min(n_i, b_i)
+        table.append({"launch": nm, "count": reps, "flops": n_i, "bytes": b_i, "oi": round(n_i / b_i, 1),
+                      "t_min_us": round(tmin * 1e6, 2), "t_us": round(t * 1e6, 2),
+                      "comp_eff": round(rl.comp_eff(n_i, t), 4), "gbps": round(b_i / t / 1e9, 1),
+                      "roofline_frac": round(tmin / t, 4)})
+    fused = [(n, b) for _, reps, n, b, _ in rows for _ in range(reps)]
+    T_f, C_f = rl.waterline(fused)
+    unf = []
+    h, ww = H, W
+    for s_, (d, c) in enumerate(zip(depths, widths)):
+        if s_ > 0:
+            unf.append((rl.down_flops(N, h, ww, widths[s_ - 1], c), rl.down_bytes(N, h, ww, widths[s_ - 1], c)))
+            h, ww = h // 2, ww // 2
+        ops = rl.block_unfused_ops(N, h, ww, c, E, k)
+        bts = rl.block_bytes_unfused(N, h, ww, c, E, k)
+        unf += [(o, b) for o, b in zip(ops, bts)] * d
+    T_u, C_u = rl.waterline(unf)
+    measured = sum(t * reps for _, reps, _, _, t in rows)
+    return {"launches": table, "sum_measured_us": round(measured * 1e6, 1),
+            "fused_T_min_us": round(T_f * 1e6, 1), "fused_C_max": round(C_f, 4), "fused_kernels": len(fused),
+            "unfused_T_min_us": round(T_u * 1e6, 1), "unfused_C_max": round(C_u, 4), "unfused_kernels": len(unf)}
+
+
+def shader_clock_mhz_under_load(fn, seconds_of_work: float, launch_seconds: float):
+    """GFX clock (MHz, mean over the XCDs) read with amd-smi while about
+    `seconds_of_work` of launches of `fn` are queued on the GPU, so the reading
+    is taken under the benchmark's own load (an idle GPU drops to ~100 MHz).
+    None when amd-smi is unavailable."""
+    import subprocess
+    n = max(1, int(seconds_of_work / max(launch_seconds, 1e-6)))
+    for i in range(n):
+        fn(i)
+    try:
+        r = subprocess.run(["amd-smi", "metric", "-c", "--json"], capture_output=True, text=True, timeout=30)
+        d = json.loads(r.stdout)
+        gpu = d["gpu_data"][0] if isinstance(d, dict) else d[0]
+        vals = [float(v["clk"]["value"]) for k, v in gpu["clock"].items()
+                if k.startswith("gfx_") and isinstance(v, dict) and isinstance(v.get("clk"), dict)]
+        clk = sum(vals) / len(vals) if vals else None
+    except Exception:
+        clk = None
+    torch.cuda.synchronize()
+    return clk
+
+
 def cpu_baseline(name: str, min_seconds: float = 12.0):
     """The fp64 oracle on the workload's full batch, all host cores, repeated
     until at least `min_seconds` of CPU work have been timed."""
@@ -206,6 +311,44 @@ def cpu_baseline(name: str, min_seconds: float = 12.0):
     return {"value": round(images / dt, 2), "unit": "images/s", "cores": int(used), "kind": "oracle",
             "sample": "%d passes over the %d-image batch of %s (fp64 C loops), %.1f s"
                       % (passes, w["N"], name, dt)}
+
+
+def cpu_other_workloads(min_seconds: float = 1.0):
+    """The oracle on the other workloads: each block workload repeated for at
+    least `min_seconds` on all host cores (and on one thread for the N = 1
+    latency blocks), the four-stage stack once over its whole batch."""
+    import oracle
+    out = {}
+    for name, w in WORKLOADS.items():
+        if name == BENCH_WORKLOAD:
+            continue
+        if w["kind"] == "stack":
+            x = synth.to_f64(synth.activations(w["seed"], w["N"], w["H"], w["W"], w["widths"][0], w["dtype"]))
+            layers = [(kd, synth.params_f64(p)) for kd, p in
+                      synth.stack_layers(w["seed"], w["depths"], w["widths"], w["E"], w["k"], w["dtype"])]
+            t0 = time.perf_counter()
+            oracle.stack_forward(x, layers)
+            dt = time.perf_counter() - t0
+            out[name] = {"images_per_s": round(w["N"] / dt, 2), "seconds": round(dt, 2), "passes": 1}
+            continue
+        x = synth.to_f64(synth.activations(w["seed"], w["N"], w["H"], w["W"], w["C"], w["dtype"]))
+        p = synth.params_f64(synth.block_params(w["seed"], 0, w["C"], w["E"], w["k"], w["dtype"]))
+        e = {}
+        for label, nth in (("all_cores", 0), ("one_thread", 1)):
+            if label == "one_thread" and w["N"] != 1:
+                continue
+            passes, used = 0, 0
+            t0 = time.perf_counter()
+            while True:
+                _, used = oracle.block_forward(x, p, act="gelu", nthreads=nth, return_threads=True)
+                passes += 1
+                dt = time.perf_counter() - t0
+                if dt >= min_seconds:
+                    break
+            e[label] = {"images_per_s": round(passes * w["N"] / dt, 2), "ms_per_pass": round(dt / passes * 1e3, 3),
+                        "threads": int(used), "passes": passes}
+        out[name] = e
+    return out
 
 
 def main():
@@ -230,9 +373,12 @@ def main():
     cf.lib()
     name = args.workload
     w = WORKLOADS[name]
-    res = block_case(name, args.steps, args.warmup, per_launch=True)
+    res = block_case(name, args.steps, args.warmup)
     t = res["seconds"]
-    tk = res["kernel_seconds"]
+    # a step is one launch of the kernel: the timed region's average per step
+    # is the kernel's average launch duration (events bracketing each launch
+    # separately would add the host's launch gaps)
+    tk = t
     N = res["N"]
     ips = N / t
     eff = rl.comp_eff(res["flops"], t)
@@ -272,10 +418,19 @@ def main():
     if not args.no_extra:
         extra = {}
         u = block_case(name, max(5, args.steps // 5), 2, unfused=True)
+        # the layer-by-layer schedule's own waterline (three kernels), so the
+        # speed-up can be read against what that schedule could reach
+        ops_u = rl.block_unfused_ops(w["N"], w["H"], w["W"], w["C"], w["E"], w["k"])
+        bytes_u = rl.block_bytes_unfused(w["N"], w["H"], w["W"], w["C"], w["E"], w["k"])
+        T_u, C_u = rl.waterline(list(zip(ops_u, bytes_u)))
         extra["unfused_same_workload"] = {"ms": round(u["seconds"] * 1e3, 4),
                                           "images_per_s": round(u["N"] / u["seconds"], 1),
                                           "comp_eff": round(rl.comp_eff(u["flops"], u["seconds"]), 4),
-                                          "fused_speedup": round(u["seconds"] / t, 2)}
+                                          "fused_speedup": round(u["seconds"] / t, 2),
+                                          "waterline_T_min_us": round(T_u * 1e6, 2),
+                                          "waterline_C_max": round(C_u, 4),
+                                          "frac_of_own_waterline": round(T_u / u["seconds"], 4),
+                                          "fused_speedup_vs_unfused_waterline": round(T_u / t, 2)}
         r = block_case(name, max(5, args.steps // 5), 2, act="relu")
         extra["relu_same_workload"] = {"ms": round(r["seconds"] * 1e3, 4),
                                        "comp_eff": round(rl.comp_eff(r["flops"], r["seconds"]), 4)}
@@ -287,21 +442,37 @@ def main():
                 b = block_case(nm, max(5, args.steps // 2), 3)
                 e = {"ms": round(b["seconds"] * 1e3, 4), "images_per_s": round(b["N"] / b["seconds"], 1),
                      "comp_eff": round(rl.comp_eff(b["flops"], b["seconds"]), 4)}
+                if wk["N"] > 1:
+                    e["roofline"] = roofline_entry(b["flops"], b["bytes"], b["seconds"])
                 if wk["N"] * wk["H"] * wk["W"] <= 256:
                     s = split_case(nm, max(5, args.steps // 2), 3)
                     e["split_ms"] = round(s["seconds"] * 1e3, 4)
                 extra[nm] = e
             else:
                 s = stack_case(nm, max(3, args.steps // 5), 2)
+                wl = stack_waterline(nm, max(3, args.steps // 5), 2)
                 extra[nm] = {"ms": round(s["seconds"] * 1e3, 4), "images_per_s": round(s["N"] / s["seconds"], 1),
                              "comp_eff": round(rl.comp_eff(s["flops"], s["seconds"]), 4),
                              "mode": s["mode"], "eager_ms": round(s["eager_seconds"] * 1e3, 4),
-                             "waterline_C_max": round(s["waterline_C_max"], 4)}
+                             "waterline_C_max": round(s["waterline_C_max"], 4),
+                             "roofline": {"bound": "waterline", "achieved_us": round(s["seconds"] * 1e6, 1),
+                                          "T_min_us": round(s["waterline_T_min_s"] * 1e6, 1),
+                                          "frac": round(s["waterline_T_min_s"] / s["seconds"], 4)},
+                             "waterline": wl}
+        # the paper's own block at the shapes of its kernel benchmark table
+        extra["paper_block_table"] = {nm: gblock_case(nm, max(5, args.steps // 2), 3) for nm in GBLOCK_WORKLOADS}
         out["other_workloads"] = extra
     if args.calib_copy:
         calib_copy()
+    clk = shader_clock_mhz_under_load(res["launch"], 1.0, t)
+    out["sclk_mhz_under_load"] = None if clk is None else round(clk, 1)
+    if clk:
+        # computational efficiency against the peak at the clock the GPU ran at
+        out["comp_eff_at_sclk"] = round(eff * 2400.0 / clk, 4)
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(name, args.cpu_seconds)
+        if not args.no_extra:
+            out["cpu_baseline"]["other_workloads"] = cpu_other_workloads()
     print(json.dumps(out), flush=True)
 
 
