@@ -372,6 +372,21 @@ def main():
         sys.exit(2)
     cf.lib()
     name = args.workload
+    if name in GBLOCK_WORKLOADS:
+        # one of the paper's own block shapes as the timed workload (used for
+        # profiles of that kernel); the default is the benchmark workload
+        g = gblock_case(name, args.steps, args.warmup)
+        wg = GBLOCK_WORKLOADS[name]
+        print(json.dumps({"metric": "images/sec and % of fp16 MFMA peak (computational efficiency), batch 128",
+                          "value": g["images_per_s"], "unit": "images/s", "n_gpus": 1, "steps": args.steps,
+                          "warmup": args.warmup, "ms_per_step": g["ms"], "higher_is_better": True,
+                          "scaling": "weak", "vs_baseline": None, "dtype": "f16",
+                          "data": "synthetic (seeded N(0,1) activations, N(0,1/fan_in) weights)",
+                          "config": {"workload": name, "N": wg["N"], "H": wg["H"], "W": wg["W"], "C": wg["C"],
+                                     "E": wg["E"], "k": wg["k"], "act": wg["act"],
+                                     "kernel": "fused grouped-conv block (1 launch)"},
+                          "comp_eff": g["comp_eff"], "roofline": g["roofline"]}), flush=True)
+        return
     w = WORKLOADS[name]
     res = block_case(name, args.steps, args.warmup)
     t = res["seconds"]

@@ -151,7 +151,7 @@ size_t cf_split_workspace_bytes(int N, int H, int W, int C, int E, int groups);
  *   gw_w  [k][k][C][8]  grouped taps: torch's grouped nn.Conv2d weight
  *                       [C][8][k][k] permuted to (2, 3, 0, 1)
  *   w1, w2, and the fp32 vectors as in cf_block_params.
- * Supported: k = 3; C a multiple of 16 from 16 to 128; any E >= 1 (E*C need
+ * Supported: k = 3; C a multiple of 16 from 16 to 112; any E >= 1 (E*C need
  * not be a multiple of 32); any N, H, W >= 1.  C not a multiple of 8 returns
  * CF_ERR_INVALID, other unsupported shapes CF_ERR_UNSUPPORTED.  fp16 or bf16
  * I/O, fp32 accumulation; the conv output and the hidden values are rounded

@@ -485,9 +485,12 @@ cf_status cf_gblock_forward(const void *x, void *y, const cf_gblock_params *p, i
     if (k != 3)
         return fail(CF_ERR_UNSUPPORTED, "%s: k=%d has no kernel (supported: 3)", what, k);
     if (!cf::gblock_supported_c(C))
-        return fail(CF_ERR_UNSUPPORTED, "%s: C=%d has no kernel (supported: multiples of 16 up to 128)", what, C);
+        return fail(CF_ERR_UNSUPPORTED, "%s: C=%d has no kernel (supported: multiples of 16 up to 112)", what, C);
     if ((double)N * H * W > 2147483647.0 - 4096.0)
         return fail(CF_ERR_UNSUPPORTED, "%s: N*H*W must stay below 2^31 pixels", what);
+    if ((double)W * C * 6.0 > 2147483647.0)
+        return fail(CF_ERR_UNSUPPORTED, "%s: W*C=%.0f is too wide (6 rows must stay below 2^31 elements)", what,
+                    (double)W * C);
     cf::GBlockW w;
     w.gw = p->gw_w;
     w.s0 = p->gw_scale;

@@ -5,30 +5,38 @@
 // the residual shortcut; batch norms folded to per-channel scale and bias.
 // Instantiated per channel count in cf_gblock_c*.hip.
 //
-// Work unit: a block of 2 image rows x 16 columns (32 pixels) of one image.
-// A workgroup of NW waves runs NW blocks at a time, one per wave; waves share
-// the FFN weights, which stream through a two-slot LDS ring one chunk of 32
-// hidden channels at a time (one workgroup barrier per chunk), and keep their
-// own halo (4 rows x 18 columns) in a private LDS region.
+// Work unit: a block of 4 image rows x 16 columns (64 pixels) of one image.
+// A workgroup of NW waves runs NW blocks at a time, one per wave; each wave
+// keeps its own halo (6 rows x 18 columns) in a private LDS region.  Four
+// rows per wave halve the LDS reads of the FFN weights per pixel against two
+// rows (every weight fragment read feeds four products).  The FFN
+// weights are either resident in LDS for the whole kernel (when every chunk
+// of 32 hidden channels fits beside the halos: no barrier after the start)
+// or stream through a two-slot LDS ring, one chunk per workgroup barrier,
+// each chunk's global loads issued two chunks before it is needed.
 //
 // All products are v_mfma_f32_16x16x32 (fp16 or bf16 in, fp32 accumulate).
 // Layouts (lane l, q = l >> 4, j = l & 15): A row j, k = 8q..8q+7; B column j,
 // k = 8q..8q+7; D column j, rows 4q..4q+3.
 //
-//  * Grouped conv on the matrix unit.  For group g (channels 8g..8g+7) one
-//    16 x 16 x 32 product per tap column dj evaluates 16 output pixels x 2
-//    rows at once: D row m = 8s + o is output channel 8g + o of block row s,
-//    D column j is block column j, and the K index is (tap row R of the
-//    4-row halo window, input channel t) -- B lane (j, q) reads halo pixel
-//    (row q, column j + dj), channels 8g..8g+7, one 16-byte LDS read; A row
+//  * Grouped conv on the matrix unit.  For group g (channels 8g..8g+7) and
+//    the block's row pair p, one 16 x 16 x 32 product per tap column dj
+//    evaluates 16 output pixels x 2 rows at once: D row m = 8s + o is output
+//    channel 8g + o of block row 2p + s, D column j is block column j, and
+//    the K index is (tap row R of the 4-row halo window starting at halo row
+//    2p, input channel t) -- B lane (j, q) reads halo pixel (row 2p + q,
+//    column j + dj), channels 8g..8g+7, one 16-byte LDS read; A row
 //    (s, o) at (R, t) is the tap W[R - s][dj][8g + o][t], zero when R - s is
 //    outside 0..2.  Three products per group cover the 3 x 3 taps; 72 of
 //    every 96 multiply-adds are useful (a block-diagonal product with 16
 //    output channels and 16 input channels per step would use 50% or less).
 //  * The conv output d = s0 * conv + b0, rounded to the I/O dtype, goes to the
-//    wave's LDS region (it overlays the halo, which the wave has finished
-//    reading) and comes back as the expand's B fragments, read once per
-//    block and kept in registers for every hidden chunk.
+//    wave's LDS region and comes back as the expand's B fragments, read once
+//    per block and kept in registers for every hidden chunk.  Group g's d
+//    values overwrite only the bytes of its own 8 channels, which later
+//    groups do not read, and row pair 0's d (pixels 0..31 of the region)
+//    lies below the halo rows row pair 1 reads (pixels 36 on), so they are
+//    stored as soon as they are computed.
 //  * Expand: two 16-row products per chunk and K step, with the W1 rows of a
 //    chunk ordered so that expand tile t row m is hidden channel
 //    8 (m >> 2) + 4 t + (m & 3): lane group q then holds hidden channels
@@ -38,9 +46,13 @@
 //  * Project: C/16 products per chunk into fp32 accumulators; the epilogue
 //    adds s2, b2 and the block input x (re-read from global memory, an L2
 //    hit) and stores the output once.
-//  * The next block's halo is loaded during the FFN, a few 16-byte pieces per
-//    lane per chunk, into the wave's region (free once the D fragments are in
-//    registers).  Pixels outside the image are stored as zeros.
+//  * Halo prefetch.  With few channels (PREF2) a block's halo is loaded into
+//    registers a whole block ahead: when block r's D fragments are in
+//    registers, the halo of block r+1 (loaded during block r-1) goes into the
+//    wave's region and the loads of block r+2's halo are issued.  With many
+//    channels the registers do not allow that; block r+1's halo is then
+//    loaded during block r's FFN, a few 16-byte pieces per lane per chunk.
+//    Pixels outside the image are stored as zeros.
 #pragma once
 #include "cf_device.h"
 #include "cf_fused_impl.h"
@@ -49,14 +61,11 @@
 namespace cf {
 namespace gblk {
 
-using fused::FastDiv;
-using fused::fdiv;
-
 constexpr int GW = 8;               // group width of the grouped conv
-constexpr int BR = 2, BC = 16;      // block: 2 rows x 16 columns
+constexpr int BR = 4, BC = 16;      // block: 4 rows x 16 columns
 constexpr int HR = BR + 2, HC = BC + 2;
 constexpr int HPIX = HR * HC;       // halo pixels of a block (3 x 3 taps)
-constexpr int HSTEP = 4;            // halo pieces per lane per FFN chunk
+constexpr int HSTEP = 4;            // halo pieces per lane per FFN chunk (many channels)
 
 struct Args {
     const uint16_t *x;
@@ -69,10 +78,11 @@ struct Args {
     const float *s2, *b2;
     int H, W, EC;
     int nch;                        // chunks of 32 hidden channels, ceil(EC / 32)
-    int RP, SEG;                    // row pairs ceil(H/2), 16-column segments ceil(W/16)
-    int nblocks;                    // N * RP * SEG
+    int RB, SEG;                    // row bands ceil(H/4), 16-column segments ceil(W/16)
+    int nblocks;                    // N * RB * SEG
     int rbase, rextra;              // rounds (NW blocks) per workgroup: rbase, +1 for the first rextra
     int xcd_map;                    // 1: workgroup i takes range (i % 8) * (G / 8) + i / 8
+    uint32_t off_halo;              // LDS offset of the halo regions (after the weights)
 };
 
 __device__ __forceinline__ u32x4 lds16(const uint8_t *base, uint32_t off) {
@@ -82,10 +92,9 @@ __device__ __forceinline__ void sts16(uint8_t *base, uint32_t off, const u32x4 &
     *reinterpret_cast<u32x4 *>(base + off) = v;
 }
 
-template <int C, int NW, typename T, int ACT>
-struct GB {
+template <int C>
+struct Geo {
     static_assert(C % 16 == 0 && C >= 16, "C must be a multiple of 16");
-    static constexpr int NT = NW * 64;
     static constexpr int PB = 2 * C + 16;          // LDS bytes per pixel (odd multiple of 16)
     static constexpr int C8 = C / 8;               // 16-byte pieces per pixel
     static constexpr int NG = C / GW;              // groups
@@ -96,50 +105,99 @@ struct GB {
     static constexpr int W2B = MO * 1024;          //        W2 fragments
     static constexpr int CHB = W1B + W2B + 256;    //        then s1[32], b1[32]
     static constexpr int GROW = 3 * C * 16 + 128;  // conv taps of one tap row (+128: conflict-free)
-    static constexpr int OFF_VEC = 3 * GROW;                  // s0, b0, s2, b2: C floats each
-    static constexpr int OFF_RING = (OFF_VEC + 16 * C + 255) & ~255;
-    static constexpr int OFF_HALO = OFF_RING + 2 * CHB;
-    static constexpr int LDS = OFF_HALO + NW * HALO;
+    static constexpr int OFF_VEC = 3 * GROW;       // s0, b0, s2, b2: C floats each
+    static constexpr int OFF_W = (OFF_VEC + 16 * C + 255) & ~255;
     static constexpr int HPIECES = HPIX * C8;      // 16-byte pieces of a halo
+    static constexpr int HPL = (HPIECES + 63) / 64;
     static constexpr int HSTEPS = (HPIECES + 64 * HSTEP - 1) / (64 * HSTEP);
     static constexpr int CPIECES = (2 * KST + MO) * 64 + 16;
-    static constexpr int CPT = (CPIECES + NT - 1) / NT;
-    static_assert(LDS <= 160 * 1024, "LDS plan exceeds 160 KB");
+    // a whole block's halo in registers (one block ahead) while it is cheap
+    static constexpr bool PREF2 = HPL <= 9;
+};
 
-    // ---- one chunk of FFN weights, fragment order, staged through registers
-    static __device__ __forceinline__ void chunk_load(const Args &a, int ch, int tid, u32x4 (&r)[CPT]) {
-#pragma unroll
-        for (int u = 0; u < CPT; u++) {
-            const int p = u * NT + tid;
-            u32x4 v = {0u, 0u, 0u, 0u};
-            if (p < 2 * KST * 64) {
-                const int f = p >> 6, ln = p & 63, t = f / KST, kk = f - t * KST;
-                const int m = ln & 15, qq = ln >> 4;
-                const int row = ch * 32 + 8 * (m >> 2) + 4 * t + (m & 3);
-                const int col = 32 * kk + 8 * qq;
-                if (row < a.EC && col < C)
-                    v = *reinterpret_cast<const u32x4 *>(a.w1 + (size_t)row * C + col);
-            } else if (p < (2 * KST + MO) * 64) {
-                const int pp = p - 2 * KST * 64;
-                const int mo = pp >> 6, ln = pp & 63;
-                const int o = 16 * mo + (ln & 15), hc = ch * 32 + 8 * (ln >> 4);
-                if (hc < a.EC)
-                    v = *reinterpret_cast<const u32x4 *>(a.w2 + (size_t)o * a.EC + hc);
-            } else if (p < CPIECES) {
-                const int jv = p - (2 * KST + MO) * 64;  // 0..7: s1, 8..15: b1
-                const int hid = ch * 32 + 4 * (jv & 7);
-                float4v f = {0.f, 0.f, 0.f, 0.f};
-                if (hid < a.EC) {
-                    const float *src = jv < 8 ? a.s1 : a.b1;
-                    if (src)
-                        f = *reinterpret_cast<const float4v *>(src + hid);
-                    else if (jv < 8)
-                        f = float4v{1.f, 1.f, 1.f, 1.f};
-                }
-                v = __builtin_bit_cast(u32x4, f);
-            }
-            r[u] = v;
+// waves per workgroup for a channel count: 8 where their halo regions fit
+constexpr int nw_for(int C) { return C <= 64 ? 8 : 4; }
+
+// LDS bytes of a configuration: resident weights (nch chunks) or the ring
+template <int C>
+inline size_t lds_bytes(int nch, bool resident) {
+    using G = Geo<C>;
+    return (size_t)G::OFF_W + (size_t)(resident ? nch : 2) * G::CHB + (size_t)nw_for(C) * G::HALO;
+}
+
+template <int C, int NW, typename T, int ACT, bool RES>
+struct GB {
+    using G = Geo<C>;
+    static constexpr int NT = NW * 64;
+    static constexpr int PB = G::PB, C8 = G::C8, NG = G::NG, KST = G::KST, MO = G::MO, HALO = G::HALO;
+    static constexpr int W1B = G::W1B, W2B = G::W2B, CHB = G::CHB, GROW = G::GROW;
+    static constexpr int HPIECES = G::HPIECES, HPL = G::HPL, HSTEPS = G::HSTEPS, CPIECES = G::CPIECES;
+    static constexpr bool PREF2 = G::PREF2;
+    static constexpr int CPT = (CPIECES + NT - 1) / NT;
+    // ReLU and identity: s1 is folded into the staged W1 rows and b1 starts
+    // the expand accumulators, so the activation is a packed convert (and a
+    // packed max); GELU applies s1, b1 and erf in fp32
+    static constexpr bool FOLD = ACT != ACT_GELU;
+
+    // ---- 16-byte piece p of a chunk of the FFN weights, in fragment order.
+    // Where a piece comes from does not depend on the chunk except through a
+    // chunk offset, so each thread sets its pieces up once (PieceRef) and a
+    // chunk load is an add and a compare per piece.
+    struct PieceRef {
+        int kind;      // 0 W1, 1 W2, 2 s1 / b1, 3 none
+        int rowc;      // W1: row within the chunk; W2: hidden column within the chunk; 2: hidden within the chunk
+        int off;       // element offset at chunk 0 (W1: row * C + col; W2: o * EC + col; 2: hidden)
+        int sel;       // W1: col < C; 2: 0 = s1, 1 = b1
+    };
+    static __device__ __forceinline__ PieceRef piece_ref(const Args &a, int p) {
+        PieceRef r{3, 0, 0, 0};
+        if (p < 2 * KST * 64) {
+            const int f = p >> 6, ln = p & 63, t = f / KST, kk = f - t * KST;
+            const int m = ln & 15, qq = ln >> 4;
+            const int row = 8 * (m >> 2) + 4 * t + (m & 3);
+            const int col = 32 * kk + 8 * qq;
+            r = PieceRef{0, row, row * C + col, col < C ? 1 : 0};
+        } else if (p < (2 * KST + MO) * 64) {
+            const int pp = p - 2 * KST * 64;
+            const int mo = pp >> 6, ln = pp & 63;
+            const int o = 16 * mo + (ln & 15), hc = 8 * (ln >> 4);
+            r = PieceRef{1, hc, o * a.EC + hc, 0};
+        } else if (p < CPIECES) {
+            const int jv = p - (2 * KST + MO) * 64;  // 0..7: s1, 8..15: b1
+            r = PieceRef{2, 4 * (jv & 7), 4 * (jv & 7), jv >> 3};
         }
+        return r;
+    }
+    static __device__ __forceinline__ u32x4 piece_at(const Args &a, const PieceRef &r, int ch) {
+        u32x4 v = {0u, 0u, 0u, 0u};
+        const int h0 = ch * 32;
+        if (r.kind == 0) {
+            if (r.sel && h0 + r.rowc < a.EC) {
+                v = *reinterpret_cast<const u32x4 *>(a.w1 + (size_t)h0 * C + r.off);
+                if (FOLD && a.s1)
+                    v = fused::scale8<T>(v, a.s1[h0 + r.rowc]);
+            }
+        } else if (r.kind == 1) {
+            if (h0 + r.rowc < a.EC)
+                v = *reinterpret_cast<const u32x4 *>(a.w2 + r.off + h0);
+        } else if (r.kind == 2) {
+            float4v f = {0.f, 0.f, 0.f, 0.f};
+            if (h0 + r.rowc < a.EC) {
+                const float *src = r.sel ? a.b1 : a.s1;
+                if (src)
+                    f = *reinterpret_cast<const float4v *>(src + h0 + r.off);
+                else if (!r.sel)
+                    f = float4v{1.f, 1.f, 1.f, 1.f};
+            }
+            v = __builtin_bit_cast(u32x4, f);
+        }
+        return v;
+    }
+    static __device__ __forceinline__ void chunk_load(const Args &a, const PieceRef (&pr)[CPT], int ch,
+                                                      u32x4 (&r)[CPT]) {
+#pragma unroll
+        for (int u = 0; u < CPT; u++)
+            r[u] = piece_at(a, pr[u], ch);
     }
     static __device__ __forceinline__ void chunk_store(uint8_t *slot, int tid, const u32x4 (&r)[CPT]) {
 #pragma unroll
@@ -150,7 +208,7 @@ struct GB {
         }
     }
 
-    // ---- block geometry
+    // ---- block geometry (wave-uniform: scalar registers)
     struct Blk {
         int n, r0, c0;  // image, first row, first column
         bool valid;
@@ -160,40 +218,58 @@ struct GB {
         k.valid = b < a.nblocks;
         const int bb = k.valid ? b : 0;
         const int seg = bb % a.SEG, t = bb / a.SEG;
-        const int rp = t % a.RP;
-        k.n = t / a.RP;
-        k.r0 = 2 * rp;
-        k.c0 = 16 * seg;
+        const int rb = t % a.RB;
+        k.n = t / a.RB;
+        k.r0 = BR * rb;
+        k.c0 = BC * seg;
         return k;
     }
 
-    // halo piece i of block k: global source (or null for a zero pixel) and
-    // LDS offset within the wave's region
-    static __device__ __forceinline__ u32x4 halo_piece(const Args &a, const Blk &k, int i, uint32_t &dst) {
+    // halo of block k: pieces are (pixel px = r * HC + cc of the 6 x 18
+    // window, 16-byte channel piece cq); the window's top-left pixel
+    // (r0 - 1, c0 - 1) is the base, so a piece is a 32-bit offset from it
+    struct HaloCtx {
+        const uint16_t *base;  // element address of window pixel (0, 0) (may lie outside x; read only in bounds)
+        int rlo, rhi, clo, chi;  // window rows r with rlo <= r < rhi and columns likewise lie in the image
+        int WC;                  // W * C
+    };
+    static __device__ __forceinline__ HaloCtx halo_ctx(const Args &a, const Blk &k) {
+        HaloCtx h;
+        const int64_t pix0 = ((int64_t)k.n * a.H + (k.r0 - 1)) * a.W + (k.c0 - 1);
+        h.base = a.x + pix0 * C;
+        h.rlo = k.valid ? 1 - k.r0 : HR;   // an invalid block reads nothing
+        h.rhi = a.H - k.r0 + 1;
+        h.clo = 1 - k.c0;
+        h.chi = a.W - k.c0 + 1;
+        h.WC = a.W * C;
+        return h;
+    }
+    static __device__ __forceinline__ u32x4 halo_piece(const HaloCtx &h, int i, uint32_t &dst) {
         const int px = i / C8, cq = i - px * C8;
         const int r = px / HC, cc = px - r * HC;
-        const int h = k.r0 - 1 + r, w = k.c0 - 1 + cc;
         dst = (uint32_t)px * PB + (uint32_t)cq * 16;
         u32x4 v = {0u, 0u, 0u, 0u};
-        if (k.valid && h >= 0 && h < a.H && w >= 0 && w < a.W)
-            v = *reinterpret_cast<const u32x4 *>(a.x + (((size_t)k.n * a.H + h) * a.W + w) * C + 8 * cq);
+        if (r >= h.rlo && r < h.rhi && cc >= h.clo && cc < h.chi)
+            v = *reinterpret_cast<const u32x4 *>(h.base + (r * h.WC + cc * C + 8 * cq));
         return v;
     }
-    static __device__ __forceinline__ void halo_step_load(const Args &a, const Blk &k, int step, int lane,
-                                                          u32x4 (&v)[HSTEP], uint32_t (&d)[HSTEP]) {
+    // the lane's pieces (first + u) * 64 + lane, u < NP
+    template <int NP>
+    static __device__ __forceinline__ void halo_load(const HaloCtx &h, int first, int lane, u32x4 (&v)[NP],
+                                                     uint32_t (&d)[NP]) {
 #pragma unroll
-        for (int u = 0; u < HSTEP; u++) {
-            const int i = (step * HSTEP + u) * 64 + lane;
+        for (int u = 0; u < NP; u++) {
+            const int i = (first + u) * 64 + lane;
             d[u] = 0xffffffffu;
             v[u] = u32x4{0u, 0u, 0u, 0u};
             if (i < HPIECES)
-                v[u] = halo_piece(a, k, i, d[u]);
+                v[u] = halo_piece(h, i, d[u]);
         }
     }
-    static __device__ __forceinline__ void halo_step_store(uint8_t *reg, const u32x4 (&v)[HSTEP],
-                                                           const uint32_t (&d)[HSTEP]) {
+    template <int NP>
+    static __device__ __forceinline__ void halo_store(uint8_t *reg, const u32x4 (&v)[NP], const uint32_t (&d)[NP]) {
 #pragma unroll
-        for (int u = 0; u < HSTEP; u++)
+        for (int u = 0; u < NP; u++)
             if (d[u] != 0xffffffffu)
                 sts16(reg, d[u], v[u]);
     }
@@ -208,18 +284,20 @@ struct GB {
     }
 
     static __device__ void run(const Args &a, uint8_t *smem) {
-        const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+        const int tid = threadIdx.x, lane = tid & 63;
+        const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: block indices stay scalar
         const int q = lane >> 4, jl = lane & 15;
-        const int G = gridDim.x;
-        const int gi = a.xcd_map ? (int)(blockIdx.x % 8) * (G / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
+        const int Gn = gridDim.x;
+        const int gi = a.xcd_map ? (int)(blockIdx.x % 8) * (Gn / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
         const int nr = a.rbase + (gi < a.rextra ? 1 : 0);
         const int rstart = gi * a.rbase + (gi < a.rextra ? gi : a.rextra);
         if (nr == 0)
             return;  // uniform over the workgroup, before any barrier
 
         uint8_t *gwl = smem;
-        uint8_t *ring = smem + OFF_RING;
-        uint8_t *reg = smem + OFF_HALO + wv * HALO;
+        uint8_t *wts = smem + G::OFF_W;
+        uint8_t *reg = smem + a.off_halo + wv * HALO;
+        const float *vec = reinterpret_cast<const float *>(smem + G::OFF_VEC);
 
         // grouped-conv taps: tap row i at i * GROW, then (column, channel) x 16 B
         for (int i = tid; i < 9 * C; i += NT) {
@@ -231,20 +309,39 @@ struct GB {
         for (int i = tid; i < 4 * C; i += NT) {
             const int v = i / C, c = i - v * C;
             const float *src = v == 0 ? a.s0 : v == 1 ? a.b0 : v == 2 ? a.s2 : a.b2;
-            reinterpret_cast<float *>(smem + OFF_VEC)[i] = src ? src[c] : (v == 0 || v == 2 ? 1.0f : 0.0f);
+            reinterpret_cast<float *>(smem + G::OFF_VEC)[i] = src ? src[c] : (v == 0 || v == 2 ? 1.0f : 0.0f);
         }
-        const float *vec = reinterpret_cast<const float *>(smem + OFF_VEC);
-        u32x4 cst[CPT];
-        chunk_load(a, 0, tid, cst);
-        chunk_store(ring, tid, cst);
-        // the first block's halo
+        // FFN weights: every chunk (resident), or chunk 0 in slot 0 with chunk
+        // 1 waiting in registers (ring)
+        u32x4 cA[CPT], cB[CPT];
+        PieceRef pref[CPT];
+#pragma unroll
+        for (int u = 0; u < CPT; u++)
+            pref[u] = piece_ref(a, u * NT + tid);
+        if constexpr (RES) {
+            for (int ch = 0; ch < a.nch; ch++) {
+                chunk_load(a, pref, ch, cA);
+                chunk_store(wts + (uint32_t)ch * CHB, tid, cA);
+            }
+        } else {
+            chunk_load(a, pref, 0, cA);
+            chunk_store(wts, tid, cA);
+            chunk_load(a, pref, a.nch > 1 ? 1 : 0, cA);
+        }
+        // halo of the first block; with PREF2 the second block's waits in registers
+        u32x4 hv[PREF2 ? HPL : 1];
+        uint32_t hd[PREF2 ? HPL : 1];
         {
-            const Blk k0 = decode(a, rstart * NW + wv);
+            const HaloCtx h0 = halo_ctx(a, decode(a, rstart * NW + wv));
             for (int s = 0; s < HSTEPS; s++) {
                 u32x4 v[HSTEP];
                 uint32_t d[HSTEP];
-                halo_step_load(a, k0, s, lane, v, d);
-                halo_step_store(reg, v, d);
+                halo_load<HSTEP>(h0, s * HSTEP, lane, v, d);
+                halo_store<HSTEP>(reg, v, d);
+            }
+            if constexpr (PREF2) {
+                if (nr > 1)
+                    halo_load<HPL>(halo_ctx(a, decode(a, (rstart + 1) * NW + wv)), 0, lane, hv, hd);
             }
         }
         __syncthreads();
@@ -254,165 +351,216 @@ struct GB {
         const int ti = q - cs;
         const bool tap_ok = ti >= 0 && ti <= 2;
         const uint32_t a_off = (uint32_t)(tap_ok ? ti : 0) * GROW + (uint32_t)co * 16;
-        // D rows of this lane: block row q >> 1, channels 8g + 4 (q & 1) + e
+        // D rows of this lane: block row 2p + (q >> 1), channels 8g + 4 (q & 1) + e
         const int drow = q >> 1, dch = 4 * (q & 1);
 
-        int slot = 0;
-        for (int r = 0; r < nr; r++) {
-            const Blk k = decode(a, (rstart + r) * NW + wv);
+        // block state
+        u32x4 dfr[BR][KST];
+        float4v acc[BR][MO];
+        Blk kcur;
+        int cur_r = 0;
 
-            // 1. grouped conv, one group at a time.  Group g's d values overwrite
-            //    only bytes of channels 8g..8g+7 of the wave's first 32 halo
-            //    pixels, which later groups do not read, and this group's own
-            //    halo reads precede the writes in the wave's LDS queue.
+        // ---- start of block r: conv, d, B fragments, halo prefetch
+        auto block_begin = [&](int r) {
+            cur_r = r;
+            kcur = decode(a, (rstart + r) * NW + wv);
 #pragma unroll
             for (int g = 0; g < NG; g++) {
-                float4v acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int dj = 0; dj < 3; dj++) {
-                    const u32x4 av = tap_ok ? lds16(gwl, a_off + (uint32_t)(dj * C + GW * g) * 16)
-                                            : u32x4{0u, 0u, 0u, 0u};
-                    const u32x4 bv = lds16(reg, (uint32_t)(q * HC + jl + dj) * PB + (uint32_t)g * 16);
-                    acc = T::mfma(av, bv, acc);
-                }
                 const int c = GW * g + dch;
                 const float4v sc = *reinterpret_cast<const float4v *>(vec + c);
                 const float4v bi = *reinterpret_cast<const float4v *>(vec + C + c);
-                float v[4];
+                u32x4 av[3];
 #pragma unroll
-                for (int e = 0; e < 4; e++)
-                    v[e] = fmaf(acc[e], sc[e], bi[e]);
-                *reinterpret_cast<u32x2 *>(reg + (uint32_t)(drow * BC + jl) * PB + (uint32_t)c * 2) =
-                    u32x2{T::pack2(v[0], v[1]), T::pack2(v[2], v[3])};
+                for (int dj = 0; dj < 3; dj++)
+                    av[dj] = tap_ok ? lds16(gwl, a_off + (uint32_t)(dj * C + GW * g) * 16) : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+                for (int pr = 0; pr < BR / 2; pr++) {
+                    float4v cacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int dj = 0; dj < 3; dj++) {
+                        const u32x4 bv =
+                            lds16(reg, (uint32_t)((2 * pr + q) * HC + jl + dj) * PB + (uint32_t)g * 16);
+                        cacc = T::mfma(av[dj], bv, cacc);
+                    }
+                    float v[4];
+#pragma unroll
+                    for (int e = 0; e < 4; e++)
+                        v[e] = fmaf(cacc[e], sc[e], bi[e]);
+                    *reinterpret_cast<u32x2 *>(reg + (uint32_t)((2 * pr + drow) * BC + jl) * PB + (uint32_t)c * 2) =
+                        u32x2{T::pack2(v[0], v[1]), T::pack2(v[2], v[3])};
+                }
             }
-            // 2. d comes back as the expand's B fragments
-            u32x4 dfr[2][KST];
 #pragma unroll
-            for (int nt = 0; nt < 2; nt++)
+            for (int nt = 0; nt < BR; nt++)
 #pragma unroll
                 for (int kk = 0; kk < KST; kk++)
                     dfr[nt][kk] = (32 * kk + 8 * q < C)
                                       ? lds16(reg, (uint32_t)(nt * BC + jl) * PB + (uint32_t)(32 * kk + 8 * q) * 2)
                                       : u32x4{0u, 0u, 0u, 0u};
-
-            // 3. FFN over the hidden chunks; the next block's halo arrives meanwhile
-            const bool more = r + 1 < nr;
-            const Blk kn = decode(a, (rstart + r + 1) * NW + wv);
-            float4v acc[2][MO];
 #pragma unroll
-            for (int nt = 0; nt < 2; nt++)
+            for (int nt = 0; nt < BR; nt++)
 #pragma unroll
                 for (int mo = 0; mo < MO; mo++)
                     acc[nt][mo] = float4v{0.f, 0.f, 0.f, 0.f};
-            for (int ch = 0; ch < a.nch; ch++) {
-                const int nxt = ch + 1 < a.nch ? ch + 1 : 0;
-                chunk_load(a, nxt, tid, cst);
-                u32x4 hv[HSTEP];
-                uint32_t hd[HSTEP];
-                const bool hstep = more && ch < HSTEPS;
-                if (hstep)
-                    halo_step_load(a, kn, ch, lane, hv, hd);
+            if constexpr (PREF2) {
+                // the region is free: block r+1's halo in, block r+2's loads out
+                if (r + 1 < nr)
+                    halo_store<HPL>(reg, hv, hd);
+                if (r + 2 < nr)
+                    halo_load<HPL>(halo_ctx(a, decode(a, (rstart + r + 2) * NW + wv)), 0, lane, hv, hd);
+            }
+        };
 
-                const uint8_t *cur = ring + slot * CHB;
-                float s1v[8], b1v[8];
-                {
-                    const float4v s_lo = *reinterpret_cast<const float4v *>(cur + W1B + W2B + 32 * q);
-                    const float4v s_hi = *reinterpret_cast<const float4v *>(cur + W1B + W2B + 32 * q + 16);
-                    const float4v b_lo = *reinterpret_cast<const float4v *>(cur + W1B + W2B + 128 + 32 * q);
-                    const float4v b_hi = *reinterpret_cast<const float4v *>(cur + W1B + W2B + 128 + 32 * q + 16);
+        // ---- one hidden chunk of the current block from weights at `cw`
+        auto chunk = [&](int ch, const uint8_t *cw) {
+            u32x4 sv[HSTEP];
+            uint32_t sd[HSTEP];
+            const bool hstep = !PREF2 && cur_r + 1 < nr && ch < HSTEPS;
+            if (hstep)
+                halo_load<HSTEP>(halo_ctx(a, decode(a, (rstart + cur_r + 1) * NW + wv)), ch * HSTEP, lane, sv, sd);
+            float s1v[8], b1v[8];
+            {
+                const float4v s_lo = *reinterpret_cast<const float4v *>(cw + W1B + W2B + 32 * q);
+                const float4v s_hi = *reinterpret_cast<const float4v *>(cw + W1B + W2B + 32 * q + 16);
+                const float4v b_lo = *reinterpret_cast<const float4v *>(cw + W1B + W2B + 128 + 32 * q);
+                const float4v b_hi = *reinterpret_cast<const float4v *>(cw + W1B + W2B + 128 + 32 * q + 16);
 #pragma unroll
-                    for (int e = 0; e < 4; e++) {
-                        s1v[e] = s_lo[e];
-                        s1v[4 + e] = s_hi[e];
-                        b1v[e] = b_lo[e];
-                        b1v[4 + e] = b_hi[e];
-                    }
+                for (int e = 0; e < 4; e++) {
+                    s1v[e] = s_lo[e];
+                    s1v[4 + e] = s_hi[e];
+                    b1v[e] = b_lo[e];
+                    b1v[4 + e] = b_hi[e];
                 }
-                u32x4 a1[2][KST];
+            }
+            u32x4 a1[2][KST];
 #pragma unroll
-                for (int t = 0; t < 2; t++)
+            for (int t = 0; t < 2; t++)
+#pragma unroll
+                for (int kk = 0; kk < KST; kk++)
+                    a1[t][kk] = lds16(cw, (uint32_t)(t * KST + kk) * 1024 + (uint32_t)lane * 16);
+            u32x4 gfr[BR];
+#pragma unroll
+            for (int nt = 0; nt < BR; nt++) {
+                float u[8];
+#pragma unroll
+                for (int t = 0; t < 2; t++) {
+                    float4v e = FOLD ? float4v{b1v[4 * t], b1v[4 * t + 1], b1v[4 * t + 2], b1v[4 * t + 3]}
+                                     : float4v{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                     for (int kk = 0; kk < KST; kk++)
-                        a1[t][kk] = lds16(cur, (uint32_t)(t * KST + kk) * 1024 + (uint32_t)lane * 16);
-                u32x4 gfr[2];
+                        e = T::mfma(a1[t][kk], dfr[nt][kk], e);
 #pragma unroll
-                for (int nt = 0; nt < 2; nt++) {
-                    float u[8];
+                    for (int i = 0; i < 4; i++)
+                        u[4 * t + i] = FOLD ? e[i] : act(fmaf(e[i], s1v[4 * t + i], b1v[4 * t + i]));
+                }
+                if constexpr (FOLD && ACT == ACT_RELU && !T::is_bf16) {
+                    // round, then the packed max: max(round(u), 0) = round(max(u, 0))
+                    u32x4 g;
 #pragma unroll
-                    for (int t = 0; t < 2; t++) {
-                        float4v e = {0.f, 0.f, 0.f, 0.f};
+                    for (int i = 0; i < 4; i++)
+                        g[i] = __builtin_bit_cast(
+                            uint32_t, __builtin_elementwise_max(__builtin_bit_cast(half2v, T::pack2(u[2 * i], u[2 * i + 1])),
+                                                                half2v{(_Float16)0.0f, (_Float16)0.0f}));
+                    gfr[nt] = g;
+                } else {
+                    if constexpr (FOLD && ACT == ACT_RELU)
 #pragma unroll
-                        for (int kk = 0; kk < KST; kk++)
-                            e = T::mfma(a1[t][kk], dfr[nt][kk], e);
-#pragma unroll
-                        for (int i = 0; i < 4; i++)
-                            u[4 * t + i] = act(fmaf(e[i], s1v[4 * t + i], b1v[4 * t + i]));
-                    }
+                        for (int i = 0; i < 8; i++)
+                            u[i] = fmaxf(u[i], 0.0f);
                     gfr[nt] = u32x4{T::pack2(u[0], u[1]), T::pack2(u[2], u[3]), T::pack2(u[4], u[5]),
                                     T::pack2(u[6], u[7])};
                 }
-#pragma unroll
-                for (int mo = 0; mo < MO; mo++) {
-                    const u32x4 a2 = lds16(cur, (uint32_t)W1B + (uint32_t)mo * 1024 + (uint32_t)lane * 16);
-#pragma unroll
-                    for (int nt = 0; nt < 2; nt++)
-                        acc[nt][mo] = T::mfma(a2, gfr[nt], acc[nt][mo]);
-                }
-                chunk_store(ring + (slot ^ 1) * CHB, tid, cst);
-                if (hstep)
-                    halo_step_store(reg, hv, hd);
-                __syncthreads();
-                slot ^= 1;
             }
-            // halo steps the chunks did not cover
-            if (more) {
-                for (int s = a.nch; s < HSTEPS; s++) {
-                    u32x4 hv[HSTEP];
-                    uint32_t hd[HSTEP];
-                    halo_step_load(a, kn, s, lane, hv, hd);
-                    halo_step_store(reg, hv, hd);
-                }
+#pragma unroll
+            for (int mo = 0; mo < MO; mo++) {
+                const u32x4 a2 = lds16(cw, (uint32_t)W1B + (uint32_t)mo * 1024 + (uint32_t)lane * 16);
+#pragma unroll
+                for (int nt = 0; nt < BR; nt++)
+                    acc[nt][mo] = T::mfma(a2, gfr[nt], acc[nt][mo]);
             }
+            if (hstep)
+                halo_store<HSTEP>(reg, sv, sd);
+        };
 
-            // 4. epilogue: y = x + s2 * acc + b2 for the block's valid pixels
-            if (k.valid) {
-#pragma unroll
-                for (int nt = 0; nt < 2; nt++) {
-                    const int h = k.r0 + nt, w = k.c0 + jl;
-                    if (h >= a.H || w >= a.W)
-                        continue;
-                    const size_t pix = ((size_t)k.n * a.H + h) * a.W + w;
-#pragma unroll
-                    for (int mo = 0; mo < MO; mo++) {
-                        const int c = 16 * mo + 4 * q;
-                        const u32x2 xv = *reinterpret_cast<const u32x2 *>(a.x + pix * C + c);
-                        const float4v sc = *reinterpret_cast<const float4v *>(vec + 2 * C + c);
-                        const float4v bi = *reinterpret_cast<const float4v *>(vec + 3 * C + c);
-                        float o[4];
-#pragma unroll
-                        for (int e = 0; e < 4; e++)
-                            o[e] = fmaf(acc[nt][mo][e], sc[e], bi[e]);
-                        const u32x2 ov = {T::pack2(T::lo(xv[0]) + o[0], T::hi(xv[0]) + o[1]),
-                                          T::pack2(T::lo(xv[1]) + o[2], T::hi(xv[1]) + o[3])};
-                        *reinterpret_cast<u32x2 *>(a.y + pix * C + c) = ov;
+        // ---- end of block: remaining halo steps, epilogue y = x + s2 acc + b2
+        auto block_end = [&]() {
+            if constexpr (!PREF2) {
+                if (cur_r + 1 < nr) {
+                    const HaloCtx hn = halo_ctx(a, decode(a, (rstart + cur_r + 1) * NW + wv));
+                    for (int s = a.nch; s < HSTEPS; s++) {
+                        u32x4 v[HSTEP];
+                        uint32_t d[HSTEP];
+                        halo_load<HSTEP>(hn, s * HSTEP, lane, v, d);
+                        halo_store<HSTEP>(reg, v, d);
                     }
                 }
+            }
+            if (!kcur.valid)
+                return;
+#pragma unroll
+            for (int nt = 0; nt < BR; nt++) {
+                const int h = kcur.r0 + nt, w = kcur.c0 + jl;
+                if (h >= a.H || w >= a.W)
+                    continue;
+                const size_t pix = ((size_t)kcur.n * a.H + h) * a.W + w;
+#pragma unroll
+                for (int mo = 0; mo < MO; mo++) {
+                    const int c = 16 * mo + 4 * q;
+                    const u32x2 xv = *reinterpret_cast<const u32x2 *>(a.x + pix * C + c);
+                    const float4v sc = *reinterpret_cast<const float4v *>(vec + 2 * C + c);
+                    const float4v bi = *reinterpret_cast<const float4v *>(vec + 3 * C + c);
+                    float o[4];
+#pragma unroll
+                    for (int e = 0; e < 4; e++)
+                        o[e] = fmaf(acc[nt][mo][e], sc[e], bi[e]);
+                    const u32x2 ov = {T::pack2(T::lo(xv[0]) + o[0], T::hi(xv[0]) + o[1]),
+                                      T::pack2(T::lo(xv[1]) + o[2], T::hi(xv[1]) + o[3])};
+                    *reinterpret_cast<u32x2 *>(a.y + pix * C + c) = ov;
+                }
+            }
+        };
+
+        if constexpr (RES) {
+            // every chunk resident: the waves run independently from here on
+            for (int r = 0; r < nr; r++) {
+                block_begin(r);
+                for (int ch = 0; ch < a.nch; ch++)
+                    chunk(ch, wts + (uint32_t)ch * CHB);
+                block_end();
+            }
+        } else {
+            // ring: global chunk step j = r * nch + ch uses slot j & 1.  On
+            // entry to step j the slot holds chunk j and the register set
+            // `pend` holds chunk j+1; the step loads chunk j+2 into the other
+            // set, computes chunk j, stores `pend` into the other slot and
+            // passes the barrier.  Steps go in pairs so that each register
+            // set keeps a fixed role.
+            const int total = nr * a.nch;
+            auto step = [&](int j, u32x4 (&pend)[CPT], u32x4 (&next)[CPT]) {
+                const int r = j / a.nch, ch = j - r * a.nch;
+                if (ch == 0)
+                    block_begin(r);
+                chunk_load(a, pref, (j + 2) % a.nch, next);  // (past the last step: unused reloads)
+                chunk(ch, wts + (uint32_t)(j & 1) * CHB);
+                chunk_store(wts + (uint32_t)((j + 1) & 1) * CHB, tid, pend);
+                __syncthreads();
+                if (ch == a.nch - 1)
+                    block_end();
+            };
+            for (int j = 0; j < total; j += 2) {
+                step(j, cA, cB);
+                if (j + 1 < total)
+                    step(j + 1, cB, cA);
             }
         }
     }
 };
 
-template <int C, int NW, typename T, int ACT>
+template <int C, int NW, typename T, int ACT, bool RES>
 __global__ __launch_bounds__(NW * 64, 1) void gblock_kernel(Args a) {
     extern __shared__ __attribute__((aligned(256))) uint8_t smem[];
-    GB<C, NW, T, ACT>::run(a, smem);
+    GB<C, NW, T, ACT, RES>::run(a, smem);
 }
-
-// waves per workgroup for a channel count: 8 where their halo regions fit
-constexpr int nw_for(int C) { return C <= 96 ? 8 : 4; }
-
-template <int C>
-constexpr size_t lds_for() { return (size_t)GB<C, nw_for(C), F16, ACT_RELU>::LDS; }
 
 template <int C>
 hipError_t launch_c(const void *x, void *y, const GBlockW &w, const Shape &s, hipStream_t st) {
@@ -433,26 +581,31 @@ hipError_t launch_c(const void *x, void *y, const GBlockW &w, const Shape &s, hi
     a.W = s.W;
     a.EC = s.E * C;
     a.nch = (a.EC + 31) / 32;
-    a.RP = (s.H + 1) / 2;
-    a.SEG = (s.W + 15) / 16;
-    const int64_t nb = (int64_t)s.N * a.RP * a.SEG;
+    a.RB = (s.H + BR - 1) / BR;
+    a.SEG = (s.W + BC - 1) / BC;
+    const int64_t nb = (int64_t)s.N * a.RB * a.SEG;
     if (nb > ((int64_t)1 << 30))
         return hipErrorInvalidValue;
     a.nblocks = (int)nb;
     const int rounds = (int)((nb + NW - 1) / NW);
     const int cus = device_cu_count();
-    const int G = rounds < cus ? rounds : cus;
-    a.rbase = rounds / G;
-    a.rextra = rounds % G;
-    a.xcd_map = (G % 8 == 0) ? 1 : 0;
-    const size_t lds = GB<C, NW, F16, ACT_RELU>::LDS;
+    const int Gn = rounds < cus ? rounds : cus;
+    a.rbase = rounds / Gn;
+    a.rextra = rounds % Gn;
+    a.xcd_map = (Gn % 8 == 0) ? 1 : 0;
+    const size_t lds_res = lds_bytes<C>(a.nch, true);
+    const bool res = lds_res <= 160 * 1024;
+    const size_t lds = res ? lds_res : lds_bytes<C>(a.nch, false);
+    if (lds > 160 * 1024)
+        return hipErrorInvalidConfiguration;
+    a.off_halo = (uint32_t)(lds - (size_t)NW * Geo<C>::HALO);
     hipError_t e;
-#define CF_GB_LAUNCH(TT, AC)                                           \
-    {                                                                  \
-        auto kf = gblock_kernel<C, NW, TT, AC>;                        \
-        if ((e = allow_full_lds((const void *)kf)) != hipSuccess)      \
-            return e;                                                  \
-        hipLaunchKernelGGL(kf, dim3(G), dim3(NW * 64), lds, st, a);    \
+#define CF_GB_LAUNCH(TT, AC)                                                                          \
+    {                                                                                                 \
+        auto kf = res ? gblock_kernel<C, NW, TT, AC, true> : gblock_kernel<C, NW, TT, AC, false>;     \
+        if ((e = allow_full_lds((const void *)kf)) != hipSuccess)                                     \
+            return e;                                                                                 \
+        hipLaunchKernelGGL(kf, dim3(Gn), dim3(NW * 64), lds, st, a);                                  \
     }
     if (s.bf16) {
         switch (s.act) {

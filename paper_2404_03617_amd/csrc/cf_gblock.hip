@@ -11,9 +11,8 @@ hipError_t launch_gblock_c64(const void *, void *, const GBlockW &, const Shape 
 hipError_t launch_gblock_c80(const void *, void *, const GBlockW &, const Shape &, hipStream_t);
 hipError_t launch_gblock_c96(const void *, void *, const GBlockW &, const Shape &, hipStream_t);
 hipError_t launch_gblock_c112(const void *, void *, const GBlockW &, const Shape &, hipStream_t);
-hipError_t launch_gblock_c128(const void *, void *, const GBlockW &, const Shape &, hipStream_t);
 
-bool gblock_supported_c(int C) { return C >= 16 && C <= 128 && C % 16 == 0; }
+bool gblock_supported_c(int C) { return C >= 16 && C <= 112 && C % 16 == 0; }
 
 hipError_t launch_gblock(const void *x, void *y, const GBlockW &w, const Shape &s, hipStream_t st) {
     switch (s.C) {
@@ -24,7 +23,6 @@ hipError_t launch_gblock(const void *x, void *y, const GBlockW &w, const Shape &
     case 80: return launch_gblock_c80(x, y, w, s, st);
     case 96: return launch_gblock_c96(x, y, w, s, st);
     case 112: return launch_gblock_c112(x, y, w, s, st);
-    case 128: return launch_gblock_c128(x, y, w, s, st);
     default: return hipErrorInvalidValue;
     }
 }

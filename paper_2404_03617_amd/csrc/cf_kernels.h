@@ -95,7 +95,7 @@ struct GBlockW {
     const void *w2;
     const float *s2, *b2;
 };
-// Channel counts with a kernel: multiples of 16 from 16 to 128.
+// Channel counts with a kernel: multiples of 16 from 16 to 112.
 bool gblock_supported_c(int C);
 // Fused grouped block; hipErrorInvalidValue for an unsupported C.
 hipError_t launch_gblock(const void *x, void *y, const GBlockW &w, const Shape &s, hipStream_t st);

@@ -352,6 +352,8 @@ def test_gblock_forward_rejects():
     assert call(y=X + 32) == cf.CF_ERR_INVALID      # overlaps x
     assert call(b1=W1 + 4) == cf.CF_ERR_INVALID     # misaligned
     assert call(C=24) == cf.CF_ERR_UNSUPPORTED      # multiple of 8, not of 16
+    assert call(C=128) == cf.CF_ERR_UNSUPPORTED
     assert call(C=256) == cf.CF_ERR_UNSUPPORTED
     assert call(k=5) == cf.CF_ERR_UNSUPPORTED
+    assert call(H=1, W=6_000_000, y=0x400000000) == cf.CF_ERR_UNSUPPORTED  # 32-bit row offsets
     assert L.cf_last_error().decode().startswith("cf_gblock_forward")

@@ -50,7 +50,8 @@ SWEEP = [
     (80, 3, 2, 6, 17),
     (96, 6, 1, 12, 12),
     (112, 2, 2, 5, 9),
-    (128, 4, 1, 9, 18),
+    (96, 1, 1, 4, 33),      # one row band, three segments
+    (112, 4, 1, 9, 18),
 ]
 
 
