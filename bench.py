@@ -479,7 +479,9 @@ def main():
         out["other_workloads"] = extra
     if args.calib_copy:
         calib_copy()
-    clk = shader_clock_mhz_under_load(res["launch"], 1.0, t)
+    # (a second of extra launches: part of the full run only, not of the
+    # short runs that profiles are taken from)
+    clk = None if args.no_extra else shader_clock_mhz_under_load(res["launch"], 1.0, t)
     out["sclk_mhz_under_load"] = None if clk is None else round(clk, 1)
     if clk:
         # computational efficiency against the peak at the clock the GPU ran at
