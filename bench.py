@@ -269,6 +269,31 @@ def stack_waterline(name: str, steps: int, warmup: int):
             "unfused_T_min_us": round(T_u * 1e6, 1), "unfused_C_max": round(C_u, 4), "unfused_kernels": len(unf)}
 
 
+STAGE_MB_WORKLOAD = "stack_n128_56x56_d2262_c64to512_e4_k3_f16"
+
+
+def stage_microbatch_case(micro_batches, steps: int, warmup: int):
+    """Stage 1 of the four-stage stack (two C = 64 blocks at 56 x 56, N = 128)
+    as the plain stage and with the micro-batch schedule of Sec. 5.5.2 at
+    several micro-batch sizes (0: the library's default)."""
+    w = WORKLOADS[STAGE_MB_WORKLOAD]
+    N, H, W, C, d = w["N"], w["H"], w["W"], w["widths"][0], w["depths"][0]
+    layers = synth.stack_layers(w["seed"], w["depths"], w["widths"], w["E"], w["k"], w["dtype"])
+    blocks = [{kk: (None if v is None else v.cuda()) for kk, v in p.items()} for _, p in layers[:d]]
+    nsets = _sets_needed(2 * N * H * W * C * 2)
+    xs = [synth.activations(w["seed"] + 100 * i, N, H, W, C, w["dtype"]).cuda() for i in range(nsets)]
+    y = torch.empty_like(xs[0])
+    stream = torch.cuda.current_stream()
+    out = {"stage": "2 blocks, N=%d %dx%d C=%d" % (N, H, W, C),
+           "plain_us": round(_time(lambda i: cf.stage_forward(xs[i % nsets], blocks, out=y), steps, warmup,
+                                   stream) * 1e6, 1)}
+    for m in micro_batches:
+        t = _time(lambda i: cf.stage_forward_microbatch(xs[i % nsets], blocks, micro_batch=m, out=y), steps,
+                  warmup, stream)
+        out["micro_batch_%s_us" % (m if m else "default")] = round(t * 1e6, 1)
+    return out
+
+
 def shader_clock_mhz_under_load(fn, seconds_of_work: float, launch_seconds: float):
     """GFX clock (MHz, mean over the XCDs) read with amd-smi while about
     `seconds_of_work` of launches of `fn` are queued on the GPU, so the reading
@@ -360,6 +385,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--stage-mb", type=int, default=None,
+                    help="time only stage 1 of the stack with this micro-batch (0: the plain stage); for profiles")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a 256 MiB elementwise copy (counter calibration)")
     args = ap.parse_args()
@@ -372,6 +399,12 @@ def main():
         sys.exit(2)
     cf.lib()
     name = args.workload
+    if args.stage_mb is not None:
+        r = stage_microbatch_case([args.stage_mb] if args.stage_mb else [], args.steps, args.warmup)
+        if args.calib_copy:
+            calib_copy()
+        print(json.dumps({"stage_microbatch": r, "micro_batch": args.stage_mb}), flush=True)
+        return
     if name in GBLOCK_WORKLOADS:
         # one of the paper's own block shapes as the timed workload (used for
         # profiles of that kernel); the default is the benchmark workload
@@ -474,6 +507,8 @@ def main():
                                           "T_min_us": round(s["waterline_T_min_s"] * 1e6, 1),
                                           "frac": round(s["waterline_T_min_s"] / s["seconds"], 4)},
                              "waterline": wl}
+        # the micro-batch schedule of a stage (Sec. 5.5.2) against the plain stage
+        extra["stage_microbatch"] = stage_microbatch_case([0, 64, 32, 16], max(5, args.steps // 2), 2)
         # the paper's own block at the shapes of its kernel benchmark table
         extra["paper_block_table"] = {nm: gblock_case(nm, max(5, args.steps // 2), 3) for nm in GBLOCK_WORKLOADS}
         out["other_workloads"] = extra

@@ -106,6 +106,29 @@ cf_status cf_stage_forward(const void *x, void *y, void *ws, size_t ws_bytes,
                            cf_dtype dt, cf_act act, void *stream);
 size_t cf_stage_workspace_bytes(int depth, int N, int H, int W, int C, cf_dtype dt);
 
+/* The stage with the micro-batch schedule of Sec. 5.5.2: the `depth` blocks
+ * run over micro-batches of `micro_batch` images -- all blocks over images
+ * 0..m-1, then all blocks over the next m images, and so on -- so the
+ * intermediate activations of one micro-batch (2 * m*H*W*C*2 bytes in the
+ * ping-pong buffers) can stay in on-chip caches between the blocks instead
+ * of making a round trip to DRAM per block.  Consecutive launches give a
+ * pixel range the same workgroup index, hence the same L2 (XCD), so a
+ * micro-batch whose activations fit the L2s is read back from them; one that
+ * fits the 256 MiB Infinity Cache is read back from it.  Only the stage's
+ * input and output need DRAM.  Results equal cf_stage_forward's up to the
+ * fp32 summation order of the hidden split it may use at C = 512 (none
+ * here).  micro_batch <= 0 picks a default: the largest micro-batch whose
+ * input and output activations fit 128 MiB (the whole batch whenever the
+ * stage's activations already fit the Infinity Cache); a micro_batch >= N
+ * runs the whole batch per block.  ws needs cf_stage_microbatch_workspace_bytes() bytes: two
+ * micro-batch buffers for depth > 2, one for depth == 2, none for depth 1. */
+cf_status cf_stage_forward_microbatch(const void *x, void *y, void *ws, size_t ws_bytes,
+                                      const cf_block_params *blocks, int depth,
+                                      int N, int H, int W, int C, int E, int k, int micro_batch,
+                                      cf_dtype dt, cf_act act, void *stream);
+size_t cf_stage_microbatch_workspace_bytes(int depth, int N, int H, int W, int C, int micro_batch,
+                                           cf_dtype dt);
+
 /* 2x2 stride-2 conv between stages: y[n][i][j][o] = scale[o] * sum_{a,b,c}
  * w[o][a][b][c] * x[n][2i+a][2j+b][c] + bias[o]  (eq. f:conv2d with R = S = 2,
  * stride 2, no padding; no activation, no residual).  H and W must be even;

@@ -23,6 +23,7 @@ from .convert import (block_params_from_modules, down_params_from_modules, down_
 
 __all__ = [
     "lib", "library_path", "block_forward", "block_autotune", "block_tuned_config", "stage_forward",
+    "stage_forward_microbatch",
     "downsample_forward",
     "block_forward_unfused", "block_forward_split", "block_forward_split_noalloc", "gblock_forward",
     "stack_forward", "capture_stack", "ConvFirstBlock",
@@ -39,7 +40,8 @@ DTYPES = {torch.float16: 0, torch.bfloat16: 1}
 ACTS = {"gelu": 0, "relu": 1, "none": 2}
 
 EXPORTED_SYMBOLS = (
-    "cf_block_forward", "cf_stage_forward", "cf_stage_workspace_bytes", "cf_downsample_forward",
+    "cf_block_forward", "cf_stage_forward", "cf_stage_workspace_bytes", "cf_stage_forward_microbatch",
+    "cf_stage_microbatch_workspace_bytes", "cf_downsample_forward",
     "cf_block_forward_unfused", "cf_unfused_workspace_bytes", "cf_block_forward_split",
     "cf_split_workspace_bytes", "cf_block_forward_split_noalloc", "cf_gblock_forward", "cf_block_autotune",
     "cf_block_tuned_config", "cf_last_error", "cf_status_string", "cf_abi_version",
@@ -88,6 +90,8 @@ def lib():
             "cf_block_forward": (i, [vp, vp, bp, i, i, i, i, i, i, i, i, vp]),
             "cf_stage_forward": (i, [vp, vp, vp, sz, bp, i, i, i, i, i, i, i, i, i, vp]),
             "cf_stage_workspace_bytes": (sz, [i, i, i, i, i, i]),
+            "cf_stage_forward_microbatch": (i, [vp, vp, vp, sz, bp, i, i, i, i, i, i, i, i, i, i, vp]),
+            "cf_stage_microbatch_workspace_bytes": (sz, [i, i, i, i, i, i, i]),
             "cf_downsample_forward": (i, [vp, vp, dp, i, i, i, i, i, i, vp]),
             "cf_block_forward_unfused": (i, [vp, vp, vp, sz, bp, i, i, i, i, i, i, i, i, vp]),
             "cf_unfused_workspace_bytes": (sz, [i, i, i, i, i, i]),
@@ -285,6 +289,33 @@ def stage_forward(x: torch.Tensor, blocks: list, act: str = "gelu", out=None, ws
     _check(L.cf_stage_forward(_ptr(x), _ptr(y), _ptr(ws), 0 if ws is None else ws.numel(),
                               arr, len(blocks), N, H, W, C, E, k, DTYPES[x.dtype], ACTS[act],
                               _stream(stream)))
+    return y
+
+
+def stage_forward_microbatch(x: torch.Tensor, blocks: list, act: str = "gelu", micro_batch: int = 0,
+                             out=None, ws=None, stream=None) -> torch.Tensor:
+    """The stage with the micro-batch schedule (Sec. 5.5.2): all blocks over
+    `micro_batch` images at a time, so the intermediate activations of a
+    micro-batch can stay in the caches between blocks (0: default size)."""
+    if not blocks:
+        raise ValueError("a stage needs at least one block")
+    if act not in ACTS:
+        raise ValueError("act must be one of %s" % sorted(ACTS))
+    keep = []
+    structs = [_block_struct(x, b, keep) for b in blocks]
+    dims = {_block_shape(x, b) for b in blocks}
+    if len(dims) != 1:
+        raise ValueError("every block of a stage must have the same shape")
+    N, H, W, C, E, k = dims.pop()
+    _check_device(x)
+    y = _out(x, out)
+    L = lib()
+    need = L.cf_stage_microbatch_workspace_bytes(len(blocks), N, H, W, C, micro_batch, DTYPES[x.dtype])
+    ws = _workspace(x, ws, need)
+    arr = (_BlockParams * len(blocks))(*structs)
+    _check(L.cf_stage_forward_microbatch(_ptr(x), _ptr(y), _ptr(ws), 0 if ws is None else ws.numel(), arr,
+                                         len(blocks), N, H, W, C, E, k, micro_batch, DTYPES[x.dtype], ACTS[act],
+                                         _stream(stream)))
     return y
 
 

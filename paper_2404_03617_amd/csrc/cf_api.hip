@@ -334,6 +334,79 @@ cf_status cf_stage_forward(const void *x, void *y, void *ws, size_t ws_bytes, co
     return CF_OK;
 }
 
+// Micro-batch size of the stage schedule: the given one clamped to [1, N], or
+// the largest whose activations (one micro-batch's input and output) fit
+// 128 MiB, half of the 256 MiB Infinity Cache.  Micro-batches small enough
+// for the L2 caches (4 MiB per XCD) leave most of the 256 CUs idle at these
+// image sizes, so the memory-side cache is the level the schedule targets.
+static int microbatch_size(int N, int H, int W, int C, int micro_batch, cf_dtype dt) {
+    if (micro_batch > 0)
+        return micro_batch < N ? micro_batch : N;
+    const double per_image = 2.0 * H * W * C * elem_bytes(dt);
+    int m = (int)((128.0 * 1024 * 1024) / per_image);
+    if (m < 1)
+        m = 1;
+    return m < N ? m : N;
+}
+
+size_t cf_stage_microbatch_workspace_bytes(int depth, int N, int H, int W, int C, int micro_batch, cf_dtype dt) {
+    if (depth <= 1 || N <= 0 || H <= 0 || W <= 0 || C <= 0)
+        return 0;
+    const int m = microbatch_size(N, H, W, C, micro_batch, dt);
+    const size_t one = round256((size_t)m * H * W * C * elem_bytes(dt));
+    return depth == 2 ? one : 2 * one;
+}
+
+cf_status cf_stage_forward_microbatch(const void *x, void *y, void *ws, size_t ws_bytes,
+                                      const cf_block_params *blocks, int depth, int N, int H, int W, int C, int E,
+                                      int k, int micro_batch, cf_dtype dt, cf_act act, void *stream) {
+    const char *what = "cf_stage_forward_microbatch";
+    if (depth <= 0 || !blocks)
+        return fail(CF_ERR_INVALID, "%s: depth must be positive and blocks non-NULL", what);
+    for (int i = 0; i < depth; i++) {
+        cf_status st = check_block(what, x, y, &blocks[i], N, H, W, C, E, k, dt, act);
+        if (st != CF_OK)
+            return st;
+    }
+    const int m = microbatch_size(N, H, W, C, micro_batch, dt);
+    const size_t need = cf_stage_microbatch_workspace_bytes(depth, N, H, W, C, micro_batch, dt);
+    const size_t bytes = (size_t)N * H * W * C * elem_bytes(dt);
+    if (need) {
+        if (!ws)
+            return fail(CF_ERR_INVALID, "%s: ws must be non-NULL for depth > 1", what);
+        if (!aligned16(ws))
+            return fail(CF_ERR_INVALID, "%s: ws must be 16-byte aligned", what);
+        if (ws_bytes < need)
+            return fail(CF_ERR_WORKSPACE, "%s: ws has %zu bytes, needs %zu", what, ws_bytes, need);
+        if (overlap(ws, need, x, bytes) || overlap(ws, need, y, bytes))
+            return fail(CF_ERR_INVALID, "%s: ws overlaps x or y", what);
+    }
+    // every micro-batch shape the loop launches must have a kernel
+    cf_status st = check_fit(what, to_shape(m, H, W, C, E, k, dt, act));
+    if (st != CF_OK)
+        return st;
+    if (N % m && (st = check_fit(what, to_shape(N % m, H, W, C, E, k, dt, act))) != CF_OK)
+        return st;
+    const size_t img = (size_t)H * W * C * elem_bytes(dt);
+    const size_t one = round256((size_t)m * img);
+    char *buf[2] = {(char *)ws, (char *)ws + one};
+    for (int n0 = 0; n0 < N; n0 += m) {
+        const int mb = N - n0 < m ? N - n0 : m;
+        cf::Shape s = to_shape(mb, H, W, C, E, k, dt, act);
+        s.cfg = tuned_config(s);
+        const void *in = (const char *)x + (size_t)n0 * img;
+        for (int i = 0; i < depth; i++) {
+            void *out = (i == depth - 1) ? (void *)((char *)y + (size_t)n0 * img) : (void *)buf[i & 1];
+            hipError_t e = cf::launch_fused_block(in, out, to_w(&blocks[i]), s, 1, nullptr, (hipStream_t)stream);
+            if (e != hipSuccess)
+                return hip_fail(e, what);
+            in = out;
+        }
+    }
+    g_err[0] = 0;
+    return CF_OK;
+}
+
 cf_status cf_downsample_forward(const void *x, void *y, const cf_down_params *p, int N, int H, int W, int Cin,
                                 int Cout, cf_dtype dt, void *stream) {
     const char *what = "cf_downsample_forward";

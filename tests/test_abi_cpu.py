@@ -357,3 +357,26 @@ def test_gblock_forward_rejects():
     assert call(k=5) == cf.CF_ERR_UNSUPPORTED
     assert call(H=1, W=6_000_000, y=0x400000000) == cf.CF_ERR_UNSUPPORTED  # 32-bit row offsets
     assert L.cf_last_error().decode().startswith("cf_gblock_forward")
+
+
+def test_microbatch_stage_workspace_and_rejects():
+    L = cf.lib()
+    # explicit micro-batch: two buffers of m images for depth > 2, one for depth 2, none for one block
+    img = 7 * 9 * 64 * 2
+    assert L.cf_stage_microbatch_workspace_bytes(3, 10, 7, 9, 64, 4, 0) == 2 * ((4 * img + 255) // 256 * 256)
+    assert L.cf_stage_microbatch_workspace_bytes(2, 10, 7, 9, 64, 4, 0) == (4 * img + 255) // 256 * 256
+    assert L.cf_stage_microbatch_workspace_bytes(1, 10, 7, 9, 64, 4, 0) == 0
+    # a micro-batch larger than the batch is the batch
+    assert L.cf_stage_microbatch_workspace_bytes(2, 3, 7, 9, 64, 50, 0) == (3 * img + 255) // 256 * 256
+    # default: one micro-batch's input and output within 128 MiB (56x56x64 fp16: 167 images,
+    # so the whole batch of 128; at 224x224x64, 10 images)
+    assert L.cf_stage_microbatch_workspace_bytes(2, 128, 56, 56, 64, 0, 0) == 128 * 56 * 56 * 64 * 2
+    assert L.cf_stage_microbatch_workspace_bytes(2, 128, 224, 224, 64, 0, 0) == 10 * 224 * 224 * 64 * 2
+    p = params()
+    arr = (cf._BlockParams * 3)(p, p, p)
+    args = (arr, 3, 10, 7, 9, 64, 4, 3, 4, 0, 0, None)
+    assert L.cf_stage_forward_microbatch(X, Y, WS, 16, *args) == cf.CF_ERR_WORKSPACE
+    assert L.cf_stage_forward_microbatch(X, Y, None, 0, *args) == cf.CF_ERR_INVALID
+    assert L.cf_stage_forward_microbatch(X, Y, X, 1 << 20, *args) == cf.CF_ERR_INVALID   # ws overlaps x
+    assert L.cf_stage_forward_microbatch(X, Y, WS, 1 << 30, arr, 0, 10, 7, 9, 64, 4, 3, 4, 0, 0,
+                                         None) == cf.CF_ERR_INVALID
