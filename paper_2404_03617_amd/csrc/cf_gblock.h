@@ -44,8 +44,10 @@
 //    no data movement.  s1, b1 and the activation are applied in fp32, the
 //    result rounded to the I/O dtype.
 //  * Project: C/16 products per chunk into fp32 accumulators; the epilogue
-//    adds s2, b2 and the block input x (re-read from global memory, an L2
-//    hit) and stores the output once.
+//    adds s2, b2 and the block input x -- read from the halo's centre pixels
+//    at the start of the block, before the conv outputs overwrite them, and
+//    kept in registers (a global re-read at the end would stall every block
+//    on a full memory latency) -- and stores the output once.
 //  * Halo prefetch.  With few channels (PREF2) a block's halo is loaded into
 //    registers a whole block ahead: when block r's D fragments are in
 //    registers, the halo of block r+1 (loaded during block r-1) goes into the
@@ -244,10 +246,9 @@ struct GB {
         h.WC = a.W * C;
         return h;
     }
-    static __device__ __forceinline__ u32x4 halo_piece(const HaloCtx &h, int i, uint32_t &dst) {
+    static __device__ __forceinline__ u32x4 halo_piece(const HaloCtx &h, int i) {
         const int px = i / C8, cq = i - px * C8;
         const int r = px / HC, cc = px - r * HC;
-        dst = (uint32_t)px * PB + (uint32_t)cq * 16;
         u32x4 v = {0u, 0u, 0u, 0u};
         if (r >= h.rlo && r < h.rhi && cc >= h.clo && cc < h.chi)
             v = *reinterpret_cast<const u32x4 *>(h.base + (r * h.WC + cc * C + 8 * cq));
@@ -255,23 +256,26 @@ struct GB {
     }
     // the lane's pieces (first + u) * 64 + lane, u < NP
     template <int NP>
-    static __device__ __forceinline__ void halo_load(const HaloCtx &h, int first, int lane, u32x4 (&v)[NP],
-                                                     uint32_t (&d)[NP]) {
+    static __device__ __forceinline__ void halo_load(const HaloCtx &h, int first, int lane, u32x4 (&v)[NP]) {
 #pragma unroll
         for (int u = 0; u < NP; u++) {
             const int i = (first + u) * 64 + lane;
-            d[u] = 0xffffffffu;
             v[u] = u32x4{0u, 0u, 0u, 0u};
             if (i < HPIECES)
-                v[u] = halo_piece(h, i, d[u]);
+                v[u] = halo_piece(h, i);
         }
     }
+    // piece i lands at pixel i / C8, channel piece i % C8 of the wave's region
     template <int NP>
-    static __device__ __forceinline__ void halo_store(uint8_t *reg, const u32x4 (&v)[NP], const uint32_t (&d)[NP]) {
+    static __device__ __forceinline__ void halo_store(uint8_t *reg, int first, int lane, const u32x4 (&v)[NP]) {
 #pragma unroll
-        for (int u = 0; u < NP; u++)
-            if (d[u] != 0xffffffffu)
-                sts16(reg, d[u], v[u]);
+        for (int u = 0; u < NP; u++) {
+            const int i = (first + u) * 64 + lane;
+            if (i < HPIECES) {
+                const int px = i / C8, cq = i - px * C8;
+                sts16(reg, (uint32_t)px * PB + (uint32_t)cq * 16, v[u]);
+            }
+        }
     }
 
     static __device__ __forceinline__ float act(float u) {
@@ -330,18 +334,16 @@ struct GB {
         }
         // halo of the first block; with PREF2 the second block's waits in registers
         u32x4 hv[PREF2 ? HPL : 1];
-        uint32_t hd[PREF2 ? HPL : 1];
         {
             const HaloCtx h0 = halo_ctx(a, decode(a, rstart * NW + wv));
             for (int s = 0; s < HSTEPS; s++) {
                 u32x4 v[HSTEP];
-                uint32_t d[HSTEP];
-                halo_load<HSTEP>(h0, s * HSTEP, lane, v, d);
-                halo_store<HSTEP>(reg, v, d);
+                halo_load<HSTEP>(h0, s * HSTEP, lane, v);
+                halo_store<HSTEP>(reg, s * HSTEP, lane, v);
             }
             if constexpr (PREF2) {
                 if (nr > 1)
-                    halo_load<HPL>(halo_ctx(a, decode(a, (rstart + 1) * NW + wv)), 0, lane, hv, hd);
+                    halo_load<HPL>(halo_ctx(a, decode(a, (rstart + 1) * NW + wv)), 0, lane, hv);
             }
         }
         __syncthreads();
@@ -357,6 +359,7 @@ struct GB {
         // block state
         u32x4 dfr[BR][KST];
         float4v acc[BR][MO];
+        u32x2 xres[BR][MO];  // the block input at the lane's output elements (residual)
         Blk kcur;
         int cur_r = 0;
 
@@ -364,6 +367,14 @@ struct GB {
         auto block_begin = [&](int r) {
             cur_r = r;
             kcur = decode(a, (rstart + r) * NW + wv);
+            // the residual comes from the halo (centre pixels), read before the
+            // conv outputs overwrite the region; no global re-read in the epilogue
+#pragma unroll
+            for (int nt = 0; nt < BR; nt++)
+#pragma unroll
+                for (int mo = 0; mo < MO; mo++)
+                    xres[nt][mo] = *reinterpret_cast<const u32x2 *>(
+                        reg + (uint32_t)((nt + 1) * HC + jl + 1) * PB + (uint32_t)(16 * mo + 4 * q) * 2);
 #pragma unroll
             for (int g = 0; g < NG; g++) {
                 const int c = GW * g + dch;
@@ -405,19 +416,18 @@ struct GB {
             if constexpr (PREF2) {
                 // the region is free: block r+1's halo in, block r+2's loads out
                 if (r + 1 < nr)
-                    halo_store<HPL>(reg, hv, hd);
+                    halo_store<HPL>(reg, 0, lane, hv);
                 if (r + 2 < nr)
-                    halo_load<HPL>(halo_ctx(a, decode(a, (rstart + r + 2) * NW + wv)), 0, lane, hv, hd);
+                    halo_load<HPL>(halo_ctx(a, decode(a, (rstart + r + 2) * NW + wv)), 0, lane, hv);
             }
         };
 
         // ---- one hidden chunk of the current block from weights at `cw`
         auto chunk = [&](int ch, const uint8_t *cw) {
             u32x4 sv[HSTEP];
-            uint32_t sd[HSTEP];
             const bool hstep = !PREF2 && cur_r + 1 < nr && ch < HSTEPS;
             if (hstep)
-                halo_load<HSTEP>(halo_ctx(a, decode(a, (rstart + cur_r + 1) * NW + wv)), ch * HSTEP, lane, sv, sd);
+                halo_load<HSTEP>(halo_ctx(a, decode(a, (rstart + cur_r + 1) * NW + wv)), ch * HSTEP, lane, sv);
             float s1v[8], b1v[8];
             {
                 const float4v s_lo = *reinterpret_cast<const float4v *>(cw + W1B + W2B + 32 * q);
@@ -479,7 +489,7 @@ struct GB {
                     acc[nt][mo] = T::mfma(a2, gfr[nt], acc[nt][mo]);
             }
             if (hstep)
-                halo_store<HSTEP>(reg, sv, sd);
+                halo_store<HSTEP>(reg, ch * HSTEP, lane, sv);
         };
 
         // ---- end of block: remaining halo steps, epilogue y = x + s2 acc + b2
@@ -489,9 +499,8 @@ struct GB {
                     const HaloCtx hn = halo_ctx(a, decode(a, (rstart + cur_r + 1) * NW + wv));
                     for (int s = a.nch; s < HSTEPS; s++) {
                         u32x4 v[HSTEP];
-                        uint32_t d[HSTEP];
-                        halo_load<HSTEP>(hn, s * HSTEP, lane, v, d);
-                        halo_store<HSTEP>(reg, v, d);
+                        halo_load<HSTEP>(hn, s * HSTEP, lane, v);
+                        halo_store<HSTEP>(reg, s * HSTEP, lane, v);
                     }
                 }
             }
@@ -506,7 +515,7 @@ struct GB {
 #pragma unroll
                 for (int mo = 0; mo < MO; mo++) {
                     const int c = 16 * mo + 4 * q;
-                    const u32x2 xv = *reinterpret_cast<const u32x2 *>(a.x + pix * C + c);
+                    const u32x2 xv = xres[nt][mo];
                     const float4v sc = *reinterpret_cast<const float4v *>(vec + 2 * C + c);
                     const float4v bi = *reinterpret_cast<const float4v *>(vec + 3 * C + c);
                     float o[4];
