@@ -60,6 +60,7 @@ def lib():
         L.cfref_grouped_conv.argtypes = [_dp, _dp] + [ci] * 9 + [_dp]
         L.cfref_gconv.argtypes = [_dp, _dp, _dp, _dp, ci, ci, ci, ci, ci, ci, _dp, ci]
         L.cfref_gblock_forward.argtypes = [_dp] * 10 + [ci] * 8 + [_dp, ci]
+        L.cfref_mbconv_forward.argtypes = [_dp] * 14 + [ci] * 8 + [_dp]
         L.cfref_default_threads.restype = ci
         _lib = L
     return _lib
@@ -196,6 +197,30 @@ def gblock_forward(x, p: dict, act: str = "relu", nthreads: int = 0):
                                     _p(vec[3]), _p(w2), _p(vec[4]), _p(vec[5]), N, H, W, C, EC // C,
                                     k, gw, ACTS[act], _p(y), nthreads)
     assert rc > 0
+    return y
+
+
+def mbconv_forward(x, p: dict):
+    """The paper's MBConv block with Squeeze & Excitation (Sec. 5.4, 5.4.1):
+    expand + SiLU, grouped k x k conv (group width gw) + SiLU, SE (average,
+    squeeze to R with ReLU, excite with sigmoid, gate), project, residual;
+    norms folded to scale and bias.  p holds w1 [E*C,C], gw_w [k,k,E*C,gw],
+    wr [R,E*C], we [E*C,R], w2 [C,E*C] and optional fp vectors s1,b1,s2,b2
+    [E*C], br [R], be [E*C], s3,b3 [C]."""
+    x = _f64(x)
+    N, H, W, C = x.shape
+    w1, a, wr, we, w2 = (_f64(p[k]) for k in ("w1", "gw_w", "wr", "we", "w2"))
+    EC = w1.shape[0]
+    k, _, _, gw = a.shape
+    R = wr.shape[0]
+    assert w1.shape == (EC, C) and a.shape == (k, k, EC, gw) and wr.shape == (R, EC)
+    assert we.shape == (EC, R) and w2.shape == (C, EC) and EC % C == 0
+    vec = [_f64(p.get(n)) for n in ("s1", "b1", "s2", "b2", "br", "be", "s3", "b3")]
+    y = np.empty_like(x)
+    rc = lib().cfref_mbconv_forward(_p(x), _p(w1), _p(vec[0]), _p(vec[1]), _p(a), _p(vec[2]), _p(vec[3]),
+                                    _p(wr), _p(vec[4]), _p(we), _p(vec[5]), _p(w2), _p(vec[6]), _p(vec[7]),
+                                    N, H, W, C, EC // C, R, k, gw, _p(y))
+    assert rc == 0
     return y
 
 

@@ -471,3 +471,109 @@ int cfref_gblock_forward(const double *x, const double *a, const double *s0, con
     J.scratch_doubles = (size_t)W * C * 2 + (size_t)W * E * C * 2;
     return run_rows(&J, nthreads);
 }
+
+/* ------------------------------------------------------------------------ */
+/* The MBConv block with Squeeze & Excitation in the paper's variant
+ * (Sec. 5.4 and the kernel description of Sec. 5.4.1): the depth-wise conv of
+ * MBConv replaced by a grouped conv of group width gw; batch norm after each
+ * conv folded into a per-channel scale and bias; SiLU after the expand and
+ * after the grouped conv; the SE layer squeezes the global average of each
+ * hidden channel to R values with ReLU and expands them back with a sigmoid,
+ * whose output gates the hidden channels; then the project and the residual.
+ * Hidden width EC = E * C.
+ *   U  = SiLU(s1 * (X W1^T) + b1)                          [N,H,W,EC]
+ *   V  = SiLU(s2 * gconv_k(U) + b2)                        [N,H,W,EC]
+ *   sq[n,c] = (1 / (H W)) sum_{h,w} V[n,h,w,c]
+ *   z[n,r]  = ReLU(sum_c Wr[r][c] sq[n,c] + br[r])         r < R
+ *   g[n,c]  = sigmoid(sum_r We[c][r] z[n,r] + be[c])
+ *   Y  = X + s3 * ((V * g) W2^T) + b3
+ * Layouts: w1 [EC][C], gwt [k][k][EC][gw], wr [R][EC], we [EC][R],
+ * w2 [C][EC].  Serial over images (each image's SE couples all its pixels);
+ * for the small late-stage shapes the block is used at. */
+static double silu(double u) { return u / (1.0 + exp(-u)); }
+static double sigmoid(double u) { return 1.0 / (1.0 + exp(-u)); }
+
+int cfref_mbconv_forward(const double *x, const double *w1, const double *s1, const double *b1,
+                         const double *gwt, const double *s2, const double *b2,
+                         const double *wr, const double *br, const double *we, const double *be,
+                         const double *w2, const double *s3, const double *b3,
+                         int N, int H, int W, int C, int E, int R, int k, int gw, double *y)
+{
+    const int EC = E * C;
+    if (gw <= 0 || EC % gw || R <= 0 || k % 2 == 0)
+        return -1;
+    const size_t P = (size_t)H * W;
+    double *U = (double *)malloc(sizeof(double) * P * EC);
+    double *V = (double *)malloc(sizeof(double) * P * EC);
+    double *sq = (double *)malloc(sizeof(double) * EC);
+    double *z = (double *)malloc(sizeof(double) * R);
+    double *g = (double *)malloc(sizeof(double) * EC);
+    if (!U || !V || !sq || !z || !g) {
+        free(U); free(V); free(sq); free(z); free(g);
+        return -2;
+    }
+    const int pad = k / 2;
+    for (int n = 0; n < N; n++) {
+        const double *xn = x + (size_t)n * P * C;
+        /* expand, folded norm, SiLU */
+        for (size_t p = 0; p < P; p++)
+            for (int r = 0; r < EC; r++) {
+                double acc = 0.0;
+                for (int c = 0; c < C; c++)
+                    acc += w1[(size_t)r * C + c] * xn[p * C + c];
+                U[p * EC + r] = silu((s1 ? s1[r] : 1.0) * acc + (b1 ? b1[r] : 0.0));
+            }
+        /* grouped conv over the hidden channels (eq. f:grouped-conv2d, K = C = EC,
+         * T = gw), zero padding, folded norm, SiLU */
+        for (int h = 0; h < H; h++)
+            for (int w = 0; w < W; w++)
+                for (int c = 0; c < EC; c++) {
+                    const int first = (c / gw) * gw;
+                    double acc = 0.0;
+                    for (int i = 0; i < k; i++) {
+                        const int hh = h + i - pad;
+                        if (hh < 0 || hh >= H)
+                            continue;
+                        for (int j = 0; j < k; j++) {
+                            const int ww = w + j - pad;
+                            if (ww < 0 || ww >= W)
+                                continue;
+                            for (int t = 0; t < gw; t++)
+                                acc += gwt[(((size_t)i * k + j) * EC + c) * gw + t] *
+                                       U[((size_t)hh * W + ww) * EC + first + t];
+                        }
+                    }
+                    V[((size_t)h * W + w) * EC + c] = silu((s2 ? s2[c] : 1.0) * acc + (b2 ? b2[c] : 0.0));
+                }
+        /* squeeze: global average, reduce to R with ReLU, expand with sigmoid */
+        for (int c = 0; c < EC; c++) {
+            double acc = 0.0;
+            for (size_t p = 0; p < P; p++)
+                acc += V[p * EC + c];
+            sq[c] = acc / (double)P;
+        }
+        for (int r = 0; r < R; r++) {
+            double acc = 0.0;
+            for (int c = 0; c < EC; c++)
+                acc += wr[(size_t)r * EC + c] * sq[c];
+            acc += br ? br[r] : 0.0;
+            z[r] = acc > 0.0 ? acc : 0.0;
+        }
+        for (int c = 0; c < EC; c++) {
+            double acc = 0.0;
+            for (int r = 0; r < R; r++)
+                acc += we[(size_t)c * R + r] * z[r];
+            g[c] = sigmoid(acc + (be ? be[c] : 0.0));
+        }
+        /* gate, project, folded norm, residual */
+        for (size_t p = 0; p < P; p++)
+            for (int o = 0; o < C; o++) {
+                double acc = 0.0;
+                for (int c = 0; c < EC; c++)
+                    acc += w2[(size_t)o * EC + c] * (V[p * EC + c] * g[c]);
+                y[((size_t)n * P + p) * C + o] = xn[p * C + o] + (s3 ? s3[o] : 1.0) * acc + (b3 ? b3[o] : 0.0);
+            }
+    }
+    free(U); free(V); free(sq); free(z); free(g);
+    return 0;
+}
