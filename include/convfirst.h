@@ -193,6 +193,59 @@ cf_status cf_gblock_forward(const void *x, void *y, const cf_gblock_params *p,
                             int N, int H, int W, int C, int E, int k,
                             cf_dtype dt, cf_act act, void *stream);
 
+/* The MBConv block with Squeeze & Excitation of Sec. 5.4 (Fig. f:mbconv:
+ * the paper's variant with a grouped 3 x 3 conv of group width 8 in place of
+ * the depth-wise one), fused into one kernel as Sec. 5.4.1 describes (Fig.
+ * f:mbconv-block-fusion-tensor-machine).  With EC = E*C hidden channels:
+ *   U[n,h,w,:] = SiLU(s1 * (w1 X[n,h,w,:]) + b1)                     expand
+ *   V[n,h,w,c] = SiLU(s2[c] * sum_{i,j<3} sum_{t<8} gw_w[i][j][c][t]
+ *                 * U[n, h+i-1, w+j-1, floor(c/8)*8 + t] + b2[c])     grouped conv
+ *   z[n] = ReLU(wr mean_{h,w} V[n,h,w,:] + br)                        squeeze
+ *   g[n] = sigmoid(we z[n] + be)                                       excitation
+ *   Y[n,h,w,:] = X[n,h,w,:] + s3 * (w2 (V[n,h,w,:] * g[n])) + b3       project, residual
+ * Tensors (row-major, I/O dtype unless noted):
+ *   x, y  [N][H][W][C]
+ *   w1    [EC][C]        expand (torch 1x1 conv weight [EC][C][1][1])
+ *   gw_w  [3][3][EC][8]  grouped taps: torch's weight [EC][8][3][3] permuted (2, 3, 0, 1)
+ *   wr    [R][EC]        squeeze;  we [EC][R] excitation;  w2 [C][EC] project
+ *   s1, b1, s2, b2, be  fp32 [EC];  br fp32 [R];  s3, b3 fp32 [C]
+ *   (NULL scale means 1, NULL bias 0; folded batch norms go into the s/b pairs)
+ * Each work item (an image and 64 of its hidden channels) computes its
+ * expand and conv layers alone; the squeeze sums over every hidden channel
+ * and the projection reads all of them, so the work items of an image
+ * exchange their conv outputs and squeeze shares through ws and meet once in
+ * global memory.  The kernel is therefore launched cooperatively, with each
+ * image's work items resident together.  The target is the late stages of a
+ * network: supported are k = 3, 1 <= H, W <= 16, C a multiple of 16, E*C a
+ * multiple of 64 and at most 4096, 1 <= R <= 256 (CF_ERR_UNSUPPORTED
+ * otherwise; C not a multiple of 8 is CF_ERR_INVALID).  y may equal x
+ * (evaluation in place); any other overlap among x, y and ws is
+ * CF_ERR_INVALID.  ws: cf_mbconv_workspace_bytes() bytes (queried on the
+ * current device) let every image the device can hold be in flight; a
+ * smaller ws runs fewer images at once, and one too small for a single image
+ * returns CF_ERR_WORKSPACE.  Once the call has completed on the stream, the
+ * first int of ws is nonzero if a barrier wait gave up (the output is then
+ * invalid; the cooperative launch rules this out).  fp16 or bf16 I/O, fp32
+ * accumulation; U, V and the gated project weights are rounded to the I/O
+ * dtype before their products.  Deterministic: every sum has a fixed order. */
+typedef struct {
+    const void *w1;
+    const float *s1, *b1;
+    const void *gw_w;
+    const float *s2, *b2;
+    const void *wr;
+    const float *br;
+    const void *we;
+    const float *be;
+    const void *w2;
+    const float *s3, *b3;
+} cf_mbconv_params;
+
+cf_status cf_mbconv_forward(const void *x, void *y, void *ws, size_t ws_bytes, const cf_mbconv_params *p,
+                            int N, int H, int W, int C, int E, int R, int k, cf_dtype dt, void *stream);
+/* 0 for shapes the kernel does not support. */
+size_t cf_mbconv_workspace_bytes(int N, int H, int W, int C, int E, int R, cf_dtype dt);
+
 /* Allocation-free variant of cf_block_forward_split, for callers that cannot
  * allocate device memory: code under stream capture, tight serving loops,
  * harnesses that forbid hipMalloc.  Same arguments and result as

@@ -26,7 +26,7 @@ __all__ = [
     "stage_forward_microbatch",
     "downsample_forward",
     "block_forward_unfused", "block_forward_split", "block_forward_split_noalloc", "gblock_forward",
-    "stack_forward", "capture_stack", "ConvFirstBlock",
+    "mbconv_forward", "mbconv_workspace_bytes", "stack_forward", "capture_stack", "ConvFirstBlock",
     "CFError", "EXPORTED_SYMBOLS", "dw_weight_from_conv2d", "grouped_weight_from_conv2d",
     "pw_weight_from_conv2d", "down_weight_from_conv2d", "fold_batchnorm", "block_params_from_modules",
     "grouped_block_params_from_modules", "down_params_from_modules",
@@ -43,7 +43,8 @@ EXPORTED_SYMBOLS = (
     "cf_block_forward", "cf_stage_forward", "cf_stage_workspace_bytes", "cf_stage_forward_microbatch",
     "cf_stage_microbatch_workspace_bytes", "cf_downsample_forward",
     "cf_block_forward_unfused", "cf_unfused_workspace_bytes", "cf_block_forward_split",
-    "cf_split_workspace_bytes", "cf_block_forward_split_noalloc", "cf_gblock_forward", "cf_block_autotune",
+    "cf_split_workspace_bytes", "cf_block_forward_split_noalloc", "cf_gblock_forward", "cf_mbconv_forward",
+    "cf_mbconv_workspace_bytes", "cf_block_autotune",
     "cf_block_tuned_config", "cf_last_error", "cf_status_string", "cf_abi_version",
 )
 
@@ -62,6 +63,11 @@ class _BlockParams(ctypes.Structure):
 class _GBlockParams(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
                 ("gw_w", "gw_scale", "gw_bias", "w1", "s1", "b1", "w2", "s2", "b2")]
+
+
+class _MBConvParams(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("w1", "s1", "b1", "gw_w", "s2", "b2", "wr", "br", "we", "be", "w2", "s3", "b3")]
 
 
 class _DownParams(ctypes.Structure):
@@ -86,6 +92,7 @@ def lib():
         i, sz, vp = ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p
         bp, dp = ctypes.POINTER(_BlockParams), ctypes.POINTER(_DownParams)
         gp = ctypes.POINTER(_GBlockParams)
+        mp = ctypes.POINTER(_MBConvParams)
         sig = {
             "cf_block_forward": (i, [vp, vp, bp, i, i, i, i, i, i, i, i, vp]),
             "cf_stage_forward": (i, [vp, vp, vp, sz, bp, i, i, i, i, i, i, i, i, i, vp]),
@@ -99,6 +106,8 @@ def lib():
             "cf_split_workspace_bytes": (sz, [i, i, i, i, i, i]),
             "cf_block_forward_split_noalloc": (i, [vp, vp, bp, i, i, i, i, i, i, i, i, i, vp]),
             "cf_gblock_forward": (i, [vp, vp, gp, i, i, i, i, i, i, i, i, vp]),
+            "cf_mbconv_forward": (i, [vp, vp, vp, sz, mp, i, i, i, i, i, i, i, i, vp]),
+            "cf_mbconv_workspace_bytes": (sz, [i, i, i, i, i, i, i]),
             "cf_block_autotune": (i, [vp, vp, bp, i, i, i, i, i, i, i, i, vp]),
             "cf_block_tuned_config": (i, [i, i, i, i, i, i, i, i]),
             "cf_last_error": (ctypes.c_char_p, []),
@@ -407,6 +416,71 @@ def gblock_forward(x: torch.Tensor, p: dict, act: str = "relu", out=None, stream
     y = _out(x, out)
     _check(lib().cf_gblock_forward(_ptr(x), _ptr(y), ctypes.byref(gp), N, H, W, C, EC // C, k,
                                    DTYPES[x.dtype], ACTS[act], _stream(stream)))
+    return y
+
+
+# MBConv parameters: shape as a function of (C, E*C, R), and whether the
+# tensor is a weight in x's dtype ("w") or an fp32 vector ("v").
+_MBCONV_SHAPES = {
+    "w1": (lambda C, EC, R: (EC, C), "w"),
+    "gw_w": (lambda C, EC, R: (3, 3, EC, GROUP_WIDTH), "w"),
+    "wr": (lambda C, EC, R: (R, EC), "w"),
+    "we": (lambda C, EC, R: (EC, R), "w"),
+    "w2": (lambda C, EC, R: (C, EC), "w"),
+    "s1": (lambda C, EC, R: (EC,), "v"), "b1": (lambda C, EC, R: (EC,), "v"),
+    "s2": (lambda C, EC, R: (EC,), "v"), "b2": (lambda C, EC, R: (EC,), "v"),
+    "br": (lambda C, EC, R: (R,), "v"), "be": (lambda C, EC, R: (EC,), "v"),
+    "s3": (lambda C, EC, R: (C,), "v"), "b3": (lambda C, EC, R: (C,), "v"),
+}
+
+
+def mbconv_workspace_bytes(N: int, H: int, W: int, C: int, E: int, R: int, dtype=torch.float16) -> int:
+    """Recommended workspace of mbconv_forward on the current device (0 for a
+    shape without a kernel)."""
+    return int(lib().cf_mbconv_workspace_bytes(N, H, W, C, E, R, DTYPES[dtype]))
+
+
+def mbconv_forward(x: torch.Tensor, p: dict, out=None, ws=None, stream=None) -> torch.Tensor:
+    """The paper's MBConv block with Squeeze & Excitation (Sec. 5.4) fused
+    into one cooperative kernel (Sec. 5.4.1).  p holds w1 [E*C,C], gw_w
+    [3,3,E*C,8], wr [R,E*C], we [E*C,R], w2 [C,E*C] in x's dtype and optional
+    fp32 s1,b1,s2,b2,be [E*C], br [R], s3,b3 [C].  out may be x itself
+    (evaluation in place).  ws: a uint8 workspace, by default one of
+    mbconv_workspace_bytes(); a smaller one runs fewer images at a time."""
+    N, H, W, C = _dims(x)
+    for key in ("w1", "gw_w", "wr", "we", "w2"):
+        if not isinstance(p.get(key), torch.Tensor):
+            raise ValueError("MBConv parameter %s is required" % key)
+    if p["w1"].dim() != 2 or p["wr"].dim() != 2:
+        raise ValueError("w1 must be [E*C, C] and wr [R, E*C]")
+    EC, R = int(p["w1"].shape[0]), int(p["wr"].shape[0])
+    if EC % C or EC == 0:
+        raise ValueError("w1 rows must be a positive multiple of C")
+    if p["gw_w"].dim() != 4 or p["gw_w"].shape[0] != p["gw_w"].shape[1]:
+        raise ValueError("gw_w must be [k, k, E*C, 8]")
+    k = int(p["gw_w"].shape[0])
+    unknown = set(p) - set(_MBCONV_SHAPES)
+    if unknown:
+        raise ValueError("unknown MBConv parameters: %s" % sorted(unknown))
+    vals, keep = {}, []
+    for key, (shape_of, kind) in _MBCONV_SHAPES.items():
+        t = p.get(key)
+        if t is not None:
+            shape = shape_of(C, EC, R)
+            if key == "gw_w":
+                shape = (k, k, EC, GROUP_WIDTH)
+            _check_tensor(key, t, shape, x.dtype if kind == "w" else torch.float32, x.device)
+            keep.append(t)
+        vals[key] = None if t is None else t.data_ptr()
+    mp = _MBConvParams(**vals)
+    _check_device(x)
+    y = _out(x, out)
+    if ws is None:
+        ws = _workspace(x, None, max(1, mbconv_workspace_bytes(N, H, W, C, EC // C, R, x.dtype)))
+    else:
+        _workspace(x, ws, 0)
+    _check(lib().cf_mbconv_forward(_ptr(x), _ptr(y), _ptr(ws), ws.numel(), ctypes.byref(mp), N, H, W, C, EC // C,
+                                   R, k, DTYPES[x.dtype], _stream(stream)))
     return y
 
 

@@ -100,6 +100,34 @@ bool gblock_supported_c(int C);
 // Fused grouped block; hipErrorInvalidValue for an unsupported C.
 hipError_t launch_gblock(const void *x, void *y, const GBlockW &w, const Shape &s, hipStream_t st);
 
+// The paper's MBConv block with Squeeze & Excitation (Sec. 5.4): expand w1
+// [EC][C], grouped conv gw [3][3][EC][8], squeeze wr [R][EC], excitation we
+// [EC][R], project w2 [C][EC]; fp32 scale/bias vectors, NULL meaning 1 / 0.
+struct MBConvW {
+    const void *w1;
+    const float *s1, *b1;
+    const void *gw;
+    const float *s2, *b2;
+    const void *wr;
+    const float *br;
+    const void *we;
+    const float *be;
+    const void *w2;
+    const float *s3, *b3;
+};
+// Shapes with a kernel: H, W <= 16, C % 16 == 0, E*C % 64 == 0, E*C <= 4096,
+// 1 <= R <= 256.
+bool mbconv_supported(int H, int W, int C, int E, int R);
+// Images the device can hold in flight at once (all their work items resident).
+hipError_t mbconv_resident_slots(int H, int W, int C, int E, int R, int bf16, int *slots);
+// Workspace bytes for `slots` images in flight.
+size_t mbconv_workspace_bytes(int N, int H, int W, int C, int E, int R, int slots);
+// Fused MBConv block; ws of ws_bytes >= mbconv_workspace_bytes(..., 1)
+// (hipErrorInvalidValue otherwise).  The first int of ws is nonzero after the
+// kernel if a barrier wait gave up.
+hipError_t launch_mbconv(const void *x, void *y, const MBConvW &w, int N, int H, int W, int C, int E, int R,
+                         int bf16, void *ws, size_t ws_bytes, hipStream_t st);
+
 // Upper bound of dynamic LDS the fused kernel needs for this shape (bytes);
 // 0 when no kernel configuration fits.
 size_t fused_lds_bytes(const Shape &s);

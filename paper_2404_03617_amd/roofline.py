@@ -48,6 +48,24 @@ def gblock_bytes_fused(N, H, W, C, E, k=3, gw=8, eb=2) -> int:
     return 2 * N * H * W * C * eb + eb * (k * k * gw * C + 2 * E * C * C) + 4 * (4 * C + 2 * E * C)
 
 
+def mbconv_flops(N, H, W, C, E, R, k=3, gw=8) -> int:
+    """MBConv + SE (Sec. 5.4): expand 2 P E C^2, grouped conv 2 P E C k^2 gw,
+    squeeze and excitation 4 E C R per image, project 2 P E C^2 -- the
+    columns Exp, Conv, Sqz Exc and Prj of the paper's projection tables."""
+    P = H * W
+    EC = E * C
+    return N * (2 * P * EC * C + 2 * P * EC * k * k * gw + 4 * EC * R + 2 * P * C * EC)
+
+
+def mbconv_bytes_fused(N, H, W, C, E, R, k=3, gw=8, eb=2) -> int:
+    """x read once, y written once, the five weight tensors and the fp32
+    vectors once."""
+    EC = E * C
+    weights = eb * (2 * EC * C + k * k * gw * EC + 2 * R * EC)
+    vectors = 4 * (5 * EC + R + 2 * C)
+    return 2 * N * H * W * C * eb + weights + vectors
+
+
 def block_weight_bytes(C, E, k, eb=2, vec_bytes=4) -> int:
     """dw taps, W1, W2 in the I/O dtype plus six fp32 scale/bias vectors."""
     return eb * (k * k * C + 2 * E * C * C) + vec_bytes * (2 * C + 2 * E * C + 2 * C)

@@ -97,6 +97,31 @@ def gblock_params(seed: int, layer: int, C: int, E: int, k: int = 3, dtype: str 
     return p
 
 
+def mbconv_params(seed: int, layer: int, C: int, E: int, R: int, dtype: str = "f16",
+                  scales: str = "ones", bias_std: float | None = 0.1, gw: int = 8) -> dict:
+    """Weights of one MBConv block with Squeeze & Excitation (expand, grouped
+    3x3 conv of group width gw, squeeze to R, excitation, project); tensor ids
+    100*(layer+1) + 0..12.  Weights ~ N(0, 1/fan_in): C (expand), 9*gw
+    (grouped conv), E*C (squeeze, project), R (excitation)."""
+    base = 100 * (layer + 1)
+    EC = E * C
+    return {
+        "w1": to_io(draw(seed, base + 0, (EC, C), (1.0 / C) ** 0.5), dtype),
+        "s1": _vec(seed, base + 1, EC, "scale", bias_std, scales),
+        "b1": _vec(seed, base + 2, EC, "bias", bias_std, scales),
+        "gw_w": to_io(draw(seed, base + 3, (3, 3, EC, gw), (1.0 / (9 * gw)) ** 0.5), dtype),
+        "s2": _vec(seed, base + 4, EC, "scale", bias_std, scales),
+        "b2": _vec(seed, base + 5, EC, "bias", bias_std, scales),
+        "wr": to_io(draw(seed, base + 6, (R, EC), (1.0 / EC) ** 0.5), dtype),
+        "br": _vec(seed, base + 7, R, "bias", bias_std, scales),
+        "we": to_io(draw(seed, base + 8, (EC, R), (1.0 / R) ** 0.5), dtype),
+        "be": _vec(seed, base + 9, EC, "bias", bias_std, scales),
+        "w2": to_io(draw(seed, base + 10, (C, EC), (1.0 / EC) ** 0.5), dtype),
+        "s3": _vec(seed, base + 11, C, "scale", bias_std, scales),
+        "b3": _vec(seed, base + 12, C, "bias", bias_std, scales),
+    }
+
+
 def down_params(seed: int, layer: int, Cin: int, Cout: int, dtype: str = "f16",
                 scales: str = "ones", bias_std: float | None = 0.1) -> dict:
     """Weights of one 2x2 stride-2 down-sampling layer; ids 100*(layer+1) + 0..2."""

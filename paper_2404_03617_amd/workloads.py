@@ -39,3 +39,18 @@ GBLOCK_WORKLOADS = {
         (16, 3, 128, 35.1, 0.42), (32, 3, 128, 46.6, 0.99), (32, 6, 64, 66.9, 0.30), (48, 6, 64, 71.6, 0.59),
         (64, 6, 64, 76.2, 0.96), (48, 6, 32, 67.0, 0.16), (64, 6, 32, 74.0, 0.25), (96, 6, 32, 68.7, 0.58)])
 }
+
+# The MBConv + Squeeze & Excitation kernel benchmark (Sec. 5.4.1, Table
+# t:mbconv-speed): channels 128..256, expansion 4, SE ratio 0.25 of the input
+# channels (R = C/4), height = width 16 or 8, batch 128, fp16.  paper_pct is
+# the block-fusion kernel's fraction of an A5000's peak in that table (context
+# only: other hardware).
+MBCONV_WORKLOADS = {
+    "mbconv_n128_%dx%d_c%d_e4_r%d_f16" % (hw, hw, c, c // 4): dict(kind="mbconv", N=128, H=hw, W=hw, C=c, E=4,
+                                                                 R=c // 4, k=3, dtype="f16", seed=40 + i,
+                                                                 paper_pct=pct, paper_ms=ms)
+    for i, (c, hw, pct, ms) in enumerate([
+        (128, 16, 46.2, 2.48), (144, 16, 44.4, 3.19), (160, 16, 41.9, 4.09), (192, 16, 44.4, 5.39),
+        (256, 16, 51.0, 8.01), (128, 8, 45.0, 0.64), (144, 8, 32.5, 1.09), (160, 8, 31.3, 1.37),
+        (192, 8, 43.1, 1.39), (256, 8, 51.4, 1.99)])
+}

@@ -380,3 +380,48 @@ def test_microbatch_stage_workspace_and_rejects():
     assert L.cf_stage_forward_microbatch(X, Y, X, 1 << 20, *args) == cf.CF_ERR_INVALID   # ws overlaps x
     assert L.cf_stage_forward_microbatch(X, Y, WS, 1 << 30, arr, 0, 10, 7, 9, 64, 4, 3, 4, 0, 0,
                                          None) == cf.CF_ERR_INVALID
+
+
+def test_mbconv_forward_rejects():
+    """The MBConv + SE entry point: every check happens on the host, and the
+    workspace size is a function of the shape (one image in flight without a
+    device to ask)."""
+    L = cf.lib()
+    GW, WR, WE = 0x43000000, 0x44000000, 0x45000000
+
+    def need(N, H, W, C, E, R):
+        G = E * C // 64
+        return 256 + (N * 4 + 255) // 256 * 256 + (N * G * R * 4 + 255) // 256 * 256 + 2 * H * W * E * C * 2
+
+    def call(x=X, y=Y, ws=WS, ws_bytes=1 << 30, N=2, H=8, W=8, C=64, E=4, R=16, k=3, dt=0, **kw):
+        p = cf._MBConvParams(w1=W1, s1=None, b1=None, gw_w=GW, s2=None, b2=None, wr=WR, br=None, we=WE, be=None,
+                             w2=W2, s3=None, b3=None)
+        for f, v in kw.items():
+            setattr(p, f, v)
+        return L.cf_mbconv_forward(x, y, ws, ws_bytes, ctypes.byref(p), N, H, W, C, E, R, k, dt, None)
+
+    assert L.cf_mbconv_workspace_bytes(2, 8, 8, 64, 4, 16, 0) >= need(2, 8, 8, 64, 4, 16)
+    assert L.cf_mbconv_workspace_bytes(2, 17, 8, 64, 4, 16, 0) == 0     # H > 16
+    assert L.cf_mbconv_workspace_bytes(2, 8, 8, 48, 1, 16, 0) == 0      # E*C not a multiple of 64
+    assert L.cf_mbconv_workspace_bytes(2, 8, 8, 64, 4, 300, 0) == 0     # R > 256
+    assert call(x=None) == cf.CF_ERR_INVALID
+    assert call(gw_w=None) == cf.CF_ERR_INVALID
+    assert call(we=None) == cf.CF_ERR_INVALID
+    assert call(R=0) == cf.CF_ERR_INVALID
+    assert call(C=20) == cf.CF_ERR_INVALID           # not a multiple of the group width
+    assert call(k=4) == cf.CF_ERR_INVALID
+    assert call(dt=5) == cf.CF_ERR_INVALID
+    assert call(y=X + 32) == cf.CF_ERR_INVALID       # overlaps x without being x
+    assert call(b3=W1 + 4) == cf.CF_ERR_INVALID      # misaligned
+    assert call(ws=X) == cf.CF_ERR_INVALID           # ws overlaps x
+    assert call(k=5) == cf.CF_ERR_UNSUPPORTED
+    assert call(H=17) == cf.CF_ERR_UNSUPPORTED
+    assert call(W=32) == cf.CF_ERR_UNSUPPORTED
+    assert call(C=40, E=8) == cf.CF_ERR_UNSUPPORTED  # C not a multiple of 16
+    assert call(C=48, E=1) == cf.CF_ERR_UNSUPPORTED  # E*C not a multiple of 64
+    assert call(R=257) == cf.CF_ERR_UNSUPPORTED
+    assert call(C=512, E=16) == cf.CF_ERR_UNSUPPORTED   # E*C > 4096
+    n = need(2, 8, 8, 64, 4, 16)
+    assert call(ws_bytes=n - 1) == cf.CF_ERR_WORKSPACE
+    assert call(ws=None, ws_bytes=0) == cf.CF_ERR_WORKSPACE
+    assert L.cf_last_error().decode().startswith("cf_mbconv_forward")
