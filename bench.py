@@ -32,7 +32,7 @@ import torch
 import paper_2404_03617_amd as cf
 from paper_2404_03617_amd import roofline as rl
 from paper_2404_03617_amd import synth
-from paper_2404_03617_amd.workloads import BENCH_WORKLOAD, GBLOCK_WORKLOADS, WORKLOADS
+from paper_2404_03617_amd.workloads import BENCH_WORKLOAD, GBLOCK_WORKLOADS, MBCONV_WORKLOADS, WORKLOADS
 
 MALL_BYTES = 256 << 20
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -206,6 +206,30 @@ def gblock_case(name: str, steps: int, warmup: int):
             "paper_A5000_comp_eff": round(w["paper_pct"] / 100, 3), "paper_A5000_ms": w["paper_ms"]}
 
 
+def mbconv_case(name: str, steps: int, warmup: int):
+    """The MBConv block with Squeeze & Excitation (Sec. 5.4.1) at one of the
+    shapes of the paper's MBConv table, batch 128: one cooperative launch
+    (plus the counter-clearing kernel) per step."""
+    w = MBCONV_WORKLOADS[name]
+    N, H, W, C, E, R = w["N"], w["H"], w["W"], w["C"], w["E"], w["R"]
+    nsets = _sets_needed(2 * N * H * W * C * 2)
+    xs = [synth.activations(w["seed"] + 100 * i, N, H, W, C, w["dtype"]).cuda() for i in range(nsets)]
+    ys = [torch.empty_like(xs[0]) for _ in range(nsets)]
+    p = {kk: (None if v is None else v.cuda()) for kk, v in
+         synth.mbconv_params(w["seed"], 0, C, E, R, w["dtype"]).items()}
+    ws = torch.empty(cf.mbconv_workspace_bytes(N, H, W, C, E, R), dtype=torch.uint8, device="cuda")
+    t = _time(lambda i: cf.mbconv_forward(xs[i % nsets], p, out=ys[i % nsets], ws=ws), steps, warmup,
+              torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    if int(ws[:4].view(torch.int32).item()) != 0:
+        raise RuntimeError("%s: a barrier wait of the MBConv kernel gave up" % name)
+    flops = rl.mbconv_flops(N, H, W, C, E, R)
+    nbytes = rl.mbconv_bytes_fused(N, H, W, C, E, R)
+    return {"ms": round(t * 1e3, 4), "images_per_s": round(N / t, 1), "tflops": round(flops / t / 1e12, 1),
+            "comp_eff": round(rl.comp_eff(flops, t), 4), "roofline": roofline_entry(flops, nbytes, t),
+            "paper_A5000_comp_eff": round(w["paper_pct"] / 100, 3)}
+
+
 def stack_waterline(name: str, steps: int, warmup: int):
     """Per-launch waterline of the four-stage stack (Sec. 4, eqs.
     e:total-attainable-latency and e:max-comp-eff): for every launch its
@@ -373,6 +397,16 @@ def cpu_other_workloads(min_seconds: float = 1.0):
             e[label] = {"images_per_s": round(passes * w["N"] / dt, 2), "ms_per_pass": round(dt / passes * 1e3, 3),
                         "threads": int(used), "passes": passes}
         out[name] = e
+    # the MBConv + SE oracle on a sample of images of the first MBConv shape
+    # (its images are independent: the rate scales to the batch)
+    nm = next(iter(MBCONV_WORKLOADS))
+    w = MBCONV_WORKLOADS[nm]
+    x = synth.to_f64(synth.activations(w["seed"], 2, w["H"], w["W"], w["C"], w["dtype"]))
+    p = synth.params_f64(synth.mbconv_params(w["seed"], 0, w["C"], w["E"], w["R"], w["dtype"]))
+    t0 = time.perf_counter()
+    oracle.mbconv_forward(x, p)
+    dt = time.perf_counter() - t0
+    out[nm] = {"images_per_s": round(2 / dt, 3), "seconds": round(dt, 2), "sample": "2 images", "threads": 1}
     return out
 
 
@@ -405,20 +439,22 @@ def main():
             calib_copy()
         print(json.dumps({"stage_microbatch": r, "micro_batch": args.stage_mb}), flush=True)
         return
-    if name in GBLOCK_WORKLOADS:
+    if name in GBLOCK_WORKLOADS or name in MBCONV_WORKLOADS:
         # one of the paper's own block shapes as the timed workload (used for
         # profiles of that kernel); the default is the benchmark workload
-        g = gblock_case(name, args.steps, args.warmup)
-        wg = GBLOCK_WORKLOADS[name]
+        mb = name in MBCONV_WORKLOADS
+        g = mbconv_case(name, args.steps, args.warmup) if mb else gblock_case(name, args.steps, args.warmup)
+        wg = MBCONV_WORKLOADS[name] if mb else GBLOCK_WORKLOADS[name]
+        cfg = ({"workload": name, "N": wg["N"], "H": wg["H"], "W": wg["W"], "C": wg["C"], "E": wg["E"],
+                "R": wg["R"], "k": wg["k"], "kernel": "fused MBConv + SE block (1 cooperative launch)"} if mb else
+               {"workload": name, "N": wg["N"], "H": wg["H"], "W": wg["W"], "C": wg["C"], "E": wg["E"],
+                "k": wg["k"], "act": wg["act"], "kernel": "fused grouped-conv block (1 launch)"})
         print(json.dumps({"metric": "images/sec and % of fp16 MFMA peak (computational efficiency), batch 128",
                           "value": g["images_per_s"], "unit": "images/s", "n_gpus": 1, "steps": args.steps,
                           "warmup": args.warmup, "ms_per_step": g["ms"], "higher_is_better": True,
                           "scaling": "weak", "vs_baseline": None, "dtype": "f16",
                           "data": "synthetic (seeded N(0,1) activations, N(0,1/fan_in) weights)",
-                          "config": {"workload": name, "N": wg["N"], "H": wg["H"], "W": wg["W"], "C": wg["C"],
-                                     "E": wg["E"], "k": wg["k"], "act": wg["act"],
-                                     "kernel": "fused grouped-conv block (1 launch)"},
-                          "comp_eff": g["comp_eff"], "roofline": g["roofline"]}), flush=True)
+                          "config": cfg, "comp_eff": g["comp_eff"], "roofline": g["roofline"]}), flush=True)
         return
     w = WORKLOADS[name]
     res = block_case(name, args.steps, args.warmup)
@@ -511,6 +547,8 @@ def main():
         extra["stage_microbatch"] = stage_microbatch_case([0, 64, 32, 16], max(5, args.steps // 2), 2)
         # the paper's own block at the shapes of its kernel benchmark table
         extra["paper_block_table"] = {nm: gblock_case(nm, max(5, args.steps // 2), 3) for nm in GBLOCK_WORKLOADS}
+        # the MBConv + SE block at the shapes of the paper's MBConv table
+        extra["paper_mbconv_table"] = {nm: mbconv_case(nm, max(5, args.steps // 2), 3) for nm in MBCONV_WORKLOADS}
         out["other_workloads"] = extra
     if args.calib_copy:
         calib_copy()

@@ -217,8 +217,11 @@ cf_status cf_gblock_forward(const void *x, void *y, const cf_gblock_params *p,
  * global memory.  The kernel is therefore launched cooperatively, with each
  * image's work items resident together.  The target is the late stages of a
  * network: supported are k = 3, 1 <= H, W <= 16, C a multiple of 16, E*C a
- * multiple of 64 and at most 4096, 1 <= R <= 256 (CF_ERR_UNSUPPORTED
- * otherwise; C not a multiple of 8 is CF_ERR_INVALID).  y may equal x
+ * multiple of 64 and at most 4096, 1 <= R <= 256, and a shared-memory layout
+ * (the group's W1 rows, the gates of all E*C channels, the staged hidden
+ * layer) within the 160 KB of a CU: C up to 768 at E = 2, 512 at E = 4, 256
+ * at E = 8 (CF_ERR_UNSUPPORTED otherwise; C not a multiple of 8 is
+ * CF_ERR_INVALID).  y may equal x
  * (evaluation in place); any other overlap among x, y and ws is
  * CF_ERR_INVALID.  ws: cf_mbconv_workspace_bytes() bytes (queried on the
  * current device) let every image the device can hold be in flight; a

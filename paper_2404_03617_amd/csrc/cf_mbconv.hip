@@ -9,10 +9,10 @@
 // As in the paper, a work item is one image and one group of 64 hidden
 // channels, and the expand and conv layers of that group run on one
 // processor without other work items:
-//  1. expand: the group's 64 rows of W1 against every pixel of the image
-//     (v_mfma_f32_16x16x32, x read straight from global memory as B
-//     fragments, one K step prefetched), SiLU in fp32, rounded into an LDS
-//     buffer with a zero border;
+//  1. expand: the group's 64 rows of W1 (in LDS for the whole launch)
+//     against every pixel of the image (v_mfma_f32_16x16x32, x read straight
+//     from global memory as B fragments in batches of four K steps), SiLU in
+//     fp32, rounded into an LDS buffer with a zero border;
 //  2. grouped conv of the 64 channels (8 groups of 8, self-contained) as one
 //     product per tap column: 16 columns x 2 output rows against K = 4 halo
 //     rows x 8 channels; SiLU; V goes to the image's exchange buffer in
@@ -24,11 +24,14 @@
 //     and its squeeze share;
 //  5. the squeeze (shares added in group order), ReLU, and the excitation
 //     and sigmoid for all E*C hidden channels;
-//  6. the projection: the image's output is cut into tiles of 16 pixels x 16
-//     channels, dealt round-robin to the image's work items; each tile is a
-//     product over all E*C hidden channels of W2 (gate folded into its
-//     fragments) and the exchanged V, then s3, b3 and the residual, and y is
-//     written once.
+//  6. the projection: the image's output is cut into units of 16 pixels and
+//     a range of 16-channel tiles, dealt round-robin to the image's work
+//     items; a unit's 16 pixels of V, times the gates, are read once into LDS
+//     and every tile of the unit is a product over all E*C hidden channels of
+//     W2 rows (batches of eight K steps, the next batch in flight) and the
+//     staged V; then s3, b3 and the residual, and y is written once.  The
+//     conv taps stay in registers and the scale/bias vectors in LDS for the
+//     whole launch.
 // Where the paper adds the groups' projections into y with atomics, the
 // work items here exchange the (4x smaller) gated-layer input instead; the
 // result is deterministic and needs one synchronisation per image.  The
@@ -51,7 +54,9 @@
 // the later waits of the launch are skipped, and the kernel always ends.
 //
 // Images up to 16 x 16 (the late-stage shapes the paper targets); C a
-// multiple of 16; E*C a multiple of 64 and at most 4096; 1 <= R <= 256.
+// multiple of 16; E*C a multiple of 64 and at most 4096; 1 <= R <= 256; the
+// LDS layout within 160 KB (it grows with C and E*C: C up to 768 at E = 2,
+// 512 at E = 4, 256 at E = 8).
 #include "cf_device.h"
 #include "cf_kernels.h"
 
@@ -86,7 +91,7 @@ struct Args {
     int N, H, W, C, EC, R, G;
     int slots;
     int xcd_map;                   // 1: the workgroups of a slot share an XCD
-    uint32_t off_gate, off_z, off_cs;  // LDS layout (U at 0)
+    uint32_t off_gate, off_z, off_cs, off_vec, off_w1;  // LDS layout (U at 0)
 };
 
 __device__ __forceinline__ u32x4 ld16(const void *p) { return *reinterpret_cast<const u32x4 *>(p); }
@@ -131,6 +136,9 @@ __device__ __forceinline__ void image_barrier(int *cnt, int target, int *flag) {
 template <typename T, int NWV, int NPW>
 struct MB {
     static constexpr int NT = NWV * 64;
+    static constexpr int NGG = 8 / NWV;  // 8-channel conv groups per wave
+    static constexpr int KE = NPW == 4 ? 2 : 4;  // expand K steps per load batch
+    static constexpr int KB = NPW == 2 ? 8 : 4;  // output K steps per load batch (two batches in flight)
 
     static __device__ void run(const Args &a, uint8_t *smem) {
         const int tid = threadIdx.x, lane = tid & 63;
@@ -149,16 +157,57 @@ struct MB {
         float *gate = reinterpret_cast<float *>(smem + a.off_gate);  // [EC]
         float *zl = reinterpret_cast<float *>(smem + a.off_z);       // [R]
         float *csum = reinterpret_cast<float *>(smem + a.off_cs);    // [64]
+        float *vec = reinterpret_cast<float *>(smem + a.off_vec);    // s1, b1, s2, b2 [64] each; s3, b3 [C]
+        float *s1l = vec, *b1l = vec + 64, *s2l = vec + 128, *b2l = vec + 192, *s3l = vec + 256, *b3l = s3l + C;
 
-        // the U border (row 0, rows past H, column 0, columns past W) stays zero
-        for (uint32_t i = tid; i < a.off_gate / 16; i += NT)
-            reinterpret_cast<u32x4 *>(smem)[i] = u32x4{0u, 0u, 0u, 0u};
+        // once per workgroup: the scale/bias vectors the group uses
+        for (int i = tid; i < 64; i += NT) {
+            s1l[i] = a.s1 ? a.s1[h0 + i] : 1.0f;
+            b1l[i] = a.b1 ? a.b1[h0 + i] : 0.0f;
+            s2l[i] = a.s2 ? a.s2[h0 + i] : 1.0f;
+            b2l[i] = a.b2 ? a.b2[h0 + i] : 0.0f;
+        }
+        for (int i = tid; i < C; i += NT) {
+            s3l[i] = a.s3 ? a.s3[i] : 1.0f;
+            b3l[i] = a.b3 ? a.b3[i] : 0.0f;
+        }
+        // the group's 64 rows of W1 (pitch 2C + 16 bytes: an odd multiple of
+        // 16, conflict-free fragment reads)
+        const uint32_t w1p = 2 * C + 16;
+        uint8_t *w1l = smem + a.off_w1;
+        for (int i = tid; i < 64 * (C / 8); i += NT) {
+            const int row = i / (C / 8), c8 = i - row * (C / 8);
+            *reinterpret_cast<u32x4 *>(w1l + (uint32_t)row * w1p + (uint32_t)c8 * 16) =
+                ld16(a.w1 + (size_t)(h0 + row) * C + 8 * c8);
+        }
+        // the conv taps of this wave's 8-channel groups stay in registers
+        const int cs = jl >> 3, co = jl & 7;
+        const int ti = q - cs;  // the tap row this lane's K slice meets
+        const bool tap_ok = ti >= 0 && ti <= 2;
+        u32x4 cav[NGG][3];
+#pragma unroll
+        for (int j = 0; j < NGG; j++)
+#pragma unroll
+            for (int dj = 0; dj < 3; dj++)
+                cav[j][dj] = tap_ok ? ld16(a.gw + ((size_t)(ti * 3 + dj) * EC + h0 + 8 * (wv + NWV * j) + co) * 8)
+                                    : u32x4{0u, 0u, 0u, 0u};
         __syncthreads();
 
         int it = 0;
         for (int n = slot; n < a.N; n += a.slots, it++) {
             const uint16_t *xn = a.x + (size_t)n * P * C;
             uint16_t *vx = a.vx + ((size_t)(it & 1) * a.slots + slot) * P * EC;
+
+            // the U border (row 0, rows past H, column 0, columns past W) is
+            // zero; the output staging of the previous image overwrote it
+            {
+                const int urows = 2 * RP + 2;
+                for (int i = tid; i < urows * UC * (PB / 16); i += NT) {
+                    const int cell = i / (PB / 16), row = cell / UC, col = cell - row * UC;
+                    if (row == 0 || row > a.H || col == 0 || col > a.W)
+                        *reinterpret_cast<u32x4 *>(U + (uint32_t)i * 16) = u32x4{0u, 0u, 0u, 0u};
+                }
+            }
 
             // ---- 1. expand + SiLU into U; wave wv takes the 16-pixel tiles wv + NWV i
             {
@@ -169,46 +218,40 @@ struct MB {
                     for (int i = 0; i < NPW; i++)
                         acc[mt][i] = float4v{0.f, 0.f, 0.f, 0.f};
                 const int ks = (C + 31) / 32;
-                auto load = [&](int kk, u32x4 *av, u32x4 *bv) {
-                    const int k0 = 32 * kk + 8 * q;
-                    const bool kin = k0 < C;  // C % 32 == 16: the last step is half padding
+                for (int k0 = 0; k0 < ks; k0 += KE) {
+                    u32x4 bv[KE][NPW];
 #pragma unroll
-                    for (int mt = 0; mt < 4; mt++)
-                        av[mt] = kin ? ld16(a.w1 + (size_t)(h0 + 16 * mt + jl) * C + k0) : u32x4{0u, 0u, 0u, 0u};
+                    for (int j = 0; j < KE; j++) {
+                        const int k = 32 * (k0 + j) + 8 * q;
+                        const bool kin = k < C;  // past ks, or the half-padded last step of C % 32 == 16
 #pragma unroll
-                    for (int i = 0; i < NPW; i++) {
-                        const int p = 16 * (wv + NWV * i) + jl;
-                        bv[i] = kin && p < P ? ld16(xn + (size_t)p * C + k0) : u32x4{0u, 0u, 0u, 0u};
+                        for (int i = 0; i < NPW; i++) {
+                            const int p = 16 * (wv + NWV * i) + jl;
+                            bv[j][i] = kin && p < P ? ld16(xn + (size_t)p * C + k) : u32x4{0u, 0u, 0u, 0u};
+                        }
                     }
-                };
-                auto mma = [&](const u32x4 *av, const u32x4 *bv) {
 #pragma unroll
-                    for (int mt = 0; mt < 4; mt++)
+                    for (int j = 0; j < KE; j++) {
+                        if (k0 + j >= ks)  // wave-uniform
+                            break;
+                        const int k = 32 * (k0 + j) + 8 * q;
 #pragma unroll
-                        for (int i = 0; i < NPW; i++)
-                            acc[mt][i] = T::mfma(av[mt], bv[i], acc[mt][i]);
-                };
-                u32x4 a0[4], b0[NPW], a1[4], b1[NPW];
-                load(0, a0, b0);
-                for (int kk = 0; kk < ks; kk += 2) {
-                    if (kk + 1 < ks)
-                        load(kk + 1, a1, b1);
-                    mma(a0, b0);
-                    if (kk + 1 < ks) {
-                        if (kk + 2 < ks)
-                            load(kk + 2, a0, b0);
-                        mma(a1, b1);
+                        for (int mt = 0; mt < 4; mt++) {
+                            // A rows of W1; a K slice past C multiplies zero x
+                            const u32x4 av = k < C ? *reinterpret_cast<const u32x4 *>(
+                                                         w1l + (uint32_t)(16 * mt + jl) * w1p + (uint32_t)k * 2)
+                                                   : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+                            for (int i = 0; i < NPW; i++)
+                                acc[mt][i] = T::mfma(av, bv[j][i], acc[mt][i]);
+                        }
                     }
                 }
 #pragma unroll
                 for (int mt = 0; mt < 4; mt++) {
                     const int hl = 16 * mt + 4 * q;  // local hidden channels hl .. hl+3 of this lane
-                    float sc[4], bi[4];
-#pragma unroll
-                    for (int e = 0; e < 4; e++) {
-                        sc[e] = a.s1 ? a.s1[h0 + hl + e] : 1.0f;
-                        bi[e] = a.b1 ? a.b1[h0 + hl + e] : 0.0f;
-                    }
+                    const float4v sc = *reinterpret_cast<const float4v *>(s1l + hl);
+                    const float4v bi = *reinterpret_cast<const float4v *>(b1l + hl);
 #pragma unroll
                     for (int i = 0; i < NPW; i++) {
                         const int p = 16 * (wv + NWV * i) + jl;
@@ -229,57 +272,46 @@ struct MB {
             // ---- 2. grouped conv + SiLU -> exchange buffer, channel sums.  A rows
             //      (s, o): output row 2rp+s, channel o of the 8-group; K (t, j):
             //      halo row 2rp+t, input channel j
-            {
-                const int cs = jl >> 3, co = jl & 7;
-                const int ti = q - cs;  // the tap row this lane's K slice meets
-                const bool tap_ok = ti >= 0 && ti <= 2;
-                for (int gg = wv; gg < 8; gg += NWV) {
-                    u32x4 av[3];
 #pragma unroll
-                    for (int dj = 0; dj < 3; dj++)
-                        av[dj] = tap_ok ? ld16(a.gw + ((size_t)(ti * 3 + dj) * EC + h0 + 8 * gg + co) * 8)
-                                        : u32x4{0u, 0u, 0u, 0u};
-                    const int hl = 8 * gg + 4 * (q & 1);  // output channels of this lane's D rows
-                    float sc[4], bi[4], sum[4] = {0.f, 0.f, 0.f, 0.f};
+            for (int j = 0; j < NGG; j++) {
+                const int gg = wv + NWV * j;
+                const int hl = 8 * gg + 4 * (q & 1);  // output channels of this lane's D rows
+                const float4v sc = *reinterpret_cast<const float4v *>(s2l + hl);
+                const float4v bi = *reinterpret_cast<const float4v *>(b2l + hl);
+                float sum[4] = {0.f, 0.f, 0.f, 0.f};
+                for (int rp = 0; rp < RP; rp++) {
+                    float4v acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                    for (int e = 0; e < 4; e++) {
-                        sc[e] = a.s2 ? a.s2[h0 + hl + e] : 1.0f;
-                        bi[e] = a.b2 ? a.b2[h0 + hl + e] : 0.0f;
+                    for (int dj = 0; dj < 3; dj++) {
+                        const u32x4 bv = *reinterpret_cast<const u32x4 *>(
+                            U + (uint32_t)((2 * rp + q) * UC + jl + dj) * PB + (uint32_t)gg * 16);
+                        acc = T::mfma(cav[j][dj], bv, acc);
                     }
-                    for (int rp = 0; rp < RP; rp++) {
-                        float4v acc = {0.f, 0.f, 0.f, 0.f};
+                    const int r = 2 * rp + (q >> 1), c = jl;
+                    if (r < a.H && c < a.W) {
+                        float u[4];
 #pragma unroll
-                        for (int dj = 0; dj < 3; dj++) {
-                            const u32x4 bv = *reinterpret_cast<const u32x4 *>(
-                                U + (uint32_t)((2 * rp + q) * UC + jl + dj) * PB + (uint32_t)gg * 16);
-                            acc = T::mfma(av[dj], bv, acc);
+                        for (int e = 0; e < 4; e++) {
+                            u[e] = silu_f32(fmaf(acc[e], sc[e], bi[e]));
+                            sum[e] += u[e];
                         }
-                        const int r = 2 * rp + (q >> 1), c = jl;
-                        if (r < a.H && c < a.W) {
-                            float u[4];
-#pragma unroll
-                            for (int e = 0; e < 4; e++) {
-                                u[e] = silu_f32(fmaf(acc[e], sc[e], bi[e]));
-                                sum[e] += u[e];
-                            }
-                            st8_dev(vx + (size_t)(r * a.W + c) * EC + h0 + hl,
-                                    u32x2{T::pack2(u[0], u[1]), T::pack2(u[2], u[3])});
-                        }
+                        st8_dev(vx + (size_t)(r * a.W + c) * EC + h0 + hl,
+                                u32x2{T::pack2(u[0], u[1]), T::pack2(u[2], u[3])});
                     }
-                    // sum over the 16 columns (lane bits 0-3) and the two rows of a
-                    // pair (lane bit 5); lanes 0 and 16 hold channels hl .. hl+3
+                }
+                // sum over the 16 columns (lane bits 0-3) and the two rows of a
+                // pair (lane bit 5); lanes 0 and 16 hold channels hl .. hl+3
 #pragma unroll
-                    for (int e = 0; e < 4; e++) {
+                for (int e = 0; e < 4; e++) {
 #pragma unroll
-                        for (int m = 1; m <= 8; m <<= 1)
-                            sum[e] += __shfl_xor(sum[e], m);
-                        sum[e] += __shfl_xor(sum[e], 32);
-                    }
-                    if (jl == 0 && q < 2) {
+                    for (int m = 1; m <= 8; m <<= 1)
+                        sum[e] += __shfl_xor(sum[e], m);
+                    sum[e] += __shfl_xor(sum[e], 32);
+                }
+                if (jl == 0 && q < 2) {
 #pragma unroll
-                        for (int e = 0; e < 4; e++)
-                            csum[hl + e] = sum[e];
-                    }
+                    for (int e = 0; e < 4; e++)
+                        csum[hl + e] = sum[e];
                 }
             }
             __syncthreads();
@@ -289,14 +321,15 @@ struct MB {
                 const float inv = 1.0f / (float)P;
                 float s = 0.0f;
                 const uint16_t *wrow = a.wr + (size_t)tid * EC + h0;
+                Pack8 w[GH / 8];
 #pragma unroll
-                for (int c = 0; c < GH; c += 8) {
-                    Pack8 w;
-                    w.u = ld16(wrow + c);
+                for (int c = 0; c < GH / 8; c++)
+                    w[c].u = ld16(wrow + 8 * c);
+#pragma unroll
+                for (int c = 0; c < GH / 8; c++)
 #pragma unroll
                     for (int e = 0; e < 4; e++)
-                        s += T::lo(w.w[e]) * csum[c + 2 * e] + T::hi(w.w[e]) * csum[c + 2 * e + 1];
-                }
+                        s += T::lo(w[c].w[e]) * csum[8 * c + 2 * e] + T::hi(w[c].w[e]) * csum[8 * c + 2 * e + 1];
                 __hip_atomic_store(a.sq + ((size_t)n * G + g) * R + tid, s * inv, __ATOMIC_RELAXED,
                                    __HIP_MEMORY_SCOPE_AGENT);
             }
@@ -306,10 +339,20 @@ struct MB {
 
             // ---- 5. squeeze (shares in group order), excitation, gates of all channels
             for (int r = tid; r < R; r += NT) {
+                const float *sp = a.sq + (size_t)n * G * R + r;
                 float s = a.br ? a.br[r] : 0.0f;
-                for (int gg = 0; gg < G; gg++)
-                    s += __hip_atomic_load(a.sq + ((size_t)n * G + gg) * R + r, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
+                int gg = 0;
+                for (; gg + 8 <= G; gg += 8) {
+                    float v[8];
+#pragma unroll
+                    for (int u = 0; u < 8; u++)
+                        v[u] = __hip_atomic_load(sp + (size_t)(gg + u) * R, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+                    for (int u = 0; u < 8; u++)
+                        s += v[u];
+                }
+                for (; gg < G; gg++)
+                    s += __hip_atomic_load(sp + (size_t)gg * R, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 zl[r] = s > 0.0f ? s : 0.0f;
             }
             __syncthreads();
@@ -318,6 +361,18 @@ struct MB {
                 float s = a.be ? a.be[c] : 0.0f;
                 int r = 0;
                 if ((R & 7) == 0) {
+                    for (; r + 64 <= R; r += 64) {  // eight 16-byte loads in flight
+                        Pack8 w[8];
+#pragma unroll
+                        for (int u = 0; u < 8; u++)
+                            w[u].u = ld16(wrow + r + 8 * u);
+#pragma unroll
+                        for (int u = 0; u < 8; u++)
+#pragma unroll
+                            for (int e = 0; e < 4; e++)
+                                s += T::lo(w[u].w[e]) * zl[r + 8 * u + 2 * e] +
+                                     T::hi(w[u].w[e]) * zl[r + 8 * u + 2 * e + 1];
+                    }
                     for (; r < R; r += 8) {
                         Pack8 w;
                         w.u = ld16(wrow + r);
@@ -332,71 +387,117 @@ struct MB {
             }
             __syncthreads();
 
-            // ---- 6. output tiles t = g + G (wv + NWV i): 16 pixels x 16 channels, K = EC
+            // ---- 6. output.  The image's pixel tiles x output-channel tiles are
+            //      cut into units of one pixel tile and a range of channel
+            //      tiles, dealt round-robin to the image's work items (more
+            //      channel ranges per pixel tile when the work items outnumber
+            //      the pixel tiles, so a work item then has one unit; otherwise
+            //      every unit spans all channel tiles).  The work item's units
+            //      of V, times the gates, are staged in LDS over the dead U
+            //      buffer; each channel tile is a product over all EC hidden
+            //      channels of W2 rows (loaded in batches of KB steps, the next
+            //      batch in flight, each fragment serving two units) and the
+            //      staged V; then s3, b3 and the residual, and y is written once.
             {
-                const int PT = (P + 15) / 16, T16 = PT * (C / 16);
+                const int PT = (P + 15) / 16, OT = C / 16;
+                const int NOG = G > PT ? G / PT : 1;
+                const int per = (OT + NOG - 1) / NOG;  // channel tiles per unit
+                const int units = PT * NOG;
+                const int nu = g < units ? (units - g + G - 1) / G : 0;  // units g + G u of this work item
+                const int ot0 = NOG > 1 ? (g / PT) * per : 0, ot1 = min(OT, ot0 + per);
                 const int kst = EC / 32;
-                for (int t = g + G * wv; t < T16; t += G * NWV) {
-                    const int pt = t % PT, ot = t / PT;
-                    const int p = 16 * pt + jl;
-                    const bool pin = p < P;
-                    const uint16_t *wrow = a.w2 + (size_t)(16 * ot + jl) * EC + 8 * q;
-                    const uint16_t *vrow = vx + (size_t)(pin ? p : 0) * EC + 8 * q;
-                    float4v acc = {0.f, 0.f, 0.f, 0.f};
-                    auto load = [&](int kk, u32x4 &w, u32x4 &v) {
-                        w = ld16(wrow + 32 * kk);
-                        if (pin) {
-                            const u32x2 lo = ld8_dev(vrow + 32 * kk), hi = ld8_dev(vrow + 32 * kk + 4);
-                            v = u32x4{lo[0], lo[1], hi[0], hi[1]};
-                        } else {
-                            v = u32x4{0u, 0u, 0u, 0u};
-                        }
-                    };
-                    auto mma = [&](int kk, const u32x4 &w, const u32x4 &v) {
-                        const float4v g0 = *reinterpret_cast<const float4v *>(gate + 32 * kk + 8 * q);
-                        const float4v g1 = *reinterpret_cast<const float4v *>(gate + 32 * kk + 8 * q + 4);
-                        u32x4 av;
-                        av[0] = T::pack2(T::lo(w[0]) * g0[0], T::hi(w[0]) * g0[1]);
-                        av[1] = T::pack2(T::lo(w[1]) * g0[2], T::hi(w[1]) * g0[3]);
-                        av[2] = T::pack2(T::lo(w[2]) * g1[0], T::hi(w[2]) * g1[1]);
-                        av[3] = T::pack2(T::lo(w[3]) * g1[2], T::hi(w[3]) * g1[3]);
-                        acc = T::mfma(av, v, acc);
-                    };
-                    u32x4 w0, v0, w1, v1;
-                    load(0, w0, v0);
-                    for (int kk = 0; kk < kst; kk += 2) {
-                        load(kk + 1, w1, v1);  // kst is even: EC is a multiple of 64
-                        mma(kk, w0, v0);
-                        if (kk + 2 < kst)
-                            load(kk + 2, w0, v0);
-                        mma(kk + 1, w1, v1);
+                const int nbat = (kst + KB - 1) / KB;
+                const uint32_t pitch = 2 * EC + 16;  // staged bytes per pixel: an odd multiple of 16
+                const int c4n = EC / 4;
+                // stage the gated V of every unit (zero past P)
+                for (int idx = tid; idx < nu * 16 * c4n; idx += NT) {
+                    const int row = idx / c4n, c4 = idx - row * c4n;  // row = 16 u + pixel
+                    const int p = 16 * ((g + G * (row >> 4)) % PT) + (row & 15);
+                    u32x2 v = {0u, 0u};
+                    if (p < P) {
+                        const u32x2 raw = ld8_dev(vx + (size_t)p * EC + 4 * c4);
+                        const float4v gv = *reinterpret_cast<const float4v *>(gate + 4 * c4);
+                        v[0] = T::pack2(T::lo(raw[0]) * gv[0], T::hi(raw[0]) * gv[1]);
+                        v[1] = T::pack2(T::lo(raw[1]) * gv[2], T::hi(raw[1]) * gv[3]);
                     }
-                    if (pin) {
+                    *reinterpret_cast<u32x2 *>(U + (uint32_t)row * pitch + (uint32_t)c4 * 8) = v;
+                }
+                __syncthreads();
+                for (int u0 = 0; u0 < nu; u0 += 2) {
+                    const bool two = u0 + 1 < nu;  // wave-uniform
+                    const int p0 = 16 * ((g + G * u0) % PT) + jl;
+                    const int p1 = 16 * ((g + G * (u0 + 1)) % PT) + jl;
+                    const uint8_t *vl0 = U + (uint32_t)(16 * u0 + jl) * pitch + (uint32_t)q * 16;
+                    const uint8_t *vl1 = vl0 + 16 * pitch;
+                    for (int ot = ot0 + wv; ot < ot1; ot += NWV) {
+                        const uint16_t *wrow = a.w2 + (size_t)(16 * ot + jl) * EC + 8 * q;
                         const int o = 16 * ot + 4 * q;
-                        const float4v sc =
-                            a.s3 ? *reinterpret_cast<const float4v *>(a.s3 + o) : float4v{1.f, 1.f, 1.f, 1.f};
-                        const float4v bi =
-                            a.b3 ? *reinterpret_cast<const float4v *>(a.b3 + o) : float4v{0.f, 0.f, 0.f, 0.f};
-                        const size_t e = ((size_t)n * P + p) * C + o;
-                        const u32x2 xv = *reinterpret_cast<const u32x2 *>(a.x + e);
-                        u32x2 out;
-                        out[0] = T::pack2(T::lo(xv[0]) + fmaf(acc[0], sc[0], bi[0]),
-                                          T::hi(xv[0]) + fmaf(acc[1], sc[1], bi[1]));
-                        out[1] = T::pack2(T::lo(xv[1]) + fmaf(acc[2], sc[2], bi[2]),
-                                          T::hi(xv[1]) + fmaf(acc[3], sc[3], bi[3]));
-                        *reinterpret_cast<u32x2 *>(a.y + e) = out;
+                        u32x2 xv0 = {0u, 0u}, xv1 = {0u, 0u};
+                        if (p0 < P)
+                            xv0 = *reinterpret_cast<const u32x2 *>(a.x + ((size_t)n * P + p0) * C + o);
+                        if (two && p1 < P)
+                            xv1 = *reinterpret_cast<const u32x2 *>(a.x + ((size_t)n * P + p1) * C + o);
+                        float4v acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+                        auto loadb = [&](int b, u32x4 *w) {
+#pragma unroll
+                            for (int j = 0; j < KB; j++) {
+                                const int kk = KB * b + j;
+                                if (kk < kst)
+                                    w[j] = ld16(wrow + 32 * kk);
+                            }
+                        };
+                        auto mmab = [&](int b, const u32x4 *w) {
+#pragma unroll
+                            for (int j = 0; j < KB; j++) {
+                                const int kk = KB * b + j;
+                                if (kk >= kst)
+                                    break;
+                                acc0 = T::mfma(w[j], *reinterpret_cast<const u32x4 *>(vl0 + (uint32_t)kk * 64), acc0);
+                                if (two)
+                                    acc1 = T::mfma(w[j], *reinterpret_cast<const u32x4 *>(vl1 + (uint32_t)kk * 64),
+                                                   acc1);
+                            }
+                        };
+                        u32x4 wA[KB], wB[KB];
+                        loadb(0, wA);
+                        for (int b = 0; b < nbat; b += 2) {
+                            if (b + 1 < nbat)
+                                loadb(b + 1, wB);
+                            mmab(b, wA);
+                            if (b + 1 < nbat) {
+                                if (b + 2 < nbat)
+                                    loadb(b + 2, wA);
+                                mmab(b + 1, wB);
+                            }
+                        }
+                        const float4v sc = *reinterpret_cast<const float4v *>(s3l + o);
+                        const float4v bi = *reinterpret_cast<const float4v *>(b3l + o);
+                        auto store = [&](int p, const u32x2 &xv, const float4v &acc) {
+                            u32x2 out;
+                            out[0] = T::pack2(T::lo(xv[0]) + fmaf(acc[0], sc[0], bi[0]),
+                                              T::hi(xv[0]) + fmaf(acc[1], sc[1], bi[1]));
+                            out[1] = T::pack2(T::lo(xv[1]) + fmaf(acc[2], sc[2], bi[2]),
+                                              T::hi(xv[1]) + fmaf(acc[3], sc[3], bi[3]));
+                            *reinterpret_cast<u32x2 *>(a.y + ((size_t)n * P + p) * C + o) = out;
+                        };
+                        if (p0 < P)
+                            store(p0, xv0, acc0);
+                        if (two && p1 < P)
+                            store(p1, xv1, acc1);
                     }
                 }
+                __syncthreads();  // the staging area is U again for the next image
             }
-            // U, the gates and the sums are rewritten only after the next
-            // image's first __syncthreads, which every thread reaches after
-            // its last read of them here
+            // the next image rewrites U (its border first, then the interior)
+            // after the __syncthreads that ends the last unit above
         }
     }
 };
 
+// registers for two waves per SIMD: one 8-wave or two 4-wave workgroups per
+// CU (the LDS layout of three or more would not fit with W1 resident)
 template <typename T, int NWV, int NPW>
-__global__ __launch_bounds__(NWV * 64) void mbconv_kernel(Args a) {
+__global__ __launch_bounds__(NWV * 64) __attribute__((amdgpu_waves_per_eu(2))) void mbconv_kernel(Args a) {
     extern __shared__ __attribute__((aligned(256))) uint8_t smem[];
     MB<T, NWV, NPW>::run(a, smem);
 }
@@ -410,23 +511,32 @@ __global__ void clear_kernel(int *p, int n) {
 }
 
 struct Layout {
-    uint32_t off_gate, off_z, off_cs, lds;
+    uint32_t off_gate, off_z, off_cs, off_vec, off_w1, lds;
     int nwv;
 };
 
 // LDS layout for an H x W image.  U holds the border row above the image,
 // its H rows, and zero rows below up to an even count of row pairs plus one
-// (the conv reads halo rows 2rp .. 2rp+3 for every row pair rp); then the
-// gates of all EC channels, the squeeze vector and the group's channel sums.
-Layout layout(int H, int W, int EC, int R) {
+// (the conv reads halo rows 2rp .. 2rp+3 for every row pair rp); the output
+// phase stages the work item's units of gated V over the same bytes.  Then
+// the gates of all EC channels, the squeeze vector, the group's channel sums,
+// the fp32 scale/bias vectors (the group's s1, b1, s2, b2; all of s3, b3) and
+// the group's rows of W1.
+Layout layout(int H, int W, int C, int EC, int R) {
     Layout l;
-    const int P = H * W;
-    l.nwv = P > 128 ? 8 : 4;
+    const int P = H * W, G = EC / GH, PT = (P + 15) / 16;
     const uint32_t urows = (uint32_t)(2 * ((H + 1) / 2) + 2);
-    l.off_gate = urows * UC * PB;
+    const uint32_t nu = G > PT ? 1 : (uint32_t)((PT + G - 1) / G);  // output units of a work item
+    const uint32_t ubytes = urows * UC * PB, stage = nu * 16 * (2 * (uint32_t)EC + 16);
+    l.off_gate = ubytes > stage ? ubytes : stage;
     l.off_z = l.off_gate + (uint32_t)EC * 4;
     l.off_cs = l.off_z + (((uint32_t)R * 4 + 15) & ~15u);
-    l.lds = l.off_cs + GH * 4;
+    l.off_vec = l.off_cs + GH * 4;
+    l.off_w1 = l.off_vec + (4 * GH + 2 * (uint32_t)C) * 4;
+    l.lds = l.off_w1 + 64 * (2 * (uint32_t)C + 16);
+    // 4-wave workgroups, two or more per CU; 8-wave ones for 16 x 16 images
+    // whose layout leaves room for only one workgroup
+    l.nwv = P > 128 && l.lds > 80 * 1024 ? 8 : 4;
     return l;
 }
 
@@ -437,18 +547,21 @@ size_t sq_bytes(int N, int G, int R) { return ((size_t)N * G * R * 4 + 255) & ~(
 
 bool mbconv_supported(int H, int W, int C, int E, int R) {
     return H >= 1 && W >= 1 && H <= mbc::HMAX && W <= mbc::WMAX && C >= 16 && C % 16 == 0 && E >= 1 &&
-           (E * C) % mbc::GH == 0 && E * C <= mbc::ECMAX && R >= 1 && R <= mbc::RMAX;
+           (E * C) % mbc::GH == 0 && E * C <= mbc::ECMAX && R >= 1 && R <= mbc::RMAX &&
+           mbc::layout(H, W, C, E * C, R).lds <= 160 * 1024;
 }
 
 namespace {
 
 // The kernel instance for the shape and its launch size.
-const void *mbconv_kernel_for(int H, int W, int EC, int R, int bf16, mbc::Layout *l, int *nt) {
-    *l = mbc::layout(H, W, EC, R);
+const void *mbconv_kernel_for(int H, int W, int C, int EC, int R, int bf16, mbc::Layout *l, int *nt) {
+    *l = mbc::layout(H, W, C, EC, R);
     *nt = l->nwv * 64;
     const int P = H * W;
     if (l->nwv == 8)
         return bf16 ? (const void *)mbc::mbconv_kernel<BF16, 8, 2> : (const void *)mbc::mbconv_kernel<F16, 8, 2>;
+    if (P > 128)
+        return bf16 ? (const void *)mbc::mbconv_kernel<BF16, 4, 4> : (const void *)mbc::mbconv_kernel<F16, 4, 4>;
     if (P > 64)
         return bf16 ? (const void *)mbc::mbconv_kernel<BF16, 4, 2> : (const void *)mbc::mbconv_kernel<F16, 4, 2>;
     return bf16 ? (const void *)mbc::mbconv_kernel<BF16, 4, 1> : (const void *)mbc::mbconv_kernel<F16, 4, 1>;
@@ -459,7 +572,7 @@ const void *mbconv_kernel_for(int H, int W, int EC, int R, int bf16, mbc::Layout
 hipError_t mbconv_resident_slots(int H, int W, int C, int E, int R, int bf16, int *slots) {
     mbc::Layout l;
     int nt = 0;
-    const void *kf = mbconv_kernel_for(H, W, E * C, R, bf16, &l, &nt);
+    const void *kf = mbconv_kernel_for(H, W, C, E * C, R, bf16, &l, &nt);
     hipError_t e = allow_full_lds(kf);
     if (e != hipSuccess)
         return e;
@@ -502,10 +615,12 @@ hipError_t launch_mbconv(const void *x, void *y, const MBConvW &w, int N, int H,
     a.G = a.EC / mbc::GH;
     mbc::Layout l;
     int nt = 0;
-    const void *kf = mbconv_kernel_for(H, W, a.EC, R, bf16, &l, &nt);
+    const void *kf = mbconv_kernel_for(H, W, C, a.EC, R, bf16, &l, &nt);
     a.off_gate = l.off_gate;
     a.off_z = l.off_z;
     a.off_cs = l.off_cs;
+    a.off_vec = l.off_vec;
+    a.off_w1 = l.off_w1;
     const size_t fixed = mbc::head_bytes(N) + mbc::sq_bytes(N, a.G, R);
     const size_t per_slot = 2 * (size_t)H * W * a.EC * 2;
     if (ws_bytes < fixed + per_slot)

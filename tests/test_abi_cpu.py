@@ -421,6 +421,8 @@ def test_mbconv_forward_rejects():
     assert call(C=48, E=1) == cf.CF_ERR_UNSUPPORTED  # E*C not a multiple of 64
     assert call(R=257) == cf.CF_ERR_UNSUPPORTED
     assert call(C=512, E=16) == cf.CF_ERR_UNSUPPORTED   # E*C > 4096
+    assert call(C=1024, E=1) == cf.CF_ERR_UNSUPPORTED   # W1 rows, gates, staged V and vectors exceed 160 KB of LDS
+    assert call(C=512, E=8) == cf.CF_ERR_UNSUPPORTED
     n = need(2, 8, 8, 64, 4, 16)
     assert call(ws_bytes=n - 1) == cf.CF_ERR_WORKSPACE
     assert call(ws=None, ws_bytes=0) == cf.CF_ERR_WORKSPACE
