@@ -226,9 +226,22 @@ cf_status cf_gblock_forward(const void *x, void *y, const cf_gblock_params *p,
  * CF_ERR_INVALID.  ws: cf_mbconv_workspace_bytes() bytes (queried on the
  * current device) let every image the device can hold be in flight; a
  * smaller ws runs fewer images at once, and one too small for a single image
- * returns CF_ERR_WORKSPACE.  Once the call has completed on the stream, the
- * first int of ws is nonzero if a barrier wait gave up (the output is then
- * invalid; the cooperative launch rules this out).  fp16 or bf16 I/O, fp32
+ * returns CF_ERR_WORKSPACE.  ws must be zero-filled before its first use:
+ * its first 256 + 2048 * 128 bytes hold the barrier lines of the images in
+ * flight, and every call leaves them zero again, whatever the shapes of the
+ * calls that share the workspace, so a call is a single launch.  If a
+ * barrier wait ever gives up (that call's output is then invalid; the
+ * cooperative launch rules this out), the first int of ws is set to 1 and the
+ * library never clears it.  Calls that share a workspace must not overlap in
+ * time.
+ * launch: CF_LAUNCH_COOPERATIVE (hipLaunchCooperativeKernel: the runtime
+ * makes every workgroup resident at once, and refuses a grid that cannot be)
+ * or CF_LAUNCH_EXCLUSIVE, an ordinary launch of the same grid (sized to what
+ * fits on the device) for callers that own the device for the call -- no
+ * kernel of theirs or anyone else's runs beside it.  It saves the cooperative
+ * launch's fixed cost (about 17 us per call measured on MI355X); if other
+ * work does keep a workgroup from starting, a wait gives up after about a
+ * second and the flag above is set (the kernel still ends).  fp16 or bf16 I/O, fp32
  * accumulation; U, V and the gated project weights are rounded to the I/O
  * dtype before their products.  Deterministic: every sum has a fixed order. */
 typedef struct {
@@ -244,8 +257,11 @@ typedef struct {
     const float *s3, *b3;
 } cf_mbconv_params;
 
+typedef enum { CF_LAUNCH_COOPERATIVE = 0, CF_LAUNCH_EXCLUSIVE = 1 } cf_launch;
+
 cf_status cf_mbconv_forward(const void *x, void *y, void *ws, size_t ws_bytes, const cf_mbconv_params *p,
-                            int N, int H, int W, int C, int E, int R, int k, cf_dtype dt, void *stream);
+                            int N, int H, int W, int C, int E, int R, int k, cf_dtype dt, cf_launch launch,
+                            void *stream);
 /* 0 for shapes the kernel does not support. */
 size_t cf_mbconv_workspace_bytes(int N, int H, int W, int C, int E, int R, cf_dtype dt);
 

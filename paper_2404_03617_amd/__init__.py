@@ -106,7 +106,7 @@ def lib():
             "cf_split_workspace_bytes": (sz, [i, i, i, i, i, i]),
             "cf_block_forward_split_noalloc": (i, [vp, vp, bp, i, i, i, i, i, i, i, i, i, vp]),
             "cf_gblock_forward": (i, [vp, vp, gp, i, i, i, i, i, i, i, i, vp]),
-            "cf_mbconv_forward": (i, [vp, vp, vp, sz, mp, i, i, i, i, i, i, i, i, vp]),
+            "cf_mbconv_forward": (i, [vp, vp, vp, sz, mp, i, i, i, i, i, i, i, i, i, vp]),
             "cf_mbconv_workspace_bytes": (sz, [i, i, i, i, i, i, i]),
             "cf_block_autotune": (i, [vp, vp, bp, i, i, i, i, i, i, i, i, vp]),
             "cf_block_tuned_config": (i, [i, i, i, i, i, i, i, i]),
@@ -440,13 +440,23 @@ def mbconv_workspace_bytes(N: int, H: int, W: int, C: int, E: int, R: int, dtype
     return int(lib().cf_mbconv_workspace_bytes(N, H, W, C, E, R, DTYPES[dtype]))
 
 
-def mbconv_forward(x: torch.Tensor, p: dict, out=None, ws=None, stream=None) -> torch.Tensor:
+LAUNCHES = {"cooperative": 0, "exclusive": 1}
+
+
+def mbconv_forward(x: torch.Tensor, p: dict, out=None, ws=None, launch: str = "cooperative",
+                   stream=None) -> torch.Tensor:
     """The paper's MBConv block with Squeeze & Excitation (Sec. 5.4) fused
     into one cooperative kernel (Sec. 5.4.1).  p holds w1 [E*C,C], gw_w
     [3,3,E*C,8], wr [R,E*C], we [E*C,R], w2 [C,E*C] in x's dtype and optional
     fp32 s1,b1,s2,b2,be [E*C], br [R], s3,b3 [C].  out may be x itself
-    (evaluation in place).  ws: a uint8 workspace, by default one of
-    mbconv_workspace_bytes(); a smaller one runs fewer images at a time."""
+    (evaluation in place).  ws: a uint8 workspace, by default a zeroed one of
+    mbconv_workspace_bytes(); a smaller one runs fewer images at a time.  A
+    caller's ws must be zeroed before its first use (every call leaves it
+    reusable); its first int32 becomes 1 if a barrier wait ever gave up.
+    launch="exclusive" replaces the cooperative launch by an ordinary one,
+    for callers that own the device (see the C header)."""
+    if launch not in LAUNCHES:
+        raise ValueError("launch must be one of %s" % sorted(LAUNCHES))
     N, H, W, C = _dims(x)
     for key in ("w1", "gw_w", "wr", "we", "w2"):
         if not isinstance(p.get(key), torch.Tensor):
@@ -476,11 +486,12 @@ def mbconv_forward(x: torch.Tensor, p: dict, out=None, ws=None, stream=None) -> 
     _check_device(x)
     y = _out(x, out)
     if ws is None:
-        ws = _workspace(x, None, max(1, mbconv_workspace_bytes(N, H, W, C, EC // C, R, x.dtype)))
+        ws = torch.zeros(max(1, mbconv_workspace_bytes(N, H, W, C, EC // C, R, x.dtype)), dtype=torch.uint8,
+                         device=x.device)
     else:
         _workspace(x, ws, 0)
     _check(lib().cf_mbconv_forward(_ptr(x), _ptr(y), _ptr(ws), ws.numel(), ctypes.byref(mp), N, H, W, C, EC // C,
-                                   R, k, DTYPES[x.dtype], _stream(stream)))
+                                   R, k, DTYPES[x.dtype], LAUNCHES[launch], _stream(stream)))
     return y
 
 

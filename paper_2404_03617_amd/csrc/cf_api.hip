@@ -592,7 +592,7 @@ size_t cf_mbconv_workspace_bytes(int N, int H, int W, int C, int E, int R, cf_dt
 }
 
 cf_status cf_mbconv_forward(const void *x, void *y, void *ws, size_t ws_bytes, const cf_mbconv_params *p, int N,
-                            int H, int W, int C, int E, int R, int k, cf_dtype dt, void *stream) {
+                            int H, int W, int C, int E, int R, int k, cf_dtype dt, cf_launch launch, void *stream) {
     const char *what = "cf_mbconv_forward";
     if (!x || !y)
         return fail(CF_ERR_INVALID, "%s: x and y must be non-NULL", what);
@@ -607,6 +607,8 @@ cf_status cf_mbconv_forward(const void *x, void *y, void *ws, size_t ws_bytes, c
         return fail(CF_ERR_INVALID, "%s: C=%d is not a multiple of the group width %d", what, C, CF_GROUP_WIDTH);
     if ((int)dt != CF_F16 && (int)dt != CF_BF16)
         return fail(CF_ERR_INVALID, "%s: unknown dtype %d", what, (int)dt);
+    if ((int)launch != CF_LAUNCH_COOPERATIVE && (int)launch != CF_LAUNCH_EXCLUSIVE)
+        return fail(CF_ERR_INVALID, "%s: unknown launch mode %d", what, (int)launch);
     if ((double)N * H * W * C > 4.0e12 || (double)E * C > 65536.0)
         return fail(CF_ERR_INVALID, "%s: tensor too large", what);
     const void *ptrs[] = {x, y, ws, p->w1, p->gw_w, p->wr, p->we, p->w2, p->s1, p->b1,
@@ -644,7 +646,8 @@ cf_status cf_mbconv_forward(const void *x, void *y, void *ws, size_t ws_bytes, c
     w.w2 = p->w2;
     w.s3 = p->s3;
     w.b3 = p->b3;
-    hipError_t e = cf::launch_mbconv(x, y, w, N, H, W, C, E, R, dt == CF_BF16, ws, ws_bytes, (hipStream_t)stream);
+    hipError_t e = cf::launch_mbconv(x, y, w, N, H, W, C, E, R, dt == CF_BF16, ws, ws_bytes,
+                                     launch == CF_LAUNCH_COOPERATIVE, (hipStream_t)stream);
     if (e == hipErrorInvalidConfiguration)
         return fail(CF_ERR_UNSUPPORTED, "%s: the %d work items of one image do not fit on the device at once", what,
                     E * C / 64);

@@ -123,10 +123,11 @@ hipError_t mbconv_resident_slots(int H, int W, int C, int E, int R, int bf16, in
 // Workspace bytes for `slots` images in flight.
 size_t mbconv_workspace_bytes(int N, int H, int W, int C, int E, int R, int slots);
 // Fused MBConv block; ws of ws_bytes >= mbconv_workspace_bytes(..., 1)
-// (hipErrorInvalidValue otherwise).  The first int of ws is nonzero after the
-// kernel if a barrier wait gave up.
+// (hipErrorInvalidValue otherwise), its header zero.  The first int of ws is
+// set if a barrier wait gave up.  coop: hipLaunchCooperativeKernel, else an
+// ordinary launch of the same grid.
 hipError_t launch_mbconv(const void *x, void *y, const MBConvW &w, int N, int H, int W, int C, int E, int R,
-                         int bf16, void *ws, size_t ws_bytes, hipStream_t st);
+                         int bf16, void *ws, size_t ws_bytes, bool coop, hipStream_t st);
 
 // Upper bound of dynamic LDS the fused kernel needs for this shape (bytes);
 // 0 when no kernel configuration fits.

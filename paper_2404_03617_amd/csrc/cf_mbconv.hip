@@ -50,8 +50,12 @@
 // device, `slots` images in flight, each slot's workgroups walking the same
 // sequence of images; the exchange buffer of a slot alternates between two
 // halves, so an image's V never overwrites the previous image's while it is
-// read.  The wait is bounded; one that gives up sets a flag in the workspace,
-// the later waits of the launch are skipped, and the kernel always ends.
+// read.  Each slot has a line in the workspace header (arrivals, give-up,
+// exits) that its last work item zeroes on the way out, so a call is one
+// launch and the header, zeroed once before first use, stays zero between
+// calls whatever shapes share the workspace.  The wait is bounded; one that
+// gives up sets a flag in the workspace, the slot's later waits of the call
+// are skipped, and the kernel always ends.
 //
 // Images up to 16 x 16 (the late-stage shapes the paper targets); C a
 // multiple of 16; E*C a multiple of 64 and at most 4096; 1 <= R <= 256; the
@@ -59,6 +63,7 @@
 // 512 at E = 4, 256 at E = 8).
 #include "cf_device.h"
 #include "cf_kernels.h"
+
 
 namespace cf {
 namespace mbc {
@@ -70,6 +75,7 @@ constexpr int PB = 2 * GH + 16;   // LDS bytes per pixel: an odd multiple of 16,
 constexpr int RMAX = 256;
 constexpr int ECMAX = 4096;
 constexpr int SPIN_LIMIT = 1 << 20;
+constexpr int SLOTMAX = 2048;     // images in flight the workspace header has lines for
 
 struct Args {
     const uint16_t *x;
@@ -84,8 +90,8 @@ struct Args {
     const float *be;
     const uint16_t *w2;            // [C][EC]
     const float *s3, *b3;
-    int *flag;                     // nonzero once a barrier wait gave up
-    int *cnt;                      // [N] arrivals per image
+    int *flag;                     // set to 1 when a barrier wait gives up (never cleared here)
+    int *line;                     // [SLOTMAX][32]: per slot arrivals, give-up, exits (zero between calls)
     float *sq;                     // [N][G][R] squeeze shares
     uint16_t *vx;                  // [2][slots][P][EC] exchanged conv output
     int N, H, W, C, EC, R, G;
@@ -109,28 +115,42 @@ __device__ __forceinline__ u32x2 ld8_dev(const uint16_t *p) {
 __device__ __forceinline__ float silu_f32(float u) { return u * __builtin_amdgcn_rcpf(1.0f + __expf(-u)); }
 __device__ __forceinline__ float sigmoid_f32(float u) { return __builtin_amdgcn_rcpf(1.0f + __expf(-u)); }
 
-// Every thread's device-scope stores so far are complete when the workgroup
-// adds its arrival to cnt; returns once cnt reaches target (or a wait gave up).
-__device__ __forceinline__ void image_barrier(int *cnt, int target, int *flag) {
+// Barrier of a slot's work items at the end of their `target` / G-th image:
+// every thread's device-scope stores so far are complete when the workgroup
+// adds its arrival to the slot's count (it grows by G per image); returns once
+// the count reaches `target`.  The wait is bounded: a work item that gives up
+// marks the slot's line (the slot's later waits in this call are then
+// skipped) and sets the workspace flag, which stays set for the caller.
+__device__ __forceinline__ void slot_barrier(const Args &a, int *line, int target) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     if (threadIdx.x == 0) {
-        __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
-            int spins = 0;
-            while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-                if (++spins > SPIN_LIMIT) {
-                    __hip_atomic_store(flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    break;
+        __hip_atomic_fetch_add(line, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        int spins = 0;
+        while (__hip_atomic_load(line, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+            const bool over = ++spins > SPIN_LIMIT;
+            if (over || ((spins & 63) == 1 && __hip_atomic_load(line + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) {
+                if (over) {
+                    __hip_atomic_store(line + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(a.flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
-                // another workgroup gave up: stop waiting too
-                if ((spins & 63) == 0 && __hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
-                    break;
-                __builtin_amdgcn_s_sleep(1);
+                break;
             }
+            __builtin_amdgcn_s_sleep(1);
         }
     }
     __syncthreads();
+}
+
+// After its last image a work item adds its exit to the slot's line; the last
+// of the slot's G exits (every wait of the slot is over) zeroes the line, so
+// each call leaves the header as it found it.
+__device__ __forceinline__ void slot_exit(int *line, int G) {
+    if (threadIdx.x == 0 && __hip_atomic_fetch_add(line + 2, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == G - 1) {
+        __hip_atomic_store(line, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(line + 1, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(line + 2, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
 }
 
 template <typename T, int NWV, int NPW>
@@ -159,6 +179,7 @@ struct MB {
         float *csum = reinterpret_cast<float *>(smem + a.off_cs);    // [64]
         float *vec = reinterpret_cast<float *>(smem + a.off_vec);    // s1, b1, s2, b2 [64] each; s3, b3 [C]
         float *s1l = vec, *b1l = vec + 64, *s2l = vec + 128, *b2l = vec + 192, *s3l = vec + 256, *b3l = s3l + C;
+        int *line = a.line + 32 * (size_t)slot;
 
         // once per workgroup: the scale/bias vectors the group uses
         for (int i = tid; i < 64; i += NT) {
@@ -335,7 +356,7 @@ struct MB {
             }
 
             // ---- 4. every work item of image n has written its V and its share
-            image_barrier(a.cnt + n, G, a.flag);
+            slot_barrier(a, line, G * (it + 1));
 
             // ---- 5. squeeze (shares in group order), excitation, gates of all channels
             for (int r = tid; r < R; r += NT) {
@@ -491,6 +512,7 @@ struct MB {
             // the next image rewrites U (its border first, then the interior)
             // after the __syncthreads that ends the last unit above
         }
+        slot_exit(line, G);
     }
 };
 
@@ -500,14 +522,6 @@ template <typename T, int NWV, int NPW>
 __global__ __launch_bounds__(NWV * 64) __attribute__((amdgpu_waves_per_eu(2))) void mbconv_kernel(Args a) {
     extern __shared__ __attribute__((aligned(256))) uint8_t smem[];
     MB<T, NWV, NPW>::run(a, smem);
-}
-
-// clears the give-up flag and the arrival counters (a kernel rather than a
-// memset, so that a captured graph replays it faithfully)
-__global__ void clear_kernel(int *p, int n) {
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n)
-        p[i] = 0;
 }
 
 struct Layout {
@@ -540,7 +554,7 @@ Layout layout(int H, int W, int C, int EC, int R) {
     return l;
 }
 
-size_t head_bytes(int N) { return 256 + (((size_t)N * 4 + 255) & ~(size_t)255); }
+size_t head_bytes() { return 256 + (size_t)SLOTMAX * 128; }
 size_t sq_bytes(int N, int G, int R) { return ((size_t)N * G * R * 4 + 255) & ~(size_t)255; }
 
 }  // namespace mbc
@@ -585,11 +599,11 @@ hipError_t mbconv_resident_slots(int H, int W, int C, int E, int R, int bf16, in
 
 size_t mbconv_workspace_bytes(int N, int H, int W, int C, int E, int R, int slots) {
     const int G = E * C / mbc::GH;
-    return mbc::head_bytes(N) + mbc::sq_bytes(N, G, R) + 2 * (size_t)slots * H * W * E * C * 2;
+    return mbc::head_bytes() + mbc::sq_bytes(N, G, R) + 2 * (size_t)slots * H * W * E * C * 2;
 }
 
 hipError_t launch_mbconv(const void *x, void *y, const MBConvW &w, int N, int H, int W, int C, int E, int R,
-                         int bf16, void *ws, size_t ws_bytes, hipStream_t st) {
+                         int bf16, void *ws, size_t ws_bytes, bool coop, hipStream_t st) {
     mbc::Args a{};
     a.x = (const uint16_t *)x;
     a.y = (uint16_t *)y;
@@ -621,18 +635,19 @@ hipError_t launch_mbconv(const void *x, void *y, const MBConvW &w, int N, int H,
     a.off_cs = l.off_cs;
     a.off_vec = l.off_vec;
     a.off_w1 = l.off_w1;
-    const size_t fixed = mbc::head_bytes(N) + mbc::sq_bytes(N, a.G, R);
+    const size_t fixed = mbc::head_bytes() + mbc::sq_bytes(N, a.G, R);
     const size_t per_slot = 2 * (size_t)H * W * a.EC * 2;
     if (ws_bytes < fixed + per_slot)
         return hipErrorInvalidValue;
     char *base = (char *)ws;
     a.flag = (int *)base;
-    a.cnt = (int *)(base + 256);
-    a.sq = (float *)(base + mbc::head_bytes(N));
+    a.line = (int *)(base + 256);
+    a.sq = (float *)(base + mbc::head_bytes());
     // every work item of an image must be resident with the others (the
     // barrier waits for them): the grid holds at most what fits on the device
     // and is launched cooperatively, which the runtime refuses rather than
-    // run partly
+    // run partly -- or, for a caller that owns the device, as an ordinary
+    // launch, which then starts every workgroup at once
     int slots = 0;
     hipError_t e = mbconv_resident_slots(H, W, C, E, R, bf16, &slots);
     if (e != hipSuccess)
@@ -641,18 +656,21 @@ hipError_t launch_mbconv(const void *x, void *y, const MBConvW &w, int N, int H,
         return hipErrorInvalidConfiguration;  // the groups of one image do not fit at once
     if (slots > N)
         slots = N;
+    if (slots > mbc::SLOTMAX)
+        slots = mbc::SLOTMAX;
     if ((size_t)slots * per_slot > ws_bytes - fixed)
         slots = (int)((ws_bytes - fixed) / per_slot);
+    // as few images in flight as the same number of passes over the batch needs
+    const int passes = (N + slots - 1) / slots;
+    slots = (N + passes - 1) / passes;
     a.slots = slots;
     a.vx = (uint16_t *)(base + fixed);
     const int grid = slots * a.G;
     // a slot's workgroups on one XCD when the grid allows it
     a.xcd_map = grid % 8 == 0 && (grid / 8) % a.G == 0 ? 1 : 0;
-    hipLaunchKernelGGL(mbc::clear_kernel, dim3((64 + N + 255) / 256), dim3(256), 0, st, a.flag, 64 + N);
-    if ((e = hipGetLastError()) != hipSuccess)
-        return e;
     void *args[] = {&a};
-    return hipLaunchCooperativeKernel(kf, dim3(grid), dim3(nt), args, l.lds, st);
+    return coop ? hipLaunchCooperativeKernel(kf, dim3(grid), dim3(nt), args, l.lds, st)
+                : hipLaunchKernel(kf, dim3(grid), dim3(nt), args, l.lds, st);
 }
 
 }  // namespace cf

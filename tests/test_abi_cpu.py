@@ -391,14 +391,14 @@ def test_mbconv_forward_rejects():
 
     def need(N, H, W, C, E, R):
         G = E * C // 64
-        return 256 + (N * 4 + 255) // 256 * 256 + (N * G * R * 4 + 255) // 256 * 256 + 2 * H * W * E * C * 2
+        return 256 + 2048 * 128 + (N * G * R * 4 + 255) // 256 * 256 + 2 * H * W * E * C * 2
 
-    def call(x=X, y=Y, ws=WS, ws_bytes=1 << 30, N=2, H=8, W=8, C=64, E=4, R=16, k=3, dt=0, **kw):
+    def call(x=X, y=Y, ws=WS, ws_bytes=1 << 30, N=2, H=8, W=8, C=64, E=4, R=16, k=3, dt=0, launch=0, **kw):
         p = cf._MBConvParams(w1=W1, s1=None, b1=None, gw_w=GW, s2=None, b2=None, wr=WR, br=None, we=WE, be=None,
                              w2=W2, s3=None, b3=None)
         for f, v in kw.items():
             setattr(p, f, v)
-        return L.cf_mbconv_forward(x, y, ws, ws_bytes, ctypes.byref(p), N, H, W, C, E, R, k, dt, None)
+        return L.cf_mbconv_forward(x, y, ws, ws_bytes, ctypes.byref(p), N, H, W, C, E, R, k, dt, launch, None)
 
     assert L.cf_mbconv_workspace_bytes(2, 8, 8, 64, 4, 16, 0) >= need(2, 8, 8, 64, 4, 16)
     assert L.cf_mbconv_workspace_bytes(2, 17, 8, 64, 4, 16, 0) == 0     # H > 16
@@ -411,6 +411,7 @@ def test_mbconv_forward_rejects():
     assert call(C=20) == cf.CF_ERR_INVALID           # not a multiple of the group width
     assert call(k=4) == cf.CF_ERR_INVALID
     assert call(dt=5) == cf.CF_ERR_INVALID
+    assert call(launch=2) == cf.CF_ERR_INVALID
     assert call(y=X + 32) == cf.CF_ERR_INVALID       # overlaps x without being x
     assert call(b3=W1 + 4) == cf.CF_ERR_INVALID      # misaligned
     assert call(ws=X) == cf.CF_ERR_INVALID           # ws overlaps x

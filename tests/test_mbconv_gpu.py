@@ -44,7 +44,7 @@ def run(x, p, **kw):
     N, H, W, C = x.shape
     EC, R = p["w1"].shape[0], p["wr"].shape[0]
     xd = x.cuda()
-    ws = torch.empty(max(1, cf.mbconv_workspace_bytes(N, H, W, C, EC // C, R, x.dtype)), dtype=torch.uint8,
+    ws = torch.zeros(max(1, cf.mbconv_workspace_bytes(N, H, W, C, EC // C, R, x.dtype)), dtype=torch.uint8,
                      device="cuda")
     y = cf.mbconv_forward(xd, to_dev(p), ws=ws, **kw)
     torch.cuda.synchronize()
@@ -81,6 +81,10 @@ def test_mbconv_matches_oracle(case, dtype):
     y, ws = run(x, p)
     assert barrier_flag(ws) == 0
     assert_close(y, ref(x, p), what="mbconv %s %s" % (case, dtype), diag=DIAG_F16 if dtype == "f16" else None)
+    # the ordinary launch of the same grid gives the same bits
+    ye, wse = run(x, p, launch="exclusive")
+    assert barrier_flag(wse) == 0
+    assert torch.equal(ye, y)
 
 
 def test_mbconv_null_scales_and_biases():
@@ -111,12 +115,12 @@ def test_mbconv_in_place_and_small_workspace_match_bitwise(dtype):
     assert torch.equal(xd, y)
     lib = cf.lib()
     full = lib.cf_mbconv_workspace_bytes(N, H, W, C, E, R, cf.DTYPES[x.dtype])
-    # the workspace for one image in flight: flag and counters, squeeze
+    # the workspace for one image in flight: flag and barrier lines, squeeze
     # shares, the two halves of one image's exchange buffer
     G = E * C // 64
-    one_slot = 256 + ((N * 4 + 255) // 256) * 256 + ((N * G * R * 4 + 255) // 256) * 256 + 2 * H * W * E * C * 2
+    one_slot = 256 + 2048 * 128 + ((N * G * R * 4 + 255) // 256) * 256 + 2 * H * W * E * C * 2
     assert one_slot <= full
-    ws = torch.empty(one_slot, dtype=torch.uint8, device="cuda")
+    ws = torch.zeros(one_slot, dtype=torch.uint8, device="cuda")
     y1 = cf.mbconv_forward(x.cuda(), pd, ws=ws)
     torch.cuda.synchronize()
     assert barrier_flag(ws) == 0
@@ -159,3 +163,21 @@ def test_mbconv_paper_table_shapes(name):
     assert barrier_flag(ws) == 0
     assert torch.isfinite(y.float()).all()
     assert_close(y.cpu()[SAMPLE], ref(x[SAMPLE], p), what=name, diag=DIAG_F16)
+
+
+def test_mbconv_workspace_reused_across_calls():
+    """One zeroed workspace serves a sequence of calls of different shapes
+    and batch sizes (every call leaves the barrier lines at zero): each output
+    equals, bit for bit, the output with a fresh workspace."""
+    shapes = [(128, 4, 32, 6, 16, 16), (128, 4, 32, 9, 8, 8), (256, 4, 64, 3, 5, 7), (64, 2, 16, 20, 4, 4),
+              (128, 4, 32, 6, 16, 16)]
+    need = max(cf.mbconv_workspace_bytes(N, H, W, C, E, R) for C, E, R, N, H, W in shapes)
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+    for i, (C, E, R, N, H, W) in enumerate(shapes):
+        x, p = make(90 + i, N, H, W, C, E, R)
+        xd, pd = x.cuda(), to_dev(p)
+        for _ in range(2):
+            y = cf.mbconv_forward(xd, pd, ws=ws)
+            torch.cuda.synchronize()
+            assert barrier_flag(ws) == 0
+            assert torch.equal(y, cf.mbconv_forward(xd, pd))
