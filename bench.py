@@ -312,11 +312,16 @@ def stage_microbatch_case(micro_batches, steps: int, warmup: int):
     xs = [synth.activations(w["seed"] + 100 * i, N, H, W, C, w["dtype"]).cuda() for i in range(nsets)]
     y = torch.empty_like(xs[0])
     stream = torch.cuda.current_stream()
+    # workspaces allocated before the timed region (an allocation inside it
+    # can cost a device allocation per call)
+    ws = torch.empty(cf.lib().cf_stage_workspace_bytes(d, N, H, W, C, 0), dtype=torch.uint8, device="cuda")
     out = {"stage": "2 blocks, N=%d %dx%d C=%d" % (N, H, W, C),
-           "plain_us": round(_time(lambda i: cf.stage_forward(xs[i % nsets], blocks, out=y), steps, warmup,
+           "plain_us": round(_time(lambda i: cf.stage_forward(xs[i % nsets], blocks, out=y, ws=ws), steps, warmup,
                                    stream) * 1e6, 1)}
     for m in micro_batches:
-        t = _time(lambda i: cf.stage_forward_microbatch(xs[i % nsets], blocks, micro_batch=m, out=y), steps,
+        wm = torch.empty(max(1, cf.lib().cf_stage_microbatch_workspace_bytes(d, N, H, W, C, m, 0)),
+                         dtype=torch.uint8, device="cuda")
+        t = _time(lambda i: cf.stage_forward_microbatch(xs[i % nsets], blocks, micro_batch=m, out=y, ws=wm), steps,
                   warmup, stream)
         out["micro_batch_%s_us" % (m if m else "default")] = round(t * 1e6, 1)
     return out
