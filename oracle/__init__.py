@@ -200,6 +200,31 @@ def gblock_forward(x, p: dict, act: str = "relu", nthreads: int = 0):
     return y
 
 
+def stem_forward(x, w, scale=None, bias=None):
+    """The network's stem (App. A: a 3 x 3 convolution with stride 2 from the
+    image's 3 channels to the first stage's C channels; caption of Fig.
+    f:convfirstnet: ReLU), its batch norm folded to scale and bias: the
+    grouped convolution of eq. f:grouped-conv2d with one group, stride 2 and
+    one pixel of zero padding, then s * conv + b and ReLU.
+    x [N,H,W,3], w [C,3,3,3] in the paper's [K][R][S][T] order -> [N,ceil(H/2),ceil(W/2),C]."""
+    w = _f64(w)
+    K, R, S, T = w.shape
+    assert R == S == 3 and T == _f64(x).shape[3]
+    u = grouped_conv(x, w, groups=1, stride=2, pad=1)
+    if scale is not None:
+        u = u * _f64(scale)
+    if bias is not None:
+        u = u + _f64(bias)
+    return np.maximum(u, 0.0)
+
+
+def stem_gblock_forward(x, stem: dict, p: dict, act: str = "relu"):
+    """The stem followed by the first ConvFirst block (App. A: the stem
+    would be fused with the kernel of the first block): gblock_forward of
+    stem_forward.  stem holds sw [C,3,3,3] and optional ss, sb [C]."""
+    return gblock_forward(stem_forward(x, stem["sw"], stem.get("ss"), stem.get("sb")), p, act=act)
+
+
 def mbconv_forward(x, p: dict):
     """The paper's MBConv block with Squeeze & Excitation (Sec. 5.4, 5.4.1):
     expand + SiLU, grouped k x k conv (group width gw) + SiLU, SE (average,
