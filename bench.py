@@ -32,7 +32,7 @@ import torch
 import paper_2404_03617_amd as cf
 from paper_2404_03617_amd import roofline as rl
 from paper_2404_03617_amd import synth
-from paper_2404_03617_amd.workloads import BENCH_WORKLOAD, GBLOCK_WORKLOADS, MBCONV_WORKLOADS, WORKLOADS
+from paper_2404_03617_amd.workloads import BENCH_WORKLOAD, GBLOCK_WORKLOADS, MBCONV_WORKLOADS, STEM_WORKLOADS, WORKLOADS
 
 MALL_BYTES = 256 << 20
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -232,6 +232,37 @@ def mbconv_case(name: str, steps: int, warmup: int):
             "comp_eff": round(rl.comp_eff(flops, t), 4), "roofline": roofline_entry(flops, nbytes, t),
             "exclusive_launch_ms": round(te * 1e3, 4), "exclusive_launch_comp_eff": round(rl.comp_eff(flops, te), 4),
             "paper_A5000_comp_eff": round(w["paper_pct"] / 100, 3)}
+
+
+def stem_case(name: str, steps: int, warmup: int):
+    """The stem (App. A: 3x3 stride-2 conv from the 3-channel image, folded
+    norm, ReLU) fused into the first grouped block, batch 128: one launch per
+    step; beside it the two-launch sequence stem kernel -> block kernel on the
+    same inputs."""
+    w = STEM_WORKLOADS[name]
+    N, Hin, Win, C, E, k = w["N"], w["Hin"], w["Win"], w["C"], w["E"], w["k"]
+    Hs, Ws = (Hin + 1) // 2, (Win + 1) // 2
+    nsets = _sets_needed(N * Hin * Win * 3 * 2 + N * Hs * Ws * C * 2)
+    xs = [synth.activations(w["seed"] + 100 * i, N, Hin, Win, 3, w["dtype"]).cuda() for i in range(nsets)]
+    ys = [torch.empty((N, Hs, Ws, C), dtype=xs[0].dtype, device="cuda") for _ in range(nsets)]
+    mid = torch.empty_like(ys[0])
+    st = {kk: (None if v is None else v.cuda()) for kk, v in synth.stem_params(w["seed"], 0, C, w["dtype"]).items()}
+    p = {kk: (None if v is None else v.cuda()) for kk, v in
+         synth.gblock_params(w["seed"], 1, C, E, k, w["dtype"]).items()}
+    stream = torch.cuda.current_stream()
+    t = _time(lambda i: cf.stem_gblock_forward(xs[i % nsets], st, p, act=w["act"], out=ys[i % nsets]),
+              steps, warmup, stream)
+
+    def two(i):
+        cf.stem_forward(xs[i % nsets], st, out=mid)
+        cf.gblock_forward(mid, p, act=w["act"], out=ys[i % nsets])
+
+    tu = _time(two, steps, warmup, stream)
+    flops = rl.stem_flops(N, Hin, Win, C) + rl.gblock_flops(N, Hs, Ws, C, E, k)
+    nbytes = rl.stem_gblock_bytes_fused(N, Hin, Win, C, E, k)
+    return {"ms": round(t * 1e3, 4), "images_per_s": round(N / t, 1), "tflops": round(flops / t / 1e12, 1),
+            "comp_eff": round(rl.comp_eff(flops, t), 4), "roofline": roofline_entry(flops, nbytes, t),
+            "two_launch_ms": round(tu * 1e3, 4), "speedup_vs_two_launch": round(tu / t, 3)}
 
 
 def stack_waterline(name: str, steps: int, warmup: int):
@@ -448,6 +479,21 @@ def main():
             calib_copy()
         print(json.dumps({"stage_microbatch": r, "micro_batch": args.stage_mb}), flush=True)
         return
+    if name in STEM_WORKLOADS:
+        g = stem_case(name, args.steps, args.warmup)
+        wg = STEM_WORKLOADS[name]
+        cfg = {"workload": name, "N": wg["N"], "H": wg["Hin"], "W": wg["Win"], "C": wg["C"], "E": wg["E"],
+               "k": wg["k"], "act": wg["act"], "kernel": "stem fused into the first grouped block (1 launch)"}
+        print(json.dumps({"metric": "images/sec and % of fp16 MFMA peak (computational efficiency), batch 128",
+                          "value": g["images_per_s"], "unit": "images/s", "n_gpus": 1, "steps": args.steps,
+                          "warmup": args.warmup, "ms_per_step": g["ms"], "higher_is_better": True,
+                          "scaling": "weak", "vs_baseline": None, "dtype": "f16",
+                          "data": "synthetic (seeded N(0,1) images, N(0,1/fan_in) weights)",
+                          "config": cfg, "comp_eff": g["comp_eff"], "roofline": g["roofline"],
+                          "two_launch_ms": g["two_launch_ms"]}), flush=True)
+        if args.calib_copy:
+            calib_copy()
+        return
     if name in GBLOCK_WORKLOADS or name in MBCONV_WORKLOADS:
         # one of the paper's own block shapes as the timed workload (used for
         # profiles of that kernel); the default is the benchmark workload
@@ -561,6 +607,8 @@ def main():
         extra["paper_block_table"] = {nm: gblock_case(nm, max(5, args.steps // 2), 3) for nm in GBLOCK_WORKLOADS}
         # the MBConv + SE block at the shapes of the paper's MBConv table
         extra["paper_mbconv_table"] = {nm: mbconv_case(nm, max(5, args.steps // 2), 3) for nm in MBCONV_WORKLOADS}
+        # the stem fused into the first block (App. A's first rows)
+        extra["stem_first_block"] = {nm: stem_case(nm, max(5, args.steps // 2), 3) for nm in STEM_WORKLOADS}
         out["other_workloads"] = extra
     if args.calib_copy:
         calib_copy()

@@ -193,6 +193,38 @@ cf_status cf_gblock_forward(const void *x, void *y, const cf_gblock_params *p,
                             int N, int H, int W, int C, int E, int k,
                             cf_dtype dt, cf_act act, void *stream);
 
+/* The network's stem (App. A: a 3 x 3 convolution with stride 2 from the
+ * image's 3 channels to the first stage's channels; caption of Fig.
+ * f:convfirstnet: ReLU), its batch norm folded to a scale and a bias:
+ *   S[n,i,j,c] = ReLU(scale[c] * sum_{r,s<3} sum_{t<3} w[c][r][s][t]
+ *                 * X[n, 2i+r-1, 2j+s-1, t] + bias[c])     (zero outside X)
+ *   x [N][Hin][Win][3]; y [N][ceil(Hin/2)][ceil(Win/2)][C]
+ *   w [C][3][3][3]: torch's conv weight [C][3][3][3] permuted (0, 2, 3, 1),
+ *   the paper's [K][R][S][T] order; scale, bias fp32 [C] (NULL: 1, 0).
+ * C = 16, 24 or 32, the paper's three stem widths (another multiple of 8
+ * returns CF_ERR_UNSUPPORTED, C not a multiple of 8 CF_ERR_INVALID).  fp16 or
+ * bf16, fp32 accumulation, output rounded once to the I/O dtype.  x and y
+ * must not overlap; pointers 16-byte aligned. */
+typedef struct {
+    const void *w;
+    const float *scale, *bias;
+} cf_stem_params;
+
+cf_status cf_stem_forward(const void *x, void *y, const cf_stem_params *p, int N, int Hin, int Win, int C,
+                          cf_dtype dt, void *stream);
+
+/* The stem fused into the first ConvFirst block, as App. A proposes:
+ * y = cf_gblock_forward(stem(x)) in one kernel.  Each block's halo of stem
+ * output is computed from the image on the matrix unit and kept in LDS, so
+ * the stem output never reaches memory; it is rounded to the I/O dtype as a
+ * stored one would be.  x [N][Hin][Win][3]; y [N][ceil(Hin/2)][ceil(Win/2)][C];
+ * blk as for cf_gblock_forward with this C, k = 3 and act (the paper's first
+ * block uses ReLU); C = 16 or 32 (the grouped block has no C = 24 kernel:
+ * its channel tiles are 16 wide; C = 24 returns CF_ERR_UNSUPPORTED). */
+cf_status cf_stem_gblock_forward(const void *x, void *y, const cf_stem_params *stem, const cf_gblock_params *blk,
+                                 int N, int Hin, int Win, int C, int E, int k, cf_dtype dt, cf_act act,
+                                 void *stream);
+
 /* The MBConv block with Squeeze & Excitation of Sec. 5.4 (Fig. f:mbconv:
  * the paper's variant with a grouped 3 x 3 conv of group width 8 in place of
  * the depth-wise one), fused into one kernel as Sec. 5.4.1 describes (Fig.

@@ -19,17 +19,17 @@ import torch
 
 from .convert import (block_params_from_modules, down_params_from_modules, down_weight_from_conv2d,
                       dw_weight_from_conv2d, fold_batchnorm, grouped_block_params_from_modules,
-                      grouped_weight_from_conv2d, pw_weight_from_conv2d)
+                      grouped_weight_from_conv2d, pw_weight_from_conv2d, stem_params_from_modules)
 
 __all__ = [
     "lib", "library_path", "block_forward", "block_autotune", "block_tuned_config", "stage_forward",
     "stage_forward_microbatch",
     "downsample_forward",
     "block_forward_unfused", "block_forward_split", "block_forward_split_noalloc", "gblock_forward",
-    "mbconv_forward", "mbconv_workspace_bytes", "stack_forward", "capture_stack", "ConvFirstBlock",
+    "mbconv_forward", "mbconv_workspace_bytes", "stem_forward", "stem_gblock_forward", "stack_forward", "capture_stack", "ConvFirstBlock",
     "CFError", "EXPORTED_SYMBOLS", "dw_weight_from_conv2d", "grouped_weight_from_conv2d",
     "pw_weight_from_conv2d", "down_weight_from_conv2d", "fold_batchnorm", "block_params_from_modules",
-    "grouped_block_params_from_modules", "down_params_from_modules",
+    "grouped_block_params_from_modules", "down_params_from_modules", "stem_params_from_modules",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -44,7 +44,7 @@ EXPORTED_SYMBOLS = (
     "cf_stage_microbatch_workspace_bytes", "cf_downsample_forward",
     "cf_block_forward_unfused", "cf_unfused_workspace_bytes", "cf_block_forward_split",
     "cf_split_workspace_bytes", "cf_block_forward_split_noalloc", "cf_gblock_forward", "cf_mbconv_forward",
-    "cf_mbconv_workspace_bytes", "cf_block_autotune",
+    "cf_mbconv_workspace_bytes", "cf_stem_forward", "cf_stem_gblock_forward", "cf_block_autotune",
     "cf_block_tuned_config", "cf_last_error", "cf_status_string", "cf_abi_version",
 )
 
@@ -63,6 +63,10 @@ class _BlockParams(ctypes.Structure):
 class _GBlockParams(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
                 ("gw_w", "gw_scale", "gw_bias", "w1", "s1", "b1", "w2", "s2", "b2")]
+
+
+class _StemParams(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("w", "scale", "bias")]
 
 
 class _MBConvParams(ctypes.Structure):
@@ -93,6 +97,7 @@ def lib():
         bp, dp = ctypes.POINTER(_BlockParams), ctypes.POINTER(_DownParams)
         gp = ctypes.POINTER(_GBlockParams)
         mp = ctypes.POINTER(_MBConvParams)
+        sp = ctypes.POINTER(_StemParams)
         sig = {
             "cf_block_forward": (i, [vp, vp, bp, i, i, i, i, i, i, i, i, vp]),
             "cf_stage_forward": (i, [vp, vp, vp, sz, bp, i, i, i, i, i, i, i, i, i, vp]),
@@ -108,6 +113,8 @@ def lib():
             "cf_gblock_forward": (i, [vp, vp, gp, i, i, i, i, i, i, i, i, vp]),
             "cf_mbconv_forward": (i, [vp, vp, vp, sz, mp, i, i, i, i, i, i, i, i, i, vp]),
             "cf_mbconv_workspace_bytes": (sz, [i, i, i, i, i, i, i]),
+            "cf_stem_forward": (i, [vp, vp, sp, i, i, i, i, i, vp]),
+            "cf_stem_gblock_forward": (i, [vp, vp, sp, gp, i, i, i, i, i, i, i, i, vp]),
             "cf_block_autotune": (i, [vp, vp, bp, i, i, i, i, i, i, i, i, vp]),
             "cf_block_tuned_config": (i, [i, i, i, i, i, i, i, i]),
             "cf_last_error": (ctypes.c_char_p, []),
@@ -416,6 +423,83 @@ def gblock_forward(x: torch.Tensor, p: dict, act: str = "relu", out=None, stream
     y = _out(x, out)
     _check(lib().cf_gblock_forward(_ptr(x), _ptr(y), ctypes.byref(gp), N, H, W, C, EC // C, k,
                                    DTYPES[x.dtype], ACTS[act], _stream(stream)))
+    return y
+
+
+def _stem_struct(x: torch.Tensor, stem: dict, C: int):
+    """The checked stem parameters (sw [C,3,3,3] in x's dtype, ss, sb fp32 [C])."""
+    if not isinstance(stem.get("sw"), torch.Tensor):
+        raise ValueError("stem parameter sw is required")
+    unknown = set(stem) - {"sw", "ss", "sb"}
+    if unknown:
+        raise ValueError("unknown stem parameters: %s" % sorted(unknown))
+    _check_tensor("sw", stem["sw"], (C, 3, 3, 3), x.dtype, x.device)
+    for key in ("ss", "sb"):
+        if stem.get(key) is not None:
+            _check_tensor(key, stem[key], (C,), torch.float32, x.device)
+    return _StemParams(w=stem["sw"].data_ptr(), scale=_ptr_val(stem.get("ss")), bias=_ptr_val(stem.get("sb")))
+
+
+def _ptr_val(t):
+    return None if t is None else t.data_ptr()
+
+
+def _image_dims(x: torch.Tensor):
+    N, H, W, C = _dims(x)
+    if C != 3:
+        raise ValueError("the stem's input must be an image [N, H, W, 3]")
+    return N, H, W
+
+
+def stem_forward(x: torch.Tensor, stem: dict, out=None, stream=None) -> torch.Tensor:
+    """The network stem (App. A): 3x3 stride-2 conv of the image x [N,H,W,3]
+    to C = 16 or 32 channels, folded norm, ReLU; stem holds sw [C,3,3,3] and
+    optional fp32 ss, sb [C].  Returns [N, ceil(H/2), ceil(W/2), C]."""
+    N, H, W = _image_dims(x)
+    if not isinstance(stem.get("sw"), torch.Tensor) or stem["sw"].dim() != 4:
+        raise ValueError("stem parameter sw [C, 3, 3, 3] is required")
+    C = int(stem["sw"].shape[0])
+    sp = _stem_struct(x, stem, C)
+    _check_device(x)
+    y = _out(x, out, (N, (H + 1) // 2, (W + 1) // 2, C))
+    _check(lib().cf_stem_forward(_ptr(x), _ptr(y), ctypes.byref(sp), N, H, W, C, DTYPES[x.dtype], _stream(stream)))
+    return y
+
+
+def stem_gblock_forward(x: torch.Tensor, stem: dict, p: dict, act: str = "relu", out=None,
+                        stream=None) -> torch.Tensor:
+    """The stem fused into the first ConvFirst block (App. A): one kernel
+    computing gblock_forward(stem_forward(x)); p as for gblock_forward with
+    C = 16 or 32."""
+    if act not in ACTS:
+        raise ValueError("act must be one of %s" % sorted(ACTS))
+    N, H, W = _image_dims(x)
+    if not isinstance(stem.get("sw"), torch.Tensor) or stem["sw"].dim() != 4:
+        raise ValueError("stem parameter sw [C, 3, 3, 3] is required")
+    C = int(stem["sw"].shape[0])
+    sp = _stem_struct(x, stem, C)
+    for key in ("gw_w", "w1", "w2"):
+        if not isinstance(p.get(key), torch.Tensor):
+            raise ValueError("grouped-block parameter %s is required" % key)
+    if p["gw_w"].dim() != 4 or p["w1"].dim() != 2:
+        raise ValueError("gw_w must be [k, k, C, 8] and w1 [E*C, C]")
+    k, EC = int(p["gw_w"].shape[0]), int(p["w1"].shape[0])
+    if EC % C or EC == 0:
+        raise ValueError("w1 rows must be a positive multiple of C")
+    unknown = set(p) - set(_GBLOCK_SHAPES)
+    if unknown:
+        raise ValueError("unknown grouped-block parameters: %s" % sorted(unknown))
+    vals = {}
+    for key, (shape_of, kind) in _GBLOCK_SHAPES.items():
+        t = p.get(key)
+        if t is not None:
+            _check_tensor(key, t, shape_of(C, EC, k), x.dtype if kind == "w" else torch.float32, x.device)
+        vals[_GFIELDS[key]] = _ptr_val(t)
+    gp = _GBlockParams(**vals)
+    _check_device(x)
+    y = _out(x, out, (N, (H + 1) // 2, (W + 1) // 2, C))
+    _check(lib().cf_stem_gblock_forward(_ptr(x), _ptr(y), ctypes.byref(sp), ctypes.byref(gp), N, H, W, C, EC // C, k,
+                                        DTYPES[x.dtype], ACTS[act], _stream(stream)))
     return y
 
 

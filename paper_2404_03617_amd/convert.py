@@ -134,6 +134,18 @@ def grouped_block_params_from_modules(conv: torch.nn.Conv2d, bn0, pw1, bn1, pw2,
     return p
 
 
+def stem_params_from_modules(conv: torch.nn.Conv2d, bn=None, dtype=torch.float16) -> dict:
+    """Parameters of cf_stem_forward / cf_stem_gblock_forward from the stem's
+    3 x 3 stride-2 conv (3 input channels, padding 1) and its BN: taps
+    [C][3][3][3] (torch [C][3][3][3] permuted (0, 2, 3, 1)), folded scale and bias."""
+    if (tuple(conv.weight.shape[1:]) != (3, 3, 3) or conv.stride not in ((2, 2), 2) or conv.groups != 1
+            or conv.padding not in ((1, 1), 1)):
+        raise ValueError("conv must be a 3x3 stride-2 conv from 3 channels with padding 1")
+    p = {"sw": conv.weight.detach().permute(0, 2, 3, 1).contiguous().to(dtype)}
+    p["ss"], p["sb"] = _pair(conv, bn, conv.weight.shape[0])
+    return p
+
+
 def down_params_from_modules(conv: torch.nn.Conv2d, bn=None, dtype=torch.float16) -> dict:
     """Parameters of cf_downsample_forward from a 2x2 stride-2 conv and its BN."""
     if tuple(conv.weight.shape[2:]) != (2, 2) or conv.stride not in ((2, 2), 2):

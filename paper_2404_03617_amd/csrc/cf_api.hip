@@ -218,6 +218,47 @@ hipError_t scratch_on_current_device(void **out) {
     return hipSuccess;
 }
 
+// Checks of the stem's own arguments (image x [N][Hin][Win][3], output
+// [N][ceil(Hin/2)][ceil(Win/2)][C] at y).
+cf_status check_stem(const char *what, const void *x, const void *y, const cf_stem_params *p, int N, int Hin,
+                     int Win, int C, cf_dtype dt) {
+    if (!x || !y)
+        return fail(CF_ERR_INVALID, "%s: x and y must be non-NULL", what);
+    if (!p || !p->w)
+        return fail(CF_ERR_INVALID, "%s: stem params and w must be non-NULL", what);
+    if (N <= 0 || Hin <= 0 || Win <= 0 || C <= 0)
+        return fail(CF_ERR_INVALID, "%s: sizes must be positive (N=%d Hin=%d Win=%d C=%d)", what, N, Hin, Win, C);
+    if (C % CF_GROUP_WIDTH)
+        return fail(CF_ERR_INVALID, "%s: C=%d is not a multiple of %d", what, C, CF_GROUP_WIDTH);
+    if ((int)dt != CF_F16 && (int)dt != CF_BF16)
+        return fail(CF_ERR_INVALID, "%s: unknown dtype %d", what, (int)dt);
+    const void *ptrs[] = {x, y, p->w, p->scale, p->bias};
+    for (const void *q : ptrs)
+        if (q && !aligned16(q))
+            return fail(CF_ERR_INVALID, "%s: every tensor pointer must be 16-byte aligned", what);
+    const double hs = (Hin + 1) / 2, ws = (Win + 1) / 2;
+    if ((double)N * Hin * Win * 3 > 4.0e12 || (double)N * hs * ws * C > 4.0e12)
+        return fail(CF_ERR_INVALID, "%s: tensor too large", what);
+    const size_t xb = (size_t)N * Hin * Win * 3 * elem_bytes(dt);
+    const size_t yb = (size_t)N * (size_t)hs * (size_t)ws * C * elem_bytes(dt);
+    if (overlap(x, xb, y, yb))
+        return fail(CF_ERR_INVALID, "%s: x and y overlap", what);
+    if ((double)N * hs * ws > 2147483647.0 - 4096.0 || (double)Hin * Win * 3 > 2147483647.0)
+        return fail(CF_ERR_UNSUPPORTED, "%s: image too large for 32-bit pixel offsets", what);
+    return CF_OK;
+}
+
+cf::StemW to_stem(const void *x, const cf_stem_params *p, int Hin, int Win) {
+    cf::StemW s;
+    s.x = x;
+    s.w = p->w;
+    s.s = p->scale;
+    s.b = p->bias;
+    s.Hin = Hin;
+    s.Win = Win;
+    return s;
+}
+
 }  // namespace
 
 extern "C" {
@@ -575,6 +616,65 @@ cf_status cf_gblock_forward(const void *x, void *y, const cf_gblock_params *p, i
     w.s2 = p->s2;
     w.b2 = p->b2;
     hipError_t e = cf::launch_gblock(x, y, w, to_shape(N, H, W, C, E, k, dt, act), (hipStream_t)stream);
+    if (e != hipSuccess)
+        return hip_fail(e, what);
+    g_err[0] = 0;
+    return CF_OK;
+}
+
+cf_status cf_stem_forward(const void *x, void *y, const cf_stem_params *p, int N, int Hin, int Win, int C,
+                          cf_dtype dt, void *stream) {
+    const char *what = "cf_stem_forward";
+    cf_status st = check_stem(what, x, y, p, N, Hin, Win, C, dt);
+    if (st != CF_OK)
+        return st;
+    if (C != 16 && C != 24 && C != 32)
+        return fail(CF_ERR_UNSUPPORTED, "%s: C=%d has no kernel (supported: 16, 24, 32)", what, C);
+    hipError_t e = cf::launch_stem(to_stem(x, p, Hin, Win), y, N, C, dt == CF_BF16, (hipStream_t)stream);
+    if (e != hipSuccess)
+        return hip_fail(e, what);
+    g_err[0] = 0;
+    return CF_OK;
+}
+
+cf_status cf_stem_gblock_forward(const void *x, void *y, const cf_stem_params *stem, const cf_gblock_params *p,
+                                 int N, int Hin, int Win, int C, int E, int k, cf_dtype dt, cf_act act,
+                                 void *stream) {
+    const char *what = "cf_stem_gblock_forward";
+    cf_status st = check_stem(what, x, y, stem, N, Hin, Win, C, dt);
+    if (st != CF_OK)
+        return st;
+    if (!p || !p->gw_w || !p->w1 || !p->w2)
+        return fail(CF_ERR_INVALID, "%s: block params, gw_w, w1 and w2 must be non-NULL", what);
+    if (E <= 0 || k <= 0 || k % 2 == 0 || k > 7)
+        return fail(CF_ERR_INVALID, "%s: E must be positive and k odd up to 7 (E=%d k=%d)", what, E, k);
+    if ((int)act != CF_ACT_GELU_ERF && (int)act != CF_ACT_RELU && (int)act != CF_ACT_NONE)
+        return fail(CF_ERR_INVALID, "%s: unknown activation %d", what, (int)act);
+    if ((double)E * C > 65536.0)
+        return fail(CF_ERR_INVALID, "%s: tensor too large", what);
+    const void *ptrs[] = {p->gw_w, p->w1, p->w2, p->gw_scale, p->gw_bias, p->s1, p->b1, p->s2, p->b2};
+    for (const void *q : ptrs)
+        if (q && !aligned16(q))
+            return fail(CF_ERR_INVALID, "%s: every tensor pointer must be 16-byte aligned", what);
+    if (k != 3)
+        return fail(CF_ERR_UNSUPPORTED, "%s: k=%d has no kernel (supported: 3)", what, k);
+    if (C != 16 && C != 32)
+        return fail(CF_ERR_UNSUPPORTED, "%s: C=%d has no kernel (supported: 16, 32)", what, C);
+    const int Hs = (Hin + 1) / 2, Ws = (Win + 1) / 2;
+    if ((double)Ws * C * 6.0 > 2147483647.0)
+        return fail(CF_ERR_UNSUPPORTED, "%s: image too wide", what);
+    cf::GBlockW w;
+    w.gw = p->gw_w;
+    w.s0 = p->gw_scale;
+    w.b0 = p->gw_bias;
+    w.w1 = p->w1;
+    w.s1 = p->s1;
+    w.b1 = p->b1;
+    w.w2 = p->w2;
+    w.s2 = p->s2;
+    w.b2 = p->b2;
+    hipError_t e = cf::launch_stem_gblock(to_stem(x, stem, Hin, Win), y, w, to_shape(N, Hs, Ws, C, E, k, dt, act),
+                                          (hipStream_t)stream);
     if (e != hipSuccess)
         return hip_fail(e, what);
     g_err[0] = 0;

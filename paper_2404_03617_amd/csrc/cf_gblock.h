@@ -85,6 +85,13 @@ struct Args {
     int rbase, rextra;              // rounds (NW blocks) per workgroup: rbase, +1 for the first rextra
     int xcd_map;                    // 1: workgroup i takes range (i % 8) * (G / 8) + i / 8
     uint32_t off_halo;              // LDS offset of the halo regions (after the weights)
+    // the network stem in front of the block (STEM kernels): x is then the
+    // stem output, computed per halo from the image and never stored
+    const uint16_t *xs;             // image [N][Hin][Win][3]
+    const uint16_t *sw;             // stem taps [C][3][3][3]
+    const float *ss, *sb;           // stem scale, bias (NULL: 1, 0)
+    int Hin, Win;
+    uint32_t off_stage;             // LDS offset of the waves' image windows (STEM)
 };
 
 __device__ __forceinline__ u32x4 lds16(const uint8_t *base, uint32_t off) {
@@ -92,6 +99,76 @@ __device__ __forceinline__ u32x4 lds16(const uint8_t *base, uint32_t off) {
 }
 __device__ __forceinline__ void sts16(uint8_t *base, uint32_t off, const u32x4 &v) {
     *reinterpret_cast<u32x4 *>(base + off) = v;
+}
+
+// The image window a block's halo needs: rows 2 r0 - 3 .. 2 r0 + 9, columns
+// 2 c0 - 3 .. 2 c0 + 33 (13 x 37 pixels), staged in LDS as 4 values a pixel
+// (the 3 channels and a zero) with a 38th, zero pixel closing each row.  The
+// fused kernel orders the stem's K for that layout: slot (tap row kh, tap
+// column pair kw0 = 0 or 2, channel 0..3) -- 6 slices of 8, K = 64 in two
+// products -- so a B fragment is one 16-byte read of two staged pixels (the
+// slots of tap column 3 and channel 3 have zero weights).
+constexpr int SWR = 2 * HR + 1, SWP = 2 * HC + 1;       // 13 rows, 37 pixels
+constexpr int SWPIX = SWR * SWP;                         // 481
+constexpr int SWL = (SWPIX + 63) / 64;                   // window pixels per lane
+constexpr int SPITCH = (SWP + 1) * 8;                    // 304 bytes a staged row (a multiple of 16)
+constexpr int STG = 4096;                                // LDS bytes of a wave's window (>= SWR SPITCH)
+
+// A fragment of output channel o (taps [o][3][3][3]) for product m, K slice q
+// of the staged-pixel order above (the stem kernel alone uses the same order,
+// so both round the stem output alike).
+__device__ __forceinline__ u32x4 stem_afrag_px(const uint16_t *sw, int o, int m, int q) {
+    const int sl = 4 * m + q;
+    uint32_t e[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+    if (sl < 6) {
+        const int kh = sl >> 1, kw0 = 2 * (sl & 1);
+#pragma unroll
+        for (int j = 0; j < 8; j++) {
+            const int kw = kw0 + j / 4, ci = j % 4;
+            if (ci < 3 && kw < 3)
+                e[j] = sw[(size_t)o * 27 + (kh * 3 + kw) * 3 + ci];
+        }
+    }
+    return u32x4{e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16), e[6] | (e[7] << 16)};
+}
+
+// A fragment of output channel o (taps [o][3][3][3]) for K slice q.
+__device__ __forceinline__ u32x4 stem_afrag(const uint16_t *sw, int o, int q) {
+    const uint16_t *wo = sw + (size_t)o * 27;
+    uint32_t e[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+    if (q < 3) {
+#pragma unroll
+        for (int j = 0; j < 8; j++)
+            e[j] = wo[9 * q + j];
+    } else {
+        e[0] = wo[8];
+        e[1] = wo[17];
+        e[2] = wo[26];
+    }
+    return u32x4{e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16), e[6] | (e[7] << 16)};
+}
+
+// The B fragment of output pixel (sr, sc) for product m, K slice q of that
+// order, gathered from the image (zero outside it); the stem kernel alone.
+__device__ __forceinline__ u32x4 stem_bfrag_px(const uint16_t *img, int Hin, int Win, int sr, int sc, int m, int q,
+                                              bool in) {
+    const int sl = 4 * m + q;
+    uint32_t e[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+    if (in && sl < 6) {
+        const int ir = 2 * sr - 1 + (sl >> 1);
+        if (ir >= 0 && ir < Hin) {
+#pragma unroll
+            for (int pp = 0; pp < 2; pp++) {
+                const int ic = 2 * sc - 1 + 2 * (sl & 1) + pp;
+                if (ic >= 0 && ic < Win) {
+#pragma unroll
+                    for (int ci = 0; ci < 3; ci++)
+                        e[4 * pp + ci] = img[((size_t)ir * Win + ic) * 3 + ci];
+                }
+            }
+        }
+    }
+    return u32x4{e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16), e[6] | (e[7] << 16)};
 }
 
 template <int C>
@@ -127,7 +204,7 @@ inline size_t lds_bytes(int nch, bool resident) {
     return (size_t)G::OFF_W + (size_t)(resident ? nch : 2) * G::CHB + (size_t)nw_for(C) * G::HALO;
 }
 
-template <int C, int NW, typename T, int ACT, bool RES>
+template <int C, int NW, typename T, int ACT, bool RES, bool STEM = false>
 struct GB {
     using G = Geo<C>;
     static constexpr int NT = NW * 64;
@@ -136,6 +213,10 @@ struct GB {
     static constexpr int HPIECES = G::HPIECES, HPL = G::HPL, HSTEPS = G::HSTEPS, CPIECES = G::CPIECES;
     static constexpr bool PREF2 = G::PREF2;
     static constexpr int CPT = (CPIECES + NT - 1) / NT;
+    static constexpr int STT = (HPIX + 15) / 16;  // stem: 16-pixel MFMA tiles of a halo
+    static constexpr int SMT = C / 16;            // stem: 16-channel output tiles
+    static constexpr int HVN = STEM ? 1 : (PREF2 ? HPL : 1);
+    static_assert(!STEM || PREF2, "the stem path prefetches one block ahead");
     // ReLU and identity: s1 is folded into the staged W1 rows and b1 starts
     // the expand accumulators, so the activation is a packed convert (and a
     // packed max); GELU applies s1, b1 and erf in fp32
@@ -278,6 +359,97 @@ struct GB {
         }
     }
 
+    // ---- the stem (STEM kernels).  The halo of a block is computed from the
+    // image instead of read: halo pixel px of the 6 x 18 window is stem output
+    // (sr, sc) = (r0 - 1 + px / 18, c0 - 1 + px % 18), one B column of the
+    // stem products (the staged-pixel K order).  The image window is read one
+    // block ahead into registers and staged in the wave's LDS window when the
+    // halo is due.
+    // the lane's pixels i = 64 u + lane of block k's image window, read as
+    // they lie in memory: v[u] the aligned 32-bit word holding two of the
+    // pixel's three values, h[u] the third one.  Bit u of m says the pixel
+    // lies in the image (else pixel 0 of the image is read in its place), bit
+    // 8 + u that its first element index is odd (the word then holds channels
+    // 1, 2).  Nothing here waits for the loads (no branch, no use of a loaded
+    // value): stem_store puts the values together a block later
+    static __device__ __forceinline__ void stem_load(const Args &a, const Blk &k, int lane, uint32_t (&v)[SWL],
+                                                     uint16_t (&h)[SWL], uint32_t &m) {
+        const uint16_t *img = a.xs + (size_t)k.n * a.Hin * a.Win * 3;
+        const int row0 = 2 * k.r0 - 3, col0 = 2 * k.c0 - 3;
+        const int par0 = k.n & a.Hin & a.Win & 1;  // parity of the image's first element index
+        m = 0u;
+#pragma unroll
+        for (int u = 0; u < SWL; u++) {
+            const int i = u * 64 + lane;
+            const int rr = i / SWP, pc = i - rr * SWP;
+            const int ir = row0 + rr, ic = col0 + pc;
+            const bool in = k.valid & (i < SWPIX) & ((unsigned)ir < (unsigned)a.Hin) & ((unsigned)ic < (unsigned)a.Win);
+            const int pix = in ? ir * a.Win + ic : 0;
+            const int odd = (par0 ^ pix) & 1;
+            const uint16_t *e = img + (size_t)pix * 3;
+            v[u] = *reinterpret_cast<const uint32_t *>(e + odd);
+            h[u] = e[2 - 2 * odd];
+            m |= (in ? 1u : 0u) << u | (uint32_t)odd << (8 + u);
+        }
+    }
+    // stages block k's window (this wave only: its LDS operations run in
+    // order), runs the two products of each 16-pixel halo tile from it,
+    // applies s, b and ReLU, zeroes pixels outside the stem output (the
+    // block's padding) and writes the halo region as the block's loads would
+    // have
+    static __device__ __forceinline__ void stem_store(uint8_t *reg, uint8_t *stage, const Args &a, const Blk &k,
+                                                      int lane, const uint32_t (&v)[SWL], const uint16_t (&h)[SWL], uint32_t m,
+                                                      const u32x4 (&sa)[SMT][2], const float4v (&ssv)[SMT],
+                                                      const float4v (&sbv)[SMT]) {
+        const int q = lane >> 4, jl = lane & 15;
+#pragma unroll
+        for (int u = 0; u < SWL; u++) {
+            const int i = u * 64 + lane;
+            const int rr = i / SWP, pc = i - rr * SWP;
+            // channels 0, 1 | channel 2, zero; zero outside the image
+            const bool in = (m >> u) & 1u, odd = (m >> (8 + u)) & 1u;
+            const uint32_t w0 = odd ? ((uint32_t)h[u] | (v[u] << 16)) : v[u];
+            const uint32_t w1 = odd ? (v[u] >> 16) : (uint32_t)h[u];
+            if (i < SWPIX)
+                *reinterpret_cast<u32x2 *>(stage + (uint32_t)rr * SPITCH + (uint32_t)pc * 8) =
+                    u32x2{in ? w0 : 0u, in ? w1 : 0u};
+        }
+        // every tile's B fragments first, so the reads overlap the products
+        u32x4 bv[STT][2];
+#pragma unroll
+        for (int t = 0; t < STT; t++) {
+            const int px = 16 * t + jl;
+            const int hr = px / HC, hc = px - hr * HC;
+#pragma unroll
+            for (int m = 0; m < 2; m++) {
+                const int sl = 4 * m + q;  // slot slice: tap row sl / 2, tap columns 2 (sl % 2) and +1
+                bv[t][m] = (sl < 6 && px < HPIX)
+                               ? *reinterpret_cast<const u32x4 *>(stage + (uint32_t)(2 * hr + (sl >> 1)) * SPITCH +
+                                                                  (uint32_t)(2 * hc + 2 * (sl & 1)) * 8)
+                               : u32x4{0u, 0u, 0u, 0u};
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < STT; t++) {
+            const int px = 16 * t + jl;
+            const int hr = px / HC, hc = px - hr * HC;
+            const int sr = k.r0 - 1 + hr, sc = k.c0 - 1 + hc;
+            const bool in = k.valid & (px < HPIX) & ((unsigned)sr < (unsigned)a.H) & ((unsigned)sc < (unsigned)a.W);
+#pragma unroll
+            for (int mt = 0; mt < SMT; mt++) {
+                float4v acc = T::mfma(sa[mt][0], bv[t][0], float4v{0.f, 0.f, 0.f, 0.f});
+                acc = T::mfma(sa[mt][1], bv[t][1], acc);
+                float uu[4];
+#pragma unroll
+                for (int e4 = 0; e4 < 4; e4++)
+                    uu[e4] = in ? fmaxf(fmaf(acc[e4], ssv[mt][e4], sbv[mt][e4]), 0.0f) : 0.0f;
+                if (px < HPIX)
+                    *reinterpret_cast<u32x2 *>(reg + (uint32_t)px * PB + (uint32_t)(16 * mt + 4 * q) * 2) =
+                        u32x2{T::pack2(uu[0], uu[1]), T::pack2(uu[2], uu[3])};
+            }
+        }
+    }
+
     static __device__ __forceinline__ float act(float u) {
         if constexpr (ACT == ACT_RELU)
             return fmaxf(u, 0.0f);
@@ -332,9 +504,38 @@ struct GB {
             chunk_store(wts, tid, cA);
             chunk_load(a, pref, a.nch > 1 ? 1 : 0, cA);
         }
+        // stem (STEM kernels): the lane's A fragments (output channel 16 mt +
+        // jl, K slice q as in stem_load) and the scale/bias of its D rows
+        u32x4 sa[STEM ? SMT : 1][2];
+        float4v ssv[STEM ? SMT : 1], sbv[STEM ? SMT : 1];
+        if constexpr (STEM) {
+            // the wave's window: its pad slots (the 38th pixel of a row) stay zero
+            for (int i = lane; i < STG / 16; i += 64)
+                *reinterpret_cast<u32x4 *>(smem + a.off_stage + wv * STG + i * 16) = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int mt = 0; mt < SMT; mt++) {
+                sa[mt][0] = stem_afrag_px(a.sw, 16 * mt + jl, 0, q);
+                sa[mt][1] = stem_afrag_px(a.sw, 16 * mt + jl, 1, q);
+#pragma unroll
+                for (int e4 = 0; e4 < 4; e4++) {
+                    const int c = 16 * mt + 4 * q + e4;
+                    ssv[mt][e4] = a.ss ? a.ss[c] : 1.0f;
+                    sbv[mt][e4] = a.sb ? a.sb[c] : 0.0f;
+                }
+            }
+        }
         // halo of the first block; with PREF2 the second block's waits in registers
-        u32x4 hv[PREF2 ? HPL : 1];
-        {
+        u32x4 hv[HVN];
+        uint32_t hs[STEM ? SWL : 1], hm = 0u;
+        uint16_t hh[STEM ? SWL : 1];
+        uint8_t *stage = smem + a.off_stage + wv * STG;
+        if constexpr (STEM) {
+            const Blk k0 = decode(a, rstart * NW + wv);
+            stem_load(a, k0, lane, hs, hh, hm);
+            stem_store(reg, stage, a, k0, lane, hs, hh, hm, sa, ssv, sbv);
+            if (nr > 1)
+                stem_load(a, decode(a, (rstart + 1) * NW + wv), lane, hs, hh, hm);
+        } else {
             const HaloCtx h0 = halo_ctx(a, decode(a, rstart * NW + wv));
             for (int s = 0; s < HSTEPS; s++) {
                 u32x4 v[HSTEP];
@@ -413,7 +614,14 @@ struct GB {
 #pragma unroll
                 for (int mo = 0; mo < MO; mo++)
                     acc[nt][mo] = float4v{0.f, 0.f, 0.f, 0.f};
-            if constexpr (PREF2) {
+            if constexpr (STEM) {
+                // the region is free: block r+1's stem output in, block r+2's
+                // image fragments out
+                if (r + 1 < nr)
+                    stem_store(reg, stage, a, decode(a, (rstart + r + 1) * NW + wv), lane, hs, hh, hm, sa, ssv, sbv);
+                if (r + 2 < nr)
+                    stem_load(a, decode(a, (rstart + r + 2) * NW + wv), lane, hs, hh, hm);
+            } else if constexpr (PREF2) {
                 // the region is free: block r+1's halo in, block r+2's loads out
                 if (r + 1 < nr)
                     halo_store<HPL>(reg, 0, lane, hv);
@@ -565,16 +773,27 @@ struct GB {
     }
 };
 
-template <int C, int NW, typename T, int ACT, bool RES>
+template <int C, int NW, typename T, int ACT, bool RES, bool STEM = false>
 __global__ __launch_bounds__(NW * 64, 1) void gblock_kernel(Args a) {
     extern __shared__ __attribute__((aligned(256))) uint8_t smem[];
-    GB<C, NW, T, ACT, RES>::run(a, smem);
+    GB<C, NW, T, ACT, RES, STEM>::run(a, smem);
 }
 
-template <int C>
-hipError_t launch_c(const void *x, void *y, const GBlockW &w, const Shape &s, hipStream_t st) {
+// The grouped block on x, or (STEM) the stem and the block on the image
+// stem->x; s describes the block (its H, W are the stem output's).
+template <int C, bool STEM = false>
+hipError_t launch_c(const void *x, void *y, const GBlockW &w, const Shape &s, hipStream_t st,
+                    const StemW *stem = nullptr) {
     constexpr int NW = nw_for(C);
     Args a{};
+    if constexpr (STEM) {
+        a.xs = (const uint16_t *)stem->x;
+        a.sw = (const uint16_t *)stem->w;
+        a.ss = stem->s;
+        a.sb = stem->b;
+        a.Hin = stem->Hin;
+        a.Win = stem->Win;
+    }
     a.x = (const uint16_t *)x;
     a.y = (uint16_t *)y;
     a.gw = (const uint16_t *)w.gw;
@@ -602,16 +821,18 @@ hipError_t launch_c(const void *x, void *y, const GBlockW &w, const Shape &s, hi
     a.rbase = rounds / Gn;
     a.rextra = rounds % Gn;
     a.xcd_map = (Gn % 8 == 0) ? 1 : 0;
-    const size_t lds_res = lds_bytes<C>(a.nch, true);
+    const size_t stg = STEM ? (size_t)NW * STG : 0;  // the waves' image windows, after the halos
+    const size_t lds_res = lds_bytes<C>(a.nch, true) + stg;
     const bool res = lds_res <= 160 * 1024;
-    const size_t lds = res ? lds_res : lds_bytes<C>(a.nch, false);
+    const size_t lds = res ? lds_res : lds_bytes<C>(a.nch, false) + stg;
     if (lds > 160 * 1024)
         return hipErrorInvalidConfiguration;
-    a.off_halo = (uint32_t)(lds - (size_t)NW * Geo<C>::HALO);
+    a.off_stage = (uint32_t)(lds - stg);
+    a.off_halo = (uint32_t)(lds - stg - (size_t)NW * Geo<C>::HALO);
     hipError_t e;
 #define CF_GB_LAUNCH(TT, AC)                                                                          \
     {                                                                                                 \
-        auto kf = res ? gblock_kernel<C, NW, TT, AC, true> : gblock_kernel<C, NW, TT, AC, false>;     \
+        auto kf = res ? gblock_kernel<C, NW, TT, AC, true, STEM> : gblock_kernel<C, NW, TT, AC, false, STEM>; \
         if ((e = allow_full_lds((const void *)kf)) != hipSuccess)                                     \
             return e;                                                                                 \
         hipLaunchKernelGGL(kf, dim3(Gn), dim3(NW * 64), lds, st, a);                                  \

@@ -95,8 +95,21 @@ struct GBlockW {
     const void *w2;
     const float *s2, *b2;
 };
+// The network stem in front of a grouped block: 3 x 3 stride-2 conv of the
+// image x [N][Hin][Win][3] with taps w [C][3][3][3], scale/bias, ReLU.
+struct StemW {
+    const void *x;
+    const void *w;
+    const float *s, *b;
+    int Hin, Win;
+};
 // Channel counts with a kernel: multiples of 16 from 16 to 112.
 bool gblock_supported_c(int C);
+// Stem + grouped block in one kernel (C = 16 or 32); s describes the block
+// (H, W of the stem output).  hipErrorInvalidValue for another C.
+hipError_t launch_stem_gblock(const StemW &stem, void *y, const GBlockW &w, const Shape &s, hipStream_t st);
+// The stem alone: y [N][ceil(Hin/2)][ceil(Win/2)][C] (C = 16 or 32).
+hipError_t launch_stem(const StemW &stem, void *y, int N, int C, int bf16, hipStream_t st);
 // Fused grouped block; hipErrorInvalidValue for an unsupported C.
 hipError_t launch_gblock(const void *x, void *y, const GBlockW &w, const Shape &s, hipStream_t st);
 

@@ -48,6 +48,19 @@ def gblock_bytes_fused(N, H, W, C, E, k=3, gw=8, eb=2) -> int:
     return 2 * N * H * W * C * eb + eb * (k * k * gw * C + 2 * E * C * C) + 4 * (4 * C + 2 * E * C)
 
 
+def stem_flops(N, Hin, Win, C) -> int:
+    """The stem: 2 * 27 * C per output pixel (App. A's Conv column: 14.16 M
+    per image at 256 x 256 -> 128 x 128, C = 16)."""
+    return N * ((Hin + 1) // 2) * ((Win + 1) // 2) * 2 * 27 * C
+
+
+def stem_gblock_bytes_fused(N, Hin, Win, C, E, k=3, gw=8, eb=2) -> int:
+    """Image read once, block output written once, weights once."""
+    Hs, Ws = (Hin + 1) // 2, (Win + 1) // 2
+    return (N * Hin * Win * 3 + N * Hs * Ws * C) * eb + eb * (27 * C + k * k * gw * C + 2 * E * C * C) + \
+        4 * (2 * C + 4 * C + 2 * E * C)
+
+
 def mbconv_flops(N, H, W, C, E, R, k=3, gw=8) -> int:
     """MBConv + SE (Sec. 5.4): expand 2 P E C^2, grouped conv 2 P E C k^2 gw,
     squeeze and excitation 4 E C R per image, project 2 P E C^2 -- the

@@ -97,6 +97,18 @@ def gblock_params(seed: int, layer: int, C: int, E: int, k: int = 3, dtype: str 
     return p
 
 
+def stem_params(seed: int, layer: int, C: int, dtype: str = "f16", scales: str = "ones",
+                bias_std: float | None = 0.1) -> dict:
+    """The network stem (3x3 stride-2 conv from 3 channels): taps [C, 3, 3, 3]
+    ~ N(0, 1/27) (fan-in 27), ids 100*(layer+1) + 0..2."""
+    base = 100 * (layer + 1)
+    return {
+        "sw": to_io(draw(seed, base + 0, (C, 3, 3, 3), (1.0 / 27) ** 0.5), dtype),
+        "ss": _vec(seed, base + 1, C, "scale", bias_std, scales),
+        "sb": _vec(seed, base + 2, C, "bias", bias_std, scales),
+    }
+
+
 def mbconv_params(seed: int, layer: int, C: int, E: int, R: int, dtype: str = "f16",
                   scales: str = "ones", bias_std: float | None = 0.1, gw: int = 8) -> dict:
     """Weights of one MBConv block with Squeeze & Excitation (expand, grouped

@@ -54,3 +54,14 @@ MBCONV_WORKLOADS = {
         (256, 16, 51.0, 8.01), (128, 8, 45.0, 0.64), (144, 8, 32.5, 1.09), (160, 8, 31.3, 1.37),
         (192, 8, 43.1, 1.39), (256, 8, 51.4, 1.99)])
 }
+
+# The network stem (a 3x3 stride-2 conv from the 256 x 256 image's 3 channels,
+# ReLU) fused into the first ConvFirst block at 128 x 128 (App. A, the first two
+# rows of the speed-projection tables: the Pico stem 3 -> 16 before ConvFirst
+# C = 16, alpha = 3; the 3 -> 32 stem before ConvFirst C = 32, alpha = 3), batch
+# 128, fp16, ReLU.  The image is seed-drawn N(0, 1).
+STEM_WORKLOADS = {
+    "stem_gblock_n128_256x256_c%d_e3_f16" % c: dict(kind="stem_gblock", N=128, Hin=256, Win=256, C=c, E=3, k=3,
+                                                    dtype="f16", act="relu", seed=60 + i)
+    for i, c in enumerate([16, 32])
+}

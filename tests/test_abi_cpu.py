@@ -428,3 +428,38 @@ def test_mbconv_forward_rejects():
     assert call(ws_bytes=n - 1) == cf.CF_ERR_WORKSPACE
     assert call(ws=None, ws_bytes=0) == cf.CF_ERR_WORKSPACE
     assert L.cf_last_error().decode().startswith("cf_mbconv_forward")
+
+
+def test_stem_entry_points_reject():
+    """The stem and the stem + first block: every check happens on the host."""
+    L = cf.lib()
+    SW, GW = 0x46000000, 0x43000000
+
+    def stem(x=X, y=Y, w=SW, N=2, Hin=16, Win=16, C=16, dt=0, **kw):
+        p = cf._StemParams(w=w, scale=None, bias=None)
+        for f, v in kw.items():
+            setattr(p, f, v)
+        return L.cf_stem_forward(x, y, ctypes.byref(p), N, Hin, Win, C, dt, None)
+
+    def fused(x=X, y=Y, w=SW, gw=GW, N=2, Hin=16, Win=16, C=16, E=3, k=3, dt=0, act=1):
+        sp = cf._StemParams(w=w, scale=None, bias=None)
+        gp = cf._GBlockParams(gw_w=gw, gw_scale=None, gw_bias=None, w1=W1, s1=None, b1=None, w2=W2, s2=None, b2=None)
+        return L.cf_stem_gblock_forward(x, y, ctypes.byref(sp), ctypes.byref(gp), N, Hin, Win, C, E, k, dt, act, None)
+
+    assert stem(x=None) == cf.CF_ERR_INVALID
+    assert stem(w=None) == cf.CF_ERR_INVALID
+    assert stem(Hin=0) == cf.CF_ERR_INVALID
+    assert stem(C=20) == cf.CF_ERR_INVALID            # not a multiple of 8
+    assert stem(dt=3) == cf.CF_ERR_INVALID
+    assert stem(y=X + 64) == cf.CF_ERR_INVALID        # overlaps the image
+    assert stem(scale=W1 + 4) == cf.CF_ERR_INVALID    # misaligned
+    assert stem(C=64) == cf.CF_ERR_UNSUPPORTED
+    assert stem(C=40) == cf.CF_ERR_UNSUPPORTED
+    assert L.cf_last_error().decode().startswith("cf_stem_forward")
+    assert fused(gw=None) == cf.CF_ERR_INVALID
+    assert fused(E=0) == cf.CF_ERR_INVALID
+    assert fused(k=4) == cf.CF_ERR_INVALID
+    assert fused(act=7) == cf.CF_ERR_INVALID
+    assert fused(C=24) == cf.CF_ERR_UNSUPPORTED        # a paper stem width without a block kernel
+    assert fused(k=5) == cf.CF_ERR_UNSUPPORTED
+    assert L.cf_last_error().decode().startswith("cf_stem_gblock_forward")
