@@ -183,6 +183,23 @@ def test_downsample_from_torch_modules_matches_the_modules():
     np.testing.assert_allclose(got, ref, rtol=0, atol=1e-5 * np.abs(ref).max())
 
 
+def test_stem_from_torch_modules_matches_the_modules():
+    """The stem conv (3 -> 24, 3x3, stride 2, padding 1) with its BN and ReLU,
+    on an odd-sized image, against the oracle on the converted parameters."""
+    conv = _rand_conv(nn.Conv2d(3, 24, 3, stride=2, padding=1, bias=True).double(), 31)
+    bn = _bn(24, 32)
+    x = torch.randn(2, 3, 9, 12, dtype=torch.float64, generator=torch.Generator().manual_seed(33))
+    with torch.no_grad():
+        ref = F.relu(bn(conv(x))).permute(0, 2, 3, 1).numpy()
+    p = cf.stem_params_from_modules(conv, bn, dtype=torch.float64)
+    assert tuple(p["sw"].shape) == (24, 3, 3, 3)
+    got = oracle.stem_forward(x.permute(0, 2, 3, 1).numpy(), p["sw"].numpy(), p["ss"].numpy(), p["sb"].numpy())
+    assert got.shape == (2, 5, 6, 24)
+    np.testing.assert_allclose(got, ref, rtol=0, atol=1e-5 * np.abs(ref).max())
+    with pytest.raises(ValueError):
+        cf.stem_params_from_modules(nn.Conv2d(3, 16, 3, stride=1, padding=1))
+
+
 def test_fold_batchnorm_rejects_training_mode():
     with pytest.raises(ValueError):
         cf.fold_batchnorm(nn.BatchNorm2d(4))
