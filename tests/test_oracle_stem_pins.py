@@ -23,7 +23,7 @@ def torch_stem(x, w, s=None, b=None):
     return F.relu(u).permute(0, 2, 3, 1).numpy()
 
 
-@pytest.mark.parametrize("H,W,C", [(8, 8, 16), (7, 9, 16), (1, 1, 32), (2, 5, 16), (13, 6, 32)])
+@pytest.mark.parametrize("H,W,C", [(8, 8, 16), (7, 9, 16), (1, 1, 32), (2, 5, 16), (13, 6, 32), (11, 10, 24)])
 def test_stem_matches_torch(H, W, C):
     x = RNG.standard_normal((2, H, W, 3))
     w = RNG.standard_normal((C, 3, 3, 3)) / 5.0           # [K][R][S][T]
