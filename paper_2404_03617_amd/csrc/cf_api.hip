@@ -110,17 +110,12 @@ cf::Shape to_shape(int N, int H, int W, int C, int E, int k, cf_dtype dt, cf_act
     return s;
 }
 
-cf_status check_fit(const char *what, const cf::Shape &s) {
-    const size_t lds = cf::fused_lds_bytes(s);
-    if (lds > 0 && lds <= 160 * 1024)
+// slice_ok: the caller runs one hidden group, so the slice kernel may serve
+// a shape no tile kernel fits
+cf_status check_fit(const char *what, const cf::Shape &s, bool slice_ok = true) {
+    if (cf::tile_fits(s) || (slice_ok && cf::slice_applies(s)))
         return CF_OK;
-    // C = 512 in bf16 runs the single-group small kernel (one 128-pixel tile per
-    // workgroup) whenever its halo and D buffer fit
-    if (s.C == 512 && s.bf16) {
-        const size_t sl = cf::small_split_lds_bytes(s, true);
-        if (sl > 0 && sl <= 160 * 1024)
-            return CF_OK;
-    }
+    const size_t lds = cf::fused_lds_bytes(s);
     return fail(CF_ERR_UNSUPPORTED, "%s: tile for W=%d C=%d k=%d needs %zu bytes of LDS (limit 163840)", what, s.W,
                 s.C, s.k, lds);
 }
@@ -185,7 +180,7 @@ cf_status check_split(const char *what, const void *x, const void *y, const cf_b
     *need = (size_t)groups * N * H * W * C * sizeof(float);
     const cf::Shape s = to_shape(N, H, W, C, E, k, dt, act);
     const size_t small_lds = cf::small_split_lds_bytes(s);
-    if (!(small_lds > 0 && small_lds <= 160 * 1024) && (st = check_fit(what, s)) != CF_OK)
+    if (!(small_lds > 0 && small_lds <= 160 * 1024) && (st = check_fit(what, s, groups <= 1)) != CF_OK)
         return st;
     return CF_OK;
 }
@@ -355,7 +350,8 @@ cf_status cf_stage_forward(const void *x, void *y, void *ws, size_t ws_bytes, co
     // the workspace holds them
     int groups = 1;
     float *partial = nullptr;
-    const int g = stage_groups(N, H, W, C, E, dt);
+    // (a handful of pixels: the slice kernel, which needs no partials)
+    const int g = cf::slice_applies(s) ? 1 : stage_groups(N, H, W, C, E, dt);
     const size_t pbytes = (size_t)g * N * H * W * C * sizeof(float);
     if (g > 1 && ws && aligned16(ws) && ws_bytes >= need + pbytes &&
         !overlap((char *)ws + need, pbytes, x, bytes) && !overlap((char *)ws + need, pbytes, y, bytes)) {

@@ -118,6 +118,10 @@ hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Sha
             done = true;
         }
     }
+    // a handful of pixels: the slice kernel (no workspace) unless the
+    // autotuner chose the tile kernels (CFG_TILE) or the generic one
+    if (!done && groups <= 1 && s.cfg == CFG_DEFAULT && slice_applies(s))
+        return launch_slice(x, y, w, s, st);
     const bool special = s.cfg != CFG_GENERIC;
     // C = 512 in bf16 has no streaming kernel of its own: the single-group
     // small kernel (one workgroup per 128-pixel tile and 128 output channels,
@@ -177,11 +181,25 @@ hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Sha
     return hipGetLastError();
 }
 
+bool tile_fits(const Shape &s) {
+    const size_t lds = fused_lds_bytes(s);
+    if (lds > 0 && lds <= 160 * 1024)
+        return true;
+    // C = 512 in bf16 runs the single-group small kernel (one 128-pixel tile per
+    // workgroup) whenever its halo and D buffer fit
+    if (s.C == 512 && s.bf16) {
+        const size_t sl = small_split_lds_bytes(s, true);
+        return sl > 0 && sl <= 160 * 1024;
+    }
+    return false;
+}
+
 bool cfg_applies(const Shape &s, int cfg) {
     switch (cfg) {
     case CFG_DEFAULT: return true;
     case CFG_GENERIC: return fused_lds_bytes(s) > 0 && fused_lds_bytes(s) <= 160 * 1024;
     case CFG_HALF_TILE: return s.C == 64 && !s.bf16;
+    case CFG_TILE: return slice_applies(s) && tile_fits(s);
     default: return false;
     }
 }

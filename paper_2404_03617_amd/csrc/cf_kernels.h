@@ -53,10 +53,13 @@ enum {
     CFG_DEFAULT = 0,     // the shape's specialised kernel, full-size tiles
     CFG_GENERIC = 1,     // the generic fused kernel (cf_fused_impl.h)
     CFG_HALF_TILE = 2,   // C = 64 fp16 kernel with tiles of at most half the blocks
-    CFG_COUNT = 3
+    CFG_TILE = 3,        // N*H*W <= 64: the tile kernels where the default is the slice kernel
+    CFG_COUNT = 4
 };
 // Whether configuration cfg applies to shape s.
 bool cfg_applies(const Shape &s, int cfg);
+// Whether a tile kernel (every configuration but the slice kernel) fits the LDS for s.
+bool tile_fits(const Shape &s);
 
 // Fused block.  groups > 1 selects the hidden-split variant: partial (fp32,
 // [groups][N*H*W][C]) receives each group's projection and a reduction kernel
@@ -70,6 +73,13 @@ hipError_t launch_fused_block(const void *x, void *y, const BlockW &w, const Sha
 // hipErrorInvalidConfiguration when the shape does not suit it.
 hipError_t launch_small_split(const void *x, const BlockW &w, const Shape &s, int groups, float *partial,
                               hipStream_t st, void *y = nullptr);
+
+// Block for N*H*W <= 64 (C = 128, 256, 512) without a workspace: one
+// workgroup per 32 output channels, each recomputing the expand and summing
+// its waves' projections in LDS.  slice_applies tells whether the shape suits
+// it; launch_slice returns hipErrorInvalidConfiguration otherwise.
+bool slice_applies(const Shape &s);
+hipError_t launch_slice(const void *x, void *y, const BlockW &w, const Shape &s, hipStream_t st);
 
 // LDS bytes of the small-batch kernel for this shape; 0 when it does not apply.
 // direct: one hidden group writing y (no tile-count limit); otherwise the

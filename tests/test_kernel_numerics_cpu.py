@@ -127,3 +127,71 @@ def test_grouped_block_operation_count_reproduces_the_papers_table(row):
     got = rl.gblock_flops(128, H, W, C, E) / (ms * 1e-3) / 1e12
     assert got == pytest.approx(tflops, rel=0.02)
     assert tflops / 76.7 * 100 == pytest.approx(pct, abs=0.2)
+
+
+# ---- the slice kernel's fp32 GELU: erf by Abramowitz & Stegun 7.1.26
+SLICE_HIP = os.path.join(ROOT, "paper_2404_03617_amd", "csrc", "cf_slice.hip")
+AS_BOUND = 1.5e-7  # the published bound of 7.1.26 on |erf error|
+
+
+def slice_gelu_constants():
+    """(p, a5, a4, a3, a2, a1) as the kernel writes them, in Horner order."""
+    src = open(SLICE_HIP).read()
+    body = src[src.index("float gelu_as(float u)"):]
+    body = body[:body.index("\n}\n")]
+    nums = [float(v) for v in re.findall(r"(-?\d+\.\d+)f", body)]
+    # in source order: 1/sqrt(2), p, 1.0, a5, a4, a3, a2, a1, -log2(e), 1.0, 0.5
+    assert len(nums) == 11 and nums[2] == 1.0 and nums[9] == 1.0 and nums[10] == 0.5, nums
+    return [nums[0], nums[1], nums[3], nums[4], nums[5], nums[6], nums[7], -nums[8]]
+
+
+def f32(v):
+    return np.asarray(v, dtype=np.float64).astype(np.float32).astype(np.float64)
+
+
+def slice_gelu(u, nums):
+    """The kernel's sequence in float32 (each operation rounded once; the
+    reciprocal and exponential as correctly rounded float32 results)."""
+    r2, p, a5, a4, a3, a2, a1, l2e = [float(f32(v)) for v in nums[:8]]
+    u = f32(u)
+    x = f32(np.abs(u) * r2)
+    t = f32(1.0 / f32(p * x + 1.0))
+    q = f32(a5 * t + a4)
+    q = f32(q * t + a3)
+    q = f32(q * t + a2)
+    q = f32(q * t + a1)
+    q = f32(q * t)
+    e = f32(np.exp2(f32(f32(x * x) * -l2e)))
+    erf_x = f32(-q * e + 1.0)
+    hu = f32(0.5 * u)
+    return f32(hu * np.copysign(erf_x, u) + hu)
+
+
+def test_slice_gelu_constants_are_the_published_ones():
+    nums = slice_gelu_constants()
+    assert nums[:7] == [0.70710678118654752, 0.3275911, 1.061405429, -1.453152027, 1.421413741, -0.284496736,
+                        0.254829592]
+    assert abs(nums[7] - 1.4426950408889634) < 1e-15
+
+
+def _slice_gelu_max_error(nums):
+    u = np.concatenate([np.linspace(-12.0, 12.0, 480001), np.array([-1e4, -50.0, 50.0, 1e4, 1e-30, -1e-30, 0.0])])
+    got = slice_gelu(u, nums)
+    ref = exact_gelu(u)
+    return np.max(np.abs(got - ref) / np.maximum(1.0, np.abs(u)))
+
+
+def test_slice_gelu_meets_the_erf_bound():
+    """|GELU_kernel(u) - u Phi(u)| <= (0.5 * 1.5e-7 + float32 rounding) * max(1, |u|)."""
+    err = _slice_gelu_max_error(slice_gelu_constants())
+    assert err < 3e-7, err
+
+
+def test_slice_gelu_bound_catches_a_wrong_coefficient():
+    nums = slice_gelu_constants()
+    bad = list(nums)
+    bad[2] *= 1.001  # a5
+    assert _slice_gelu_max_error(bad) > 3e-7
+    bad = list(nums)
+    bad[1] = 0.33  # p
+    assert _slice_gelu_max_error(bad) > 3e-7
