@@ -61,7 +61,8 @@ typedef enum { CF_F16 = 0, CF_BF16 = 1 } cf_dtype;
  * Gaussian-CDF form u * Phi(u).  The fused fp16 kernels evaluate it with a
  * packed-fp16 polynomial whose absolute error is below 3.4e-3 for |u| < 10
  * and zero beyond (it saturates to 0 and u); the fused bf16 kernels and the
- * layer-by-layer kernels use fp32 erf.
+ * layer-by-layer kernels use fp32 erf, the kernel for N*H*W <= 64 the fp32
+ * erf of Abramowitz & Stegun 7.1.26 (|error| <= 1.5e-7).
  * CF_ACT_NONE makes the block affine (used by tests). */
 typedef enum { CF_ACT_GELU_ERF = 0, CF_ACT_RELU = 1, CF_ACT_NONE = 2 } cf_act;
 
@@ -87,7 +88,11 @@ typedef struct {
 
 /* One ConvFirst block, fused (Sec. 5.3.1, eq. e:ffn-eff): y = block(x).
  * x, y: [N][H][W][C].  Supported: C in {64, 128, 256, 512}, E >= 1,
- * k in {1, 3, 5, 7}; any N, H, W >= 1.  Other C return CF_ERR_UNSUPPORTED. */
+ * k in {1, 3, 5, 7}; any N, H, W >= 1.  Other C return CF_ERR_UNSUPPORTED.
+ * With N*H*W <= 64 and C >= 128 the block runs on one workgroup per 32
+ * output channels (each recomputing the expand, no workspace; Sec. 4.1.2:
+ * the weights are the bytes), unless the autotuner cached another
+ * configuration for the shape. */
 cf_status cf_block_forward(const void *x, void *y, const cf_block_params *p,
                            int N, int H, int W, int C, int E, int k,
                            cf_dtype dt, cf_act act, void *stream);
