@@ -61,6 +61,8 @@ def lib():
         L.cfref_gconv.argtypes = [_dp, _dp, _dp, _dp, ci, ci, ci, ci, ci, ci, _dp, ci]
         L.cfref_gblock_forward.argtypes = [_dp] * 10 + [ci] * 8 + [_dp, ci]
         L.cfref_mbconv_forward.argtypes = [_dp] * 14 + [ci] * 8 + [_dp]
+        L.cfref_mbconv_s2_forward.argtypes = [_dp] * 14 + [ci] * 9 + [_dp]
+        L.cfref_blurpool_tri3.argtypes = [_dp, ci, ci, ci, ci, _dp]
         L.cfref_default_threads.restype = ci
         _lib = L
     return _lib
@@ -245,6 +247,42 @@ def mbconv_forward(x, p: dict):
     rc = lib().cfref_mbconv_forward(_p(x), _p(w1), _p(vec[0]), _p(vec[1]), _p(a), _p(vec[2]), _p(vec[3]),
                                     _p(wr), _p(vec[4]), _p(we), _p(vec[5]), _p(w2), _p(vec[6]), _p(vec[7]),
                                     N, H, W, C, EC // C, R, k, gw, _p(y))
+    assert rc == 0
+    return y
+
+
+def blurpool_tri3(x):
+    """BlurPool with the Triangle-3 filter (Sec. 5.4: the down-sampling layer
+    of the stride-2 MBConv block): per channel, taps [1, 2, 1]/4 in each
+    direction, one pixel of reflect padding, stride 2.  x [N,H,W,Ch] with
+    H, W >= 2 -> [N, ceil(H/2), ceil(W/2), Ch]."""
+    x = _f64(x)
+    N, H, W, Ch = x.shape
+    y = np.empty((N, (H + 1) // 2, (W + 1) // 2, Ch))
+    assert lib().cfref_blurpool_tri3(_p(x), N, H, W, Ch, _p(y)) == 0
+    return y
+
+
+def mbconv_s2_forward(x, p: dict):
+    """The stride-2 MBConv block (Fig. f:mbconv, stride 2; Sec. 5.4): as
+    mbconv_forward up to the grouped conv's SiLU, then blurpool_tri3, the
+    squeeze over the down-sampled map, the gates, and the project to K
+    channels without a residual (the output has another shape).  p as for
+    mbconv_forward with w2 [K,E*C] and s3, b3 [K].  x [N,H,W,C] -> [N,
+    ceil(H/2), ceil(W/2), K]."""
+    x = _f64(x)
+    N, H, W, C = x.shape
+    w1, a, wr, we, w2 = (_f64(p[k]) for k in ("w1", "gw_w", "wr", "we", "w2"))
+    EC = w1.shape[0]
+    k, _, _, gw = a.shape
+    R, K = wr.shape[0], w2.shape[0]
+    assert w1.shape == (EC, C) and a.shape == (k, k, EC, gw) and wr.shape == (R, EC)
+    assert we.shape == (EC, R) and w2.shape == (K, EC) and EC % C == 0
+    vec = [_f64(p.get(n)) for n in ("s1", "b1", "s2", "b2", "br", "be", "s3", "b3")]
+    y = np.empty((N, (H + 1) // 2, (W + 1) // 2, K))
+    rc = lib().cfref_mbconv_s2_forward(_p(x), _p(w1), _p(vec[0]), _p(vec[1]), _p(a), _p(vec[2]), _p(vec[3]),
+                                       _p(wr), _p(vec[4]), _p(we), _p(vec[5]), _p(w2), _p(vec[6]), _p(vec[7]),
+                                       N, H, W, C, EC // C, R, K, k, gw, _p(y))
     assert rc == 0
     return y
 

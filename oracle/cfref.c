@@ -488,28 +488,73 @@ int cfref_gblock_forward(const double *x, const double *a, const double *s0, con
  *   g[n,c]  = sigmoid(sum_r We[c][r] z[n,r] + be[c])
  *   Y  = X + s3 * ((V * g) W2^T) + b3
  * Layouts: w1 [EC][C], gwt [k][k][EC][gw], wr [R][EC], we [EC][R],
- * w2 [C][EC].  Serial over images (each image's SE couples all its pixels);
+ * w2 [C][EC] (stride 2: [K][EC]).  Serial over images (each image's SE couples all its pixels);
  * for the small late-stage shapes the block is used at. */
 static double silu(double u) { return u / (1.0 + exp(-u)); }
 static double sigmoid(double u) { return 1.0 / (1.0 + exp(-u)); }
 
-int cfref_mbconv_forward(const double *x, const double *w1, const double *s1, const double *b1,
-                         const double *gwt, const double *s2, const double *b2,
-                         const double *wr, const double *br, const double *we, const double *be,
-                         const double *w2, const double *s3, const double *b3,
-                         int N, int H, int W, int C, int E, int R, int k, int gw, double *y)
+/* BlurPool with the Triangle-3 filter (Sec. 5.4: the down-sampling layer of
+ * the stride-2 MBConv block, after the grouped convolution), on one image
+ * [H][W][Ch]: a per-channel low-pass with the separable taps [1, 2, 1] / 4
+ * in each direction, then every second pixel:
+ *   Vd[i][j][c] = sum_{a<3} sum_{b<3} t[a] t[b] V[r(2i + a - 1)][r(2j + b - 1)][c]
+ * with one pixel of reflect padding, r(-1) = 1, r(H) = H - 2 (H, W >= 2).
+ * Output ceil(H/2) x ceil(W/2). */
+static void blurpool_tri3(const double *V, int H, int W, int Ch, double *Vd)
+{
+    static const double t[3] = {0.25, 0.5, 0.25};
+    const int Ho = (H + 1) / 2, Wo = (W + 1) / 2;
+    for (int i = 0; i < Ho; i++)
+        for (int j = 0; j < Wo; j++)
+            for (int c = 0; c < Ch; c++) {
+                double acc = 0.0;
+                for (int a = 0; a < 3; a++) {
+                    int r = 2 * i + a - 1;
+                    r = r < 0 ? -r : (r >= H ? 2 * (H - 1) - r : r);
+                    for (int b = 0; b < 3; b++) {
+                        int q = 2 * j + b - 1;
+                        q = q < 0 ? -q : (q >= W ? 2 * (W - 1) - q : q);
+                        acc += t[a] * t[b] * V[((size_t)r * W + q) * Ch + c];
+                    }
+                }
+                Vd[((size_t)i * Wo + j) * Ch + c] = acc;
+            }
+}
+
+int cfref_blurpool_tri3(const double *x, int N, int H, int W, int Ch, double *y)
+{
+    if (H < 2 || W < 2 || Ch <= 0)
+        return -1;
+    const size_t in = (size_t)H * W * Ch, out = (size_t)((H + 1) / 2) * ((W + 1) / 2) * Ch;
+    for (int n = 0; n < N; n++)
+        blurpool_tri3(x + n * in, H, W, Ch, y + n * out);
+    return 0;
+}
+
+/* The block for stride 1 (K = C, residual) and stride 2 (BlurPool after the
+ * grouped conv's activation, the squeeze over the down-sampled map, the
+ * project to K channels, no residual: the output has another shape). */
+static int mbconv_core(const double *x, const double *w1, const double *s1, const double *b1,
+                       const double *gwt, const double *s2, const double *b2,
+                       const double *wr, const double *br, const double *we, const double *be,
+                       const double *w2, const double *s3, const double *b3,
+                       int N, int H, int W, int C, int E, int R, int k, int gw, int stride, int K, double *y)
 {
     const int EC = E * C;
-    if (gw <= 0 || EC % gw || R <= 0 || k % 2 == 0)
+    if (gw <= 0 || EC % gw || R <= 0 || k % 2 == 0 || K <= 0 || (stride == 1 && K != C) ||
+        (stride != 1 && stride != 2) || (stride == 2 && (H < 2 || W < 2)))
         return -1;
     const size_t P = (size_t)H * W;
+    const int Ho = stride == 2 ? (H + 1) / 2 : H, Wo = stride == 2 ? (W + 1) / 2 : W;
+    const size_t Po = (size_t)Ho * Wo;
     double *U = (double *)malloc(sizeof(double) * P * EC);
     double *V = (double *)malloc(sizeof(double) * P * EC);
+    double *Vd = stride == 2 ? (double *)malloc(sizeof(double) * Po * EC) : V;
     double *sq = (double *)malloc(sizeof(double) * EC);
     double *z = (double *)malloc(sizeof(double) * R);
     double *g = (double *)malloc(sizeof(double) * EC);
-    if (!U || !V || !sq || !z || !g) {
-        free(U); free(V); free(sq); free(z); free(g);
+    if (!U || !V || !Vd || !sq || !z || !g) {
+        free(U); free(V); if (Vd != V) free(Vd); free(sq); free(z); free(g);
         return -2;
     }
     const int pad = k / 2;
@@ -545,12 +590,14 @@ int cfref_mbconv_forward(const double *x, const double *w1, const double *s1, co
                     }
                     V[((size_t)h * W + w) * EC + c] = silu((s2 ? s2[c] : 1.0) * acc + (b2 ? b2[c] : 0.0));
                 }
+        if (stride == 2)
+            blurpool_tri3(V, H, W, EC, Vd);
         /* squeeze: global average, reduce to R with ReLU, expand with sigmoid */
         for (int c = 0; c < EC; c++) {
             double acc = 0.0;
-            for (size_t p = 0; p < P; p++)
-                acc += V[p * EC + c];
-            sq[c] = acc / (double)P;
+            for (size_t p = 0; p < Po; p++)
+                acc += Vd[p * EC + c];
+            sq[c] = acc / (double)Po;
         }
         for (int r = 0; r < R; r++) {
             double acc = 0.0;
@@ -565,15 +612,36 @@ int cfref_mbconv_forward(const double *x, const double *w1, const double *s1, co
                 acc += we[(size_t)c * R + r] * z[r];
             g[c] = sigmoid(acc + (be ? be[c] : 0.0));
         }
-        /* gate, project, folded norm, residual */
-        for (size_t p = 0; p < P; p++)
-            for (int o = 0; o < C; o++) {
+        /* gate, project, folded norm, residual (stride 1) */
+        for (size_t p = 0; p < Po; p++)
+            for (int o = 0; o < K; o++) {
                 double acc = 0.0;
                 for (int c = 0; c < EC; c++)
-                    acc += w2[(size_t)o * EC + c] * (V[p * EC + c] * g[c]);
-                y[((size_t)n * P + p) * C + o] = xn[p * C + o] + (s3 ? s3[o] : 1.0) * acc + (b3 ? b3[o] : 0.0);
+                    acc += w2[(size_t)o * EC + c] * (Vd[p * EC + c] * g[c]);
+                y[((size_t)n * Po + p) * K + o] =
+                    (stride == 1 ? xn[p * C + o] : 0.0) + (s3 ? s3[o] : 1.0) * acc + (b3 ? b3[o] : 0.0);
             }
     }
-    free(U); free(V); free(sq); free(z); free(g);
+    free(U); free(V); if (Vd != V) free(Vd); free(sq); free(z); free(g);
     return 0;
+}
+
+int cfref_mbconv_forward(const double *x, const double *w1, const double *s1, const double *b1,
+                         const double *gwt, const double *s2, const double *b2,
+                         const double *wr, const double *br, const double *we, const double *be,
+                         const double *w2, const double *s3, const double *b3,
+                         int N, int H, int W, int C, int E, int R, int k, int gw, double *y)
+{
+    return mbconv_core(x, w1, s1, b1, gwt, s2, b2, wr, br, we, be, w2, s3, b3, N, H, W, C, E, R, k, gw, 1, C, y);
+}
+
+/* The stride-2 MBConv block (Fig. f:mbconv, stride 2; Sec. 5.4): y is
+ * [N][ceil(H/2)][ceil(W/2)][K], w2 [K][E*C], s3, b3 [K]. */
+int cfref_mbconv_s2_forward(const double *x, const double *w1, const double *s1, const double *b1,
+                            const double *gwt, const double *s2, const double *b2,
+                            const double *wr, const double *br, const double *we, const double *be,
+                            const double *w2, const double *s3, const double *b3,
+                            int N, int H, int W, int C, int E, int R, int K, int k, int gw, double *y)
+{
+    return mbconv_core(x, w1, s1, b1, gwt, s2, b2, wr, br, we, be, w2, s3, b3, N, H, W, C, E, R, k, gw, 2, K, y);
 }
