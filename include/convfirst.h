@@ -302,6 +302,37 @@ cf_status cf_mbconv_forward(const void *x, void *y, void *ws, size_t ws_bytes, c
 /* 0 for shapes the kernel does not support. */
 size_t cf_mbconv_workspace_bytes(int N, int H, int W, int C, int E, int R, cf_dtype dt);
 
+/* The stride-2 MBConv block (Fig. f:mbconv with stride 2; Sec. 5.4), the
+ * first block of a stage that halves the image and changes the channel
+ * count.  Same expand, grouped conv and SiLU as cf_mbconv_forward; then
+ *   V'[n,i,j,c] = sum_{a,b<3} t[a] t[b] V[n, rf(2i+a-1, H), rf(2j+b-1, W), c]
+ *                 with t = (1, 2, 1) / 4 and rf reflecting one pixel past the
+ *                 border (rf(-1) = 1, rf(H) = H - 2)          BlurPool, Triangle-3
+ *   z[n] = ReLU(wr mean_{i,j} V'[n,i,j,:] + br);  g[n] = sigmoid(we z[n] + be)
+ *   Y[n,i,j,:] = s3 * (w2 (V'[n,i,j,:] * g[n])) + b3           project, no residual
+ * The paper names the BlurPool filter and places the down-sampling in the
+ * stride-2 block but leaves the padding and the squeeze's input unstated;
+ * reflect padding and the squeeze over the down-sampled map are the readings
+ * taken here.  Tensors as for cf_mbconv_forward except
+ *   x [N][H][W][C];  y [N][ceil(H/2)][ceil(W/2)][K];  w2 [K][EC];
+ *   s3, b3 fp32 [K].
+ * Supported: as cf_mbconv_forward, plus 2 <= H, W (reflect padding needs a
+ * second row and column) and K a positive multiple of 16 with the LDS layout
+ * (now also holding the work item's full-resolution V, H*W*144 bytes)
+ * within 160 KB; K <= 0 or H, W < 2 is CF_ERR_INVALID, K not a multiple of
+ * 16 CF_ERR_UNSUPPORTED.  y must not overlap x (no in-place form: the shapes
+ * differ); ws as for cf_mbconv_forward, sized by
+ * cf_mbconv_s2_workspace_bytes (the exchanged map is V', a quarter of V).
+ * Each work item blurs its own 64 channels from its LDS copy of V before the
+ * exchange, so the block is still one launch with one barrier per image.
+ * V and V' are rounded to the I/O dtype (V' sums 9 rounded V values in fp32);
+ * the squeeze sums the unrounded fp32 V'.  Deterministic. */
+cf_status cf_mbconv_s2_forward(const void *x, void *y, void *ws, size_t ws_bytes, const cf_mbconv_params *p,
+                               int N, int H, int W, int C, int E, int R, int K, int k, cf_dtype dt,
+                               cf_launch launch, void *stream);
+/* 0 for shapes the kernel does not support. */
+size_t cf_mbconv_s2_workspace_bytes(int N, int H, int W, int C, int E, int R, int K, cf_dtype dt);
+
 /* Allocation-free variant of cf_block_forward_split, for callers that cannot
  * allocate device memory: code under stream capture, tight serving loops,
  * harnesses that forbid hipMalloc.  Same arguments and result as

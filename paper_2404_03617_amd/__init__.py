@@ -26,7 +26,8 @@ __all__ = [
     "stage_forward_microbatch",
     "downsample_forward",
     "block_forward_unfused", "block_forward_split", "block_forward_split_noalloc", "gblock_forward",
-    "mbconv_forward", "mbconv_workspace_bytes", "stem_forward", "stem_gblock_forward", "stack_forward", "capture_stack", "ConvFirstBlock",
+    "mbconv_forward", "mbconv_workspace_bytes", "mbconv_s2_forward", "mbconv_s2_workspace_bytes", "stem_forward",
+    "stem_gblock_forward", "stack_forward", "capture_stack", "ConvFirstBlock",
     "CFError", "EXPORTED_SYMBOLS", "dw_weight_from_conv2d", "grouped_weight_from_conv2d",
     "pw_weight_from_conv2d", "down_weight_from_conv2d", "fold_batchnorm", "block_params_from_modules",
     "grouped_block_params_from_modules", "down_params_from_modules", "stem_params_from_modules",
@@ -44,7 +45,8 @@ EXPORTED_SYMBOLS = (
     "cf_stage_microbatch_workspace_bytes", "cf_downsample_forward",
     "cf_block_forward_unfused", "cf_unfused_workspace_bytes", "cf_block_forward_split",
     "cf_split_workspace_bytes", "cf_block_forward_split_noalloc", "cf_gblock_forward", "cf_mbconv_forward",
-    "cf_mbconv_workspace_bytes", "cf_stem_forward", "cf_stem_gblock_forward", "cf_block_autotune",
+    "cf_mbconv_workspace_bytes", "cf_mbconv_s2_forward", "cf_mbconv_s2_workspace_bytes", "cf_stem_forward",
+    "cf_stem_gblock_forward", "cf_block_autotune",
     "cf_block_tuned_config", "cf_last_error", "cf_status_string", "cf_abi_version",
 )
 
@@ -113,6 +115,8 @@ def lib():
             "cf_gblock_forward": (i, [vp, vp, gp, i, i, i, i, i, i, i, i, vp]),
             "cf_mbconv_forward": (i, [vp, vp, vp, sz, mp, i, i, i, i, i, i, i, i, i, vp]),
             "cf_mbconv_workspace_bytes": (sz, [i, i, i, i, i, i, i]),
+            "cf_mbconv_s2_forward": (i, [vp, vp, vp, sz, mp, i, i, i, i, i, i, i, i, i, i, vp]),
+            "cf_mbconv_s2_workspace_bytes": (sz, [i, i, i, i, i, i, i, i]),
             "cf_stem_forward": (i, [vp, vp, sp, i, i, i, i, i, vp]),
             "cf_stem_gblock_forward": (i, [vp, vp, sp, gp, i, i, i, i, i, i, i, i, vp]),
             "cf_block_autotune": (i, [vp, vp, bp, i, i, i, i, i, i, i, i, vp]),
@@ -503,18 +507,19 @@ def stem_gblock_forward(x: torch.Tensor, stem: dict, p: dict, act: str = "relu",
     return y
 
 
-# MBConv parameters: shape as a function of (C, E*C, R), and whether the
-# tensor is a weight in x's dtype ("w") or an fp32 vector ("v").
+# MBConv parameters: shape as a function of (C, E*C, R, K) with K the output
+# channels (C for stride 1), and whether the tensor is a weight in x's dtype
+# ("w") or an fp32 vector ("v").
 _MBCONV_SHAPES = {
-    "w1": (lambda C, EC, R: (EC, C), "w"),
-    "gw_w": (lambda C, EC, R: (3, 3, EC, GROUP_WIDTH), "w"),
-    "wr": (lambda C, EC, R: (R, EC), "w"),
-    "we": (lambda C, EC, R: (EC, R), "w"),
-    "w2": (lambda C, EC, R: (C, EC), "w"),
-    "s1": (lambda C, EC, R: (EC,), "v"), "b1": (lambda C, EC, R: (EC,), "v"),
-    "s2": (lambda C, EC, R: (EC,), "v"), "b2": (lambda C, EC, R: (EC,), "v"),
-    "br": (lambda C, EC, R: (R,), "v"), "be": (lambda C, EC, R: (EC,), "v"),
-    "s3": (lambda C, EC, R: (C,), "v"), "b3": (lambda C, EC, R: (C,), "v"),
+    "w1": (lambda C, EC, R, K: (EC, C), "w"),
+    "gw_w": (lambda C, EC, R, K: (3, 3, EC, GROUP_WIDTH), "w"),
+    "wr": (lambda C, EC, R, K: (R, EC), "w"),
+    "we": (lambda C, EC, R, K: (EC, R), "w"),
+    "w2": (lambda C, EC, R, K: (K, EC), "w"),
+    "s1": (lambda C, EC, R, K: (EC,), "v"), "b1": (lambda C, EC, R, K: (EC,), "v"),
+    "s2": (lambda C, EC, R, K: (EC,), "v"), "b2": (lambda C, EC, R, K: (EC,), "v"),
+    "br": (lambda C, EC, R, K: (R,), "v"), "be": (lambda C, EC, R, K: (EC,), "v"),
+    "s3": (lambda C, EC, R, K: (K,), "v"), "b3": (lambda C, EC, R, K: (K,), "v"),
 }
 
 
@@ -524,7 +529,49 @@ def mbconv_workspace_bytes(N: int, H: int, W: int, C: int, E: int, R: int, dtype
     return int(lib().cf_mbconv_workspace_bytes(N, H, W, C, E, R, DTYPES[dtype]))
 
 
+def mbconv_s2_workspace_bytes(N: int, H: int, W: int, C: int, E: int, R: int, K: int,
+                              dtype=torch.float16) -> int:
+    """Recommended workspace of mbconv_s2_forward on the current device (0 for
+    a shape without a kernel)."""
+    return int(lib().cf_mbconv_s2_workspace_bytes(N, H, W, C, E, R, K, DTYPES[dtype]))
+
+
 LAUNCHES = {"cooperative": 0, "exclusive": 1}
+
+
+def _mbconv_args(x: torch.Tensor, p: dict, launch: str, stride2: bool):
+    """Checks an MBConv call's tensors; returns the sizes, the C struct of
+    pointers and the tensors it points into (kept alive by the caller)."""
+    if launch not in LAUNCHES:
+        raise ValueError("launch must be one of %s" % sorted(LAUNCHES))
+    N, H, W, C = _dims(x)
+    for key in ("w1", "gw_w", "wr", "we", "w2"):
+        if not isinstance(p.get(key), torch.Tensor):
+            raise ValueError("MBConv parameter %s is required" % key)
+    if p["w1"].dim() != 2 or p["wr"].dim() != 2 or p["w2"].dim() != 2:
+        raise ValueError("w1 must be [E*C, C], wr [R, E*C] and w2 [K, E*C]")
+    EC, R = int(p["w1"].shape[0]), int(p["wr"].shape[0])
+    K = int(p["w2"].shape[0]) if stride2 else C
+    if EC % C or EC == 0:
+        raise ValueError("w1 rows must be a positive multiple of C")
+    if p["gw_w"].dim() != 4 or p["gw_w"].shape[0] != p["gw_w"].shape[1]:
+        raise ValueError("gw_w must be [k, k, E*C, 8]")
+    k = int(p["gw_w"].shape[0])
+    unknown = set(p) - set(_MBCONV_SHAPES)
+    if unknown:
+        raise ValueError("unknown MBConv parameters: %s" % sorted(unknown))
+    vals, keep = {}, []
+    for key, (shape_of, kind) in _MBCONV_SHAPES.items():
+        t = p.get(key)
+        if t is not None:
+            shape = shape_of(C, EC, R, K)
+            if key == "gw_w":
+                shape = (k, k, EC, GROUP_WIDTH)
+            _check_tensor(key, t, shape, x.dtype if kind == "w" else torch.float32, x.device)
+            keep.append(t)
+        vals[key] = None if t is None else t.data_ptr()
+    _check_device(x)
+    return (N, H, W, C, EC // C, R, K, k), _MBConvParams(**vals), keep
 
 
 def mbconv_forward(x: torch.Tensor, p: dict, out=None, ws=None, launch: str = "cooperative",
@@ -539,43 +586,36 @@ def mbconv_forward(x: torch.Tensor, p: dict, out=None, ws=None, launch: str = "c
     reusable); its first int32 becomes 1 if a barrier wait ever gave up.
     launch="exclusive" replaces the cooperative launch by an ordinary one,
     for callers that own the device (see the C header)."""
-    if launch not in LAUNCHES:
-        raise ValueError("launch must be one of %s" % sorted(LAUNCHES))
-    N, H, W, C = _dims(x)
-    for key in ("w1", "gw_w", "wr", "we", "w2"):
-        if not isinstance(p.get(key), torch.Tensor):
-            raise ValueError("MBConv parameter %s is required" % key)
-    if p["w1"].dim() != 2 or p["wr"].dim() != 2:
-        raise ValueError("w1 must be [E*C, C] and wr [R, E*C]")
-    EC, R = int(p["w1"].shape[0]), int(p["wr"].shape[0])
-    if EC % C or EC == 0:
-        raise ValueError("w1 rows must be a positive multiple of C")
-    if p["gw_w"].dim() != 4 or p["gw_w"].shape[0] != p["gw_w"].shape[1]:
-        raise ValueError("gw_w must be [k, k, E*C, 8]")
-    k = int(p["gw_w"].shape[0])
-    unknown = set(p) - set(_MBCONV_SHAPES)
-    if unknown:
-        raise ValueError("unknown MBConv parameters: %s" % sorted(unknown))
-    vals, keep = {}, []
-    for key, (shape_of, kind) in _MBCONV_SHAPES.items():
-        t = p.get(key)
-        if t is not None:
-            shape = shape_of(C, EC, R)
-            if key == "gw_w":
-                shape = (k, k, EC, GROUP_WIDTH)
-            _check_tensor(key, t, shape, x.dtype if kind == "w" else torch.float32, x.device)
-            keep.append(t)
-        vals[key] = None if t is None else t.data_ptr()
-    mp = _MBConvParams(**vals)
-    _check_device(x)
+    (N, H, W, C, E, R, _, k), mp, keep = _mbconv_args(x, p, launch, False)
     y = _out(x, out)
     if ws is None:
-        ws = torch.zeros(max(1, mbconv_workspace_bytes(N, H, W, C, EC // C, R, x.dtype)), dtype=torch.uint8,
+        ws = torch.zeros(max(1, mbconv_workspace_bytes(N, H, W, C, E, R, x.dtype)), dtype=torch.uint8,
                          device=x.device)
     else:
         _workspace(x, ws, 0)
-    _check(lib().cf_mbconv_forward(_ptr(x), _ptr(y), _ptr(ws), ws.numel(), ctypes.byref(mp), N, H, W, C, EC // C,
+    _check(lib().cf_mbconv_forward(_ptr(x), _ptr(y), _ptr(ws), ws.numel(), ctypes.byref(mp), N, H, W, C, E,
                                    R, k, DTYPES[x.dtype], LAUNCHES[launch], _stream(stream)))
+    return y
+
+
+def mbconv_s2_forward(x: torch.Tensor, p: dict, out=None, ws=None, launch: str = "cooperative",
+                      stream=None) -> torch.Tensor:
+    """The stride-2 MBConv block (Fig. f:mbconv with stride 2; Sec. 5.4): as
+    mbconv_forward, then BlurPool with the Triangle-3 filter (reflect padding,
+    stride 2) on the conv output, the squeeze over the down-sampled map, the
+    project to K channels and no residual, in one launch.  p as for
+    mbconv_forward except w2 [K,E*C] and s3,b3 [K]; the result is
+    [N, ceil(H/2), ceil(W/2), K] and must not overlap x.  ws as for
+    mbconv_forward, sized by mbconv_s2_workspace_bytes()."""
+    (N, H, W, C, E, R, K, k), mp, keep = _mbconv_args(x, p, launch, True)
+    y = _out(x, out, (N, (H + 1) // 2, (W + 1) // 2, K))
+    if ws is None:
+        ws = torch.zeros(max(1, mbconv_s2_workspace_bytes(N, H, W, C, E, R, K, x.dtype)), dtype=torch.uint8,
+                         device=x.device)
+    else:
+        _workspace(x, ws, 0)
+    _check(lib().cf_mbconv_s2_forward(_ptr(x), _ptr(y), _ptr(ws), ws.numel(), ctypes.byref(mp), N, H, W, C, E,
+                                      R, K, k, DTYPES[x.dtype], LAUNCHES[launch], _stream(stream)))
     return y
 
 

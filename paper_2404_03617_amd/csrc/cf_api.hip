@@ -254,6 +254,87 @@ cf::StemW to_stem(const void *x, const cf_stem_params *p, int Hin, int Win) {
     return s;
 }
 
+// MBConv + SE, stride 1 (K = 0: C output channels, residual) or stride 2
+// (K output channels on a ceil(H/2) x ceil(W/2) map, no residual).
+size_t mbconv_ws(int N, int H, int W, int C, int E, int R, int K, cf_dtype dt) {
+    if (N <= 0 || E <= 0 || (double)E * C > 65536.0 || !cf::mbconv_supported(H, W, C, E, R, K) ||
+        ((int)dt != CF_F16 && (int)dt != CF_BF16))
+        return 0;
+    int slots = 0;
+    if (cf::mbconv_resident_slots(H, W, C, E, R, K, dt == CF_BF16, &slots) != hipSuccess || slots < 1)
+        slots = 1;
+    return cf::mbconv_workspace_bytes(N, H, W, C, E, R, K, slots < N ? slots : N);
+}
+
+cf_status mbconv_call(const char *what, const void *x, void *y, void *ws, size_t ws_bytes, const cf_mbconv_params *p,
+                      int N, int H, int W, int C, int E, int R, int K, int k, cf_dtype dt, cf_launch launch,
+                      void *stream) {
+    if (!x || !y)
+        return fail(CF_ERR_INVALID, "%s: x and y must be non-NULL", what);
+    if (!p || !p->w1 || !p->gw_w || !p->wr || !p->we || !p->w2)
+        return fail(CF_ERR_INVALID, "%s: params, w1, gw_w, wr, we and w2 must be non-NULL", what);
+    if (N <= 0 || H <= 0 || W <= 0 || C <= 0 || E <= 0 || R <= 0 || k <= 0)
+        return fail(CF_ERR_INVALID, "%s: sizes must be positive (N=%d H=%d W=%d C=%d E=%d R=%d k=%d)", what, N, H,
+                    W, C, E, R, k);
+    if (k % 2 == 0)
+        return fail(CF_ERR_INVALID, "%s: k must be odd (got %d)", what, k);
+    if (C % CF_GROUP_WIDTH)
+        return fail(CF_ERR_INVALID, "%s: C=%d is not a multiple of the group width %d", what, C, CF_GROUP_WIDTH);
+    if (K > 0 && (H < 2 || W < 2))
+        return fail(CF_ERR_INVALID, "%s: BlurPool's reflect padding needs H, W >= 2 (H=%d W=%d)", what, H, W);
+    if ((int)dt != CF_F16 && (int)dt != CF_BF16)
+        return fail(CF_ERR_INVALID, "%s: unknown dtype %d", what, (int)dt);
+    if ((int)launch != CF_LAUNCH_COOPERATIVE && (int)launch != CF_LAUNCH_EXCLUSIVE)
+        return fail(CF_ERR_INVALID, "%s: unknown launch mode %d", what, (int)launch);
+    if ((double)N * H * W * C > 4.0e12 || (double)E * C > 65536.0 || (double)K > 65536.0)
+        return fail(CF_ERR_INVALID, "%s: tensor too large", what);
+    const void *ptrs[] = {x, y, ws, p->w1, p->gw_w, p->wr, p->we, p->w2, p->s1, p->b1,
+                          p->s2, p->b2, p->br, p->be, p->s3, p->b3};
+    for (const void *q : ptrs)
+        if (q && !aligned16(q))
+            return fail(CF_ERR_INVALID, "%s: every tensor pointer must be 16-byte aligned", what);
+    const size_t xbytes = (size_t)N * H * W * C * elem_bytes(dt);
+    const size_t ybytes = K > 0 ? (size_t)N * ((H + 1) / 2) * ((W + 1) / 2) * K * elem_bytes(dt) : xbytes;
+    if (K > 0 ? overlap(x, xbytes, y, ybytes) : (x != y && overlap(x, xbytes, y, ybytes)))
+        return fail(CF_ERR_INVALID, K > 0 ? "%s: x and y overlap" : "%s: x and y overlap without being equal", what);
+    if (k != 3)
+        return fail(CF_ERR_UNSUPPORTED, "%s: k=%d has no kernel (supported: 3)", what, k);
+    if (!cf::mbconv_supported(H, W, C, E, R, K))
+        return fail(CF_ERR_UNSUPPORTED,
+                    "%s: no kernel for H=%d W=%d C=%d E=%d R=%d K=%d (supported: H, W <= 16, C %% 16 == 0, "
+                    "E*C %% 64 == 0, E*C <= 4096, R <= 256, K %% 16 == 0)",
+                    what, H, W, C, E, R, K);
+    const size_t need = cf::mbconv_workspace_bytes(N, H, W, C, E, R, K, 1);
+    if (!ws || ws_bytes < need)
+        return fail(CF_ERR_WORKSPACE, "%s: ws has %zu bytes, needs at least %zu", what, ws ? ws_bytes : (size_t)0,
+                    need);
+    if (overlap(ws, ws_bytes, x, xbytes) || overlap(ws, ws_bytes, y, ybytes))
+        return fail(CF_ERR_INVALID, "%s: ws overlaps x or y", what);
+    cf::MBConvW w;
+    w.w1 = p->w1;
+    w.s1 = p->s1;
+    w.b1 = p->b1;
+    w.gw = p->gw_w;
+    w.s2 = p->s2;
+    w.b2 = p->b2;
+    w.wr = p->wr;
+    w.br = p->br;
+    w.we = p->we;
+    w.be = p->be;
+    w.w2 = p->w2;
+    w.s3 = p->s3;
+    w.b3 = p->b3;
+    hipError_t e = cf::launch_mbconv(x, y, w, N, H, W, C, E, R, K, dt == CF_BF16, ws, ws_bytes,
+                                     launch == CF_LAUNCH_COOPERATIVE, (hipStream_t)stream);
+    if (e == hipErrorInvalidConfiguration)
+        return fail(CF_ERR_UNSUPPORTED, "%s: the %d work items of one image do not fit on the device at once", what,
+                    E * C / 64);
+    if (e != hipSuccess)
+        return hip_fail(e, what);
+    g_err[0] = 0;
+    return CF_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -678,79 +759,24 @@ cf_status cf_stem_gblock_forward(const void *x, void *y, const cf_stem_params *s
 }
 
 size_t cf_mbconv_workspace_bytes(int N, int H, int W, int C, int E, int R, cf_dtype dt) {
-    if (N <= 0 || E <= 0 || (double)E * C > 65536.0 || !cf::mbconv_supported(H, W, C, E, R) ||
-        ((int)dt != CF_F16 && (int)dt != CF_BF16))
-        return 0;
-    int slots = 0;
-    if (cf::mbconv_resident_slots(H, W, C, E, R, dt == CF_BF16, &slots) != hipSuccess || slots < 1)
-        slots = 1;
-    return cf::mbconv_workspace_bytes(N, H, W, C, E, R, slots < N ? slots : N);
+    return mbconv_ws(N, H, W, C, E, R, 0, dt);
+}
+
+size_t cf_mbconv_s2_workspace_bytes(int N, int H, int W, int C, int E, int R, int K, cf_dtype dt) {
+    return K > 0 ? mbconv_ws(N, H, W, C, E, R, K, dt) : 0;
 }
 
 cf_status cf_mbconv_forward(const void *x, void *y, void *ws, size_t ws_bytes, const cf_mbconv_params *p, int N,
                             int H, int W, int C, int E, int R, int k, cf_dtype dt, cf_launch launch, void *stream) {
-    const char *what = "cf_mbconv_forward";
-    if (!x || !y)
-        return fail(CF_ERR_INVALID, "%s: x and y must be non-NULL", what);
-    if (!p || !p->w1 || !p->gw_w || !p->wr || !p->we || !p->w2)
-        return fail(CF_ERR_INVALID, "%s: params, w1, gw_w, wr, we and w2 must be non-NULL", what);
-    if (N <= 0 || H <= 0 || W <= 0 || C <= 0 || E <= 0 || R <= 0 || k <= 0)
-        return fail(CF_ERR_INVALID, "%s: sizes must be positive (N=%d H=%d W=%d C=%d E=%d R=%d k=%d)", what, N, H,
-                    W, C, E, R, k);
-    if (k % 2 == 0)
-        return fail(CF_ERR_INVALID, "%s: k must be odd (got %d)", what, k);
-    if (C % CF_GROUP_WIDTH)
-        return fail(CF_ERR_INVALID, "%s: C=%d is not a multiple of the group width %d", what, C, CF_GROUP_WIDTH);
-    if ((int)dt != CF_F16 && (int)dt != CF_BF16)
-        return fail(CF_ERR_INVALID, "%s: unknown dtype %d", what, (int)dt);
-    if ((int)launch != CF_LAUNCH_COOPERATIVE && (int)launch != CF_LAUNCH_EXCLUSIVE)
-        return fail(CF_ERR_INVALID, "%s: unknown launch mode %d", what, (int)launch);
-    if ((double)N * H * W * C > 4.0e12 || (double)E * C > 65536.0)
-        return fail(CF_ERR_INVALID, "%s: tensor too large", what);
-    const void *ptrs[] = {x, y, ws, p->w1, p->gw_w, p->wr, p->we, p->w2, p->s1, p->b1,
-                          p->s2, p->b2, p->br, p->be, p->s3, p->b3};
-    for (const void *q : ptrs)
-        if (q && !aligned16(q))
-            return fail(CF_ERR_INVALID, "%s: every tensor pointer must be 16-byte aligned", what);
-    const size_t bytes = (size_t)N * H * W * C * elem_bytes(dt);
-    if (x != y && overlap(x, bytes, y, bytes))
-        return fail(CF_ERR_INVALID, "%s: x and y overlap without being equal", what);
-    if (k != 3)
-        return fail(CF_ERR_UNSUPPORTED, "%s: k=%d has no kernel (supported: 3)", what, k);
-    if (!cf::mbconv_supported(H, W, C, E, R))
-        return fail(CF_ERR_UNSUPPORTED,
-                    "%s: no kernel for H=%d W=%d C=%d E=%d R=%d (supported: H, W <= 16, C %% 16 == 0, "
-                    "E*C %% 64 == 0, E*C <= 4096, R <= 256)",
-                    what, H, W, C, E, R);
-    const size_t need = cf::mbconv_workspace_bytes(N, H, W, C, E, R, 1);
-    if (!ws || ws_bytes < need)
-        return fail(CF_ERR_WORKSPACE, "%s: ws has %zu bytes, needs at least %zu", what, ws ? ws_bytes : (size_t)0,
-                    need);
-    if (overlap(ws, ws_bytes, x, bytes) || overlap(ws, ws_bytes, y, bytes))
-        return fail(CF_ERR_INVALID, "%s: ws overlaps x or y", what);
-    cf::MBConvW w;
-    w.w1 = p->w1;
-    w.s1 = p->s1;
-    w.b1 = p->b1;
-    w.gw = p->gw_w;
-    w.s2 = p->s2;
-    w.b2 = p->b2;
-    w.wr = p->wr;
-    w.br = p->br;
-    w.we = p->we;
-    w.be = p->be;
-    w.w2 = p->w2;
-    w.s3 = p->s3;
-    w.b3 = p->b3;
-    hipError_t e = cf::launch_mbconv(x, y, w, N, H, W, C, E, R, dt == CF_BF16, ws, ws_bytes,
-                                     launch == CF_LAUNCH_COOPERATIVE, (hipStream_t)stream);
-    if (e == hipErrorInvalidConfiguration)
-        return fail(CF_ERR_UNSUPPORTED, "%s: the %d work items of one image do not fit on the device at once", what,
-                    E * C / 64);
-    if (e != hipSuccess)
-        return hip_fail(e, what);
-    g_err[0] = 0;
-    return CF_OK;
+    return mbconv_call("cf_mbconv_forward", x, y, ws, ws_bytes, p, N, H, W, C, E, R, 0, k, dt, launch, stream);
+}
+
+cf_status cf_mbconv_s2_forward(const void *x, void *y, void *ws, size_t ws_bytes, const cf_mbconv_params *p, int N,
+                               int H, int W, int C, int E, int R, int K, int k, cf_dtype dt, cf_launch launch,
+                               void *stream) {
+    if (K <= 0)
+        return fail(CF_ERR_INVALID, "cf_mbconv_s2_forward: K must be positive (got %d)", K);
+    return mbconv_call("cf_mbconv_s2_forward", x, y, ws, ws_bytes, p, N, H, W, C, E, R, K, k, dt, launch, stream);
 }
 
 cf_status cf_block_autotune(const void *x, void *y, const cf_block_params *p, int N, int H, int W, int C, int E,

@@ -138,18 +138,21 @@ struct MBConvW {
     const void *w2;
     const float *s3, *b3;
 };
-// Shapes with a kernel: H, W <= 16, C % 16 == 0, E*C % 64 == 0, E*C <= 4096,
-// 1 <= R <= 256.
-bool mbconv_supported(int H, int W, int C, int E, int R);
+// K = 0: the stride-1 block (C output channels, residual); K > 0: the
+// stride-2 block (BlurPool after the grouped conv, K output channels on a
+// ceil(H/2) x ceil(W/2) map, no residual).
+// Shapes with a kernel: H, W <= 16 (>= 2 for stride 2), C % 16 == 0,
+// E*C % 64 == 0, E*C <= 4096, 1 <= R <= 256, K % 16 == 0.
+bool mbconv_supported(int H, int W, int C, int E, int R, int K = 0);
 // Images the device can hold in flight at once (all their work items resident).
-hipError_t mbconv_resident_slots(int H, int W, int C, int E, int R, int bf16, int *slots);
+hipError_t mbconv_resident_slots(int H, int W, int C, int E, int R, int K, int bf16, int *slots);
 // Workspace bytes for `slots` images in flight.
-size_t mbconv_workspace_bytes(int N, int H, int W, int C, int E, int R, int slots);
+size_t mbconv_workspace_bytes(int N, int H, int W, int C, int E, int R, int K, int slots);
 // Fused MBConv block; ws of ws_bytes >= mbconv_workspace_bytes(..., 1)
 // (hipErrorInvalidValue otherwise), its header zero.  The first int of ws is
 // set if a barrier wait gave up.  coop: hipLaunchCooperativeKernel, else an
 // ordinary launch of the same grid.
-hipError_t launch_mbconv(const void *x, void *y, const MBConvW &w, int N, int H, int W, int C, int E, int R,
+hipError_t launch_mbconv(const void *x, void *y, const MBConvW &w, int N, int H, int W, int C, int E, int R, int K,
                          int bf16, void *ws, size_t ws_bytes, bool coop, hipStream_t st);
 
 // Upper bound of dynamic LDS the fused kernel needs for this shape (bytes);

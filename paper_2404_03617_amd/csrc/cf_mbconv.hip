@@ -93,8 +93,10 @@ struct Args {
     int *flag;                     // set to 1 when a barrier wait gives up (never cleared here)
     int *line;                     // [SLOTMAX][32]: per slot arrivals, give-up, exits (zero between calls)
     float *sq;                     // [N][G][R] squeeze shares
-    uint16_t *vx;                  // [2][slots][P][EC] exchanged conv output
+    uint16_t *vx;                  // [2][slots][Po][EC] exchanged conv output (stride 2: after BlurPool)
     int N, H, W, C, EC, R, G;
+    int K, Ho, Wo;                 // output channels and size (stride 1: C, H, W)
+    uint32_t off_vb;               // stride 2: LDS copy of the group's conv output [H*W][PB]
     int slots;
     int xcd_map;                   // 1: the workgroups of a slot share an XCD
     uint32_t off_gate, off_z, off_cs, off_vec, off_w1;  // LDS layout (U at 0)
@@ -153,7 +155,7 @@ __device__ __forceinline__ void slot_exit(int *line, int G) {
     }
 }
 
-template <typename T, int NWV, int NPW>
+template <typename T, int NWV, int NPW, bool S2 = false>
 struct MB {
     static constexpr int NT = NWV * 64;
     static constexpr int NGG = 8 / NWV;  // 8-channel conv groups per wave
@@ -171,6 +173,8 @@ struct MB {
         const int g = lin % a.G, slot = lin / a.G;
         const int C = a.C, EC = a.EC, R = a.R, G = a.G;
         const int P = a.H * a.W;
+        const int Po = S2 ? a.Ho * a.Wo : P;  // output pixels
+        const int KO = S2 ? a.K : C;           // output channels
         const int RP = (a.H + 1) / 2;
         const int h0 = g * GH;  // first hidden channel of the group
         uint8_t *U = smem;
@@ -178,7 +182,7 @@ struct MB {
         float *zl = reinterpret_cast<float *>(smem + a.off_z);       // [R]
         float *csum = reinterpret_cast<float *>(smem + a.off_cs);    // [64]
         float *vec = reinterpret_cast<float *>(smem + a.off_vec);    // s1, b1, s2, b2 [64] each; s3, b3 [C]
-        float *s1l = vec, *b1l = vec + 64, *s2l = vec + 128, *b2l = vec + 192, *s3l = vec + 256, *b3l = s3l + C;
+        float *s1l = vec, *b1l = vec + 64, *s2l = vec + 128, *b2l = vec + 192, *s3l = vec + 256, *b3l = s3l + KO;
         int *line = a.line + 32 * (size_t)slot;
 
         // once per workgroup: the scale/bias vectors the group uses
@@ -188,7 +192,7 @@ struct MB {
             s2l[i] = a.s2 ? a.s2[h0 + i] : 1.0f;
             b2l[i] = a.b2 ? a.b2[h0 + i] : 0.0f;
         }
-        for (int i = tid; i < C; i += NT) {
+        for (int i = tid; i < KO; i += NT) {
             s3l[i] = a.s3 ? a.s3[i] : 1.0f;
             b3l[i] = a.b3 ? a.b3[i] : 0.0f;
         }
@@ -217,7 +221,7 @@ struct MB {
         int it = 0;
         for (int n = slot; n < a.N; n += a.slots, it++) {
             const uint16_t *xn = a.x + (size_t)n * P * C;
-            uint16_t *vx = a.vx + ((size_t)(it & 1) * a.slots + slot) * P * EC;
+            uint16_t *vx = a.vx + ((size_t)(it & 1) * a.slots + slot) * Po * EC;
 
             // the U border (row 0, rows past H, column 0, columns past W) is
             // zero; the output staging of the previous image overwrote it
@@ -316,10 +320,16 @@ struct MB {
                             u[e] = silu_f32(fmaf(acc[e], sc[e], bi[e]));
                             sum[e] += u[e];
                         }
-                        st8_dev(vx + (size_t)(r * a.W + c) * EC + h0 + hl,
-                                u32x2{T::pack2(u[0], u[1]), T::pack2(u[2], u[3])});
+                        const u32x2 pk = {T::pack2(u[0], u[1]), T::pack2(u[2], u[3])};
+                        if constexpr (S2)  // the group's copy in LDS, for the BlurPool below
+                            *reinterpret_cast<u32x2 *>(smem + a.off_vb + (uint32_t)(r * a.W + c) * PB +
+                                                       (uint32_t)hl * 2) = pk;
+                        else
+                            st8_dev(vx + (size_t)(r * a.W + c) * EC + h0 + hl, pk);
                     }
                 }
+                if constexpr (S2)
+                    continue;  // the channel sums are those of the down-sampled map (below)
                 // sum over the 16 columns (lane bits 0-3) and the two rows of a
                 // pair (lane bit 5); lanes 0 and 16 hold channels hl .. hl+3
 #pragma unroll
@@ -337,9 +347,59 @@ struct MB {
             }
             __syncthreads();
 
+            if constexpr (S2) {
+                // ---- 2b. BlurPool of the group's 64 channels (Triangle-3 taps
+                //      [1, 2, 1] / 4 in each direction, one pixel of reflect
+                //      padding, stride 2) from the LDS copy of V, rounded V'
+                //      to the exchange buffer; the channel sums of V' (fp32,
+                //      before rounding) in a fixed order: per thread over its
+                //      pixels, then over the threads through the free U area
+                float *part = reinterpret_cast<float *>(U);  // [NT / 16][64]
+                constexpr int NPG = NT / 16;
+                const int c4 = tid & 15, pg = tid >> 4;  // channels 4 c4 .. 4 c4 + 3
+                const uint8_t *vb = smem + a.off_vb + (uint32_t)c4 * 8;
+                float s4[4] = {0.f, 0.f, 0.f, 0.f};
+                for (int pp = pg; pp < Po; pp += NPG) {
+                    const int i = pp / a.Wo, j = pp - i * a.Wo;
+                    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int ta = 0; ta < 3; ta++) {
+                        int r = 2 * i + ta - 1;
+                        r = r < 0 ? -r : (r >= a.H ? 2 * (a.H - 1) - r : r);
+#pragma unroll
+                        for (int tb = 0; tb < 3; tb++) {
+                            int c = 2 * j + tb - 1;
+                            c = c < 0 ? -c : (c >= a.W ? 2 * (a.W - 1) - c : c);
+                            const float wt = (ta == 1 ? 0.5f : 0.25f) * (tb == 1 ? 0.5f : 0.25f);
+                            const u32x2 v = *reinterpret_cast<const u32x2 *>(vb + (uint32_t)(r * a.W + c) * PB);
+                            acc[0] = fmaf(wt, T::lo(v[0]), acc[0]);
+                            acc[1] = fmaf(wt, T::hi(v[0]), acc[1]);
+                            acc[2] = fmaf(wt, T::lo(v[1]), acc[2]);
+                            acc[3] = fmaf(wt, T::hi(v[1]), acc[3]);
+                        }
+                    }
+#pragma unroll
+                    for (int e = 0; e < 4; e++)
+                        s4[e] += acc[e];
+                    st8_dev(vx + (size_t)pp * EC + h0 + 4 * c4,
+                            u32x2{T::pack2(acc[0], acc[1]), T::pack2(acc[2], acc[3])});
+                }
+#pragma unroll
+                for (int e = 0; e < 4; e++)
+                    part[pg * 64 + 4 * c4 + e] = s4[e];
+                __syncthreads();
+                if (tid < 64) {
+                    float sm = 0.0f;
+                    for (int g2 = 0; g2 < NPG; g2++)
+                        sm += part[g2 * 64 + tid];
+                    csum[tid] = sm;
+                }
+                __syncthreads();
+            }
+
             // ---- 3. the group's share of the squeeze: Wr[:, group] . mean(V)
             if (tid < R) {
-                const float inv = 1.0f / (float)P;
+                const float inv = 1.0f / (float)Po;
                 float s = 0.0f;
                 const uint16_t *wrow = a.wr + (size_t)tid * EC + h0;
                 Pack8 w[GH / 8];
@@ -420,7 +480,7 @@ struct MB {
             //      batch in flight, each fragment serving two units) and the
             //      staged V; then s3, b3 and the residual, and y is written once.
             {
-                const int PT = (P + 15) / 16, OT = C / 16;
+                const int PT = (Po + 15) / 16, OT = KO / 16;
                 const int NOG = G > PT ? G / PT : 1;
                 const int per = (OT + NOG - 1) / NOG;  // channel tiles per unit
                 const int units = PT * NOG;
@@ -435,7 +495,7 @@ struct MB {
                     const int row = idx / c4n, c4 = idx - row * c4n;  // row = 16 u + pixel
                     const int p = 16 * ((g + G * (row >> 4)) % PT) + (row & 15);
                     u32x2 v = {0u, 0u};
-                    if (p < P) {
+                    if (p < Po) {
                         const u32x2 raw = ld8_dev(vx + (size_t)p * EC + 4 * c4);
                         const float4v gv = *reinterpret_cast<const float4v *>(gate + 4 * c4);
                         v[0] = T::pack2(T::lo(raw[0]) * gv[0], T::hi(raw[0]) * gv[1]);
@@ -453,10 +513,10 @@ struct MB {
                     for (int ot = ot0 + wv; ot < ot1; ot += NWV) {
                         const uint16_t *wrow = a.w2 + (size_t)(16 * ot + jl) * EC + 8 * q;
                         const int o = 16 * ot + 4 * q;
-                        u32x2 xv0 = {0u, 0u}, xv1 = {0u, 0u};
-                        if (p0 < P)
+                        u32x2 xv0 = {0u, 0u}, xv1 = {0u, 0u};  // the residual (stride 1 only)
+                        if (!S2 && p0 < P)
                             xv0 = *reinterpret_cast<const u32x2 *>(a.x + ((size_t)n * P + p0) * C + o);
-                        if (two && p1 < P)
+                        if (!S2 && two && p1 < P)
                             xv1 = *reinterpret_cast<const u32x2 *>(a.x + ((size_t)n * P + p1) * C + o);
                         float4v acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
                         auto loadb = [&](int b, u32x4 *w) {
@@ -499,11 +559,11 @@ struct MB {
                                               T::hi(xv[0]) + fmaf(acc[1], sc[1], bi[1]));
                             out[1] = T::pack2(T::lo(xv[1]) + fmaf(acc[2], sc[2], bi[2]),
                                               T::hi(xv[1]) + fmaf(acc[3], sc[3], bi[3]));
-                            *reinterpret_cast<u32x2 *>(a.y + ((size_t)n * P + p) * C + o) = out;
+                            *reinterpret_cast<u32x2 *>(a.y + ((size_t)n * Po + p) * KO + o) = out;
                         };
-                        if (p0 < P)
+                        if (p0 < Po)
                             store(p0, xv0, acc0);
-                        if (two && p1 < P)
+                        if (two && p1 < Po)
                             store(p1, xv1, acc1);
                     }
                 }
@@ -518,14 +578,14 @@ struct MB {
 
 // registers for two waves per SIMD: one 8-wave or two 4-wave workgroups per
 // CU (the LDS layout of three or more would not fit with W1 resident)
-template <typename T, int NWV, int NPW>
+template <typename T, int NWV, int NPW, bool S2 = false>
 __global__ __launch_bounds__(NWV * 64) __attribute__((amdgpu_waves_per_eu(2))) void mbconv_kernel(Args a) {
     extern __shared__ __attribute__((aligned(256))) uint8_t smem[];
-    MB<T, NWV, NPW>::run(a, smem);
+    MB<T, NWV, NPW, S2>::run(a, smem);
 }
 
 struct Layout {
-    uint32_t off_gate, off_z, off_cs, off_vec, off_w1, lds;
+    uint32_t off_gate, off_z, off_cs, off_vec, off_w1, off_vb, lds;
     int nwv;
 };
 
@@ -535,10 +595,12 @@ struct Layout {
 // phase stages the work item's units of gated V over the same bytes.  Then
 // the gates of all EC channels, the squeeze vector, the group's channel sums,
 // the fp32 scale/bias vectors (the group's s1, b1, s2, b2; all of s3, b3) and
-// the group's rows of W1.
-Layout layout(int H, int W, int C, int EC, int R) {
+// the group's rows of W1; for stride 2 (K > 0 output channels) last the
+// group's copy of the full-resolution conv output.
+Layout layout(int H, int W, int C, int EC, int R, int K = 0) {
     Layout l;
-    const int P = H * W, G = EC / GH, PT = (P + 15) / 16;
+    const int P = H * W, Po = K > 0 ? ((H + 1) / 2) * ((W + 1) / 2) : P, KO = K > 0 ? K : C;
+    const int G = EC / GH, PT = (Po + 15) / 16;
     const uint32_t urows = (uint32_t)(2 * ((H + 1) / 2) + 2);
     const uint32_t nu = G > PT ? 1 : (uint32_t)((PT + G - 1) / G);  // output units of a work item
     const uint32_t ubytes = urows * UC * PB, stage = nu * 16 * (2 * (uint32_t)EC + 16);
@@ -546,8 +608,9 @@ Layout layout(int H, int W, int C, int EC, int R) {
     l.off_z = l.off_gate + (uint32_t)EC * 4;
     l.off_cs = l.off_z + (((uint32_t)R * 4 + 15) & ~15u);
     l.off_vec = l.off_cs + GH * 4;
-    l.off_w1 = l.off_vec + (4 * GH + 2 * (uint32_t)C) * 4;
-    l.lds = l.off_w1 + 64 * (2 * (uint32_t)C + 16);
+    l.off_w1 = l.off_vec + (4 * GH + 2 * (uint32_t)KO) * 4;
+    l.off_vb = l.off_w1 + 64 * (2 * (uint32_t)C + 16);
+    l.lds = l.off_vb + (K > 0 ? (uint32_t)P * PB : 0u);
     // 4-wave workgroups, two or more per CU; 8-wave ones for 16 x 16 images
     // whose layout leaves room for only one workgroup
     l.nwv = P > 128 && l.lds > 80 * 1024 ? 8 : 4;
@@ -559,34 +622,38 @@ size_t sq_bytes(int N, int G, int R) { return ((size_t)N * G * R * 4 + 255) & ~(
 
 }  // namespace mbc
 
-bool mbconv_supported(int H, int W, int C, int E, int R) {
-    return H >= 1 && W >= 1 && H <= mbc::HMAX && W <= mbc::WMAX && C >= 16 && C % 16 == 0 && E >= 1 &&
-           (E * C) % mbc::GH == 0 && E * C <= mbc::ECMAX && R >= 1 && R <= mbc::RMAX &&
-           mbc::layout(H, W, C, E * C, R).lds <= 160 * 1024;
+bool mbconv_supported(int H, int W, int C, int E, int R, int K) {
+    return H >= (K > 0 ? 2 : 1) && W >= (K > 0 ? 2 : 1) && H <= mbc::HMAX && W <= mbc::WMAX && C >= 16 &&
+           C % 16 == 0 && E >= 1 && (E * C) % mbc::GH == 0 && E * C <= mbc::ECMAX && R >= 1 && R <= mbc::RMAX &&
+           K >= 0 && K % 16 == 0 && K <= mbc::ECMAX && mbc::layout(H, W, C, E * C, R, K).lds <= 160 * 1024;
 }
 
 namespace {
 
 // The kernel instance for the shape and its launch size.
-const void *mbconv_kernel_for(int H, int W, int C, int EC, int R, int bf16, mbc::Layout *l, int *nt) {
-    *l = mbc::layout(H, W, C, EC, R);
-    *nt = l->nwv * 64;
-    const int P = H * W;
-    if (l->nwv == 8)
-        return bf16 ? (const void *)mbc::mbconv_kernel<BF16, 8, 2> : (const void *)mbc::mbconv_kernel<F16, 8, 2>;
+template <bool S2>
+const void *kernel_s(int nwv, int P, int bf16) {
+    if (nwv == 8)
+        return bf16 ? (const void *)mbc::mbconv_kernel<BF16, 8, 2, S2> : (const void *)mbc::mbconv_kernel<F16, 8, 2, S2>;
     if (P > 128)
-        return bf16 ? (const void *)mbc::mbconv_kernel<BF16, 4, 4> : (const void *)mbc::mbconv_kernel<F16, 4, 4>;
+        return bf16 ? (const void *)mbc::mbconv_kernel<BF16, 4, 4, S2> : (const void *)mbc::mbconv_kernel<F16, 4, 4, S2>;
     if (P > 64)
-        return bf16 ? (const void *)mbc::mbconv_kernel<BF16, 4, 2> : (const void *)mbc::mbconv_kernel<F16, 4, 2>;
-    return bf16 ? (const void *)mbc::mbconv_kernel<BF16, 4, 1> : (const void *)mbc::mbconv_kernel<F16, 4, 1>;
+        return bf16 ? (const void *)mbc::mbconv_kernel<BF16, 4, 2, S2> : (const void *)mbc::mbconv_kernel<F16, 4, 2, S2>;
+    return bf16 ? (const void *)mbc::mbconv_kernel<BF16, 4, 1, S2> : (const void *)mbc::mbconv_kernel<F16, 4, 1, S2>;
+}
+
+const void *mbconv_kernel_for(int H, int W, int C, int EC, int R, int K, int bf16, mbc::Layout *l, int *nt) {
+    *l = mbc::layout(H, W, C, EC, R, K);
+    *nt = l->nwv * 64;
+    return K > 0 ? kernel_s<true>(l->nwv, H * W, bf16) : kernel_s<false>(l->nwv, H * W, bf16);
 }
 
 }  // namespace
 
-hipError_t mbconv_resident_slots(int H, int W, int C, int E, int R, int bf16, int *slots) {
+hipError_t mbconv_resident_slots(int H, int W, int C, int E, int R, int K, int bf16, int *slots) {
     mbc::Layout l;
     int nt = 0;
-    const void *kf = mbconv_kernel_for(H, W, C, E * C, R, bf16, &l, &nt);
+    const void *kf = mbconv_kernel_for(H, W, C, E * C, R, K, bf16, &l, &nt);
     hipError_t e = allow_full_lds(kf);
     if (e != hipSuccess)
         return e;
@@ -597,12 +664,17 @@ hipError_t mbconv_resident_slots(int H, int W, int C, int E, int R, int bf16, in
     return hipSuccess;
 }
 
-size_t mbconv_workspace_bytes(int N, int H, int W, int C, int E, int R, int slots) {
-    const int G = E * C / mbc::GH;
-    return mbc::head_bytes() + mbc::sq_bytes(N, G, R) + 2 * (size_t)slots * H * W * E * C * 2;
+// pixels of the exchanged map: the block's output size
+static size_t mbconv_out_pixels(int H, int W, int K) {
+    return K > 0 ? (size_t)((H + 1) / 2) * ((W + 1) / 2) : (size_t)H * W;
 }
 
-hipError_t launch_mbconv(const void *x, void *y, const MBConvW &w, int N, int H, int W, int C, int E, int R,
+size_t mbconv_workspace_bytes(int N, int H, int W, int C, int E, int R, int K, int slots) {
+    const int G = E * C / mbc::GH;
+    return mbc::head_bytes() + mbc::sq_bytes(N, G, R) + 2 * (size_t)slots * mbconv_out_pixels(H, W, K) * E * C * 2;
+}
+
+hipError_t launch_mbconv(const void *x, void *y, const MBConvW &w, int N, int H, int W, int C, int E, int R, int K,
                          int bf16, void *ws, size_t ws_bytes, bool coop, hipStream_t st) {
     mbc::Args a{};
     a.x = (const uint16_t *)x;
@@ -627,16 +699,20 @@ hipError_t launch_mbconv(const void *x, void *y, const MBConvW &w, int N, int H,
     a.EC = E * C;
     a.R = R;
     a.G = a.EC / mbc::GH;
+    a.K = K > 0 ? K : C;
+    a.Ho = K > 0 ? (H + 1) / 2 : H;
+    a.Wo = K > 0 ? (W + 1) / 2 : W;
     mbc::Layout l;
     int nt = 0;
-    const void *kf = mbconv_kernel_for(H, W, C, a.EC, R, bf16, &l, &nt);
+    const void *kf = mbconv_kernel_for(H, W, C, a.EC, R, K, bf16, &l, &nt);
     a.off_gate = l.off_gate;
     a.off_z = l.off_z;
     a.off_cs = l.off_cs;
     a.off_vec = l.off_vec;
     a.off_w1 = l.off_w1;
+    a.off_vb = l.off_vb;
     const size_t fixed = mbc::head_bytes() + mbc::sq_bytes(N, a.G, R);
-    const size_t per_slot = 2 * (size_t)H * W * a.EC * 2;
+    const size_t per_slot = 2 * mbconv_out_pixels(H, W, K) * a.EC * 2;
     if (ws_bytes < fixed + per_slot)
         return hipErrorInvalidValue;
     char *base = (char *)ws;
@@ -649,7 +725,7 @@ hipError_t launch_mbconv(const void *x, void *y, const MBConvW &w, int N, int H,
     // run partly -- or, for a caller that owns the device, as an ordinary
     // launch, which then starts every workgroup at once
     int slots = 0;
-    hipError_t e = mbconv_resident_slots(H, W, C, E, R, bf16, &slots);
+    hipError_t e = mbconv_resident_slots(H, W, C, E, R, K, bf16, &slots);
     if (e != hipSuccess)
         return e;
     if (slots < 1)

@@ -110,13 +110,15 @@ def stem_params(seed: int, layer: int, C: int, dtype: str = "f16", scales: str =
 
 
 def mbconv_params(seed: int, layer: int, C: int, E: int, R: int, dtype: str = "f16",
-                  scales: str = "ones", bias_std: float | None = 0.1, gw: int = 8) -> dict:
+                  scales: str = "ones", bias_std: float | None = 0.1, gw: int = 8, K: int | None = None) -> dict:
     """Weights of one MBConv block with Squeeze & Excitation (expand, grouped
-    3x3 conv of group width gw, squeeze to R, excitation, project); tensor ids
-    100*(layer+1) + 0..12.  Weights ~ N(0, 1/fan_in): C (expand), 9*gw
-    (grouped conv), E*C (squeeze, project), R (excitation)."""
+    3x3 conv of group width gw, squeeze to R, excitation, project to K
+    channels, C unless given); tensor ids 100*(layer+1) + 0..12.  Weights ~
+    N(0, 1/fan_in): C (expand), 9*gw (grouped conv), E*C (squeeze, project),
+    R (excitation)."""
     base = 100 * (layer + 1)
     EC = E * C
+    K = C if K is None else K
     return {
         "w1": to_io(draw(seed, base + 0, (EC, C), (1.0 / C) ** 0.5), dtype),
         "s1": _vec(seed, base + 1, EC, "scale", bias_std, scales),
@@ -128,9 +130,9 @@ def mbconv_params(seed: int, layer: int, C: int, E: int, R: int, dtype: str = "f
         "br": _vec(seed, base + 7, R, "bias", bias_std, scales),
         "we": to_io(draw(seed, base + 8, (EC, R), (1.0 / R) ** 0.5), dtype),
         "be": _vec(seed, base + 9, EC, "bias", bias_std, scales),
-        "w2": to_io(draw(seed, base + 10, (C, EC), (1.0 / EC) ** 0.5), dtype),
-        "s3": _vec(seed, base + 11, C, "scale", bias_std, scales),
-        "b3": _vec(seed, base + 12, C, "bias", bias_std, scales),
+        "w2": to_io(draw(seed, base + 10, (K, EC), (1.0 / EC) ** 0.5), dtype),
+        "s3": _vec(seed, base + 11, K, "scale", bias_std, scales),
+        "b3": _vec(seed, base + 12, K, "bias", bias_std, scales),
     }
 
 

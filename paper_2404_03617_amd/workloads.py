@@ -55,6 +55,18 @@ MBCONV_WORKLOADS = {
         (192, 8, 43.1, 1.39), (256, 8, 51.4, 1.99)])
 }
 
+# The stride-2 MBConv + SE blocks of the speed-projection tables at 16 x 16
+# (App. A: the four model sizes' C = K = 128, 160, 192, 256, E = 4, down to
+# 8 x 8), batch 128, fp16, squeeze R = C/4 as for the stride-1 rows.  The
+# paper builds no kernel for them: paper_proj_ms is its projection (80% of
+# the stride-1 kernel's efficiency), not a measurement.
+MBCONV_S2_WORKLOADS = {
+    "mbconv_s2_n128_16x16_c%d_k%d_e4_r%d_f16" % (c, c, c // 4): dict(kind="mbconv_s2", N=128, H=16, W=16, C=c,
+                                                                    E=4, R=c // 4, K=c, k=3, dtype="f16",
+                                                                    seed=70 + i, paper_proj_ms=ms)
+    for i, (c, ms) in enumerate([(128, 0.282), (160, 0.595), (192, 0.819), (256, 0.835)])
+}
+
 # The network stem (a 3x3 stride-2 conv from the 256 x 256 image's 3 channels,
 # ReLU) fused into the first ConvFirst block at 128 x 128 (App. A, the first two
 # rows of the speed-projection tables: the Pico stem 3 -> 16 before ConvFirst

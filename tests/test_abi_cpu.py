@@ -19,7 +19,7 @@ pytestmark = pytest.mark.skipif(not os.path.exists(cf.library_path()),
 def declared_functions():
     src = open(HEADER).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(cf_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(cf_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_header_declares_the_binding_symbols():
@@ -428,6 +428,55 @@ def test_mbconv_forward_rejects():
     assert call(ws_bytes=n - 1) == cf.CF_ERR_WORKSPACE
     assert call(ws=None, ws_bytes=0) == cf.CF_ERR_WORKSPACE
     assert L.cf_last_error().decode().startswith("cf_mbconv_forward")
+
+
+def test_mbconv_s2_forward_rejects():
+    """The stride-2 MBConv entry point: the stride-1 checks plus K, the 2 x 2
+    minimum image (reflect padding) and no overlap of x and y at all; its
+    workspace holds the down-sampled map."""
+    L = cf.lib()
+    GW, WR, WE = 0x43000000, 0x44000000, 0x45000000
+
+    def need(N, H, W, C, E, R):
+        G = E * C // 64
+        return 256 + 2048 * 128 + (N * G * R * 4 + 255) // 256 * 256 + 2 * ((H + 1) // 2) * ((W + 1) // 2) * E * C * 2
+
+    def call(x=X, y=Y, ws=WS, ws_bytes=1 << 30, N=2, H=8, W=8, C=64, E=4, R=16, K=128, k=3, dt=0, launch=0, **kw):
+        p = cf._MBConvParams(w1=W1, s1=None, b1=None, gw_w=GW, s2=None, b2=None, wr=WR, br=None, we=WE, be=None,
+                             w2=W2, s3=None, b3=None)
+        for f, v in kw.items():
+            setattr(p, f, v)
+        return L.cf_mbconv_s2_forward(x, y, ws, ws_bytes, ctypes.byref(p), N, H, W, C, E, R, K, k, dt, launch, None)
+
+    assert L.cf_mbconv_s2_workspace_bytes(2, 8, 8, 64, 4, 16, 128, 0) >= need(2, 8, 8, 64, 4, 16)
+    assert L.cf_mbconv_s2_workspace_bytes(2, 7, 5, 64, 4, 16, 32, 1) >= need(2, 7, 5, 64, 4, 16)
+    assert L.cf_mbconv_s2_workspace_bytes(2, 8, 8, 64, 4, 16, 0, 0) == 0      # K = 0
+    assert L.cf_mbconv_s2_workspace_bytes(2, 8, 8, 64, 4, 16, 40, 0) == 0     # K not a multiple of 16
+    assert L.cf_mbconv_s2_workspace_bytes(2, 1, 8, 64, 4, 16, 64, 0) == 0     # H < 2
+    assert L.cf_mbconv_s2_workspace_bytes(2, 17, 8, 64, 4, 16, 64, 0) == 0    # H > 16
+    assert call(x=None) == cf.CF_ERR_INVALID
+    assert call(w2=None) == cf.CF_ERR_INVALID
+    assert call(K=0) == cf.CF_ERR_INVALID
+    assert call(K=-16) == cf.CF_ERR_INVALID
+    assert call(H=1) == cf.CF_ERR_INVALID           # reflect padding needs a second row
+    assert call(W=1) == cf.CF_ERR_INVALID
+    assert call(C=20) == cf.CF_ERR_INVALID
+    assert call(k=4) == cf.CF_ERR_INVALID
+    assert call(dt=5) == cf.CF_ERR_INVALID
+    assert call(launch=2) == cf.CF_ERR_INVALID
+    assert call(y=X) == cf.CF_ERR_INVALID            # no in-place form
+    assert call(y=X + 4096) == cf.CF_ERR_INVALID     # y overlaps x
+    assert call(s3=W1 + 4) == cf.CF_ERR_INVALID      # misaligned
+    assert call(ws=X) == cf.CF_ERR_INVALID           # ws overlaps x
+    assert call(k=5) == cf.CF_ERR_UNSUPPORTED
+    assert call(K=40) == cf.CF_ERR_UNSUPPORTED       # not a multiple of 16
+    assert call(H=17) == cf.CF_ERR_UNSUPPORTED
+    assert call(C=48, E=1) == cf.CF_ERR_UNSUPPORTED
+    assert call(C=512, E=4, H=16, W=16, K=512) == cf.CF_ERR_UNSUPPORTED  # V's LDS copy exceeds 160 KB
+    n = need(2, 8, 8, 64, 4, 16)
+    assert call(ws_bytes=n - 1) == cf.CF_ERR_WORKSPACE
+    assert call(ws=None, ws_bytes=0) == cf.CF_ERR_WORKSPACE
+    assert L.cf_last_error().decode().startswith("cf_mbconv_s2_forward")
 
 
 def test_stem_entry_points_reject():
