@@ -32,7 +32,8 @@ import torch
 import paper_2404_03617_amd as cf
 from paper_2404_03617_amd import roofline as rl
 from paper_2404_03617_amd import synth
-from paper_2404_03617_amd.workloads import BENCH_WORKLOAD, GBLOCK_WORKLOADS, MBCONV_WORKLOADS, STEM_WORKLOADS, WORKLOADS
+from paper_2404_03617_amd.workloads import (BENCH_WORKLOAD, GBLOCK_WORKLOADS, MBCONV_S2_WORKLOADS, MBCONV_WORKLOADS,
+                                            STEM_WORKLOADS, WORKLOADS)
 
 MALL_BYTES = 256 << 20
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -258,6 +259,35 @@ def mbconv_case(name: str, steps: int, warmup: int):
             "comp_eff": round(rl.comp_eff(flops, t), 4), "roofline": roofline_entry(flops, nbytes, t),
             "exclusive_launch_ms": round(te * 1e3, 4), "exclusive_launch_comp_eff": round(rl.comp_eff(flops, te), 4),
             "paper_A5000_comp_eff": round(w["paper_pct"] / 100, 3)}
+
+
+def mbconv_s2_case(name: str, steps: int, warmup: int):
+    """The stride-2 MBConv + SE block (BlurPool after the grouped conv, project
+    to K at half resolution) at one of the 16 x 16 rows of the paper's speed
+    projections, batch 128: one cooperative launch per step, and the same
+    grid as an ordinary launch."""
+    w = MBCONV_S2_WORKLOADS[name]
+    N, H, W, C, E, R, K = w["N"], w["H"], w["W"], w["C"], w["E"], w["R"], w["K"]
+    Ho, Wo = (H + 1) // 2, (W + 1) // 2
+    nsets = _sets_needed(N * H * W * C * 2 + N * Ho * Wo * K * 2)
+    xs = [synth.activations(w["seed"] + 100 * i, N, H, W, C, w["dtype"]).cuda() for i in range(nsets)]
+    ys = [torch.empty((N, Ho, Wo, K), dtype=xs[0].dtype, device="cuda") for _ in range(nsets)]
+    p = {kk: (None if v is None else v.cuda()) for kk, v in
+         synth.mbconv_params(w["seed"], 0, C, E, R, w["dtype"], K=K).items()}
+    ws = torch.zeros(cf.mbconv_s2_workspace_bytes(N, H, W, C, E, R, K), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    t = _time(lambda i: cf.mbconv_s2_forward(xs[i % nsets], p, out=ys[i % nsets], ws=ws), steps, warmup, stream)
+    te = _time(lambda i: cf.mbconv_s2_forward(xs[i % nsets], p, out=ys[i % nsets], ws=ws, launch="exclusive"),
+               steps, warmup, stream)
+    torch.cuda.synchronize()
+    if int(ws[:4].view(torch.int32).item()) != 0:
+        raise RuntimeError("%s: a barrier wait of the MBConv kernel gave up" % name)
+    flops = rl.mbconv_s2_flops(N, H, W, C, E, R, K)
+    nbytes = rl.mbconv_s2_bytes_fused(N, H, W, C, E, R, K)
+    return {"ms": round(t * 1e3, 4), "images_per_s": round(N / t, 1), "tflops": round(flops / t / 1e12, 1),
+            "comp_eff": round(rl.comp_eff(flops, t), 4), "roofline": roofline_entry(flops, nbytes, t),
+            "exclusive_launch_ms": round(te * 1e3, 4), "exclusive_launch_comp_eff": round(rl.comp_eff(flops, te), 4),
+            "paper_projection_ms_A5000": w["paper_proj_ms"]}
 
 
 def stem_case(name: str, steps: int, warmup: int):
@@ -520,6 +550,22 @@ def main():
         if args.calib_copy:
             calib_copy()
         return
+    if name in MBCONV_S2_WORKLOADS:
+        g = mbconv_s2_case(name, args.steps, args.warmup)
+        wg = MBCONV_S2_WORKLOADS[name]
+        cfg = {"workload": name, "N": wg["N"], "H": wg["H"], "W": wg["W"], "C": wg["C"], "E": wg["E"],
+               "R": wg["R"], "K": wg["K"], "k": wg["k"],
+               "kernel": "fused stride-2 MBConv + SE block with BlurPool (1 cooperative launch)"}
+        print(json.dumps({"metric": "images/sec and % of fp16 MFMA peak (computational efficiency), batch 128",
+                          "value": g["images_per_s"], "unit": "images/s", "n_gpus": 1, "steps": args.steps,
+                          "warmup": args.warmup, "ms_per_step": g["ms"], "higher_is_better": True,
+                          "scaling": "weak", "vs_baseline": None, "dtype": "f16",
+                          "data": "synthetic (seeded N(0,1) activations, N(0,1/fan_in) weights)",
+                          "config": cfg, "comp_eff": g["comp_eff"], "roofline": g["roofline"],
+                          "exclusive_launch_ms": g["exclusive_launch_ms"]}), flush=True)
+        if args.calib_copy:
+            calib_copy()
+        return
     if name in GBLOCK_WORKLOADS or name in MBCONV_WORKLOADS:
         # one of the paper's own block shapes as the timed workload (used for
         # profiles of that kernel); the default is the benchmark workload
@@ -643,6 +689,7 @@ def main():
         extra["paper_mbconv_table"] = {nm: mbconv_case(nm, max(5, args.steps // 2), 3) for nm in MBCONV_WORKLOADS}
         # the stem fused into the first block (App. A's first rows)
         extra["stem_first_block"] = {nm: stem_case(nm, max(5, args.steps // 2), 3) for nm in STEM_WORKLOADS}
+        extra["mbconv_stride2"] = {nm: mbconv_s2_case(nm, max(5, args.steps // 2), 3) for nm in MBCONV_S2_WORKLOADS}
         out["other_workloads"] = extra
     if args.calib_copy:
         calib_copy()

@@ -79,6 +79,26 @@ def mbconv_bytes_fused(N, H, W, C, E, R, k=3, gw=8, eb=2) -> int:
     return 2 * N * H * W * C * eb + weights + vectors
 
 
+def mbconv_s2_flops(N, H, W, C, E, R, K, k=3, gw=8) -> int:
+    """Stride-2 MBConv + SE (Fig. f:mbconv, stride 2): expand and grouped conv
+    at the input size, squeeze and excitation, project from E*C to K channels
+    at ceil(H/2) x ceil(W/2) -- the same four columns of the projection
+    tables, which leave out the BlurPool (9 multiply-adds per down-sampled
+    hidden value, not a matrix product)."""
+    P, Po = H * W, ((H + 1) // 2) * ((W + 1) // 2)
+    EC = E * C
+    return N * (2 * P * EC * C + 2 * P * EC * k * k * gw + 4 * EC * R + 2 * Po * K * EC)
+
+
+def mbconv_s2_bytes_fused(N, H, W, C, E, R, K, k=3, gw=8, eb=2) -> int:
+    """x read once, the down-sampled y written once, the five weight tensors
+    and the fp32 vectors once."""
+    EC = E * C
+    weights = eb * (EC * C + k * k * gw * EC + 2 * R * EC + K * EC)
+    vectors = 4 * (5 * EC + R + 2 * K)
+    return N * H * W * C * eb + N * ((H + 1) // 2) * ((W + 1) // 2) * K * eb + weights + vectors
+
+
 def block_weight_bytes(C, E, k, eb=2, vec_bytes=4) -> int:
     """dw taps, W1, W2 in the I/O dtype plus six fp32 scale/bias vectors."""
     return eb * (k * k * C + 2 * E * C * C) + vec_bytes * (2 * C + 2 * E * C + 2 * C)

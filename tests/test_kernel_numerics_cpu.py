@@ -129,6 +129,51 @@ def test_grouped_block_operation_count_reproduces_the_papers_table(row):
     assert tflops / 76.7 * 100 == pytest.approx(pct, abs=0.2)
 
 
+def _mbconv_rows():
+    rows = []
+    with open(os.path.join(ROOT, "tests", "golden", "mbconv_projection_rows.txt")) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                v = line.split()
+                rows.append(tuple(int(a) for a in v[:6]) + tuple(float(a) for a in v[6:10]) + (int(v[10]),
+                                                                                            float(v[11])))
+    return rows
+
+
+@pytest.mark.parametrize("row", _mbconv_rows(), ids=lambda r: "s%d_%dx%d_C%d_K%d" % (r[0], r[1], r[2], r[3], r[5]))
+def test_mbconv_operation_counts_reproduce_the_projection_tables(row):
+    """Each printed column of the paper's MBConv rows (two decimals, in
+    millions per image) from the operation count of the stride-1 or stride-2
+    block: the total, and each layer isolated by zeroing the other layers'
+    widths (zero pixels leave the squeeze/excitation, group width 0 removes
+    the grouped conv, K = 0 the project of the stride-2 block; the stride-1
+    expand and project count alike)."""
+    from paper_2404_03617_amd import roofline as rl
+    s, H, W, C, EC, K, conv, exp, prj, se, depth, total = row
+    E, R = EC // C, C // 4
+    assert E * C == EC
+
+    def f(H=H, W=W, gw=8, K=K):
+        if s == 1:
+            return rl.mbconv_flops(1, H, W, C, E, R, gw=gw) / 1e6
+        return rl.mbconv_s2_flops(1, H, W, C, E, R, K, gw=gw) / 1e6
+
+    if s == 1:
+        assert K == C
+    full = f()
+    assert full == pytest.approx(total / depth, abs=0.015)
+    assert full == pytest.approx(conv + exp + prj + se, abs=0.015)
+    assert f(H=0, W=0) == pytest.approx(se, abs=0.005)
+    assert full - f(gw=0) == pytest.approx(conv, abs=0.005)
+    if s == 1:
+        assert (f(gw=0) - f(H=0, W=0)) / 2 == pytest.approx(prj, abs=0.005)
+        assert exp == prj
+    else:
+        assert full - f(K=0) == pytest.approx(prj, abs=0.005)
+        assert f(gw=0, K=0) - f(H=0, W=0, K=0) == pytest.approx(exp, abs=0.005)
+
+
 # ---- the slice kernel's fp32 GELU: erf by Abramowitz & Stegun 7.1.26
 SLICE_HIP = os.path.join(ROOT, "paper_2404_03617_amd", "csrc", "cf_slice.hip")
 AS_BOUND = 1.5e-7  # the published bound of 7.1.26 on |erf error|
