@@ -10,11 +10,15 @@
 //     depth-wise conv writes D = s0 * conv + b0 to LDS over the taps (fp32
 //     accumulation; an item is a pixel and 8 channels, a thread keeps one
 //     channel chunk and its items in registers);
-//  2. wave w runs hidden chunks w, w + 8, ...: the expand (W1 fragments
-//     straight from global memory, four groups of K steps ahead, D fragments
-//     from LDS), phi(s1 u + b1) in fp32, and the projection onto the
-//     workgroup's 32 output channels (v_mfma_f32_32x32x16, weights as the A
-//     operand in the sigma / tau row orders of cf_fused_impl.h);
+//  2. wave w runs hidden chunks w, w + 8, ...: the expand on
+//     v_mfma_f32_16x16x32 (W1 straight from global memory, four adjacent
+//     lanes on 64 contiguous bytes of a row, four groups of K steps ahead,
+//     each dword then moved to its fragment lane by ds_bpermute one group
+//     ahead of its products; D fragments from LDS), phi(s1 u + b1) in fp32
+//     (s1, b1 staged in LDS), one exchange of quads between lanes l and
+//     l ^ 16, and the projection onto the workgroup's 32 output channels
+//     (v_mfma_f32_32x32x16, W2 rows in the tau order of cf_fused_impl.h as
+//     the A operand, loaded one chunk ahead);
 //  3. the waves' projections are summed in wave order and
 //     y = x + s2 * sum + b2 is stored.
 #include <algorithm>
@@ -28,7 +32,6 @@ namespace slice {
 
 using fused::float16v;
 using fused::mfma32;
-using fused::sigma_row;
 using fused::tau_row;
 
 constexpr int NW = 8, NT = NW * 64;
@@ -61,9 +64,9 @@ __device__ __forceinline__ float gelu_as(float u) {
 
 template <typename T, int C, int PB>
 struct Kern {
-    static constexpr int KST = C / 16, C8 = C / 8;
-    static constexpr int KG = KST >= 32 ? 4 : 2;        // K steps per W1 fragment group
-    static constexpr int NG = KST / KG;                 // groups per chunk (a multiple of the ring's 4)
+    static constexpr int KS = C / 32, C8 = C / 8;      // 32-element K steps of the expand
+    static constexpr int KG = KS >= 16 ? 2 : 1;         // K steps per W1 fragment group (4 KB or 2 KB a wave)
+    static constexpr int NG = KS / KG;                  // groups per chunk (a multiple of the ring's 4)
     static constexpr uint32_t XP = C * 2;               // LDS bytes per x pixel
     static constexpr uint32_t DP = C * 2 + 16;          // LDS bytes per D pixel (16-byte pad)
     static constexpr int NPX = PB * 32;
@@ -76,7 +79,8 @@ struct Kern {
     }
 
     static __device__ void run(const Args &a, uint8_t *smem) {
-        const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+        const int tid = threadIdx.x, lane = tid & 63;
+        const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: scalar loop control
         const int h = lane >> 5, m = lane & 31;
         const int o0 = blockIdx.x * 32;  // the workgroup's first output channel
 
@@ -103,6 +107,80 @@ struct Kern {
                     *reinterpret_cast<const u32x4 *>(a.dw_w + (size_t)i * 8);
         }
         __syncthreads();
+
+        // The wave's hidden chunks.  The expand runs on 16 x 16 x 32
+        // products: A = W1 rows 32 ch + 16 mt + r (r = lane & 15), elements
+        // 32 ks + 8 q .. + 7 (q = lane >> 4); B = D, pixel 32 pb + 16 nt + r, channels
+        // 32 ks + 8 q ..  Lane (q, r) then holds hidden 32 ch + 16 mt + 4 q + i
+        // of pixel 32 pb + 16 nt + r.  The projection (32 x 32 x 16, W2 rows
+        // o0 + tau(m) as the A operand) takes hidden 16 kk .. 16 kk + 15 of
+        // the chunk in natural order as its K step kk: lane (h, m) with
+        // m = 16 b + r needs hidden 16 kk + 8 h .. + 7 of pixel m; it holds
+        // the quad 16 kk + 8 h + 4 b of that pixel and receives the quad
+        // 16 kk + 8 h + 4 (1 - b) from lane l ^ 16, to which it sends its
+        // values of the partner's pixel.
+        const int NCH = a.EC / 32;
+        const int r = lane & 15, q = lane >> 4, b = q & 1;
+        const uint32_t dbase = a.off_d + (uint32_t)r * DP + (uint32_t)q * 16;
+        // W1 is read with lanes 4 i .. 4 i + 3 on 64 contiguous bytes of row i
+        // (the memory unit merges adjacent lanes only: in the fragment order
+        // every lane would start a row of its own) and each dword is then
+        // moved to its fragment lane (q, r), which takes row r, piece q from
+        // lane 4 r + q
+        const uint16_t *w1l = a.w1 + (size_t)(lane >> 2) * C + 8 * (lane & 3);
+        const int perm = (4 * r + q) * 4;  // ds_bpermute source address
+        const uint16_t *w2l = a.w2 + (size_t)(o0 + tau_row(m)) * a.EC + 8 * h;
+        float16v acc[PB];
+#pragma unroll
+        for (int pb = 0; pb < PB; pb++)
+#pragma unroll
+            for (int e = 0; e < 16; e++)
+                acc[pb][e] = 0.0f;
+        // W1 fragments stream through a ring of four groups held in
+        // registers: stream step st is group st % NG of the wave's chunk
+        // st / NG, loaded four steps before its products (across chunks)
+        const int ncw = wv < NCH ? (NCH - wv + NW - 1) / NW : 0;
+        const int steps = ncw * NG;
+        u32x4 f0[KG][2], f1[KG][2], f2[KG][2], f3[KG][2];
+        // (steps past the wave's last one reload its last group: every load
+        // is unconditional, so the compiler's count of loads in flight stays
+        // exact across the loop and it waits for one group, not all of them)
+        auto load_step = [&](int st, u32x4(&f)[KG][2]) {
+            const int sc = st < steps ? st : (steps > 0 ? steps - 1 : 0);
+            const int ch = steps > 0 ? wv + NW * (sc / NG) : 0, g = sc % NG;
+            const uint16_t *p = w1l + (size_t)ch * 32 * C + 32 * KG * g;
+#pragma unroll
+            for (int kk = 0; kk < KG; kk++)
+#pragma unroll
+                for (int mt = 0; mt < 2; mt++)
+                    f[kk][mt] = *reinterpret_cast<const u32x4 *>(p + (size_t)16 * mt * C + 32 * kk);
+        };
+        // W2 fragments of a chunk (output rows o0 + tau(m), hidden 32 ch + 16 kk
+        // + 8 h ..), loaded one chunk ahead into one of two register sets
+        auto load_w2 = [&](int cn, u32x4(&w)[2]) {
+            const int cc = cn < ncw ? cn : (ncw > 0 ? ncw - 1 : 0);
+            const int ch = ncw > 0 ? wv + NW * cc : 0;
+#pragma unroll
+            for (int kk = 0; kk < 2; kk++)
+                w[kk] = *reinterpret_cast<const u32x4 *>(w2l + ch * 32 + 16 * kk);
+        };
+        // the raw ring slots moved into fragment lanes (lane (q, r): row r, piece q)
+        auto permute = [&](const u32x4(&f)[KG][2], u32x4(&fa)[KG][2]) {
+#pragma unroll
+            for (int kk = 0; kk < KG; kk++)
+#pragma unroll
+                for (int mt = 0; mt < 2; mt++)
+#pragma unroll
+                    for (int d = 0; d < 4; d++)
+                        fa[kk][mt][d] = (uint32_t)__builtin_amdgcn_ds_bpermute(perm, (int)f[kk][mt][d]);
+        };
+        u32x4 wa[2], wb[2], pa[KG][2], pq[KG][2];
+        load_step(0, f0);
+        load_step(1, f1);
+        load_step(2, f2);
+        load_step(3, f3);
+        load_w2(0, wa);
+        // (the first ring groups and W2 fragments load during the depth-wise conv)
 
         // 1b. depth-wise conv; thread keeps channel chunk q and items
         // pl = tid / C8 + it * NT / C8 in registers, each tap read once from LDS
@@ -156,7 +234,14 @@ struct Kern {
                 sc[e] = a.s0 ? a.s0[q * 8 + e] : 1.0f;
                 bi[e] = a.b0 ? a.b0[q * 8 + e] : 0.0f;
             }
-            __syncthreads();  // every thread is done with the taps: D may overwrite them
+            __syncthreads();  // every thread is done with x and the taps: D and s1, b1 may overwrite them
+            // s1, b1 of every hidden channel (fp32) over the x pixels, so that
+            // the chunk loop reads them without a branch on null vectors
+            float *s1l = reinterpret_cast<float *>(smem), *b1l = s1l + a.EC;
+            for (int i = tid; i < a.EC; i += NT) {
+                s1l[i] = a.s1 ? a.s1[i] : 1.0f;
+                b1l[i] = a.b1 ? a.b1[i] : 0.0f;
+            }
 #pragma unroll
             for (int it = 0; it < IT; it++) {
                 const int pl = tid / C8 + it * (NT / C8);
@@ -171,104 +256,114 @@ struct Kern {
         }
         __syncthreads();
 
-        // 2. this wave's hidden chunks.  D fragment (block pb, K step ks):
-        // pixel 32 pb + m, channels 16 ks + 8 h ..; W1 fragment (chunk ch, K
-        // step ks): row 32 ch + sigma(m), elements 16 ks + 8 h ..; W2 fragment
-        // (chunk ch, K step kk): row o0 + tau(m), elements 32 ch + 16 kk + 8 h ..
-        const int NCH = a.EC / 32;
-        const uint32_t dbase = a.off_d + (uint32_t)m * DP + (uint32_t)h * 16;
-        const uint16_t *w1l = a.w1 + (size_t)sigma_row(m) * C + 8 * h;
-        const uint16_t *w2l = a.w2 + (size_t)(o0 + tau_row(m)) * a.EC + 8 * h;
-        float16v acc[PB];
-#pragma unroll
-        for (int pb = 0; pb < PB; pb++)
-#pragma unroll
-            for (int e = 0; e < 16; e++)
-                acc[pb][e] = 0.0f;
-        // W1 fragments stream through a ring of four groups held in
-        // registers: stream step st is group st % NG of the wave's chunk
-        // st / NG, loaded four steps before its products (across chunks)
-        const int ncw = wv < NCH ? (NCH - wv + NW - 1) / NW : 0;
-        const int steps = ncw * NG;
-        u32x4 f0[KG], f1[KG], f2[KG], f3[KG];
-        auto load_step = [&](int st, u32x4(&f)[KG]) {
-            if (st < steps) {
-                const int ch = wv + NW * (st / NG), g = st % NG;
-                const uint16_t *p = w1l + (size_t)ch * 32 * C + 16 * KG * g;
-#pragma unroll
-                for (int kk = 0; kk < KG; kk++)
-                    f[kk] = *reinterpret_cast<const u32x4 *>(p + 16 * kk);
-            }
-        };
-        load_step(0, f0);
-        load_step(1, f1);
-        load_step(2, f2);
-        load_step(3, f3);
-        for (int c = 0; c < ncw; c++) {
+        // 2. the wave's chunks (the ring and the first W2 fragments are in
+        // flight); the first group is permuted and its slot refilled
+        permute(f0, pa);
+        load_step(4, f0);
+        auto run_chunk = [&](int c, const u32x4(&w2c)[2], u32x4(&w2n)[2]) {
             const int ch = wv + NW * c;
-            // s1, b1 of the lane's hidden values (register e = 4t + i <->
-            // hidden 32 ch + 16 (t >> 1) + 8 h + 4 (t & 1) + i) and W2
-            float4v s1v[4], b1v[4];
+            // s1, b1 of the lane's hidden values (hidden 32 ch + 16 mt + 4 q + i)
+            const float *s1l = reinterpret_cast<const float *>(smem), *b1l = s1l + a.EC;
+            float4v s1v[2], b1v[2];
 #pragma unroll
-            for (int t = 0; t < 4; t++) {
-                const int r = ch * 32 + 16 * (t >> 1) + 8 * h + 4 * (t & 1);
-                s1v[t] = a.s1 ? *reinterpret_cast<const float4v *>(a.s1 + r) : float4v{1.f, 1.f, 1.f, 1.f};
-                b1v[t] = a.b1 ? *reinterpret_cast<const float4v *>(a.b1 + r) : float4v{0.f, 0.f, 0.f, 0.f};
+            for (int mt = 0; mt < 2; mt++) {
+                const int hr = ch * 32 + 16 * mt + 4 * q;
+                s1v[mt] = *reinterpret_cast<const float4v *>(s1l + hr);
+                b1v[mt] = *reinterpret_cast<const float4v *>(b1l + hr);
             }
-            u32x4 w2r[2];
-#pragma unroll
-            for (int kk = 0; kk < 2; kk++)
-                w2r[kk] = *reinterpret_cast<const u32x4 *>(w2l + ch * 32 + 16 * kk);
-            float16v hh[PB];
+            float4v hh[PB][2][2];  // [block][pixel half nt][hidden half mt]
 #pragma unroll
             for (int pb = 0; pb < PB; pb++)
 #pragma unroll
-                for (int e = 0; e < 16; e++)
-                    hh[pb][e] = 0.0f;
-            auto mma_group = [&](int g, const u32x4(&f)[KG]) {
+                for (int nt = 0; nt < 2; nt++)
+#pragma unroll
+                    for (int mt = 0; mt < 2; mt++)
+                        hh[pb][nt][mt] = float4v{0.f, 0.f, 0.f, 0.f};
+            auto mma_group = [&](int g, const u32x4(&fa)[KG][2]) {
 #pragma unroll
                 for (int kk = 0; kk < KG; kk++)
 #pragma unroll
-                    for (int pb = 0; pb < PB; pb++) {
-                        const u32x4 b = *reinterpret_cast<const u32x4 *>(
-                            smem + dbase + (uint32_t)pb * 32 * DP + (uint32_t)(g * KG + kk) * 32);
-                        hh[pb] = mfma32(f[kk], b, hh[pb], T{});
-                    }
+                    for (int pb = 0; pb < PB; pb++)
+#pragma unroll
+                        for (int nt = 0; nt < 2; nt++) {
+                            const u32x4 bd = *reinterpret_cast<const u32x4 *>(
+                                smem + dbase + (uint32_t)(32 * pb + 16 * nt) * DP + (uint32_t)(g * KG + kk) * 64);
+#pragma unroll
+                            for (int mt = 0; mt < 2; mt++)
+                                hh[pb][nt][mt] = T::mfma(fa[kk][mt], bd, hh[pb][nt][mt]);
+                        }
             };
             // four groups per pass (a runtime loop keeps the reads of D that
-            // the scheduler hoists to one pass)
+            // the scheduler hoists to one pass).  While group j's products
+            // run, group j + 1's fragments are permuted into the other
+            // buffer and their raw slot is refilled four groups ahead; the
+            // order is pinned
 #pragma unroll 1
             for (int g = 0; g < NG; g += 4) {
                 const int st = c * NG + g;
-                mma_group(g, f0);
-                load_step(st + 4, f0);
-                mma_group(g + 1, f1);
+                mma_group(g, pa);
+                permute(f1, pq);
                 load_step(st + 5, f1);
-                mma_group(g + 2, f2);
+                __builtin_amdgcn_sched_barrier(0);
+                mma_group(g + 1, pq);
+                permute(f2, pa);
                 load_step(st + 6, f2);
-                mma_group(g + 3, f3);
+                __builtin_amdgcn_sched_barrier(0);
+                mma_group(g + 2, pa);
+                permute(f3, pq);
                 load_step(st + 7, f3);
+                __builtin_amdgcn_sched_barrier(0);
+                mma_group(g + 3, pq);
+                permute(f0, pa);
+                load_step(st + 8, f0);
+                __builtin_amdgcn_sched_barrier(0);
             }
-            // phi(s1 u + b1), rounded to the I/O dtype: the B operand of the projection
+            // the next chunk's W2 fragments, behind this chunk's ring refills
+            load_w2(c + 1, w2n);
+            // phi(s1 u + b1), rounded to the I/O dtype; the lane pair (l, l ^ 16)
+            // trades quads so that each lane holds hidden 16 kk + 8 h .. + 7 of
+            // its pixel m: the B operand of the projection
 #pragma unroll
             for (int pb = 0; pb < PB; pb++) {
-                uint32_t gq[8];
+                uint32_t pk[2][2][2];  // [nt][mt][pair]
 #pragma unroll
-                for (int q2 = 0; q2 < 8; q2++) {
-                    const int e0 = 2 * q2, e1 = e0 + 1;
-                    const float u0 = act(fmaf(hh[pb][e0], s1v[e0 >> 2][e0 & 3], b1v[e0 >> 2][e0 & 3]), a.act);
-                    const float u1 = act(fmaf(hh[pb][e1], s1v[e1 >> 2][e1 & 3], b1v[e1 >> 2][e1 & 3]), a.act);
-                    gq[q2] = T::pack2(u0, u1);
-                }
+                for (int nt = 0; nt < 2; nt++)
+#pragma unroll
+                    for (int mt = 0; mt < 2; mt++)
+#pragma unroll
+                        for (int j = 0; j < 2; j++) {
+                            const float u0 = act(fmaf(hh[pb][nt][mt][2 * j], s1v[mt][2 * j], b1v[mt][2 * j]), a.act);
+                            const float u1 =
+                                act(fmaf(hh[pb][nt][mt][2 * j + 1], s1v[mt][2 * j + 1], b1v[mt][2 * j + 1]), a.act);
+                            pk[nt][mt][j] = T::pack2(u0, u1);
+                        }
 #pragma unroll
                 for (int kk = 0; kk < 2; kk++) {
-                    const u32x4 hid = {gq[4 * kk], gq[4 * kk + 1], gq[4 * kk + 2], gq[4 * kk + 3]};
-                    acc[pb] = mfma32(w2r[kk], hid, acc[pb], T{});
+                    uint32_t own[2], rcv[2];
+#pragma unroll
+                    for (int j = 0; j < 2; j++) {
+                        own[j] = b ? pk[1][kk][j] : pk[0][kk][j];
+                        const uint32_t snd = b ? pk[0][kk][j] : pk[1][kk][j];
+                        rcv[j] = (uint32_t)__shfl_xor((int)snd, 16);
+                    }
+                    const u32x4 hid =
+                        b ? u32x4{rcv[0], rcv[1], own[0], own[1]} : u32x4{own[0], own[1], rcv[0], rcv[1]};
+                    acc[pb] = mfma32(w2c[kk], hid, acc[pb], T{});
                 }
             }
+        };
+        // two chunks per iteration, so the W2 register sets alternate without a copy
+        int c = 0;
+        for (; c + 1 < ncw; c += 2) {
+            run_chunk(c, wa, wb);
+            run_chunk(c + 1, wb, wa);
         }
+        if (c < ncw)
+            run_chunk(c, wa, wb);
 
-        // 3. projections into the x area (free since the depth-wise barrier):
+        __syncthreads();  // every wave is done with s1, b1
+
+        // 3. projections into the x area:
         // wave w, block pb, register quad g4 of lane l at float index
         // ((w * PB + pb) * 4 + g4) * 256 + 4 l; register e of lane (h, m) is
         // channel o0 + 16 h + e of pixel 32 pb + m
@@ -312,7 +407,7 @@ __global__ __launch_bounds__(NT, 1) void slice_kernel(Args a) {
     Kern<T, C, PB>::run(a, smem);
 }
 
-// LDS layout: [x pixels | the waves' projections] [zero piece] [taps | D pixels]
+// LDS layout: [x pixels | s1, b1 (fp32) | the waves' projections] [zero piece] [taps | D pixels]
 struct Plan {
     int pb;
     uint32_t off_zero, off_d;
@@ -326,7 +421,7 @@ inline bool plan(const Shape &s, Plan &pl) {
         return false;
     pl.pb = P <= 32 ? 1 : 2;
     const size_t npx = (size_t)pl.pb * 32;
-    const size_t r0 = std::max(npx * s.C * 2, (size_t)NW * pl.pb * 4096);
+    const size_t r0 = std::max(std::max(npx * s.C * 2, (size_t)NW * pl.pb * 4096), (size_t)s.E * s.C * 8);
     pl.off_zero = (uint32_t)((r0 + 255) & ~(size_t)255);
     pl.off_d = pl.off_zero + 256;
     // the D region first holds the taps [k][k][C]
