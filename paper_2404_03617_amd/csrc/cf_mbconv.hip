@@ -166,6 +166,22 @@ struct MB {
         const int tid = threadIdx.x, lane = tid & 63;
         const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
         const int q = lane >> 4, jl = lane & 15;
+        // Fragments read straight from global memory (x in the expand, W2 in
+        // the projection) are loaded with four adjacent lanes on 64
+        // contiguous bytes of one row (lane l: row l / 4, piece l % 4) -- the
+        // memory unit merges only adjacent lanes, and in fragment order every
+        // lane would start a row of its own -- and each dword then moves to
+        // its fragment lane (q, jl), which takes row jl, piece q from lane
+        // 4 jl + q
+        const int lr = lane >> 2, lp = lane & 3;
+        const int perm = (4 * jl + q) * 4;  // ds_bpermute source address
+        auto permute = [&](const u32x4 &v) {
+            u32x4 o;
+#pragma unroll
+            for (int d = 0; d < 4; d++)
+                o[d] = (uint32_t)__builtin_amdgcn_ds_bpermute(perm, (int)v[d]);
+            return o;
+        };
         const int M = gridDim.x;
         int lin = blockIdx.x;
         if (a.xcd_map)  // workgroup i runs on XCD i % 8
@@ -247,14 +263,19 @@ struct MB {
                     u32x4 bv[KE][NPW];
 #pragma unroll
                     for (int j = 0; j < KE; j++) {
-                        const int k = 32 * (k0 + j) + 8 * q;
+                        const int k = 32 * (k0 + j) + 8 * lp;
                         const bool kin = k < C;  // past ks, or the half-padded last step of C % 32 == 16
 #pragma unroll
                         for (int i = 0; i < NPW; i++) {
-                            const int p = 16 * (wv + NWV * i) + jl;
+                            const int p = 16 * (wv + NWV * i) + lr;
                             bv[j][i] = kin && p < P ? ld16(xn + (size_t)p * C + k) : u32x4{0u, 0u, 0u, 0u};
                         }
                     }
+#pragma unroll
+                    for (int j = 0; j < KE; j++)
+#pragma unroll
+                        for (int i = 0; i < NPW; i++)
+                            bv[j][i] = permute(bv[j][i]);
 #pragma unroll
                     for (int j = 0; j < KE; j++) {
                         if (k0 + j >= ks)  // wave-uniform
@@ -511,7 +532,7 @@ struct MB {
                     const uint8_t *vl0 = U + (uint32_t)(16 * u0 + jl) * pitch + (uint32_t)q * 16;
                     const uint8_t *vl1 = vl0 + 16 * pitch;
                     for (int ot = ot0 + wv; ot < ot1; ot += NWV) {
-                        const uint16_t *wrow = a.w2 + (size_t)(16 * ot + jl) * EC + 8 * q;
+                        const uint16_t *wrow = a.w2 + (size_t)(16 * ot + lr) * EC + 8 * lp;
                         const int o = 16 * ot + 4 * q;
                         u32x2 xv0 = {0u, 0u}, xv1 = {0u, 0u};  // the residual (stride 1 only)
                         if (!S2 && p0 < P)
@@ -533,9 +554,10 @@ struct MB {
                                 const int kk = KB * b + j;
                                 if (kk >= kst)
                                     break;
-                                acc0 = T::mfma(w[j], *reinterpret_cast<const u32x4 *>(vl0 + (uint32_t)kk * 64), acc0);
+                                const u32x4 wf = permute(w[j]);
+                                acc0 = T::mfma(wf, *reinterpret_cast<const u32x4 *>(vl0 + (uint32_t)kk * 64), acc0);
                                 if (two)
-                                    acc1 = T::mfma(w[j], *reinterpret_cast<const u32x4 *>(vl1 + (uint32_t)kk * 64),
+                                    acc1 = T::mfma(wf, *reinterpret_cast<const u32x4 *>(vl1 + (uint32_t)kk * 64),
                                                    acc1);
                             }
                         };
