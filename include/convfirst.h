@@ -137,7 +137,8 @@ size_t cf_stage_microbatch_workspace_bytes(int depth, int N, int H, int W, int C
 /* 2x2 stride-2 conv between stages: y[n][i][j][o] = scale[o] * sum_{a,b,c}
  * w[o][a][b][c] * x[n][2i+a][2j+b][c] + bias[o]  (eq. f:conv2d with R = S = 2,
  * stride 2, no padding; no activation, no residual).  H and W must be even;
- * y is [N][H/2][W/2][Cout].  Cin and Cout must be multiples of 32. */
+ * y is [N][H/2][W/2][Cout].  Cin must be a multiple of 32, Cout of 64, and
+ * N*(H/2)*(W/2) below 2^31 (CF_ERR_UNSUPPORTED otherwise). */
 cf_status cf_downsample_forward(const void *x, void *y, const cf_down_params *p,
                                 int N, int H, int W, int Cin, int Cout,
                                 cf_dtype dt, void *stream);

@@ -508,10 +508,17 @@ cf_status cf_stage_forward_microbatch(const void *x, void *y, void *ws, size_t w
     const size_t img = (size_t)H * W * C * elem_bytes(dt);
     const size_t one = round256((size_t)m * img);
     char *buf[2] = {(char *)ws, (char *)ws + one};
+    // the schedule reproduces the plain stage bit for bit: a micro-batch small
+    // enough for the slice kernel (whose expand sums in another order) runs
+    // the tile kernels of the whole batch when that batch is not itself a
+    // slice shape
+    const bool full_slice = cf::slice_applies(to_shape(N, H, W, C, E, k, dt, act));
     for (int n0 = 0; n0 < N; n0 += m) {
         const int mb = N - n0 < m ? N - n0 : m;
         cf::Shape s = to_shape(mb, H, W, C, E, k, dt, act);
         s.cfg = tuned_config(s);
+        if (s.cfg == cf::CFG_DEFAULT && !full_slice && cf::slice_applies(s) && cf::tile_fits(s))
+            s.cfg = cf::CFG_TILE;
         const void *in = (const char *)x + (size_t)n0 * img;
         for (int i = 0; i < depth; i++) {
             void *out = (i == depth - 1) ? (void *)((char *)y + (size_t)n0 * img) : (void *)buf[i & 1];
@@ -548,6 +555,8 @@ cf_status cf_downsample_forward(const void *x, void *y, const cf_down_params *p,
     if (Cin % 32 || Cout % 64)
         return fail(CF_ERR_UNSUPPORTED, "%s: needs Cin %% 32 == 0 and Cout %% 64 == 0 (got %d, %d)", what, Cin,
                     Cout);
+    if ((int64_t)N * (H / 2) * (W / 2) >= ((int64_t)1 << 31))
+        return fail(CF_ERR_UNSUPPORTED, "%s: N*(H/2)*(W/2) must be below 2^31", what);
     hipError_t e = cf::launch_downsample(x, y, p->w, p->scale, p->bias, N, H, W, Cin, Cout, dt == CF_BF16,
                                          (hipStream_t)stream);
     if (e != hipSuccess)

@@ -51,22 +51,9 @@ namespace fused {
 
 typedef float float16v __attribute__((ext_vector_type(16)));
 
-// n / d for n < 2^31 by multiply-high (Granlund-Montgomery): q = (umulhi(n, m) + n) >> s.
-struct FastDiv {
-    uint32_t d, m, s;
-};
-
-inline FastDiv make_fastdiv(uint32_t d) {
-    uint32_t s = 0;
-    while ((1ull << s) < d)
-        s++;
-    const uint64_t m = (((1ull << s) - d) << 32) / d + 1;
-    return FastDiv{d, (uint32_t)m, s};
-}
-
-__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv &f) {
-    return (__umulhi(n, f.m) + n) >> f.s;
-}
+using cf::FastDiv;
+using cf::fdiv;
+using cf::make_fastdiv;
 
 struct FusedArgs {
     const uint16_t *x;

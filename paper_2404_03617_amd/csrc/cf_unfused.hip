@@ -16,21 +16,39 @@ namespace {
 
 // ---------------------------------------------------------------------------
 // Depth-wise k x k conv, NHWC, zero padding k/2: one thread = 8 channels of
-// one pixel, fp32 accumulation, d = s0 * acc + b0.
+// one pixel, fp32 accumulation, d = s0 * acc + b0.  The thread index is split
+// into (pixel, channel group) and the pixel into (n, h, w) by 32-bit
+// multiply-high division when N*H*W*C/8 < 2^31 (64-bit division otherwise).
+struct DwDiv {
+    FastDiv c8, w, h;
+    int small;  // N*H*W*C/8 < 2^31
+};
+
 template <typename T, int KS>
 __global__ __launch_bounds__(256) void dw_kernel(const uint16_t *x, uint16_t *d, const uint16_t *w, const float *s0,
-                                                 const float *b0, int N, int H, int W, int C) {
+                                                 const float *b0, int N, int H, int W, int C, DwDiv dv) {
     const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int c8 = C / 8;
     const int64_t total = (int64_t)N * H * W * c8;
     if (t >= total)
         return;
-    const int q8 = (int)(t % c8);
-    const int64_t pix = t / c8;
-    const int wc = (int)(pix % W);
-    const int64_t nh = pix / W;
-    const int h = (int)(nh % H);
-    const int64_t n = nh / H;
+    int q8, wc, h;
+    int64_t pix, n;
+    if (dv.small) {
+        const uint32_t tt = (uint32_t)t, px = fdiv(tt, dv.c8), nh = fdiv(px, dv.w), nn = fdiv(nh, dv.h);
+        q8 = (int)(tt - px * (uint32_t)c8);
+        wc = (int)(px - nh * (uint32_t)W);
+        h = (int)(nh - nn * (uint32_t)H);
+        pix = px;
+        n = nn;
+    } else {
+        q8 = (int)(t % c8);
+        pix = t / c8;
+        wc = (int)(pix % W);
+        const int64_t nh = pix / W;
+        h = (int)(nh % H);
+        n = nh / H;
+    }
     const int c0 = q8 * 8;
     constexpr int PAD = KS / 2;
     float acc[8];
@@ -88,7 +106,9 @@ struct GemmArgs {
     int K, NO;
     int act;
     // space-to-depth view: x is [N][2*Ho][2*Wo][Cin], row p = (n, i, j), K = 4*Cin
+    // (P < 2^31: 32-bit multiply-high division by Wo, Ho and Cin)
     int Ho, Wo, Cin;
+    FastDiv divWo, divHo, divCin;
 };
 
 
@@ -101,12 +121,10 @@ __device__ __forceinline__ const uint16_t *a_row_start(const GemmArgs &g, int64_
     if constexpr (AMODE == A_PLAIN) {
         return g.a + p * g.K;
     } else {
-        const int64_t ni = p / g.Wo;
-        const int j = (int)(p - ni * g.Wo);
-        const int64_t n = ni / g.Ho;
-        const int i = (int)(ni - n * g.Ho);
-        const int64_t W = 2 * (int64_t)g.Wo;
-        return g.a + ((n * 2 * g.Ho + 2 * i) * W + 2 * j) * g.Cin;
+        const uint32_t pp = (uint32_t)p, ni = fdiv(pp, g.divWo), j = pp - ni * (uint32_t)g.Wo;
+        const uint32_t n = fdiv(ni, g.divHo), i = ni - n * (uint32_t)g.Ho;
+        const size_t W = 2 * (size_t)g.Wo;
+        return g.a + (((size_t)n * 2 * g.Ho + 2 * i) * W + 2 * j) * g.Cin;
     }
 }
 // offset of element k from the row start
@@ -115,7 +133,7 @@ __device__ __forceinline__ int64_t a_col_off(const GemmArgs &g, int k) {
     if constexpr (AMODE == A_PLAIN) {
         return k;
     } else {
-        const int ab = k / g.Cin, c = k - ab * g.Cin;
+        const int ab = (int)fdiv((uint32_t)k, g.divCin), c = k - ab * g.Cin;
         return ((int64_t)(ab >> 1) * 2 * g.Wo + (ab & 1)) * g.Cin + c;
     }
 }
@@ -327,11 +345,16 @@ hipError_t dw(const void *x, void *d, const BlockW &w, const Shape &s, hipStream
     const uint16_t *xx = (const uint16_t *)x;
     uint16_t *dd = (uint16_t *)d;
     const uint16_t *ww = (const uint16_t *)w.dw_w;
+    DwDiv dv;
+    dv.c8 = make_fastdiv((uint32_t)(s.C / 8));
+    dv.w = make_fastdiv((uint32_t)s.W);
+    dv.h = make_fastdiv((uint32_t)s.H);
+    dv.small = total < ((int64_t)1 << 31) ? 1 : 0;
     switch (s.k) {
-    case 1: hipLaunchKernelGGL((dw_kernel<T, 1>), dim3(nb), dim3(256), 0, st, xx, dd, ww, w.s0, w.b0, s.N, s.H, s.W, s.C); break;
-    case 3: hipLaunchKernelGGL((dw_kernel<T, 3>), dim3(nb), dim3(256), 0, st, xx, dd, ww, w.s0, w.b0, s.N, s.H, s.W, s.C); break;
-    case 5: hipLaunchKernelGGL((dw_kernel<T, 5>), dim3(nb), dim3(256), 0, st, xx, dd, ww, w.s0, w.b0, s.N, s.H, s.W, s.C); break;
-    case 7: hipLaunchKernelGGL((dw_kernel<T, 7>), dim3(nb), dim3(256), 0, st, xx, dd, ww, w.s0, w.b0, s.N, s.H, s.W, s.C); break;
+    case 1: hipLaunchKernelGGL((dw_kernel<T, 1>), dim3(nb), dim3(256), 0, st, xx, dd, ww, w.s0, w.b0, s.N, s.H, s.W, s.C, dv); break;
+    case 3: hipLaunchKernelGGL((dw_kernel<T, 3>), dim3(nb), dim3(256), 0, st, xx, dd, ww, w.s0, w.b0, s.N, s.H, s.W, s.C, dv); break;
+    case 5: hipLaunchKernelGGL((dw_kernel<T, 5>), dim3(nb), dim3(256), 0, st, xx, dd, ww, w.s0, w.b0, s.N, s.H, s.W, s.C, dv); break;
+    case 7: hipLaunchKernelGGL((dw_kernel<T, 7>), dim3(nb), dim3(256), 0, st, xx, dd, ww, w.s0, w.b0, s.N, s.H, s.W, s.C, dv); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -391,6 +414,11 @@ hipError_t launch_downsample(const void *x, void *y, const void *wd, const float
     g.P = (int64_t)N * g.Ho * g.Wo;
     g.K = 4 * Cin;
     g.NO = Cout;
+    if (g.P >= ((int64_t)1 << 31))
+        return hipErrorInvalidValue;
+    g.divWo = make_fastdiv((uint32_t)g.Wo);
+    g.divHo = make_fastdiv((uint32_t)g.Ho);
+    g.divCin = make_fastdiv((uint32_t)Cin);
     return bf16 ? gemm<BF16, EPI_AFFINE, A_SPACE_TO_DEPTH>(g, st) : gemm<F16, EPI_AFFINE, A_SPACE_TO_DEPTH>(g, st);
 }
 
