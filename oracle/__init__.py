@@ -63,6 +63,7 @@ def lib():
         L.cfref_mbconv_forward.argtypes = [_dp] * 14 + [ci] * 8 + [_dp]
         L.cfref_mbconv_s2_forward.argtypes = [_dp] * 14 + [ci] * 9 + [_dp]
         L.cfref_blurpool_tri3.argtypes = [_dp, ci, ci, ci, ci, _dp]
+        L.cfref_convfirst_s2_forward.argtypes = [_dp] * 10 + [ci] * 9 + [_dp]
         L.cfref_default_threads.restype = ci
         _lib = L
     return _lib
@@ -283,6 +284,29 @@ def mbconv_s2_forward(x, p: dict):
     rc = lib().cfref_mbconv_s2_forward(_p(x), _p(w1), _p(vec[0]), _p(vec[1]), _p(a), _p(vec[2]), _p(vec[3]),
                                        _p(wr), _p(vec[4]), _p(we), _p(vec[5]), _p(w2), _p(vec[6]), _p(vec[7]),
                                        N, H, W, C, EC // C, R, K, k, gw, _p(y))
+    assert rc == 0
+    return y
+
+
+def convfirst_s2_forward(x, p: dict, act: str = "relu"):
+    """The stride-2 ConvFirst block (Fig. f:convfirst-block (c)) in the
+    reading the speed-projection counts support (App. A): grouped conv C -> C
+    with its folded norm at the input size, blurpool_tri3 of the conv output
+    and of the block input, the two concatenated (2C channels, conv output
+    first), expand to R with activation, project to K, no residual.  p holds
+    gw_w [k,k,C,gw], w1 [R,2C], w2 [K,R] and optional s0,b0 [C], s1,b1 [R],
+    s2,b2 [K].  x [N,H,W,C] with H, W >= 2 -> [N, ceil(H/2), ceil(W/2), K]."""
+    x = _f64(x)
+    N, H, W, C = x.shape
+    a, w1, w2 = _f64(p["gw_w"]), _f64(p["w1"]), _f64(p["w2"])
+    k, _, _, gw = a.shape
+    R, K = w1.shape[0], w2.shape[0]
+    assert a.shape == (k, k, C, gw) and w1.shape == (R, 2 * C) and w2.shape == (K, R)
+    vec = [_f64(p.get(n)) for n in ("s0", "b0", "s1", "b1", "s2", "b2")]
+    y = np.empty((N, (H + 1) // 2, (W + 1) // 2, K))
+    rc = lib().cfref_convfirst_s2_forward(_p(x), _p(a), _p(vec[0]), _p(vec[1]), _p(w1), _p(vec[2]), _p(vec[3]),
+                                          _p(w2), _p(vec[4]), _p(vec[5]), N, H, W, C, R, K, k, gw, ACTS[act],
+                                          _p(y))
     assert rc == 0
     return y
 

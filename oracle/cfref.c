@@ -645,3 +645,68 @@ int cfref_mbconv_s2_forward(const double *x, const double *w1, const double *s1,
 {
     return mbconv_core(x, w1, s1, b1, gwt, s2, b2, wr, br, we, be, w2, s3, b3, N, H, W, C, E, R, k, gw, 2, K, y);
 }
+
+/* ------------------------------------------------------------------------ */
+/* The stride-2 ConvFirst block (Fig. f:convfirst-block (c): the variant that
+ * down-samples with BlurPool, Triangle-3).  Reading taken (the figure is not
+ * in the text): the grouped k x k conv C -> C at the input size with its
+ * folded norm, D = s0 * gconv(X) + b0; BlurPool of D and of the block input
+ * X; the two down-sampled maps concatenated along channels, Z = [bp(D),
+ * bp(X)] (2C channels, D's first); then the FFN at the output size,
+ *   U = phi(s1 * (W1 Z) + b1),  Y = s2 * (W2 U) + b2,
+ * with no residual (the output has K channels on a ceil(H/2) x ceil(W/2)
+ * map).  Per image this counts 2 H W C k^2 gw (conv), 2 Ho Wo 2C R (expand)
+ * and 2 Ho Wo R K (project) operations, the Conv, Exp and Prj columns of
+ * the stride-2 ConvFirst rows of the speed-projection tables (App. A).
+ *   x [N][H][W][C], gwt [k][k][C][gw], w1 [R][2C], w2 [K][R]; s0, b0 [C];
+ *   s1, b1 [R]; s2, b2 [K]; y [N][ceil(H/2)][ceil(W/2)][K]; H, W >= 2. */
+int cfref_convfirst_s2_forward(const double *x, const double *gwt, const double *s0, const double *b0,
+                               const double *w1, const double *s1, const double *b1, const double *w2,
+                               const double *s2, const double *b2, int N, int H, int W, int C, int R,
+                               int K, int k, int gw, int act, double *y)
+{
+    if (N < 0 || H < 2 || W < 2 || C <= 0 || R <= 0 || K <= 0 || k <= 0 || k % 2 == 0 || gw <= 0 || C % gw)
+        return -1;
+    const int Ho = (H + 1) / 2, Wo = (W + 1) / 2, C2 = 2 * C;
+    const size_t P = (size_t)H * W, Po = (size_t)Ho * Wo;
+    double *D = malloc(sizeof(double) * P * C);
+    double *Dd = malloc(sizeof(double) * Po * C);
+    double *Xd = malloc(sizeof(double) * Po * C);
+    double *Z = malloc(sizeof(double) * C2);
+    double *U = malloc(sizeof(double) * R);
+    if (!D || !Dd || !Xd || !Z || !U) {
+        free(D); free(Dd); free(Xd); free(Z); free(U);
+        return -1;
+    }
+    for (int n = 0; n < N; n++) {
+        /* the grouped conv and its norm at the input size */
+        for (int h = 0; h < H; h++)
+            for (int w = 0; w < W; w++)
+                gconv_pixel(x, gwt, s0, b0, H, W, C, k, gw, n, h, w, D + ((size_t)h * W + w) * C);
+        /* both maps down-sampled */
+        blurpool_tri3(D, H, W, C, Dd);
+        blurpool_tri3(x + (size_t)n * P * C, H, W, C, Xd);
+        for (size_t p = 0; p < Po; p++) {
+            for (int c = 0; c < C; c++) {
+                Z[c] = Dd[p * C + c];
+                Z[C + c] = Xd[p * C + c];
+            }
+            /* expand, norm, activation */
+            for (int r = 0; r < R; r++) {
+                double acc = 0.0;
+                for (int c = 0; c < C2; c++)
+                    acc += w1[(size_t)r * C2 + c] * Z[c];
+                U[r] = cfref_act((s1 ? s1[r] : 1.0) * acc + (b1 ? b1[r] : 0.0), act);
+            }
+            /* project and norm */
+            for (int o = 0; o < K; o++) {
+                double acc = 0.0;
+                for (int r = 0; r < R; r++)
+                    acc += w2[(size_t)o * R + r] * U[r];
+                y[((size_t)n * Po + p) * K + o] = (s2 ? s2[o] : 1.0) * acc + (b2 ? b2[o] : 0.0);
+            }
+        }
+    }
+    free(D); free(Dd); free(Xd); free(Z); free(U);
+    return 0;
+}

@@ -41,6 +41,10 @@ int cfref_mbconv_forward(const double *x, const double *w1, const double *s1, co
                          const double *s2, const double *b2, const double *wr, const double *br, const double *we,
                          const double *be, const double *w2, const double *s3, const double *b3, int N, int H,
                          int W, int C, int E, int R, int k, int gw, double *y);
+int cfref_convfirst_s2_forward(const double *x, const double *gwt, const double *s0, const double *b0,
+                               const double *w1, const double *s1, const double *b1, const double *w2,
+                               const double *s2, const double *b2, int N, int H, int W, int C, int R,
+                               int K, int k, int gw, int act, double *y);
 
 static uint64_t rng = 0x9e3779b97f4a7c15ull;
 
@@ -142,6 +146,22 @@ static void mbconv_case(int N, int H, int W, int C, int E, int R, int k, int wit
     free(s1); free(b1); free(s2); free(b2); free(br); free(be); free(s3); free(b3);
 }
 
+static void convfirst_s2_case(int N, int H, int W, int C, int R, int K, int with_vectors)
+{
+    const int Ho = (H + 1) / 2, Wo = (W + 1) / 2;
+    double *x = buf((size_t)N * H * W * C), *gwt = buf((size_t)9 * C * 8), *w1 = buf((size_t)R * 2 * C);
+    double *w2 = buf((size_t)K * R), *y = buf((size_t)N * Ho * Wo * K);
+    double *s0 = with_vectors ? buf(C) : NULL, *b0 = with_vectors ? buf(C) : NULL;
+    double *s1 = with_vectors ? buf(R) : NULL, *b1 = with_vectors ? buf(R) : NULL;
+    double *s2 = with_vectors ? buf(K) : NULL, *b2 = with_vectors ? buf(K) : NULL;
+    expect(cfref_convfirst_s2_forward(x, gwt, s0, b0, w1, s1, b1, w2, s2, b2, N, H, W, C, R, K, 3, 8, 1, y) == 0,
+           "convfirst_s2");
+    expect(cfref_convfirst_s2_forward(x, gwt, s0, b0, w1, s1, b1, w2, s2, b2, N, 1, W, C, R, K, 3, 8, 1, y) < 0,
+           "convfirst_s2 rejects H < 2");
+    free(x); free(gwt); free(w1); free(w2); free(y);
+    free(s0); free(b0); free(s1); free(b1); free(s2); free(b2);
+}
+
 int main(void)
 {
     /* depth-wise block: one pixel, H, W < k, odd sizes, several images and threads */
@@ -172,6 +192,10 @@ int main(void)
     mbconv_case(1, 1, 1, 16, 1, 4, 3, 1);
     mbconv_case(2, 3, 5, 16, 2, 8, 3, 0);
     mbconv_case(1, 4, 4, 8, 4, 1, 5, 1);
+    /* stride-2 ConvFirst: the smallest image, odd sizes, NULL vectors */
+    convfirst_s2_case(1, 2, 2, 8, 16, 8, 1);
+    convfirst_s2_case(2, 5, 7, 16, 24, 16, 0);
+    convfirst_s2_case(1, 9, 4, 24, 32, 8, 1);
     if (fails) {
         fprintf(stderr, "%d check(s) failed\n", fails);
         return 1;
