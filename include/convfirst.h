@@ -199,6 +199,33 @@ cf_status cf_gblock_forward(const void *x, void *y, const cf_gblock_params *p,
                             int N, int H, int W, int C, int E, int k,
                             cf_dtype dt, cf_act act, void *stream);
 
+/* The stride-2 ConvFirst block (Fig. f:convfirst-block (c): the variant that
+ * down-samples with BlurPool, Triangle-3), in one kernel.  The figure is not
+ * in the paper's text; the layer order and sizes are the reading its
+ * speed-projection tables fix (App. A: the conv at the input size over C
+ * channels, the expand at the output size over 2C, the project to K):
+ *   D  = s0 * gconv3x3(X) + b0                     grouped conv, C -> C (as
+ *                                                  cf_gblock_forward's D)
+ *   Z  = [bp(D), bp(X)]                            2C channels, D's first;
+ *   bp(V)[i,j,c] = sum_{a,b<3} t[a] t[b] V[rf(2i+a-1), rf(2j+b-1), c],
+ *        t = (1, 2, 1) / 4, one pixel of reflect padding (rf(-1) = 1,
+ *        rf(H) = H - 2)
+ *   Y  = s2 * (w2 act(s1 * (w1 Z) + b1)) + b2      no residual
+ * Tensors (row-major, I/O dtype unless noted):
+ *   x [N][H][W][C];  y [N][ceil(H/2)][ceil(W/2)][K]
+ *   p->gw_w [3][3][C][8] (with gw_scale, gw_bias fp32 [C]);  p->w1 [R][2C];
+ *   p->w2 [K][R];  s1, b1 fp32 [R];  s2, b2 fp32 [K]  (NULL scale 1, bias 0).
+ * The paper's block uses ReLU; GELU and identity are available too.
+ * Supported: k = 3; C = 16, 24, 32, 48 or 64; R a multiple of 16 up to 1024;
+ * K a multiple of 8 up to 128; H, W >= 2.  C not a multiple of 8, H or W below 2, or y
+ * overlapping x return CF_ERR_INVALID, other shapes CF_ERR_UNSUPPORTED.  fp16
+ * or bf16 I/O; the conv accumulates pair products in fp32; D, the blurred
+ * maps and the hidden values are rounded to the I/O dtype before the next
+ * product.  Deterministic. */
+cf_status cf_convfirst_s2_forward(const void *x, void *y, const cf_gblock_params *p,
+                                  int N, int H, int W, int C, int R, int K, int k,
+                                  cf_dtype dt, cf_act act, void *stream);
+
 /* The network's stem (App. A: a 3 x 3 convolution with stride 2 from the
  * image's 3 channels to the first stage's channels; caption of Fig.
  * f:convfirstnet: ReLU), its batch norm folded to a scale and a bias:

@@ -26,6 +26,7 @@ __all__ = [
     "stage_forward_microbatch",
     "downsample_forward",
     "block_forward_unfused", "block_forward_split", "block_forward_split_noalloc", "gblock_forward",
+    "convfirst_s2_forward",
     "mbconv_forward", "mbconv_workspace_bytes", "mbconv_s2_forward", "mbconv_s2_workspace_bytes", "stem_forward",
     "stem_gblock_forward", "stack_forward", "capture_stack", "ConvFirstBlock",
     "CFError", "EXPORTED_SYMBOLS", "dw_weight_from_conv2d", "grouped_weight_from_conv2d",
@@ -44,7 +45,8 @@ EXPORTED_SYMBOLS = (
     "cf_block_forward", "cf_stage_forward", "cf_stage_workspace_bytes", "cf_stage_forward_microbatch",
     "cf_stage_microbatch_workspace_bytes", "cf_downsample_forward",
     "cf_block_forward_unfused", "cf_unfused_workspace_bytes", "cf_block_forward_split",
-    "cf_split_workspace_bytes", "cf_block_forward_split_noalloc", "cf_gblock_forward", "cf_mbconv_forward",
+    "cf_split_workspace_bytes", "cf_block_forward_split_noalloc", "cf_gblock_forward", "cf_convfirst_s2_forward",
+    "cf_mbconv_forward",
     "cf_mbconv_workspace_bytes", "cf_mbconv_s2_forward", "cf_mbconv_s2_workspace_bytes", "cf_stem_forward",
     "cf_stem_gblock_forward", "cf_block_autotune",
     "cf_block_tuned_config", "cf_last_error", "cf_status_string", "cf_abi_version",
@@ -113,6 +115,7 @@ def lib():
             "cf_split_workspace_bytes": (sz, [i, i, i, i, i, i]),
             "cf_block_forward_split_noalloc": (i, [vp, vp, bp, i, i, i, i, i, i, i, i, i, vp]),
             "cf_gblock_forward": (i, [vp, vp, gp, i, i, i, i, i, i, i, i, vp]),
+            "cf_convfirst_s2_forward": (i, [vp, vp, gp, i, i, i, i, i, i, i, i, i, vp]),
             "cf_mbconv_forward": (i, [vp, vp, vp, sz, mp, i, i, i, i, i, i, i, i, i, vp]),
             "cf_mbconv_workspace_bytes": (sz, [i, i, i, i, i, i, i]),
             "cf_mbconv_s2_forward": (i, [vp, vp, vp, sz, mp, i, i, i, i, i, i, i, i, i, i, vp]),
@@ -427,6 +430,56 @@ def gblock_forward(x: torch.Tensor, p: dict, act: str = "relu", out=None, stream
     y = _out(x, out)
     _check(lib().cf_gblock_forward(_ptr(x), _ptr(y), ctypes.byref(gp), N, H, W, C, EC // C, k,
                                    DTYPES[x.dtype], ACTS[act], _stream(stream)))
+    return y
+
+
+# stride-2 ConvFirst parameters: shape as a function of (C, R, K)
+_CFS2_SHAPES = {
+    "gw_w": (lambda C, R, K: (3, 3, C, GROUP_WIDTH), "w"),
+    "w1": (lambda C, R, K: (R, 2 * C), "w"),
+    "w2": (lambda C, R, K: (K, R), "w"),
+    "s0": (lambda C, R, K: (C,), "v"), "b0": (lambda C, R, K: (C,), "v"),
+    "s1": (lambda C, R, K: (R,), "v"), "b1": (lambda C, R, K: (R,), "v"),
+    "s2": (lambda C, R, K: (K,), "v"), "b2": (lambda C, R, K: (K,), "v"),
+}
+
+
+def convfirst_s2_forward(x: torch.Tensor, p: dict, act: str = "relu", out=None, stream=None) -> torch.Tensor:
+    """The stride-2 ConvFirst block (Fig. f:convfirst-block (c)) in one
+    kernel, in the reading the speed-projection tables fix (App. A): grouped
+    3x3 conv C -> C with s0, b0 at the input size, BlurPool (Triangle-3,
+    reflect) of the conv output and of x, the two concatenated (2C channels,
+    conv output first), expand to R with s1, b1 and the activation, project
+    to K with s2, b2, no residual.  p holds gw_w [3,3,C,8], w1 [R,2C], w2
+    [K,R] in x's dtype and optional fp32 s0,b0 [C], s1,b1 [R], s2,b2 [K].
+    Returns [N, ceil(H/2), ceil(W/2), K]; out must not overlap x."""
+    if act not in ACTS:
+        raise ValueError("act must be one of %s" % sorted(ACTS))
+    N, H, W, C = _dims(x)
+    for key in ("gw_w", "w1", "w2"):
+        if not isinstance(p.get(key), torch.Tensor):
+            raise ValueError("stride-2 ConvFirst parameter %s is required" % key)
+    if p["gw_w"].dim() != 4 or p["w1"].dim() != 2 or p["w2"].dim() != 2:
+        raise ValueError("gw_w must be [3, 3, C, 8], w1 [R, 2C] and w2 [K, R]")
+    k, R, K = int(p["gw_w"].shape[0]), int(p["w1"].shape[0]), int(p["w2"].shape[0])
+    unknown = set(p) - set(_CFS2_SHAPES)
+    if unknown:
+        raise ValueError("unknown stride-2 ConvFirst parameters: %s" % sorted(unknown))
+    vals, keep = {}, []
+    for key, (shape_of, kind) in _CFS2_SHAPES.items():
+        t = p.get(key)
+        if t is not None:
+            shape = shape_of(C, R, K)
+            if key == "gw_w":
+                shape = (k, k, C, GROUP_WIDTH)
+            _check_tensor(key, t, shape, x.dtype if kind == "w" else torch.float32, x.device)
+            keep.append(t)
+        vals[_GFIELDS[key]] = None if t is None else t.data_ptr()
+    gp = _GBlockParams(**vals)
+    _check_device(x)
+    y = _out(x, out, (N, (H + 1) // 2, (W + 1) // 2, K))
+    _check(lib().cf_convfirst_s2_forward(_ptr(x), _ptr(y), ctypes.byref(gp), N, H, W, C, R, K, k,
+                                         DTYPES[x.dtype], ACTS[act], _stream(stream)))
     return y
 
 

@@ -708,6 +708,62 @@ cf_status cf_gblock_forward(const void *x, void *y, const cf_gblock_params *p, i
     return CF_OK;
 }
 
+cf_status cf_convfirst_s2_forward(const void *x, void *y, const cf_gblock_params *p, int N, int H, int W, int C,
+                                  int R, int K, int k, cf_dtype dt, cf_act act, void *stream) {
+    const char *what = "cf_convfirst_s2_forward";
+    if (!x || !y)
+        return fail(CF_ERR_INVALID, "%s: x and y must be non-NULL", what);
+    if (!p || !p->gw_w || !p->w1 || !p->w2)
+        return fail(CF_ERR_INVALID, "%s: params, gw_w, w1 and w2 must be non-NULL", what);
+    if (N <= 0 || H <= 0 || W <= 0 || C <= 0 || R <= 0 || K <= 0 || k <= 0)
+        return fail(CF_ERR_INVALID, "%s: sizes must be positive (N=%d H=%d W=%d C=%d R=%d K=%d k=%d)", what, N, H,
+                    W, C, R, K, k);
+    if (k % 2 == 0)
+        return fail(CF_ERR_INVALID, "%s: k must be odd (got %d)", what, k);
+    if (H < 2 || W < 2)
+        return fail(CF_ERR_INVALID, "%s: BlurPool's reflect padding needs H, W >= 2 (H=%d W=%d)", what, H, W);
+    if (C % CF_GROUP_WIDTH)
+        return fail(CF_ERR_INVALID, "%s: C=%d is not a multiple of the group width %d", what, C, CF_GROUP_WIDTH);
+    if ((int)dt != CF_F16 && (int)dt != CF_BF16)
+        return fail(CF_ERR_INVALID, "%s: unknown dtype %d", what, (int)dt);
+    if ((int)act != CF_ACT_GELU_ERF && (int)act != CF_ACT_RELU && (int)act != CF_ACT_NONE)
+        return fail(CF_ERR_INVALID, "%s: unknown activation %d", what, (int)act);
+    if ((double)N * H * W * C > 4.0e12 || (double)R * C > 1.0e7 || (double)K * R > 1.0e7)
+        return fail(CF_ERR_INVALID, "%s: tensor too large", what);
+    const void *ptrs[] = {x, y, p->gw_w, p->w1, p->w2, p->gw_scale, p->gw_bias, p->s1, p->b1, p->s2, p->b2};
+    for (const void *q : ptrs)
+        if (q && !aligned16(q))
+            return fail(CF_ERR_INVALID, "%s: every tensor pointer must be 16-byte aligned", what);
+    const size_t xbytes = (size_t)N * H * W * C * elem_bytes(dt);
+    const size_t ybytes = (size_t)N * ((H + 1) / 2) * ((W + 1) / 2) * K * elem_bytes(dt);
+    if (overlap(x, xbytes, y, ybytes))
+        return fail(CF_ERR_INVALID, "%s: x and y overlap", what);
+    if (k != 3)
+        return fail(CF_ERR_UNSUPPORTED, "%s: k=%d has no kernel (supported: 3)", what, k);
+    if (!cf::convfirst_s2_supported(H, W, C, R, K))
+        return fail(CF_ERR_UNSUPPORTED,
+                    "%s: no kernel for C=%d R=%d K=%d (supported: C = 16, 24, 32, 48, 64; R a multiple of 16 "
+                    "up to 1024; K a multiple of 8 up to 128)",
+                    what, C, R, K);
+    if ((double)N * H * W > 2147483647.0)
+        return fail(CF_ERR_UNSUPPORTED, "%s: N*H*W must stay below 2^31 pixels", what);
+    cf::BlockW w;
+    w.dw_w = p->gw_w;
+    w.s0 = p->gw_scale;
+    w.b0 = p->gw_bias;
+    w.w1 = p->w1;
+    w.s1 = p->s1;
+    w.b1 = p->b1;
+    w.w2 = p->w2;
+    w.s2 = p->s2;
+    w.b2 = p->b2;
+    hipError_t e = cf::launch_convfirst_s2(x, y, w, N, H, W, C, R, K, dt == CF_BF16, (int)act, (hipStream_t)stream);
+    if (e != hipSuccess)
+        return hip_fail(e, what);
+    g_err[0] = 0;
+    return CF_OK;
+}
+
 cf_status cf_stem_forward(const void *x, void *y, const cf_stem_params *p, int N, int Hin, int Win, int C,
                           cf_dtype dt, void *stream) {
     const char *what = "cf_stem_forward";

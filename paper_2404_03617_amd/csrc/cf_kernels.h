@@ -78,6 +78,10 @@ hipError_t launch_small_split(const void *x, const BlockW &w, const Shape &s, in
 // workgroup per 32 output channels, each recomputing the expand and summing
 // its waves' projections in LDS.  slice_applies tells whether the shape suits
 // it; launch_slice returns hipErrorInvalidConfiguration otherwise.
+// the stride-2 ConvFirst block (cf_cfs2.hip)
+bool convfirst_s2_supported(int H, int W, int C, int R, int K);
+hipError_t launch_convfirst_s2(const void *x, void *y, const BlockW &w, int N, int H, int W, int C, int R, int K,
+                               int bf16, int act, hipStream_t st);
 bool slice_applies(const Shape &s);
 hipError_t launch_slice(const void *x, void *y, const BlockW &w, const Shape &s, hipStream_t st);
 

@@ -136,6 +136,26 @@ def mbconv_params(seed: int, layer: int, C: int, E: int, R: int, dtype: str = "f
     }
 
 
+def convfirst_s2_params(seed: int, layer: int, C: int, R: int, K: int, dtype: str = "f16",
+                        scales: str = "ones", bias_std: float | None = 0.1, gw: int = 8) -> dict:
+    """Weights of one stride-2 ConvFirst block (grouped 3x3 conv of group
+    width gw, expand from the 2C concatenated channels to R, project to K);
+    tensor ids 100*(layer+1) + 0..8.  Weights ~ N(0, 1/fan_in): 9*gw (conv),
+    2C (expand), R (project)."""
+    base = 100 * (layer + 1)
+    return {
+        "gw_w": to_io(draw(seed, base + 0, (3, 3, C, gw), (1.0 / (9 * gw)) ** 0.5), dtype),
+        "s0": _vec(seed, base + 1, C, "scale", bias_std, scales),
+        "b0": _vec(seed, base + 2, C, "bias", bias_std, scales),
+        "w1": to_io(draw(seed, base + 3, (R, 2 * C), (1.0 / (2 * C)) ** 0.5), dtype),
+        "s1": _vec(seed, base + 4, R, "scale", bias_std, scales),
+        "b1": _vec(seed, base + 5, R, "bias", bias_std, scales),
+        "w2": to_io(draw(seed, base + 6, (K, R), (1.0 / R) ** 0.5), dtype),
+        "s2": _vec(seed, base + 7, K, "scale", bias_std, scales),
+        "b2": _vec(seed, base + 8, K, "bias", bias_std, scales),
+    }
+
+
 def down_params(seed: int, layer: int, Cin: int, Cout: int, dtype: str = "f16",
                 scales: str = "ones", bias_std: float | None = 0.1) -> dict:
     """Weights of one 2x2 stride-2 down-sampling layer; ids 100*(layer+1) + 0..2."""

@@ -67,6 +67,19 @@ MBCONV_S2_WORKLOADS = {
     for i, (c, ms) in enumerate([(128, 0.282), (160, 0.595), (192, 0.819), (256, 0.835)])
 }
 
+# The stride-2 ConvFirst blocks of the speed-projection tables (App. A: the
+# distinct stride-2 ConvFirst rows over the four model sizes), batch 128,
+# fp16, ReLU: input H = W, C channels, hidden R, output K.  The paper builds
+# no kernel for them: paper_proj_ms is its projection, not a measurement.
+CONVFIRST_S2_WORKLOADS = {
+    "convfirst_s2_n128_%dx%d_c%d_r%d_k%d_f16" % (hw, hw, c, r, k): dict(kind="convfirst_s2", N=128, H=hw, W=hw, C=c,
+                                                                      R=r, K=k, dtype="f16", act="relu",
+                                                                      seed=80 + i, paper_proj_ms=ms)
+    for i, (hw, c, r, k, ms) in enumerate([
+        (128, 16, 96, 32, 0.275), (64, 32, 192, 48, 0.196), (128, 24, 144, 48, 0.495), (64, 48, 288, 64, 0.336),
+        (64, 48, 288, 72, 0.380), (128, 32, 192, 64, 0.758), (64, 64, 384, 96, 0.650)])
+}
+
 # The network stem (a 3x3 stride-2 conv from the 256 x 256 image's 3 channels,
 # ReLU) fused into the first ConvFirst block at 128 x 128 (App. A, the first two
 # rows of the speed-projection tables: the Pico stem 3 -> 16 before ConvFirst

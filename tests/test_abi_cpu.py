@@ -479,6 +479,39 @@ def test_mbconv_s2_forward_rejects():
     assert L.cf_last_error().decode().startswith("cf_mbconv_s2_forward")
 
 
+def test_convfirst_s2_forward_rejects():
+    """The stride-2 ConvFirst entry point: every check happens on the host."""
+    L = cf.lib()
+    GW = 0x43000000
+
+    def call(x=X, y=Y, N=2, H=8, W=8, C=16, R=96, K=32, k=3, dt=0, act=1, **kw):
+        p = cf._GBlockParams(gw_w=GW, gw_scale=None, gw_bias=None, w1=W1, s1=None, b1=None, w2=W2, s2=None,
+                             b2=None)
+        for f, v in kw.items():
+            setattr(p, f, v)
+        return L.cf_convfirst_s2_forward(x, y, ctypes.byref(p), N, H, W, C, R, K, k, dt, act, None)
+
+    assert call(x=None) == cf.CF_ERR_INVALID
+    assert call(w1=None) == cf.CF_ERR_INVALID
+    assert call(R=0) == cf.CF_ERR_INVALID
+    assert call(k=4) == cf.CF_ERR_INVALID
+    assert call(H=1) == cf.CF_ERR_INVALID           # reflect padding needs a second row
+    assert call(W=1) == cf.CF_ERR_INVALID
+    assert call(C=20) == cf.CF_ERR_INVALID          # not a multiple of the group width
+    assert call(dt=5) == cf.CF_ERR_INVALID
+    assert call(act=7) == cf.CF_ERR_INVALID
+    assert call(y=X + 1024) == cf.CF_ERR_INVALID    # y overlaps x
+    assert call(s2=W1 + 4) == cf.CF_ERR_INVALID     # misaligned
+    assert call(k=5) == cf.CF_ERR_UNSUPPORTED
+    assert call(C=40) == cf.CF_ERR_UNSUPPORTED      # no kernel for C = 40
+    assert call(C=128) == cf.CF_ERR_UNSUPPORTED
+    assert call(R=104) == cf.CF_ERR_UNSUPPORTED     # R not a multiple of 16
+    assert call(R=2048) == cf.CF_ERR_UNSUPPORTED
+    assert call(K=36) == cf.CF_ERR_UNSUPPORTED      # K not a multiple of 8
+    assert call(K=136) == cf.CF_ERR_UNSUPPORTED
+    assert L.cf_last_error().decode().startswith("cf_convfirst_s2_forward")
+
+
 def test_stem_entry_points_reject():
     """The stem and the stem + first block: every check happens on the host."""
     L = cf.lib()
