@@ -32,8 +32,8 @@ import torch
 import paper_2404_03617_amd as cf
 from paper_2404_03617_amd import roofline as rl
 from paper_2404_03617_amd import synth
-from paper_2404_03617_amd.workloads import (BENCH_WORKLOAD, GBLOCK_WORKLOADS, MBCONV_S2_WORKLOADS, MBCONV_WORKLOADS,
-                                            STEM_WORKLOADS, WORKLOADS)
+from paper_2404_03617_amd.workloads import (BENCH_WORKLOAD, CONVFIRST_S2_WORKLOADS, GBLOCK_WORKLOADS,
+                                            MBCONV_S2_WORKLOADS, MBCONV_WORKLOADS, STEM_WORKLOADS, WORKLOADS)
 
 MALL_BYTES = 256 << 20
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -287,6 +287,27 @@ def mbconv_s2_case(name: str, steps: int, warmup: int):
     return {"ms": round(t * 1e3, 4), "images_per_s": round(N / t, 1), "tflops": round(flops / t / 1e12, 1),
             "comp_eff": round(rl.comp_eff(flops, t), 4), "roofline": roofline_entry(flops, nbytes, t),
             "exclusive_launch_ms": round(te * 1e3, 4), "exclusive_launch_comp_eff": round(rl.comp_eff(flops, te), 4),
+            "paper_projection_ms_A5000": w["paper_proj_ms"]}
+
+
+def convfirst_s2_case(name: str, steps: int, warmup: int):
+    """The stride-2 ConvFirst block (grouped conv, BlurPool of the conv output
+    and of the input, FFN at half size) at one of the stride-2 rows of the
+    paper's speed projections, batch 128: one launch per step."""
+    w = CONVFIRST_S2_WORKLOADS[name]
+    N, H, W, C, R, K = w["N"], w["H"], w["W"], w["C"], w["R"], w["K"]
+    Ho, Wo = (H + 1) // 2, (W + 1) // 2
+    nsets = _sets_needed(N * H * W * C * 2 + N * Ho * Wo * K * 2)
+    xs = [synth.activations(w["seed"] + 100 * i, N, H, W, C, w["dtype"]).cuda() for i in range(nsets)]
+    ys = [torch.empty((N, Ho, Wo, K), dtype=xs[0].dtype, device="cuda") for _ in range(nsets)]
+    p = {kk: (None if v is None else v.cuda()) for kk, v in
+         synth.convfirst_s2_params(w["seed"], 0, C, R, K, w["dtype"]).items()}
+    t = _time(lambda i: cf.convfirst_s2_forward(xs[i % nsets], p, act=w["act"], out=ys[i % nsets]), steps, warmup,
+              torch.cuda.current_stream())
+    flops = rl.convfirst_s2_flops(N, H, W, C, R, K)
+    nbytes = rl.convfirst_s2_bytes_fused(N, H, W, C, R, K)
+    return {"ms": round(t * 1e3, 4), "images_per_s": round(N / t, 1), "tflops": round(flops / t / 1e12, 1),
+            "comp_eff": round(rl.comp_eff(flops, t), 4), "roofline": roofline_entry(flops, nbytes, t),
             "paper_projection_ms_A5000": w["paper_proj_ms"]}
 
 
@@ -550,6 +571,21 @@ def main():
         if args.calib_copy:
             calib_copy()
         return
+    if name in CONVFIRST_S2_WORKLOADS:
+        g = convfirst_s2_case(name, args.steps, args.warmup)
+        wg = CONVFIRST_S2_WORKLOADS[name]
+        cfg = {"workload": name, "N": wg["N"], "H": wg["H"], "W": wg["W"], "C": wg["C"], "R": wg["R"],
+               "K": wg["K"], "k": 3, "act": wg["act"],
+               "kernel": "fused stride-2 ConvFirst block with BlurPool (1 launch)"}
+        print(json.dumps({"metric": "images/sec and % of fp16 MFMA peak (computational efficiency), batch 128",
+                          "value": g["images_per_s"], "unit": "images/s", "n_gpus": 1, "steps": args.steps,
+                          "warmup": args.warmup, "ms_per_step": g["ms"], "higher_is_better": True,
+                          "scaling": "weak", "vs_baseline": None, "dtype": "f16",
+                          "data": "synthetic (seeded N(0,1) activations, N(0,1/fan_in) weights)",
+                          "config": cfg, "comp_eff": g["comp_eff"], "roofline": g["roofline"]}), flush=True)
+        if args.calib_copy:
+            calib_copy()
+        return
     if name in MBCONV_S2_WORKLOADS:
         g = mbconv_s2_case(name, args.steps, args.warmup)
         wg = MBCONV_S2_WORKLOADS[name]
@@ -690,6 +726,8 @@ def main():
         # the stem fused into the first block (App. A's first rows)
         extra["stem_first_block"] = {nm: stem_case(nm, max(5, args.steps // 2), 3) for nm in STEM_WORKLOADS}
         extra["mbconv_stride2"] = {nm: mbconv_s2_case(nm, max(5, args.steps // 2), 3) for nm in MBCONV_S2_WORKLOADS}
+        extra["convfirst_stride2"] = {nm: convfirst_s2_case(nm, max(5, args.steps // 2), 3)
+                                      for nm in CONVFIRST_S2_WORKLOADS}
         out["other_workloads"] = extra
     if args.calib_copy:
         calib_copy()

@@ -99,6 +99,24 @@ def mbconv_s2_bytes_fused(N, H, W, C, E, R, K, k=3, gw=8, eb=2) -> int:
     return N * H * W * C * eb + N * ((H + 1) // 2) * ((W + 1) // 2) * K * eb + weights + vectors
 
 
+def convfirst_s2_flops(N, H, W, C, R, K, k=3, gw=8) -> int:
+    """Stride-2 ConvFirst block (Fig. f:convfirst-block (c)): grouped conv
+    2 H W C k^2 gw at the input size, expand 2 Ho Wo (2C) R and project
+    2 Ho Wo R K at the output size -- the Conv, Exp and Prj columns of the
+    projection tables (the BlurPool is not counted)."""
+    Po = ((H + 1) // 2) * ((W + 1) // 2)
+    return N * (2 * H * W * C * k * k * gw + 2 * Po * 2 * C * R + 2 * Po * R * K)
+
+
+def convfirst_s2_bytes_fused(N, H, W, C, R, K, k=3, gw=8, eb=2) -> int:
+    """x read once, the down-sampled y written once, the weights and fp32
+    vectors once."""
+    Po = ((H + 1) // 2) * ((W + 1) // 2)
+    weights = eb * (k * k * C * gw + 2 * C * R + R * K)
+    vectors = 4 * (2 * C + 2 * R + 2 * K)
+    return N * H * W * C * eb + N * Po * K * eb + weights + vectors
+
+
 def block_weight_bytes(C, E, k, eb=2, vec_bytes=4) -> int:
     """dw taps, W1, W2 in the I/O dtype plus six fp32 scale/bias vectors."""
     return eb * (k * k * C + 2 * E * C * C) + vec_bytes * (2 * C + 2 * E * C + 2 * C)

@@ -155,3 +155,11 @@ def test_layer_sizes_reproduce_the_projection_tables(row):
     assert 2 * Ho * Wo * p["w2"].size / 1e6 == pytest.approx(prj, abs=0.005)
     assert (conv + exp + prj) == pytest.approx(total, abs=0.015)
     assert 2 * Ho * Wo * C * R / 1e6 == pytest.approx(exp / 2, abs=0.005)
+
+
+@pytest.mark.parametrize("row", _rows(), ids=lambda r: "%dx%d_C%d_R%d_K%d" % r[:5])
+def test_roofline_count_reproduces_the_projection_tables(row):
+    """roofline.convfirst_s2_flops per image equals the printed row total."""
+    from paper_2404_03617_amd import roofline as rl
+    H, W, C, R, K, conv, exp, prj, total = row
+    assert rl.convfirst_s2_flops(1, H, W, C, R, K) / 1e6 == pytest.approx(total, abs=0.015)
