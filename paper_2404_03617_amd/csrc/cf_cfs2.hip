@@ -5,26 +5,49 @@
 // of the block input, the two maps concatenated (2C channels, conv output
 // first) into the expand, activation, project to K, no residual.
 //
-// Work unit: 16 output pixels of one output row (columns j0 .. j0 + 15), one
-// per wave, in a private LDS region:
+// Work unit: 16 output pixels of one output row (columns j0 .. j0 + 15).
+// The waves are persistent: each takes units blockIdx * nw + wave, then
+// every gridDim * nw-th, in a private LDS region; the taps, s0, b0, s1, b1,
+// s2 and b2 are staged in LDS once per workgroup.  Per unit:
 //  1. the input window, rows 2i - 2 .. 2i + 2 and columns 2j0 - 2 .. 2j0 + 32,
-//     zero outside the image (the conv's padding);
-//  2. the grouped conv at the full-resolution positions the blur reads --
-//     virtual rows 2i - 1 .. 2i + 1 and columns 2j0 - 1 .. 2j0 + 31, each
-//     evaluated at its reflected position, so the blur needs no reflection --
-//     on the VALU: a lane takes one position and one group of 8 channels,
-//     eight outputs of 72 products each as pair products accumulated in
-//     fp32 (v_dot2_f32_f16 / _bf16); s0, b0; rounded to the I/O dtype;
-//  3. the blur of both maps (fp32, rounded to the I/O dtype) into a 16-pixel
-//     tile of 2C channels, zero-padded to a multiple of 32;
-//  4. the FFN on v_mfma_f32_16x16x32: expand tiles of 16 hidden channels (A =
-//     W1 rows, B = the tile), s1, b1 and the activation in fp32, rounded; two
-//     tiles form the B operand of the project with the K order position
-//     8q + e <-> hidden 32kk + 4q + e (e < 4) or 32kk + 16 + 4q + e - 4, the
-//     lane layout the expand leaves, and the W2 fragments are read in that
-//     order; s2, b2; y stored once.
+//     zero outside the image (the conv's padding): every lane's pieces are
+//     loaded with one batch of 16-byte loads (addresses clamped into the
+//     image, the zeros selected at the LDS store); with up to 32 channels
+//     the next unit's window is loaded during this unit's conv and FFN;
+//  2. the grouped conv at full resolution, rows 2i - 1 .. 2i + 1 and columns
+//     2j0 - 1 .. 2j0 + 31 (the positions the blur reads, before reflection),
+//     on v_mfma_f32_16x16x32: for group g and tap column dj, A row m = 8s + o
+//     at K index 8R + t is the tap W[R - s][dj][8g + o][t] (zero unless
+//     0 <= R - s <= 2) and B column j at K index 8R + t is window pixel
+//     (w0 + R, c + j + dj), channel 8g + t, so one product per tap column
+//     gives conv rows w0 and w0 + 1 of 16 columns; two row sets (w0 = 0, and
+//     w0 = 1 keeping only its second row) and three column tiles (the third
+//     for column 2j0 + 31 alone) cover the 3 x 33 positions.  The A
+//     fragments of a group (one per tap column) stay in registers for all
+//     its products; s0, b0; rounded to the I/O dtype;
+//  3. the blur of both maps (fp32, rounded to the I/O dtype), each read at
+//     the reflected positions, into a 16-pixel tile of 2C channels,
+//     zero-padded to a multiple of 32;
+//  4. the FFN on v_mfma_f32_16x16x32 in chunks of 32 hidden channels:
+//     expand tiles of 16 hidden channels (A = W1 rows, B = the tile), s1, b1
+//     and the activation in fp32, rounded; two tiles form the B operand of
+//     the project with the K order position 8q + e <-> hidden 32kk + 4q + e
+//     (e < 4) or 32kk + 16 + 4q + e - 4, the lane layout the expand leaves,
+//     and the W2 fragments are read in that order; s2, b2; y stored once.
+//     A chunk's W1 and W2 pieces are loaded from global memory (L2) one
+//     chunk ahead, the first chunk's during the conv.  Every load of the loop is unconditional (addresses clamped; the
+//     rows past R meet zero hidden values, the rows past K are not stored),
+//     so the waits count exactly.  The loads are row-major -- lane 4r + p
+//     takes piece p of row r, four adjacent lanes on one contiguous run --
+//     and ds_bpermute from lane 4 jl + q moves each dword to the fragment
+//     lane (jl, q) when the chunk is used (a fragment-order load, sixteen
+//     rows in sixteen adjacent lanes, costs the memory unit several times
+//     more per byte).
 // The input windows of neighbouring units overlap by three columns and the
 // conv positions on the unit's border columns are evaluated by both units.
+// Conv positions outside the image are evaluated on the zero padding and
+// never read: the blur's reflection of row -1 is row 1, of row H is H - 2,
+// both inside the unit's rows (and likewise for columns).
 #include "cf_device.h"
 #include "cf_kernels.h"
 
@@ -32,7 +55,7 @@ namespace cf {
 namespace cfs2 {
 
 constexpr int XR = 5, XC = 35;  // input window: rows 2i-2 .. 2i+2, columns 2j0-2 .. 2j0+32
-constexpr int VR = 3, VC = 33;  // conv outputs: virtual rows 2i-1 .. 2i+1, columns 2j0-1 .. 2j0+31
+constexpr int VR = 3, VC = 33;  // conv outputs: rows 2i-1 .. 2i+1, columns 2j0-1 .. 2j0+31
 constexpr int UPX = 16;         // output pixels per unit
 constexpr int KMAX = 128;       // output channels
 constexpr int RMAX = 1024;      // hidden channels
@@ -49,15 +72,10 @@ struct Args {
     int H, W, Ho, Wo, R, K, act;
     int units, jt;        // units = N * Ho * jt, jt = ceil(Wo / 16)
     int nw;               // waves per workgroup
-    uint32_t off_region;  // LDS: the taps at 0, then one region per wave
+    uint32_t off_region;  // LDS: taps, s0, b0, s1, b1, s2, b2, then one region per wave
 };
 
-__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c, F16) {
-    return __builtin_amdgcn_fdot2(__builtin_bit_cast(half2v, a), __builtin_bit_cast(half2v, b), c, false);
-}
-__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c, BF16) {
-    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
-}
+__device__ __forceinline__ int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
 
 // one pixel of reflect padding (-1 -> 1, n -> n - 2); past that (the padded
 // pixels of a unit at the right edge, whose outputs are not stored) the last
@@ -78,7 +96,12 @@ __device__ __forceinline__ float act_f(float u, int act) {
     return u;
 }
 
-template <typename T, int C>
+// LDS bytes of the staged taps and vectors
+__host__ __device__ inline uint32_t staged_bytes(int C, int R, int K) {
+    return ((uint32_t)(9 * C * 16 + 4 * (2 * C + 2 * R + 2 * K)) + 255) & ~255u;
+}
+
+template <typename T, int C, int OTM>
 struct Kern {
     static constexpr int G = C / 8;                            // groups of the conv
     static constexpr uint32_t PP = 2 * C + 16;                 // LDS bytes per window / conv pixel
@@ -87,212 +110,327 @@ struct Kern {
     static constexpr uint32_t PZ = 2 * C2P + 16;               // LDS bytes per tile pixel
     static constexpr uint32_t XB = XR * XC * PP, VB = VR * VC * PP, ZB = UPX * PZ;
     static constexpr uint32_t REGION = XB + VB + ZB;
+    static constexpr int NX = XR * XC * G;                     // 16-byte pieces of a window
+    static constexpr int NIT = (NX + 63) / 64;                 // per lane
+    static constexpr bool PREF = G <= 4;                       // next window loaded during this unit
+
+    struct Frag {
+        u32x4 w1[2][KS];
+        u32x2 w2[OTM][2];
+    };
+
+    struct Unit {
+        int n, i, j0;
+    };
+
+    static __device__ __forceinline__ Unit decode(const Args &a, int u) {
+        const int jt = u % a.jt, ni = u / a.jt;
+        return Unit{ni / a.Ho, ni % a.Ho, jt * UPX};
+    }
+
+    // window piece it of this lane: pixel (rr, cc) of the window, 16-byte
+    // piece pc; adjacent lanes on adjacent pieces
+    static __device__ __forceinline__ void load_window(const Args &a, int u, int lane, u32x4 (&xv)[NIT]) {
+        const Unit un = decode(a, u);
+        const uint16_t *xn = a.x + (size_t)un.n * a.H * a.W * C;
+        const int r0 = 2 * un.i - 2, c0 = 2 * un.j0 - 2;
+#pragma unroll
+        for (int it = 0; it < NIT; it++) {
+            const int t = lane + 64 * it, tt = t < NX ? t : NX - 1;
+            const int px = tt / G, pc = tt - px * G, rr = px / XC, cc = px - rr * XC;
+            const int gr = clampi(r0 + rr, 0, a.H - 1), gc = clampi(c0 + cc, 0, a.W - 1);
+            xv[it] = *reinterpret_cast<const u32x4 *>(xn + ((size_t)gr * a.W + gc) * C + pc * 8);
+        }
+    }
+
+    static __device__ __forceinline__ void store_window(const Args &a, int u, int lane, const u32x4 (&xv)[NIT],
+                                                        uint8_t *X) {
+        const Unit un = decode(a, u);
+        const int r0 = 2 * un.i - 2, c0 = 2 * un.j0 - 2;
+#pragma unroll
+        for (int it = 0; it < NIT; it++) {
+            const int t = lane + 64 * it;
+            if (t < NX) {
+                const int px = t / G, pc = t - px * G, rr = px / XC, cc = px - rr * XC;
+                const int gr = r0 + rr, gc = c0 + cc;
+                const bool in = gr >= 0 && gr < a.H && gc >= 0 && gc < a.W;
+                *reinterpret_cast<u32x4 *>(X + (uint32_t)px * PP + (uint32_t)pc * 16) =
+                    in ? xv[it] : u32x4{0u, 0u, 0u, 0u};
+            }
+        }
+    }
+
+    // the W1 and W2 pieces of hidden chunk kk in row-major lane order: lane
+    // 4r + p holds W1 row 32kk + 16t + r, columns 32ks + 8p .. + 7 (the
+    // fragment piece of lane (r, p)), and W2 row 16 ot + r, hidden
+    // 32kk + 4p .. + 3 and 32kk + 16 + 4p .. + 3.  Rows are clamped into the
+    // matrices; W1 columns past 2C meet zero tile entries.
+    static __device__ __forceinline__ void load_frag(const Args &a, int kk, int lr, int lp, Frag &f) {
+        const int R = a.R;
+#pragma unroll
+        for (int t = 0; t < 2; t++) {
+            const int hr = min(32 * kk + 16 * t + lr, R - 1);
+            const uint16_t *wr = a.w1 + (size_t)hr * C2;
+#pragma unroll
+            for (int ks = 0; ks < KS; ks++) {
+                const int k = 32 * ks + 8 * lp;
+                f.w1[t][ks] = *reinterpret_cast<const u32x4 *>(wr + (k < C2 ? k : 0));
+            }
+        }
+        const int ha = 32 * kk + 4 * lp, hb = ha + 16 < R ? ha + 16 : ha;
+#pragma unroll
+        for (int ot = 0; ot < OTM; ot++) {
+            const uint16_t *wr = a.w2 + (size_t)min(16 * ot + lr, a.K - 1) * R;
+            f.w2[ot][0] = *reinterpret_cast<const u32x2 *>(wr + ha);
+            f.w2[ot][1] = *reinterpret_cast<const u32x2 *>(wr + hb);
+        }
+    }
+
+    static __device__ __forceinline__ uint32_t perm(int idx, uint32_t v) {
+        return (uint32_t)__builtin_amdgcn_ds_bpermute(idx, (int)v);
+    }
 
     static __device__ void run(const Args &a, uint8_t *smem) {
         const int tid = threadIdx.x, lane = tid & 63;
         const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-        // the taps [3][3][C][8], once per workgroup
+        const int R = a.R, K = a.K;
+        // the taps [3][3][C][8] and the vectors, once per workgroup
         for (int i = tid; i < 9 * C; i += a.nw * 64)
             *reinterpret_cast<u32x4 *>(smem + (uint32_t)i * 16) =
                 *reinterpret_cast<const u32x4 *>(a.gw + (size_t)i * 8);
+        float *s0l = reinterpret_cast<float *>(smem + 9 * C * 16), *b0l = s0l + C, *s1l = b0l + C, *b1l = s1l + R,
+              *s2l = b1l + R, *b2l = s2l + K;
+        for (int c = tid; c < C; c += a.nw * 64) {
+            s0l[c] = a.s0 ? a.s0[c] : 1.0f;
+            b0l[c] = a.b0 ? a.b0[c] : 0.0f;
+        }
+        for (int h = tid; h < R; h += a.nw * 64) {
+            s1l[h] = a.s1 ? a.s1[h] : 1.0f;
+            b1l[h] = a.b1 ? a.b1[h] : 0.0f;
+        }
+        for (int o = tid; o < K; o += a.nw * 64) {
+            s2l[o] = a.s2 ? a.s2[o] : 1.0f;
+            b2l[o] = a.b2 ? a.b2[o] : 0.0f;
+        }
         __syncthreads();
-        const int unit = (int)blockIdx.x * a.nw + wv;
+        int unit = (int)blockIdx.x * a.nw + wv;
         if (unit >= a.units)
             return;  // (after the workgroup's only barrier)
-        const int jt = unit % a.jt, ni = unit / a.jt;
-        const int i = ni % a.Ho, n = ni / a.Ho;
-        const int j0 = jt * UPX;
-        const int H = a.H, W = a.W;
+        const int stride = (int)gridDim.x * a.nw;
+        const int H = a.H, W = a.W, NKK = (R + 31) / 32, OT = (K + 15) / 16;
         uint8_t *X = smem + a.off_region + (uint32_t)wv * REGION, *V = X + XB, *Z = V + VB;
-        const uint16_t *xn = a.x + (size_t)n * H * W * C;
-        const int r0 = 2 * i - 2, c0 = 2 * j0 - 2;
+        u32x4 xv[NIT];
+        load_window(a, unit, lane, xv);
+        for (;;) {
+            // every lane-dependent index is recomputed from an opaque copy of
+            // the lane index in every unit: hoisted out of the loop (one per
+            // window piece, conv operand and weight row) they would hold
+            // most of the registers for the whole kernel
+            int ln = lane;
+            asm volatile("" : "+v"(ln));
+            const int q = ln >> 4, jl = ln & 15;
+            const int lr = ln >> 2, lp = ln & 3, pidx = (4 * jl + q) * 4;  // row-major lane, its fragment source
+            const Unit un = decode(a, unit);
+            const int i = un.i, j0 = un.j0, r0 = 2 * i - 2, c0 = 2 * j0 - 2;
+            // 1. the window into LDS; the first FFN chunk's fragments and,
+            //    with few channels, the next unit's window in flight
+            store_window(a, unit, ln, xv, X);
+            const int next = unit + stride;
+            Frag f;
+            load_frag(a, 0, lr, lp, f);
+            if (PREF)
+                load_window(a, next < a.units ? next : unit, ln, xv);
 
-        // 1. the input window (adjacent lanes on adjacent 16-byte pieces)
-        for (int t = lane; t < XR * XC * G; t += 64) {
-            const int px = t / G, pc = t - px * G, rr = px / XC, cc = px - rr * XC;
-            const int gr = r0 + rr, gc = c0 + cc;
-            u32x4 v = {0u, 0u, 0u, 0u};
-            if (gr >= 0 && gr < H && gc >= 0 && gc < W)
-                v = *reinterpret_cast<const u32x4 *>(xn + ((size_t)gr * W + gc) * C + pc * 8);
-            *reinterpret_cast<u32x4 *>(X + (uint32_t)px * PP + (uint32_t)pc * 16) = v;
-        }
-
-        // 2. the grouped conv at the virtual positions; task = (group, position),
-        //    group-major so that the lanes of a pass share the taps they read
-        for (int t = lane; t < VR * VC * G; t += 64) {
-            const int g = t / (VR * VC), pos = t - g * (VR * VC), vr = pos / VC, vc = pos - vr * VC;
-            const int ar = refl(2 * i - 1 + vr, H) - r0, ac = refl(2 * j0 - 1 + vc, W) - c0;  // window coordinates
-            float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+            // 2. the grouped conv on the matrix unit (one group at a time:
+            //    an unrolled group loop hoists the LDS reads of later groups
+            //    and runs out of registers)
 #pragma unroll 1
-            for (int di = 0; di < 3; di++)  // (rolled: the 72 tap reads of an unrolled body would fill the registers)
+            for (int g = 0; g < G; g++) {
+                // A lane (row jl = 8s + o, K 8q .. 8q + 7): tap row q - s
+                const int di = q - (jl >> 3);
+                const bool tap = di >= 0 && di <= 2;
+                u32x4 av[3];
 #pragma unroll
                 for (int dj = 0; dj < 3; dj++) {
-                    Pack8 xv;
-                    xv.u = *reinterpret_cast<const u32x4 *>(X + (uint32_t)((ar + di - 1) * XC + ac + dj - 1) * PP +
-                                                            (uint32_t)g * 16);
-                    const uint8_t *tp = smem + (uint32_t)(((di * 3 + dj) * C + 8 * g) * 16);
-#pragma unroll
-                    for (int o = 0; o < 8; o++) {
-                        Pack8 w8;
-                        w8.u = *reinterpret_cast<const u32x4 *>(tp + o * 16);
-#pragma unroll
-                        for (int e = 0; e < 4; e++)
-                            acc[o] = dot2(xv.w[e], w8.w[e], acc[o], T{});
-                    }
+                    const u32x4 v = *reinterpret_cast<const u32x4 *>(
+                        smem + (uint32_t)((((tap ? di : 0) * 3 + dj) * C + 8 * g + (jl & 7)) * 16));
+                    av[dj] = tap ? v : u32x4{0u, 0u, 0u, 0u};
                 }
-            u32x4 out;
+                // D lane (column jl, rows 4q .. 4q + 3): conv row w0 + (q >> 1),
+                // channels 8g + 4 (q & 1) .. + 3
+                const int cd = 8 * g + 4 * (q & 1);
+                float sc[4], bi[4];
 #pragma unroll
-            for (int e = 0; e < 4; e++) {
-                const int c = 8 * g + 2 * e;
-                const float sa = a.s0 ? a.s0[c] : 1.0f, sb = a.s0 ? a.s0[c + 1] : 1.0f;
-                const float ba = a.b0 ? a.b0[c] : 0.0f, bb = a.b0 ? a.b0[c + 1] : 0.0f;
-                out[e] = T::pack2(fmaf(acc[2 * e], sa, ba), fmaf(acc[2 * e + 1], sb, bb));
+                for (int e = 0; e < 4; e++) {
+                    sc[e] = s0l[cd + e];
+                    bi[e] = b0l[cd + e];
+                }
+#pragma unroll
+                for (int rs = 0; rs < 2; rs++)
+#pragma unroll
+                    for (int ct = 0; ct < 3; ct++) {
+                        const int vc = 16 * ct + jl, vcl = vc < VC ? vc : VC - 1;  // columns past 32 are not kept
+                        const uint8_t *bp = X + (uint32_t)((rs + q) * XC + vcl) * PP + (uint32_t)g * 16;
+                        float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                        for (int dj = 0; dj < 3; dj++)
+                            d = T::mfma(av[dj], *reinterpret_cast<const u32x4 *>(bp + dj * PP), d);
+                        if ((rs == 0 || q >= 2) && vc < VC)
+                            *reinterpret_cast<u32x2 *>(V + (uint32_t)((rs + (q >> 1)) * VC + vc) * PP +
+                                                       (uint32_t)cd * 2) =
+                                u32x2{T::pack2(fmaf(d[0], sc[0], bi[0]), fmaf(d[1], sc[1], bi[1])),
+                                      T::pack2(fmaf(d[2], sc[2], bi[2]), fmaf(d[3], sc[3], bi[3]))};
+                    }
             }
-            *reinterpret_cast<u32x4 *>(V + (uint32_t)pos * PP + (uint32_t)g * 16) = out;
-        }
 
-        // 3. BlurPool of the conv output (virtual layout) and of the input
-        //    (reflected window positions) into the tile [16][C2P]
-        for (int t = lane; t < UPX * (C2P / 4); t += 64) {
-            const int px = t / (C2P / 4), c = 4 * (t - px * (C2P / 4));
-            float acc[4] = {0.f, 0.f, 0.f, 0.f};
-            if (c < C2) {
+            // 3. BlurPool of the conv output and of the input (reflected
+            //    positions; the conv map sits one row and one column inside
+            //    the window) into the tile [16][C2P]
+#pragma unroll 2
+            for (int t = lane; t < UPX * (C2P / 4); t += 64) {
+                const int px = t / (C2P / 4), c = 4 * (t - px * (C2P / 4));
+                float acc[4] = {0.f, 0.f, 0.f, 0.f};
+                if (c < C2) {
 #pragma unroll
-                for (int ta = 0; ta < 3; ta++)
+                    for (int ta = 0; ta < 3; ta++)
 #pragma unroll
-                    for (int tb = 0; tb < 3; tb++) {
-                        const float wt = (ta == 1 ? 0.5f : 0.25f) * (tb == 1 ? 0.5f : 0.25f);
-                        const uint8_t *src;
-                        if (c < C) {
-                            src = V + (uint32_t)(ta * VC + 2 * px + tb) * PP + (uint32_t)c * 2;
-                        } else {
+                        for (int tb = 0; tb < 3; tb++) {
+                            const float wt = (ta == 1 ? 0.5f : 0.25f) * (tb == 1 ? 0.5f : 0.25f);
                             const int xr = refl(2 * i + ta - 1, H) - r0, xc = refl(2 * (j0 + px) + tb - 1, W) - c0;
-                            src = X + (uint32_t)(xr * XC + xc) * PP + (uint32_t)(c - C) * 2;
+                            const uint8_t *src = c < C
+                                                     ? V + (uint32_t)((xr - 1) * VC + xc - 1) * PP + (uint32_t)c * 2
+                                                     : X + (uint32_t)(xr * XC + xc) * PP + (uint32_t)(c - C) * 2;
+                            const u32x2 v = *reinterpret_cast<const u32x2 *>(src);
+                            acc[0] = fmaf(wt, T::lo(v[0]), acc[0]);
+                            acc[1] = fmaf(wt, T::hi(v[0]), acc[1]);
+                            acc[2] = fmaf(wt, T::lo(v[1]), acc[2]);
+                            acc[3] = fmaf(wt, T::hi(v[1]), acc[3]);
                         }
-                        const u32x2 v = *reinterpret_cast<const u32x2 *>(src);
-                        acc[0] = fmaf(wt, T::lo(v[0]), acc[0]);
-                        acc[1] = fmaf(wt, T::hi(v[0]), acc[1]);
-                        acc[2] = fmaf(wt, T::lo(v[1]), acc[2]);
-                        acc[3] = fmaf(wt, T::hi(v[1]), acc[3]);
-                    }
+                }
+                *reinterpret_cast<u32x2 *>(Z + (uint32_t)px * PZ + (uint32_t)c * 2) =
+                    u32x2{T::pack2(acc[0], acc[1]), T::pack2(acc[2], acc[3])};
             }
-            *reinterpret_cast<u32x2 *>(Z + (uint32_t)px * PZ + (uint32_t)c * 2) =
-                u32x2{T::pack2(acc[0], acc[1]), T::pack2(acc[2], acc[3])};
-        }
 
-        // 4. the FFN
-        const int q = lane >> 4, jl = lane & 15;
-        u32x4 zf[KS];
+            // 4. the FFN
+            u32x4 zf[KS];
 #pragma unroll
-        for (int ks = 0; ks < KS; ks++)
-            zf[ks] = *reinterpret_cast<const u32x4 *>(Z + (uint32_t)jl * PZ + (uint32_t)(32 * ks + 8 * q) * 2);
-        const int R = a.R, OT = (a.K + 15) / 16;  // K % 16 == 8: the last tile's upper half is masked
-        float4v acc_o[KMAX / 16];
+            for (int ks = 0; ks < KS; ks++)
+                zf[ks] = *reinterpret_cast<const u32x4 *>(Z + (uint32_t)jl * PZ + (uint32_t)(32 * ks + 8 * q) * 2);
+            float4v acc_o[OTM];
 #pragma unroll
-        for (int ot = 0; ot < KMAX / 16; ot++)
-            acc_o[ot] = float4v{0.f, 0.f, 0.f, 0.f};
-        for (int kk = 0; kk < (R + 31) / 32; kk++) {
-            uint32_t hp[4];
+            for (int ot = 0; ot < OTM; ot++)
+                acc_o[ot] = float4v{0.f, 0.f, 0.f, 0.f};
+            auto chunk = [&](int kk) {
+                // the fragments from the row-major pieces; then the next
+                // chunk's pieces are loaded into the same registers
+                u32x4 w1f[2][KS], w2f[OTM];
 #pragma unroll
-            for (int t = 0; t < 2; t++) {
-                const int h0 = 32 * kk + 16 * t;  // the expand tile's first hidden channel
-                float4v u = {0.f, 0.f, 0.f, 0.f};
-                if (h0 < R) {  // wave-uniform
-                    const uint16_t *wr = a.w1 + (size_t)(h0 + jl) * C2;
+                for (int t = 0; t < 2; t++)
 #pragma unroll
-                    for (int ks = 0; ks < KS; ks++) {
-                        const int k = 32 * ks + 8 * q;
-                        const u32x4 av = k < C2 ? *reinterpret_cast<const u32x4 *>(wr + k) : u32x4{0u, 0u, 0u, 0u};
-                        u = T::mfma(av, zf[ks], u);
-                    }
-                }
-                // lane (q, jl) holds hidden h0 + 4q + e of pixel jl
-                const int hh = h0 + 4 * q;
+                    for (int ks = 0; ks < KS; ks++)
 #pragma unroll
-                for (int e2 = 0; e2 < 2; e2++) {
-                    float v[2];
+                        for (int d = 0; d < 4; d++)
+                            w1f[t][ks][d] = perm(pidx, f.w1[t][ks][d]);
 #pragma unroll
-                    for (int s = 0; s < 2; s++) {
-                        const int h = hh + 2 * e2 + s;
-                        v[s] = 0.0f;
-                        if (h0 < R) {
-                            const float sc = a.s1 ? a.s1[h] : 1.0f, bi = a.b1 ? a.b1[h] : 0.0f;
-                            v[s] = act_f(fmaf(u[2 * e2 + s], sc, bi), a.act);
+                for (int ot = 0; ot < OTM; ot++)
+                    if (ot < OT)
+#pragma unroll
+                        for (int d = 0; d < 4; d++)
+                            w2f[ot][d] = perm(pidx, f.w2[ot][d >> 1][d & 1]);
+                load_frag(a, min(kk + 1, NKK - 1), lr, lp, f);
+                uint32_t hp[4];
+#pragma unroll
+                for (int t = 0; t < 2; t++) {
+                    const int h0 = 32 * kk + 16 * t;  // the expand tile's first hidden channel
+                    float4v u = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int ks = 0; ks < KS; ks++)
+                        u = T::mfma(w1f[t][ks], zf[ks], u);
+                    // lane (q, jl) holds hidden h0 + 4q + e of pixel jl; the
+                    // tile past R (R % 32 == 16) is zero
+                    const bool live = h0 < R;  // wave-uniform
+                    const int hh = live ? h0 + 4 * q : 0;
+#pragma unroll
+                    for (int e2 = 0; e2 < 2; e2++) {
+                        float v[2];
+#pragma unroll
+                        for (int s = 0; s < 2; s++) {
+                            const int h = hh + 2 * e2 + s;
+                            v[s] = live ? act_f(fmaf(u[2 * e2 + s], s1l[h], b1l[h]), a.act) : 0.0f;
                         }
+                        hp[2 * t + e2] = T::pack2(v[0], v[1]);
                     }
-                    hp[2 * t + e2] = T::pack2(v[0], v[1]);
+                }
+                const u32x4 ub = {hp[0], hp[1], hp[2], hp[3]};
+#pragma unroll
+                for (int ot = 0; ot < OTM; ot++)
+                    if (ot < OT)
+                        acc_o[ot] = T::mfma(w2f[ot], ub, acc_o[ot]);
+            };
+#pragma unroll 1
+            for (int kk = 0; kk < NKK; kk++)
+                chunk(kk);
+            // y = s2 * acc + b2: lane (q, jl) holds channels 16 ot + 4q .. + 3 of pixel j0 + jl
+            if (j0 + jl < a.Wo) {
+                uint16_t *yp = a.y + (((size_t)un.n * a.Ho + i) * a.Wo + j0 + jl) * K;
+#pragma unroll
+                for (int ot = 0; ot < OTM; ot++) {
+                    const int o = 16 * ot + 4 * q;
+                    if (o >= K)
+                        continue;
+                    float r[4];
+#pragma unroll
+                    for (int e = 0; e < 4; e++)
+                        r[e] = fmaf(acc_o[ot][e], s2l[o + e], b2l[o + e]);
+                    *reinterpret_cast<u32x2 *>(yp + o) = u32x2{T::pack2(r[0], r[1]), T::pack2(r[2], r[3])};
                 }
             }
-            const u32x4 ub = {hp[0], hp[1], hp[2], hp[3]};
-            // W2 rows 16 ot + jl at hidden 32kk + 4q .. + 3 and 32kk + 16 + 4q .. + 3
-            const int ha = 32 * kk + 4 * q, hb = ha + 16;
-#pragma unroll
-            for (int ot = 0; ot < KMAX / 16; ot++) {
-                if (ot >= OT)
-                    break;
-                const bool row = 16 * ot + jl < a.K;
-                const uint16_t *wr = a.w2 + (size_t)(row ? 16 * ot + jl : 0) * R;
-                const u32x2 pa = row ? *reinterpret_cast<const u32x2 *>(wr + ha) : u32x2{0u, 0u};
-                const u32x2 pb = row && hb < R ? *reinterpret_cast<const u32x2 *>(wr + hb) : u32x2{0u, 0u};
-                acc_o[ot] = T::mfma(u32x4{pa[0], pa[1], pb[0], pb[1]}, ub, acc_o[ot]);
-            }
-        }
-        // y = s2 * acc + b2: lane (q, jl) holds channels 16 ot + 4q .. + 3 of pixel j0 + jl
-        if (j0 + jl < a.Wo) {
-            uint16_t *yp = a.y + (((size_t)n * a.Ho + i) * a.Wo + j0 + jl) * a.K;
-#pragma unroll
-            for (int ot = 0; ot < KMAX / 16; ot++) {
-                if (ot >= OT)
-                    break;
-                const int o = 16 * ot + 4 * q;
-                if (o >= a.K)
-                    continue;
-                float r[4];
-#pragma unroll
-                for (int e = 0; e < 4; e++)
-                    r[e] = fmaf(acc_o[ot][e], a.s2 ? a.s2[o + e] : 1.0f, a.b2 ? a.b2[o + e] : 0.0f);
-                *reinterpret_cast<u32x2 *>(yp + o) = u32x2{T::pack2(r[0], r[1]), T::pack2(r[2], r[3])};
-            }
+            if (next >= a.units)
+                break;
+            unit = next;
+            if (!PREF)
+                load_window(a, unit, ln, xv);
         }
     }
 };
 
-template <typename T, int C>
+template <typename T, int C, int OTM>
 __global__ __launch_bounds__(256) void cfs2_kernel(Args a) {
     extern __shared__ __attribute__((aligned(256))) uint8_t smem[];
-    Kern<T, C>::run(a, smem);
+    Kern<T, C, OTM>::run(a, smem);
 }
-
-template <int C>
-uint32_t region_bytes() {
-    return Kern<F16, C>::REGION;
-}
-
-inline uint32_t taps_bytes(int C) { return ((uint32_t)(9 * C * 8 * 2) + 255) & ~255u; }
 
 inline uint32_t region_for(int C) {
     switch (C) {
-    case 16: return region_bytes<16>();
-    case 24: return region_bytes<24>();
-    case 32: return region_bytes<32>();
-    case 48: return region_bytes<48>();
-    case 64: return region_bytes<64>();
+    case 16: return Kern<F16, 16, 4>::REGION;
+    case 24: return Kern<F16, 24, 4>::REGION;
+    case 32: return Kern<F16, 32, 4>::REGION;
+    case 48: return Kern<F16, 48, 4>::REGION;
+    case 64: return Kern<F16, 64, 4>::REGION;
     default: return 0;
     }
 }
 
-// waves per workgroup: as many as four regions fit beside the taps
-inline int waves_for(int C) {
-    const uint32_t r = region_for(C);
-    if (!r)
-        return 0;
-    int nw = (int)((160u * 1024u - taps_bytes(C)) / r);
-    return nw > 4 ? 4 : nw;
+// waves per workgroup (1 .. 4): the count that lets a compute unit's LDS
+// hold the most waves (every workgroup stages its own taps and vectors);
+// 0 when not even one wave fits
+inline int waves_for(int C, int R, int K) {
+    const uint32_t r = region_for(C), st = staged_bytes(C, R, K), lds = 160u * 1024u;
+    int best = 0, best_waves = 0;
+    for (int nw = 1; r && nw <= 4; nw++) {
+        const uint32_t wg = st + (uint32_t)nw * r;
+        const int waves = wg <= lds ? nw * (int)(lds / wg) : 0;
+        if (waves >= best_waves && waves > 0) {
+            best = nw;
+            best_waves = waves;
+        }
+    }
+    return best;
 }
 
-template <typename T, int C>
+template <typename T, int C, int OTM>
 hipError_t launch_t(const Args &a, size_t lds, int grid, hipStream_t st) {
-    auto kf = cfs2_kernel<T, C>;
+    auto kf = cfs2_kernel<T, C, OTM>;
     hipError_t e = allow_full_lds((const void *)kf);
     if (e != hipSuccess)
         return e;
@@ -300,14 +438,21 @@ hipError_t launch_t(const Args &a, size_t lds, int grid, hipStream_t st) {
     return hipGetLastError();
 }
 
+template <typename T, int C>
+hipError_t launch_k(const Args &a, size_t lds, int grid, hipStream_t st) {
+    if (a.K <= 32)
+        return launch_t<T, C, 2>(a, lds, grid, st);
+    return a.K <= 64 ? launch_t<T, C, 4>(a, lds, grid, st) : launch_t<T, C, 8>(a, lds, grid, st);
+}
+
 template <typename T>
 hipError_t launch_c(const Args &a, int C, size_t lds, int grid, hipStream_t st) {
     switch (C) {
-    case 16: return launch_t<T, 16>(a, lds, grid, st);
-    case 24: return launch_t<T, 24>(a, lds, grid, st);
-    case 32: return launch_t<T, 32>(a, lds, grid, st);
-    case 48: return launch_t<T, 48>(a, lds, grid, st);
-    case 64: return launch_t<T, 64>(a, lds, grid, st);
+    case 16: return launch_k<T, 16>(a, lds, grid, st);
+    case 24: return launch_k<T, 24>(a, lds, grid, st);
+    case 32: return launch_k<T, 32>(a, lds, grid, st);
+    case 48: return launch_k<T, 48>(a, lds, grid, st);
+    case 64: return launch_k<T, 64>(a, lds, grid, st);
     default: return hipErrorInvalidValue;
     }
 }
@@ -315,8 +460,8 @@ hipError_t launch_c(const Args &a, int C, size_t lds, int grid, hipStream_t st) 
 }  // namespace cfs2
 
 bool convfirst_s2_supported(int H, int W, int C, int R, int K) {
-    return H >= 2 && W >= 2 && cfs2::waves_for(C) >= 1 && R >= 16 && R % 16 == 0 && R <= cfs2::RMAX &&
-           K >= 8 && K % 8 == 0 && K <= cfs2::KMAX;
+    return H >= 2 && W >= 2 && R >= 16 && R % 16 == 0 && R <= cfs2::RMAX && K >= 8 && K % 8 == 0 &&
+           K <= cfs2::KMAX && cfs2::waves_for(C, R, K) >= 1;
 }
 
 hipError_t launch_convfirst_s2(const void *x, void *y, const BlockW &w, int N, int H, int W, int C, int R, int K,
@@ -349,10 +494,14 @@ hipError_t launch_convfirst_s2(const void *x, void *y, const BlockW &w, int N, i
     if (units > (int64_t)1 << 30)
         return hipErrorInvalidValue;
     a.units = (int)units;
-    a.nw = cfs2::waves_for(C);
-    a.off_region = cfs2::taps_bytes(C);
+    a.nw = cfs2::waves_for(C, R, K);
+    a.off_region = cfs2::staged_bytes(C, R, K);
     const size_t lds = a.off_region + (size_t)a.nw * cfs2::region_for(C);
-    const int grid = (a.units + a.nw - 1) / a.nw;
+    // persistent workgroups: as many as the LDS lets every compute unit hold
+    const int per_cu = (int)((160u * 1024u) / lds);
+    const int64_t need = (a.units + a.nw - 1) / a.nw;
+    const int64_t cap = (int64_t)(per_cu > 0 ? per_cu : 1) * device_cu_count();
+    const int grid = (int)(need < cap ? need : cap);
     return bf16 ? cfs2::launch_c<BF16>(a, C, lds, grid, st) : cfs2::launch_c<F16>(a, C, lds, grid, st);
 }
 
