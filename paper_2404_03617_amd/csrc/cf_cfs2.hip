@@ -77,15 +77,16 @@ struct Args {
 
 __device__ __forceinline__ int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
 
+// v_mul_u32_u24 (both factors below 2^24)
+__device__ __forceinline__ uint32_t mul24(uint32_t a, uint32_t b) { return (uint32_t)__umul24(a, b); }
+
 // one pixel of reflect padding (-1 -> 1, n -> n - 2); past that (the padded
 // pixels of a unit at the right edge, whose outputs are not stored) the last
 // column
 __device__ __forceinline__ int refl(int v, int n) {
-    if (v < 0)
-        return -v;
-    if (v == n)
-        return n - 2;
-    return v > n ? n - 1 : v;
+    int r = v < 0 ? -v : v;
+    r = r == n ? n - 2 : r;
+    return r < n ? r : n - 1;
 }
 
 __device__ __forceinline__ float act_f(float u, int act) {
@@ -130,33 +131,50 @@ struct Kern {
 
     // window piece it of this lane: pixel (rr, cc) of the window, 16-byte
     // piece pc; adjacent lanes on adjacent pieces
-    static __device__ __forceinline__ void load_window(const Args &a, int u, int lane, u32x4 (&xv)[NIT]) {
-        const Unit un = decode(a, u);
-        const uint16_t *xn = a.x + (size_t)un.n * a.H * a.W * C;
-        const int r0 = 2 * un.i - 2, c0 = 2 * un.j0 - 2;
-#pragma unroll
-        for (int it = 0; it < NIT; it++) {
-            const int t = lane + 64 * it, tt = t < NX ? t : NX - 1;
-            const int px = tt / G, pc = tt - px * G, rr = px / XC, cc = px - rr * XC;
-            const int gr = clampi(r0 + rr, 0, a.H - 1), gc = clampi(c0 + cc, 0, a.W - 1);
-            xv[it] = *reinterpret_cast<const u32x4 *>(xn + ((size_t)gr * a.W + gc) * C + pc * 8);
-        }
+    // piece it of a lane: window pixel px = (rr, cc), 16-byte piece pc;
+    // adjacent lanes on adjacent pieces; lanes past the last piece take the
+    // last piece again
+    struct Piece {
+        int px, pc, rr, cc;
+    };
+    static __device__ __forceinline__ Piece piece(int lane, int it) {
+        const int t = lane + 64 * it, tt = t < NX ? t : NX - 1;
+        const int px = tt / G, rr = px / XC;
+        return Piece{px, tt - px * G, rr, px - rr * XC};
     }
 
-    static __device__ __forceinline__ void store_window(const Args &a, int u, int lane, const u32x4 (&xv)[NIT],
-                                                        uint8_t *X) {
+    // the piece's 16 bytes of image n at window origin (r0, c0), the
+    // position clamped into the image (the pieces outside are stored as
+    // zeros)
+    static __device__ __forceinline__ u32x4 load_piece(const Args &a, const Unit &un, const Piece &p) {
+        const int gr = clampi(2 * un.i - 2 + p.rr, 0, a.H - 1), gc = clampi(2 * un.j0 - 2 + p.cc, 0, a.W - 1);
+        const uint32_t pix = mul24((uint32_t)gr, (uint32_t)a.W) + (uint32_t)gc;
+        const uint16_t *xn = a.x + (size_t)un.n * a.H * a.W * C;
+        return *reinterpret_cast<const u32x4 *>(xn + (size_t)pix * C + p.pc * 8);
+    }
+
+    static __device__ __forceinline__ void load_window(const Args &a, int u, int lane, u32x4 (&xv)[NIT]) {
         const Unit un = decode(a, u);
+#pragma unroll
+        for (int it = 0; it < NIT; it++)
+            xv[it] = load_piece(a, un, piece(lane, it));
+    }
+
+    // this unit's window into LDS; with PREF the next unit's pieces are
+    // loaded into the same registers as they are stored
+    static __device__ __forceinline__ void store_window(const Args &a, int u, int next, int lane, u32x4 (&xv)[NIT],
+                                                        uint8_t *X) {
+        const Unit un = decode(a, u), nx = decode(a, next);
         const int r0 = 2 * un.i - 2, c0 = 2 * un.j0 - 2;
 #pragma unroll
         for (int it = 0; it < NIT; it++) {
-            const int t = lane + 64 * it;
-            if (t < NX) {
-                const int px = t / G, pc = t - px * G, rr = px / XC, cc = px - rr * XC;
-                const int gr = r0 + rr, gc = c0 + cc;
-                const bool in = gr >= 0 && gr < a.H && gc >= 0 && gc < a.W;
-                *reinterpret_cast<u32x4 *>(X + (uint32_t)px * PP + (uint32_t)pc * 16) =
-                    in ? xv[it] : u32x4{0u, 0u, 0u, 0u};
-            }
+            const Piece p = piece(lane, it);
+            const int gr = r0 + p.rr, gc = c0 + p.cc;
+            const bool in = gr >= 0 && gr < a.H && gc >= 0 && gc < a.W;
+            *reinterpret_cast<u32x4 *>(X + (uint32_t)p.px * PP + (uint32_t)p.pc * 16) =
+                in ? xv[it] : u32x4{0u, 0u, 0u, 0u};
+            if (PREF)
+                xv[it] = load_piece(a, nx, p);
         }
     }
 
@@ -234,12 +252,10 @@ struct Kern {
             const int i = un.i, j0 = un.j0, r0 = 2 * i - 2, c0 = 2 * j0 - 2;
             // 1. the window into LDS; the first FFN chunk's fragments and,
             //    with few channels, the next unit's window in flight
-            store_window(a, unit, ln, xv, X);
             const int next = unit + stride;
             Frag f;
             load_frag(a, 0, lr, lp, f);
-            if (PREF)
-                load_window(a, next < a.units ? next : unit, ln, xv);
+            store_window(a, unit, next < a.units ? next : unit, ln, xv, X);
 
             // 2. the grouped conv on the matrix unit (one group at a time:
             //    an unrolled group loop hoists the LDS reads of later groups
@@ -286,29 +302,38 @@ struct Kern {
             // 3. BlurPool of the conv output and of the input (reflected
             //    positions; the conv map sits one row and one column inside
             //    the window) into the tile [16][C2P]
+            //    Lane-constant per pass: the pixel, the four channels, the
+            //    map they come from (its base and row stride); the rows'
+            //    reflections are wave-uniform.
+            const uint32_t xr0 = refl(2 * i - 1, H) - r0, xr1 = 2, xr2 = refl(2 * i + 1, H) - r0;
 #pragma unroll 2
-            for (int t = lane; t < UPX * (C2P / 4); t += 64) {
+            for (int t = ln; t < UPX * (C2P / 4); t += 64) {
                 const int px = t / (C2P / 4), c = 4 * (t - px * (C2P / 4));
+                const bool cz = C2P == C2 || c < C2;      // zero padding past 2C
+                const int cc = cz ? c : 0;
+                const bool isv = cc < C;
+                const uint32_t base = isv ? (uint32_t)(V - X) - (uint32_t)(VC + 1) * PP + (uint32_t)cc * 2
+                                          : (uint32_t)(cc - C) * 2;
+                const uint32_t rst = isv ? (uint32_t)VC * PP : (uint32_t)XC * PP;
+                const uint32_t ro[3] = {mul24(xr0, rst), mul24(xr1, rst), mul24(xr2, rst)};
+                uint32_t co[3];
+#pragma unroll
+                for (int tb = 0; tb < 3; tb++)
+                    co[tb] = mul24((uint32_t)(refl(2 * (j0 + px) + tb - 1, W) - c0), PP);
                 float acc[4] = {0.f, 0.f, 0.f, 0.f};
-                if (c < C2) {
 #pragma unroll
-                    for (int ta = 0; ta < 3; ta++)
+                for (int ta = 0; ta < 3; ta++)
 #pragma unroll
-                        for (int tb = 0; tb < 3; tb++) {
-                            const float wt = (ta == 1 ? 0.5f : 0.25f) * (tb == 1 ? 0.5f : 0.25f);
-                            const int xr = refl(2 * i + ta - 1, H) - r0, xc = refl(2 * (j0 + px) + tb - 1, W) - c0;
-                            const uint8_t *src = c < C
-                                                     ? V + (uint32_t)((xr - 1) * VC + xc - 1) * PP + (uint32_t)c * 2
-                                                     : X + (uint32_t)(xr * XC + xc) * PP + (uint32_t)(c - C) * 2;
-                            const u32x2 v = *reinterpret_cast<const u32x2 *>(src);
-                            acc[0] = fmaf(wt, T::lo(v[0]), acc[0]);
-                            acc[1] = fmaf(wt, T::hi(v[0]), acc[1]);
-                            acc[2] = fmaf(wt, T::lo(v[1]), acc[2]);
-                            acc[3] = fmaf(wt, T::hi(v[1]), acc[3]);
-                        }
-                }
+                    for (int tb = 0; tb < 3; tb++) {
+                        const float wt = (ta == 1 ? 0.5f : 0.25f) * (tb == 1 ? 0.5f : 0.25f);
+                        const u32x2 v = *reinterpret_cast<const u32x2 *>(X + base + ro[ta] + co[tb]);
+                        acc[0] = fmaf(wt, T::lo(v[0]), acc[0]);
+                        acc[1] = fmaf(wt, T::hi(v[0]), acc[1]);
+                        acc[2] = fmaf(wt, T::lo(v[1]), acc[2]);
+                        acc[3] = fmaf(wt, T::hi(v[1]), acc[3]);
+                    }
                 *reinterpret_cast<u32x2 *>(Z + (uint32_t)px * PZ + (uint32_t)c * 2) =
-                    u32x2{T::pack2(acc[0], acc[1]), T::pack2(acc[2], acc[3])};
+                    cz ? u32x2{T::pack2(acc[0], acc[1]), T::pack2(acc[2], acc[3])} : u32x2{0u, 0u};
             }
 
             // 4. the FFN
@@ -350,13 +375,15 @@ struct Kern {
                     // tile past R (R % 32 == 16) is zero
                     const bool live = h0 < R;  // wave-uniform
                     const int hh = live ? h0 + 4 * q : 0;
+                    const float4v sc = *reinterpret_cast<const float4v *>(s1l + hh),
+                                  bi = *reinterpret_cast<const float4v *>(b1l + hh);
 #pragma unroll
                     for (int e2 = 0; e2 < 2; e2++) {
                         float v[2];
 #pragma unroll
                         for (int s = 0; s < 2; s++) {
-                            const int h = hh + 2 * e2 + s;
-                            v[s] = live ? act_f(fmaf(u[2 * e2 + s], s1l[h], b1l[h]), a.act) : 0.0f;
+                            const int e = 2 * e2 + s;
+                            v[s] = live ? act_f(fmaf(u[e], sc[e], bi[e]), a.act) : 0.0f;
                         }
                         hp[2 * t + e2] = T::pack2(v[0], v[1]);
                     }
