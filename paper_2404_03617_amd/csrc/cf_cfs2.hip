@@ -34,8 +34,12 @@
 //     the project with the K order position 8q + e <-> hidden 32kk + 4q + e
 //     (e < 4) or 32kk + 16 + 4q + e - 4, the lane layout the expand leaves,
 //     and the W2 fragments are read in that order; s2, b2; y stored once.
-//     A chunk's W1 and W2 pieces are loaded from global memory (L2) one
-//     chunk ahead, the first chunk's during the conv.  Every load of the loop is unconditional (addresses clamped; the
+//     When W1 and W2 fit in LDS beside the regions with two waves per
+//     SIMD (or as many as without them), the workgroup stages them there
+//     once (rows padded by 16 bytes, so the sixteen rows of a fragment read
+//     fall in distinct banks) and the fragments are read from LDS.  Otherwise a chunk's W1 and W2
+//     pieces are loaded from global memory (L2) one chunk ahead, the first
+//     chunk's during the conv.  Every load of the loop is unconditional (addresses clamped; the
 //     rows past R meet zero hidden values, the rows past K are not stored),
 //     so the waits count exactly.  The loads are row-major -- lane 4r + p
 //     takes piece p of row r, four adjacent lanes on one contiguous run --
@@ -72,7 +76,8 @@ struct Args {
     int H, W, Ho, Wo, R, K, act;
     int units, jt;        // units = N * Ho * jt, jt = ceil(Wo / 16)
     int nw;               // waves per workgroup
-    uint32_t off_region;  // LDS: taps, s0, b0, s1, b1, s2, b2, then one region per wave
+    uint32_t off_w1, off_w2;  // LDS: taps, s0, b0, s1, b1, s2, b2; W1 and W2 when staged;
+    uint32_t off_region;      // then one region per wave
 };
 
 __device__ __forceinline__ int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
@@ -102,7 +107,14 @@ __host__ __device__ inline uint32_t staged_bytes(int C, int R, int K) {
     return ((uint32_t)(9 * C * 16 + 4 * (2 * C + 2 * R + 2 * K)) + 255) & ~255u;
 }
 
-template <typename T, int C, int OTM>
+// row strides of W1 and W2 staged in LDS
+__host__ __device__ inline uint32_t w1_stride(int C) { return (uint32_t)(4 * C + 16); }
+__host__ __device__ inline uint32_t w2_stride(int R) { return (uint32_t)(2 * R + 16); }
+__host__ __device__ inline uint32_t weights_bytes(int C, int R, int K) {
+    return ((uint32_t)R * w1_stride(C) + (uint32_t)K * w2_stride(R) + 255) & ~255u;
+}
+
+template <typename T, int C, int OTM, bool WL>
 struct Kern {
     static constexpr int G = C / 8;                            // groups of the conv
     static constexpr uint32_t PP = 2 * C + 16;                 // LDS bytes per window / conv pixel
@@ -230,6 +242,20 @@ struct Kern {
             s2l[o] = a.s2 ? a.s2[o] : 1.0f;
             b2l[o] = a.b2 ? a.b2[o] : 0.0f;
         }
+        if constexpr (WL) {
+            // W1 [R][2C] and W2 [K][R] in 16-byte pieces, adjacent threads on
+            // adjacent pieces
+            for (int i = tid; i < R * (C / 4); i += a.nw * 64) {
+                const int r = i / (C / 4), pc = i - r * (C / 4);
+                *reinterpret_cast<u32x4 *>(smem + a.off_w1 + (uint32_t)r * w1_stride(C) + (uint32_t)pc * 16) =
+                    *reinterpret_cast<const u32x4 *>(a.w1 + (size_t)i * 8);
+            }
+            for (int i = tid; i < K * (R / 8); i += a.nw * 64) {
+                const int r = i / (R / 8), pc = i - r * (R / 8);
+                *reinterpret_cast<u32x4 *>(smem + a.off_w2 + (uint32_t)r * w2_stride(R) + (uint32_t)pc * 16) =
+                    *reinterpret_cast<const u32x4 *>(a.w2 + (size_t)i * 8);
+            }
+        }
         __syncthreads();
         int unit = (int)blockIdx.x * a.nw + wv;
         if (unit >= a.units)
@@ -254,7 +280,8 @@ struct Kern {
             //    with few channels, the next unit's window in flight
             const int next = unit + stride;
             Frag f;
-            load_frag(a, 0, lr, lp, f);
+            if constexpr (!WL)
+                load_frag(a, 0, lr, lp, f);
             store_window(a, unit, next < a.units ? next : unit, ln, xv, X);
 
             // 2. the grouped conv on the matrix unit (one group at a time:
@@ -346,23 +373,47 @@ struct Kern {
             for (int ot = 0; ot < OTM; ot++)
                 acc_o[ot] = float4v{0.f, 0.f, 0.f, 0.f};
             auto chunk = [&](int kk) {
-                // the fragments from the row-major pieces; then the next
-                // chunk's pieces are loaded into the same registers
                 u32x4 w1f[2][KS], w2f[OTM];
+                if constexpr (WL) {
+                    // the fragments straight from the staged rows (clamped)
 #pragma unroll
-                for (int t = 0; t < 2; t++)
+                    for (int t = 0; t < 2; t++) {
+                        const uint8_t *wr =
+                            smem + a.off_w1 + (uint32_t)min(32 * kk + 16 * t + jl, R - 1) * w1_stride(C);
 #pragma unroll
-                    for (int ks = 0; ks < KS; ks++)
+                        for (int ks = 0; ks < KS; ks++) {
+                            const int k = 32 * ks + 8 * q;
+                            w1f[t][ks] = *reinterpret_cast<const u32x4 *>(wr + (k < C2 ? k : 0) * 2);
+                        }
+                    }
+                    const int ha = 32 * kk + 4 * q, hb = ha + 16 < R ? ha + 16 : ha;
 #pragma unroll
-                        for (int d = 0; d < 4; d++)
-                            w1f[t][ks][d] = perm(pidx, f.w1[t][ks][d]);
+                    for (int ot = 0; ot < OTM; ot++)
+                        if (ot < OT) {
+                            const uint8_t *wr =
+                                smem + a.off_w2 + (uint32_t)min(16 * ot + jl, K - 1) * w2_stride(R);
+                            const u32x2 pa = *reinterpret_cast<const u32x2 *>(wr + ha * 2),
+                                        pb = *reinterpret_cast<const u32x2 *>(wr + hb * 2);
+                            w2f[ot] = u32x4{pa[0], pa[1], pb[0], pb[1]};
+                        }
+                } else {
+                    // the fragments from the row-major pieces; then the next
+                    // chunk's pieces are loaded into the same registers
 #pragma unroll
-                for (int ot = 0; ot < OTM; ot++)
-                    if (ot < OT)
+                    for (int t = 0; t < 2; t++)
 #pragma unroll
-                        for (int d = 0; d < 4; d++)
-                            w2f[ot][d] = perm(pidx, f.w2[ot][d >> 1][d & 1]);
-                load_frag(a, min(kk + 1, NKK - 1), lr, lp, f);
+                        for (int ks = 0; ks < KS; ks++)
+#pragma unroll
+                            for (int d = 0; d < 4; d++)
+                                w1f[t][ks][d] = perm(pidx, f.w1[t][ks][d]);
+#pragma unroll
+                    for (int ot = 0; ot < OTM; ot++)
+                        if (ot < OT)
+#pragma unroll
+                            for (int d = 0; d < 4; d++)
+                                w2f[ot][d] = perm(pidx, f.w2[ot][d >> 1][d & 1]);
+                    load_frag(a, min(kk + 1, NKK - 1), lr, lp, f);
+                }
                 uint32_t hp[4];
 #pragma unroll
                 for (int t = 0; t < 2; t++) {
@@ -421,28 +472,30 @@ struct Kern {
     }
 };
 
-template <typename T, int C, int OTM>
+template <typename T, int C, int OTM, bool WL>
 __global__ __launch_bounds__(256) void cfs2_kernel(Args a) {
     extern __shared__ __attribute__((aligned(256))) uint8_t smem[];
-    Kern<T, C, OTM>::run(a, smem);
+    Kern<T, C, OTM, WL>::run(a, smem);
 }
 
 inline uint32_t region_for(int C) {
     switch (C) {
-    case 16: return Kern<F16, 16, 4>::REGION;
-    case 24: return Kern<F16, 24, 4>::REGION;
-    case 32: return Kern<F16, 32, 4>::REGION;
-    case 48: return Kern<F16, 48, 4>::REGION;
-    case 64: return Kern<F16, 64, 4>::REGION;
+    case 16: return Kern<F16, 16, 4, false>::REGION;
+    case 24: return Kern<F16, 24, 4, false>::REGION;
+    case 32: return Kern<F16, 32, 4, false>::REGION;
+    case 48: return Kern<F16, 48, 4, false>::REGION;
+    case 64: return Kern<F16, 64, 4, false>::REGION;
     default: return 0;
     }
 }
 
 // waves per workgroup (1 .. 4): the count that lets a compute unit's LDS
-// hold the most waves (every workgroup stages its own taps and vectors);
-// 0 when not even one wave fits
-inline int waves_for(int C, int R, int K) {
-    const uint32_t r = region_for(C), st = staged_bytes(C, R, K), lds = 160u * 1024u;
+// hold the most waves (every workgroup stages its own taps and vectors, and
+// the weights when wl); 0 when not even one wave fits.  *per_cu receives
+// that many waves.
+inline int waves_for(int C, int R, int K, bool wl, int *per_cu = nullptr) {
+    const uint32_t r = region_for(C), lds = 160u * 1024u;
+    const uint32_t st = staged_bytes(C, R, K) + (wl ? weights_bytes(C, R, K) : 0u);
     int best = 0, best_waves = 0;
     for (int nw = 1; r && nw <= 4; nw++) {
         const uint32_t wg = st + (uint32_t)nw * r;
@@ -452,12 +505,24 @@ inline int waves_for(int C, int R, int K) {
             best_waves = waves;
         }
     }
+    if (per_cu)
+        *per_cu = best_waves;
     return best;
 }
 
-template <typename T, int C, int OTM>
+// the weights go to LDS when that still leaves two waves per SIMD, or as
+// many waves as without them (measured: at 128 x 128 x 16, 8 waves with the
+// weights in LDS beat 10 without; at 64 x 64 x 32, 4 lose to 6)
+inline bool weights_in_lds(int C, int R, int K) {
+    int wl = 0, wg = 0;
+    waves_for(C, R, K, true, &wl);
+    waves_for(C, R, K, false, &wg);
+    return wl >= 1 && (wl >= 8 || wl >= wg);
+}
+
+template <typename T, int C, int OTM, bool WL>
 hipError_t launch_t(const Args &a, size_t lds, int grid, hipStream_t st) {
-    auto kf = cfs2_kernel<T, C, OTM>;
+    auto kf = cfs2_kernel<T, C, OTM, WL>;
     hipError_t e = allow_full_lds((const void *)kf);
     if (e != hipSuccess)
         return e;
@@ -465,21 +530,26 @@ hipError_t launch_t(const Args &a, size_t lds, int grid, hipStream_t st) {
     return hipGetLastError();
 }
 
-template <typename T, int C>
-hipError_t launch_k(const Args &a, size_t lds, int grid, hipStream_t st) {
+template <typename T, int C, bool WL>
+hipError_t launch_w(const Args &a, size_t lds, int grid, hipStream_t st) {
     if (a.K <= 32)
-        return launch_t<T, C, 2>(a, lds, grid, st);
-    return a.K <= 64 ? launch_t<T, C, 4>(a, lds, grid, st) : launch_t<T, C, 8>(a, lds, grid, st);
+        return launch_t<T, C, 2, WL>(a, lds, grid, st);
+    return a.K <= 64 ? launch_t<T, C, 4, WL>(a, lds, grid, st) : launch_t<T, C, 8, WL>(a, lds, grid, st);
+}
+
+template <typename T, int C>
+hipError_t launch_k(const Args &a, bool wl, size_t lds, int grid, hipStream_t st) {
+    return wl ? launch_w<T, C, true>(a, lds, grid, st) : launch_w<T, C, false>(a, lds, grid, st);
 }
 
 template <typename T>
-hipError_t launch_c(const Args &a, int C, size_t lds, int grid, hipStream_t st) {
+hipError_t launch_c(const Args &a, int C, bool wl, size_t lds, int grid, hipStream_t st) {
     switch (C) {
-    case 16: return launch_k<T, 16>(a, lds, grid, st);
-    case 24: return launch_k<T, 24>(a, lds, grid, st);
-    case 32: return launch_k<T, 32>(a, lds, grid, st);
-    case 48: return launch_k<T, 48>(a, lds, grid, st);
-    case 64: return launch_k<T, 64>(a, lds, grid, st);
+    case 16: return launch_k<T, 16>(a, wl, lds, grid, st);
+    case 24: return launch_k<T, 24>(a, wl, lds, grid, st);
+    case 32: return launch_k<T, 32>(a, wl, lds, grid, st);
+    case 48: return launch_k<T, 48>(a, wl, lds, grid, st);
+    case 64: return launch_k<T, 64>(a, wl, lds, grid, st);
     default: return hipErrorInvalidValue;
     }
 }
@@ -488,7 +558,7 @@ hipError_t launch_c(const Args &a, int C, size_t lds, int grid, hipStream_t st) 
 
 bool convfirst_s2_supported(int H, int W, int C, int R, int K) {
     return H >= 2 && W >= 2 && R >= 16 && R % 16 == 0 && R <= cfs2::RMAX && K >= 8 && K % 8 == 0 &&
-           K <= cfs2::KMAX && cfs2::waves_for(C, R, K) >= 1;
+           K <= cfs2::KMAX && cfs2::waves_for(C, R, K, false) >= 1;
 }
 
 hipError_t launch_convfirst_s2(const void *x, void *y, const BlockW &w, int N, int H, int W, int C, int R, int K,
@@ -521,15 +591,18 @@ hipError_t launch_convfirst_s2(const void *x, void *y, const BlockW &w, int N, i
     if (units > (int64_t)1 << 30)
         return hipErrorInvalidValue;
     a.units = (int)units;
-    a.nw = cfs2::waves_for(C, R, K);
-    a.off_region = cfs2::staged_bytes(C, R, K);
+    const bool wl = cfs2::weights_in_lds(C, R, K);
+    a.nw = cfs2::waves_for(C, R, K, wl);
+    a.off_w1 = cfs2::staged_bytes(C, R, K);
+    a.off_w2 = a.off_w1 + (uint32_t)R * cfs2::w1_stride(C);
+    a.off_region = a.off_w1 + (wl ? cfs2::weights_bytes(C, R, K) : 0u);
     const size_t lds = a.off_region + (size_t)a.nw * cfs2::region_for(C);
     // persistent workgroups: as many as the LDS lets every compute unit hold
     const int per_cu = (int)((160u * 1024u) / lds);
     const int64_t need = (a.units + a.nw - 1) / a.nw;
     const int64_t cap = (int64_t)(per_cu > 0 ? per_cu : 1) * device_cu_count();
     const int grid = (int)(need < cap ? need : cap);
-    return bf16 ? cfs2::launch_c<BF16>(a, C, lds, grid, st) : cfs2::launch_c<F16>(a, C, lds, grid, st);
+    return bf16 ? cfs2::launch_c<BF16>(a, C, wl, lds, grid, st) : cfs2::launch_c<F16>(a, C, wl, lds, grid, st);
 }
 
 }  // namespace cf
