@@ -102,9 +102,16 @@ cf_status cf_block_forward(const void *x, void *y, const cf_block_params *p,
  * y and ws; blocks[depth] are host-side structs of device pointers.
  * cf_stage_workspace_bytes() returns the recommended ws size.  The minimum is
  * N*H*W*C*2 bytes (rounded up to 256) for depth > 1 and 0 for depth == 1;
- * for C = 512 fp16 the recommended size adds room for fp32 partial outputs,
- * and with it each block splits its hidden layer over several workgroups
- * (results identical up to fp32 summation order, still deterministic). */
+ * for C = 512 fp16 the recommended size adds 16*N*H*W*C bytes.  With that
+ * room, at N*H*W >= 4096 pixels, E <= 6 and every scale and bias pointer
+ * 16-byte aligned (or NULL), each block runs layer by layer (Sec. 5.2):
+ * a depth-wise kernel, the expand and project as hipBLASLt GEMMs with the
+ * hidden tensor in ws, and two elementwise kernels (s1, b1, activation;
+ * s2, b2, residual), rounding the GEMM outputs to fp16 before their scale
+ * and bias (within the block tolerance of the fused kernels; deterministic).
+ * Otherwise, with the room, each block splits its hidden layer over several
+ * workgroups (results identical up to fp32 summation order, deterministic).
+ * The library GEMMs are given no workspace of their own. */
 cf_status cf_stage_forward(const void *x, void *y, void *ws, size_t ws_bytes,
                            const cf_block_params *blocks, int depth,
                            int N, int H, int W, int C, int E, int k,

@@ -427,6 +427,27 @@ cf_status cf_stage_forward(const void *x, void *y, void *ws, size_t ws_bytes, co
     cf_status st = check_fit("cf_stage_forward", s);
     if (st != CF_OK)
         return st;
+    // wide blocks over many pixels: depth-wise conv, two library GEMMs and
+    // two elementwise passes, the hidden tensor in the workspace after the
+    // ping-pong buffer, when the workspace holds it
+    size_t lbytes = cf::libgemm_applies(s) ? cf::libgemm_scratch_bytes(s) : 0;
+    for (int i = 0; lbytes && i < depth; i++)
+        if (!cf::libgemm_vectors_ok(to_w(&blocks[i])))
+            lbytes = 0;
+    if (lbytes && ws && aligned16(ws) && ws_bytes >= need + lbytes && !overlap((char *)ws + need, lbytes, x, bytes) &&
+        !overlap((char *)ws + need, lbytes, y, bytes) && cf::libgemm_ready(s)) {
+        void *scratch = (char *)ws + need;
+        const void *in = x;
+        for (int i = 0; i < depth; i++) {
+            void *out = ((depth - 1 - i) % 2 == 0) ? y : ws;
+            hipError_t e = cf::launch_block_libgemm(in, out, to_w(&blocks[i]), s, scratch, (hipStream_t)stream);
+            if (e != hipSuccess)
+                return hip_fail(e, "cf_stage_forward");
+            in = out;
+        }
+        g_err[0] = 0;
+        return CF_OK;
+    }
     // hidden-layer split with fp32 partials after the ping-pong buffer, when
     // the workspace holds them
     int groups = 1;

@@ -91,6 +91,19 @@ hipError_t launch_slice(const void *x, void *y, const BlockW &w, const Shape &s,
 size_t small_split_lds_bytes(const Shape &s, bool direct = false);
 
 // Layer-by-layer path: depth-wise -> d, expand + act -> h, project + residual -> y.
+// The depth-wise conv of a block with s0, b0: D [N][H][W][C] (cf_unfused.hip).
+hipError_t launch_depthwise(const void *x, void *d, const BlockW &w, const Shape &s, hipStream_t st);
+
+// A block as depth-wise conv, two library GEMMs and two elementwise passes
+// (cf_libgemm.hip), for fp16 blocks at C = 512 over at least 4096 pixels;
+// scratch holds libgemm_scratch_bytes(s) bytes, 256-byte aligned.
+bool libgemm_applies(const Shape &s);
+bool libgemm_ready(const Shape &s);  // creates the GEMM plans; false when the library has none
+bool libgemm_vectors_ok(const BlockW &w);  // scales and biases 16-byte aligned (or null)
+size_t libgemm_scratch_bytes(const Shape &s);
+hipError_t launch_block_libgemm(const void *x, void *y, const BlockW &w, const Shape &s, void *scratch,
+                                hipStream_t st);
+
 hipError_t launch_unfused_block(const void *x, void *y, void *d, void *h, const BlockW &w,
                                 const Shape &s, hipStream_t st);
 

@@ -395,6 +395,10 @@ hipError_t unfused(const void *x, void *y, void *d, void *h, const BlockW &w, co
 
 }  // namespace
 
+hipError_t launch_depthwise(const void *x, void *d, const BlockW &w, const Shape &s, hipStream_t st) {
+    return s.bf16 ? dw<BF16>(x, d, w, s, st) : dw<F16>(x, d, w, s, st);
+}
+
 hipError_t launch_unfused_block(const void *x, void *y, void *d, void *h, const BlockW &w, const Shape &s,
                                 hipStream_t st) {
     return s.bf16 ? unfused<BF16>(x, y, d, h, w, s, st) : unfused<F16>(x, y, d, h, w, s, st);
