@@ -103,9 +103,8 @@ cf_status cf_block_forward(const void *x, void *y, const cf_block_params *p,
  * cf_stage_workspace_bytes() returns the recommended ws size.  The minimum is
  * N*H*W*C*2 bytes (rounded up to 256) for depth > 1 and 0 for depth == 1;
  * for C = 512 fp16 the recommended size adds 16*N*H*W*C bytes.  With that
- * room, at N*H*W >= 4096 pixels, E <= 6 and every scale and bias pointer
- * 16-byte aligned (or NULL), each block runs layer by layer (Sec. 5.2):
- * a depth-wise kernel, the expand and project as hipBLASLt GEMMs with the
+ * room, at N*H*W >= 4096 pixels and E <= 6, each block runs layer by layer
+ * (Sec. 5.2): a depth-wise kernel, the expand and project as hipBLASLt GEMMs with the
  * hidden tensor in ws, and two elementwise kernels (s1, b1, activation;
  * s2, b2, residual), rounding the GEMM outputs to fp16 before their scale
  * and bias (within the block tolerance of the fused kernels; deterministic).

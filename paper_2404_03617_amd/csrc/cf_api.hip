@@ -430,12 +430,9 @@ cf_status cf_stage_forward(const void *x, void *y, void *ws, size_t ws_bytes, co
     // wide blocks over many pixels: depth-wise conv, two library GEMMs and
     // two elementwise passes, the hidden tensor in the workspace after the
     // ping-pong buffer, when the workspace holds it
-    size_t lbytes = cf::libgemm_applies(s) ? cf::libgemm_scratch_bytes(s) : 0;
-    for (int i = 0; lbytes && i < depth; i++)
-        if (!cf::libgemm_vectors_ok(to_w(&blocks[i])))
-            lbytes = 0;
+    const size_t lbytes = cf::libgemm_applies(s) ? cf::libgemm_scratch_bytes(s) : 0;
     if (lbytes && ws && aligned16(ws) && ws_bytes >= need + lbytes && !overlap((char *)ws + need, lbytes, x, bytes) &&
-        !overlap((char *)ws + need, lbytes, y, bytes) && cf::libgemm_ready(s)) {
+        !overlap((char *)ws + need, lbytes, y, bytes) && cf::libgemm_ready(s, (hipStream_t)stream)) {
         void *scratch = (char *)ws + need;
         const void *in = x;
         for (int i = 0; i < depth; i++) {

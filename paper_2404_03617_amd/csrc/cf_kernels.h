@@ -98,8 +98,8 @@ hipError_t launch_depthwise(const void *x, void *d, const BlockW &w, const Shape
 // (cf_libgemm.hip), for fp16 blocks at C = 512 over at least 4096 pixels;
 // scratch holds libgemm_scratch_bytes(s) bytes, 256-byte aligned.
 bool libgemm_applies(const Shape &s);
-bool libgemm_ready(const Shape &s);  // creates the GEMM plans; false when the library has none
-bool libgemm_vectors_ok(const BlockW &w);  // scales and biases 16-byte aligned (or null)
+// creates the GEMM plans (outside a stream capture); false when they are missing
+bool libgemm_ready(const Shape &s, hipStream_t st);
 size_t libgemm_scratch_bytes(const Shape &s);
 hipError_t launch_block_libgemm(const void *x, void *y, const BlockW &w, const Shape &s, void *scratch,
                                 hipStream_t st);

@@ -48,14 +48,15 @@ int g_nplans = 0;
 // D [n][m] (row-major, fp16) = B [n][k] . A [m][k]^T: in the library's
 // column-major terms D (m x n) = op(A) (m x k, A stored k x m, transposed)
 // times B (k x n).  Plans (descriptors and the heuristic's first algorithm)
-// are cached per device and shape; the caller holds g_mu.
-hipError_t plan_for(int dev, int m, int n, int k, const Plan **out) {
+// are cached per device and shape; the caller holds g_mu.  With create
+// false only an existing plan is returned.
+hipError_t plan_for(int dev, int m, int n, int k, const Plan **out, bool create = true) {
     for (int i = 0; i < g_nplans; i++)
         if (g_plans[i].dev == dev && g_plans[i].m == m && g_plans[i].n == n && g_plans[i].k == k) {
             *out = &g_plans[i];
             return hipSuccess;
         }
-    if (g_nplans == MAX_SHAPES)
+    if (!create || g_nplans == MAX_SHAPES)
         return hipErrorNotSupported;
     if (!g_handle[dev] && hipblasLtCreate(&g_handle[dev]) != HIPBLAS_STATUS_SUCCESS)
         return hipErrorNotSupported;
@@ -279,22 +280,21 @@ unsigned grid_for(uint32_t n8, uint32_t ch8) {
 
 }  // namespace lgm
 
-bool libgemm_ready(const Shape &s) {
+bool libgemm_ready(const Shape &s, hipStream_t st) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= lgm::MAX_DEV)
         return false;
+    // inside a stream capture only plans made before are used: creating the
+    // library handle allocates device memory, which a capture forbids
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st, &cap) != hipSuccess)
+        return false;
+    const bool create = cap == hipStreamCaptureStatusNone;
     const int P = (int)((int64_t)s.N * s.H * s.W), C = s.C, EC = s.E * s.C;
     std::lock_guard<std::mutex> lk(lgm::g_mu);
     const lgm::Plan *p1 = nullptr, *p2 = nullptr;
-    return lgm::plan_for(dev, EC, P, C, &p1) == hipSuccess && lgm::plan_for(dev, C, P, EC, &p2) == hipSuccess;
-}
-
-bool libgemm_vectors_ok(const BlockW &w) {
-    const float *v[6] = {w.s0, w.b0, w.s1, w.b1, w.s2, w.b2};
-    for (const float *p : v)
-        if (p && ((uintptr_t)p & 15))
-            return false;
-    return true;
+    return lgm::plan_for(dev, EC, P, C, &p1, create) == hipSuccess &&
+           lgm::plan_for(dev, C, P, EC, &p2, create) == hipSuccess;
 }
 
 bool libgemm_applies(const Shape &s) {
