@@ -33,8 +33,14 @@ namespace lgm {
 constexpr int MAX_DEV = 16;
 constexpr int MAX_SHAPES = 16;
 
+// epilogues: none, or the expand's s1 (a per-row alpha vector), b1 (bias)
+// and activation fused into the GEMM
+enum { EPI_NONE = 0, EPI_VEC = 1, EPI_VEC_BIAS = 2 };
+
 struct Plan {
     int dev = -1, m = 0, n = 0, k = 0;
+    int epi = EPI_NONE, act = 0;
+    bool valid = false;  // false: the library had no algorithm (not asked again)
     hipblasLtMatmulDesc_t op = nullptr;
     hipblasLtMatrixLayout_t la = nullptr, lb = nullptr, lc = nullptr;
     hipblasLtMatmulAlgo_t algo{};
@@ -50,11 +56,13 @@ int g_nplans = 0;
 // times B (k x n).  Plans (descriptors and the heuristic's first algorithm)
 // are cached per device and shape; the caller holds g_mu.  With create
 // false only an existing plan is returned.
-hipError_t plan_for(int dev, int m, int n, int k, const Plan **out, bool create = true) {
+hipError_t plan_for(int dev, int m, int n, int k, const Plan **out, bool create = true, int epi = EPI_NONE,
+                    int act = 0) {
     for (int i = 0; i < g_nplans; i++)
-        if (g_plans[i].dev == dev && g_plans[i].m == m && g_plans[i].n == n && g_plans[i].k == k) {
+        if (g_plans[i].dev == dev && g_plans[i].m == m && g_plans[i].n == n && g_plans[i].k == k &&
+            g_plans[i].epi == epi && g_plans[i].act == act) {
             *out = &g_plans[i];
-            return hipSuccess;
+            return g_plans[i].valid ? hipSuccess : hipErrorNotSupported;
         }
     if (!create || g_nplans == MAX_SHAPES)
         return hipErrorNotSupported;
@@ -65,7 +73,18 @@ hipError_t plan_for(int dev, int m, int n, int k, const Plan **out, bool create 
     p.m = m;
     p.n = n;
     p.k = k;
+    p.epi = epi;
+    p.act = act;
     const hipblasOperation_t ta = HIPBLAS_OP_T, tb = HIPBLAS_OP_N;
+    uint32_t ep = HIPBLASLT_EPILOGUE_DEFAULT;
+    if (epi != EPI_NONE) {
+        const bool bias = epi == EPI_VEC_BIAS;
+        ep = act == ACT_GELU   ? (bias ? HIPBLASLT_EPILOGUE_GELU_BIAS : HIPBLASLT_EPILOGUE_GELU)
+             : act == ACT_RELU ? (bias ? HIPBLASLT_EPILOGUE_RELU_BIAS : HIPBLASLT_EPILOGUE_RELU)
+                               : (bias ? HIPBLASLT_EPILOGUE_BIAS : HIPBLASLT_EPILOGUE_DEFAULT);
+    }
+    const int32_t pmode = HIPBLASLT_POINTER_MODE_ALPHA_DEVICE_VECTOR_BETA_HOST;
+    const int32_t btype = HIP_R_32F;
     hipblasLtMatmulPreference_t pref = nullptr;
     const uint64_t no_ws = 0;
     hipblasLtMatmulHeuristicResult_t res[1];
@@ -75,6 +94,13 @@ hipError_t plan_for(int dev, int m, int n, int k, const Plan **out, bool create 
                   HIPBLAS_STATUS_SUCCESS &&
               hipblasLtMatmulDescSetAttribute(p.op, HIPBLASLT_MATMUL_DESC_TRANSB, &tb, sizeof(tb)) ==
                   HIPBLAS_STATUS_SUCCESS &&
+              hipblasLtMatmulDescSetAttribute(p.op, HIPBLASLT_MATMUL_DESC_EPILOGUE, &ep, sizeof(ep)) ==
+                  HIPBLAS_STATUS_SUCCESS &&
+              (epi == EPI_NONE || hipblasLtMatmulDescSetAttribute(p.op, HIPBLASLT_MATMUL_DESC_POINTER_MODE, &pmode,
+                                                                  sizeof(pmode)) == HIPBLAS_STATUS_SUCCESS) &&
+              (epi != EPI_VEC_BIAS || hipblasLtMatmulDescSetAttribute(p.op, HIPBLASLT_MATMUL_DESC_BIAS_DATA_TYPE,
+                                                                      &btype, sizeof(btype)) ==
+                                          HIPBLAS_STATUS_SUCCESS) &&
               hipblasLtMatrixLayoutCreate(&p.la, HIP_R_16F, k, m, k) == HIPBLAS_STATUS_SUCCESS &&
               hipblasLtMatrixLayoutCreate(&p.lb, HIP_R_16F, k, n, k) == HIPBLAS_STATUS_SUCCESS &&
               hipblasLtMatrixLayoutCreate(&p.lc, HIP_R_16F, m, n, m) == HIPBLAS_STATUS_SUCCESS &&
@@ -95,15 +121,22 @@ hipError_t plan_for(int dev, int m, int n, int k, const Plan **out, bool create 
             hipblasLtMatrixLayoutDestroy(p.lb);
         if (p.lc)
             hipblasLtMatrixLayoutDestroy(p.lc);
+        p.op = nullptr;
+        p.la = p.lb = p.lc = nullptr;
+        g_plans[g_nplans++] = p;  // remembered as missing
         return hipErrorNotSupported;
     }
+    p.valid = true;
     p.algo = res[0].algo;
     g_plans[g_nplans] = p;
     *out = &g_plans[g_nplans++];
     return hipSuccess;
 }
 
-hipError_t gemm_nt(const void *a, const void *b, void *d, int m, int n, int k, hipStream_t st) {
+// With epi != EPI_NONE: d = act(svec (a b) + bias) per row of D, svec and
+// bias fp32 device vectors of m entries (bias only for EPI_VEC_BIAS).
+hipError_t gemm_nt(const void *a, const void *b, void *d, int m, int n, int k, hipStream_t st, int epi = EPI_NONE,
+                   int act = 0, const float *svec = nullptr, const float *bias = nullptr) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess)
@@ -112,11 +145,16 @@ hipError_t gemm_nt(const void *a, const void *b, void *d, int m, int n, int k, h
         return hipErrorNotSupported;
     std::lock_guard<std::mutex> lk(g_mu);
     const Plan *p = nullptr;
-    e = plan_for(dev, m, n, k, &p);
+    e = plan_for(dev, m, n, k, &p, true, epi, act);
     if (e != hipSuccess)
         return e;
-    const float alpha = 1.0f, beta = 0.0f;
-    return hipblasLtMatmul(g_handle[dev], p->op, &alpha, a, p->la, b, p->lb, &beta, d, p->lc, d, p->lc, &p->algo,
+    if (epi == EPI_VEC_BIAS &&
+        hipblasLtMatmulDescSetAttribute(p->op, HIPBLASLT_MATMUL_DESC_BIAS_POINTER, &bias, sizeof(bias)) !=
+            HIPBLAS_STATUS_SUCCESS)
+        return hipErrorLaunchFailure;
+    const float one = 1.0f, beta = 0.0f;
+    const void *alpha = epi == EPI_NONE ? (const void *)&one : (const void *)svec;
+    return hipblasLtMatmul(g_handle[dev], p->op, alpha, a, p->la, b, p->lb, &beta, d, p->lc, d, p->lc, &p->algo,
                            nullptr, 0, st) == HIPBLAS_STATUS_SUCCESS
                ? hipSuccess
                : hipErrorLaunchFailure;
@@ -292,9 +330,25 @@ bool libgemm_ready(const Shape &s, hipStream_t st) {
     const bool create = cap == hipStreamCaptureStatusNone;
     const int P = (int)((int64_t)s.N * s.H * s.W), C = s.C, EC = s.E * s.C;
     std::lock_guard<std::mutex> lk(lgm::g_mu);
-    const lgm::Plan *p1 = nullptr, *p2 = nullptr;
-    return lgm::plan_for(dev, EC, P, C, &p1, create) == hipSuccess &&
-           lgm::plan_for(dev, C, P, EC, &p2, create) == hipSuccess;
+    const lgm::Plan *p1 = nullptr, *p2 = nullptr, *p3 = nullptr;
+    const bool ok = lgm::plan_for(dev, EC, P, C, &p1, create) == hipSuccess &&
+                    lgm::plan_for(dev, C, P, EC, &p2, create) == hipSuccess;
+    // the expand with s1, b1 and the activation in its epilogue, when the
+    // library has an algorithm for it (else the separate pass runs)
+    if (ok)
+        lgm::plan_for(dev, EC, P, C, &p3, create, lgm::EPI_VEC_BIAS, s.act);
+    return ok;
+}
+
+// whether the expand's epilogue plan exists (made by libgemm_ready)
+static bool fused_epilogue_ready(const Shape &s) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= lgm::MAX_DEV)
+        return false;
+    const int P = (int)((int64_t)s.N * s.H * s.W), C = s.C, EC = s.E * s.C;
+    std::lock_guard<std::mutex> lk(lgm::g_mu);
+    const lgm::Plan *p = nullptr;
+    return lgm::plan_for(dev, EC, P, C, &p, false, lgm::EPI_VEC_BIAS, s.act) == hipSuccess;
 }
 
 bool libgemm_applies(const Shape &s) {
@@ -322,15 +376,22 @@ hipError_t launch_block_libgemm(const void *x, void *y, const BlockW &w, const S
     hipError_t e = lgm::depthwise(x, d, w, s, st);
     if (e != hipSuccess)
         return e;
-    e = lgm::gemm_nt(w.w1, d, h, EC, (int)P, C, st);
-    if (e != hipSuccess)
-        return e;
-    const uint32_t nh = (uint32_t)(P * EC / 8);
-    hipLaunchKernelGGL(lgm::hidden_kernel, dim3(lgm::grid_for(nh, EC / 8)), dim3(256), 0, st, h, w.s1, w.b1, nh,
-                       (uint32_t)(EC / 8), s.act);
-    e = hipGetLastError();
-    if (e != hipSuccess)
-        return e;
+    if (w.s1 && w.b1 && fused_epilogue_ready(s)) {
+        // s1, b1 and the activation in the expand's epilogue
+        e = lgm::gemm_nt(w.w1, d, h, EC, (int)P, C, st, lgm::EPI_VEC_BIAS, s.act, w.s1, w.b1);
+        if (e != hipSuccess)
+            return e;
+    } else {
+        e = lgm::gemm_nt(w.w1, d, h, EC, (int)P, C, st);
+        if (e != hipSuccess)
+            return e;
+        const uint32_t nh = (uint32_t)(P * EC / 8);
+        hipLaunchKernelGGL(lgm::hidden_kernel, dim3(lgm::grid_for(nh, EC / 8)), dim3(256), 0, st, h, w.s1, w.b1,
+                           nh, (uint32_t)(EC / 8), s.act);
+        e = hipGetLastError();
+        if (e != hipSuccess)
+            return e;
+    }
     e = lgm::gemm_nt(w.w2, h, t, C, (int)P, EC, st);
     if (e != hipSuccess)
         return e;
