@@ -104,10 +104,13 @@ cf_status cf_block_forward(const void *x, void *y, const cf_block_params *p,
  * N*H*W*C*2 bytes (rounded up to 256) for depth > 1 and 0 for depth == 1;
  * for C = 512 fp16 the recommended size adds 16*N*H*W*C bytes.  With that
  * room, at N*H*W >= 4096 pixels and E <= 6, each block runs layer by layer
- * (Sec. 5.2): a depth-wise kernel, the expand and project as hipBLASLt GEMMs with the
- * hidden tensor in ws, and two elementwise kernels (s1, b1, activation;
- * s2, b2, residual), rounding the GEMM outputs to fp16 before their scale
- * and bias (within the block tolerance of the fused kernels; deterministic).
+ * (Sec. 5.2): a depth-wise kernel, the expand and project as hipBLASLt
+ * GEMMs with the hidden tensor in ws (s1, b1 and the activation in the
+ * expand's epilogue, with the library's GELU, when s1 and b1 are given;
+ * else an elementwise kernel after it), and an elementwise kernel for s2,
+ * b2 and the residual; the project's output is rounded to fp16 before its
+ * scale and bias (within the block tolerance of the fused kernels;
+ * deterministic).
  * Otherwise, with the room, each block splits its hidden layer over several
  * workgroups (results identical up to fp32 summation order, deterministic).
  * The library GEMMs are given no workspace of their own. */

@@ -12,14 +12,17 @@
 //   1. depth-wise k x k conv, s0, b0 -> D [P][C]            (small images and
 //      k = 3: one image slice per workgroup in LDS; else cf_unfused.hip)
 //   2. Hraw = D W1^T                  -> H [P][E C]          (hipBLASLt, fp32 accumulate)
-//   3. H = act(s1 Hraw + b1)          in place; s1, b1 in fp32, GELU as the
+//   3. H = act(s1 Hraw + b1): in the GEMM's epilogue (alpha vector, bias,
+//      the library's GELU / ReLU) when s1 and b1 are given and the library
+//      has such an algorithm; else in place, s1, b1 in fp32, GELU as the
 //      fused fp16 kernels evaluate it (packed fp16 on u / 4)
 //   4. T = H W2^T                     -> T [P][C]            (hipBLASLt)
 //   5. y = s2 T + b2 + x                                      fp32 math, rounded
 // The GEMMs get no library workspace, so the library picks no algorithm that
 // clears memory on the stream (safe inside a captured graph).  Rounding
-// points differ from the fused kernels (Hraw and T are rounded to fp16
-// before their scale and bias); the results stay within the block tolerance.
+// points differ from the fused kernels (T, and Hraw without the epilogue,
+// are rounded to fp16 before their scale and bias); the results stay within
+// the block tolerance.
 #include <hipblaslt/hipblaslt.h>
 
 #include <mutex>
