@@ -107,10 +107,10 @@ cf_status cf_block_forward(const void *x, void *y, const cf_block_params *p,
  * (Sec. 5.2): a depth-wise kernel, the expand and project as hipBLASLt
  * GEMMs with the hidden tensor in ws (s1, b1 and the activation in the
  * expand's epilogue, with the library's GELU, when s1 and b1 are given;
- * else an elementwise kernel after it), and an elementwise kernel for s2,
- * b2 and the residual; the project's output is rounded to fp16 before its
- * scale and bias (within the block tolerance of the fused kernels;
- * deterministic).
+ * else an elementwise kernel after it), and s2, b2 and the residual in the
+ * project's epilogue (else an elementwise kernel after it, the project's
+ * output rounded to fp16 first); within the block tolerance of the fused
+ * kernels, deterministic.
  * Otherwise, with the room, each block splits its hidden layer over several
  * workgroups (results identical up to fp32 summation order, deterministic).
  * The library GEMMs are given no workspace of their own. */

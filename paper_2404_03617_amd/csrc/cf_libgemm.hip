@@ -18,6 +18,8 @@
 //      fused fp16 kernels evaluate it (packed fp16 on u / 4)
 //   4. T = H W2^T                     -> T [P][C]            (hipBLASLt)
 //   5. y = s2 T + b2 + x                                      fp32 math, rounded
+//      (4 and 5 as one GEMM with the alpha vector s2, x as the C operand
+//      and the bias b2 in its epilogue, when s2 and b2 are given)
 // The GEMMs get no library workspace, so the library picks no algorithm that
 // clears memory on the stream (safe inside a captured graph).  Rounding
 // points differ from the fused kernels (T, and Hraw without the epilogue,
@@ -136,10 +138,12 @@ hipError_t plan_for(int dev, int m, int n, int k, const Plan **out, bool create 
     return hipSuccess;
 }
 
-// With epi != EPI_NONE: d = act(svec (a b) + bias) per row of D, svec and
-// bias fp32 device vectors of m entries (bias only for EPI_VEC_BIAS).
+// With epi != EPI_NONE: d = act(svec (a b) + beta c + bias) per row of D,
+// svec and bias fp32 device vectors of m entries (bias only for
+// EPI_VEC_BIAS), c (D's layout) only when beta != 0.
 hipError_t gemm_nt(const void *a, const void *b, void *d, int m, int n, int k, hipStream_t st, int epi = EPI_NONE,
-                   int act = 0, const float *svec = nullptr, const float *bias = nullptr) {
+                   int act = 0, const float *svec = nullptr, const float *bias = nullptr, const void *c = nullptr,
+                   float beta = 0.0f) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess)
@@ -155,10 +159,10 @@ hipError_t gemm_nt(const void *a, const void *b, void *d, int m, int n, int k, h
         hipblasLtMatmulDescSetAttribute(p->op, HIPBLASLT_MATMUL_DESC_BIAS_POINTER, &bias, sizeof(bias)) !=
             HIPBLAS_STATUS_SUCCESS)
         return hipErrorLaunchFailure;
-    const float one = 1.0f, beta = 0.0f;
+    const float one = 1.0f;
     const void *alpha = epi == EPI_NONE ? (const void *)&one : (const void *)svec;
-    return hipblasLtMatmul(g_handle[dev], p->op, alpha, a, p->la, b, p->lb, &beta, d, p->lc, d, p->lc, &p->algo,
-                           nullptr, 0, st) == HIPBLAS_STATUS_SUCCESS
+    return hipblasLtMatmul(g_handle[dev], p->op, alpha, a, p->la, b, p->lb, &beta, beta != 0.0f ? c : d, p->lc, d,
+                           p->lc, &p->algo, nullptr, 0, st) == HIPBLAS_STATUS_SUCCESS
                ? hipSuccess
                : hipErrorLaunchFailure;
 }
@@ -336,22 +340,27 @@ bool libgemm_ready(const Shape &s, hipStream_t st) {
     const lgm::Plan *p1 = nullptr, *p2 = nullptr, *p3 = nullptr;
     const bool ok = lgm::plan_for(dev, EC, P, C, &p1, create) == hipSuccess &&
                     lgm::plan_for(dev, C, P, EC, &p2, create) == hipSuccess;
-    // the expand with s1, b1 and the activation in its epilogue, when the
-    // library has an algorithm for it (else the separate pass runs)
-    if (ok)
+    // the expand with s1, b1 and the activation in its epilogue, the project
+    // with s2, b2 and the residual, when the library has algorithms for them
+    // (else the separate passes run)
+    if (ok) {
         lgm::plan_for(dev, EC, P, C, &p3, create, lgm::EPI_VEC_BIAS, s.act);
+        lgm::plan_for(dev, C, P, EC, &p3, create, lgm::EPI_VEC_BIAS, ACT_NONE);
+    }
     return ok;
 }
 
-// whether the expand's epilogue plan exists (made by libgemm_ready)
-static bool fused_epilogue_ready(const Shape &s) {
+// whether an epilogue plan exists (made by libgemm_ready): the expand's
+// (project = false) or the project's
+static bool fused_epilogue_ready(const Shape &s, bool project) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= lgm::MAX_DEV)
         return false;
     const int P = (int)((int64_t)s.N * s.H * s.W), C = s.C, EC = s.E * s.C;
     std::lock_guard<std::mutex> lk(lgm::g_mu);
     const lgm::Plan *p = nullptr;
-    return lgm::plan_for(dev, EC, P, C, &p, false, lgm::EPI_VEC_BIAS, s.act) == hipSuccess;
+    return project ? lgm::plan_for(dev, C, P, EC, &p, false, lgm::EPI_VEC_BIAS, ACT_NONE) == hipSuccess
+                   : lgm::plan_for(dev, EC, P, C, &p, false, lgm::EPI_VEC_BIAS, s.act) == hipSuccess;
 }
 
 bool libgemm_applies(const Shape &s) {
@@ -379,7 +388,7 @@ hipError_t launch_block_libgemm(const void *x, void *y, const BlockW &w, const S
     hipError_t e = lgm::depthwise(x, d, w, s, st);
     if (e != hipSuccess)
         return e;
-    if (w.s1 && w.b1 && fused_epilogue_ready(s)) {
+    if (w.s1 && w.b1 && fused_epilogue_ready(s, false)) {
         // s1, b1 and the activation in the expand's epilogue
         e = lgm::gemm_nt(w.w1, d, h, EC, (int)P, C, st, lgm::EPI_VEC_BIAS, s.act, w.s1, w.b1);
         if (e != hipSuccess)
@@ -395,6 +404,8 @@ hipError_t launch_block_libgemm(const void *x, void *y, const BlockW &w, const S
         if (e != hipSuccess)
             return e;
     }
+    if (w.s2 && w.b2 && fused_epilogue_ready(s, true))  // y = s2 (W2 h) + x + b2 in the epilogue
+        return lgm::gemm_nt(w.w2, h, y, C, (int)P, EC, st, lgm::EPI_VEC_BIAS, ACT_NONE, w.s2, w.b2, x, 1.0f);
     e = lgm::gemm_nt(w.w2, h, t, C, (int)P, EC, st);
     if (e != hipSuccess)
         return e;
